@@ -1,0 +1,209 @@
+"""Pins for propose / verify / commit (Sec. 3.2).
+
+The plain definition the method must reach is greedy decoding of the target
+(Eq. stage1 at temperature 0): speculative decoding keeps the target's exact
+greedy output (Sec. 2).  These tests check the oracle's loop against that,
+against brute-force enumeration of the accept rule, against a fresh prefill of
+the committed sequence, and the reporting formulas against Table main."""
+import dataclasses
+import itertools
+
+import numpy as np
+import pytest
+
+import workloads as W
+from oracle import model as M
+from oracle import report
+from oracle import spec as OS
+from tests import _support as S
+
+
+def _tiny(K=4, max_new=12, stop=-1, vocab=256, prefix=48):
+    base = W.get("C1")
+    lay = W.SeqLayout(prefix, (W.VisionBlock(0, 1, 5, 6),))
+    return base.with_(vocab=vocab, seqs=(lay,), K=K, max_new_tokens=max_new, stop_token=stop)
+
+
+@pytest.fixture(scope="module")
+def tiny():
+    w = _tiny()
+    hp = W.HostWeights(w)
+    T, D = S.oracle_decoders(w, hp)
+    seq = S.oracle_sequence(w, 0, T, D)
+    trace = list(OS.greedy_trace(seq))
+    return w, hp, T, D, trace
+
+
+# --- Eq. accept -------------------------------------------------------------------
+
+def _first_mismatch(d, r):
+    eq = np.asarray(d) == np.asarray(r)[:len(d)]
+    return int(np.argmin(eq)) if not eq.all() else len(d)
+
+
+def test_accept_length_bruteforce_small_vocab():
+    # every draft in {0..7}^3 against several target argmax vectors
+    for rstar in [(0, 1, 2, 3), (5, 5, 5, 5), (7, 0, 7, 1)]:
+        for d in itertools.product(range(8), repeat=3):
+            assert OS.accept_length(d, rstar) == _first_mismatch(d, rstar)
+
+
+def test_accept_length_random_large_vocab():
+    rng = np.random.default_rng(0)
+    for _ in range(2000):
+        K = int(rng.integers(0, 17))
+        r = rng.integers(0, 1024, size=K + 1)
+        d = np.where(rng.random(K) < 0.8, r[:K], rng.integers(0, 1024, size=K))
+        assert OS.accept_length(d, r) == _first_mismatch(d, r)
+
+
+def test_commit_rule_bonus_stop_and_budget():
+    toks, fin = OS.commit_tokens([4, 5, 6], [4, 5, 9, 8], 2)
+    assert toks == [4, 5, 9] and not fin
+    toks, fin = OS.commit_tokens([4, 5, 6], [4, 5, 6, 8], 3)
+    assert toks == [4, 5, 6, 8] and not fin                     # l = K commits K+1
+    toks, fin = OS.commit_tokens([4, 5, 6], [4, 5, 6, 8], 3, stop_token=5)
+    assert toks == [4, 5] and fin
+    toks, fin = OS.commit_tokens([4, 5, 6], [4, 5, 6, 8], 3, budget=2)
+    assert toks == [4, 5] and fin
+
+
+# --- whole loop vs greedy decoding -----------------------------------------------
+
+def test_trace_is_greedy_by_definition(tiny):
+    # each greedy token is the argmax of a single-row pass over all earlier tokens
+    w, hp, T, D, trace = tiny
+    seq = S.oracle_sequence(w, 0, T, None, with_draft=False)
+    toks = [seq.pending] + trace
+    n0 = seq.seq_len
+    for j in range(len(trace)):
+        z = T.forward([toks[j]], [n0 + j], seq.tc)
+        assert int(np.argmax(z[0])) == trace[j]
+
+
+@pytest.mark.parametrize("p", [0.0, 0.5, 0.8, 1.0])
+def test_spec_loop_equals_greedy_synthetic_drafts(tiny, p):
+    w, hp, T, D, trace = tiny
+    w2 = w.with_(p_accept=(p,))
+    seq = S.oracle_sequence(w2, 0, T, None, with_draft=False)
+    synth = W.DraftSynth(w2, 0)
+
+    def proposer(s):
+        i = len(s.generated)
+        return list(synth.propose(np.array(trace[i:]), w.K))
+
+    out = OS.spec_loop(seq, proposer)
+    assert out == trace
+    if p == 1.0:
+        assert all(l == w.K for l in seq.history[:-1])
+    if p == 0.0:
+        assert max(seq.history) <= 1    # only accidental matches
+
+
+def test_spec_loop_equals_greedy_with_draft_model(tiny):
+    w, hp, T, D, trace = tiny
+    seq = S.oracle_sequence(w, 0, T, D)
+    out = OS.spec_loop(seq, lambda s: s.propose())
+    assert out == trace
+
+
+def test_accept_zero_is_one_greedy_step_and_full_accept(tiny):
+    w, hp, T, D, trace = tiny
+    seq = S.oracle_sequence(w, 0, T, None, with_draft=False)
+    wrong = [(trace[0] + 1) % w.vocab] * w.K
+    r = seq.verify(wrong)
+    assert r.accept_len == 0 and r.committed == [trace[0]]
+    r = seq.verify(trace[1:1 + w.K])
+    assert r.accept_len == w.K and r.committed == trace[1:2 + w.K]
+
+
+def test_commit_leaves_cache_equal_to_fresh_prefill(tiny):
+    # After rounds with rejected drafts, every valid slot equals what a fresh
+    # one-token-at-a-time pass over the committed tokens stores.
+    w, hp, T, D, trace = tiny
+    a = S.oracle_sequence(w, 0, T, D)
+    rng = np.random.default_rng(5)
+    for _ in range(3):
+        a.propose()
+        i = len(a.generated)
+        d = [t if rng.random() < 0.6 else int(rng.integers(0, w.vocab)) for t in trace[i:i + w.K]]
+        d += [0] * (w.K - len(d))
+        a.verify(d)
+    b = S.oracle_sequence(w, 0, T, D)
+    for _ in range(len(a.generated)):
+        b.greedy_step()
+    assert a.generated == b.generated
+    n = a.seq_len
+    for li in range(w.target.layers):
+        assert np.allclose(a.tc.k[li][:n], b.tc.k[li][:n], rtol=1e-9, atol=1e-12)
+        assert np.allclose(a.tc.v[li][:n], b.tc.v[li][:n], rtol=1e-9, atol=1e-12)
+    # draft: its valid slots equal a fresh draft pass over the committed tokens
+    c = S.oracle_sequence(w, 0, T, D)
+    toks = [c.pending] + a.generated
+    P = c.P
+    D.forward(toks[:a.draft_len - P], list(range(P, a.draft_len)), c.dc)
+    for li in range(w.draft.layers):
+        assert np.allclose(a.dc.k[li][:a.draft_len], c.dc.k[li][:a.draft_len], rtol=1e-9, atol=1e-12)
+    assert a.draft_len <= a.seq_len
+
+
+def test_draft_catch_up_rows_after_override(tiny):
+    # Draft proposals overridden by the verifier: the next draft step re-consumes
+    # the committed tokens it has not seen and proposes what a fresh draft would.
+    w, hp, T, D, trace = tiny
+    a = S.oracle_sequence(w, 0, T, D)
+    props = a.propose()
+    override = trace[:w.K]
+    r = a.verify(override)
+    d_next, z_next = a.draft_step()
+    c = S.oracle_sequence(w, 0, T, D)
+    toks = [c.pending] + a.generated
+    z = D.forward(toks, list(range(c.P, a.seq_len + 1)), c.dc)
+    assert d_next == int(np.argmax(z[-1]))
+    assert np.allclose(z_next, z[-1], rtol=1e-9, atol=1e-12)
+
+
+def test_stop_token_and_budget(tiny):
+    w, hp, T, D, trace = tiny
+    stop = trace[5]
+    cut = trace.index(stop)
+    w2 = w.with_(stop_token=stop)
+    seq = S.oracle_sequence(w2, 0, T, D)
+    assert OS.spec_loop(seq, lambda s: s.propose()) == trace[:cut + 1]
+    w3 = w.with_(max_new_tokens=7)
+    seq = S.oracle_sequence(w3, 0, T, D)
+    assert OS.spec_loop(seq, lambda s: s.propose()) == trace[:7]
+
+
+# --- reporting (Eq. L-and-speedup, Sec. 5.1, Table main) -------------------------
+
+def test_table_main_speedups_from_L_and_c():
+    # EAGLE-3 chain draft: c = 15 * 0.047 = 0.705; block-diffusion: c = 0.18.
+    c_ar, c_bd = 15 * 0.047, 0.18
+    rows = [  # (L, printed S, c, tolerance)
+        (7.33, 4.30, c_ar, 0.015), (6.99, 4.11, c_ar, 0.015), (7.41, 4.36, c_ar, 0.015),
+        (7.35, 4.32, c_ar, 0.015), (6.95, 4.08, c_ar, 0.015), (7.30, 4.29, c_ar, 0.015),
+        (5.16, 4.39, c_bd, 0.03), (4.65, 3.97, c_bd, 0.03), (4.95, 4.21, c_bd, 0.03),
+        (5.17, 4.40, c_bd, 0.03), (4.67, 3.97, c_bd, 0.03),
+    ]
+    for L, S_print, c, tol in rows:
+        assert abs(report.theoretical_speedup(L, c) - S_print) <= tol
+    # the tok/s column is the 34 tok/s target-only rate times off-shelf S
+    for S_off, tps in [(4.23, 143.8), (4.36, 148.2), (4.29, 145.9), (4.21, 143.1)]:
+        assert round(34.0 * S_off, 1) == tps
+    # "L = 4.6 -> about 78% of tokens from the routine path": (L - 1) / L
+    assert round((4.6 - 1) / 4.6, 2) == 0.78
+
+
+def test_iid_expected_L_by_enumeration():
+    # E[l+1] for independent matches, by enumerating every match pattern with
+    # its probability and applying the accept rule to it.
+    for p, K in [(0.75, 8), (0.5, 5), (0.9, 4)]:
+        e = 0.0
+        for pat in itertools.product([True, False], repeat=K):
+            prob = np.prod([p if m else 1 - p for m in pat])
+            d = [0 if m else 1 for m in pat]
+            e += prob * (OS.accept_length(d, [0] * (K + 1)) + 1)
+        assert e == pytest.approx(report.iid_expected_L(p, K), rel=1e-12)
+        assert e == pytest.approx((1 - p ** (K + 1)) / (1 - p), rel=1e-12)
+    assert report.mean_accepted_length([3, 0, 8]) == pytest.approx(14 / 3)
