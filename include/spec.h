@@ -1,0 +1,228 @@
+/*
+ * spec.h -- C ABI of the MI355X speculative verify-and-commit library
+ * (libspecdec.so, gfx950).
+ *
+ * The library runs the propose / verify / commit loop of two-reasoner
+ * speculative decoding (Sec. 3.2 and Sec. 4.1 of "Reasoning-aware Speculative
+ * Decoding for Efficient Vision-Language-Action Models in Autonomous
+ * Driving"):
+ *   draft_step   one step of the routine reasoner, which proposes the next token
+ *                with FlatRoPE (Eq. propose, Eq. flatrope-proj); K calls give d_1..d_K.
+ *   spec_verify  the deliberative reasoner (target, 3D M-RoPE, Eq. rope-3d)
+ *                evaluates [pending, d_1..d_K] in one forward pass, takes the
+ *                greedy token of every row (Eq. verify) and the longest matching
+ *                prefix l (Eq. accept).
+ *   spec_commit  commits (d_1..d_l, r*_{l+1}), advances the lengths by l+1 and
+ *                rolls back both KV caches (Eq. commit).
+ *
+ * Conventions
+ *   - Every entry point returns a spec_status; nothing throws or exits.
+ *   - "device" pointers are HIP device memory on the device that is current at
+ *     spec_init; "host" pointers are ordinary memory.
+ *   - bf16 means IEEE bfloat16 stored as 16-bit words; matrices are row-major
+ *     [out_features][in_features].  All row lengths must be multiples of 8
+ *     elements and all device pointers 16-byte aligned.
+ *   - All work is enqueued on the stream given to spec_init and returns
+ *     without waiting, except the calls documented as synchronising.
+ *   - Arguments are validated on the host before anything is enqueued; on an
+ *     error the context is left unchanged.  A HIP runtime error poisons the
+ *     context: afterwards only spec_last_error and spec_destroy are valid.
+ *   - One context is not safe to use from two threads at once.
+ */
+#ifndef SPECDEC_SPEC_H
+#define SPECDEC_SPEC_H
+
+#include <stddef.h>
+#include <stdint.h>
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define SPEC_MAX_K      16   /* draft block size limit (the paper verifies blocks of 16) */
+#define SPEC_MAX_BATCH  16   /* sequences per context */
+#define SPEC_MAX_LAYERS 256
+
+typedef struct spec_ctx spec_ctx;   /* opaque; owned by the library */
+
+typedef enum spec_status {
+  SPEC_OK = 0,
+  SPEC_E_INVAL = 1,     /* bad argument, or a token id out of range was seen on the device */
+  SPEC_E_STATE = 2,     /* call out of order (see the state machine below) */
+  SPEC_E_CAPACITY = 3,  /* workspace too small or sequence capacity exceeded */
+  SPEC_E_HIP = 5,       /* HIP runtime error; the context is poisoned */
+  SPEC_E_NUMERIC = 6    /* NaN logits were seen on the device */
+} spec_status;
+
+/* Shape of one decoder stack.  The block is pre-norm: RMSNorm -> q,k,v (no
+ * bias) -> rotary -> causal grouped-query attention -> o projection + residual
+ * -> RMSNorm -> SwiGLU (silu(gate) * up) -> down projection + residual. */
+typedef struct spec_dims {
+  int32_t layers;            /* 1..SPEC_MAX_LAYERS */
+  int32_t hidden;            /* model width; multiple of 16 */
+  int32_t q_heads;           /* query heads; multiple of kv_heads */
+  int32_t kv_heads;          /* key/value heads */
+  int32_t head_dim;          /* 64 or 128 */
+  int32_t ffn;               /* SwiGLU inner width; multiple of 16 */
+  int32_t mrope_section[3];  /* (s_T, s_H, s_W) rotary pairs per axis, summing to
+                                head_dim/2 (Eq. rope-3d); ignored by the draft */
+  int32_t interleaved;       /* 0: blocked axis assignment, 1: d mod 3 (Eq. axis-assign) */
+  float rope_base;           /* theta_d = rope_base^(-2d/head_dim) (Eq. mrope-phase) */
+  float rms_eps;             /* RMSNorm epsilon */
+} spec_dims;
+
+#define SPEC_FLAG_NO_GRAPHS 1  /* launch kernels one by one instead of replaying HIP graphs */
+
+typedef struct spec_config {
+  spec_dims target;          /* deliberative reasoner (3D M-RoPE) */
+  spec_dims draft;           /* routine reasoner (FlatRoPE); draft.layers = 0 means no draft.
+                                hidden, head_dim and rope_base must equal the target's: the draft
+                                shares the embedding and the theta table (Sec. 4.2). */
+  int32_t vocab;             /* tied embedding / LM head rows; multiple of 16 */
+  int32_t K;                 /* draft block size, 0..SPEC_MAX_K (0: plain greedy decoding) */
+  int32_t batch;             /* independent sequences, 1..SPEC_MAX_BATCH */
+  int32_t max_new_tokens;    /* committed-token budget per sequence, >= 1 */
+  int32_t stop_token;        /* committing this token ends a sequence; -1: none */
+  int32_t flags;             /* SPEC_FLAG_* */
+} spec_config;
+
+/* Borrowed device pointers (bf16).  They must stay valid until spec_destroy. */
+typedef struct spec_layer_weights {
+  const void* attn_norm;     /* [hidden]                        */
+  const void* wq;            /* [q_heads*head_dim][hidden]      */
+  const void* wk;            /* [kv_heads*head_dim][hidden]     */
+  const void* wv;            /* [kv_heads*head_dim][hidden]     */
+  const void* wo;            /* [hidden][q_heads*head_dim]      */
+  const void* ffn_norm;      /* [hidden]                        */
+  const void* w_gate;        /* [ffn][hidden]                   */
+  const void* w_up;          /* [ffn][hidden]                   */
+  const void* w_down;        /* [hidden][ffn]                   */
+} spec_layer_weights;
+
+typedef struct spec_model_weights {
+  const spec_layer_weights* layers;  /* host array of dims.layers entries */
+  const void* final_norm;            /* [hidden] bf16, device */
+} spec_model_weights;
+
+/* A (t, h, w) grid of vision patches occupying sequence indices
+ * [start, start + t*h*w), stored t-major, then h, then w.  Its patch (t, h, w)
+ * gets the 3D position (start+t, start+h, start+w); every index outside the
+ * blocks is text and gets (i, i, i) (Sec. 3.3, Sec. 4.2). */
+typedef struct spec_vision_block {
+  int32_t start, t, h, w;
+} spec_vision_block;
+
+/* One sequence's prompt.  Its first prefix_len KV slots are filled from the
+ * given pre-rotation keys and values; index prefix_len holds pending_token,
+ * the first row of the first verify. */
+typedef struct spec_seq_init {
+  int32_t prefix_len;                 /* >= 1 */
+  int32_t n_blocks;
+  const spec_vision_block* blocks;    /* host; inside [0, prefix_len), non-overlapping */
+  int32_t pending_token;              /* in [0, vocab) */
+  const void* const* tgt_k;           /* host array [target.layers] of device pointers to
+                                         [prefix_len][kv_heads][head_dim] bf16 keys before rotation */
+  const void* const* tgt_v;           /* same shape, values */
+  const void* const* drf_k;           /* host array [draft.layers]; NULL without a draft */
+  const void* const* drf_v;
+} spec_seq_init;
+
+/* Bytes of device workspace spec_init needs (KV caches, positions, rotary
+ * table, activations, partial sums, per-sequence state). */
+spec_status spec_workspace_bytes(const spec_config* cfg, const spec_seq_init* seqs /* [batch] */,
+                                 size_t* bytes);
+
+/* Creates a context.  embed: [vocab][hidden] bf16 device, the tied token
+ * embedding and LM head shared by target and draft.  draft must be NULL
+ * exactly when cfg->draft.layers == 0 (then draft_step is unavailable and
+ * spec_verify needs explicit draft tokens).
+ * The workspace (device, 256-byte aligned, at least spec_workspace_bytes) is
+ * owned by the caller and must outlive the context; the library allocates no
+ * device memory of its own.  Prefix K/V may be freed once the stream has
+ * passed this call.  Builds the 3D position table and the cos/sin table,
+ * rotates the prefix keys of every layer into the caches, and leaves the
+ * context READY. */
+spec_status spec_init(const spec_config* cfg, const void* embed,
+                      const spec_model_weights* target, const spec_model_weights* draft,
+                      const spec_seq_init* seqs, void* workspace, size_t workspace_bytes,
+                      hipStream_t stream, spec_ctx** out);
+
+/* One draft step (Eq. propose as a chain of single-token steps).  The draft
+ * first consumes the committed tokens it has not yet seen (one row normally,
+ * up to K+1 after the verifier overrode its proposals), then proposes a token
+ * from its last row with a greedy argmax.  Call j (0-based) of a round writes
+ * column j of d_draft_tokens [batch][K] (device int32; may be NULL).
+ * State: READY or DRAFTING with fewer than K steps taken -> DRAFTING. */
+spec_status draft_step(spec_ctx* ctx, int32_t* d_draft_tokens);
+
+/* One verify pass (Eq. verify, Eq. accept).  Rows [pending, d_1..d_K] of every
+ * sequence go through the target in one forward pass; row j's greedy token is
+ * r*_{j+1} (argmax over fp32 logits, lowest index on ties, NaN as -inf).
+ * d_draft_tokens: [batch][K] device int32 proposals, or NULL to use the
+ * draft's own K proposals of this round.  d_logits: [batch][K+1][vocab] bf16
+ * device output, or NULL.  Finished sequences are skipped.
+ * State: READY (with d_draft_tokens, or K == 0) or DRAFTING after K steps -> VERIFIED. */
+spec_status spec_verify(spec_ctx* ctx, const int32_t* d_draft_tokens, void* d_logits);
+
+/* Commit (Eq. commit): appends (d_1..d_l, r*_{l+1}), cut after a stop token
+ * or at the token budget, to each unfinished sequence; the target keeps KV
+ * slots up to the new length and the draft keeps the slots whose inputs still
+ * match the committed tokens (the rest are rolled back and later
+ * overwritten).  Optional device outputs (int32): d_accept_len [batch] = l,
+ * d_committed [batch][K+1] (first d_n_committed[b] entries valid),
+ * d_n_committed [batch], d_finished [batch].
+ * State: VERIFIED -> READY. */
+spec_status spec_commit(spec_ctx* ctx, int32_t* d_accept_len, int32_t* d_committed,
+                        int32_t* d_n_committed, int32_t* d_finished);
+
+/* Synchronising: waits for the stream, then reports how many sequences have
+ * finished (*n_finished, may be NULL) and returns SPEC_E_INVAL / SPEC_E_NUMERIC
+ * if a device-side check failed since spec_init (an out-of-range draft token,
+ * which was replaced by token 0, or NaN logits). */
+spec_status spec_sync(spec_ctx* ctx, int32_t* n_finished);
+
+void spec_destroy(spec_ctx* ctx);
+
+/* Text of the last error of this context (or of the last failed spec_init if
+ * ctx is NULL).  Valid until the next call on the context. */
+const char* spec_last_error(const spec_ctx* ctx);
+
+/* ---- inspection (synchronising; for tests and tools) --------------------- */
+
+/* 3D positions (p_T, p_H, p_W) of sequence b's slots 0..len-1 into
+ * host_out [3][len] int32.  len <= capacity. */
+spec_status spec_debug_positions(spec_ctx* ctx, int32_t b, int32_t* host_out, int32_t len);
+
+/* Sequence b's state into host_out [8] int32: seq_len (slots with target KV =
+ * index of the pending token), draft_len, pending token, committed-token
+ * count, finished, accept length of the last verify, tokens committed by the
+ * last commit, device error bits. */
+spec_status spec_debug_state(spec_ctx* ctx, int32_t b, int32_t* host_out);
+
+/* Cached keys (which = 0, after rotation) or values (which = 1) of sequence
+ * b, model 0 = target / 1 = draft, layer, slots [pos0, pos0+npos) into
+ * host_out [npos][kv_heads][head_dim] bf16. */
+spec_status spec_debug_kv(spec_ctx* ctx, int32_t b, int32_t model, int32_t layer, int32_t which,
+                          int32_t pos0, int32_t npos, void* host_out);
+
+/* Per-kernel timing with HIP events on the context's stream.  While enabled,
+ * calls launch kernels one by one (no graph replay) and bracket each launch
+ * with events.  spec_timing_read (synchronising) returns, for kernel class
+ * `kind`, the number of launches, their summed duration in milliseconds and
+ * the summed algorithmic bytes (weights and activations each launch must
+ * move; 0 for kinds without a byte model) since timing was last enabled. */
+enum spec_kernel_kind {
+  SPEC_KERNEL_GEMV = 0,      /* weight-streaming projections of every layer */
+  SPEC_KERNEL_LMHEAD = 1,    /* tied LM head with the fused per-tile argmax */
+  SPEC_KERNEL_ATTN = 2,      /* split-KV attention */
+  SPEC_KERNEL_OTHER = 3,     /* norms, rotary + KV append, combine, accept, commit */
+  SPEC_KERNEL_KINDS = 4
+};
+spec_status spec_timing(spec_ctx* ctx, int32_t enable);
+spec_status spec_timing_read(spec_ctx* ctx, int32_t kind, int64_t* launches, double* ms, double* bytes);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* SPECDEC_SPEC_H */

@@ -1,0 +1,138 @@
+// Internal definitions shared by the host runtime (runtime.cpp) and the
+// gfx950 kernels (kernels.hip).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include <string>
+#include <vector>
+
+#include "../../include/spec.h"
+
+namespace specdec {
+
+typedef uint16_t bf16_t;
+
+constexpr int kMaxRows = SPEC_MAX_K + 1;     // rows per sequence in one pass
+constexpr int kTile = 16;                    // output rows per GEMV tile (one MFMA block)
+constexpr int kKeyBlock = 32;                // keys per attention inner step
+
+// Per-sequence state, resident in device memory.  Only kernels change it
+// between spec_init and spec_destroy, so a captured graph stays valid for
+// every round.
+struct SeqState {
+  int32_t seq_len;      // slots holding target K/V = index of the pending token
+  int32_t draft_len;    // slots holding draft K/V
+  int32_t pending;      // token at index seq_len
+  int32_t n_gen;        // committed tokens so far
+  int32_t finished;
+  int32_t dstep;        // draft steps taken this round
+  int32_t accept_len;   // l of the last verify
+  int32_t n_commit;     // tokens the last verify commits (after stop / budget cut)
+  int32_t fin_pending;  // the last verify ends the sequence
+  int32_t err;          // sticky ERR_* bits
+  int32_t prefix_len;
+  int32_t want_logits;  // the current verify copies bf16 logits out
+  int32_t base;         // slot of row 0 of the current pass
+  int32_t count;        // valid rows of the current pass (0 when idle)
+  int32_t pad[2];
+  int32_t vtok[kMaxRows];       // verify rows: pending, d_1..d_K
+  int32_t rstar[kMaxRows];      // greedy token of each verify row
+  int32_t committed[kMaxRows];  // tokens of the last verify to commit
+  int32_t props[kMaxRows];      // the draft's own proposals this round
+};
+
+enum { ERR_TOKEN = 1, ERR_NUMERIC = 2, ERR_STATE = 4 };
+
+enum PassMode { PASS_VERIFY = 0, PASS_DRAFT = 1 };
+
+struct LayerW {
+  const bf16_t *attn_norm, *wq, *wk, *wv, *wo, *ffn_norm, *wg, *wu, *wd;
+};
+
+struct Model {
+  spec_dims d{};
+  bool flat = false;                // FlatRoPE (draft) instead of 3D M-RoPE (target)
+  std::vector<LayerW> L;
+  const bf16_t* final_norm = nullptr;
+  bf16_t* kc = nullptr;             // [layers][B][kv_heads][cap][head_dim], rotated keys
+  bf16_t* vt = nullptr;             // [layers][B][kv_heads][head_dim][cap], values transposed
+  int8_t* axis = nullptr;           // [head_dim/2] axis (0 T, 1 H, 2 W) of each rotary pair
+  int s_qkv = 1, s_o = 1, s_gu = 1, s_down = 1;   // GEMV k-splits
+  size_t kv_layer = 0;              // elements of one layer's key (or value) cache
+};
+
+struct TimingRec {
+  int kind;
+  double bytes;
+  hipEvent_t e0, e1;
+};
+
+struct Ctx {
+  spec_config cfg{};
+  int B = 1, K = 0, R = 1, M = 1, Mpad = 16, V = 0, cap = 0;
+  int attn_chunk = 128, attn_splits = 1;
+  hipStream_t stream = nullptr;      // caller's stream
+  hipStream_t cap_stream = nullptr;  // private stream used only for graph capture
+  int device = 0;
+
+  // workspace carve-out
+  SeqState* st = nullptr;           // [B]
+  int32_t* hist = nullptr;          // [B][cap] token at each index >= prefix_len
+  int32_t* pos3 = nullptr;          // [B][3][cap] target rotary positions
+  float2* cs = nullptr;             // [cap][head_dim/2] (cos, sin) of theta_d * p
+  float* x = nullptr;               // [Mpad][hidden] residual stream
+  bf16_t* a = nullptr;              // [Mpad][hidden] normalised GEMV input
+  bf16_t* q = nullptr;              // [Mpad][q_heads*head_dim] rotated queries
+  bf16_t* o = nullptr;              // [Mpad][q_heads*head_dim] attention output
+  bf16_t* u = nullptr;              // [Mpad][ffn] SwiGLU output (max of both models)
+  float* part = nullptr;            // GEMV k-split partial sums
+  size_t part_elems = 0;
+  float* op = nullptr;              // [splits][B][q_heads][R][head_dim] attention partials
+  float* mp = nullptr;              // [splits][B][q_heads][R] running max (log2 units)
+  float* lp = nullptr;              // [splits][B][q_heads][R] running sum
+  float* amax_v = nullptr;          // [vocab/16][Mpad] per-tile maximum logit
+  int32_t* amax_i = nullptr;        // [vocab/16][Mpad] its index
+  bf16_t* logits = nullptr;         // [Mpad][vocab] bf16 logits of the last verify
+  bf16_t* a_last = nullptr;         // [16][hidden] draft: normalised last row per sequence
+
+  const bf16_t* embed = nullptr;
+  Model tgt, drf;
+  bool has_draft = false;
+
+  // host state machine
+  enum Phase { READY = 0, DRAFTING = 1, VERIFIED = 2 } phase = READY;
+  int dsteps = 0;
+  bool poisoned = false;
+  std::string err;
+
+  // graphs
+  bool use_graphs = true;
+  hipGraphExec_t g_verify = nullptr, g_draft = nullptr;
+
+  // timing
+  bool timing = false;
+  std::vector<TimingRec> trec;
+  std::vector<hipEvent_t> ev_pool;
+  size_t ev_used = 0;
+  int64_t t_launches[SPEC_KERNEL_KINDS] = {};
+  double t_ms[SPEC_KERNEL_KINDS] = {}, t_bytes[SPEC_KERNEL_KINDS] = {};
+};
+
+// ---- launchers (kernels.hip) ------------------------------------------------
+// Each returns hipSuccess or the launch error.
+
+hipError_t launch_zero(Ctx& c, void* p, size_t bytes);
+hipError_t launch_prefix_kv(Ctx& c, Model& m, int layer, int b, int prefix_len,
+                            const bf16_t* k_pre, const bf16_t* v);
+hipError_t launch_stage_verify(Ctx& c, const int32_t* d_override, int want_logits);
+hipError_t launch_forward(Ctx& c, PassMode mode);   // embed .. accept / draft pick
+hipError_t launch_draft_out(Ctx& c, int32_t* d_tokens);
+hipError_t launch_commit(Ctx& c, int32_t* acc, int32_t* committed, int32_t* ncommit, int32_t* fin);
+hipError_t launch_logits_out(Ctx& c, void* d_logits);
+
+// GEMV k-split choice for an [N][Kd] weight (also used to size the partials).
+int pick_splits(int N, int Kd);
+
+}  // namespace specdec

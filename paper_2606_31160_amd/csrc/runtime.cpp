@@ -1,0 +1,711 @@
+// Host runtime behind include/spec.h: validation, workspace carving, the 3D
+// position table and the rotary (cos, sin) table, the call state machine,
+// HIP-graph capture and per-kernel event timing.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cmath>
+#include <cstdio>
+#include <cstring>
+#include <exception>
+#include <new>
+#include <string>
+#include <vector>
+
+#include "ctx.h"
+
+using namespace specdec;
+
+struct spec_ctx {
+  Ctx c;
+};
+
+namespace {
+
+thread_local std::string g_init_error;
+
+constexpr size_t kAlign = 256;
+
+size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
+
+struct Carver {
+  char* base;
+  size_t off = 0;
+  template <class T>
+  T* take(size_t n) {
+    off = align_up(off, kAlign);
+    T* p = base ? reinterpret_cast<T*>(base + off) : nullptr;
+    off += n * sizeof(T);
+    return p;
+  }
+};
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+// ---- validation -------------------------------------------------------------
+
+bool check_dims(const spec_dims& d, bool is_target, std::string& err, const char* who) {
+  char buf[256];
+  auto bad = [&](const char* what) {
+    snprintf(buf, sizeof buf, "%s: %s", who, what);
+    err = buf;
+    return false;
+  };
+  if (d.layers < 1 || d.layers > SPEC_MAX_LAYERS) return bad("layers out of range");
+  if (d.hidden < 16 || d.hidden % 16) return bad("hidden must be a positive multiple of 16");
+  if (d.head_dim != 64 && d.head_dim != 128) return bad("head_dim must be 64 or 128");
+  if (d.kv_heads < 1 || d.q_heads < 1 || d.q_heads % d.kv_heads) return bad("q_heads must be a multiple of kv_heads");
+  if ((d.q_heads * d.head_dim) % 16) return bad("q_heads*head_dim must be a multiple of 16");
+  if (d.ffn < 16 || d.ffn % 16) return bad("ffn must be a positive multiple of 16");
+  if (!(d.rope_base > 1.0f) || !std::isfinite(d.rope_base)) return bad("rope_base must be > 1");
+  if (!(d.rms_eps >= 0.0f) || !std::isfinite(d.rms_eps)) return bad("rms_eps must be >= 0");
+  if (is_target) {
+    if (d.interleaved != 0 && d.interleaved != 1) return bad("interleaved must be 0 or 1");
+    const int* s = d.mrope_section;
+    if (s[0] < 0 || s[1] < 0 || s[2] < 0 || s[0] + s[1] + s[2] != d.head_dim / 2)
+      return bad("mrope_section must be non-negative and sum to head_dim/2");
+  }
+  return true;
+}
+
+bool check_config(const spec_config* cfg, const spec_seq_init* seqs, bool has_draft, std::string& err) {
+  if (!cfg || !seqs) {
+    err = "null config or sequences";
+    return false;
+  }
+  if (cfg->batch < 1 || cfg->batch > SPEC_MAX_BATCH) {
+    err = "batch out of range";
+    return false;
+  }
+  if (cfg->K < 0 || cfg->K > SPEC_MAX_K) {
+    err = "K out of range";
+    return false;
+  }
+  if (cfg->batch * (cfg->K + 1) > 64) {
+    err = "batch*(K+1) rows per pass must not exceed 64";
+    return false;
+  }
+  if (cfg->vocab < 16 || cfg->vocab % 16) {
+    err = "vocab must be a positive multiple of 16";
+    return false;
+  }
+  if (cfg->max_new_tokens < 1) {
+    err = "max_new_tokens must be >= 1";
+    return false;
+  }
+  if (cfg->stop_token < -1 || cfg->stop_token >= cfg->vocab) {
+    err = "stop_token out of range";
+    return false;
+  }
+  if (!check_dims(cfg->target, true, err, "target")) return false;
+  if (has_draft) {
+    if (!check_dims(cfg->draft, false, err, "draft")) return false;
+    if (cfg->draft.hidden != cfg->target.hidden || cfg->draft.head_dim != cfg->target.head_dim ||
+        cfg->draft.rope_base != cfg->target.rope_base) {
+      err = "draft hidden, head_dim and rope_base must equal the target's";
+      return false;
+    }
+  }
+  for (int b = 0; b < cfg->batch; ++b) {
+    const spec_seq_init& s = seqs[b];
+    char buf[160];
+    if (s.prefix_len < 1) {
+      snprintf(buf, sizeof buf, "sequence %d: prefix_len must be >= 1", b);
+      err = buf;
+      return false;
+    }
+    if (s.pending_token < 0 || s.pending_token >= cfg->vocab) {
+      snprintf(buf, sizeof buf, "sequence %d: pending_token out of range", b);
+      err = buf;
+      return false;
+    }
+    if (s.n_blocks < 0 || (s.n_blocks > 0 && !s.blocks)) {
+      snprintf(buf, sizeof buf, "sequence %d: bad vision blocks", b);
+      err = buf;
+      return false;
+    }
+    std::vector<char> taken(s.prefix_len, 0);
+    for (int i = 0; i < s.n_blocks; ++i) {
+      const spec_vision_block& v = s.blocks[i];
+      const long long n = (long long)v.t * v.h * v.w;
+      if (v.t < 1 || v.h < 1 || v.w < 1 || v.start < 0 || v.start + n > s.prefix_len) {
+        snprintf(buf, sizeof buf, "sequence %d: vision block %d outside [0, prefix_len)", b, i);
+        err = buf;
+        return false;
+      }
+      for (long long k = v.start; k < v.start + n; ++k) {
+        if (taken[k]) {
+          snprintf(buf, sizeof buf, "sequence %d: vision blocks overlap", b);
+          err = buf;
+          return false;
+        }
+        taken[k] = 1;
+      }
+    }
+    if (!s.tgt_k || !s.tgt_v) {
+      snprintf(buf, sizeof buf, "sequence %d: missing target prefix K/V", b);
+      err = buf;
+      return false;
+    }
+    for (int l = 0; l < cfg->target.layers; ++l)
+      if (!s.tgt_k[l] || !s.tgt_v[l] || !aligned16(s.tgt_k[l]) || !aligned16(s.tgt_v[l])) {
+        snprintf(buf, sizeof buf, "sequence %d: target prefix K/V of layer %d null or misaligned", b, l);
+        err = buf;
+        return false;
+      }
+    if (has_draft) {
+      if (!s.drf_k || !s.drf_v) {
+        snprintf(buf, sizeof buf, "sequence %d: missing draft prefix K/V", b);
+        err = buf;
+        return false;
+      }
+      for (int l = 0; l < cfg->draft.layers; ++l)
+        if (!s.drf_k[l] || !s.drf_v[l] || !aligned16(s.drf_k[l]) || !aligned16(s.drf_v[l])) {
+          snprintf(buf, sizeof buf, "sequence %d: draft prefix K/V of layer %d null or misaligned", b, l);
+          err = buf;
+          return false;
+        }
+    }
+  }
+  return true;
+}
+
+bool check_weights(const spec_model_weights* w, const spec_dims& d, std::string& err, const char* who) {
+  char buf[160];
+  if (!w || !w->layers || !w->final_norm || !aligned16(w->final_norm)) {
+    snprintf(buf, sizeof buf, "%s weights: null or misaligned", who);
+    err = buf;
+    return false;
+  }
+  for (int l = 0; l < d.layers; ++l) {
+    const spec_layer_weights& L = w->layers[l];
+    const void* ps[] = {L.attn_norm, L.wq, L.wk, L.wv, L.wo, L.ffn_norm, L.w_gate, L.w_up, L.w_down};
+    for (const void* p : ps)
+      if (!p || !aligned16(p)) {
+        snprintf(buf, sizeof buf, "%s weights: layer %d has a null or misaligned tensor", who, l);
+        err = buf;
+        return false;
+      }
+  }
+  return true;
+}
+
+// ---- layout -------------------------------------------------------------------
+
+struct Layout {
+  int B, K, R, M, Mpad, V, cap, chunk, splits;
+};
+
+Layout make_layout(const spec_config* cfg, const spec_seq_init* seqs) {
+  Layout L{};
+  L.B = cfg->batch;
+  L.K = cfg->K;
+  L.R = cfg->K + 1;
+  L.M = L.B * L.R;
+  L.Mpad = (int)align_up(L.M, 16);
+  L.V = cfg->vocab;
+  int maxP = 0;
+  for (int b = 0; b < L.B; ++b) maxP = std::max(maxP, seqs[b].prefix_len);
+  L.cap = (int)align_up((size_t)maxP + cfg->max_new_tokens + cfg->K + 2, 64);
+  L.chunk = 128;
+  if (const char* e = getenv("SPECDEC_ATTN_CHUNK")) {
+    const int v = atoi(e);
+    if (v >= 32 && v % 32 == 0) L.chunk = v;
+  }
+  L.splits = (L.cap + L.chunk - 1) / L.chunk;
+  return L;
+}
+
+void set_splits(Model& m) {
+  const spec_dims& d = m.d;
+  m.s_qkv = pick_splits((d.q_heads + 2 * d.kv_heads) * d.head_dim, d.hidden);
+  m.s_o = pick_splits(d.hidden, d.q_heads * d.head_dim);
+  m.s_gu = pick_splits(2 * d.ffn, d.hidden);
+  m.s_down = pick_splits(d.hidden, d.ffn);
+}
+
+size_t part_elems_for(const Model& m, int M) {
+  const spec_dims& d = m.d;
+  size_t e = 0;
+  e = std::max(e, (size_t)m.s_qkv * M * (d.q_heads + 2 * d.kv_heads) * d.head_dim);
+  e = std::max(e, (size_t)m.s_o * M * d.hidden);
+  e = std::max(e, (size_t)m.s_gu * M * 2 * d.ffn);
+  e = std::max(e, (size_t)m.s_down * M * d.hidden);
+  return e;
+}
+
+// Carves the workspace (base == nullptr only measures).  Returns total bytes.
+size_t carve(Ctx& c, const spec_config* cfg, const spec_seq_init* seqs, bool has_draft, char* base) {
+  const Layout L = make_layout(cfg, seqs);
+  c.B = L.B;
+  c.K = L.K;
+  c.R = L.R;
+  c.M = L.M;
+  c.Mpad = L.Mpad;
+  c.V = L.V;
+  c.cap = L.cap;
+  c.attn_chunk = L.chunk;
+  c.attn_splits = L.splits;
+  c.tgt.d = cfg->target;
+  c.tgt.flat = false;
+  set_splits(c.tgt);
+  if (has_draft) {
+    c.drf.d = cfg->draft;
+    c.drf.flat = true;
+    set_splits(c.drf);
+  }
+  const spec_dims& t = cfg->target;
+  const int H = t.hidden, D = t.head_dim;
+  int nqD = t.q_heads * D, F = t.ffn, nq = t.q_heads;
+  size_t part = part_elems_for(c.tgt, L.M);
+  if (has_draft) {
+    nqD = std::max(nqD, cfg->draft.q_heads * D);
+    F = std::max(F, cfg->draft.ffn);
+    nq = std::max(nq, cfg->draft.q_heads);
+    part = std::max(part, part_elems_for(c.drf, L.M));
+  }
+  Carver cv{base};
+  c.st = cv.take<SeqState>(L.B);
+  c.hist = cv.take<int32_t>((size_t)L.B * L.cap);
+  c.pos3 = cv.take<int32_t>((size_t)L.B * 3 * L.cap);
+  c.cs = cv.take<float2>((size_t)L.cap * (D / 2));
+  c.tgt.axis = cv.take<int8_t>(D / 2);
+  c.drf.axis = cv.take<int8_t>(D / 2);
+  c.x = cv.take<float>((size_t)L.Mpad * H);
+  c.a = cv.take<bf16_t>((size_t)L.Mpad * H);
+  c.q = cv.take<bf16_t>((size_t)L.Mpad * nqD);
+  c.o = cv.take<bf16_t>((size_t)L.Mpad * nqD);
+  c.u = cv.take<bf16_t>((size_t)L.Mpad * F);
+  c.part = cv.take<float>(part);
+  c.part_elems = part;
+  const size_t attn_rows = (size_t)L.splits * L.B * nq * L.R;
+  c.op = cv.take<float>(attn_rows * D);
+  c.mp = cv.take<float>(attn_rows);
+  c.lp = cv.take<float>(attn_rows);
+  c.amax_v = cv.take<float>((size_t)(L.V / kTile) * L.Mpad);
+  c.amax_i = cv.take<int32_t>((size_t)(L.V / kTile) * L.Mpad);
+  c.logits = cv.take<bf16_t>((size_t)L.Mpad * L.V);
+  c.a_last = cv.take<bf16_t>((size_t)16 * H);
+  c.tgt.kv_layer = (size_t)L.B * t.kv_heads * L.cap * D;
+  c.tgt.kc = cv.take<bf16_t>(c.tgt.kv_layer * t.layers);
+  c.tgt.vt = cv.take<bf16_t>(c.tgt.kv_layer * t.layers);
+  if (has_draft) {
+    c.drf.kv_layer = (size_t)L.B * cfg->draft.kv_heads * L.cap * D;
+    c.drf.kc = cv.take<bf16_t>(c.drf.kv_layer * cfg->draft.layers);
+    c.drf.vt = cv.take<bf16_t>(c.drf.kv_layer * cfg->draft.layers);
+  }
+  return align_up(cv.off, kAlign);
+}
+
+// (p_T, p_H, p_W) per index: text -> (i, i, i); patch (t, h, w) of a block
+// starting at s -> (s+t, s+h, s+w) (Sec. 3.3, Sec. 4.2).
+void build_positions(const spec_seq_init& s, int cap, int32_t* out) {
+  for (int i = 0; i < cap; ++i) out[i] = out[cap + i] = out[2 * cap + i] = i;
+  for (int k = 0; k < s.n_blocks; ++k) {
+    const spec_vision_block& v = s.blocks[k];
+    int idx = v.start;
+    for (int t = 0; t < v.t; ++t)
+      for (int h = 0; h < v.h; ++h)
+        for (int w = 0; w < v.w; ++w, ++idx) {
+          out[idx] = v.start + t;
+          out[cap + idx] = v.start + h;
+          out[2 * cap + idx] = v.start + w;
+        }
+  }
+}
+
+// a(d) of Eq. axis-assign.
+void build_axis(const spec_dims& d, bool flat, int8_t* out) {
+  const int half = d.head_dim / 2;
+  for (int i = 0; i < half; ++i) {
+    if (flat) {
+      out[i] = 0;
+    } else if (d.interleaved) {
+      out[i] = (int8_t)(i % 3);
+    } else {
+      out[i] = (int8_t)(i < d.mrope_section[0] ? 0 : (i < d.mrope_section[0] + d.mrope_section[1] ? 1 : 2));
+    }
+  }
+}
+
+spec_status fail_hip(Ctx& c, hipError_t e, const char* where) {
+  c.poisoned = true;
+  c.err = std::string(where) + ": " + hipGetErrorString(e);
+  return SPEC_E_HIP;
+}
+
+spec_status set_err(Ctx& c, spec_status s, const char* msg) {
+  c.err = msg;
+  return s;
+}
+
+#define HIPCHK(c, expr, where)                       \
+  do {                                               \
+    hipError_t e_ = (expr);                          \
+    if (e_ != hipSuccess) return fail_hip(c, e_, where); \
+  } while (0)
+
+// Runs one pass either directly or through its captured graph.
+spec_status run_pass(Ctx& c, PassMode mode) {
+  const bool graphs = c.use_graphs && !c.timing;
+  if (!graphs) {
+    HIPCHK(c, launch_forward(c, mode), "forward pass");
+    return SPEC_OK;
+  }
+  hipGraphExec_t& ge = mode == PASS_VERIFY ? c.g_verify : c.g_draft;
+  if (!ge) {
+    if (!c.cap_stream) HIPCHK(c, hipStreamCreateWithFlags(&c.cap_stream, hipStreamNonBlocking), "capture stream");
+    hipStream_t user = c.stream;
+    c.stream = c.cap_stream;
+    hipGraph_t g = nullptr;
+    hipError_t e = hipStreamBeginCapture(c.cap_stream, hipStreamCaptureModeThreadLocal);
+    hipError_t el = hipSuccess;
+    if (e == hipSuccess) {
+      el = launch_forward(c, mode);
+      e = hipStreamEndCapture(c.cap_stream, &g);
+    }
+    c.stream = user;
+    if (el != hipSuccess) {
+      if (g) (void)hipGraphDestroy(g);
+      return fail_hip(c, el, "graph capture launch");
+    }
+    HIPCHK(c, e, "graph capture");
+    e = hipGraphInstantiate(&ge, g, nullptr, nullptr, 0);
+    (void)hipGraphDestroy(g);
+    HIPCHK(c, e, "graph instantiate");
+  }
+  HIPCHK(c, hipGraphLaunch(ge, c.stream), "graph launch");
+  return SPEC_OK;
+}
+
+template <class F>
+spec_status guarded(spec_ctx* ctx, F f) {
+  if (!ctx) return SPEC_E_INVAL;
+  if (ctx->c.poisoned) return SPEC_E_HIP;
+  try {
+    return f(ctx->c);
+  } catch (const std::bad_alloc&) {
+    ctx->c.err = "host out of memory";
+    return SPEC_E_CAPACITY;
+  } catch (const std::exception& ex) {
+    ctx->c.err = ex.what();
+    return SPEC_E_INVAL;
+  }
+}
+
+}  // namespace
+
+extern "C" {
+
+spec_status spec_workspace_bytes(const spec_config* cfg, const spec_seq_init* seqs, size_t* bytes) {
+  if (!cfg || !seqs || !bytes) return SPEC_E_INVAL;
+  try {
+    std::string err;
+    const bool has_draft = cfg->draft.layers > 0;
+    if (!check_config(cfg, seqs, has_draft, err)) {
+      g_init_error = err;
+      return SPEC_E_INVAL;
+    }
+    Ctx c;
+    *bytes = carve(c, cfg, seqs, has_draft, nullptr);
+    return SPEC_OK;
+  } catch (...) {
+    return SPEC_E_INVAL;
+  }
+}
+
+spec_status spec_init(const spec_config* cfg, const void* embed, const spec_model_weights* target,
+                      const spec_model_weights* draft, const spec_seq_init* seqs, void* workspace,
+                      size_t workspace_bytes, hipStream_t stream, spec_ctx** out) {
+  if (!out) return SPEC_E_INVAL;
+  *out = nullptr;
+  std::string err;
+  const bool has_draft = cfg && cfg->draft.layers > 0;
+  if (cfg && has_draft != (draft != nullptr)) {
+    g_init_error = "draft weights must be given exactly when draft.layers > 0";
+    return SPEC_E_INVAL;
+  }
+  if (!check_config(cfg, seqs, has_draft, err)) {
+    g_init_error = err;
+    return SPEC_E_INVAL;
+  }
+  if (!embed || !aligned16(embed)) {
+    g_init_error = "embed: null or misaligned";
+    return SPEC_E_INVAL;
+  }
+  if (!check_weights(target, cfg->target, err, "target") ||
+      (has_draft && !check_weights(draft, cfg->draft, err, "draft"))) {
+    g_init_error = err;
+    return SPEC_E_INVAL;
+  }
+  if (!workspace || (reinterpret_cast<uintptr_t>(workspace) % kAlign)) {
+    g_init_error = "workspace: null or not 256-byte aligned";
+    return SPEC_E_INVAL;
+  }
+  spec_ctx* ctx = nullptr;
+  try {
+    ctx = new spec_ctx();
+    Ctx& c = ctx->c;
+    const size_t need = carve(c, cfg, seqs, has_draft, nullptr);
+    if (workspace_bytes < need) {
+      g_init_error = "workspace too small (query spec_workspace_bytes)";
+      delete ctx;
+      return SPEC_E_CAPACITY;
+    }
+    carve(c, cfg, seqs, has_draft, static_cast<char*>(workspace));
+    c.cfg = *cfg;
+    c.stream = stream;
+    c.has_draft = has_draft;
+    c.use_graphs = !(cfg->flags & SPEC_FLAG_NO_GRAPHS);
+    c.embed = static_cast<const bf16_t*>(embed);
+    auto load_model = [&](Model& m, const spec_model_weights* w) {
+      m.final_norm = static_cast<const bf16_t*>(w->final_norm);
+      m.L.resize(m.d.layers);
+      for (int l = 0; l < m.d.layers; ++l) {
+        const spec_layer_weights& s = w->layers[l];
+        m.L[l] = LayerW{static_cast<const bf16_t*>(s.attn_norm), static_cast<const bf16_t*>(s.wq),
+                        static_cast<const bf16_t*>(s.wk),        static_cast<const bf16_t*>(s.wv),
+                        static_cast<const bf16_t*>(s.wo),        static_cast<const bf16_t*>(s.ffn_norm),
+                        static_cast<const bf16_t*>(s.w_gate),    static_cast<const bf16_t*>(s.w_up),
+                        static_cast<const bf16_t*>(s.w_down)};
+      }
+    };
+    load_model(c.tgt, target);
+    if (has_draft) load_model(c.drf, draft);
+    if (hipGetDevice(&c.device) != hipSuccess) c.device = 0;
+
+    // host-built tables
+    const int D = cfg->target.head_dim, half = D / 2;
+    std::vector<int32_t> pos((size_t)c.B * 3 * c.cap);
+    for (int b = 0; b < c.B; ++b) build_positions(seqs[b], c.cap, pos.data() + (size_t)b * 3 * c.cap);
+    std::vector<float2> cs((size_t)c.cap * half);
+    for (int p = 0; p < c.cap; ++p)
+      for (int d = 0; d < half; ++d) {
+        const double th = std::pow((double)cfg->target.rope_base, -2.0 * d / D);
+        const double ang = th * (double)p;
+        cs[(size_t)p * half + d] = make_float2((float)std::cos(ang), (float)std::sin(ang));
+      }
+    std::vector<int8_t> ax_t(half), ax_d(half);
+    build_axis(cfg->target, false, ax_t.data());
+    build_axis(cfg->draft, true, ax_d.data());
+    std::vector<SeqState> st(c.B);
+    std::vector<int32_t> hist((size_t)c.B * c.cap, 0);
+    for (int b = 0; b < c.B; ++b) {
+      SeqState s{};
+      s.seq_len = seqs[b].prefix_len;
+      s.draft_len = seqs[b].prefix_len;
+      s.pending = seqs[b].pending_token;
+      s.prefix_len = seqs[b].prefix_len;
+      st[b] = s;
+      hist[(size_t)b * c.cap + seqs[b].prefix_len] = seqs[b].pending_token;
+    }
+
+    auto hip_fail = [&](hipError_t e, const char* where) {
+      g_init_error = std::string(where) + ": " + hipGetErrorString(e);
+      delete ctx;
+      return SPEC_E_HIP;
+    };
+    hipError_t e;
+    if ((e = launch_zero(c, workspace, need)) != hipSuccess) return hip_fail(e, "workspace clear");
+    if ((e = hipMemcpyAsync(c.pos3, pos.data(), pos.size() * 4, hipMemcpyHostToDevice, stream)) != hipSuccess ||
+        (e = hipMemcpyAsync(c.cs, cs.data(), cs.size() * sizeof(float2), hipMemcpyHostToDevice, stream)) !=
+            hipSuccess ||
+        (e = hipMemcpyAsync(c.tgt.axis, ax_t.data(), half, hipMemcpyHostToDevice, stream)) != hipSuccess ||
+        (e = hipMemcpyAsync(c.drf.axis, ax_d.data(), half, hipMemcpyHostToDevice, stream)) != hipSuccess ||
+        (e = hipMemcpyAsync(c.st, st.data(), st.size() * sizeof(SeqState), hipMemcpyHostToDevice, stream)) !=
+            hipSuccess ||
+        (e = hipMemcpyAsync(c.hist, hist.data(), hist.size() * 4, hipMemcpyHostToDevice, stream)) != hipSuccess)
+      return hip_fail(e, "table upload");
+    for (int b = 0; b < c.B; ++b) {
+      for (int l = 0; l < c.tgt.d.layers; ++l)
+        if ((e = launch_prefix_kv(c, c.tgt, l, b, seqs[b].prefix_len, static_cast<const bf16_t*>(seqs[b].tgt_k[l]),
+                                  static_cast<const bf16_t*>(seqs[b].tgt_v[l]))) != hipSuccess)
+          return hip_fail(e, "prefix K/V");
+      if (has_draft)
+        for (int l = 0; l < c.drf.d.layers; ++l)
+          if ((e = launch_prefix_kv(c, c.drf, l, b, seqs[b].prefix_len,
+                                    static_cast<const bf16_t*>(seqs[b].drf_k[l]),
+                                    static_cast<const bf16_t*>(seqs[b].drf_v[l]))) != hipSuccess)
+            return hip_fail(e, "prefix K/V");
+    }
+    // The host tables above are pageable and local: wait for the uploads.
+    if ((e = hipStreamSynchronize(stream)) != hipSuccess) return hip_fail(e, "init sync");
+    *out = ctx;
+    return SPEC_OK;
+  } catch (const std::bad_alloc&) {
+    delete ctx;
+    g_init_error = "host out of memory";
+    return SPEC_E_CAPACITY;
+  } catch (const std::exception& ex) {
+    delete ctx;
+    g_init_error = ex.what();
+    return SPEC_E_INVAL;
+  }
+}
+
+spec_status draft_step(spec_ctx* ctx, int32_t* d_draft_tokens) {
+  return guarded(ctx, [&](Ctx& c) -> spec_status {
+    if (!c.has_draft) return set_err(c, SPEC_E_STATE, "draft_step: no draft model");
+    if (c.K < 1) return set_err(c, SPEC_E_STATE, "draft_step: K is 0");
+    if (c.phase == Ctx::VERIFIED) return set_err(c, SPEC_E_STATE, "draft_step: commit the last verify first");
+    if (c.dsteps >= c.K) return set_err(c, SPEC_E_STATE, "draft_step: K steps already taken this round");
+    spec_status s = run_pass(c, PASS_DRAFT);
+    if (s != SPEC_OK) return s;
+    HIPCHK(c, launch_draft_out(c, d_draft_tokens), "draft output");
+    c.dsteps += 1;
+    c.phase = Ctx::DRAFTING;
+    return SPEC_OK;
+  });
+}
+
+spec_status spec_verify(spec_ctx* ctx, const int32_t* d_draft_tokens, void* d_logits) {
+  return guarded(ctx, [&](Ctx& c) -> spec_status {
+    if (c.phase == Ctx::VERIFIED) return set_err(c, SPEC_E_STATE, "spec_verify: commit the last verify first");
+    if (!d_draft_tokens && c.K > 0 && c.dsteps != c.K)
+      return set_err(c, SPEC_E_STATE, "spec_verify: no draft tokens given and fewer than K draft steps taken");
+    HIPCHK(c, launch_stage_verify(c, c.K > 0 ? d_draft_tokens : nullptr, d_logits ? 1 : 0), "verify staging");
+    spec_status s = run_pass(c, PASS_VERIFY);
+    if (s != SPEC_OK) return s;
+    HIPCHK(c, launch_logits_out(c, d_logits), "logits copy");
+    c.phase = Ctx::VERIFIED;
+    return SPEC_OK;
+  });
+}
+
+spec_status spec_commit(spec_ctx* ctx, int32_t* d_accept_len, int32_t* d_committed, int32_t* d_n_committed,
+                        int32_t* d_finished) {
+  return guarded(ctx, [&](Ctx& c) -> spec_status {
+    if (c.phase != Ctx::VERIFIED) return set_err(c, SPEC_E_STATE, "spec_commit: no verify to commit");
+    HIPCHK(c, launch_commit(c, d_accept_len, d_committed, d_n_committed, d_finished), "commit");
+    c.phase = Ctx::READY;
+    c.dsteps = 0;
+    return SPEC_OK;
+  });
+}
+
+spec_status spec_sync(spec_ctx* ctx, int32_t* n_finished) {
+  return guarded(ctx, [&](Ctx& c) -> spec_status {
+    std::vector<SeqState> st(c.B);
+    HIPCHK(c, hipMemcpyAsync(st.data(), c.st, st.size() * sizeof(SeqState), hipMemcpyDeviceToHost, c.stream),
+           "state read");
+    HIPCHK(c, hipStreamSynchronize(c.stream), "sync");
+    int fin = 0, err = 0;
+    for (const SeqState& s : st) {
+      fin += s.finished ? 1 : 0;
+      err |= s.err;
+    }
+    if (n_finished) *n_finished = fin;
+    if (err & ERR_NUMERIC) return set_err(c, SPEC_E_NUMERIC, "NaN logits seen on the device");
+    if (err & ERR_TOKEN) return set_err(c, SPEC_E_INVAL, "a draft token id was out of range (replaced by 0)");
+    if (err & ERR_STATE) return set_err(c, SPEC_E_STATE, "draft catch-up exceeded K+1 rows");
+    return SPEC_OK;
+  });
+}
+
+void spec_destroy(spec_ctx* ctx) {
+  if (!ctx) return;
+  Ctx& c = ctx->c;
+  if (c.stream) (void)hipStreamSynchronize(c.stream);
+  if (c.g_verify) (void)hipGraphExecDestroy(c.g_verify);
+  if (c.g_draft) (void)hipGraphExecDestroy(c.g_draft);
+  if (c.cap_stream) (void)hipStreamDestroy(c.cap_stream);
+  for (hipEvent_t e : c.ev_pool) (void)hipEventDestroy(e);
+  delete ctx;
+}
+
+const char* spec_last_error(const spec_ctx* ctx) {
+  if (!ctx) return g_init_error.c_str();
+  return ctx->c.err.c_str();
+}
+
+spec_status spec_debug_positions(spec_ctx* ctx, int32_t b, int32_t* host_out, int32_t len) {
+  return guarded(ctx, [&](Ctx& c) -> spec_status {
+    if (b < 0 || b >= c.B || !host_out || len < 0 || len > c.cap) return set_err(c, SPEC_E_INVAL, "bad arguments");
+    HIPCHK(c, hipStreamSynchronize(c.stream), "sync");
+    for (int a = 0; a < 3; ++a)
+      HIPCHK(c, hipMemcpy(host_out + (size_t)a * len, c.pos3 + ((size_t)b * 3 + a) * c.cap, (size_t)len * 4,
+                          hipMemcpyDeviceToHost),
+             "positions read");
+    return SPEC_OK;
+  });
+}
+
+spec_status spec_debug_state(spec_ctx* ctx, int32_t b, int32_t* host_out) {
+  return guarded(ctx, [&](Ctx& c) -> spec_status {
+    if (b < 0 || b >= c.B || !host_out) return set_err(c, SPEC_E_INVAL, "bad arguments");
+    SeqState s;
+    HIPCHK(c, hipStreamSynchronize(c.stream), "sync");
+    HIPCHK(c, hipMemcpy(&s, c.st + b, sizeof s, hipMemcpyDeviceToHost), "state read");
+    const int32_t v[8] = {s.seq_len, s.draft_len, s.pending, s.n_gen, s.finished, s.accept_len, s.n_commit, s.err};
+    memcpy(host_out, v, sizeof v);
+    return SPEC_OK;
+  });
+}
+
+spec_status spec_debug_kv(spec_ctx* ctx, int32_t b, int32_t model, int32_t layer, int32_t which, int32_t pos0,
+                          int32_t npos, void* host_out) {
+  return guarded(ctx, [&](Ctx& c) -> spec_status {
+    if (model != 0 && !(model == 1 && c.has_draft)) return set_err(c, SPEC_E_INVAL, "bad model");
+    Model& m = model == 0 ? c.tgt : c.drf;
+    if (b < 0 || b >= c.B || layer < 0 || layer >= m.d.layers || (which != 0 && which != 1) || pos0 < 0 ||
+        npos < 0 || pos0 + npos > c.cap || !host_out)
+      return set_err(c, SPEC_E_INVAL, "bad arguments");
+    HIPCHK(c, hipStreamSynchronize(c.stream), "sync");
+    const int nkv = m.d.kv_heads, D = m.d.head_dim;
+    bf16_t* out = static_cast<bf16_t*>(host_out);
+    const size_t per_seq = (size_t)nkv * c.cap * D;
+    std::vector<bf16_t> tmp((size_t)npos * D);
+    for (int h = 0; h < nkv; ++h) {
+      if (which == 0) {
+        const bf16_t* src = m.kc + m.kv_layer * layer + per_seq * b + ((size_t)h * c.cap + pos0) * D;
+        HIPCHK(c, hipMemcpy(tmp.data(), src, tmp.size() * 2, hipMemcpyDeviceToHost), "kv read");
+        for (int s = 0; s < npos; ++s) memcpy(out + ((size_t)s * nkv + h) * D, tmp.data() + (size_t)s * D, D * 2);
+      } else {
+        const bf16_t* src = m.vt + m.kv_layer * layer + per_seq * b + (size_t)h * D * c.cap + pos0;
+        HIPCHK(c, hipMemcpy2D(tmp.data(), (size_t)npos * 2, src, (size_t)c.cap * 2, (size_t)npos * 2, D,
+                              hipMemcpyDeviceToHost),
+               "kv read");
+        for (int s = 0; s < npos; ++s)
+          for (int d = 0; d < D; ++d) out[((size_t)s * nkv + h) * D + d] = tmp[(size_t)d * npos + s];
+      }
+    }
+    return SPEC_OK;
+  });
+}
+
+spec_status spec_timing(spec_ctx* ctx, int32_t enable) {
+  return guarded(ctx, [&](Ctx& c) -> spec_status {
+    HIPCHK(c, hipStreamSynchronize(c.stream), "sync");
+    c.timing = enable != 0;
+    c.trec.clear();
+    c.ev_used = 0;
+    for (int k = 0; k < SPEC_KERNEL_KINDS; ++k) {
+      c.t_launches[k] = 0;
+      c.t_ms[k] = 0.0;
+      c.t_bytes[k] = 0.0;
+    }
+    return SPEC_OK;
+  });
+}
+
+spec_status spec_timing_read(spec_ctx* ctx, int32_t kind, int64_t* launches, double* ms, double* bytes) {
+  return guarded(ctx, [&](Ctx& c) -> spec_status {
+    if (kind < 0 || kind >= SPEC_KERNEL_KINDS) return set_err(c, SPEC_E_INVAL, "bad kernel kind");
+    HIPCHK(c, hipStreamSynchronize(c.stream), "sync");
+    for (const TimingRec& r : c.trec) {
+      float t = 0.f;
+      HIPCHK(c, hipEventElapsedTime(&t, r.e0, r.e1), "event time");
+      c.t_launches[r.kind] += 1;
+      c.t_ms[r.kind] += t;
+      c.t_bytes[r.kind] += r.bytes;
+    }
+    c.trec.clear();
+    c.ev_used = 0;
+    if (launches) *launches = c.t_launches[kind];
+    if (ms) *ms = c.t_ms[kind];
+    if (bytes) *bytes = c.t_bytes[kind];
+    return SPEC_OK;
+  });
+}
+
+}  // extern "C"

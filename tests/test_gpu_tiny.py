@@ -1,0 +1,317 @@
+"""GPU parity on the tiny workload: 2-layer target (hidden 256, 4 q / 2 kv heads,
+head_dim 64, M-RoPE sections 8/12/12, SwiGLU 688, vocab 1024), 1-layer FlatRoPE
+draft, prompt of 320 tokens (1x16x16 vision grid + 64 text), K = 4.
+
+Bit-exact: position ids, accept lengths, committed tokens, lengths, the GPU's
+speculative output against its own greedy decoding.  Within 2e-2 normwise:
+logits and cached K/V against the float64 oracle.  Argmax decisions are
+compared on rows whose oracle top-1 margin exceeds 2e-2; on the other rows
+the GPU token must be within that margin of the oracle's top-1."""
+import dataclasses
+
+import numpy as np
+import pytest
+
+import workloads as W
+from oracle import model as OM
+from oracle import numerics as ON
+from oracle import positions as OP
+from oracle import spec as OS
+from tests import _support as S
+
+pytestmark = pytest.mark.gpu
+
+
+def _session(w, **kw):
+    from paper_2606_31160_amd.harness import Session
+    return Session(w, **kw)
+
+
+@pytest.fixture(scope="module")
+def c1():
+    w = W.get("C1")
+    hp = W.HostWeights(w)
+    T, D = S.oracle_decoders(w, hp)
+    seq = S.oracle_sequence(w, 0, T, D)
+    trace = OS.greedy_trace(seq)
+    return w, hp, T, D, trace
+
+
+def _blocks(w, b=0):
+    return [(x.start, x.t, x.h, x.w) for x in w.seqs[b].blocks]
+
+
+def run_loop(s, mode, synth=None, trace=None, max_rounds=100):
+    """Drive propose/verify/commit on sequence 0 until it finishes.
+    mode 'draft': the draft model's own K proposals; 'synth': DraftSynth over
+    `trace`; 'ar': K = 0.  Returns (tokens, accept lengths, proposals per round)."""
+    out, accs, props = [], [], []
+    for _ in range(max_rounds):
+        if mode == "draft":
+            for _ in range(s.K):
+                s.draft_step()
+            props.append(s.dtok[0].cpu().numpy().copy())
+            s.verify(None)
+        elif mode == "synth":
+            i = len(out)
+            s.verify(synth.propose(np.array(trace[i:]), s.K)[None, :])
+        else:
+            s.verify(None)
+        s.commit()
+        coms, acc, fin = s.committed()
+        out += [int(t) for t in coms[0]]
+        accs.append(int(acc[0]))
+        if fin[0]:
+            break
+    assert s.sync() == s.B
+    return out, accs, props
+
+
+# ---------------------------------------------------------------------------
+
+LAYOUTS = {
+    "c1": None,
+    "frames": W.SeqLayout(200, (W.VisionBlock(0, 2, 6, 8), W.VisionBlock(100, 1, 4, 5))),
+    "interleaved": W.SeqLayout(150, (W.VisionBlock(10, 3, 5, 4),)),
+}
+
+
+@pytest.mark.parametrize("name", list(LAYOUTS))
+def test_positions_bit_exact(c1, name):
+    w = c1[0]
+    if LAYOUTS[name] is not None:
+        w = w.with_(seqs=(LAYOUTS[name],))
+    if name == "interleaved":
+        w = w.with_(target=dataclasses.replace(w.target, interleaved=True))
+    s = _session(w)
+    L = w.seqs[0].prefix_len + w.max_new_tokens + w.K + 1
+    assert np.array_equal(s.positions(0, L), OP.target_positions(L, _blocks(w)))
+    s.close()
+
+
+def test_prefix_caches(c1):
+    w, hp, T, D, trace = c1
+    s = _session(w)
+    seq = S.oracle_sequence(w, 0, T, D)
+    P = w.seqs[0].prefix_len
+    for model, dec, cache in ((0, T, seq.tc), (1, D, seq.dc)):
+        for li in range(dec.s.layers):
+            k = ON.decode(s.kv(0, model, li, 0, 0, P))
+            assert S.normwise_err(k, cache.k[li][:P]) <= 1e-2, (model, li)
+            v = s.kv(0, model, li, 1, 0, P)
+            assert np.array_equal(v, W.prefix_kv_host(w, 0, "target" if model == 0 else "draft", li, "v"))
+    s.close()
+
+
+def test_one_verify_logits_accept_commit(c1):
+    w, hp, T, D, trace = c1
+    s = _session(w)
+    seq = S.oracle_sequence(w, 0, T, D)
+    drafts = W.DraftSynth(w, 0).propose(np.array(trace), w.K)
+    s.verify(drafts[None, :], logits=True)
+    s.commit()
+    ref = seq.verify(drafts)
+    gl = s.logits[0].float().cpu().numpy()
+    for j in range(w.K + 1):
+        assert S.normwise_err(gl[j], ref.logits[j]) <= S.LOGIT_RTOL, j
+    coms, acc, fin = s.committed()
+    l = int(acc[0])
+    pinned = S.margin(ref.logits) > S.MARGIN
+    if pinned[:ref.accept_len + 1].all():
+        assert l == ref.accept_len
+        assert coms[0] == ref.committed
+    assert coms[0][:l] == list(drafts[:l])
+    S.check_argmax_rows(coms[0][l:l + 1], ref.logits[l:l + 1])
+    st = s.state(0)
+    assert st["seq_len"] == w.seqs[0].prefix_len + l + 1
+    assert st["pending"] == coms[0][-1]
+    # the new keys/values the verify appended, rows 0..K
+    P = w.seqs[0].prefix_len
+    for li in range(w.target.layers):
+        k = ON.decode(s.kv(0, 0, li, 0, P, w.K + 1))
+        v = ON.decode(s.kv(0, 0, li, 1, P, w.K + 1))
+        assert S.normwise_err(k, seq.tc.k[li][P:P + w.K + 1]) <= S.LOGIT_RTOL
+        assert S.normwise_err(v, seq.tc.v[li][P:P + w.K + 1]) <= S.LOGIT_RTOL
+    s.close()
+
+
+def test_spec_loop_equals_greedy_and_oracle(c1):
+    w, hp, T, D, trace = c1
+    spec_out, accs, props = run_loop(_session(w), "draft")
+    ar_out, _, _ = run_loop(_session(w, K=0, with_draft=False), "ar")
+    assert spec_out == ar_out                       # Eq. commit keeps greedy output exactly
+    assert len(spec_out) == w.max_new_tokens
+    # oracle check of every committed token, teacher-forced along the GPU sequence
+    seq = S.oracle_sequence(w, 0, T, None, with_draft=False)
+    P = w.seqs[0].prefix_len
+    toks = [seq.pending] + spec_out[:-1]
+    z = T.forward(toks, list(range(P, P + len(toks))), seq.tc)
+    pinned = S.check_argmax_rows(spec_out, z)
+    if pinned.all():
+        assert spec_out == trace
+
+
+def test_draft_proposals_match_oracle(c1):
+    w, hp, T, D, trace = c1
+    s = _session(w)
+    gpu_out, _, gpu_props = run_loop(s, "draft")
+    seq = S.oracle_sequence(w, 0, T, D)
+    rec = []
+
+    def proposer(sq):
+        out = []
+        for _ in range(w.K):
+            d, z = sq.draft_step()
+            out.append(d)
+            rec.append(z)
+        return out
+
+    ref_out = OS.spec_loop(seq, proposer)
+    if ref_out != gpu_out:
+        pytest.skip("GPU and oracle histories diverged at an unpinned row")
+    S.check_argmax_rows(np.concatenate(gpu_props), np.stack(rec))
+
+
+def test_caches_and_lengths_after_rounds(c1):
+    w, hp, T, D, trace = c1
+    s = _session(w)
+    seq = S.oracle_sequence(w, 0, T, D)
+    rng = np.random.default_rng(11)
+    for _ in range(3):
+        for _ in range(w.K):
+            s.draft_step()
+        seq.propose()
+        i = len(seq.generated)
+        d = np.array([t if rng.random() < 0.6 else int(rng.integers(0, w.vocab)) for t in trace[i:i + w.K]],
+                     dtype=np.int32)
+        s.verify(d[None, :])
+        s.commit()
+        seq.verify(d)
+    st = s.state(0)
+    assert (st["seq_len"], st["draft_len"], st["pending"], st["n_gen"]) == \
+        (seq.seq_len, seq.draft_len, seq.pending, len(seq.generated))
+    n = seq.seq_len
+    for li in range(w.target.layers):
+        for which, ref in ((0, seq.tc.k[li]), (1, seq.tc.v[li])):
+            got = ON.decode(s.kv(0, 0, li, which, 0, n))
+            assert S.normwise_err(got, ref[:n]) <= S.LOGIT_RTOL
+    for li in range(w.draft.layers):
+        got = ON.decode(s.kv(0, 1, li, 0, 0, seq.draft_len))
+        assert S.normwise_err(got, seq.dc.k[li][:seq.draft_len]) <= S.LOGIT_RTOL
+    s.close()
+
+
+def test_stop_token_and_budget(c1):
+    w, hp, T, D, trace = c1
+    ar, _, _ = run_loop(_session(w, K=0, with_draft=False), "ar")
+    stop = ar[6]
+    cut = ar.index(stop)
+    out, _, _ = run_loop(_session(w, stop_token=stop), "draft")
+    assert out == ar[:cut + 1]
+    out, _, _ = run_loop(_session(w, max_new_tokens=7), "synth", synth=W.DraftSynth(w, 0), trace=ar)
+    assert out == ar[:7]
+
+
+def test_out_of_range_draft_token_is_flagged(c1):
+    from paper_2606_31160_amd import binding as B
+    w = c1[0]
+    s = _session(w)
+    s.verify(np.array([[1, 2, w.vocab + 5, 3]], dtype=np.int32))
+    s.commit()
+    with pytest.raises(B.SpecError) as e:
+        s.sync()
+    assert e.value.status == 1
+    s.close()
+
+
+def test_call_order_enforced(c1):
+    from paper_2606_31160_amd import binding as B
+    w = c1[0]
+    s = _session(w)
+    with pytest.raises(B.SpecError):
+        s.commit()                      # nothing verified
+    with pytest.raises(B.SpecError):
+        s.verify(None)                  # no proposals yet
+    for _ in range(w.K):
+        s.draft_step()
+    with pytest.raises(B.SpecError):
+        s.draft_step()                  # K steps already taken
+    s.verify(None)
+    with pytest.raises(B.SpecError):
+        s.verify(None)                  # commit first
+    s.commit()
+    s.close()
+
+
+def test_graphs_and_direct_launches_agree(c1):
+    from paper_2606_31160_amd import binding as B
+    w, hp, T, D, trace = c1
+    outs = []
+    for flags in (0, B.SPEC_FLAG_NO_GRAPHS):
+        s = _session(w, flags=flags)
+        for _ in range(w.K):
+            s.draft_step()
+        s.verify(None, logits=True)
+        s.commit()
+        lg = s.logits.clone()
+        o, _, _ = run_loop(s, "draft")
+        outs.append((o, lg))
+    assert outs[0][0] == outs[1][0]
+    assert bool((outs[0][1] == outs[1][1]).all())
+
+
+def run_batch(s, mode, max_rounds=100):
+    outs = [[] for _ in range(s.B)]
+    done = [False] * s.B
+    for _ in range(max_rounds):
+        if mode == "draft":
+            for _ in range(s.K):
+                s.draft_step()
+        s.verify(None)
+        s.commit()
+        coms, acc, fin = s.committed()
+        for b in range(s.B):
+            if not done[b]:
+                outs[b] += [int(t) for t in coms[b]]
+                done[b] = bool(fin[b])
+            else:
+                assert coms[b] == []
+        if all(done):
+            break
+    assert s.sync() == s.B
+    return outs
+
+
+def test_batch_of_two(c1):
+    w, hp, T, D, trace = c1
+    lay2 = W.SeqLayout(260, (W.VisionBlock(20, 2, 8, 8),))
+    wb = w.with_(seqs=(w.seqs[0], lay2), p_accept=(0.8, 0.8))
+    spec = run_batch(_session(wb), "draft")
+    ar = run_batch(_session(wb, K=0, with_draft=False), "ar")
+    assert spec == ar
+    single, _, _ = run_loop(_session(w), "draft")
+    assert spec[0] == single
+    Tb, _ = S.oracle_decoders(wb, W.HostWeights(wb))
+    seq = S.oracle_sequence(wb, 1, Tb, None, with_draft=False)
+    P = lay2.prefix_len
+    toks = [seq.pending] + spec[1][:-1]
+    z = Tb.forward(toks, list(range(P, P + len(toks))), seq.tc)
+    S.check_argmax_rows(spec[1], z)
+
+
+def test_block_of_16_with_two_row_blocks(c1):
+    # K = 16 (M = 17 rows, two 16-row MFMA blocks in every GEMV) and 4 q heads
+    # per kv head (68 query rows per kv head: two attention row blocks).
+    w = c1[0]
+    w16 = w.with_(K=16, target=dataclasses.replace(w.target, q_heads=8, kv_heads=2),
+                  draft=dataclasses.replace(w.draft, q_heads=8, kv_heads=2))
+    ar, _, _ = run_loop(_session(w16, K=0, with_draft=False), "ar")
+    out, accs, _ = run_loop(_session(w16), "synth", synth=W.DraftSynth(w16, 0), trace=ar)
+    assert out == ar
+    hp = W.HostWeights(w16)
+    T, _ = S.oracle_decoders(w16, hp)
+    seq = S.oracle_sequence(w16, 0, T, None, with_draft=False)
+    P = w16.seqs[0].prefix_len
+    toks = [seq.pending] + out[:-1]
+    z = T.forward(toks, list(range(P, P + len(toks))), seq.tc)
+    S.check_argmax_rows(out, z)
