@@ -17,6 +17,8 @@ typedef uint16_t bf16_t;
 constexpr int kMaxRows = SPEC_MAX_K + 1;     // rows per sequence in one pass
 constexpr int kTile = 16;                    // output rows per GEMV tile (one MFMA block)
 constexpr int kKeyBlock = 32;                // keys per attention inner step
+constexpr int kGemvWaves = 16;               // waves per GEMV workgroup
+constexpr int kGemvSteps = 8;                // max 32-wide k-steps per GEMV wave
 
 // Per-sequence state, resident in device memory.  Only kernels change it
 // between spec_init and spec_destroy, so a captured graph stays valid for
@@ -59,7 +61,7 @@ struct Model {
   bf16_t* kc = nullptr;             // [layers][B][kv_heads][cap][head_dim], rotated keys
   bf16_t* vt = nullptr;             // [layers][B][kv_heads][head_dim][cap], values transposed
   int8_t* axis = nullptr;           // [head_dim/2] axis (0 T, 1 H, 2 W) of each rotary pair
-  int s_qkv = 1, s_o = 1, s_gu = 1, s_down = 1;   // GEMV k-splits
+  int s_down = 1;                  // k-splits of the down projection
   size_t kv_layer = 0;              // elements of one layer's key (or value) cache
 };
 
@@ -83,10 +85,12 @@ struct Ctx {
   int32_t* pos3 = nullptr;          // [B][3][cap] target rotary positions
   float2* cs = nullptr;             // [cap][head_dim/2] (cos, sin) of theta_d * p
   float* x = nullptr;               // [Mpad][hidden] residual stream
-  bf16_t* a = nullptr;              // [Mpad][hidden] normalised GEMV input
   bf16_t* q = nullptr;              // [Mpad][q_heads*head_dim] rotated queries
   bf16_t* o = nullptr;              // [Mpad][q_heads*head_dim] attention output
   bf16_t* u = nullptr;              // [Mpad][ffn] SwiGLU output (max of both models)
+  bf16_t* xg = nullptr;             // [Mpad][hidden] bf16(x * gain of the next RMSNorm)
+  float* ss = nullptr;              // [hidden/16][Mpad] per-16-column sums of x^2
+  float2* rcs = nullptr;            // [Mpad][head_dim/2] (cos, sin) of each row's rotary pairs
   float* part = nullptr;            // GEMV k-split partial sums
   size_t part_elems = 0;
   float* op = nullptr;              // [splits][B][q_heads][R][head_dim] attention partials
@@ -95,7 +99,6 @@ struct Ctx {
   float* amax_v = nullptr;          // [vocab/16][Mpad] per-tile maximum logit
   int32_t* amax_i = nullptr;        // [vocab/16][Mpad] its index
   bf16_t* logits = nullptr;         // [Mpad][vocab] bf16 logits of the last verify
-  bf16_t* a_last = nullptr;         // [16][hidden] draft: normalised last row per sequence
 
   const bf16_t* embed = nullptr;
   Model tgt, drf;
@@ -132,7 +135,12 @@ hipError_t launch_draft_out(Ctx& c, int32_t* d_tokens);
 hipError_t launch_commit(Ctx& c, int32_t* acc, int32_t* committed, int32_t* ncommit, int32_t* fin);
 hipError_t launch_logits_out(Ctx& c, void* d_logits);
 
-// GEMV k-split choice for an [N][Kd] weight (also used to size the partials).
-int pick_splits(int N, int Kd);
+// Dynamic LDS bytes one GEMV workgroup needs (TT tiles, M rows, span k-steps)
+// and the device limit; k-splits of a GEMV whose workgroups cannot hold all
+// of x.
+size_t gemv_lds_bytes(int TT, int M, int span_steps);
+int gemv_lds_limit();
+int down_splits(int M, int Kd);
+void init_kernel_attributes();
 
 }  // namespace specdec

@@ -45,13 +45,15 @@ __device__ __forceinline__ f32x4 mfma16x16x32(u32x4 a, u32x4 b, f32x4 c) {
                                                  0, 0, 0);
 }
 
-// Block-wide sum of one float per thread (blockDim.x == 256).
-__device__ float block_sum256(float v, float* sh) {
+// Block-wide sum of one float per thread (blockDim.x a multiple of 64, <= 1024),
+// in a fixed order.
+__device__ float block_sum(float v, float* sh) {
   for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
-  const int w = threadIdx.x >> 6, l = threadIdx.x & 63;
+  const int w = threadIdx.x >> 6, l = threadIdx.x & 63, nw = blockDim.x >> 6;
   if (l == 0) sh[w] = v;
   __syncthreads();
-  float t = sh[0] + sh[1] + sh[2] + sh[3];
+  float t = 0.f;
+  for (int i = 0; i < nw; ++i) t += sh[i];
   __syncthreads();
   return t;
 }
@@ -132,10 +134,15 @@ __global__ void k_stage_verify(SeqState* st, const int32_t* over, int K, int V, 
 }
 
 // ---------------------------------------------------------------------------
-// Row plan + embedding gather + first RMSNorm.  grid (R, B), 256 threads.
+// Row plan + embedding gather.  grid (R, B), 1024 threads.
 // Verify: rows at slots seq_len .. seq_len+K, tokens vtok.
 // Draft: rows at slots draft_len .. seq_len+dstep (catch-up), tokens from the
 // committed history up to seq_len and the draft's own proposals after it.
+// Writes the residual stream x, xg = bf16(x * g) with the first layer's
+// attention-norm gain, per-16-column sums of x^2 (the next GEMV applies 1/rms;
+// see k_gemv), and each row's (cos, sin) of every rotary pair at its slot:
+// target angle theta_d * p_{a(d)}(slot) (Eq. mrope-phase), draft theta_d * slot
+// (Eq. flatrope-proj), gathered from the host-built table.
 // ---------------------------------------------------------------------------
 struct EmbedArgs {
   SeqState* st;
@@ -143,13 +150,17 @@ struct EmbedArgs {
   const bf16_t* E;       // [V][H]
   const bf16_t* g;       // first layer's attention-norm gain
   float* x;              // [Mpad][H]
-  bf16_t* a;             // [Mpad][H]
-  int H, R, cap, mode;
-  float eps;
+  bf16_t* xg;            // [Mpad][H]
+  float* ss;             // [H/16][Mpad]
+  float2* rcs;           // [Mpad][D/2] (cos, sin) of each row's rotary pairs
+  const int32_t* pos3;   // [B][3][cap]
+  const float2* cs;      // [cap][D/2]
+  const int8_t* axis;    // [D/2]
+  int H, R, cap, mode, mpad, D, flat;
 };
 
-__global__ __launch_bounds__(256) void k_embed(EmbedArgs p) {
-  __shared__ float sh[4];
+__global__ __launch_bounds__(1024) void k_embed(EmbedArgs p) {
+  extern __shared__ float sq[];   // [H]
   const int j = blockIdx.x, b = blockIdx.y;
   const SeqState& s = p.st[b];
   int base, count, tok = 0;
@@ -174,213 +185,332 @@ __global__ __launch_bounds__(256) void k_embed(EmbedArgs p) {
     p.st[b].count = count;
   }
   const size_t r = (size_t)b * p.R + j;
-  float* xr = p.x + r * p.H;
-  bf16_t* ar = p.a + r * p.H;
-  if (j >= count) {
-    for (int n = threadIdx.x; n < p.H; n += 256) {
-      xr[n] = 0.f;
-      ar[n] = 0;
-    }
-    return;
-  }
+  const bool live = j < count;
   const bf16_t* er = p.E + (size_t)tok * p.H;
-  float ss = 0.f;
-  for (int n = threadIdx.x; n < p.H; n += 256) {
-    const float v = bf2f(er[n]);
-    xr[n] = v;
-    ss += v * v;
+  for (int n = threadIdx.x; n < p.H; n += blockDim.x) {
+    const float v = live ? bf2f(er[n]) : 0.f;
+    p.x[r * p.H + n] = v;
+    p.xg[r * p.H + n] = f2bf(v * bf2f(p.g[n]));
+    sq[n] = v * v;
   }
-  const float inv = rsqrtf(block_sum256(ss, sh) / p.H + p.eps);
-  for (int n = threadIdx.x; n < p.H; n += 256) ar[n] = f2bf(xr[n] * inv * bf2f(p.g[n]));
+  if (live && threadIdx.x < p.D / 2) {
+    const int slot = base + j, d = threadIdx.x;
+    const int pos = p.flat ? slot : p.pos3[((size_t)b * 3 + p.axis[d]) * p.cap + slot];
+    p.rcs[r * (p.D / 2) + d] = p.cs[(size_t)pos * (p.D / 2) + d];
+  }
+  __syncthreads();
+  for (int t = threadIdx.x; t < p.H / kTile; t += blockDim.x) {
+    float v = 0.f;
+    for (int c = 0; c < kTile; ++c) v += sq[t * kTile + c];
+    p.ss[(size_t)t * p.mpad + r] = v;
+  }
 }
 
 // ---------------------------------------------------------------------------
-// Thin-M weight-streaming GEMV on MFMA:  y[m][n] = sum_k x[m][k] * W[n][k].
+// Thin-M weight-streaming GEMV on MFMA:  y[m][n] = sum_k x[m][k] * W[n][k],
+// with the consumer's step fused into the epilogue.
 //
-// A workgroup (4 waves) owns 16 consecutive weight rows and a k-range; each
-// wave takes every 4th 32-wide k-step of that range.  With
-// v_mfma_f32_16x16x32_bf16 the A operand is the weight tile: lane l holds
-// W[n0 + (l&15)][k0 + 8*(l>>4) .. +8] (one 16-byte load), the B operand is
-// x^T: lane l holds x[m = l&15][same 8 k] (rows beyond M are zero padding in
-// the activation buffer), and the result lane l holds y[m = l&15][n0 +
-// 4*(l>>4) + i], i = 0..3.  The four waves' results are summed through LDS in
-// a fixed order (deterministic).  M up to 16*MB rows reuse each weight
-// fragment MB times.
+// A workgroup of NW waves owns TT tiles of 16 weight rows and a k-range of
+// 32-wide steps; wave w streams a contiguous chunk of at most SMAX steps of
+// every tile.  Row-major weights: for one step, lane l reads
+// W[row (l&15)][8*(l>>4) .. +8] (16 bytes).  All of a wave's weight loads are
+// issued first; the workgroup then stages its live x rows for the k-range in
+// LDS with coalesced loads, so each x fragment is fetched from L2 once per
+// workgroup and feeds TT MFMAs.  v_mfma_f32_16x16x32_bf16 takes the weight
+// fragment as A and x^T as B (lane l: x[m = l&15][same 8 k]); lane l ends with
+// y[m = l&15][n0 + 4*(l>>4) + i].  The NW per-wave partial tiles are summed
+// through LDS in a fixed order (deterministic), then the epilogue runs on
+// complete outputs.  Which rows are live (row m is row m % rps of sequence
+// m / rps, live while below that sequence's row count) is read through the
+// scalar cache, which does not wait behind the weight stream.
+//
+// RMSNorm: producers store xg = bf16(x * g) and per-16-column sums of x^2;
+// consumers of a normalised input scale y by 1/rms(x), a per-row scalar
+// (RMSNorm(x) g W^T = (x g) W^T / rms(x)).
 // ---------------------------------------------------------------------------
-enum { EPI_PARTIAL = 0, EPI_ARGMAX = 1 };
+enum {
+  EPI_STORE = 0,   // out[split][m][n]: k-split partial sums (down projection)
+  EPI_ROPE = 1,    // y/rms; rotation of q/k at the row's position, q store, K / V^T cache append (QKV)
+  EPI_RESID = 2,   // x += y; xg = bf16(x * g); sums of x^2 (O projection)
+  EPI_SWIGLU = 3,  // y/rms; tiles (gate t, up t): u = silu(gate) * up (gate/up)
+  EPI_ARGMAX = 4   // y/rms; per-tile (max, index) of the logits, optional bf16 logits (LM head)
+};
 
 struct GemvArgs {
   const bf16_t* w[3];
-  int row0[3];           // first output row of each segment
+  int row0[3];           // first output row of each weight segment (multiples of 16)
   int nseg;
   int N, Kd;
-  const bf16_t* x;       // [Mpad][ldx]
+  const bf16_t* x;       // [M][ldx]
   int ldx, M, splits;
-  float* part;           // EPI_PARTIAL: [splits][M][N]
-  float* amax_v;         // EPI_ARGMAX: [N/16][Mpad]
+  const SeqState* st;
+  int rps;               // rows per sequence
+  int mpad;              // row stride of ss / amax
+  const float* ss_in;    // [H/16][mpad] sums of x^2 of the input rows (ROPE, SWIGLU, ARGMAX)
+  int H;                 // row length those sums cover
+  float eps;
+  float* out;            // EPI_STORE: [splits][M][N]
+  // EPI_ROPE
+  bf16_t* q;             // [M][nq*D]
+  bf16_t *kc, *vt;       // layer bases [B][nkv][cap][D], [B][nkv][D][cap]
+  const float2* rcs;     // [Mpad][D/2] (cos, sin) per row
+  int nq, nkv, D, cap;
+  // EPI_RESID
+  float* x32;            // [M][N] residual stream
+  const bf16_t* gain;    // [N] gain of the next RMSNorm
+  bf16_t* xg;            // [M][N] bf16(x * gain)
+  float* ss_out;         // [N/16][mpad] sums of x^2
+  // EPI_SWIGLU
+  bf16_t* u;             // [M][N/2]
+  // EPI_ARGMAX
+  float* amax_v;         // [N/16][mpad]
   int32_t* amax_i;
-  bf16_t* logits;        // EPI_ARGMAX: [Mpad][N] when the row's sequence wants logits
-  SeqState* st;          // EPI_ARGMAX: flags
-  int rps;               // rows per sequence (row m belongs to sequence m / rps)
-  int mpad;
+  bf16_t* logits;        // [M][N]
   int allow_logits;
 };
 
-template <int MB, int EPI, int U>
-__global__ __launch_bounds__(256) void k_gemv(GemvArgs a) {
-  __shared__ f32x4 red[4][MB][64];
-  const int tile = blockIdx.x, split = blockIdx.y;
+template <int MB, int NW, int SMAX, int TT, int EPI>
+__global__ __launch_bounds__(NW * 64) void k_gemv(GemvArgs a) {
+  extern __shared__ __align__(16) unsigned char lds[];
+  __shared__ float inv_rms[MB * 16];
+  const int tg = blockIdx.x, split = blockIdx.y;
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
-  const int n0 = tile * kTile;
-  int sg = 0;
-#pragma unroll
-  for (int i = 1; i < 3; ++i)
-    if (i < a.nseg && n0 >= a.row0[i]) sg = i;
   const int Kd = a.Kd;
   const int kq = 8 * (lane >> 4);
-  const bf16_t* wp = a.w[sg] + (size_t)(n0 - a.row0[sg] + (lane & 15)) * Kd + kq;
-  const bf16_t* xp[MB];
-#pragma unroll
-  for (int mb = 0; mb < MB; ++mb) xp[mb] = a.x + (size_t)(mb * 16 + (lane & 15)) * a.ldx + kq;
-
-  const int T = (Kd + 31) >> 5;       // 32-wide k-steps
-  const int Tfull = Kd >> 5;          // steps with no tail
+  const int T = (Kd + 31) >> 5;
   const int s0 = (int)((long long)split * T / a.splits);
   const int s1 = (int)((long long)(split + 1) * T / a.splits);
-  const int s1f = s1 < Tfull ? s1 : Tfull;
+  const int chunk = (s1 - s0 + NW - 1) / NW;
+  const int w0 = s0 + wave * chunk;
+  const int w1 = min(w0 + chunk, s1);
+  constexpr bool kNorm = EPI == EPI_ROPE || EPI == EPI_SWIGLU || EPI == EPI_ARGMAX;
 
-  f32x4 acc[MB];
+  int tile[TT];
 #pragma unroll
-  for (int mb = 0; mb < MB; ++mb) acc[mb] = f32x4{0.f, 0.f, 0.f, 0.f};
+  for (int tt = 0; tt < TT; ++tt) tile[tt] = (EPI == EPI_SWIGLU) ? tg + tt * (a.N / 32) : tg * TT + tt;
 
-  int st = s0 + wave;
-  for (; st + 4 * (U - 1) < s1f; st += 4 * U) {
-    u32x4 wv[U], xv[U][MB];
+  // 1. weight fragments -> registers
+  u32x4 wv[TT][SMAX];
 #pragma unroll
-    for (int u = 0; u < U; ++u) {
-      const int k = (st + 4 * u) << 5;
-      wv[u] = ld16(wp + k);
+  for (int tt = 0; tt < TT; ++tt) {
+    const int n0 = tile[tt] * kTile;
+    int sg = 0;
 #pragma unroll
-      for (int mb = 0; mb < MB; ++mb) xv[u][mb] = ld16(xp[mb] + k);
-    }
+    for (int i = 1; i < 3; ++i)
+      if (i < a.nseg && n0 >= a.row0[i]) sg = i;
+    const bf16_t* wp = a.w[sg] + (size_t)(n0 - a.row0[sg] + (lane & 15)) * Kd + kq;
 #pragma unroll
-    for (int u = 0; u < U; ++u)
-#pragma unroll
-      for (int mb = 0; mb < MB; ++mb) acc[mb] = mfma16x16x32(wv[u], xv[u][mb], acc[mb]);
-  }
-  for (; st < s1; st += 4) {
-    const int k = st << 5;
-    const bool ok = k + kq < Kd;      // Kd % 8 == 0: a lane's 8 elements are all in or all out
-    u32x4 wv = ok ? ld16(wp + k) : u32x4{0, 0, 0, 0};
-#pragma unroll
-    for (int mb = 0; mb < MB; ++mb) {
-      u32x4 xv = ok ? ld16(xp[mb] + k) : u32x4{0, 0, 0, 0};
-      acc[mb] = mfma16x16x32(wv, xv, acc[mb]);
+    for (int i = 0; i < SMAX; ++i) {
+      const int k = (w0 + i) << 5;
+      wv[tt][i] = (w0 + i < w1 && k + kq < Kd) ? ld16(wp + k) : u32x4{0, 0, 0, 0};
     }
   }
-#pragma unroll
-  for (int mb = 0; mb < MB; ++mb) red[wave][mb][lane] = acc[mb];
+
+  // 2. live rows (scalar cache)
+  uint64_t live = 0;
+  {
+    const int nseq = (a.M + a.rps - 1) / a.rps;
+    for (int b = 0; b < nseq; ++b) {
+      const int n = min(a.st[b].count, a.rps);
+      if (n > 0) live |= ((1ull << n) - 1ull) << (b * a.rps);
+    }
+  }
+
+  // 3. live x rows, steps [s0, s1) -> LDS (row stride: span bf16)
+  const int per_row = (s1 - s0) * 4;              // 16-byte chunks per row
+  u32x4* xs = reinterpret_cast<u32x4*>(lds);
+  for (int c = threadIdx.x; per_row > 0 && c < a.M * per_row; c += NW * 64) {
+    const int m = c / per_row, q = c - m * per_row;
+    if (!((live >> m) & 1)) continue;
+    const int k = s0 * 32 + q * 8;
+    xs[c] = k < Kd ? ld16(a.x + (size_t)m * a.ldx + k) : u32x4{0, 0, 0, 0};
+  }
+  if constexpr (kNorm) {
+    // 1 / rms of each row from the per-16-column sums of squares (fixed order)
+    for (int m = wave; m < MB * 16; m += NW) {
+      float v = 0.f;
+      if ((live >> m) & 1)
+        for (int t = lane; t < a.H / kTile; t += 64) v += a.ss_in[(size_t)t * a.mpad + m];
+      for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
+      if (lane == 0) inv_rms[m] = rsqrtf(v / a.H + a.eps);
+    }
+  }
   __syncthreads();
 
-  const int t = threadIdx.x;
-  const int L = t >> 2, i = t & 3;
-  if constexpr (EPI == EPI_PARTIAL) {
+  // 4. MFMAs
+  f32x4 acc[TT][MB];
 #pragma unroll
-    for (int mb = 0; mb < MB; ++mb) {
-      const float v = red[0][mb][L][i] + red[1][mb][L][i] + red[2][mb][L][i] + red[3][mb][L][i];
-      const int m = mb * 16 + (L & 15);
-      const int n = n0 + 4 * (L >> 4) + i;
-      if (m < a.M) a.part[((size_t)split * a.M + m) * a.N + n] = v;
+  for (int tt = 0; tt < TT; ++tt)
+#pragma unroll
+    for (int mb = 0; mb < MB; ++mb) acc[tt][mb] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int i = 0; i < SMAX; ++i) {
+    if (w0 + i < w1) {
+#pragma unroll
+      for (int mb = 0; mb < MB; ++mb) {
+        const int m = mb * 16 + (lane & 15);
+        const u32x4 xv = ((live >> m) & 1) ? xs[m * per_row + (w0 + i - s0) * 4 + (lane >> 4)] : u32x4{0, 0, 0, 0};
+#pragma unroll
+        for (int tt = 0; tt < TT; ++tt) acc[tt][mb] = mfma16x16x32(wv[tt][i], xv, acc[tt][mb]);
+      }
     }
-  } else {
-    __shared__ float lg[MB * 16][17];
+  }
+  __syncthreads();   // x no longer needed: reuse LDS
+
+  // 5. sum the NW wave partials: y[tt][m][c] (c = column inside the tile)
+  f32x4* red = reinterpret_cast<f32x4*>(lds);                                        // [NW][TT][MB][64]
+  float* y = reinterpret_cast<float*>(lds + (size_t)NW * TT * MB * 64 * 16);         // [TT][MB*16][17]
 #pragma unroll
-    for (int mb = 0; mb < MB; ++mb) {
-      const float v = red[0][mb][L][i] + red[1][mb][L][i] + red[2][mb][L][i] + red[3][mb][L][i];
-      const int m = mb * 16 + (L & 15);
-      const int nn = 4 * (L >> 4) + i;
-      lg[m][nn] = v;
-      if (a.allow_logits && m < a.M && a.st[m / a.rps].want_logits) a.logits[(size_t)m * a.N + n0 + nn] = f2bf(v);
+  for (int tt = 0; tt < TT; ++tt)
+#pragma unroll
+    for (int mb = 0; mb < MB; ++mb) red[((wave * TT + tt) * MB + mb) * 64 + lane] = acc[tt][mb];
+  __syncthreads();
+  for (int t = threadIdx.x; t < TT * MB * 256; t += NW * 64) {
+    const int tt = t / (MB * 256), r = t % (MB * 256);
+    const int mb = r >> 8, L = (r & 255) >> 2, i = r & 3;
+    float v = 0.f;
+#pragma unroll
+    for (int w = 0; w < NW; ++w) v += red[((w * TT + tt) * MB + mb) * 64 + L][i];
+    const int m = mb * 16 + (L & 15);
+    y[(tt * MB * 16 + m) * 17 + 4 * (L >> 4) + i] = kNorm ? v * inv_rms[m] : v;
+  }
+  __syncthreads();
+
+  // 6. epilogue on complete 16-column tiles
+  const int nrow = MB * 16;
+  if constexpr (EPI == EPI_STORE) {
+    for (int t = threadIdx.x; t < TT * nrow * 16; t += NW * 64) {
+      const int tt = t / (nrow * 16), m = (t / 16) % nrow, c = t & 15;
+      if (m < a.M) a.out[((size_t)split * a.M + m) * a.N + tile[tt] * 16 + c] = y[(tt * nrow + m) * 17 + c];
+    }
+  } else if constexpr (EPI == EPI_ROPE) {
+    // one thread per (row, rotary pair); TT == 1
+    const int t = threadIdx.x, m = t >> 3, pr = t & 7;
+    if (t < nrow * 8 && m < a.M && ((live >> m) & 1)) {
+      const int b = m / a.rps, j = m - b * a.rps;
+      const int slot = a.st[b].base + j;
+      const int n0 = tile[0] * kTile;
+      const int head = n0 / a.D, d = ((n0 % a.D) >> 1) + pr;
+      const float e = y[m * 17 + 2 * pr], o = y[m * 17 + 2 * pr + 1];
+      if (head < a.nq + a.nkv) {
+        const float2 cs = a.rcs[(size_t)m * (a.D / 2) + d];
+        const float re = e * cs.x - o * cs.y, ro = e * cs.y + o * cs.x;
+        if (head < a.nq) {
+          *reinterpret_cast<uint32_t*>(a.q + ((size_t)m * a.nq + head) * a.D + 2 * d) = pack2(re, ro);
+        } else {
+          const int h = head - a.nq;
+          *reinterpret_cast<uint32_t*>(a.kc + (((size_t)b * a.nkv + h) * a.cap + slot) * a.D + 2 * d) =
+              pack2(re, ro);
+        }
+      } else {
+        const int h = head - a.nq - a.nkv;
+        bf16_t* vp = a.vt + (((size_t)b * a.nkv + h) * a.D + 2 * d) * a.cap + slot;
+        vp[0] = f2bf(e);
+        vp[a.cap] = f2bf(o);
+      }
+    }
+  } else if constexpr (EPI == EPI_RESID) {
+    // TT == 1; rows whose sequence is idle keep their stream untouched
+    const int t = threadIdx.x, m = t >> 4, c = t & 15;
+    const int n = tile[0] * kTile + c;
+    float xn = 0.f;
+    if (t < nrow * 16 && m < a.M) {
+      xn = a.x32[(size_t)m * a.N + n];
+      if ((live >> m) & 1) {
+        xn += y[m * 17 + c];
+        a.x32[(size_t)m * a.N + n] = xn;
+      }
+      a.xg[(size_t)m * a.N + n] = f2bf(xn * bf2f(a.gain[n]));
     }
     __syncthreads();
-    if (t < MB * 16 && t < a.M) {
+    if (t < nrow * 16) y[m * 17 + c] = xn * xn;
+    __syncthreads();
+    if (threadIdx.x < nrow) {
+      float v = 0.f;
+      for (int c2 = 0; c2 < 16; ++c2) v += y[threadIdx.x * 17 + c2];
+      a.ss_out[(size_t)tile[0] * a.mpad + threadIdx.x] = v;
+    }
+  } else if constexpr (EPI == EPI_SWIGLU) {
+    const int F = a.N / 2;
+    const int n0 = tile[0] * kTile;
+    const int t = threadIdx.x, m = t >> 4, c = t & 15;
+    if (t < nrow * 16 && m < a.M) {
+      const float g = y[m * 17 + c];
+      const float up = y[(nrow + m) * 17 + c];
+      a.u[(size_t)m * F + n0 + c] = f2bf(g / (1.f + expf(-g)) * up);
+    }
+  } else {   // EPI_ARGMAX, TT tiles of the vocabulary
+    for (int t = threadIdx.x; t < TT * nrow * 16; t += NW * 64) {
+      const int tt = t / (nrow * 16), m = (t / 16) % nrow, c = t & 15;
+      if (a.allow_logits && m < a.M && a.st[m / a.rps].want_logits)
+        a.logits[(size_t)m * a.N + tile[tt] * 16 + c] = f2bf(y[(tt * nrow + m) * 17 + c]);
+    }
+    for (int t = threadIdx.x; t < TT * nrow; t += NW * 64) {
+      const int tt = t / nrow, m = t % nrow;
+      if (m >= a.M) continue;
       float best = -INFINITY;
-      int bi = n0;
+      int bi = tile[tt] * 16;
       bool nan = false;
       for (int c = 0; c < 16; ++c) {
-        float v = lg[t][c];
+        float v = y[(tt * nrow + m) * 17 + c];
         if (v != v) {
           nan = true;
           v = -INFINITY;
         }
         if (v > best) {
           best = v;
-          bi = n0 + c;
+          bi = tile[tt] * 16 + c;
         }
       }
-      a.amax_v[(size_t)tile * a.mpad + t] = best;
-      a.amax_i[(size_t)tile * a.mpad + t] = bi;
-      if (nan) atomicOr(&a.st[t / a.rps].err, ERR_NUMERIC);
+      a.amax_v[(size_t)tile[tt] * a.mpad + m] = best;
+      a.amax_i[(size_t)tile[tt] * a.mpad + m] = bi;
+      if (nan) atomicOr(const_cast<int32_t*>(&a.st[m / a.rps].err), ERR_NUMERIC);
     }
   }
 }
 
+size_t gemv_lds_bytes(int TT, int M, int span_steps) {
+  const int MB = (M + 15) / 16;
+  const size_t x = (size_t)M * span_steps * 64;
+  const size_t red = (size_t)kGemvWaves * TT * MB * 64 * 16 + (size_t)TT * MB * 16 * 17 * 4;
+  return std::max(x, red);
+}
+
 // ---------------------------------------------------------------------------
-// QKV finish: sum k-split partials, rotate q and k at the row's position,
-// store q (bf16), append k to the key cache and v to the transposed value
-// cache.  grid (R, B), 256 threads, one thread per (head, rotary pair).
-// Target: angle theta_d * p_{a(d)}(slot) (Eq. mrope-phase); draft: theta_d *
-// slot (Eq. flatrope-proj).  (cos, sin) come from the host-built table.
+// Down-projection finish: x += sum of the k-split partials (residual), then
+// xg = bf16(x * g_next) and per-16-column sums of x^2 for the next norm.
+// select_last: only each sequence's last live row, stored as row b (the
+// draft proposes from it).  grid (H/256, M), one column of one row per thread.
 // ---------------------------------------------------------------------------
-struct QkvArgs {
+struct FinishArgs {
   const SeqState* st;
-  const float* part;     // [S][M][N], N = (nq + 2 nkv) D
-  int S, M, R;
-  bf16_t* q;             // [Mpad][nq][D]
-  bf16_t* kc;            // layer base [B][nkv][cap][D]
-  bf16_t* vt;            // layer base [B][nkv][D][cap]
-  const int32_t* pos3;   // [B][3][cap]
-  const float2* cs;
-  const int8_t* axis;
-  int nq, nkv, D, cap, flat;
+  const float* part;     // [S][M][H]
+  int S, M, rps, H, mpad, select_last;
+  float* x;              // [M][H]
+  const bf16_t* gain;
+  bf16_t* xg;
+  float* ss;             // [H/16][mpad]
 };
 
-__global__ __launch_bounds__(256) void k_qkv_rope(QkvArgs p) {
-  const int j = blockIdx.x, b = blockIdx.y;
-  const SeqState& s = p.st[b];
-  if (j >= s.count) return;
-  const int slot = s.base + j;
-  const int r = b * p.R + j;
-  const int half = p.D / 2;
-  const int N = (p.nq + 2 * p.nkv) * p.D;
-  for (int pr = threadIdx.x; pr < N / 2; pr += 256) {
-    const int col = 2 * pr;
-    const int head = col / p.D;
-    const int d = (col % p.D) >> 1;
-    float e = 0.f, o = 0.f;
-    for (int sp = 0; sp < p.S; ++sp) {
-      const float* pp = p.part + ((size_t)sp * p.M + r) * N + col;
-      e += pp[0];
-      o += pp[1];
-    }
-    if (head < p.nq + p.nkv) {
-      const int pos = p.flat ? slot : p.pos3[((size_t)b * 3 + p.axis[d]) * p.cap + slot];
-      const float2 c = p.cs[(size_t)pos * half + d];
-      const float re = e * c.x - o * c.y, ro = e * c.y + o * c.x;
-      if (head < p.nq) {
-        *reinterpret_cast<uint32_t*>(p.q + ((size_t)r * p.nq + head) * p.D + 2 * d) = pack2(re, ro);
-      } else {
-        const int h = head - p.nq;
-        *reinterpret_cast<uint32_t*>(p.kc + (((size_t)b * p.nkv + h) * p.cap + slot) * p.D + 2 * d) =
-            pack2(re, ro);
-      }
-    } else {
-      const int h = head - p.nq - p.nkv;
-      bf16_t* vp = p.vt + (((size_t)b * p.nkv + h) * p.D + 2 * d) * p.cap + slot;
-      vp[0] = f2bf(e);
-      vp[p.cap] = f2bf(o);
-    }
+__global__ __launch_bounds__(256) void k_down_finish(FinishArgs p) {
+  const int m = blockIdx.y, n = blockIdx.x * 256 + threadIdx.x;
+  if (n >= p.H) return;                            // H % 16 == 0: whole 16-lane groups exit together
+  const int b = m / p.rps, j = m - b * p.rps;
+  const int count = p.st[b].count;
+  float* xp = p.x + (size_t)m * p.H + n;
+  float x = *xp;
+  if (j < count) {
+    float v = 0.f;
+    for (int sp = 0; sp < p.S; ++sp) v += p.part[((size_t)sp * p.M + m) * p.H + n];
+    x += v;
+    *xp = x;
   }
+  float sq = x * x;
+  for (int o = 1; o < 16; o <<= 1) sq += __shfl_xor(sq, o);
+  const int out = p.select_last ? b : m;
+  if (p.select_last && j != count - 1) return;
+  p.xg[(size_t)out * p.H + n] = f2bf(x * bf2f(p.gain[n]));
+  if ((n & 15) == 0) p.ss[(size_t)(n >> 4) * p.mpad + out] = sq;
 }
 
 // ---------------------------------------------------------------------------
@@ -461,14 +591,34 @@ __global__ __launch_bounds__(256) void k_attn(AttnArgs a) {
 #pragma unroll
   for (int dt = 0; dt < D / 16; ++dt) o[dt] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-  for (int kb = k0; kb < k1; kb += kKeyBlock) {
-    f32x4 sc[2];
+  // Fragments of one 32-key block: the K tiles (A operands of S^T = K Q^T) and
+  // the V^T tiles (A operands of O^T = V^T P^T).  Two statically named buffers:
+  // the next block's loads are issued before the current block is computed.
+  struct Frag {
+    u32x4 k[2][D / 32];
+    u32x4 v[D / 16];
+  };
+  auto load_block = [&](int kb, Frag& f) {
 #pragma unroll
     for (int h2 = 0; h2 < 2; ++h2) {
       const bf16_t* kp = Kb + (size_t)(kb + 16 * h2 + (lane & 15)) * D + 8 * g4;
+#pragma unroll
+      for (int t = 0; t < D / 32; ++t) f.k[h2][t] = ld16(kp + 32 * t);
+    }
+#pragma unroll
+    for (int dt = 0; dt < D / 16; ++dt) {
+      const bf16_t* vp = Vb + (size_t)(16 * dt + (lane & 15)) * a.cap + kb + 4 * g4;
+      const u32x2 lo = ld8(vp), hi = ld8(vp + 16);
+      f.v[dt] = u32x4{lo.x, lo.y, hi.x, hi.y};
+    }
+  };
+  auto compute_block = [&](int kb, const Frag& f) {
+    f32x4 sc[2];
+#pragma unroll
+    for (int h2 = 0; h2 < 2; ++h2) {
       f32x4 acc = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-      for (int t = 0; t < D / 32; ++t) acc = mfma16x16x32(ld16(kp + 32 * t), qf[t], acc);
+      for (int t = 0; t < D / 32; ++t) acc = mfma16x16x32(f.k[h2][t], qf[t], acc);
       sc[h2] = acc;
     }
     float p[8];
@@ -499,11 +649,17 @@ __global__ __launch_bounds__(256) void k_attn(AttnArgs a) {
     for (int dt = 0; dt < D / 16; ++dt) o[dt] *= alpha;
     const u32x4 pb = u32x4{pack2(p[0], p[1]), pack2(p[2], p[3]), pack2(p[4], p[5]), pack2(p[6], p[7])};
 #pragma unroll
-    for (int dt = 0; dt < D / 16; ++dt) {
-      const bf16_t* vp = Vb + (size_t)(16 * dt + (lane & 15)) * a.cap + kb + 4 * g4;
-      const u32x2 lo = ld8(vp), hi = ld8(vp + 16);
-      o[dt] = mfma16x16x32(u32x4{lo.x, lo.y, hi.x, hi.y}, pb, o[dt]);
-    }
+    for (int dt = 0; dt < D / 16; ++dt) o[dt] = mfma16x16x32(f.v[dt], pb, o[dt]);
+  };
+  Frag fa, fb;
+  load_block(k0, fa);
+  for (int kb = k0; kb < k1; kb += 2 * kKeyBlock) {
+    const bool has_b = kb + kKeyBlock < k1;
+    if (has_b) load_block(kb + kKeyBlock, fb);
+    compute_block(kb, fa);
+    if (!has_b) break;
+    if (kb + 2 * kKeyBlock < k1) load_block(kb + 2 * kKeyBlock, fa);
+    compute_block(kb + kKeyBlock, fb);
   }
   l_run += __shfl_xor(l_run, 16);
   l_run += __shfl_xor(l_run, 32);
@@ -519,7 +675,7 @@ __global__ __launch_bounds__(256) void k_attn(AttnArgs a) {
 }
 
 // Merge the splits of each (row, q head): o = sum_s 2^(m_s - M) O_s / sum_s
-// 2^(m_s - M) l_s.  grid (R, B), 256 threads.
+// 2^(m_s - M) l_s.  grid (R, q_heads, B), one thread per head dimension.
 struct CombineArgs {
   const SeqState* st;
   const float *op, *mp, *lp;
@@ -527,201 +683,98 @@ struct CombineArgs {
   int nq, D, R, B, chunk;
 };
 
-__global__ __launch_bounds__(256) void k_attn_combine(CombineArgs a) {
-  extern __shared__ float coef[];   // [nq][ns]
-  const int j = blockIdx.x, b = blockIdx.y;
+__global__ __launch_bounds__(128) void k_attn_combine(CombineArgs a) {
+  extern __shared__ float coef[];   // [ns]
+  const int j = blockIdx.x, h = blockIdx.y, b = blockIdx.z;
   const SeqState& s = a.st[b];
   if (j >= s.count) return;
   const int vis_end = s.base + j + 1;
   const int ns = (vis_end + a.chunk - 1) / a.chunk;   // splits holding keys this row sees
-  for (int h = threadIdx.x; h < a.nq; h += 256) {
+  const size_t row = ((size_t)b * a.nq + h) * a.R + j;
+  const size_t sstride = (size_t)a.B * a.nq * a.R;
+  if (threadIdx.x < 64) {
+    const int l = threadIdx.x;
     float M = -INFINITY;
-    for (int sp = 0; sp < ns; ++sp) M = fmaxf(M, a.mp[(((size_t)sp * a.B + b) * a.nq + h) * a.R + j]);
+    for (int sp = l; sp < ns; sp += 64) M = fmaxf(M, a.mp[sp * sstride + row]);
+    for (int o = 32; o > 0; o >>= 1) M = fmaxf(M, __shfl_xor(M, o));
     float L = 0.f;
-    for (int sp = 0; sp < ns; ++sp) {
-      const size_t i = (((size_t)sp * a.B + b) * a.nq + h) * a.R + j;
-      const float w = exp2f(a.mp[i] - M);
-      coef[h * ns + sp] = w;
-      L += w * a.lp[i];
+    for (int sp = l; sp < ns; sp += 64) {
+      const float w = exp2f(a.mp[sp * sstride + row] - M);
+      coef[sp] = w;
+      L += w * a.lp[sp * sstride + row];
     }
+    for (int o = 32; o > 0; o >>= 1) L += __shfl_xor(L, o);
     const float inv = 1.f / L;
-    for (int sp = 0; sp < ns; ++sp) coef[h * ns + sp] *= inv;
+    for (int sp = l; sp < ns; sp += 64) coef[sp] *= inv;
   }
   __syncthreads();
-  const int r = b * a.R + j;
-  for (int e = threadIdx.x; e < a.nq * a.D; e += 256) {
-    const int h = e / a.D, d = e % a.D;
+  const int d = threadIdx.x;
+  if (d < a.D) {
     float v = 0.f;
-    for (int sp = 0; sp < ns; ++sp)
-      v += coef[h * ns + sp] * a.op[((((size_t)sp * a.B + b) * a.nq + h) * a.R + j) * a.D + d];
-    a.o[(size_t)r * a.nq * a.D + e] = f2bf(v);
+    const float* src = a.op + row * a.D + d;
+    const size_t ostride = sstride * a.D;
+#pragma unroll 8
+    for (int sp = 0; sp < ns; ++sp) v += coef[sp] * src[sp * ostride];
+    a.o[(size_t)(b * a.R + j) * a.nq * a.D + h * a.D + d] = f2bf(v);
   }
 }
 
 // ---------------------------------------------------------------------------
-// Residual add of k-split partials + RMSNorm into the next GEMV input.
-// select_last: write only the row count-1 of each sequence, to out row b
-// (the draft proposes from its last row only).  grid (R, B), 256 threads.
+// Greedy token of each row (Eq. verify): reduce the LM head's per-tile
+// (max, index) pairs; larger logit wins, ties go to the lower index.
+// grid (rows per sequence, B), 1024 threads.  Verify: r*_{j+1} of row j goes
+// to rstar[j].  Draft: the proposal of the step's last row is appended to the
+// sequence's proposals and the draft length advances.
 // ---------------------------------------------------------------------------
-struct NormArgs {
-  const SeqState* st;
-  const float* part;     // [S][M][H] or null
-  int S, M, R, H;
-  float* x;
-  const bf16_t* g;
-  bf16_t* out;
-  int select_last;
-  float eps;
+struct AmaxArgs {
+  SeqState* st;
+  const float* amax_v;
+  const int32_t* amax_i;
+  int ntiles, mpad, rps, draft;
 };
 
-__global__ __launch_bounds__(256) void k_resid_norm(NormArgs p) {
-  __shared__ float sh[4];
+__global__ __launch_bounds__(1024) void k_argmax_rows(AmaxArgs p) {
+  __shared__ float shv[1024];
+  __shared__ int shi[1024];
   const int j = blockIdx.x, b = blockIdx.y;
-  const int count = p.st[b].count;
-  if (j >= count) return;
-  if (p.select_last && j != count - 1) return;
-  const int r = b * p.R + j;
-  float* xr = p.x + (size_t)r * p.H;
-  float ss = 0.f;
-  for (int n = threadIdx.x; n < p.H; n += 256) {
-    float v = xr[n];
-    if (p.part)
-      for (int sp = 0; sp < p.S; ++sp) v += p.part[((size_t)sp * p.M + r) * p.H + n];
-    xr[n] = v;
-    ss += v * v;
-  }
-  const float inv = rsqrtf(block_sum256(ss, sh) / p.H + p.eps);
-  bf16_t* orow = p.out + (size_t)(p.select_last ? b : r) * p.H;
-  for (int n = threadIdx.x; n < p.H; n += 256) orow[n] = f2bf(xr[n] * inv * bf2f(p.g[n]));
-}
-
-// SwiGLU finish: u = silu(gate) * up from the k-split partials of the fused
-// [gate; up] GEMV.  grid (R, B).
-struct SwigluArgs {
-  const SeqState* st;
-  const float* part;     // [S][M][2F]
-  int S, M, R, F;
-  bf16_t* u;             // [Mpad][F]
-};
-
-__global__ __launch_bounds__(256) void k_swiglu(SwigluArgs p) {
-  const int j = blockIdx.x, b = blockIdx.y;
-  if (j >= p.st[b].count) return;
-  const int r = b * p.R + j;
-  const size_t N = 2 * (size_t)p.F;
-  for (int n = threadIdx.x; n < p.F; n += 256) {
-    float gt = 0.f, up = 0.f;
-    for (int sp = 0; sp < p.S; ++sp) {
-      const float* pp = p.part + ((size_t)sp * p.M + r) * N;
-      gt += pp[n];
-      up += pp[p.F + n];
-    }
-    const float silu = gt / (1.f + expf(-gt));
-    p.u[(size_t)r * p.F + n] = f2bf(silu * up);
-  }
-}
-
-// ---------------------------------------------------------------------------
-// Greedy tokens of the verify rows and the accept length (Eq. verify,
-// Eq. accept), plus the commit list cut at a stop token or the budget.
-// grid B, 256 threads.
-// ---------------------------------------------------------------------------
-__device__ void reduce_amax_row(const float* av, const int32_t* ai, int ntiles, int mpad, int row, float* shv,
-                                int* shi, float& bv, int& bi) {
+  SeqState& s = p.st[b];
+  if (s.count == 0) return;
+  const int row = b * p.rps + j;
   float v = -INFINITY;
   int i = 0x7fffffff;
-  for (int t = threadIdx.x; t < ntiles; t += 256) amax_merge(v, i, av[(size_t)t * mpad + row], ai[(size_t)t * mpad + row]);
+  for (int t0 = threadIdx.x; t0 < p.ntiles; t0 += 1024 * 8) {
+    float vv[8];
+    int ii[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      const int t = t0 + 1024 * u;
+      vv[u] = t < p.ntiles ? p.amax_v[(size_t)t * p.mpad + row] : -INFINITY;
+      ii[u] = t < p.ntiles ? p.amax_i[(size_t)t * p.mpad + row] : 0x7fffffff;
+    }
+#pragma unroll
+    for (int u = 0; u < 8; ++u) amax_merge(v, i, vv[u], ii[u]);
+  }
   shv[threadIdx.x] = v;
   shi[threadIdx.x] = i;
   __syncthreads();
-  for (int o = 128; o > 0; o >>= 1) {
+  for (int o = 512; o > 0; o >>= 1) {
     if (threadIdx.x < o) {
-      float v2 = shv[threadIdx.x + o];
-      int i2 = shi[threadIdx.x + o];
       float v1 = shv[threadIdx.x];
       int i1 = shi[threadIdx.x];
-      amax_merge(v1, i1, v2, i2);
+      amax_merge(v1, i1, shv[threadIdx.x + o], shi[threadIdx.x + o]);
       shv[threadIdx.x] = v1;
       shi[threadIdx.x] = i1;
     }
     __syncthreads();
   }
-  bv = shv[0];
-  bi = shi[0];
-  __syncthreads();
-}
-
-struct AcceptArgs {
-  SeqState* st;
-  const float* amax_v;
-  const int32_t* amax_i;
-  int ntiles, mpad, R, K, stop, max_new;
-};
-
-__global__ __launch_bounds__(256) void k_accept(AcceptArgs p) {
-  __shared__ float shv[256];
-  __shared__ int shi[256];
-  const int b = blockIdx.x;
-  SeqState& s = p.st[b];
-  if (s.finished) {
-    if (threadIdx.x == 0) {
-      s.n_commit = 0;
-      s.fin_pending = 1;
-    }
-    return;
-  }
-  for (int j = 0; j < p.R; ++j) {
-    float bv;
-    int bi;
-    reduce_amax_row(p.amax_v, p.amax_i, p.ntiles, p.mpad, b * p.R + j, shv, shi, bv, bi);
-    if (threadIdx.x == 0) s.rstar[j] = bi;
-  }
   if (threadIdx.x == 0) {
-    int l = 0;
-    while (l < p.K && s.vtok[l + 1] == s.rstar[l]) ++l;
-    int c = l + 1;
-    for (int i = 0; i < l; ++i) s.committed[i] = s.vtok[i + 1];
-    s.committed[l] = s.rstar[l];
-    int fin = 0;
-    if (p.stop >= 0)
-      for (int i = 0; i < c; ++i)
-        if (s.committed[i] == p.stop) {
-          c = i + 1;
-          fin = 1;
-          break;
-        }
-    const int rem = p.max_new - s.n_gen;
-    if (c >= rem) {
-      c = rem;
-      fin = 1;
+    if (!p.draft) {
+      s.rstar[j] = shi[0];
+    } else {
+      s.props[s.dstep] = shi[0];
+      s.draft_len = s.base + s.count;
+      s.dstep += 1;
     }
-    s.accept_len = l;
-    s.n_commit = c;
-    s.fin_pending = fin;
-  }
-}
-
-// Draft proposal: argmax of the last row of the draft step.  grid B.
-struct PickArgs {
-  SeqState* st;
-  const float* amax_v;
-  const int32_t* amax_i;
-  int ntiles, mpad;
-};
-
-__global__ __launch_bounds__(256) void k_draft_pick(PickArgs p) {
-  __shared__ float shv[256];
-  __shared__ int shi[256];
-  const int b = blockIdx.x;
-  SeqState& s = p.st[b];
-  if (s.count == 0) return;
-  float bv;
-  int bi;
-  reduce_amax_row(p.amax_v, p.amax_i, p.ntiles, p.mpad, b, shv, shi, bv, bi);
-  if (threadIdx.x == 0) {
-    s.props[s.dstep] = bi;
-    s.draft_len = s.base + s.count;
-    s.dstep += 1;
   }
 }
 
@@ -730,17 +783,34 @@ __global__ void k_draft_out(const SeqState* st, int32_t* out, int K, int col) {
   out[blockIdx.x * K + col] = (s.count > 0 && s.dstep == col + 1) ? s.props[col] : -1;
 }
 
-// Commit (Eq. commit): append the committed tokens, advance the lengths, roll
-// the draft back to the first slot whose input differs from the committed
-// sequence (never past the new pending token).  grid B, 1 thread.
-__global__ void k_commit(SeqState* st, int32_t* hist, int cap, int K, int32_t* o_acc, int32_t* o_com,
-                         int32_t* o_n, int32_t* o_fin) {
+// Accept + commit (Eq. accept, Eq. commit): l = longest prefix of the verify's
+// draft tokens equal to the target's greedy tokens; commit (d_1..d_l, r*_{l+1})
+// cut after a stop token and at the token budget; append the tokens, advance
+// the lengths and roll the draft back to the first slot whose input differs
+// from the committed sequence (never past the new pending token).
+// grid B, 1 thread.
+__global__ void k_commit(SeqState* st, int32_t* hist, int cap, int K, int stop, int max_new, int32_t* o_acc,
+                         int32_t* o_com, int32_t* o_n, int32_t* o_fin) {
   const int b = blockIdx.x;
   SeqState& s = st[b];
-  int c = 0, acc = 0;
+  int c = 0, l = 0;
   if (!s.finished) {
-    c = s.n_commit;
-    acc = s.accept_len;
+    while (l < K && s.vtok[l + 1] == s.rstar[l]) ++l;
+    c = l + 1;
+    for (int i = 0; i < l; ++i) s.committed[i] = s.vtok[i + 1];
+    s.committed[l] = s.rstar[l];
+    int fin = 0;
+    if (stop >= 0)
+      for (int i = 0; i < c; ++i)
+        if (s.committed[i] == stop) {
+          c = i + 1;
+          fin = 1;
+          break;
+        }
+    if (c >= max_new - s.n_gen) {
+      c = max_new - s.n_gen;
+      fin = 1;
+    }
     const int n = s.seq_len;
     for (int i = 0; i < c; ++i) hist[(size_t)b * cap + n + 1 + i] = s.committed[i];
     int x = n + 1;
@@ -749,10 +819,12 @@ __global__ void k_commit(SeqState* st, int32_t* hist, int cap, int K, int32_t* o
     s.seq_len = n + c;
     s.pending = s.committed[c - 1];
     s.n_gen += c;
-    s.finished = s.fin_pending;
+    s.finished = fin;
+    s.accept_len = l;
+    s.n_commit = c;
   }
   s.dstep = 0;
-  if (o_acc) o_acc[b] = acc;
+  if (o_acc) o_acc[b] = l;
   if (o_n) o_n[b] = c;
   if (o_fin) o_fin[b] = s.finished;
   if (o_com)
@@ -763,12 +835,23 @@ __global__ void k_commit(SeqState* st, int32_t* hist, int cap, int K, int32_t* o
 // host-side launch helpers
 // ---------------------------------------------------------------------------
 
-int pick_splits(int N, int Kd) {
-  const int tiles = (N + kTile - 1) / kTile;
-  const int steps = (Kd + 31) / 32;
-  int s = (1024 + tiles - 1) / tiles;
-  const int smax = std::max(1, steps / 8);
-  return std::max(1, std::min(s, smax));
+int gemv_lds_limit() {
+  static int lim = -1;
+  if (lim < 0) {
+    int dev = 0, v = 0;
+    if (hipGetDevice(&dev) != hipSuccess ||
+        hipDeviceGetAttribute(&v, hipDeviceAttributeMaxSharedMemoryPerBlock, dev) != hipSuccess || v <= 0)
+      v = 65536;
+    lim = std::min(v, 160 * 1024) - 256;   // room for the small static arrays
+  }
+  return lim;
+}
+
+int down_splits(int M, int Kd) {
+  const int T = (Kd + 31) / 32;
+  int s = (T + kGemvWaves * kGemvSteps - 1) / (kGemvWaves * kGemvSteps);
+  while (s < T && gemv_lds_bytes(1, M, (T + s - 1) / s) > (size_t)gemv_lds_limit()) ++s;
+  return s;
 }
 
 namespace {
@@ -799,43 +882,45 @@ struct Timed {
 
 hipStream_t S(Ctx& c) { return c.stream; }
 
-template <int EPI>
-hipError_t gemv_dispatch(Ctx& c, const GemvArgs& g, int mb, int kind, double bytes) {
-  dim3 grid((g.N + kTile - 1) / kTile, g.splits);
+template <int EPI, int TT, int MB>
+void set_lds_limit() {
+  (void)hipFuncSetAttribute(reinterpret_cast<const void*>(&k_gemv<MB, kGemvWaves, kGemvSteps, TT, EPI>),
+                            hipFuncAttributeMaxDynamicSharedMemorySize, gemv_lds_limit());
+}
+
+template <int EPI, int TT>
+hipError_t gemv_launch(Ctx& c, const GemvArgs& g, int kind, double bytes) {
+  const int mb = (g.M + 15) / 16;
+  const int T = (g.Kd + 31) / 32;
+  const int span = (T + g.splits - 1) / g.splits;
+  const size_t lds = gemv_lds_bytes(TT, g.M, span);
+  if (lds > (size_t)gemv_lds_limit() || (span + kGemvWaves - 1) / kGemvWaves > kGemvSteps) return hipErrorInvalidValue;
+  const int groups = (EPI == EPI_SWIGLU) ? g.N / 32 : g.N / (kTile * TT);
+  const dim3 grid(groups, g.splits), block(kGemvWaves * 64);
   Timed t(c, kind, bytes);
   switch (mb) {
-    case 1: hipLaunchKernelGGL((k_gemv<1, EPI, 4>), grid, dim3(256), 0, S(c), g); break;
-    case 2: hipLaunchKernelGGL((k_gemv<2, EPI, 4>), grid, dim3(256), 0, S(c), g); break;
-    case 3: hipLaunchKernelGGL((k_gemv<3, EPI, 2>), grid, dim3(256), 0, S(c), g); break;
-    case 4: hipLaunchKernelGGL((k_gemv<4, EPI, 2>), grid, dim3(256), 0, S(c), g); break;
+    case 1: hipLaunchKernelGGL((k_gemv<1, kGemvWaves, kGemvSteps, TT, EPI>), grid, block, lds, S(c), g); break;
+    case 2: hipLaunchKernelGGL((k_gemv<2, kGemvWaves, kGemvSteps, TT, EPI>), grid, block, lds, S(c), g); break;
+    case 3: hipLaunchKernelGGL((k_gemv<3, kGemvWaves, kGemvSteps, TT, EPI>), grid, block, lds, S(c), g); break;
+    case 4: hipLaunchKernelGGL((k_gemv<4, kGemvWaves, kGemvSteps, TT, EPI>), grid, block, lds, S(c), g); break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();
 }
 
-// Algorithmic bytes of a GEMV launch: weights once, activations in, fp32 out.
-double gemv_bytes(int N, int Kd, int M, int S) {
-  return 2.0 * N * Kd + 2.0 * M * Kd + 4.0 * S * M * N;
+// Algorithmic bytes of a GEMV launch: weights once, activations in, results out.
+double gemv_bytes(int N, int Kd, int M, double out_bytes_per_elem) {
+  return 2.0 * N * Kd + 2.0 * M * Kd + out_bytes_per_elem * (double)M * N;
 }
 
-hipError_t gemv(Ctx& c, const bf16_t* w0, int n0, const bf16_t* w1, int n1, const bf16_t* w2, int n2, int Kd,
-                const bf16_t* x, int M, int S) {
+GemvArgs gemv_base(Ctx& c, int M, int rps) {
   GemvArgs g{};
-  g.w[0] = w0;
-  g.w[1] = w1;
-  g.w[2] = w2;
-  g.row0[0] = 0;
-  g.row0[1] = n0;
-  g.row0[2] = n0 + n1;
-  g.nseg = w2 ? 3 : (w1 ? 2 : 1);
-  g.N = n0 + n1 + n2;
-  g.Kd = Kd;
-  g.x = x;
-  g.ldx = Kd;
+  g.st = c.st;
   g.M = M;
-  g.splits = S;
-  g.part = c.part;
-  return gemv_dispatch<EPI_PARTIAL>(c, g, (M + 15) / 16, SPEC_KERNEL_GEMV, gemv_bytes(g.N, Kd, M, S));
+  g.rps = rps;
+  g.splits = 1;
+  g.mpad = c.Mpad;
+  return g;
 }
 
 #define CK(x)                               \
@@ -844,23 +929,40 @@ hipError_t gemv(Ctx& c, const bf16_t* w0, int n0, const bf16_t* w1, int n1, cons
     if (e_ != hipSuccess) return e_;        \
   } while (0)
 
-hipError_t run_layer(Ctx& c, Model& m, int li, int M, bool last_layer, const bf16_t* next_gain,
-                     bf16_t* next_out, bool select_last) {
+hipError_t run_layer(Ctx& c, Model& m, int li, const bf16_t* next_gain, bool select_last) {
   const spec_dims& d = m.d;
   const int H = d.hidden, D = d.head_dim, nq = d.q_heads, nkv = d.kv_heads, F = d.ffn;
+  const int M = c.M;
   const LayerW& w = m.L[li];
-  const size_t kvl = m.kv_layer;
-  bf16_t* kc = m.kc + kvl * li;
-  bf16_t* vt = m.vt + kvl * li;
-  const dim3 rows(c.R, c.B);
+  bf16_t* kc = m.kc + m.kv_layer * li;
+  bf16_t* vt = m.vt + m.kv_layer * li;
 
-  // q, k, v
-  CK(gemv(c, w.wq, nq * D, w.wk, nkv * D, w.wv, nkv * D, H, c.a, M, m.s_qkv));
+  // q, k, v (+ 1/rms of the attention norm) + rotary + cache append
   {
-    QkvArgs p{c.st, c.part, m.s_qkv, M, c.R, c.q, kc, vt, c.pos3, c.cs, m.axis, nq, nkv, D, c.cap, m.flat ? 1 : 0};
-    Timed t(c, SPEC_KERNEL_OTHER, 0);
-    hipLaunchKernelGGL(k_qkv_rope, rows, dim3(256), 0, S(c), p);
-    CK(hipGetLastError());
+    GemvArgs g = gemv_base(c, M, c.R);
+    g.w[0] = w.wq;
+    g.w[1] = w.wk;
+    g.w[2] = w.wv;
+    g.row0[0] = 0;
+    g.row0[1] = nq * D;
+    g.row0[2] = (nq + nkv) * D;
+    g.nseg = 3;
+    g.N = (nq + 2 * nkv) * D;
+    g.Kd = H;
+    g.x = c.xg;
+    g.ldx = H;
+    g.ss_in = c.ss;
+    g.H = H;
+    g.eps = d.rms_eps;
+    g.q = c.q;
+    g.kc = kc;
+    g.vt = vt;
+    g.rcs = c.rcs;
+    g.nq = nq;
+    g.nkv = nkv;
+    g.D = D;
+    g.cap = c.cap;
+    CK((gemv_launch<EPI_ROPE, 1>(c, g, SPEC_KERNEL_GEMV, gemv_bytes(g.N, H, M, 2.0))));
   }
   // attention
   {
@@ -869,47 +971,103 @@ hipError_t run_layer(Ctx& c, Model& m, int li, int M, bool last_layer, const bf1
     AttnArgs p{c.st, c.q, kc, vt, c.op, c.mp, c.lp, nq, nkv, G, c.R, c.B, c.cap, c.attn_chunk, rb,
                kLog2e / sqrtf((float)D)};
     dim3 grid(c.attn_splits, nkv * rb, c.B);
-    // KV bytes of the cached prefix read by every sequence (upper bound: capacity is not read)
-    Timed t(c, SPEC_KERNEL_ATTN, 0);
-    if (D == 128)
-      hipLaunchKernelGGL(k_attn<128>, grid, dim3(256), 0, S(c), p);
-    else
-      hipLaunchKernelGGL(k_attn<64>, grid, dim3(256), 0, S(c), p);
-    CK(hipGetLastError());
+    {
+      Timed t(c, SPEC_KERNEL_ATTN, 0);
+      if (D == 128)
+        hipLaunchKernelGGL(k_attn<128>, grid, dim3(256), 0, S(c), p);
+      else
+        hipLaunchKernelGGL(k_attn<64>, grid, dim3(256), 0, S(c), p);
+      CK(hipGetLastError());
+    }
     CombineArgs cb{c.st, c.op, c.mp, c.lp, c.o, nq, D, c.R, c.B, c.attn_chunk};
     Timed t2(c, SPEC_KERNEL_OTHER, 0);
-    hipLaunchKernelGGL(k_attn_combine, rows, dim3(256), (size_t)nq * c.attn_splits * sizeof(float), S(c), cb);
+    hipLaunchKernelGGL(k_attn_combine, dim3(c.R, nq, c.B), dim3(128), (size_t)c.attn_splits * sizeof(float), S(c),
+                       cb);
     CK(hipGetLastError());
   }
-  // o projection + residual + ffn norm
-  CK(gemv(c, w.wo, H, nullptr, 0, nullptr, 0, nq * D, c.o, M, m.s_o));
+  // o projection + residual; bf16(x * g_ffn) and sums of x^2 for the FFN norm
   {
-    NormArgs p{c.st, c.part, m.s_o, M, c.R, H, c.x, w.ffn_norm, c.a, 0, d.rms_eps};
-    Timed t(c, SPEC_KERNEL_OTHER, 0);
-    hipLaunchKernelGGL(k_resid_norm, rows, dim3(256), 0, S(c), p);
-    CK(hipGetLastError());
+    GemvArgs g = gemv_base(c, M, c.R);
+    g.w[0] = w.wo;
+    g.nseg = 1;
+    g.N = H;
+    g.Kd = nq * D;
+    g.x = c.o;
+    g.ldx = nq * D;
+    g.x32 = c.x;
+    g.gain = w.ffn_norm;
+    g.xg = c.xg;
+    g.ss_out = c.ss;
+    CK((gemv_launch<EPI_RESID, 1>(c, g, SPEC_KERNEL_GEMV, gemv_bytes(H, nq * D, M, 10.0))));
   }
-  // SwiGLU
-  CK(gemv(c, w.wg, F, w.wu, F, nullptr, 0, H, c.a, M, m.s_gu));
+  // gate/up (+ 1/rms of the FFN norm) + SwiGLU
   {
-    SwigluArgs p{c.st, c.part, m.s_gu, M, c.R, F, c.u};
-    Timed t(c, SPEC_KERNEL_OTHER, 0);
-    hipLaunchKernelGGL(k_swiglu, rows, dim3(256), 0, S(c), p);
-    CK(hipGetLastError());
+    GemvArgs g = gemv_base(c, M, c.R);
+    g.w[0] = w.wg;
+    g.w[1] = w.wu;
+    g.row0[1] = F;
+    g.nseg = 2;
+    g.N = 2 * F;
+    g.Kd = H;
+    g.x = c.xg;
+    g.ldx = H;
+    g.ss_in = c.ss;
+    g.H = H;
+    g.eps = d.rms_eps;
+    g.u = c.u;
+    CK((gemv_launch<EPI_SWIGLU, 2>(c, g, SPEC_KERNEL_GEMV, gemv_bytes(2 * F, H, M, 1.0))));
   }
-  // down projection + residual + next norm
-  CK(gemv(c, w.wd, H, nullptr, 0, nullptr, 0, F, c.u, M, m.s_down));
+  // down projection (k-split partials) -> residual + the next norm's input
   {
-    NormArgs p{c.st, c.part, m.s_down, M, c.R, H, c.x, next_gain, next_out, select_last ? 1 : 0, d.rms_eps};
+    GemvArgs g = gemv_base(c, M, c.R);
+    g.w[0] = w.wd;
+    g.nseg = 1;
+    g.N = H;
+    g.Kd = F;
+    g.x = c.u;
+    g.ldx = F;
+    g.splits = m.s_down;
+    g.out = c.part;
+    CK((gemv_launch<EPI_STORE, 1>(c, g, SPEC_KERNEL_GEMV, gemv_bytes(H, F, M, 4.0 * m.s_down))));
+    FinishArgs p{c.st, c.part, m.s_down, M, c.R, H, c.Mpad, select_last ? 1 : 0, c.x, next_gain, c.xg, c.ss};
     Timed t(c, SPEC_KERNEL_OTHER, 0);
-    hipLaunchKernelGGL(k_resid_norm, rows, dim3(256), 0, S(c), p);
+    hipLaunchKernelGGL(k_down_finish, dim3((H + 255) / 256, M), dim3(256), 0, S(c), p);
     CK(hipGetLastError());
   }
-  (void)last_layer;
   return hipSuccess;
 }
 
 }  // namespace
+
+void init_kernel_attributes() {
+  static bool done = false;
+  if (done) return;
+  done = true;
+  set_lds_limit<EPI_STORE, 1, 1>();
+  set_lds_limit<EPI_STORE, 1, 2>();
+  set_lds_limit<EPI_STORE, 1, 3>();
+  set_lds_limit<EPI_STORE, 1, 4>();
+  set_lds_limit<EPI_ROPE, 1, 1>();
+  set_lds_limit<EPI_ROPE, 1, 2>();
+  set_lds_limit<EPI_ROPE, 1, 3>();
+  set_lds_limit<EPI_ROPE, 1, 4>();
+  set_lds_limit<EPI_RESID, 1, 1>();
+  set_lds_limit<EPI_RESID, 1, 2>();
+  set_lds_limit<EPI_RESID, 1, 3>();
+  set_lds_limit<EPI_RESID, 1, 4>();
+  set_lds_limit<EPI_SWIGLU, 2, 1>();
+  set_lds_limit<EPI_SWIGLU, 2, 2>();
+  set_lds_limit<EPI_SWIGLU, 2, 3>();
+  set_lds_limit<EPI_SWIGLU, 2, 4>();
+  set_lds_limit<EPI_ARGMAX, 2, 1>();
+  set_lds_limit<EPI_ARGMAX, 2, 2>();
+  set_lds_limit<EPI_ARGMAX, 2, 3>();
+  set_lds_limit<EPI_ARGMAX, 2, 4>();
+  set_lds_limit<EPI_ARGMAX, 1, 1>();
+  set_lds_limit<EPI_ARGMAX, 1, 2>();
+  set_lds_limit<EPI_ARGMAX, 1, 3>();
+  set_lds_limit<EPI_ARGMAX, 1, 4>();
+}
 
 hipError_t launch_zero(Ctx& c, void* p, size_t bytes) {
   const size_t n = bytes / 16;
@@ -953,47 +1111,45 @@ hipError_t launch_forward(Ctx& c, PassMode mode) {
   const spec_dims& d = m.d;
   const int M = c.M;
   {
-    EmbedArgs p{c.st, c.hist, c.embed, m.L[0].attn_norm, c.x, c.a, d.hidden, c.R, c.cap, (int)mode, d.rms_eps};
+    EmbedArgs p{c.st,    c.hist, c.embed,      m.L[0].attn_norm, c.x, c.xg,     c.ss,  c.rcs,
+                c.pos3,  c.cs,   m.axis,       d.hidden,         c.R, c.cap,    (int)mode, c.Mpad,
+                d.head_dim, m.flat ? 1 : 0};
     Timed t(c, SPEC_KERNEL_OTHER, 0);
-    hipLaunchKernelGGL(k_embed, dim3(c.R, c.B), dim3(256), 0, c.stream, p);
+    hipLaunchKernelGGL(k_embed, dim3(c.R, c.B), dim3(1024), (size_t)d.hidden * sizeof(float), c.stream, p);
     CK(hipGetLastError());
   }
   const bool draft = mode == PASS_DRAFT;
   for (int li = 0; li < d.layers; ++li) {
     const bool last = li + 1 == d.layers;
-    const bf16_t* g = last ? m.final_norm : m.L[li + 1].attn_norm;
-    bf16_t* out = (last && draft) ? c.a_last : c.a;
-    CK(run_layer(c, m, li, M, last, g, out, last && draft));
+    CK(run_layer(c, m, li, last ? m.final_norm : m.L[li + 1].attn_norm, last && draft));
   }
-  // LM head with the fused per-tile argmax
-  GemvArgs g{};
-  g.w[0] = c.embed;
-  g.row0[0] = 0;
-  g.nseg = 1;
-  g.N = c.V;
-  g.Kd = d.hidden;
-  g.x = draft ? c.a_last : c.a;
-  g.ldx = d.hidden;
-  g.M = draft ? c.B : M;
-  g.splits = 1;
-  g.amax_v = c.amax_v;
-  g.amax_i = c.amax_i;
-  g.logits = c.logits;
-  g.st = c.st;
-  g.rps = draft ? 1 : c.R;
-  g.mpad = c.Mpad;
-  g.allow_logits = draft ? 0 : 1;
-  CK(gemv_dispatch<EPI_ARGMAX>(c, g, (g.M + 15) / 16, SPEC_KERNEL_LMHEAD,
-                               2.0 * c.V * d.hidden + 2.0 * g.M * d.hidden + 8.0 * (c.V / 16) * g.M));
+  // LM head (+ 1/rms of the final norm) with the fused per-tile argmax; the
+  // draft proposes from each sequence's last row only (stored as row b)
+  {
+    GemvArgs g = gemv_base(c, draft ? c.B : M, draft ? 1 : c.R);
+    g.w[0] = c.embed;
+    g.nseg = 1;
+    g.N = c.V;
+    g.Kd = d.hidden;
+    g.x = c.xg;
+    g.ldx = d.hidden;
+    g.ss_in = c.ss;
+    g.H = d.hidden;
+    g.eps = d.rms_eps;
+    g.amax_v = c.amax_v;
+    g.amax_i = c.amax_i;
+    g.logits = c.logits;
+    g.allow_logits = draft ? 0 : 1;
+    const double bytes = gemv_bytes(c.V, d.hidden, g.M, 0.0) + 8.0 * (c.V / kTile) * g.M;
+    if ((c.V / kTile) % 2 == 0)
+      CK((gemv_launch<EPI_ARGMAX, 2>(c, g, SPEC_KERNEL_LMHEAD, bytes)));
+    else
+      CK((gemv_launch<EPI_ARGMAX, 1>(c, g, SPEC_KERNEL_LMHEAD, bytes)));
+  }
   const int ntiles = c.V / kTile;
   Timed t(c, SPEC_KERNEL_OTHER, 0);
-  if (!draft) {
-    AcceptArgs p{c.st, c.amax_v, c.amax_i, ntiles, c.Mpad, c.R, c.K, c.cfg.stop_token, c.cfg.max_new_tokens};
-    hipLaunchKernelGGL(k_accept, dim3(c.B), dim3(256), 0, c.stream, p);
-  } else {
-    PickArgs p{c.st, c.amax_v, c.amax_i, ntiles, c.Mpad};
-    hipLaunchKernelGGL(k_draft_pick, dim3(c.B), dim3(256), 0, c.stream, p);
-  }
+  AmaxArgs p{c.st, c.amax_v, c.amax_i, ntiles, c.Mpad, draft ? 1 : c.R, draft ? 1 : 0};
+  hipLaunchKernelGGL(k_argmax_rows, dim3(draft ? 1 : c.R, c.B), dim3(1024), 0, c.stream, p);
   return hipGetLastError();
 }
 
@@ -1005,8 +1161,8 @@ hipError_t launch_draft_out(Ctx& c, int32_t* d_tokens) {
 
 hipError_t launch_commit(Ctx& c, int32_t* acc, int32_t* committed, int32_t* ncommit, int32_t* fin) {
   Timed t(c, SPEC_KERNEL_OTHER, 0);
-  hipLaunchKernelGGL(k_commit, dim3(c.B), dim3(1), 0, c.stream, c.st, c.hist, c.cap, c.K, acc, committed, ncommit,
-                     fin);
+  hipLaunchKernelGGL(k_commit, dim3(c.B), dim3(1), 0, c.stream, c.st, c.hist, c.cap, c.K, c.cfg.stop_token,
+                     c.cfg.max_new_tokens, acc, committed, ncommit, fin);
   return hipGetLastError();
 }
 

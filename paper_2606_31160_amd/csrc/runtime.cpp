@@ -216,22 +216,26 @@ Layout make_layout(const spec_config* cfg, const spec_seq_init* seqs) {
   return L;
 }
 
-void set_splits(Model& m) {
-  const spec_dims& d = m.d;
-  m.s_qkv = pick_splits((d.q_heads + 2 * d.kv_heads) * d.head_dim, d.hidden);
-  m.s_o = pick_splits(d.hidden, d.q_heads * d.head_dim);
-  m.s_gu = pick_splits(2 * d.ffn, d.hidden);
-  m.s_down = pick_splits(d.hidden, d.ffn);
-}
+void set_splits(Model& m, int M) { m.s_down = down_splits(M, m.d.ffn); }
 
-size_t part_elems_for(const Model& m, int M) {
-  const spec_dims& d = m.d;
-  size_t e = 0;
-  e = std::max(e, (size_t)m.s_qkv * M * (d.q_heads + 2 * d.kv_heads) * d.head_dim);
-  e = std::max(e, (size_t)m.s_o * M * d.hidden);
-  e = std::max(e, (size_t)m.s_gu * M * 2 * d.ffn);
-  e = std::max(e, (size_t)m.s_down * M * d.hidden);
-  return e;
+size_t part_elems_for(const Model& m, int M) { return (size_t)m.s_down * M * m.d.hidden; }
+
+// The q/k/v, o, gate/up and LM-head GEMVs keep a workgroup's whole reduction
+// (one k-split): their x rows for the full reduction length must fit in LDS,
+// and each wave streams at most kGemvSteps steps.
+bool check_fits(const spec_dims& d, int M, std::string& err, const char* who) {
+  const int Ks[2] = {d.hidden, d.q_heads * d.head_dim};
+  for (int Kd : Ks) {
+    const int T = (Kd + 31) / 32;
+    if (T > kGemvWaves * kGemvSteps || gemv_lds_bytes(2, M, T) > (size_t)gemv_lds_limit()) {
+      char buf[200];
+      snprintf(buf, sizeof buf, "%s: %d rows per pass (batch*(K+1)) with width %d exceed one GEMV workgroup", who, M,
+               Kd);
+      err = buf;
+      return false;
+    }
+  }
+  return true;
 }
 
 // Carves the workspace (base == nullptr only measures).  Returns total bytes.
@@ -248,11 +252,11 @@ size_t carve(Ctx& c, const spec_config* cfg, const spec_seq_init* seqs, bool has
   c.attn_splits = L.splits;
   c.tgt.d = cfg->target;
   c.tgt.flat = false;
-  set_splits(c.tgt);
+  set_splits(c.tgt, L.M);
   if (has_draft) {
     c.drf.d = cfg->draft;
     c.drf.flat = true;
-    set_splits(c.drf);
+    set_splits(c.drf, L.M);
   }
   const spec_dims& t = cfg->target;
   const int H = t.hidden, D = t.head_dim;
@@ -272,10 +276,12 @@ size_t carve(Ctx& c, const spec_config* cfg, const spec_seq_init* seqs, bool has
   c.tgt.axis = cv.take<int8_t>(D / 2);
   c.drf.axis = cv.take<int8_t>(D / 2);
   c.x = cv.take<float>((size_t)L.Mpad * H);
-  c.a = cv.take<bf16_t>((size_t)L.Mpad * H);
   c.q = cv.take<bf16_t>((size_t)L.Mpad * nqD);
   c.o = cv.take<bf16_t>((size_t)L.Mpad * nqD);
   c.u = cv.take<bf16_t>((size_t)L.Mpad * F);
+  c.xg = cv.take<bf16_t>((size_t)L.Mpad * H);
+  c.ss = cv.take<float>((size_t)(H / kTile) * L.Mpad);
+  c.rcs = cv.take<float2>((size_t)L.Mpad * (D / 2));
   c.part = cv.take<float>(part);
   c.part_elems = part;
   const size_t attn_rows = (size_t)L.splits * L.B * nq * L.R;
@@ -285,7 +291,6 @@ size_t carve(Ctx& c, const spec_config* cfg, const spec_seq_init* seqs, bool has
   c.amax_v = cv.take<float>((size_t)(L.V / kTile) * L.Mpad);
   c.amax_i = cv.take<int32_t>((size_t)(L.V / kTile) * L.Mpad);
   c.logits = cv.take<bf16_t>((size_t)L.Mpad * L.V);
-  c.a_last = cv.take<bf16_t>((size_t)16 * H);
   c.tgt.kv_layer = (size_t)L.B * t.kv_heads * L.cap * D;
   c.tgt.kc = cv.take<bf16_t>(c.tgt.kv_layer * t.layers);
   c.tgt.vt = cv.take<bf16_t>(c.tgt.kv_layer * t.layers);
@@ -406,6 +411,11 @@ spec_status spec_workspace_bytes(const spec_config* cfg, const spec_seq_init* se
       g_init_error = err;
       return SPEC_E_INVAL;
     }
+    const int M = cfg->batch * (cfg->K + 1);
+    if (!check_fits(cfg->target, M, err, "target") || (has_draft && !check_fits(cfg->draft, M, err, "draft"))) {
+      g_init_error = err;
+      return SPEC_E_CAPACITY;
+    }
     Ctx c;
     *bytes = carve(c, cfg, seqs, has_draft, nullptr);
     return SPEC_OK;
@@ -442,6 +452,13 @@ spec_status spec_init(const spec_config* cfg, const void* embed, const spec_mode
     g_init_error = "workspace: null or not 256-byte aligned";
     return SPEC_E_INVAL;
   }
+  {
+    const int M = cfg->batch * (cfg->K + 1);
+    if (!check_fits(cfg->target, M, err, "target") || (has_draft && !check_fits(cfg->draft, M, err, "draft"))) {
+      g_init_error = err;
+      return SPEC_E_CAPACITY;
+    }
+  }
   spec_ctx* ctx = nullptr;
   try {
     ctx = new spec_ctx();
@@ -473,6 +490,7 @@ spec_status spec_init(const spec_config* cfg, const void* embed, const spec_mode
     load_model(c.tgt, target);
     if (has_draft) load_model(c.drf, draft);
     if (hipGetDevice(&c.device) != hipSuccess) c.device = 0;
+    init_kernel_attributes();
 
     // host-built tables
     const int D = cfg->target.head_dim, half = D / 2;
