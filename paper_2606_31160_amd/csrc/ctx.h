@@ -75,6 +75,7 @@ struct Ctx {
   spec_config cfg{};
   int B = 1, K = 0, R = 1, M = 1, Mpad = 16, V = 0, cap = 0;
   int attn_chunk = 128, attn_splits = 1;
+  int ncu = 256;                     // compute units of the device (persistent GEMV grids)
   hipStream_t stream = nullptr;      // caller's stream
   hipStream_t cap_stream = nullptr;  // private stream used only for graph capture
   int device = 0;
@@ -140,7 +141,9 @@ hipError_t launch_logits_out(Ctx& c, void* d_logits);
 // of x.
 size_t gemv_lds_bytes(int TT, int M, int span_steps);
 int gemv_lds_limit();
-int down_splits(int M, int Kd);
+size_t gemv_p_lds_bytes(int M, int span_steps);
+int down_splits(int M, int Kd, int ncu);
+int num_cus();
 void init_kernel_attributes();
 
 }  // namespace specdec

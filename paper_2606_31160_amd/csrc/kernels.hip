@@ -232,7 +232,7 @@ enum {
   EPI_STORE = 0,   // out[split][m][n]: k-split partial sums (down projection)
   EPI_ROPE = 1,    // y/rms; rotation of q/k at the row's position, q store, K / V^T cache append (QKV)
   EPI_RESID = 2,   // x += y; xg = bf16(x * g); sums of x^2 (O projection)
-  EPI_SWIGLU = 3,  // y/rms; tiles (gate t, up t): u = silu(gate) * up (gate/up)
+  EPI_SWIGLU = 3,  // y/rms; half-tiles (8 gate rows, 8 up rows): u = silu(gate) * up (gate/up)
   EPI_ARGMAX = 4   // y/rms; per-tile (max, index) of the logits, optional bf16 logits (LM head)
 };
 
@@ -287,7 +287,7 @@ __global__ __launch_bounds__(NW * 64) void k_gemv(GemvArgs a) {
 
   int tile[TT];
 #pragma unroll
-  for (int tt = 0; tt < TT; ++tt) tile[tt] = (EPI == EPI_SWIGLU) ? tg + tt * (a.N / 32) : tg * TT + tt;
+  for (int tt = 0; tt < TT; ++tt) tile[tt] = tg * TT + tt;
 
   // 1. weight fragments -> registers
   u32x4 wv[TT][SMAX];
@@ -299,6 +299,11 @@ __global__ __launch_bounds__(NW * 64) void k_gemv(GemvArgs a) {
     for (int i = 1; i < 3; ++i)
       if (i < a.nseg && n0 >= a.row0[i]) sg = i;
     const bf16_t* wp = a.w[sg] + (size_t)(n0 - a.row0[sg] + (lane & 15)) * Kd + kq;
+    if constexpr (EPI == EPI_SWIGLU) {
+      // half-tile: rows 0-7 are gate rows n0/2 .. +8, rows 8-15 the matching up rows
+      const int r = lane & 15;
+      wp = (r < 8 ? a.w[0] + (size_t)(n0 / 2 + r) * Kd : a.w[1] + (size_t)(n0 / 2 + r - 8) * Kd) + kq;
+    }
 #pragma unroll
     for (int i = 0; i < SMAX; ++i) {
       const int k = (w0 + i) << 5;
@@ -316,14 +321,17 @@ __global__ __launch_bounds__(NW * 64) void k_gemv(GemvArgs a) {
     }
   }
 
-  // 3. live x rows, steps [s0, s1) -> LDS (row stride: span bf16)
+  // 3. live x rows, steps [s0, s1) -> LDS.  Rows are padded by one 16-byte
+  // chunk so that the 16 rows one MFMA reads at the same k fall in different
+  // LDS banks.
   const int per_row = (s1 - s0) * 4;              // 16-byte chunks per row
+  const int xstride = per_row + 1;
   u32x4* xs = reinterpret_cast<u32x4*>(lds);
   for (int c = threadIdx.x; per_row > 0 && c < a.M * per_row; c += NW * 64) {
     const int m = c / per_row, q = c - m * per_row;
     if (!((live >> m) & 1)) continue;
     const int k = s0 * 32 + q * 8;
-    xs[c] = k < Kd ? ld16(a.x + (size_t)m * a.ldx + k) : u32x4{0, 0, 0, 0};
+    xs[m * xstride + q] = k < Kd ? ld16(a.x + (size_t)m * a.ldx + k) : u32x4{0, 0, 0, 0};
   }
   if constexpr (kNorm) {
     // 1 / rms of each row from the per-16-column sums of squares (fixed order)
@@ -349,7 +357,7 @@ __global__ __launch_bounds__(NW * 64) void k_gemv(GemvArgs a) {
 #pragma unroll
       for (int mb = 0; mb < MB; ++mb) {
         const int m = mb * 16 + (lane & 15);
-        const u32x4 xv = ((live >> m) & 1) ? xs[m * per_row + (w0 + i - s0) * 4 + (lane >> 4)] : u32x4{0, 0, 0, 0};
+        const u32x4 xv = ((live >> m) & 1) ? xs[m * xstride + (w0 + i - s0) * 4 + (lane >> 4)] : u32x4{0, 0, 0, 0};
 #pragma unroll
         for (int tt = 0; tt < TT; ++tt) acc[tt][mb] = mfma16x16x32(wv[tt][i], xv, acc[tt][mb]);
       }
@@ -431,13 +439,14 @@ __global__ __launch_bounds__(NW * 64) void k_gemv(GemvArgs a) {
       a.ss_out[(size_t)tile[0] * a.mpad + threadIdx.x] = v;
     }
   } else if constexpr (EPI == EPI_SWIGLU) {
+    // TT == 1: columns 0-7 gate, 8-15 up of output features n0/2 .. n0/2 + 8
     const int F = a.N / 2;
     const int n0 = tile[0] * kTile;
-    const int t = threadIdx.x, m = t >> 4, c = t & 15;
-    if (t < nrow * 16 && m < a.M) {
+    const int t = threadIdx.x, m = t >> 3, c = t & 7;
+    if (t < nrow * 8 && m < a.M) {
       const float g = y[m * 17 + c];
-      const float up = y[(nrow + m) * 17 + c];
-      a.u[(size_t)m * F + n0 + c] = f2bf(g / (1.f + expf(-g)) * up);
+      const float up = y[m * 17 + 8 + c];
+      a.u[(size_t)m * F + n0 / 2 + c] = f2bf(g / (1.f + expf(-g)) * up);
     }
   } else {   // EPI_ARGMAX, TT tiles of the vocabulary
     for (int t = threadIdx.x; t < TT * nrow * 16; t += NW * 64) {
@@ -469,9 +478,176 @@ __global__ __launch_bounds__(NW * 64) void k_gemv(GemvArgs a) {
   }
 }
 
+// ---------------------------------------------------------------------------
+// Persistent variant for the large projections (gate/up, down, LM head).
+// gridDim.x workgroups are split into S groups, one per k-split; workgroup g
+// of group s stages x for split s's k-range in LDS once and then streams
+// tiles g, g + G_s, g + 2 G_s, ... (G_s workgroups per group), keeping the
+// next tile's weight fragments in flight while the current tile is reduced
+// and written.  Staging x once per workgroup instead of once per tile removes
+// most of the activation traffic at several rows per pass.
+// ---------------------------------------------------------------------------
+template <int MB, int NW, int SMAX, int EPI>
+__global__ __launch_bounds__(NW * 64) void k_gemv_p(GemvArgs a) {
+  static_assert(EPI == EPI_STORE || EPI == EPI_SWIGLU || EPI == EPI_ARGMAX, "persistent epilogues");
+  extern __shared__ __align__(16) unsigned char lds[];
+  __shared__ float inv_rms[MB * 16];
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int groups = a.splits;
+  const int gsize = gridDim.x / groups;
+  const int split = blockIdx.x / gsize, g = blockIdx.x % gsize;
+  const int ntiles = a.N / kTile;
+  const int Kd = a.Kd;
+  const int kq = 8 * (lane >> 4);
+  const int T = (Kd + 31) >> 5;
+  const int s0 = (int)((long long)split * T / a.splits);
+  const int s1 = (int)((long long)(split + 1) * T / a.splits);
+  const int chunk = (s1 - s0 + NW - 1) / NW;
+  const int w0 = s0 + wave * chunk;
+  const int w1 = min(w0 + chunk, s1);
+  constexpr bool kNorm = EPI == EPI_SWIGLU || EPI == EPI_ARGMAX;
+  const int per_row = (s1 - s0) * 4, xstride = per_row + 1;
+  u32x4* xs = reinterpret_cast<u32x4*>(lds);
+  f32x4* red = reinterpret_cast<f32x4*>(lds + (size_t)a.M * xstride * 16);                 // [NW][MB][64]
+  float* y = reinterpret_cast<float*>(lds + (size_t)a.M * xstride * 16 + (size_t)NW * MB * 64 * 16);   // [MB*16][17]
+
+  auto load_tile = [&](int tile, u32x4 (&wv)[SMAX]) {
+    const int n0 = tile * kTile;
+    const bf16_t* wp;
+    if constexpr (EPI == EPI_SWIGLU) {
+      const int r = lane & 15;
+      wp = (r < 8 ? a.w[0] + (size_t)(n0 / 2 + r) * Kd : a.w[1] + (size_t)(n0 / 2 + r - 8) * Kd) + kq;
+    } else {
+      wp = a.w[0] + (size_t)(n0 + (lane & 15)) * Kd + kq;
+    }
+#pragma unroll
+    for (int i = 0; i < SMAX; ++i) {
+      const int k = (w0 + i) << 5;
+      wv[i] = (w0 + i < w1 && k + kq < Kd) ? ld16(wp + k) : u32x4{0, 0, 0, 0};
+    }
+  };
+
+  u32x4 wa[SMAX], wb[SMAX];
+  int t = g;
+  if (t < ntiles) load_tile(t, wa);
+
+  uint64_t live = 0;
+  {
+    const int nseq = (a.M + a.rps - 1) / a.rps;
+    for (int b = 0; b < nseq; ++b) {
+      const int n = min(a.st[b].count, a.rps);
+      if (n > 0) live |= ((1ull << n) - 1ull) << (b * a.rps);
+    }
+  }
+  for (int c = threadIdx.x; per_row > 0 && c < a.M * per_row; c += NW * 64) {
+    const int m = c / per_row, q = c - m * per_row;
+    if (!((live >> m) & 1)) continue;
+    const int k = s0 * 32 + q * 8;
+    xs[m * xstride + q] = k < Kd ? ld16(a.x + (size_t)m * a.ldx + k) : u32x4{0, 0, 0, 0};
+  }
+  if constexpr (kNorm) {
+    for (int m = wave; m < MB * 16; m += NW) {
+      float v = 0.f;
+      if ((live >> m) & 1)
+        for (int tt = lane; tt < a.H / kTile; tt += 64) v += a.ss_in[(size_t)tt * a.mpad + m];
+      for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
+      if (lane == 0) inv_rms[m] = rsqrtf(v / a.H + a.eps);
+    }
+  }
+  __syncthreads();
+
+  const int nrow = MB * 16;
+  auto do_tile = [&](int tile, const u32x4 (&wv)[SMAX]) {
+    f32x4 acc[MB];
+#pragma unroll
+    for (int mb = 0; mb < MB; ++mb) acc[mb] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int i = 0; i < SMAX; ++i) {
+      if (w0 + i < w1) {
+#pragma unroll
+        for (int mb = 0; mb < MB; ++mb) {
+          const int m = mb * 16 + (lane & 15);
+          const u32x4 xv = ((live >> m) & 1) ? xs[m * xstride + (w0 + i - s0) * 4 + (lane >> 4)] : u32x4{0, 0, 0, 0};
+          acc[mb] = mfma16x16x32(wv[i], xv, acc[mb]);
+        }
+      }
+    }
+#pragma unroll
+    for (int mb = 0; mb < MB; ++mb) red[(wave * MB + mb) * 64 + lane] = acc[mb];
+    __syncthreads();
+    for (int q = threadIdx.x; q < MB * 256; q += NW * 64) {
+      const int mb = q >> 8, L = (q & 255) >> 2, i = q & 3;
+      float v = 0.f;
+#pragma unroll
+      for (int w = 0; w < NW; ++w) v += red[(w * MB + mb) * 64 + L][i];
+      const int m = mb * 16 + (L & 15);
+      y[m * 17 + 4 * (L >> 4) + i] = kNorm ? v * inv_rms[m] : v;
+    }
+    __syncthreads();
+    const int n0 = tile * kTile;
+    if constexpr (EPI == EPI_STORE) {
+      for (int q = threadIdx.x; q < nrow * 16; q += NW * 64) {
+        const int m = q >> 4, c = q & 15;
+        if (m < a.M) a.out[((size_t)split * a.M + m) * a.N + n0 + c] = y[m * 17 + c];
+      }
+    } else if constexpr (EPI == EPI_SWIGLU) {
+      const int F = a.N / 2;
+      const int q = threadIdx.x, m = q >> 3, c = q & 7;
+      if (q < nrow * 8 && m < a.M) {
+        const float gt = y[m * 17 + c], up = y[m * 17 + 8 + c];
+        a.u[(size_t)m * F + n0 / 2 + c] = f2bf(gt / (1.f + expf(-gt)) * up);
+      }
+    } else {
+      for (int q = threadIdx.x; q < nrow * 16; q += NW * 64) {
+        const int m = q >> 4, c = q & 15;
+        if (a.allow_logits && m < a.M && a.st[m / a.rps].want_logits)
+          a.logits[(size_t)m * a.N + n0 + c] = f2bf(y[m * 17 + c]);
+      }
+      if (threadIdx.x < nrow && threadIdx.x < a.M) {
+        const int m = threadIdx.x;
+        float best = -INFINITY;
+        int bi = n0;
+        bool nan = false;
+        for (int c = 0; c < 16; ++c) {
+          float v = y[m * 17 + c];
+          if (v != v) {
+            nan = true;
+            v = -INFINITY;
+          }
+          if (v > best) {
+            best = v;
+            bi = n0 + c;
+          }
+        }
+        a.amax_v[(size_t)tile * a.mpad + m] = best;
+        a.amax_i[(size_t)tile * a.mpad + m] = bi;
+        if (nan) atomicOr(const_cast<int32_t*>(&a.st[m / a.rps].err), ERR_NUMERIC);
+      }
+    }
+  };
+  // workgroup-uniform loop: every thread reaches every barrier; ends after
+  // the last tile of this workgroup's stride
+  while (t < ntiles) {
+    const int t2 = t + gsize;
+    if (t2 < ntiles) load_tile(t2, wb);
+    do_tile(t, wa);
+    if (t2 >= ntiles) break;
+    const int t3 = t2 + gsize;
+    if (t3 < ntiles) load_tile(t3, wa);
+    do_tile(t2, wb);
+    t = t3;
+  }
+}
+
+// Dynamic LDS of a persistent launch: x rows + per-wave tiles + the summed tile.
+size_t gemv_p_lds_bytes(int M, int span_steps) {
+  const int MB = (M + 15) / 16;
+  return (size_t)M * (span_steps * 64 + 16) + (size_t)kGemvWaves * MB * 64 * 16 + (size_t)MB * 16 * 17 * 4;
+}
+
 size_t gemv_lds_bytes(int TT, int M, int span_steps) {
   const int MB = (M + 15) / 16;
-  const size_t x = (size_t)M * span_steps * 64;
+  const size_t x = (size_t)M * (span_steps * 64 + 16);
   const size_t red = (size_t)kGemvWaves * TT * MB * 64 * 16 + (size_t)TT * MB * 16 * 17 * 4;
   return std::max(x, red);
 }
@@ -835,6 +1011,18 @@ __global__ void k_commit(SeqState* st, int32_t* hist, int cap, int K, int stop, 
 // host-side launch helpers
 // ---------------------------------------------------------------------------
 
+int num_cus() {
+  static int n = -1;
+  if (n < 0) {
+    int dev = 0, v = 0;
+    if (hipGetDevice(&dev) != hipSuccess ||
+        hipDeviceGetAttribute(&v, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || v <= 0)
+      v = 256;
+    n = v;
+  }
+  return n;
+}
+
 int gemv_lds_limit() {
   static int lim = -1;
   if (lim < 0) {
@@ -847,10 +1035,13 @@ int gemv_lds_limit() {
   return lim;
 }
 
-int down_splits(int M, int Kd) {
+int down_splits(int M, int Kd, int ncu) {
   const int T = (Kd + 31) / 32;
   int s = (T + kGemvWaves * kGemvSteps - 1) / (kGemvWaves * kGemvSteps);
-  while (s < T && gemv_lds_bytes(1, M, (T + s - 1) / s) > (size_t)gemv_lds_limit()) ++s;
+  while (s < T && gemv_p_lds_bytes(M, (T + s - 1) / s) > (size_t)gemv_lds_limit()) ++s;
+  // prefer a split count that divides the workgroups evenly (one group per split)
+  for (int t = s; t <= 2 * s && t <= T; ++t)
+    if (ncu % t == 0) return t;
   return s;
 }
 
@@ -895,7 +1086,7 @@ hipError_t gemv_launch(Ctx& c, const GemvArgs& g, int kind, double bytes) {
   const int span = (T + g.splits - 1) / g.splits;
   const size_t lds = gemv_lds_bytes(TT, g.M, span);
   if (lds > (size_t)gemv_lds_limit() || (span + kGemvWaves - 1) / kGemvWaves > kGemvSteps) return hipErrorInvalidValue;
-  const int groups = (EPI == EPI_SWIGLU) ? g.N / 32 : g.N / (kTile * TT);
+  const int groups = g.N / (kTile * TT);
   const dim3 grid(groups, g.splits), block(kGemvWaves * 64);
   Timed t(c, kind, bytes);
   switch (mb) {
@@ -903,6 +1094,34 @@ hipError_t gemv_launch(Ctx& c, const GemvArgs& g, int kind, double bytes) {
     case 2: hipLaunchKernelGGL((k_gemv<2, kGemvWaves, kGemvSteps, TT, EPI>), grid, block, lds, S(c), g); break;
     case 3: hipLaunchKernelGGL((k_gemv<3, kGemvWaves, kGemvSteps, TT, EPI>), grid, block, lds, S(c), g); break;
     case 4: hipLaunchKernelGGL((k_gemv<4, kGemvWaves, kGemvSteps, TT, EPI>), grid, block, lds, S(c), g); break;
+    default: return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
+
+template <int EPI, int MB>
+void set_lds_limit_p() {
+  (void)hipFuncSetAttribute(reinterpret_cast<const void*>(&k_gemv_p<MB, kGemvWaves, kGemvSteps, EPI>),
+                            hipFuncAttributeMaxDynamicSharedMemorySize, gemv_lds_limit());
+}
+
+// Persistent launch: `workgroups` is a multiple of g.splits (one group per k-split).
+template <int EPI>
+hipError_t gemv_launch_p(Ctx& c, const GemvArgs& g, int workgroups, int kind, double bytes) {
+  const int mb = (g.M + 15) / 16;
+  const int T = (g.Kd + 31) / 32;
+  const int span = (T + g.splits - 1) / g.splits;
+  const size_t lds = gemv_p_lds_bytes(g.M, span);
+  if (lds > (size_t)gemv_lds_limit() || (span + kGemvWaves - 1) / kGemvWaves > kGemvSteps ||
+      workgroups % g.splits != 0)
+    return hipErrorInvalidValue;
+  const dim3 grid(workgroups), block(kGemvWaves * 64);
+  Timed t(c, kind, bytes);
+  switch (mb) {
+    case 1: hipLaunchKernelGGL((k_gemv_p<1, kGemvWaves, kGemvSteps, EPI>), grid, block, lds, S(c), g); break;
+    case 2: hipLaunchKernelGGL((k_gemv_p<2, kGemvWaves, kGemvSteps, EPI>), grid, block, lds, S(c), g); break;
+    case 3: hipLaunchKernelGGL((k_gemv_p<3, kGemvWaves, kGemvSteps, EPI>), grid, block, lds, S(c), g); break;
+    case 4: hipLaunchKernelGGL((k_gemv_p<4, kGemvWaves, kGemvSteps, EPI>), grid, block, lds, S(c), g); break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();
@@ -1015,7 +1234,7 @@ hipError_t run_layer(Ctx& c, Model& m, int li, const bf16_t* next_gain, bool sel
     g.H = H;
     g.eps = d.rms_eps;
     g.u = c.u;
-    CK((gemv_launch<EPI_SWIGLU, 2>(c, g, SPEC_KERNEL_GEMV, gemv_bytes(2 * F, H, M, 1.0))));
+    CK(gemv_launch_p<EPI_SWIGLU>(c, g, std::min(c.ncu, 2 * F / kTile), SPEC_KERNEL_GEMV, gemv_bytes(2 * F, H, M, 1.0)));
   }
   // down projection (k-split partials) -> residual + the next norm's input
   {
@@ -1028,7 +1247,8 @@ hipError_t run_layer(Ctx& c, Model& m, int li, const bf16_t* next_gain, bool sel
     g.ldx = F;
     g.splits = m.s_down;
     g.out = c.part;
-    CK((gemv_launch<EPI_STORE, 1>(c, g, SPEC_KERNEL_GEMV, gemv_bytes(H, F, M, 4.0 * m.s_down))));
+    const int per_split = std::max(1, std::min(c.ncu / m.s_down, H / kTile));
+    CK(gemv_launch_p<EPI_STORE>(c, g, per_split * m.s_down, SPEC_KERNEL_GEMV, gemv_bytes(H, F, M, 4.0 * m.s_down)));
     FinishArgs p{c.st, c.part, m.s_down, M, c.R, H, c.Mpad, select_last ? 1 : 0, c.x, next_gain, c.xg, c.ss};
     Timed t(c, SPEC_KERNEL_OTHER, 0);
     hipLaunchKernelGGL(k_down_finish, dim3((H + 255) / 256, M), dim3(256), 0, S(c), p);
@@ -1043,26 +1263,34 @@ void init_kernel_attributes() {
   static bool done = false;
   if (done) return;
   done = true;
+  set_lds_limit_p<EPI_STORE, 1>();
+  set_lds_limit_p<EPI_STORE, 2>();
+  set_lds_limit_p<EPI_STORE, 3>();
+  set_lds_limit_p<EPI_STORE, 4>();
+  set_lds_limit_p<EPI_SWIGLU, 1>();
+  set_lds_limit_p<EPI_SWIGLU, 2>();
+  set_lds_limit_p<EPI_SWIGLU, 3>();
+  set_lds_limit_p<EPI_SWIGLU, 4>();
+  set_lds_limit_p<EPI_ARGMAX, 1>();
+  set_lds_limit_p<EPI_ARGMAX, 2>();
+  set_lds_limit_p<EPI_ARGMAX, 3>();
+  set_lds_limit_p<EPI_ARGMAX, 4>();
   set_lds_limit<EPI_STORE, 1, 1>();
   set_lds_limit<EPI_STORE, 1, 2>();
   set_lds_limit<EPI_STORE, 1, 3>();
   set_lds_limit<EPI_STORE, 1, 4>();
   set_lds_limit<EPI_ROPE, 1, 1>();
+  set_lds_limit<EPI_SWIGLU, 1, 1>();
   set_lds_limit<EPI_ROPE, 1, 2>();
+  set_lds_limit<EPI_SWIGLU, 1, 2>();
   set_lds_limit<EPI_ROPE, 1, 3>();
+  set_lds_limit<EPI_SWIGLU, 1, 3>();
   set_lds_limit<EPI_ROPE, 1, 4>();
+  set_lds_limit<EPI_SWIGLU, 1, 4>();
   set_lds_limit<EPI_RESID, 1, 1>();
   set_lds_limit<EPI_RESID, 1, 2>();
   set_lds_limit<EPI_RESID, 1, 3>();
   set_lds_limit<EPI_RESID, 1, 4>();
-  set_lds_limit<EPI_SWIGLU, 2, 1>();
-  set_lds_limit<EPI_SWIGLU, 2, 2>();
-  set_lds_limit<EPI_SWIGLU, 2, 3>();
-  set_lds_limit<EPI_SWIGLU, 2, 4>();
-  set_lds_limit<EPI_ARGMAX, 2, 1>();
-  set_lds_limit<EPI_ARGMAX, 2, 2>();
-  set_lds_limit<EPI_ARGMAX, 2, 3>();
-  set_lds_limit<EPI_ARGMAX, 2, 4>();
   set_lds_limit<EPI_ARGMAX, 1, 1>();
   set_lds_limit<EPI_ARGMAX, 1, 2>();
   set_lds_limit<EPI_ARGMAX, 1, 3>();
@@ -1141,10 +1369,7 @@ hipError_t launch_forward(Ctx& c, PassMode mode) {
     g.logits = c.logits;
     g.allow_logits = draft ? 0 : 1;
     const double bytes = gemv_bytes(c.V, d.hidden, g.M, 0.0) + 8.0 * (c.V / kTile) * g.M;
-    if ((c.V / kTile) % 2 == 0)
-      CK((gemv_launch<EPI_ARGMAX, 2>(c, g, SPEC_KERNEL_LMHEAD, bytes)));
-    else
-      CK((gemv_launch<EPI_ARGMAX, 1>(c, g, SPEC_KERNEL_LMHEAD, bytes)));
+    CK(gemv_launch_p<EPI_ARGMAX>(c, g, std::min(c.ncu, c.V / kTile), SPEC_KERNEL_LMHEAD, bytes));
   }
   const int ntiles = c.V / kTile;
   Timed t(c, SPEC_KERNEL_OTHER, 0);

@@ -216,7 +216,7 @@ Layout make_layout(const spec_config* cfg, const spec_seq_init* seqs) {
   return L;
 }
 
-void set_splits(Model& m, int M) { m.s_down = down_splits(M, m.d.ffn); }
+void set_splits(Model& m, int M) { m.s_down = down_splits(M, m.d.ffn, num_cus()); }
 
 size_t part_elems_for(const Model& m, int M) { return (size_t)m.s_down * M * m.d.hidden; }
 
@@ -227,7 +227,7 @@ bool check_fits(const spec_dims& d, int M, std::string& err, const char* who) {
   const int Ks[2] = {d.hidden, d.q_heads * d.head_dim};
   for (int Kd : Ks) {
     const int T = (Kd + 31) / 32;
-    if (T > kGemvWaves * kGemvSteps || gemv_lds_bytes(2, M, T) > (size_t)gemv_lds_limit()) {
+    if (T > kGemvWaves * kGemvSteps || gemv_p_lds_bytes(M, T) > (size_t)gemv_lds_limit()) {
       char buf[200];
       snprintf(buf, sizeof buf, "%s: %d rows per pass (batch*(K+1)) with width %d exceed one GEMV workgroup", who, M,
                Kd);
@@ -249,6 +249,7 @@ size_t carve(Ctx& c, const spec_config* cfg, const spec_seq_init* seqs, bool has
   c.V = L.V;
   c.cap = L.cap;
   c.attn_chunk = L.chunk;
+  c.ncu = num_cus();
   c.attn_splits = L.splits;
   c.tgt.d = cfg->target;
   c.tgt.flat = false;
