@@ -53,6 +53,30 @@ def draft_step_bytes(w, n_ctx):
     return d.layers * layer_w + 2 * w.vocab * d.hidden + (n_ctx + 1) * kv_row
 
 
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "k_gemv_p_swiglu_7b_verify_hbm_traffic.txt")
+KERNEL_SOURCE = os.path.join(ROOT, "paper_2606_31160_amd", "csrc", "kernels.hip")
+
+
+def measured_traffic():
+    """HBM bytes per gate/up launch from the committed FETCH_SIZE / WRITE_SIZE
+    counter summary, or None when the kernel source changed since it was taken."""
+    import hashlib
+    try:
+        fields = {}
+        with open(TRAFFIC_FILE) as f:
+            for line in f:
+                if ":" in line and line.startswith("- "):
+                    k, v = line[2:].split(":", 1)
+                    fields[k.strip()] = v.strip().strip("`")
+        with open(KERNEL_SOURCE, "rb") as f:
+            digest = hashlib.sha256(f.read()).hexdigest()
+        if fields.get("kernels.hip sha256") != digest:
+            return None
+        return float(fields["traffic bytes per launch"])
+    except (OSError, KeyError, ValueError):
+        return None
+
+
 def lcp(a, b):
     n = 0
     while n < len(a) and n < len(b) and int(a[n]) == int(b[n]):
@@ -91,13 +115,14 @@ def cpu_baseline(w, src, tokens_per_round, K):
     blocks = [(b.start, b.t, b.h, b.w) for b in lay.blocks]
     cap = lay.prefix_len + K + 2
 
+    import torch
+
+    def bits(t):
+        return t.view(torch.int16).cpu().numpy().view(np.uint16)
+
     def kv(model):
-        def f(li):
-            return (W.prefix_kv_device(w, 0, model, li, "k").view(__import__("torch").int16).cpu().numpy()
-                    .view(np.uint16),
-                    W.prefix_kv_device(w, 0, model, li, "v").view(__import__("torch").int16).cpu().numpy()
-                    .view(np.uint16))
-        return f
+        return lambda li: (bits(W.prefix_kv_device(w, 0, model, li, "k")),
+                           bits(W.prefix_kv_device(w, 0, model, li, "v")))
 
     tl, dl = 2, 1
     T = OM.Decoder(Slice(src), "target", dataclasses.replace(w.target, layers=tl), vs, OM.ROTARY_MROPE,
@@ -136,16 +161,56 @@ def cpu_baseline(w, src, tokens_per_round, K):
     }
 
 
+def calibration_copy():
+    """A plain device copy of 2^30 bytes: its FETCH_SIZE / WRITE_SIZE readings
+    convert the counters of the measured kernels to bytes."""
+    import torch
+    a = torch.empty(1 << 29, dtype=torch.int16, device="cuda").fill_(1)
+    b = torch.empty_like(a)
+    torch.cuda.synchronize()
+    b.copy_(a)
+    torch.cuda.synchronize()
+    log(f"calibration copy: {a.numel() * 2} bytes read, {b.numel() * 2} written")
+
+
+def pmc_pass(rounds, K):
+    """Rounds of the timed workload, launched kernel by kernel, for counter
+    collection; prints one line per round."""
+    import torch
+    import workloads as W
+    from paper_2606_31160_amd import binding as B
+    from paper_2606_31160_amd.harness import Session
+    w = W.get("C3").with_(max_new_tokens=rounds * (K + 1) + 8)
+    s = Session(w, source="device", provider=W.DeviceWeights(w), flags=B.SPEC_FLAG_NO_GRAPHS)
+    rng = np.random.default_rng(5)
+    for r in range(rounds):
+        for _ in range(K):
+            B.draft_step(s.ctx, s.dtok.data_ptr())
+        d = torch.tensor(rng.integers(0, w.vocab, size=(1, K)), dtype=torch.int32, device="cuda")
+        B.spec_verify(s.ctx, d.data_ptr(), 0)
+        B.spec_commit(s.ctx, s.acc.data_ptr(), 0, s.ncom.data_ptr(), s.fin.data_ptr())
+        torch.cuda.synchronize()
+        log(f"round {r} done")
+    s.close()
+    calibration_copy()
+    log("pmc pass done")
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--calibration-copy", action="store_true",
+                    help="end with a plain 1 GiB device copy (reference for HBM byte counters)")
+    ap.add_argument("--pmc-pass", type=int, default=0, metavar="R",
+                    help="counter-collection pass: R speculative rounds with random drafts on direct "
+                         "launches (no timing, no JSON line), then the calibration copy")
     args = ap.parse_args()
     if args.gpus != 1:
-        print(json.dumps({"error": "this build runs on one GPU only; the multi-GPU design is described in "
-                                   "DESIGN.md (scenes shard across GPUs with no exchange)"}))
+        print(json.dumps({"error": "one GPU only: independent scenes would shard across GPUs with no "
+                                   "exchange, so the single-GPU rate is the per-GPU rate"}))
         sys.exit(2)
 
     import torch
@@ -156,6 +221,9 @@ def main():
     from paper_2606_31160_amd.harness import Session
 
     K = 8
+    if args.pmc_pass:
+        pmc_pass(args.pmc_pass, K)
+        return
     rounds_total = args.warmup + args.steps + 3
     max_new = rounds_total * (K + 1) + 8
     w = W.get("C3").with_(max_new_tokens=max_new)
@@ -237,15 +305,18 @@ def main():
     B.spec_timing(s.ctx, True)
     for r in range(args.warmup + args.steps, rounds_total - 1):
         round_(r)
-    n_g, ms_g, by_g = B.spec_timing_read(s.ctx, "gemv")
-    n_l, ms_l, by_l = B.spec_timing_read(s.ctx, "lmhead")
-    n_a, ms_a, _ = B.spec_timing_read(s.ctx, "attn")
-    n_o, ms_o, _ = B.spec_timing_read(s.ctx, "other")
+    kernels = {}
+    for kind in ("qkv", "o", "gateup", "down", "lmhead", "attn", "other"):
+        n, ms, by = B.spec_timing_read(s.ctx, kind)
+        kernels[kind] = {"launches": int(n), "avg_us": round(ms * 1e3 / max(n, 1), 2)}
+        if by > 0:
+            kernels[kind]["bytes_per_launch"] = round(by / max(n, 1))
+            kernels[kind]["gbs"] = round(by / (ms * 1e-3) / 1e9, 1)
     B.spec_timing(s.ctx, False)
     s.close()
-    gemv_gbs = by_g / (ms_g * 1e-3) / 1e9
-    log(f"kernel time per pass-set: gemv {ms_g:.2f} ms / {n_g}, lmhead {ms_l:.2f} / {n_l}, "
-        f"attn {ms_a:.2f} / {n_a}, other {ms_o:.2f} / {n_o}")
+    log("per-kernel timing: " + json.dumps(kernels))
+    gu = kernels["gateup"]
+    gu_gbs = gu["bytes_per_launch"] / (gu["avg_us"] * 1e-6) / 1e9
 
     n_ctx = n_prompt + expect // 2
     v_us = float(np.median(verify_ms)) * 1e3
@@ -280,15 +351,19 @@ def main():
         "cost_ratio_c": round(c_ratio, 4),
         "theoretical_speedup_S": round(L / (1 + c_ratio), 3),
         "target_only_tokens_per_s": round(1e3 / ar_ms_per_tok, 2),
-        "roofline": {"bound": "hbm", "kernel": "k_gemv (thin-M MFMA weight streaming, all layer projections)",
-                     "achieved": round(gemv_gbs, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
-                     "frac": round(gemv_gbs / PEAK_HBM_GBS, 4), "traffic": None,
-                     "launches": n_g, "avg_launch_us": round(ms_g * 1e3 / max(n_g, 1), 2),
-                     "bytes_per_launch": round(by_g / max(n_g, 1))},
+        "kernels": kernels,
+        "roofline": {"bound": "hbm",
+                     "kernel": "k_gemv_p SWIGLU: fused gate/up projection + SwiGLU, 2x18944x3584 bf16 weights",
+                     "achieved": round(gu_gbs, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                     "frac": round(gu_gbs / PEAK_HBM_GBS, 4), "traffic": measured_traffic(),
+                     "launches": gu["launches"], "avg_launch_us": gu["avg_us"],
+                     "bytes_per_launch": gu["bytes_per_launch"]},
     }
     if not args.no_cpu_baseline:
         log("timing the oracle on a bounded sample ...")
         out["cpu_baseline"] = cpu_baseline(w, src, L, K)
+    if args.calibration_copy:
+        calibration_copy()
     print(json.dumps(out), flush=True)
 
 

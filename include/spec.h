@@ -207,17 +207,22 @@ spec_status spec_debug_kv(spec_ctx* ctx, int32_t b, int32_t model, int32_t layer
                           int32_t pos0, int32_t npos, void* host_out);
 
 /* Per-kernel timing with HIP events on the context's stream.  While enabled,
- * calls launch kernels one by one (no graph replay) and bracket each launch
- * with events.  spec_timing_read (synchronising) returns, for kernel class
+ * calls launch kernels one by one (no graph replay), each through
+ * hipExtLaunchKernelGGL with a start/stop event pair, and every pass begins
+ * with a bounded device-side wait (a few ms) so that the host has enqueued the
+ * whole pass before its first kernel runs.  spec_timing_read (synchronising) returns, for kernel class
  * `kind`, the number of launches, their summed duration in milliseconds and
  * the summed algorithmic bytes (weights and activations each launch must
  * move; 0 for kinds without a byte model) since timing was last enabled. */
 enum spec_kernel_kind {
-  SPEC_KERNEL_GEMV = 0,      /* weight-streaming projections of every layer */
-  SPEC_KERNEL_LMHEAD = 1,    /* tied LM head with the fused per-tile argmax */
-  SPEC_KERNEL_ATTN = 2,      /* split-KV attention */
-  SPEC_KERNEL_OTHER = 3,     /* norms, rotary + KV append, combine, accept, commit */
-  SPEC_KERNEL_KINDS = 4
+  SPEC_KERNEL_QKV = 0,       /* fused Q/K/V projection with rotary and KV append */
+  SPEC_KERNEL_O = 1,         /* attention output projection with the residual add */
+  SPEC_KERNEL_GATEUP = 2,    /* fused gate/up projection with SwiGLU */
+  SPEC_KERNEL_DOWN = 3,      /* down projection partial sums (split over the FFN width) */
+  SPEC_KERNEL_LMHEAD = 4,    /* tied LM head with the fused per-tile argmax */
+  SPEC_KERNEL_ATTN = 5,      /* split-KV attention */
+  SPEC_KERNEL_OTHER = 6,     /* embed, attention combine, down reduction, accept, commit */
+  SPEC_KERNEL_KINDS = 7
 };
 spec_status spec_timing(spec_ctx* ctx, int32_t enable);
 spec_status spec_timing_read(spec_ctx* ctx, int32_t kind, int64_t* launches, double* ms, double* bytes);

@@ -21,7 +21,7 @@ SPEC_MAX_BATCH = 16
 SPEC_FLAG_NO_GRAPHS = 1
 STATUS = {0: "SPEC_OK", 1: "SPEC_E_INVAL", 2: "SPEC_E_STATE", 3: "SPEC_E_CAPACITY", 5: "SPEC_E_HIP",
           6: "SPEC_E_NUMERIC"}
-KERNEL_KINDS = {"gemv": 0, "lmhead": 1, "attn": 2, "other": 3}
+KERNEL_KINDS = {"qkv": 0, "o": 1, "gateup": 2, "down": 3, "lmhead": 4, "attn": 5, "other": 6}
 
 
 class spec_dims(Structure):

@@ -128,6 +128,7 @@ struct Ctx {
 // Each returns hipSuccess or the launch error.
 
 hipError_t launch_zero(Ctx& c, void* p, size_t bytes);
+hipError_t launch_hold(Ctx& c, double ms);   // bounded device-side wait (timing mode)
 hipError_t launch_prefix_kv(Ctx& c, Model& m, int layer, int b, int prefix_len,
                             const bf16_t* k_pre, const bf16_t* v);
 hipError_t launch_stage_verify(Ctx& c, const int32_t* d_override, int want_logits);

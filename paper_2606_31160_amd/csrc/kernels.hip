@@ -10,6 +10,7 @@
 // proposals) lives in device memory (SeqState), so one captured graph serves
 // every round.
 #include <hip/hip_runtime.h>
+#include <hip/hip_ext.h>
 
 #include <algorithm>
 #include <cmath>
@@ -69,6 +70,15 @@ __device__ __forceinline__ void amax_merge(float& v, int& i, float v2, int i2) {
 // ---------------------------------------------------------------------------
 // utility
 // ---------------------------------------------------------------------------
+
+// One thread waits `ticks` of the constant-rate wall clock, then exits.  The
+// timing mode launches it ahead of a pass so that the host has enqueued the
+// whole pass before its first kernel starts: the kernels then run back to back
+// as in a graph replay instead of each starting on an idle device.
+__global__ void k_hold(long long ticks) {
+  const long long t0 = wall_clock64();
+  while (wall_clock64() - t0 < ticks) __builtin_amdgcn_s_sleep(16);
+}
 
 __global__ void k_zero(u32x4* p, size_t n) {
   size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
@@ -1047,12 +1057,12 @@ int down_splits(int M, int Kd, int ncu) {
 
 namespace {
 
+// Per-launch timing: when enabled, the launch inside the scope passes e0/e1 to
+// hipExtLaunchKernelGGL, which stamps them with the dispatch's own start and
+// end times (no marker packets between kernels).
 struct Timed {
-  Ctx& c;
-  int kind;
-  double bytes;
-  hipEvent_t e1 = nullptr;
-  Timed(Ctx& c_, int kind_, double bytes_) : c(c_), kind(kind_), bytes(bytes_) {
+  hipEvent_t e0 = nullptr, e1 = nullptr;
+  Timed(Ctx& c, int kind, double bytes) {
     if (!c.timing) return;
     if (c.ev_used + 2 > c.ev_pool.size()) {
       for (int i = 0; i < 256; ++i) {
@@ -1061,13 +1071,9 @@ struct Timed {
       }
     }
     if (c.ev_used + 2 > c.ev_pool.size()) return;
-    hipEvent_t e0 = c.ev_pool[c.ev_used++];
+    e0 = c.ev_pool[c.ev_used++];
     e1 = c.ev_pool[c.ev_used++];
-    (void)hipEventRecord(e0, c.stream);
     c.trec.push_back(TimingRec{kind, bytes, e0, e1});
-  }
-  ~Timed() {
-    if (e1) (void)hipEventRecord(e1, c.stream);
   }
 };
 
@@ -1090,10 +1096,10 @@ hipError_t gemv_launch(Ctx& c, const GemvArgs& g, int kind, double bytes) {
   const dim3 grid(groups, g.splits), block(kGemvWaves * 64);
   Timed t(c, kind, bytes);
   switch (mb) {
-    case 1: hipLaunchKernelGGL((k_gemv<1, kGemvWaves, kGemvSteps, TT, EPI>), grid, block, lds, S(c), g); break;
-    case 2: hipLaunchKernelGGL((k_gemv<2, kGemvWaves, kGemvSteps, TT, EPI>), grid, block, lds, S(c), g); break;
-    case 3: hipLaunchKernelGGL((k_gemv<3, kGemvWaves, kGemvSteps, TT, EPI>), grid, block, lds, S(c), g); break;
-    case 4: hipLaunchKernelGGL((k_gemv<4, kGemvWaves, kGemvSteps, TT, EPI>), grid, block, lds, S(c), g); break;
+    case 1: hipExtLaunchKernelGGL((k_gemv<1, kGemvWaves, kGemvSteps, TT, EPI>), grid, block, lds, S(c), t.e0, t.e1, 0, g); break;
+    case 2: hipExtLaunchKernelGGL((k_gemv<2, kGemvWaves, kGemvSteps, TT, EPI>), grid, block, lds, S(c), t.e0, t.e1, 0, g); break;
+    case 3: hipExtLaunchKernelGGL((k_gemv<3, kGemvWaves, kGemvSteps, TT, EPI>), grid, block, lds, S(c), t.e0, t.e1, 0, g); break;
+    case 4: hipExtLaunchKernelGGL((k_gemv<4, kGemvWaves, kGemvSteps, TT, EPI>), grid, block, lds, S(c), t.e0, t.e1, 0, g); break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();
@@ -1118,10 +1124,10 @@ hipError_t gemv_launch_p(Ctx& c, const GemvArgs& g, int workgroups, int kind, do
   const dim3 grid(workgroups), block(kGemvWaves * 64);
   Timed t(c, kind, bytes);
   switch (mb) {
-    case 1: hipLaunchKernelGGL((k_gemv_p<1, kGemvWaves, kGemvSteps, EPI>), grid, block, lds, S(c), g); break;
-    case 2: hipLaunchKernelGGL((k_gemv_p<2, kGemvWaves, kGemvSteps, EPI>), grid, block, lds, S(c), g); break;
-    case 3: hipLaunchKernelGGL((k_gemv_p<3, kGemvWaves, kGemvSteps, EPI>), grid, block, lds, S(c), g); break;
-    case 4: hipLaunchKernelGGL((k_gemv_p<4, kGemvWaves, kGemvSteps, EPI>), grid, block, lds, S(c), g); break;
+    case 1: hipExtLaunchKernelGGL((k_gemv_p<1, kGemvWaves, kGemvSteps, EPI>), grid, block, lds, S(c), t.e0, t.e1, 0, g); break;
+    case 2: hipExtLaunchKernelGGL((k_gemv_p<2, kGemvWaves, kGemvSteps, EPI>), grid, block, lds, S(c), t.e0, t.e1, 0, g); break;
+    case 3: hipExtLaunchKernelGGL((k_gemv_p<3, kGemvWaves, kGemvSteps, EPI>), grid, block, lds, S(c), t.e0, t.e1, 0, g); break;
+    case 4: hipExtLaunchKernelGGL((k_gemv_p<4, kGemvWaves, kGemvSteps, EPI>), grid, block, lds, S(c), t.e0, t.e1, 0, g); break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();
@@ -1181,7 +1187,7 @@ hipError_t run_layer(Ctx& c, Model& m, int li, const bf16_t* next_gain, bool sel
     g.nkv = nkv;
     g.D = D;
     g.cap = c.cap;
-    CK((gemv_launch<EPI_ROPE, 1>(c, g, SPEC_KERNEL_GEMV, gemv_bytes(g.N, H, M, 2.0))));
+    CK((gemv_launch<EPI_ROPE, 1>(c, g, SPEC_KERNEL_QKV, gemv_bytes(g.N, H, M, 2.0))));
   }
   // attention
   {
@@ -1193,14 +1199,14 @@ hipError_t run_layer(Ctx& c, Model& m, int li, const bf16_t* next_gain, bool sel
     {
       Timed t(c, SPEC_KERNEL_ATTN, 0);
       if (D == 128)
-        hipLaunchKernelGGL(k_attn<128>, grid, dim3(256), 0, S(c), p);
+        hipExtLaunchKernelGGL(k_attn<128>, grid, dim3(256), 0, S(c), t.e0, t.e1, 0, p);
       else
-        hipLaunchKernelGGL(k_attn<64>, grid, dim3(256), 0, S(c), p);
+        hipExtLaunchKernelGGL(k_attn<64>, grid, dim3(256), 0, S(c), t.e0, t.e1, 0, p);
       CK(hipGetLastError());
     }
     CombineArgs cb{c.st, c.op, c.mp, c.lp, c.o, nq, D, c.R, c.B, c.attn_chunk};
     Timed t2(c, SPEC_KERNEL_OTHER, 0);
-    hipLaunchKernelGGL(k_attn_combine, dim3(c.R, nq, c.B), dim3(128), (size_t)c.attn_splits * sizeof(float), S(c),
+    hipExtLaunchKernelGGL(k_attn_combine, dim3(c.R, nq, c.B), dim3(128), (size_t)c.attn_splits * sizeof(float), S(c), t2.e0, t2.e1, 0,
                        cb);
     CK(hipGetLastError());
   }
@@ -1217,7 +1223,7 @@ hipError_t run_layer(Ctx& c, Model& m, int li, const bf16_t* next_gain, bool sel
     g.gain = w.ffn_norm;
     g.xg = c.xg;
     g.ss_out = c.ss;
-    CK((gemv_launch<EPI_RESID, 1>(c, g, SPEC_KERNEL_GEMV, gemv_bytes(H, nq * D, M, 10.0))));
+    CK((gemv_launch<EPI_RESID, 1>(c, g, SPEC_KERNEL_O, gemv_bytes(H, nq * D, M, 10.0))));
   }
   // gate/up (+ 1/rms of the FFN norm) + SwiGLU
   {
@@ -1234,7 +1240,7 @@ hipError_t run_layer(Ctx& c, Model& m, int li, const bf16_t* next_gain, bool sel
     g.H = H;
     g.eps = d.rms_eps;
     g.u = c.u;
-    CK(gemv_launch_p<EPI_SWIGLU>(c, g, std::min(c.ncu, 2 * F / kTile), SPEC_KERNEL_GEMV, gemv_bytes(2 * F, H, M, 1.0)));
+    CK(gemv_launch_p<EPI_SWIGLU>(c, g, std::min(c.ncu, 2 * F / kTile), SPEC_KERNEL_GATEUP, gemv_bytes(2 * F, H, M, 1.0)));
   }
   // down projection (k-split partials) -> residual + the next norm's input
   {
@@ -1248,10 +1254,10 @@ hipError_t run_layer(Ctx& c, Model& m, int li, const bf16_t* next_gain, bool sel
     g.splits = m.s_down;
     g.out = c.part;
     const int per_split = std::max(1, std::min(c.ncu / m.s_down, H / kTile));
-    CK(gemv_launch_p<EPI_STORE>(c, g, per_split * m.s_down, SPEC_KERNEL_GEMV, gemv_bytes(H, F, M, 4.0 * m.s_down)));
+    CK(gemv_launch_p<EPI_STORE>(c, g, per_split * m.s_down, SPEC_KERNEL_DOWN, gemv_bytes(H, F, M, 4.0 * m.s_down)));
     FinishArgs p{c.st, c.part, m.s_down, M, c.R, H, c.Mpad, select_last ? 1 : 0, c.x, next_gain, c.xg, c.ss};
     Timed t(c, SPEC_KERNEL_OTHER, 0);
-    hipLaunchKernelGGL(k_down_finish, dim3((H + 255) / 256, M), dim3(256), 0, S(c), p);
+    hipExtLaunchKernelGGL(k_down_finish, dim3((H + 255) / 256, M), dim3(256), 0, S(c), t.e0, t.e1, 0, p);
     CK(hipGetLastError());
   }
   return hipSuccess;
@@ -1297,6 +1303,15 @@ void init_kernel_attributes() {
   set_lds_limit<EPI_ARGMAX, 1, 4>();
 }
 
+hipError_t launch_hold(Ctx& c, double ms) {
+  int khz = 0;
+  if (hipDeviceGetAttribute(&khz, hipDeviceAttributeWallClockRate, c.device) != hipSuccess || khz <= 0)
+    khz = 100000;
+  ms = std::min(std::max(ms, 0.0), 100.0);
+  hipLaunchKernelGGL(k_hold, dim3(1), dim3(1), 0, c.stream, (long long)(ms * khz));
+  return hipGetLastError();
+}
+
 hipError_t launch_zero(Ctx& c, void* p, size_t bytes) {
   const size_t n = bytes / 16;
   if (n == 0) return hipSuccess;
@@ -1330,7 +1345,7 @@ hipError_t launch_prefix_kv(Ctx& c, Model& m, int layer, int b, int prefix_len, 
 
 hipError_t launch_stage_verify(Ctx& c, const int32_t* d_override, int want_logits) {
   Timed t(c, SPEC_KERNEL_OTHER, 0);
-  hipLaunchKernelGGL(k_stage_verify, dim3(c.B), dim3(64), 0, c.stream, c.st, d_override, c.K, c.V, want_logits);
+  hipExtLaunchKernelGGL(k_stage_verify, dim3(c.B), dim3(64), 0, c.stream, t.e0, t.e1, 0, c.st, d_override, c.K, c.V, want_logits);
   return hipGetLastError();
 }
 
@@ -1343,7 +1358,7 @@ hipError_t launch_forward(Ctx& c, PassMode mode) {
                 c.pos3,  c.cs,   m.axis,       d.hidden,         c.R, c.cap,    (int)mode, c.Mpad,
                 d.head_dim, m.flat ? 1 : 0};
     Timed t(c, SPEC_KERNEL_OTHER, 0);
-    hipLaunchKernelGGL(k_embed, dim3(c.R, c.B), dim3(1024), (size_t)d.hidden * sizeof(float), c.stream, p);
+    hipExtLaunchKernelGGL(k_embed, dim3(c.R, c.B), dim3(1024), (size_t)d.hidden * sizeof(float), c.stream, t.e0, t.e1, 0, p);
     CK(hipGetLastError());
   }
   const bool draft = mode == PASS_DRAFT;
@@ -1374,7 +1389,7 @@ hipError_t launch_forward(Ctx& c, PassMode mode) {
   const int ntiles = c.V / kTile;
   Timed t(c, SPEC_KERNEL_OTHER, 0);
   AmaxArgs p{c.st, c.amax_v, c.amax_i, ntiles, c.Mpad, draft ? 1 : c.R, draft ? 1 : 0};
-  hipLaunchKernelGGL(k_argmax_rows, dim3(draft ? 1 : c.R, c.B), dim3(1024), 0, c.stream, p);
+  hipExtLaunchKernelGGL(k_argmax_rows, dim3(draft ? 1 : c.R, c.B), dim3(1024), 0, c.stream, t.e0, t.e1, 0, p);
   return hipGetLastError();
 }
 
@@ -1386,7 +1401,7 @@ hipError_t launch_draft_out(Ctx& c, int32_t* d_tokens) {
 
 hipError_t launch_commit(Ctx& c, int32_t* acc, int32_t* committed, int32_t* ncommit, int32_t* fin) {
   Timed t(c, SPEC_KERNEL_OTHER, 0);
-  hipLaunchKernelGGL(k_commit, dim3(c.B), dim3(1), 0, c.stream, c.st, c.hist, c.cap, c.K, c.cfg.stop_token,
+  hipExtLaunchKernelGGL(k_commit, dim3(c.B), dim3(1), 0, c.stream, t.e0, t.e1, 0, c.st, c.hist, c.cap, c.K, c.cfg.stop_token,
                      c.cfg.max_new_tokens, acc, committed, ncommit, fin);
   return hipGetLastError();
 }

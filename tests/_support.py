@@ -33,6 +33,16 @@ def host_kv(w: W.Workload, b: int, model: str):
     return lambda li: (W.prefix_kv_host(w, b, model, li, "k"), W.prefix_kv_host(w, b, model, li, "v"))
 
 
+def device_kv(w: W.Workload, b: int, model: str):
+    """Prefix K/V drawn on the GPU by the device generator, read back as bf16 bits."""
+    import torch
+
+    def bits(t):
+        return t.view(torch.int16).cpu().numpy().view(np.uint16)
+    return lambda li: (bits(W.prefix_kv_device(w, b, model, li, "k")),
+                       bits(W.prefix_kv_device(w, b, model, li, "v")))
+
+
 def oracle_sequence(w: W.Workload, b: int, T, D, kv=None, capacity=None, pending=None,
                     with_draft: bool = True):
     lay = w.seqs[b]

@@ -315,3 +315,31 @@ def test_block_of_16_with_two_row_blocks(c1):
     toks = [seq.pending] + out[:-1]
     z = T.forward(toks, list(range(P, P + len(toks))), seq.tc)
     S.check_argmax_rows(out, z)
+
+
+def test_interleaved_axis_assignment_rotation():
+    """Interleaved M-RoPE (pair d reads axis d mod 3, Eq. axis-assign) on a
+    prompt with a 3x5x4 vision grid: rotated prompt keys, one verify's logits
+    and the new key rows against the oracle."""
+    base = W.get("C1")
+    w = base.with_(target=dataclasses.replace(base.target, interleaved=True),
+                   seqs=(LAYOUTS["interleaved"],), draft=None)
+    hp = W.HostWeights(w)
+    T, _ = S.oracle_decoders(w, hp)
+    s = _session(w, with_draft=False)
+    seq = S.oracle_sequence(w, 0, T, None, with_draft=False)
+    P = w.seqs[0].prefix_len
+    for li in range(w.target.layers):
+        k = ON.decode(s.kv(0, 0, li, 0, 0, P))
+        assert S.normwise_err(k, seq.tc.k[li][:P]) <= 1e-2, li
+    drafts = np.random.default_rng(3).integers(0, w.vocab, size=w.K).astype(np.int32)
+    s.verify(drafts[None, :], logits=True)
+    s.commit()
+    ref = seq.verify(drafts)
+    gl = s.logits[0].float().cpu().numpy()
+    for j in range(w.K + 1):
+        assert S.normwise_err(gl[j], ref.logits[j]) <= S.LOGIT_RTOL, j
+    for li in range(w.target.layers):
+        k = ON.decode(s.kv(0, 0, li, 0, P, w.K + 1))
+        assert S.normwise_err(k, seq.tc.k[li][P:P + w.K + 1]) <= S.LOGIT_RTOL
+    s.close()
