@@ -72,7 +72,11 @@ typedef struct spec_dims {
   float rms_eps;             /* RMSNorm epsilon */
 } spec_dims;
 
-#define SPEC_FLAG_NO_GRAPHS 1  /* launch kernels one by one instead of replaying HIP graphs */
+#define SPEC_FLAG_NO_GRAPHS 1      /* launch kernels one by one instead of replaying HIP graphs */
+#define SPEC_FLAG_PERSISTENT 2     /* run all layers of a pass in the persistent pass kernel when the
+                                      shapes allow it (else one kernel per layer step) */
+#define SPEC_FLAG_PASS_TIMELINE 4  /* the persistent pass kernel records per-phase wall-clock stamps
+                                      (see spec_debug_pass_timeline); adds a small cost */
 
 typedef struct spec_config {
   spec_dims target;          /* deliberative reasoner (3D M-RoPE) */
@@ -206,6 +210,16 @@ spec_status spec_debug_state(spec_ctx* ctx, int32_t b, int32_t* host_out);
 spec_status spec_debug_kv(spec_ctx* ctx, int32_t b, int32_t model, int32_t layer, int32_t which,
                           int32_t pos0, int32_t npos, void* host_out);
 
+/* Wall-clock stamps of the most recent persistent pass (context created with
+ * SPEC_FLAG_PASS_TIMELINE; synchronising).  host_out receives
+ * [events][workgroups] unsigned 64-bit ticks of the device's constant-rate
+ * clock (*tick_hz per second); events = 1 + 12 * layers of the pass's model:
+ * the start, then for each layer and phase (QKV, attention, combine, O,
+ * gate/up, down) the workgroup's work done and its next barrier passed.
+ * *n_events and *n_workgroups describe the layout; capacity is in elements. */
+spec_status spec_debug_pass_timeline(spec_ctx* ctx, int32_t model, unsigned long long* host_out, int64_t capacity,
+                                     int32_t* n_events, int32_t* n_workgroups, double* tick_hz);
+
 /* Per-kernel timing with HIP events on the context's stream.  While enabled,
  * calls launch kernels one by one (no graph replay), each through
  * hipExtLaunchKernelGGL with a start/stop event pair, and every pass begins
@@ -213,7 +227,8 @@ spec_status spec_debug_kv(spec_ctx* ctx, int32_t b, int32_t model, int32_t layer
  * whole pass before its first kernel runs.  spec_timing_read (synchronising) returns, for kernel class
  * `kind`, the number of launches, their summed duration in milliseconds and
  * the summed algorithmic bytes (weights and activations each launch must
- * move; 0 for kinds without a byte model) since timing was last enabled. */
+ * move, cached keys and values excluded; 0 for kinds without a byte model)
+ * since timing was last enabled. */
 enum spec_kernel_kind {
   SPEC_KERNEL_QKV = 0,       /* fused Q/K/V projection with rotary and KV append */
   SPEC_KERNEL_O = 1,         /* attention output projection with the residual add */
@@ -222,7 +237,9 @@ enum spec_kernel_kind {
   SPEC_KERNEL_LMHEAD = 4,    /* tied LM head with the fused per-tile argmax */
   SPEC_KERNEL_ATTN = 5,      /* split-KV attention */
   SPEC_KERNEL_OTHER = 6,     /* embed, attention combine, down reduction, accept, commit */
-  SPEC_KERNEL_KINDS = 7
+  SPEC_KERNEL_PASS_TARGET = 7, /* persistent kernel running every layer of a verify pass */
+  SPEC_KERNEL_PASS_DRAFT = 8,  /* persistent kernel running every layer of a draft step */
+  SPEC_KERNEL_KINDS = 9
 };
 spec_status spec_timing(spec_ctx* ctx, int32_t enable);
 spec_status spec_timing_read(spec_ctx* ctx, int32_t kind, int64_t* launches, double* ms, double* bytes);

@@ -13,10 +13,14 @@
 namespace specdec {
 
 typedef uint16_t bf16_t;
+struct PassArgs;
+struct GemvJob;
 
 constexpr int kMaxRows = SPEC_MAX_K + 1;     // rows per sequence in one pass
 constexpr int kTile = 16;                    // output rows per GEMV tile (one MFMA block)
 constexpr int kKeyBlock = 32;                // keys per attention inner step
+constexpr int kAttnChunk = 64;               // keys per attention workgroup (split-KV chunk)
+constexpr int kMaxAttnChunk = 128;
 constexpr int kGemvWaves = 16;               // waves per GEMV workgroup
 constexpr int kGemvSteps = 8;                // max 32-wide k-steps per GEMV wave
 
@@ -45,7 +49,7 @@ struct SeqState {
   int32_t props[kMaxRows];      // the draft's own proposals this round
 };
 
-enum { ERR_TOKEN = 1, ERR_NUMERIC = 2, ERR_STATE = 4 };
+enum { ERR_TOKEN = 1, ERR_NUMERIC = 2, ERR_STATE = 4, ERR_SYNC = 8 };
 
 enum PassMode { PASS_VERIFY = 0, PASS_DRAFT = 1 };
 
@@ -62,6 +66,10 @@ struct Model {
   bf16_t* vt = nullptr;             // [layers][B][kv_heads][head_dim][cap], values transposed
   int8_t* axis = nullptr;           // [head_dim/2] axis (0 T, 1 H, 2 W) of each rotary pair
   int s_down = 1;                  // k-splits of the down projection
+  int pass_splits = 1;             // k-splits of the down projection in the persistent pass
+  LayerW* lw_dev = nullptr;        // [layers] device copy of L (persistent pass)
+  PassArgs* pass_args_dev = nullptr;   // device copy of this model's pass arguments
+  GemvJob* jobs_dev = nullptr;         // [layers][kPassJobs] GEMV phases of the pass
   size_t kv_layer = 0;              // elements of one layer's key (or value) cache
 };
 
@@ -105,6 +113,16 @@ struct Ctx {
   Model tgt, drf;
   bool has_draft = false;
 
+  // persistent pass (pass.hip): per-layer activations, barrier words
+  bool use_pass = false;
+  size_t pass_lds = 0;
+  int pass_layers = 0;              // max layers over the models
+  bf16_t *p_xa = nullptr, *p_xf = nullptr, *p_q = nullptr, *p_o = nullptr, *p_u = nullptr;
+  float *p_ssa = nullptr, *p_ssf = nullptr, *p_part = nullptr;
+  unsigned *p_tile_cnt = nullptr, *p_bar = nullptr;
+  size_t p_x_layer = 0, p_ss_layer = 0, p_q_layer = 0, p_u_layer = 0;
+  unsigned long long* p_timeline = nullptr;   // SPEC_FLAG_PASS_TIMELINE
+
   // host state machine
   enum Phase { READY = 0, DRAFTING = 1, VERIFIED = 2 } phase = READY;
   int dsteps = 0;
@@ -128,6 +146,8 @@ struct Ctx {
 // Each returns hipSuccess or the launch error.
 
 hipError_t launch_zero(Ctx& c, void* p, size_t bytes);
+// Uploads the persistent pass's arguments and GEMV jobs of one model (init).
+hipError_t upload_pass_tables(Ctx& c, Model& m, bool draft);
 hipError_t launch_hold(Ctx& c, double ms);   // bounded device-side wait (timing mode)
 hipError_t launch_prefix_kv(Ctx& c, Model& m, int layer, int b, int prefix_len,
                             const bf16_t* k_pre, const bf16_t* v);

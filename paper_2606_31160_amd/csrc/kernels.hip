@@ -13,59 +13,14 @@
 #include <hip/hip_ext.h>
 
 #include <algorithm>
+#include <vector>
 #include <cmath>
 
 #include "ctx.h"
+#include "device.h"
+#include "pass.h"
 
 namespace specdec {
-
-typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
-typedef float f32x4 __attribute__((ext_vector_type(4)));
-typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
-typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
-
-constexpr float kLog2e = 1.4426950408889634f;
-
-__device__ __forceinline__ float bf2f(bf16_t h) { return __uint_as_float(((uint32_t)h) << 16); }
-
-// float -> bfloat16, round to nearest even; NaN stays NaN.
-__device__ __forceinline__ uint32_t f2bf_bits(float f) {
-  uint32_t u = __float_as_uint(f);
-  if ((u & 0x7fffffffu) > 0x7f800000u) return (u >> 16) | 0x40u;
-  u += 0x7fffu + ((u >> 16) & 1u);
-  return u >> 16;
-}
-__device__ __forceinline__ bf16_t f2bf(float f) { return (bf16_t)f2bf_bits(f); }
-__device__ __forceinline__ uint32_t pack2(float lo, float hi) { return f2bf_bits(lo) | (f2bf_bits(hi) << 16); }
-
-__device__ __forceinline__ u32x4 ld16(const bf16_t* p) { return *reinterpret_cast<const u32x4*>(p); }
-__device__ __forceinline__ u32x2 ld8(const bf16_t* p) { return *reinterpret_cast<const u32x2*>(p); }
-
-__device__ __forceinline__ f32x4 mfma16x16x32(u32x4 a, u32x4 b, f32x4 c) {
-  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, a), __builtin_bit_cast(bf16x8, b), c,
-                                                 0, 0, 0);
-}
-
-// Block-wide sum of one float per thread (blockDim.x a multiple of 64, <= 1024),
-// in a fixed order.
-__device__ float block_sum(float v, float* sh) {
-  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
-  const int w = threadIdx.x >> 6, l = threadIdx.x & 63, nw = blockDim.x >> 6;
-  if (l == 0) sh[w] = v;
-  __syncthreads();
-  float t = 0.f;
-  for (int i = 0; i < nw; ++i) t += sh[i];
-  __syncthreads();
-  return t;
-}
-
-// Argmax pair reduction: larger value wins, equal values go to the lower index.
-__device__ __forceinline__ void amax_merge(float& v, int& i, float v2, int i2) {
-  if (v2 > v || (v2 == v && i2 < i)) {
-    v = v2;
-    i = i2;
-  }
-}
 
 // ---------------------------------------------------------------------------
 // utility
@@ -731,6 +686,7 @@ struct AttnArgs {
 
 template <int D>
 __global__ __launch_bounds__(256) void k_attn(AttnArgs a) {
+  extern __shared__ __align__(16) unsigned char lds[];
   const int split = blockIdx.x;
   const int kvh = blockIdx.y / a.row_blocks, rb = blockIdx.y % a.row_blocks;
   const int b = blockIdx.z;
@@ -740,7 +696,6 @@ __global__ __launch_bounds__(256) void k_attn(AttnArgs a) {
   const int count = s.count, base = s.base;
   const int rows = count * a.G;
   const int wrow0 = rb * 64 + wave * 16;
-  if (wrow0 >= rows) return;                        // wave-uniform
   const int qr = wrow0 + (lane & 15);
   const bool rvalid = qr < rows;
   const int j = rvalid ? qr / a.G : 0;
@@ -751,7 +706,8 @@ __global__ __launch_bounds__(256) void k_attn(AttnArgs a) {
   const int vis_end = base + j + 1;
   const size_t oi = (((size_t)split * a.B + b) * a.nq + hq) * a.R + j;
 
-  if (k0 >= k1) {                                   // no keys in this split
+  if (k0 >= k1) {                                   // no keys in this split (workgroup-uniform)
+    if (wrow0 >= rows) return;
     if (rvalid && g4 == 0) {
       a.mp[oi] = -INFINITY;
       a.lp[oi] = 0.f;
@@ -763,48 +719,76 @@ __global__ __launch_bounds__(256) void k_attn(AttnArgs a) {
     return;
   }
 
+  // This wave's query rows; issued first so their latency overlaps the staging.
   u32x4 qf[D / 32];
   {
     const bf16_t* qp = a.q + ((size_t)(b * a.R + j) * a.nq + hq) * D + 8 * g4;
 #pragma unroll
-    for (int t = 0; t < D / 32; ++t) qf[t] = rvalid ? ld16(qp + 32 * t) : u32x4{0, 0, 0, 0};
+    for (int t = 0; t < D / 32; ++t) qf[t] = (rvalid && wrow0 < rows) ? ld16(qp + 32 * t) : u32x4{0, 0, 0, 0};
   }
-  const bf16_t* Kb = a.kc + ((size_t)b * a.nkv + kvh) * a.cap * D;
-  const bf16_t* Vb = a.vt + ((size_t)b * a.nkv + kvh) * D * a.cap;
+
+  // Stage the chunk once for all waves: keys [chunk][D + 8] and values
+  // transposed [D][chunk + 8] (the pads spread rows over the LDS banks).
+  // Keys at or past k1 are stored as zeros.  Every load of the thread is
+  // issued before the first LDS store so that their latencies overlap.
+  const int kst = D + 8, vst = a.chunk + 8;
+  bf16_t* Ks = reinterpret_cast<bf16_t*>(lds);
+  bf16_t* Vs = Ks + (size_t)a.chunk * kst;
+  {
+    constexpr int PER_T = kMaxAttnChunk * D / 8 / 256;   // 16-byte vectors per thread and operand
+    const bf16_t* Kb = a.kc + ((size_t)b * a.nkv + kvh) * a.cap * D;
+    const bf16_t* Vb = a.vt + ((size_t)b * a.nkv + kvh) * D * a.cap;
+    const int nvec = a.chunk * (D / 8);                   // per operand
+    const int per_row = a.chunk / 8;
+    u32x4 kr[PER_T], vr[PER_T];
+#pragma unroll
+    for (int u = 0; u < PER_T; ++u) {
+      const int i = threadIdx.x + 256 * u;
+      const int key = i / (D / 8), c8 = i % (D / 8);
+      kr[u] = (i < nvec && k0 + key < k1) ? ld16(Kb + (size_t)(k0 + key) * D + 8 * c8) : u32x4{0, 0, 0, 0};
+      const int d = i / per_row, v8 = i % per_row;
+      const int slot = k0 + 8 * v8;
+      vr[u] = (i < nvec && slot < k1) ? ld16(Vb + (size_t)d * a.cap + slot) : u32x4{0, 0, 0, 0};
+    }
+#pragma unroll
+    for (int u = 0; u < PER_T; ++u) {
+      const int i = threadIdx.x + 256 * u;
+      if (i >= nvec) break;
+      const int key = i / (D / 8), c8 = i % (D / 8);
+      *reinterpret_cast<u32x4*>(Ks + (size_t)key * kst + 8 * c8) = kr[u];
+      const int d = i / per_row, v8 = i % per_row;
+      const int slot = k0 + 8 * v8;
+      u32x4 v = vr[u];
+      if (slot < k1 && slot + 8 > k1) {             // ragged end of the valid keys
+        uint32_t w[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+        for (int e = 0; e < 8; ++e)
+          if (slot + e >= k1) w[e >> 1] &= (e & 1) ? 0x0000FFFFu : 0xFFFF0000u;
+        v = u32x4{w[0], w[1], w[2], w[3]};
+      }
+      *reinterpret_cast<u32x4*>(Vs + (size_t)d * vst + 8 * v8) = v;
+    }
+  }
+  __syncthreads();
+  if (wrow0 >= rows) return;                        // wave-uniform; no barrier follows
 
   float m_run = -INFINITY, l_run = 0.f;
   f32x4 o[D / 16];
 #pragma unroll
   for (int dt = 0; dt < D / 16; ++dt) o[dt] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-  // Fragments of one 32-key block: the K tiles (A operands of S^T = K Q^T) and
-  // the V^T tiles (A operands of O^T = V^T P^T).  Two statically named buffers:
-  // the next block's loads are issued before the current block is computed.
-  struct Frag {
-    u32x4 k[2][D / 32];
-    u32x4 v[D / 16];
-  };
-  auto load_block = [&](int kb, Frag& f) {
-#pragma unroll
-    for (int h2 = 0; h2 < 2; ++h2) {
-      const bf16_t* kp = Kb + (size_t)(kb + 16 * h2 + (lane & 15)) * D + 8 * g4;
-#pragma unroll
-      for (int t = 0; t < D / 32; ++t) f.k[h2][t] = ld16(kp + 32 * t);
-    }
-#pragma unroll
-    for (int dt = 0; dt < D / 16; ++dt) {
-      const bf16_t* vp = Vb + (size_t)(16 * dt + (lane & 15)) * a.cap + kb + 4 * g4;
-      const u32x2 lo = ld8(vp), hi = ld8(vp + 16);
-      f.v[dt] = u32x4{lo.x, lo.y, hi.x, hi.y};
-    }
-  };
-  auto compute_block = [&](int kb, const Frag& f) {
+  // One 32-key block: S^T = K Q^T (lanes own query rows), online softmax in
+  // log2 units, then O^T += V^T P^T.  The key order inside the block is the
+  // same permutation on the P^T and V^T operands, so the contraction is exact.
+  for (int kb = 0; kb < k1 - k0; kb += kKeyBlock) {
     f32x4 sc[2];
 #pragma unroll
     for (int h2 = 0; h2 < 2; ++h2) {
+      const bf16_t* kp = Ks + (size_t)(kb + 16 * h2 + (lane & 15)) * kst + 8 * g4;
       f32x4 acc = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-      for (int t = 0; t < D / 32; ++t) acc = mfma16x16x32(f.k[h2][t], qf[t], acc);
+      for (int t = 0; t < D / 32; ++t)
+        acc = mfma16x16x32(*reinterpret_cast<const u32x4*>(kp + 32 * t), qf[t], acc);
       sc[h2] = acc;
     }
     float p[8];
@@ -813,7 +797,7 @@ __global__ __launch_bounds__(256) void k_attn(AttnArgs a) {
     for (int h2 = 0; h2 < 2; ++h2)
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
-        const int key = kb + 16 * h2 + 4 * g4 + i;
+        const int key = k0 + kb + 16 * h2 + 4 * g4 + i;
         const bool ok = rvalid && key < k1 && key < vis_end;
         const float v = ok ? sc[h2][i] * a.scale_log2 : -INFINITY;
         p[h2 * 4 + i] = v;
@@ -831,21 +815,13 @@ __global__ __launch_bounds__(256) void k_attn(AttnArgs a) {
     }
     l_run = l_run * alpha + ps;
     m_run = m_new;
-#pragma unroll
-    for (int dt = 0; dt < D / 16; ++dt) o[dt] *= alpha;
     const u32x4 pb = u32x4{pack2(p[0], p[1]), pack2(p[2], p[3]), pack2(p[4], p[5]), pack2(p[6], p[7])};
 #pragma unroll
-    for (int dt = 0; dt < D / 16; ++dt) o[dt] = mfma16x16x32(f.v[dt], pb, o[dt]);
-  };
-  Frag fa, fb;
-  load_block(k0, fa);
-  for (int kb = k0; kb < k1; kb += 2 * kKeyBlock) {
-    const bool has_b = kb + kKeyBlock < k1;
-    if (has_b) load_block(kb + kKeyBlock, fb);
-    compute_block(kb, fa);
-    if (!has_b) break;
-    if (kb + 2 * kKeyBlock < k1) load_block(kb + 2 * kKeyBlock, fa);
-    compute_block(kb + kKeyBlock, fb);
+    for (int dt = 0; dt < D / 16; ++dt) {
+      const bf16_t* vp = Vs + (size_t)(16 * dt + (lane & 15)) * vst + kb + 4 * g4;
+      const u32x2 lo = *reinterpret_cast<const u32x2*>(vp), hi = *reinterpret_cast<const u32x2*>(vp + 16);
+      o[dt] = mfma16x16x32(u32x4{lo.x, lo.y, hi.x, hi.y}, pb, o[dt] * alpha);
+    }
   }
   l_run += __shfl_xor(l_run, 16);
   l_run += __shfl_xor(l_run, 32);
@@ -860,8 +836,12 @@ __global__ __launch_bounds__(256) void k_attn(AttnArgs a) {
   }
 }
 
+size_t attn_lds_bytes(int chunk, int D) {
+  return ((size_t)chunk * (D + 8) + (size_t)D * (chunk + 8)) * sizeof(bf16_t);
+}
+
 // Merge the splits of each (row, q head): o = sum_s 2^(m_s - M) O_s / sum_s
-// 2^(m_s - M) l_s.  grid (R, q_heads, B), one thread per head dimension.
+// 2^(m_s - M) l_s.  grid (R, q_heads, B), 256 threads: 8 groups of splits x 32 groups of 4 columns.
 struct CombineArgs {
   const SeqState* st;
   const float *op, *mp, *lp;
@@ -869,8 +849,8 @@ struct CombineArgs {
   int nq, D, R, B, chunk;
 };
 
-__global__ __launch_bounds__(128) void k_attn_combine(CombineArgs a) {
-  extern __shared__ float coef[];   // [ns]
+__global__ __launch_bounds__(256) void k_attn_combine(CombineArgs a) {
+  extern __shared__ float coef[];   // [ns] weights, then [8][D] partial sums
   const int j = blockIdx.x, h = blockIdx.y, b = blockIdx.z;
   const SeqState& s = a.st[b];
   if (j >= s.count) return;
@@ -894,14 +874,24 @@ __global__ __launch_bounds__(128) void k_attn_combine(CombineArgs a) {
     for (int sp = l; sp < ns; sp += 64) coef[sp] *= inv;
   }
   __syncthreads();
+  // thread = (split group sg of 8, 4-wide column group c4); D / 4 <= 32 groups
+  float* part = coef + ((ns + 3) & ~3);
+  const int c4 = threadIdx.x & 31, sg = threadIdx.x >> 5;
+  f32x4 v = f32x4{0.f, 0.f, 0.f, 0.f};
+  if (4 * c4 < a.D) {
+    const float* src = a.op + row * a.D + 4 * c4;
+    const size_t ostride = sstride * a.D;
+#pragma unroll 4
+    for (int sp = sg; sp < ns; sp += 8) v += coef[sp] * *reinterpret_cast<const f32x4*>(src + sp * ostride);
+    *reinterpret_cast<f32x4*>(part + sg * a.D + 4 * c4) = v;
+  }
+  __syncthreads();
   const int d = threadIdx.x;
   if (d < a.D) {
-    float v = 0.f;
-    const float* src = a.op + row * a.D + d;
-    const size_t ostride = sstride * a.D;
-#pragma unroll 8
-    for (int sp = 0; sp < ns; ++sp) v += coef[sp] * src[sp * ostride];
-    a.o[(size_t)(b * a.R + j) * a.nq * a.D + h * a.D + d] = f2bf(v);
+    float t = 0.f;
+#pragma unroll
+    for (int g = 0; g < 8; ++g) t += part[g * a.D + d];
+    a.o[(size_t)(b * a.R + j) * a.nq * a.D + h * a.D + d] = f2bf(t);
   }
 }
 
@@ -1199,14 +1189,15 @@ hipError_t run_layer(Ctx& c, Model& m, int li, const bf16_t* next_gain, bool sel
     {
       Timed t(c, SPEC_KERNEL_ATTN, 0);
       if (D == 128)
-        hipExtLaunchKernelGGL(k_attn<128>, grid, dim3(256), 0, S(c), t.e0, t.e1, 0, p);
+        hipExtLaunchKernelGGL(k_attn<128>, grid, dim3(256), attn_lds_bytes(c.attn_chunk, D), S(c), t.e0, t.e1, 0, p);
       else
-        hipExtLaunchKernelGGL(k_attn<64>, grid, dim3(256), 0, S(c), t.e0, t.e1, 0, p);
+        hipExtLaunchKernelGGL(k_attn<64>, grid, dim3(256), attn_lds_bytes(c.attn_chunk, D), S(c), t.e0, t.e1, 0, p);
       CK(hipGetLastError());
     }
     CombineArgs cb{c.st, c.op, c.mp, c.lp, c.o, nq, D, c.R, c.B, c.attn_chunk};
     Timed t2(c, SPEC_KERNEL_OTHER, 0);
-    hipExtLaunchKernelGGL(k_attn_combine, dim3(c.R, nq, c.B), dim3(128), (size_t)c.attn_splits * sizeof(float), S(c), t2.e0, t2.e1, 0,
+    hipExtLaunchKernelGGL(k_attn_combine, dim3(c.R, nq, c.B), dim3(256),
+                          (size_t)(((c.attn_splits + 3) & ~3) + 8 * D) * sizeof(float), S(c), t2.e0, t2.e1, 0,
                        cb);
     CK(hipGetLastError());
   }
@@ -1269,6 +1260,11 @@ void init_kernel_attributes() {
   static bool done = false;
   if (done) return;
   done = true;
+  pass_set_attributes(gemv_lds_limit());
+  (void)hipFuncSetAttribute(reinterpret_cast<const void*>(&k_attn<128>), hipFuncAttributeMaxDynamicSharedMemorySize,
+                            (int)attn_lds_bytes(kMaxAttnChunk, 128));
+  (void)hipFuncSetAttribute(reinterpret_cast<const void*>(&k_attn<64>), hipFuncAttributeMaxDynamicSharedMemorySize,
+                            (int)attn_lds_bytes(kMaxAttnChunk, 64));
   set_lds_limit_p<EPI_STORE, 1>();
   set_lds_limit_p<EPI_STORE, 2>();
   set_lds_limit_p<EPI_STORE, 3>();
@@ -1312,6 +1308,20 @@ hipError_t launch_hold(Ctx& c, double ms) {
   return hipGetLastError();
 }
 
+PassArgs pass_args(Ctx& c, Model& m, bool draft);
+
+hipError_t upload_pass_tables(Ctx& c, Model& m, bool draft) {
+  const PassArgs a = pass_args(c, m, draft);
+  std::vector<GemvJob> jobs((size_t)m.d.layers * kPassJobs);
+  pass_build_jobs(a, m.L.data(), m.final_norm, jobs.data());
+  hipError_t e = hipMemcpyAsync(m.pass_args_dev, &a, sizeof a, hipMemcpyHostToDevice, c.stream);
+  if (e == hipSuccess)
+    e = hipMemcpyAsync(m.jobs_dev, jobs.data(), jobs.size() * sizeof(GemvJob), hipMemcpyHostToDevice, c.stream);
+  // the host copies are local: wait for the uploads before they go away
+  if (e == hipSuccess) e = hipStreamSynchronize(c.stream);
+  return e;
+}
+
 hipError_t launch_zero(Ctx& c, void* p, size_t bytes) {
   const size_t n = bytes / 16;
   if (n == 0) return hipSuccess;
@@ -1349,12 +1359,79 @@ hipError_t launch_stage_verify(Ctx& c, const int32_t* d_override, int want_logit
   return hipGetLastError();
 }
 
+// Arguments of the persistent pass for one model.
+PassArgs pass_args(Ctx& c, Model& m, bool draft) {
+  const spec_dims& d = m.d;
+  PassArgs a{};
+  a.st = c.st;
+  a.layers = d.layers;
+  a.H = d.hidden;
+  a.nq = d.q_heads;
+  a.nkv = d.kv_heads;
+  a.D = d.head_dim;
+  a.F = d.ffn;
+  a.M = c.M;
+  a.R = c.R;
+  a.B = c.B;
+  a.rps = c.R;
+  a.mpad = c.Mpad;
+  a.cap = c.cap;
+  a.eps = d.rms_eps;
+  a.scale_log2 = kLog2e / sqrtf((float)d.head_dim);
+  a.lw = m.lw_dev;
+  a.jobs = m.jobs_dev;
+  a.final_norm = m.final_norm;
+  a.select_last = draft ? 1 : 0;
+  a.kc = m.kc;
+  a.vt = m.vt;
+  a.kv_layer = m.kv_layer;
+  a.rcs = c.rcs;
+  a.x = c.x;
+  a.xa = c.p_xa;
+  a.xf = c.p_xf;
+  a.ssa = c.p_ssa;
+  a.ssf = c.p_ssf;
+  a.q = c.p_q;
+  a.o = c.p_o;
+  a.u = c.p_u;
+  a.x_layer = c.p_x_layer;
+  a.ss_layer = c.p_ss_layer;
+  a.q_layer = c.p_q_layer;
+  a.u_layer = c.p_u_layer;
+  a.xg_final = c.xg;
+  a.ss_final = c.ss;
+  a.op = c.op;
+  a.mp = c.mp;
+  a.lp = c.lp;
+  a.attn_chunk = c.attn_chunk;
+  a.attn_splits = c.attn_splits;
+  a.down_splits = m.pass_splits;
+  a.part = c.p_part;
+  a.tile_cnt = c.p_tile_cnt;
+  a.bar = c.p_bar;
+  a.timeline = c.p_timeline;
+  return a;
+}
+
+// Every layer of a pass in the persistent kernel (pass.hip).
+hipError_t run_layers_persistent(Ctx& c, Model& m, bool draft) {
+  const spec_dims& d = m.d;
+  const int H = d.hidden, D = d.head_dim, nq = d.q_heads, nkv = d.kv_heads, F = d.ffn;
+  const double per_layer = gemv_bytes((nq + 2 * nkv) * D, H, c.M, 2.0) + gemv_bytes(H, nq * D, c.M, 10.0) +
+                           gemv_bytes(2 * F, H, c.M, 1.0) + gemv_bytes(H, F, c.M, 4.0 * m.pass_splits);
+  Timed t(c, draft ? SPEC_KERNEL_PASS_DRAFT : SPEC_KERNEL_PASS_TARGET, per_layer * d.layers);
+  return pass_launch(m.pass_args_dev, d.head_dim, draft, c.ncu, c.pass_lds, S(c), t.e0, t.e1);
+}
+
 hipError_t launch_forward(Ctx& c, PassMode mode) {
   Model& m = mode == PASS_VERIFY ? c.tgt : c.drf;
   const spec_dims& d = m.d;
   const int M = c.M;
+  const bool persistent = c.use_pass;
   {
-    EmbedArgs p{c.st,    c.hist, c.embed,      m.L[0].attn_norm, c.x, c.xg,     c.ss,  c.rcs,
+    // the persistent pass reads layer 0's norm input from its per-layer buffers
+    EmbedArgs p{c.st,    c.hist, c.embed,      m.L[0].attn_norm, c.x, persistent ? c.p_xa : c.xg,
+                persistent ? c.p_ssa : c.ss,  c.rcs,
                 c.pos3,  c.cs,   m.axis,       d.hidden,         c.R, c.cap,    (int)mode, c.Mpad,
                 d.head_dim, m.flat ? 1 : 0};
     Timed t(c, SPEC_KERNEL_OTHER, 0);
@@ -1362,9 +1439,13 @@ hipError_t launch_forward(Ctx& c, PassMode mode) {
     CK(hipGetLastError());
   }
   const bool draft = mode == PASS_DRAFT;
-  for (int li = 0; li < d.layers; ++li) {
-    const bool last = li + 1 == d.layers;
-    CK(run_layer(c, m, li, last ? m.final_norm : m.L[li + 1].attn_norm, last && draft));
+  if (persistent) {
+    CK(run_layers_persistent(c, m, draft));
+  } else {
+    for (int li = 0; li < d.layers; ++li) {
+      const bool last = li + 1 == d.layers;
+      CK(run_layer(c, m, li, last ? m.final_norm : m.L[li + 1].attn_norm, last && draft));
+    }
   }
   // LM head (+ 1/rms of the final norm) with the fused per-tile argmax; the
   // draft proposes from each sequence's last row only (stored as row b)

@@ -13,6 +13,7 @@
 #include <vector>
 
 #include "ctx.h"
+#include "pass.h"
 
 using namespace specdec;
 
@@ -207,16 +208,45 @@ Layout make_layout(const spec_config* cfg, const spec_seq_init* seqs) {
   int maxP = 0;
   for (int b = 0; b < L.B; ++b) maxP = std::max(maxP, seqs[b].prefix_len);
   L.cap = (int)align_up((size_t)maxP + cfg->max_new_tokens + cfg->K + 2, 64);
-  L.chunk = 128;
+  L.chunk = kAttnChunk;
   if (const char* e = getenv("SPECDEC_ATTN_CHUNK")) {
     const int v = atoi(e);
-    if (v >= 32 && v % 32 == 0) L.chunk = v;
+    if (v >= 32 && v <= kMaxAttnChunk && v % 32 == 0) L.chunk = v;
   }
   L.splits = (L.cap + L.chunk - 1) / L.chunk;
   return L;
 }
 
 void set_splits(Model& m, int M) { m.s_down = down_splits(M, m.d.ffn, num_cus()); }
+
+// Down-projection k-splits of the persistent pass for one model: the fewest
+// that divide the grid (one workgroup per CU) while every worker wave streams
+// at most kPassSteps k-steps per tile and every phase fits in LDS; 0 when the
+// shapes do not fit the persistent kernel.
+int pass_splits_for(const spec_dims& d, const Layout& L, int ncu) {
+  if (L.M > 16 || (d.head_dim != 64 && d.head_dim != 128) || L.chunk != kAttnChunk) return 0;
+  // gate/up rows are read with plain loads: whole 32-wide steps per row; the
+  // other projections use 32-bit buffer offsets: segments below 2 GiB
+  if (d.hidden % 32 != 0) return 0;
+  const long long seg = std::max({(long long)d.q_heads * d.head_dim, (long long)d.ffn}) * d.hidden * 2;
+  if (seg >= (1ll << 31)) return 0;
+  PassArgs a{};
+  a.H = d.hidden;
+  a.nq = d.q_heads;
+  a.nkv = d.kv_heads;
+  a.D = d.head_dim;
+  a.F = d.ffn;
+  a.M = L.M;
+  a.attn_chunk = L.chunk;
+  a.attn_splits = L.splits;
+  const int T = (d.ffn + 31) / 32;
+  for (int s = 1; s <= std::min(ncu, T); ++s) {
+    if (ncu % s) continue;
+    a.down_splits = s;
+    if (pass_steps(a) <= kPassSteps && pass_lds_bytes(a) <= (size_t)gemv_lds_limit()) return s;
+  }
+  return 0;
+}
 
 size_t part_elems_for(const Model& m, int M) { return (size_t)m.s_down * M * m.d.hidden; }
 
@@ -269,6 +299,10 @@ size_t carve(Ctx& c, const spec_config* cfg, const spec_seq_init* seqs, bool has
     nq = std::max(nq, cfg->draft.q_heads);
     part = std::max(part, part_elems_for(c.drf, L.M));
   }
+  const bool want_pass = (cfg->flags & SPEC_FLAG_PERSISTENT) != 0;
+  c.tgt.pass_splits = want_pass ? pass_splits_for(cfg->target, L, c.ncu) : 0;
+  c.drf.pass_splits = want_pass && has_draft ? pass_splits_for(cfg->draft, L, c.ncu) : 0;
+  c.use_pass = c.tgt.pass_splits > 0 && (!has_draft || c.drf.pass_splits > 0);
   Carver cv{base};
   c.st = cv.take<SeqState>(L.B);
   c.hist = cv.take<int32_t>((size_t)L.B * L.cap);
@@ -299,6 +333,51 @@ size_t carve(Ctx& c, const spec_config* cfg, const spec_seq_init* seqs, bool has
     c.drf.kv_layer = (size_t)L.B * cfg->draft.kv_heads * L.cap * D;
     c.drf.kc = cv.take<bf16_t>(c.drf.kv_layer * cfg->draft.layers);
     c.drf.vt = cv.take<bf16_t>(c.drf.kv_layer * cfg->draft.layers);
+  }
+  if (c.use_pass) {
+    const int nl = std::max(t.layers, has_draft ? cfg->draft.layers : 0);
+    const int S = std::max(c.tgt.pass_splits, c.drf.pass_splits);
+    c.pass_layers = nl;
+    c.p_x_layer = (size_t)L.Mpad * H;
+    c.p_ss_layer = (size_t)(H / kTile) * L.Mpad;
+    c.p_q_layer = (size_t)L.Mpad * nqD;
+    c.p_u_layer = (size_t)L.Mpad * F;
+    c.p_xa = cv.take<bf16_t>(c.p_x_layer * (nl + 1));
+    c.p_xf = cv.take<bf16_t>(c.p_x_layer * nl);
+    c.p_ssa = cv.take<float>(c.p_ss_layer * (nl + 1));
+    c.p_ssf = cv.take<float>(c.p_ss_layer * nl);
+    c.p_q = cv.take<bf16_t>(c.p_q_layer * nl);
+    c.p_o = cv.take<bf16_t>(c.p_q_layer * nl);
+    c.p_u = cv.take<bf16_t>(c.p_u_layer * nl);
+    c.p_part = cv.take<float>((size_t)S * L.M * H);
+    c.p_tile_cnt = cv.take<unsigned>((size_t)H / kTile);
+    c.p_bar = cv.take<unsigned>(kPassBarWords);
+    if (cfg->flags & SPEC_FLAG_PASS_TIMELINE)
+      c.p_timeline = cv.take<unsigned long long>((size_t)pass_timeline_events(nl) * c.ncu);
+    c.tgt.lw_dev = cv.take<LayerW>(t.layers);
+    c.tgt.pass_args_dev = cv.take<PassArgs>(1);
+    c.tgt.jobs_dev = cv.take<GemvJob>((size_t)t.layers * kPassJobs);
+    if (has_draft) {
+      c.drf.lw_dev = cv.take<LayerW>(cfg->draft.layers);
+      c.drf.pass_args_dev = cv.take<PassArgs>(1);
+      c.drf.jobs_dev = cv.take<GemvJob>((size_t)cfg->draft.layers * kPassJobs);
+    }
+    PassArgs a{};
+    a.H = H;
+    a.M = L.M;
+    a.attn_chunk = L.chunk;
+    a.attn_splits = L.splits;
+    size_t lds = 0;
+    for (int k = 0; k < (has_draft ? 2 : 1); ++k) {
+      const spec_dims& d = k ? cfg->draft : t;
+      a.nq = d.q_heads;
+      a.nkv = d.kv_heads;
+      a.D = d.head_dim;
+      a.F = d.ffn;
+      a.down_splits = k ? c.drf.pass_splits : c.tgt.pass_splits;
+      lds = std::max(lds, pass_lds_bytes(a));
+    }
+    c.pass_lds = lds;
   }
   return align_up(cv.off, kAlign);
 }
@@ -537,6 +616,15 @@ spec_status spec_init(const spec_config* cfg, const void* embed, const spec_mode
             hipSuccess ||
         (e = hipMemcpyAsync(c.hist, hist.data(), hist.size() * 4, hipMemcpyHostToDevice, stream)) != hipSuccess)
       return hip_fail(e, "table upload");
+    if (c.use_pass) {
+      if ((e = hipMemcpyAsync(c.tgt.lw_dev, c.tgt.L.data(), c.tgt.L.size() * sizeof(LayerW), hipMemcpyHostToDevice,
+                              stream)) != hipSuccess ||
+          (has_draft && (e = hipMemcpyAsync(c.drf.lw_dev, c.drf.L.data(), c.drf.L.size() * sizeof(LayerW),
+                                            hipMemcpyHostToDevice, stream)) != hipSuccess) ||
+          (e = upload_pass_tables(c, c.tgt, false)) != hipSuccess ||
+          (has_draft && (e = upload_pass_tables(c, c.drf, true)) != hipSuccess))
+        return hip_fail(e, "layer table upload");
+    }
     for (int b = 0; b < c.B; ++b) {
       for (int l = 0; l < c.tgt.d.layers; ++l)
         if ((e = launch_prefix_kv(c, c.tgt, l, b, seqs[b].prefix_len, static_cast<const bf16_t*>(seqs[b].tgt_k[l]),
@@ -619,6 +707,7 @@ spec_status spec_sync(spec_ctx* ctx, int32_t* n_finished) {
     if (err & ERR_NUMERIC) return set_err(c, SPEC_E_NUMERIC, "NaN logits seen on the device");
     if (err & ERR_TOKEN) return set_err(c, SPEC_E_INVAL, "a draft token id was out of range (replaced by 0)");
     if (err & ERR_STATE) return set_err(c, SPEC_E_STATE, "draft catch-up exceeded K+1 rows");
+    if (err & ERR_SYNC) return set_err(c, SPEC_E_HIP, "a device-wide barrier of the persistent pass timed out");
     return SPEC_OK;
   });
 }
@@ -659,6 +748,29 @@ spec_status spec_debug_state(spec_ctx* ctx, int32_t b, int32_t* host_out) {
     HIPCHK(c, hipMemcpy(&s, c.st + b, sizeof s, hipMemcpyDeviceToHost), "state read");
     const int32_t v[8] = {s.seq_len, s.draft_len, s.pending, s.n_gen, s.finished, s.accept_len, s.n_commit, s.err};
     memcpy(host_out, v, sizeof v);
+    return SPEC_OK;
+  });
+}
+
+spec_status spec_debug_pass_timeline(spec_ctx* ctx, int32_t model, unsigned long long* host_out, int64_t capacity,
+                                     int32_t* n_events, int32_t* n_workgroups, double* tick_hz) {
+  return guarded(ctx, [&](Ctx& c) -> spec_status {
+    if (!c.p_timeline) return set_err(c, SPEC_E_STATE, "the context was created without SPEC_FLAG_PASS_TIMELINE");
+    if (model != 0 && !(model == 1 && c.has_draft)) return set_err(c, SPEC_E_INVAL, "bad model");
+    const int ev = pass_timeline_events((model == 0 ? c.tgt : c.drf).d.layers);
+    const size_t n = (size_t)ev * c.ncu;
+    if (n_events) *n_events = ev;
+    if (n_workgroups) *n_workgroups = c.ncu;
+    if (tick_hz) {
+      int khz = 0;
+      if (hipDeviceGetAttribute(&khz, hipDeviceAttributeWallClockRate, c.device) != hipSuccess || khz <= 0)
+        khz = 100000;
+      *tick_hz = khz * 1e3;
+    }
+    if (!host_out) return SPEC_OK;
+    if (capacity < (int64_t)n) return set_err(c, SPEC_E_CAPACITY, "timeline buffer too small");
+    HIPCHK(c, hipStreamSynchronize(c.stream), "sync");
+    HIPCHK(c, hipMemcpy(host_out, c.p_timeline, n * sizeof(unsigned long long), hipMemcpyDeviceToHost), "timeline");
     return SPEC_OK;
   });
 }

@@ -15,6 +15,10 @@ LOGIT_RTOL = 2e-2
 MARGIN = 2e-2
 
 
+# Session flags selecting the library's execution path (see include/spec.h).
+PATH_FLAGS = {"persistent": 2, "layered": 0}
+
+
 def capacity_for(w: W.Workload, b: int) -> int:
     return w.seqs[b].prefix_len + w.max_new_tokens + w.K + 2
 

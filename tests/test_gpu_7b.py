@@ -25,8 +25,20 @@ from tests import _support as S
 pytestmark = pytest.mark.gpu
 
 
+# Every test runs on both execution paths of the library: the persistent
+# pass kernel and one kernel per layer step.
+_PATH = {"flags": 0}
+
+
+@pytest.fixture(autouse=True, params=["persistent", "layered"])
+def path(request):
+    _PATH["flags"] = S.PATH_FLAGS[request.param]
+    yield request.param
+
+
 def _session(w, **kw):
     from paper_2606_31160_amd.harness import Session
+    kw["flags"] = kw.get("flags", 0) | _PATH["flags"]
     return Session(w, **kw)
 
 

@@ -22,8 +22,20 @@ from tests import _support as S
 pytestmark = pytest.mark.gpu
 
 
+# Every test runs on both execution paths of the library: the persistent
+# pass kernel and one kernel per layer step.
+_PATH = {"flags": 0}
+
+
+@pytest.fixture(autouse=True, params=["persistent", "layered"])
+def path(request):
+    _PATH["flags"] = S.PATH_FLAGS[request.param]
+    yield request.param
+
+
 def _session(w, **kw):
     from paper_2606_31160_amd.harness import Session
+    kw["flags"] = kw.get("flags", 0) | _PATH["flags"]
     return Session(w, **kw)
 
 
@@ -342,4 +354,28 @@ def test_interleaved_axis_assignment_rotation():
     for li in range(w.target.layers):
         k = ON.decode(s.kv(0, 0, li, 0, P, w.K + 1))
         assert S.normwise_err(k, seq.tc.k[li][P:P + w.K + 1]) <= S.LOGIT_RTOL
+    s.close()
+
+
+def test_requested_execution_path_runs(c1, path):
+    """The persistent pass kernel runs every layer when it is selected, and
+    the per-layer kernels run otherwise (counted by the library's timing)."""
+    from paper_2606_31160_amd import binding as B
+    w = c1[0]
+    s = _session(w)
+    B.spec_timing(s.ctx, True)
+    s.draft_step()
+    for _ in range(w.K - 1):
+        s.draft_step()
+    s.verify(None)
+    s.commit()
+    n_pt, _, _ = B.spec_timing_read(s.ctx, "pass_target")
+    n_pd, _, _ = B.spec_timing_read(s.ctx, "pass_draft")
+    n_qkv, _, _ = B.spec_timing_read(s.ctx, "qkv")
+    B.spec_timing(s.ctx, False)
+    assert s.sync() == 0
+    if path == "persistent":
+        assert (n_pt, n_pd, n_qkv) == (1, w.K, 0)
+    else:
+        assert (n_pt, n_pd) == (0, 0) and n_qkv == w.target.layers + w.K * w.draft.layers
     s.close()
