@@ -70,6 +70,8 @@ struct Model {
   LayerW* lw_dev = nullptr;        // [layers] device copy of L (persistent pass)
   PassArgs* pass_args_dev = nullptr;   // device copy of this model's pass arguments
   GemvJob* jobs_dev = nullptr;         // [layers][kPassJobs] GEMV phases of the pass
+  PassArgs* largs_dev = nullptr;       // layered path: arguments of the one-phase GEMV kernels
+  GemvJob* ljobs_dev = nullptr;        // layered path: [layers][kPassJobs] (gate/up and down used)
   size_t kv_layer = 0;              // elements of one layer's key (or value) cache
 };
 
@@ -116,10 +118,11 @@ struct Ctx {
   // persistent pass (pass.hip): per-layer activations, barrier words
   bool use_pass = false;
   size_t pass_lds = 0;
+  size_t ljob_lds = 0;              // dynamic LDS of the layered path's one-phase GEMV kernels
   int pass_layers = 0;              // max layers over the models
   bf16_t *p_xa = nullptr, *p_xf = nullptr, *p_q = nullptr, *p_o = nullptr, *p_u = nullptr;
   float *p_ssa = nullptr, *p_ssf = nullptr, *p_part = nullptr;
-  unsigned *p_tile_cnt = nullptr, *p_bar = nullptr;
+  unsigned* p_bar = nullptr;
   size_t p_x_layer = 0, p_ss_layer = 0, p_q_layer = 0, p_u_layer = 0;
   unsigned long long* p_timeline = nullptr;   // SPEC_FLAG_PASS_TIMELINE
 
@@ -148,6 +151,8 @@ struct Ctx {
 hipError_t launch_zero(Ctx& c, void* p, size_t bytes);
 // Uploads the persistent pass's arguments and GEMV jobs of one model (init).
 hipError_t upload_pass_tables(Ctx& c, Model& m, bool draft);
+// Uploads the layered path's one-phase GEMV arguments and jobs of one model.
+hipError_t upload_layered_jobs(Ctx& c, Model& m, bool draft);
 hipError_t launch_hold(Ctx& c, double ms);   // bounded device-side wait (timing mode)
 hipError_t launch_prefix_kv(Ctx& c, Model& m, int layer, int b, int prefix_len,
                             const bf16_t* k_pre, const bf16_t* v);

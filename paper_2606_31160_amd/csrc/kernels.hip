@@ -1144,6 +1144,10 @@ GemvArgs gemv_base(Ctx& c, int M, int rps) {
     if (e_ != hipSuccess) return e_;        \
   } while (0)
 
+// Which layered projections run as one-phase GEMV kernels (pass.hip) when
+// the shapes allow it; measured per projection on the 7B-class verify.
+constexpr bool kQkvAsJob = false, kOAsJob = false, kDownAsJob = false;
+
 hipError_t run_layer(Ctx& c, Model& m, int li, const bf16_t* next_gain, bool select_last) {
   const spec_dims& d = m.d;
   const int H = d.hidden, D = d.head_dim, nq = d.q_heads, nkv = d.kv_heads, F = d.ffn;
@@ -1153,7 +1157,11 @@ hipError_t run_layer(Ctx& c, Model& m, int li, const bf16_t* next_gain, bool sel
   bf16_t* vt = m.vt + m.kv_layer * li;
 
   // q, k, v (+ 1/rms of the attention norm) + rotary + cache append
-  {
+  if (m.ljobs_dev && kQkvAsJob) {
+    Timed t(c, SPEC_KERNEL_QKV, gemv_bytes((nq + 2 * nkv) * D, H, M, 2.0));
+    CK(gemv_job_launch(kJobQkv, gemv_job_steps(H, 1), m.largs_dev, m.ljobs_dev + (size_t)li * kPassJobs + kJobQkv,
+                       c.ncu, c.ljob_lds, S(c), t.e0, t.e1));
+  } else {
     GemvArgs g = gemv_base(c, M, c.R);
     g.w[0] = w.wq;
     g.w[1] = w.wk;
@@ -1202,7 +1210,11 @@ hipError_t run_layer(Ctx& c, Model& m, int li, const bf16_t* next_gain, bool sel
     CK(hipGetLastError());
   }
   // o projection + residual; bf16(x * g_ffn) and sums of x^2 for the FFN norm
-  {
+  if (m.ljobs_dev && kOAsJob) {
+    Timed t(c, SPEC_KERNEL_O, gemv_bytes(H, nq * D, M, 10.0));
+    CK(gemv_job_launch(kJobO, gemv_job_steps(nq * D, 1), m.largs_dev, m.ljobs_dev + (size_t)li * kPassJobs + kJobO,
+                       c.ncu, c.ljob_lds, S(c), t.e0, t.e1));
+  } else {
     GemvArgs g = gemv_base(c, M, c.R);
     g.w[0] = w.wo;
     g.nseg = 1;
@@ -1217,7 +1229,11 @@ hipError_t run_layer(Ctx& c, Model& m, int li, const bf16_t* next_gain, bool sel
     CK((gemv_launch<EPI_RESID, 1>(c, g, SPEC_KERNEL_O, gemv_bytes(H, nq * D, M, 10.0))));
   }
   // gate/up (+ 1/rms of the FFN norm) + SwiGLU
-  {
+  if (m.ljobs_dev) {
+    Timed t(c, SPEC_KERNEL_GATEUP, gemv_bytes(2 * F, H, M, 1.0));
+    CK(gemv_job_launch(kJobGateUp, gemv_job_steps(H, 1), m.largs_dev, m.ljobs_dev + (size_t)li * kPassJobs + kJobGateUp,
+                       c.ncu, c.ljob_lds, S(c), t.e0, t.e1));
+  } else {
     GemvArgs g = gemv_base(c, M, c.R);
     g.w[0] = w.wg;
     g.w[1] = w.wu;
@@ -1235,18 +1251,26 @@ hipError_t run_layer(Ctx& c, Model& m, int li, const bf16_t* next_gain, bool sel
   }
   // down projection (k-split partials) -> residual + the next norm's input
   {
-    GemvArgs g = gemv_base(c, M, c.R);
-    g.w[0] = w.wd;
-    g.nseg = 1;
-    g.N = H;
-    g.Kd = F;
-    g.x = c.u;
-    g.ldx = F;
-    g.splits = m.s_down;
-    g.out = c.part;
-    const int per_split = std::max(1, std::min(c.ncu / m.s_down, H / kTile));
-    CK(gemv_launch_p<EPI_STORE>(c, g, per_split * m.s_down, SPEC_KERNEL_DOWN, gemv_bytes(H, F, M, 4.0 * m.s_down)));
-    FinishArgs p{c.st, c.part, m.s_down, M, c.R, H, c.Mpad, select_last ? 1 : 0, c.x, next_gain, c.xg, c.ss};
+    int S_down = m.s_down;
+    if (m.ljobs_dev && kDownAsJob) {
+      S_down = m.pass_splits;
+      Timed t(c, SPEC_KERNEL_DOWN, gemv_bytes(H, F, M, 4.0 * S_down));
+      CK(gemv_job_launch(kJobDown, gemv_job_steps(F, S_down), m.largs_dev,
+                         m.ljobs_dev + (size_t)li * kPassJobs + kJobDown, c.ncu, c.ljob_lds, S(c), t.e0, t.e1));
+    } else {
+      GemvArgs g = gemv_base(c, M, c.R);
+      g.w[0] = w.wd;
+      g.nseg = 1;
+      g.N = H;
+      g.Kd = F;
+      g.x = c.u;
+      g.ldx = F;
+      g.splits = m.s_down;
+      g.out = c.part;
+      const int per_split = std::max(1, std::min(c.ncu / m.s_down, H / kTile));
+      CK(gemv_launch_p<EPI_STORE>(c, g, per_split * m.s_down, SPEC_KERNEL_DOWN, gemv_bytes(H, F, M, 4.0 * m.s_down)));
+    }
+    FinishArgs p{c.st, c.part, S_down, M, c.R, H, c.Mpad, select_last ? 1 : 0, c.x, next_gain, c.xg, c.ss};
     Timed t(c, SPEC_KERNEL_OTHER, 0);
     hipExtLaunchKernelGGL(k_down_finish, dim3((H + 255) / 256, M), dim3(256), 0, S(c), t.e0, t.e1, 0, p);
     CK(hipGetLastError());
@@ -1318,6 +1342,65 @@ hipError_t upload_pass_tables(Ctx& c, Model& m, bool draft) {
   if (e == hipSuccess)
     e = hipMemcpyAsync(m.jobs_dev, jobs.data(), jobs.size() * sizeof(GemvJob), hipMemcpyHostToDevice, c.stream);
   // the host copies are local: wait for the uploads before they go away
+  if (e == hipSuccess) e = hipStreamSynchronize(c.stream);
+  return e;
+}
+
+hipError_t upload_layered_jobs(Ctx& c, Model& m, bool draft) {
+  PassArgs a = pass_args(c, m, draft);
+  a.part = c.part;                    // down partials for k_down_finish
+  a.down_splits = m.pass_splits;
+  std::vector<GemvJob> jobs((size_t)m.d.layers * kPassJobs);
+  const spec_dims& d = m.d;
+  for (int li = 0; li < d.layers; ++li) {
+    const LayerW& w = m.L[li];
+    GemvJob* j = jobs.data() + (size_t)li * kPassJobs;
+    j[kJobQkv] = GemvJob{};
+    j[kJobQkv].w[0] = w.wq;
+    j[kJobQkv].w[1] = w.wk;
+    j[kJobQkv].w[2] = w.wv;
+    j[kJobQkv].row0[1] = d.q_heads * d.head_dim;
+    j[kJobQkv].row0[2] = (d.q_heads + d.kv_heads) * d.head_dim;
+    j[kJobQkv].nseg = 3;
+    j[kJobQkv].N = (d.q_heads + 2 * d.kv_heads) * d.head_dim;
+    j[kJobQkv].Kd = d.hidden;
+    j[kJobQkv].splits = 1;
+    j[kJobQkv].x = c.xg;
+    j[kJobQkv].ss_in = c.ss;
+    j[kJobQkv].q = c.q;
+    j[kJobQkv].kc = m.kc + m.kv_layer * li;
+    j[kJobQkv].vt = m.vt + m.kv_layer * li;
+    j[kJobO] = GemvJob{};
+    j[kJobO].w[0] = j[kJobO].w[1] = j[kJobO].w[2] = w.wo;
+    j[kJobO].nseg = 1;
+    j[kJobO].N = d.hidden;
+    j[kJobO].Kd = d.q_heads * d.head_dim;
+    j[kJobO].splits = 1;
+    j[kJobO].x = c.o;
+    j[kJobO].gain = w.ffn_norm;
+    j[kJobO].xg_out = c.xg;
+    j[kJobO].ss_out = c.ss;
+    j[kJobGateUp] = GemvJob{};
+    j[kJobGateUp].w[0] = w.wg;
+    j[kJobGateUp].w[1] = j[kJobGateUp].w[2] = w.wu;
+    j[kJobGateUp].nseg = 2;
+    j[kJobGateUp].N = 2 * d.ffn;
+    j[kJobGateUp].Kd = d.hidden;
+    j[kJobGateUp].splits = 1;
+    j[kJobGateUp].x = c.xg;
+    j[kJobGateUp].ss_in = c.ss;
+    j[kJobGateUp].u = c.u;
+    j[kJobDown] = GemvJob{};
+    j[kJobDown].w[0] = j[kJobDown].w[1] = j[kJobDown].w[2] = w.wd;
+    j[kJobDown].nseg = 1;
+    j[kJobDown].N = d.hidden;
+    j[kJobDown].Kd = d.ffn;
+    j[kJobDown].splits = m.pass_splits;
+    j[kJobDown].x = c.u;
+  }
+  hipError_t e = hipMemcpyAsync(m.largs_dev, &a, sizeof a, hipMemcpyHostToDevice, c.stream);
+  if (e == hipSuccess)
+    e = hipMemcpyAsync(m.ljobs_dev, jobs.data(), jobs.size() * sizeof(GemvJob), hipMemcpyHostToDevice, c.stream);
   if (e == hipSuccess) e = hipStreamSynchronize(c.stream);
   return e;
 }
@@ -1407,7 +1490,6 @@ PassArgs pass_args(Ctx& c, Model& m, bool draft) {
   a.attn_splits = c.attn_splits;
   a.down_splits = m.pass_splits;
   a.part = c.p_part;
-  a.tile_cnt = c.p_tile_cnt;
   a.bar = c.p_bar;
   a.timeline = c.p_timeline;
   return a;

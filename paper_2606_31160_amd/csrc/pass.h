@@ -30,6 +30,7 @@ struct GemvJob {
   int select_last;           // down, last layer of a draft pass
 };
 constexpr int kPassJobs = 4;   // QKV, O, gate/up, down
+enum { kJobQkv = 0, kJobO = 1, kJobGateUp = 2, kJobDown = 3 };
 
 struct PassArgs {
   SeqState* st;
@@ -62,24 +63,31 @@ struct PassArgs {
   // down projection
   int down_splits;
   float* part;               // [down_splits][M][H]
-  unsigned* tile_cnt;        // [H/16] arrivals per output tile (reset by the last)
   unsigned* bar;             // barrier words (kPassBarWords), zero between launches
   unsigned long long* timeline;  // optional [events][workgroups] wall-clock stamps, or null
 };
 
 // Timeline events of one launch: 0 = start, then for each layer and phase
 // (QKV, attention, combine, O, gate/up, down) 2 events: the workgroup's work
-// done, the following barrier passed.
+// done, the following barrier passed (after down: the barrier before the
+// down projection's finish).
 constexpr int kPassPhases = 6;
 inline int pass_timeline_events(int layers) { return 1 + layers * kPassPhases * 2; }
 
 constexpr int kPassBarWords = 1024;
 
 size_t pass_lds_bytes(const PassArgs& a);
+size_t pass_gemv_lds_bytes(const PassArgs& a);   // the GEMV phases only
 // Fills jobs[layers][kPassJobs] from the (host) arguments and layer weights.
 void pass_build_jobs(const PassArgs& a, const LayerW* lw, const bf16_t* final_norm, GemvJob* jobs);
 int pass_steps(const PassArgs& a);
 void pass_set_attributes(int lds_limit);
+// One GEMV job (kind kJob*) as a kernel of its own; d_args supplies rows,
+// norms and buffers, d_job the weights and input/output of the phase.
+// steps: k-steps per worker wave (gemv_job_steps), at most kPassSteps.
+hipError_t gemv_job_launch(int kind, int steps, const PassArgs* d_args, const GemvJob* d_job, int workgroups,
+                           size_t lds, hipStream_t s, hipEvent_t e0, hipEvent_t e1);
+int gemv_job_steps(int Kd, int splits);
 // d_args: device copy of the arguments (constant between launches).
 hipError_t pass_launch(const PassArgs* d_args, int head_dim, bool draft, int workgroups, size_t lds, hipStream_t s,
                        hipEvent_t e0, hipEvent_t e1);

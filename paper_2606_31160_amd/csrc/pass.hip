@@ -67,6 +67,13 @@ __device__ __forceinline__ uint32_t ld_u32(const void* p) {
   return __hip_atomic_load((const GLOBAL_AS uint32_t*)(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 __device__ __forceinline__ float ld_f32(const float* p) { return __uint_as_float(ld_u32(p)); }
+__device__ __forceinline__ void st_f32x4(float* p, f32x4 v) {
+  GLOBAL_AS uint64_t* q = (GLOBAL_AS uint64_t*)(p);
+  __hip_atomic_store(q, (uint64_t)__float_as_uint(v.x) | ((uint64_t)__float_as_uint(v.y) << 32), __ATOMIC_RELAXED,
+                     __HIP_MEMORY_SCOPE_AGENT);
+  __hip_atomic_store(q + 1, (uint64_t)__float_as_uint(v.z) | ((uint64_t)__float_as_uint(v.w) << 32), __ATOMIC_RELAXED,
+                     __HIP_MEMORY_SCOPE_AGENT);
+}
 
 // A value the compiler must treat as unknown at this point: keeps per-tile
 // scalars inside the tile loop instead of hoisting them for the whole launch.
@@ -110,11 +117,16 @@ __device__ __forceinline__ bool spin_until(const unsigned* p, unsigned target) {
   return false;
 }
 
-// Called by all threads.  The caller's stores must be complete (the release
-// fence below waits for them; no weight loads are outstanding at this point).
-__device__ __forceinline__ void grid_sync(const PassArgs& a, unsigned gen, bool& failed) {
+// Called by all threads.  Every thread first waits for its own stores (no
+// loads are outstanding then); `prefetch` may then issue the next phase's
+// weight loads, which stay in flight: the rest uses raw workgroup barriers,
+// which do not wait for memory.  Wave 0 (no weight loads) runs the
+// device-wide part.
+template <class Prefetch>
+__device__ __forceinline__ void grid_sync(const PassArgs& a, unsigned gen, bool& failed, Prefetch&& prefetch) {
   __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
-  __syncthreads();
+  prefetch();
+  __builtin_amdgcn_s_barrier();
   if (threadIdx.x == 0 && !failed) {
     const unsigned G = gridDim.x;
     const unsigned grp = blockIdx.x % kBarGroups;
@@ -135,7 +147,11 @@ __device__ __forceinline__ void grid_sync(const PassArgs& a, unsigned gen, bool&
       atomicOr(&a.st[0].err, ERR_SYNC);
     }
   }
-  __syncthreads();
+  __builtin_amdgcn_s_barrier();
+}
+
+__device__ __forceinline__ void grid_sync(const PassArgs& a, unsigned gen, bool& failed) {
+  grid_sync(a, gen, failed, [] {});
 }
 
 // The last workgroup to finish clears every barrier word for the next launch.
@@ -172,78 +188,102 @@ __device__ __forceinline__ uint64_t live_rows(const PassArgs& a) {
 enum { PE_ROPE = 0, PE_RESID = 1, PE_SWIGLU = 2, PE_DOWN = 3 };
 
 
+// Work split of one GEMV phase for this thread's workgroup and wave.
+struct Geom {
+  int gsize, split, g, Kd, kq, s0, s1, w0, nw_all, ncol, nwork;
+};
+
 template <int EPI>
-__device__ __forceinline__ void gemv_phase(const PassArgs& a, const GemvJob& j, unsigned char* lds, uint64_t live) {
-  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
-  const int G = gridDim.x;
-  const int gsize = G / j.splits;
-  const int split = blockIdx.x / gsize, g = blockIdx.x % gsize;
-  const int Kd = j.Kd;
-  const int kq = 8 * (lane >> 4);
-  const int T = (Kd + 31) >> 5;
-  const int s0 = split * T / j.splits;            // T <= 2^16 and splits <= 2^10: 32-bit exact
-  const int s1 = (split + 1) * T / j.splits;
-  const int chunk = (s1 - s0 + kWorkers - 1) / kWorkers;
-  const bool worker = wave > 0;
-  const int w0 = s0 + (worker ? wave - 1 : 0) * chunk;
-  const int nw_all = worker ? max(0, min(chunk, s1 - w0)) : 0;   // steps of this wave (control: none)
-  constexpr bool kNorm = EPI == PE_ROPE || EPI == PE_SWIGLU;
-  // gate/up: each 16-column output tile is a gate tile followed by the up
-  // tile of the same rows, so every tile reads one matrix
+__device__ __forceinline__ Geom gemv_geom(const GemvJob& j) {
   constexpr bool kPair = EPI == PE_SWIGLU;
-  const int ncol = (kPair ? j.N / 2 : j.N) / kTile;              // 16-column output tiles
-  const int mine = g < ncol ? (ncol - 1 - g) / gsize + 1 : 0;   // output tiles of this workgroup
-  const int nwork = kPair ? 2 * mine : mine;                     // weight tiles it streams
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  Geom q;
+  q.gsize = gridDim.x / j.splits;
+  q.split = blockIdx.x / q.gsize;
+  q.g = blockIdx.x % q.gsize;
+  q.Kd = j.Kd;
+  q.kq = 8 * (lane >> 4);
+  const int T = (j.Kd + 31) >> 5;
+  q.s0 = q.split * T / j.splits;                   // T <= 2^16 and splits <= 2^10: 32-bit exact
+  q.s1 = (q.split + 1) * T / j.splits;
+  const int chunk = (q.s1 - q.s0 + kWorkers - 1) / kWorkers;
+  const bool worker = wave > 0;
+  q.w0 = q.s0 + (worker ? wave - 1 : 0) * chunk;
+  q.nw_all = worker ? max(0, min(chunk, q.s1 - q.w0)) : 0;   // steps of this wave (control: none)
+  // gate/up: each 16-column output tile is a gate tile followed by the up
+  // tile of the same rows, so every weight tile reads one matrix
+  q.ncol = (kPair ? j.N / 2 : j.N) / kTile;
+  const int mine = q.g < q.ncol ? (q.ncol - 1 - q.g) / q.gsize + 1 : 0;
+  q.nwork = kPair ? 2 * mine : mine;
+  return q;
+}
+
+constexpr int kOutside = 0x7FFFFF00;   // buffer offset past any segment (segments are below 2 GiB)
+
+// Weight tile k of this workgroup: a buffer resource over its matrix segment
+// and this lane's byte offset; step i is at +64 i.  Steps a wave does not own,
+// and the prefetch after the last tile, use an offset past the segment, which
+// reads zeros without touching memory (no branches in the step loop, so no
+// waits for the weights in flight are forced).
+template <int EPI>
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t gemv_source(const GemvJob& j, const Geom& q, int k, int& voff) {
+  constexpr bool kPair = EPI == PE_SWIGLU;
+  const int lane = threadIdx.x & 63;
+  const int c = q.g + (kPair ? (k >> 1) : k) * q.gsize;
+  const int N = j.N;
+  int rows, r;
+  const bf16_t* base;
+  if constexpr (kPair) {
+    base = (k & 1) ? j.w[1] : j.w[0];
+    rows = N / 2;
+    r = c * kTile;
+  } else {
+    const int n0 = c * kTile, rw1 = j.row0[1], rw2 = j.row0[2], nseg = j.nseg;
+    const bool g2 = nseg > 2 && n0 >= rw2, g1 = !g2 && nseg > 1 && n0 >= rw1;
+    const int r0 = g2 ? rw2 : (g1 ? rw1 : 0);
+    const int r1 = g2 ? N : (g1 ? (nseg > 2 ? rw2 : N) : (nseg > 1 ? rw1 : N));
+    base = g2 ? j.w[2] : (g1 ? j.w[1] : j.w[0]);
+    rows = r1 - r0;
+    r = n0 - r0;
+  }
+  voff = ((r + (lane & 15)) * q.Kd + q.kq + q.w0 * 32) * 2;
+  // built from scalar registers (else every load becomes a loop over the
+  // lanes' distinct resources)
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<bf16_t*>(opaque_p(base)), 0, opaque_s(rows * q.Kd * 2),
+                                           kBufWord3);
+}
+
+// Issues the loads of this workgroup's first weight tile of job j into wv
+// (the control wave and workgroups without tiles load zeros).
+template <int EPI, int STEPS = kPassSteps>
+__device__ __forceinline__ void gemv_prefetch(const GemvJob& j, u32x4 (&wv)[STEPS]) {
+  const Geom q = gemv_geom<EPI>(j);
+  int voff;
+  const __amdgpu_buffer_rsrc_t rs = gemv_source<EPI>(j, q, 0, voff);
+  const int nw = q.nwork > 0 ? q.nw_all : 0;
+#pragma unroll
+  for (int i = 0; i < STEPS; ++i)
+    wv[i] = __builtin_amdgcn_raw_buffer_load_b128(rs, i < nw ? voff + 64 * i : kOutside, 0, 0);
+}
+
+// The GEMV phase; wv holds the first tile's weights (gemv_prefetch).
+template <int EPI, int STEPS = kPassSteps>
+__device__ __forceinline__ void gemv_phase(const PassArgs& a, const GemvJob& j, unsigned char* lds, uint64_t live,
+                                           u32x4 (&wv)[STEPS]) {
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const Geom q = gemv_geom<EPI>(j);
+  const int split = q.split, g = q.g, gsize = q.gsize, Kd = q.Kd, s0 = q.s0, s1 = q.s1, w0 = q.w0;
+  const int nw_all = q.nw_all, nwork = q.nwork;
+  const bool worker = wave > 0;
+  constexpr bool kNorm = EPI == PE_ROPE || EPI == PE_SWIGLU;
+  constexpr bool kPair = EPI == PE_SWIGLU;
+  const int N = j.N;
   const int per_row = (s1 - s0) * 4, xstride = per_row + 1;
   u32x4* xs = reinterpret_cast<u32x4*>(lds);
   f32x4* red = reinterpret_cast<f32x4*>(lds + (size_t)a.M * xstride * 16);                 // [7][64]
   float* y = reinterpret_cast<float*>(lds + (size_t)a.M * xstride * 16 + kWorkers * 64 * 16);   // [16][17]
   float* inv_rms = y + 16 * 17;                                                             // [16]
   float* ygate = inv_rms + 16;                                                              // [16][17]
-
-  // Weight tile k of this workgroup: a buffer resource over its matrix
-  // segment and this lane's byte offset; step i is at +64 i.  Steps a wave
-  // does not own, and the prefetch after the last tile, use an offset past
-  // the segment, which reads zeros without touching memory (no branches in
-  // the step loop, so no waits for the weights in flight are forced).
-  const bf16_t* const wp0 = opaque_p(j.w[0]);
-  const bf16_t* const wp1 = opaque_p(j.w[1]);
-  const bf16_t* const wp2 = opaque_p(j.w[2]);
-  const int rw1 = j.row0[1], rw2 = j.row0[2], nseg = j.nseg, N = j.N;
-  auto source = [&](int k, int& voff) -> __amdgpu_buffer_rsrc_t {
-    const int c = g + (kPair ? (k >> 1) : k) * gsize;
-    int rows, r;
-    const bf16_t* base;
-    if constexpr (kPair) {
-      base = (k & 1) ? wp1 : wp0;
-      rows = N / 2;
-      r = c * kTile;
-    } else {
-      const int n0 = c * kTile;
-      const bool g2 = nseg > 2 && n0 >= rw2, g1 = !g2 && nseg > 1 && n0 >= rw1;
-      const int r0 = g2 ? rw2 : (g1 ? rw1 : 0);
-      const int r1 = g2 ? N : (g1 ? (nseg > 2 ? rw2 : N) : (nseg > 1 ? rw1 : N));
-      base = g2 ? wp2 : (g1 ? wp1 : wp0);
-      rows = r1 - r0;
-      r = n0 - r0;
-    }
-    voff = ((r + (lane & 15)) * Kd + kq + w0 * 32) * 2;
-    // the resource must be built from scalar registers (else every load
-    // becomes a loop over the lanes' distinct resources)
-    return __builtin_amdgcn_make_buffer_rsrc(const_cast<bf16_t*>(opaque_p(base)), 0, opaque_s(rows * Kd * 2),
-                                             kBufWord3);
-  };
-  constexpr int kOutside = 0x7FFFFF00;   // past any segment (segments are below 2 GiB)
-
-  u32x4 wv[kPassSteps];
-  {
-    int voff;
-    const __amdgpu_buffer_rsrc_t rs = source(0, voff);
-    const int nw = nwork > 0 ? nw_all : 0;
-#pragma unroll
-    for (int i = 0; i < kPassSteps; ++i)
-      wv[i] = __builtin_amdgcn_raw_buffer_load_b128(rs, i < nw ? voff + 64 * i : kOutside, 0, 0);
-  }
 
   for (int c = threadIdx.x; per_row > 0 && c < a.M * per_row; c += kPassWaves * 64) {
     const int m = c / per_row, qq = c - m * per_row;
@@ -272,10 +312,10 @@ __device__ __forceinline__ void gemv_phase(const PassArgs& a, const GemvJob& j, 
       const int nw = opaque_s(nw_all);
       const int nxt = opaque_s(k + 1 < nwork ? 1 : 0);
       int voff;
-      const __amdgpu_buffer_rsrc_t rs = source(nxt ? k + 1 : k, voff);
+      const __amdgpu_buffer_rsrc_t rs = gemv_source<EPI>(j, q, nxt ? k + 1 : k, voff);
       const u32x4* xrow = xs + m * xstride + (w0 - s0) * 4 + (lane >> 4);
 #pragma unroll
-      for (int i = 0; i < kPassSteps; ++i) {
+      for (int i = 0; i < STEPS; ++i) {
         const bool on = i < nw;
         const u32x4 xr = xrow[4 * (on ? i : 0)];
         const u32x4 xv = (on && mok) ? xr : u32x4{0, 0, 0, 0};
@@ -344,50 +384,45 @@ __device__ __forceinline__ void gemv_phase(const PassArgs& a, const GemvJob& j, 
           const float gt = ygate[m * 17 + c], up = y[m * 17 + c];
           st_u16(j.u + (size_t)m * (N / 2) + n0 + c, f2bf(gt / (1.f + expf(-gt)) * up));
         }
-      }    } else {
-      // k-split partial -> memory; the last of the splits to arrive adds the
-      // residual and writes the next norm's input.  Done by the control wave
-      // while the workers stream the next tile.
-      if (wave == 0) {
-        const int S = j.splits;
-        for (int q = lane; q < a.M * 16; q += 64) {
-          const int m = q >> 4, c = q & 15;
-          st_f32(a.part + ((size_t)split * a.M + m) * a.H + n0 + c, y[m * 17 + c]);
-        }
-        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");   // partial stores complete
-        unsigned old = 0;
-        if (lane == 0)
-          old = __hip_atomic_fetch_add((GLOBAL_AS unsigned*)(a.tile_cnt + tile), 1u, __ATOMIC_RELAXED,
-                                       __HIP_MEMORY_SCOPE_AGENT);
-        old = __shfl(old, 0);
-        if (old + 1 == (unsigned)S) {
-          if (lane == 0) st_u32(a.tile_cnt + tile, 0u);
-          for (int q0 = 0; q0 < 16 * 16; q0 += 64) {
-            const int q = q0 + lane, m = q >> 4, c = q & 15;
-            const int n = n0 + c;
-            const bool row = m < a.M;
-            const int b = row ? m / a.rps : 0, jj = row ? m - b * a.rps : 0;
-            const int count = row ? a.st[b].count : 0;
-            float xn = 0.f;
-            if (row) {
-              xn = ld_f32(a.x + (size_t)m * a.H + n);
-              if (jj < count) {
-                float v = 0.f;
-                for (int sp = 0; sp < S; ++sp) v += ld_f32(a.part + ((size_t)sp * a.M + m) * a.H + n);
-                xn += v;
-                st_f32(a.x + (size_t)m * a.H + n, xn);
-              }
-            }
-            float sq = xn * xn;
-            for (int o = 1; o < 16; o <<= 1) sq += __shfl_xor(sq, o);
-            if (row && (!j.select_last || jj == count - 1)) {
-              const int out = j.select_last ? b : m;
-              st_u16(j.xg_out + (size_t)out * a.H + n, f2bf(xn * bf2f(ldg(j.gain + n))));
-              if (c == 0) st_f32(j.ss_out + (size_t)tile * a.mpad + out, sq);
-            }
-          }
-        }
       }
+    } else {
+      // k-split partial sums; the finish phase adds them after a barrier
+      const int qd = threadIdx.x, m = qd >> 4, c = qd & 15;
+      if (qd < 256 && m < a.M) st_f32(a.part + ((size_t)split * a.M + m) * a.H + n0 + c, y[m * 17 + c]);
+    }
+  }
+}
+
+// Down projection finish: x += sum of the k-split partials (live rows), then
+// the next norm's input bf16(x * gain) and per-16-column sums of x^2; for the
+// last layer of a draft pass only each sequence's last live row, stored as
+// row b.  16-column tiles are dealt to the workgroups; 256 threads per tile.
+__device__ __forceinline__ void finish_phase(const PassArgs& a, const GemvJob& j) {
+  const int ntiles = a.H / kTile;
+  const int qd = threadIdx.x, m = qd >> 4, c = qd & 15;
+  const int S = j.splits;
+  for (int tile = blockIdx.x; tile < ntiles; tile += gridDim.x) {   // workgroup-uniform
+    if (qd >= 256) continue;
+    const int n = tile * kTile + c;
+    const bool row = m < a.M;
+    const int b = row ? m / a.rps : 0, jj = row ? m - b * a.rps : 0;
+    const int count = row ? a.st[b].count : 0;
+    float xn = 0.f;
+    if (row) {
+      xn = ld_f32(a.x + (size_t)m * a.H + n);
+      if (jj < count) {
+        float v = 0.f;
+        for (int sp = 0; sp < S; ++sp) v += ld_f32(a.part + ((size_t)sp * a.M + m) * a.H + n);
+        xn += v;
+        st_f32(a.x + (size_t)m * a.H + n, xn);
+      }
+    }
+    float sq = xn * xn;
+    for (int o = 1; o < 16; o <<= 1) sq += __shfl_xor(sq, o);
+    if (row && (!j.select_last || jj == count - 1)) {
+      const int out = j.select_last ? b : m;
+      st_u16(j.xg_out + (size_t)out * a.H + n, f2bf(xn * bf2f(ldg(j.gain + n))));
+      if (c == 0) st_f32(j.ss_out + (size_t)tile * a.mpad + out, sq);
     }
   }
 }
@@ -452,37 +487,30 @@ __device__ __forceinline__ void attn_phase(const PassArgs& a, const bf16_t* q, c
       for (int t = 0; t < D / 32; ++t) qf[t] = (work && rvalid) ? ldg16(qp + 32 * t) : u32x4{0, 0, 0, 0};
     }
     if (have && k0 < k1) {
-      // keys, then values: PER_T 16-byte loads per thread in flight at a time
+      // all of the thread's key and value loads are issued before its first
+      // LDS store, so their latencies overlap
       constexpr int PER_T = kAttnChunk * D / 8 / 256;
       const bf16_t* Kb = kc + ((size_t)b * a.nkv + kvh) * a.cap * D;
       const bf16_t* Vb = vt + ((size_t)b * a.nkv + kvh) * D * a.cap;
       const int per_row = kAttnChunk / 8;
-      u32x4 r[PER_T];
+      u32x4 rk[PER_T], rv[PER_T];
 #pragma unroll
       for (int u = 0; u < PER_T; ++u) {
         const int i = gt + 256 * u;
         const int key = i / (D / 8), c8 = i % (D / 8);
-        r[u] = k0 + key < k1 ? ldg16(Kb + (size_t)(k0 + key) * D + 8 * c8) : u32x4{0, 0, 0, 0};
+        rk[u] = k0 + key < k1 ? ldg16(Kb + (size_t)(k0 + key) * D + 8 * c8) : u32x4{0, 0, 0, 0};
+        const int d = i / per_row, v8 = i % per_row;
+        const int slot = k0 + 8 * v8;
+        rv[u] = slot < k1 ? ldg16(Vb + (size_t)d * a.cap + slot) : u32x4{0, 0, 0, 0};
       }
 #pragma unroll
       for (int u = 0; u < PER_T; ++u) {
         const int i = gt + 256 * u;
         const int key = i / (D / 8), c8 = i % (D / 8);
-        *reinterpret_cast<u32x4*>(Ks + (size_t)key * kst + 8 * c8) = r[u];
-      }
-#pragma unroll
-      for (int u = 0; u < PER_T; ++u) {
-        const int i = gt + 256 * u;
+        *reinterpret_cast<u32x4*>(Ks + (size_t)key * kst + 8 * c8) = rk[u];
         const int d = i / per_row, v8 = i % per_row;
         const int slot = k0 + 8 * v8;
-        r[u] = slot < k1 ? ldg16(Vb + (size_t)d * a.cap + slot) : u32x4{0, 0, 0, 0};
-      }
-#pragma unroll
-      for (int u = 0; u < PER_T; ++u) {
-        const int i = gt + 256 * u;
-        const int d = i / per_row, v8 = i % per_row;
-        const int slot = k0 + 8 * v8;
-        u32x4 v = r[u];
+        u32x4 v = rv[u];
         if (slot < k1 && slot + 8 > k1) {
           uint32_t w[4] = {v.x, v.y, v.z, v.w};
 #pragma unroll
@@ -502,8 +530,7 @@ __device__ __forceinline__ void attn_phase(const PassArgs& a, const bf16_t* q, c
         }
         if (rvalid) {
           float* op = a.op + oi * D;
-          for (int d = g4 * 4; d < D; d += 16)
-            for (int e = 0; e < 4; ++e) st_f32(op + d + e, 0.f);
+          for (int d = g4 * 4; d < D; d += 16) st_f32x4(op + d, f32x4{0.f, 0.f, 0.f, 0.f});
         }
       } else {
         float m_run = -INFINITY, l_run = 0.f;
@@ -558,9 +585,7 @@ __device__ __forceinline__ void attn_phase(const PassArgs& a, const bf16_t* q, c
         if (rvalid) {
           float* op = a.op + oi * D;
 #pragma unroll
-          for (int dt = 0; dt < D / 16; ++dt)
-#pragma unroll
-            for (int e = 0; e < 4; ++e) st_f32(op + 16 * dt + 4 * g4 + e, o[dt][e]);
+          for (int dt = 0; dt < D / 16; ++dt) st_f32x4(op + 16 * dt + 4 * g4, o[dt]);
           if (g4 == 0) {
             st_f32(a.mp + oi, m_run);
             st_f32(a.lp + oi, l_run);
@@ -649,12 +674,28 @@ __global__ __launch_bounds__(kPassWaves * 64) void k_pass(const PassArgs* pa) {
     if (tl && threadIdx.x == 0) tl[(size_t)ev * gridDim.x + blockIdx.x] = wall_clock64();
   };
   stamp(0);
+  // Weights of the next GEMV phase's first tile, issued before the barrier
+  // that precedes it (they do not depend on the activations): the barrier,
+  // and attention and combine for the O projection, overlap their fetch.
+  u32x4 wv[kPassSteps];
+  const bool worker = (threadIdx.x >> 6) > 0;
+  auto prefetch = [&](int li, int job) {
+    if (!worker || li >= a.layers) return;
+    const GemvJob& j = a.jobs[(size_t)li * kPassJobs + job];
+    switch (job) {
+      case 0: gemv_prefetch<PE_ROPE>(j, wv); break;
+      case 1: gemv_prefetch<PE_RESID>(j, wv); break;
+      case 2: gemv_prefetch<PE_SWIGLU>(j, wv); break;
+      default: gemv_prefetch<PE_DOWN>(j, wv); break;
+    }
+  };
+  prefetch(0, 0);
   for (int li = 0; li < a.layers; ++li) {
     const GemvJob* jl = a.jobs + (size_t)li * kPassJobs;
     const int ev = 1 + li * kPassPhases * 2;
-    gemv_phase<PE_ROPE>(a, jl[0], lds, live);
+    gemv_phase<PE_ROPE>(a, jl[0], lds, live, wv);
     stamp(ev + 0);
-    grid_sync(a, ++gen, failed);
+    grid_sync(a, ++gen, failed, [&] { prefetch(li, 1); });
     stamp(ev + 1);
     attn_phase<D>(a, a.q + a.q_layer * li, a.kc + a.kv_layer * li, a.vt + a.kv_layer * li, lds);
     stamp(ev + 2);
@@ -664,23 +705,74 @@ __global__ __launch_bounds__(kPassWaves * 64) void k_pass(const PassArgs* pa) {
     stamp(ev + 4);
     grid_sync(a, ++gen, failed);
     stamp(ev + 5);
-    gemv_phase<PE_RESID>(a, jl[1], lds, live);
+    gemv_phase<PE_RESID>(a, jl[1], lds, live, wv);
     stamp(ev + 6);
-    grid_sync(a, ++gen, failed);
+    grid_sync(a, ++gen, failed, [&] { prefetch(li, 2); });
     stamp(ev + 7);
-    gemv_phase<PE_SWIGLU>(a, jl[2], lds, live);
+    gemv_phase<PE_SWIGLU>(a, jl[2], lds, live, wv);
     stamp(ev + 8);
-    grid_sync(a, ++gen, failed);
+    grid_sync(a, ++gen, failed, [&] { prefetch(li, 3); });
     stamp(ev + 9);
-    gemv_phase<PE_DOWN>(a, jl[3], lds, live);
+    gemv_phase<PE_DOWN>(a, jl[3], lds, live, wv);
     stamp(ev + 10);
-    if (li + 1 < a.layers) grid_sync(a, ++gen, failed);
+    grid_sync(a, ++gen, failed, [&] { prefetch(li + 1, 0); });
     stamp(ev + 11);
+    finish_phase(a, jl[3]);
+    if (li + 1 < a.layers) grid_sync(a, ++gen, failed);
   }
   grid_done(a);
 }
 
+// One GEMV phase as a kernel of its own (the layered path's large
+// projections): the first tile's weights are requested before x is staged.
+template <int EPI, int STEPS>
+__global__ __launch_bounds__(kPassWaves * 64) void k_gemv_job(const PassArgs* pa, const GemvJob* job) {
+  extern __shared__ __align__(16) unsigned char lds[];
+  const PassArgs& a = *pa;
+  const uint64_t live = live_rows(a);
+  u32x4 wv[STEPS];
+  if ((threadIdx.x >> 6) > 0) gemv_prefetch<EPI, STEPS>(*job, wv);
+  gemv_phase<EPI, STEPS>(a, *job, lds, live, wv);
+}
+
 }  // namespace
+
+// Step-count variants of the one-phase kernels: the smallest that covers a
+// worker wave's k-steps (fewer idle slots in the step loop).
+#define SPECDEC_JOB_KERNELS(X) X(PE_ROPE) X(PE_RESID) X(PE_SWIGLU) X(PE_DOWN)
+
+template <int EPI>
+hipError_t job_launch_steps(int steps, const PassArgs* d_args, const GemvJob* d_job, dim3 grid, size_t lds,
+                            hipStream_t s, hipEvent_t e0, hipEvent_t e1) {
+  const dim3 block(kPassWaves * 64);
+  if (steps <= 8)
+    hipExtLaunchKernelGGL((k_gemv_job<EPI, 8>), grid, block, (uint32_t)lds, s, e0, e1, 0, d_args, d_job);
+  else if (steps <= 12)
+    hipExtLaunchKernelGGL((k_gemv_job<EPI, 12>), grid, block, (uint32_t)lds, s, e0, e1, 0, d_args, d_job);
+  else if (steps <= 16)
+    hipExtLaunchKernelGGL((k_gemv_job<EPI, 16>), grid, block, (uint32_t)lds, s, e0, e1, 0, d_args, d_job);
+  else
+    return hipErrorInvalidValue;
+  return hipGetLastError();
+}
+
+hipError_t gemv_job_launch(int kind, int steps, const PassArgs* d_args, const GemvJob* d_job, int workgroups,
+                           size_t lds, hipStream_t s, hipEvent_t e0, hipEvent_t e1) {
+  const dim3 grid(workgroups);
+  switch (kind) {
+    case kJobQkv: return job_launch_steps<PE_ROPE>(steps, d_args, d_job, grid, lds, s, e0, e1);
+    case kJobO: return job_launch_steps<PE_RESID>(steps, d_args, d_job, grid, lds, s, e0, e1);
+    case kJobGateUp: return job_launch_steps<PE_SWIGLU>(steps, d_args, d_job, grid, lds, s, e0, e1);
+    case kJobDown: return job_launch_steps<PE_DOWN>(steps, d_args, d_job, grid, lds, s, e0, e1);
+    default: return hipErrorInvalidValue;
+  }
+}
+
+int gemv_job_steps(int Kd, int splits) {
+  const int T = (Kd + 31) / 32;
+  const int span = (T + splits - 1) / splits;
+  return (span + kWorkers - 1) / kWorkers;
+}
 
 void pass_build_jobs(const PassArgs& a, const LayerW* lw, const bf16_t* final_norm, GemvJob* jobs) {
   const int D = a.D;
@@ -737,6 +829,15 @@ void pass_build_jobs(const PassArgs& a, const LayerW* lw, const bf16_t* final_no
   }
 }
 
+size_t pass_gemv_lds_bytes(const PassArgs& a) {
+  auto gemv = [&](int Kd, int splits) {
+    const int T = (Kd + 31) / 32;
+    const int span = (T + splits - 1) / splits;
+    return (size_t)a.M * (span * 4 + 1) * 16 + (size_t)kWorkers * 64 * 16 + (2 * 16 * 17 + 16) * sizeof(float);
+  };
+  return std::max({gemv(a.H, 1), gemv(a.nq * a.D, 1), gemv(a.F, a.down_splits)});
+}
+
 size_t pass_lds_bytes(const PassArgs& a) {
   auto gemv = [&](int Kd, int splits) {
     const int T = (Kd + 31) / 32;
@@ -763,6 +864,15 @@ void pass_set_attributes(int lds_limit) {
   const void* fns[] = {reinterpret_cast<const void*>(&k_pass<128, 0>), reinterpret_cast<const void*>(&k_pass<128, 1>),
                        reinterpret_cast<const void*>(&k_pass<64, 0>), reinterpret_cast<const void*>(&k_pass<64, 1>)};
   for (const void* f : fns) (void)hipFuncSetAttribute(f, hipFuncAttributeMaxDynamicSharedMemorySize, lds_limit);
+#define SPECDEC_SET_JOB_ATTR(E)                                                                                  \
+  (void)hipFuncSetAttribute(reinterpret_cast<const void*>(&k_gemv_job<E, 8>),                                    \
+                            hipFuncAttributeMaxDynamicSharedMemorySize, lds_limit);                             \
+  (void)hipFuncSetAttribute(reinterpret_cast<const void*>(&k_gemv_job<E, 12>),                                   \
+                            hipFuncAttributeMaxDynamicSharedMemorySize, lds_limit);                             \
+  (void)hipFuncSetAttribute(reinterpret_cast<const void*>(&k_gemv_job<E, 16>),                                   \
+                            hipFuncAttributeMaxDynamicSharedMemorySize, lds_limit);
+  SPECDEC_JOB_KERNELS(SPECDEC_SET_JOB_ATTR)
+#undef SPECDEC_SET_JOB_ATTR
 }
 
 hipError_t pass_launch(const PassArgs* d_args, int head_dim, bool draft, int workgroups, size_t lds, hipStream_t s,

@@ -300,9 +300,12 @@ size_t carve(Ctx& c, const spec_config* cfg, const spec_seq_init* seqs, bool has
     part = std::max(part, part_elems_for(c.drf, L.M));
   }
   const bool want_pass = (cfg->flags & SPEC_FLAG_PERSISTENT) != 0;
-  c.tgt.pass_splits = want_pass ? pass_splits_for(cfg->target, L, c.ncu) : 0;
-  c.drf.pass_splits = want_pass && has_draft ? pass_splits_for(cfg->draft, L, c.ncu) : 0;
-  c.use_pass = c.tgt.pass_splits > 0 && (!has_draft || c.drf.pass_splits > 0);
+  c.tgt.pass_splits = pass_splits_for(cfg->target, L, c.ncu);
+  c.drf.pass_splits = has_draft ? pass_splits_for(cfg->draft, L, c.ncu) : 0;
+  const bool eligible = c.tgt.pass_splits > 0 && (!has_draft || c.drf.pass_splits > 0);
+  c.use_pass = want_pass && eligible;
+  if (eligible)
+    part = std::max(part, (size_t)std::max(c.tgt.pass_splits, c.drf.pass_splits) * L.M * H);
   Carver cv{base};
   c.st = cv.take<SeqState>(L.B);
   c.hist = cv.take<int32_t>((size_t)L.B * L.cap);
@@ -334,6 +337,30 @@ size_t carve(Ctx& c, const spec_config* cfg, const spec_seq_init* seqs, bool has
     c.drf.kc = cv.take<bf16_t>(c.drf.kv_layer * cfg->draft.layers);
     c.drf.vt = cv.take<bf16_t>(c.drf.kv_layer * cfg->draft.layers);
   }
+  if (eligible) {
+    c.tgt.largs_dev = cv.take<PassArgs>(1);
+    c.tgt.ljobs_dev = cv.take<GemvJob>((size_t)t.layers * kPassJobs);
+    if (has_draft) {
+      c.drf.largs_dev = cv.take<PassArgs>(1);
+      c.drf.ljobs_dev = cv.take<GemvJob>((size_t)cfg->draft.layers * kPassJobs);
+    }
+    PassArgs a{};
+    a.H = H;
+    a.M = L.M;
+    a.attn_chunk = L.chunk;
+    a.attn_splits = L.splits;
+    size_t lds = 0;
+    for (int k = 0; k < (has_draft ? 2 : 1); ++k) {
+      const spec_dims& d = k ? cfg->draft : t;
+      a.nq = d.q_heads;
+      a.nkv = d.kv_heads;
+      a.D = d.head_dim;
+      a.F = d.ffn;
+      a.down_splits = k ? c.drf.pass_splits : c.tgt.pass_splits;
+      lds = std::max(lds, pass_gemv_lds_bytes(a));
+    }
+    c.ljob_lds = lds;
+  }
   if (c.use_pass) {
     const int nl = std::max(t.layers, has_draft ? cfg->draft.layers : 0);
     const int S = std::max(c.tgt.pass_splits, c.drf.pass_splits);
@@ -350,7 +377,6 @@ size_t carve(Ctx& c, const spec_config* cfg, const spec_seq_init* seqs, bool has
     c.p_o = cv.take<bf16_t>(c.p_q_layer * nl);
     c.p_u = cv.take<bf16_t>(c.p_u_layer * nl);
     c.p_part = cv.take<float>((size_t)S * L.M * H);
-    c.p_tile_cnt = cv.take<unsigned>((size_t)H / kTile);
     c.p_bar = cv.take<unsigned>(kPassBarWords);
     if (cfg->flags & SPEC_FLAG_PASS_TIMELINE)
       c.p_timeline = cv.take<unsigned long long>((size_t)pass_timeline_events(nl) * c.ncu);
@@ -624,6 +650,11 @@ spec_status spec_init(const spec_config* cfg, const void* embed, const spec_mode
           (e = upload_pass_tables(c, c.tgt, false)) != hipSuccess ||
           (has_draft && (e = upload_pass_tables(c, c.drf, true)) != hipSuccess))
         return hip_fail(e, "layer table upload");
+    }
+    if (c.tgt.ljobs_dev) {
+      if ((e = upload_layered_jobs(c, c.tgt, false)) != hipSuccess ||
+          (has_draft && (e = upload_layered_jobs(c, c.drf, true)) != hipSuccess))
+        return hip_fail(e, "GEMV job upload");
     }
     for (int b = 0; b < c.B; ++b) {
       for (int l = 0; l < c.tgt.d.layers; ++l)
