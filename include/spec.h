@@ -43,6 +43,8 @@ extern "C" {
 #define SPEC_MAX_K      16   /* draft block size limit (the paper verifies blocks of 16) */
 #define SPEC_MAX_BATCH  16   /* sequences per context */
 #define SPEC_MAX_LAYERS 256
+#define SPEC_MAX_ROWS   160  /* batch*(K+1): rows of one verify pass */
+#define SPEC_KV_PAGE    64   /* KV slots per cache page */
 
 typedef struct spec_ctx spec_ctx;   /* opaque; owned by the library */
 
@@ -85,7 +87,7 @@ typedef struct spec_config {
                                 shares the embedding and the theta table (Sec. 4.2). */
   int32_t vocab;             /* tied embedding / LM head rows; multiple of 16 */
   int32_t K;                 /* draft block size, 0..SPEC_MAX_K (0: plain greedy decoding) */
-  int32_t batch;             /* independent sequences, 1..SPEC_MAX_BATCH */
+  int32_t batch;             /* independent sequences, 1..SPEC_MAX_BATCH; batch*(K+1) <= SPEC_MAX_ROWS */
   int32_t max_new_tokens;    /* committed-token budget per sequence, >= 1 */
   int32_t stop_token;        /* committing this token ends a sequence; -1: none */
   int32_t flags;             /* SPEC_FLAG_* */
@@ -130,7 +132,19 @@ typedef struct spec_seq_init {
   const void* const* tgt_v;           /* same shape, values */
   const void* const* drf_k;           /* host array [draft.layers]; NULL without a draft */
   const void* const* drf_v;
+  const int32_t* page_table;          /* host; NULL, or the physical cache page of each of this
+                                         sequence's spec_seq_pages() pages of SPEC_KV_PAGE slots
+                                         (slot s lives in page page_table[s / SPEC_KV_PAGE]) */
 } spec_seq_init;
+
+/* KV pages one sequence owns: ceil((prefix_len + max_new_tokens + K + 2) /
+ * SPEC_KV_PAGE).  Each model's caches are one pool of the sum of these over
+ * the batch; a page holds SPEC_KV_PAGE slots of every kv head of one layer.
+ * Either every sequence gives a page_table or none does.  Given tables must
+ * together name every pool page exactly once (a permutation of
+ * [0, pool pages)); without them sequence b owns the pages after those of
+ * sequences 0..b-1, in order.  Both models use the same table. */
+int32_t spec_seq_pages(const spec_config* cfg, const spec_seq_init* seq);
 
 /* Bytes of device workspace spec_init needs (KV caches, positions, rotary
  * table, activations, partial sums, per-sequence state). */

@@ -18,6 +18,8 @@ LIB_PATH = os.path.join(_HERE, "libspecdec.so")
 
 SPEC_MAX_K = 16
 SPEC_MAX_BATCH = 16
+SPEC_MAX_ROWS = 160
+SPEC_KV_PAGE = 64
 SPEC_FLAG_NO_GRAPHS = 1
 SPEC_FLAG_PERSISTENT = 2
 SPEC_FLAG_PASS_TIMELINE = 4
@@ -54,7 +56,7 @@ class spec_vision_block(Structure):
 class spec_seq_init(Structure):
     _fields_ = [("prefix_len", c_int32), ("n_blocks", c_int32), ("blocks", POINTER(spec_vision_block)),
                 ("pending_token", c_int32), ("tgt_k", POINTER(c_void_p)), ("tgt_v", POINTER(c_void_p)),
-                ("drf_k", POINTER(c_void_p)), ("drf_v", POINTER(c_void_p))]
+                ("drf_k", POINTER(c_void_p)), ("drf_v", POINTER(c_void_p)), ("page_table", POINTER(c_int32))]
 
 
 class SpecError(RuntimeError):
@@ -94,6 +96,8 @@ def lib():
             f = getattr(L, name)
             f.argtypes = args
             f.restype = c_int32
+        L.spec_seq_pages.argtypes = [POINTER(spec_config), POINTER(spec_seq_init)]
+        L.spec_seq_pages.restype = c_int32
         L.spec_destroy.argtypes = [P]
         L.spec_destroy.restype = None
         L.spec_last_error.argtypes = [P]
@@ -110,6 +114,13 @@ def spec_last_error(ctx) -> str:
 def _check(status: int, func: str, ctx=None) -> None:
     if status != 0:
         raise SpecError(status, func, spec_last_error(ctx))
+
+
+def spec_seq_pages(cfg: spec_config, seq: spec_seq_init) -> int:
+    n = lib().spec_seq_pages(ctypes.byref(cfg), ctypes.byref(seq))
+    if n < 0:
+        raise SpecError(1, "spec_seq_pages", "bad arguments")
+    return n
 
 
 def spec_workspace_bytes(cfg: spec_config, seqs) -> int:

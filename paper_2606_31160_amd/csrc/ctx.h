@@ -19,8 +19,7 @@ struct GemvJob;
 constexpr int kMaxRows = SPEC_MAX_K + 1;     // rows per sequence in one pass
 constexpr int kTile = 16;                    // output rows per GEMV tile (one MFMA block)
 constexpr int kKeyBlock = 32;                // keys per attention inner step
-constexpr int kAttnChunk = 64;               // keys per attention workgroup (split-KV chunk)
-constexpr int kMaxAttnChunk = 128;
+constexpr int kAttnChunk = SPEC_KV_PAGE;     // keys per attention workgroup (split-KV chunk) = one cache page
 constexpr int kGemvWaves = 16;               // waves per GEMV workgroup
 constexpr int kGemvSteps = 8;                // max 32-wide k-steps per GEMV wave
 
@@ -62,8 +61,8 @@ struct Model {
   bool flat = false;                // FlatRoPE (draft) instead of 3D M-RoPE (target)
   std::vector<LayerW> L;
   const bf16_t* final_norm = nullptr;
-  bf16_t* kc = nullptr;             // [layers][B][kv_heads][cap][head_dim], rotated keys
-  bf16_t* vt = nullptr;             // [layers][B][kv_heads][head_dim][cap], values transposed
+  bf16_t* kc = nullptr;             // [layers][pool pages][kv_heads][kAttnChunk][head_dim], rotated keys
+  bf16_t* vt = nullptr;             // [layers][pool pages][kv_heads][head_dim][kAttnChunk], values transposed
   int8_t* axis = nullptr;           // [head_dim/2] axis (0 T, 1 H, 2 W) of each rotary pair
   int s_down = 1;                  // k-splits of the down projection
   int pass_splits = 1;             // k-splits of the down projection in the persistent pass
@@ -84,7 +83,11 @@ struct TimingRec {
 struct Ctx {
   spec_config cfg{};
   int B = 1, K = 0, R = 1, M = 1, Mpad = 16, V = 0, cap = 0;
-  int attn_chunk = 128, attn_splits = 1;
+  int attn_chunk = kAttnChunk, attn_splits = 1;
+  int pps = 1;                       // page-table entries per sequence (cap / kAttnChunk)
+  int pool = 0;                      // cache pages per layer
+  std::vector<int32_t> pt_host;      // [B][pps] physical page of each sequence page
+  std::vector<int32_t> npages;       // [B] pages each sequence owns
   int ncu = 256;                     // compute units of the device (persistent GEMV grids)
   hipStream_t stream = nullptr;      // caller's stream
   hipStream_t cap_stream = nullptr;  // private stream used only for graph capture
@@ -93,6 +96,7 @@ struct Ctx {
   // workspace carve-out
   SeqState* st = nullptr;           // [B]
   int32_t* hist = nullptr;          // [B][cap] token at each index >= prefix_len
+  int32_t* pt = nullptr;            // [B][pps] page table (slot s of sequence b: page pt[b][s / kAttnChunk])
   int32_t* pos3 = nullptr;          // [B][3][cap] target rotary positions
   float2* cs = nullptr;             // [cap][head_dim/2] (cos, sin) of theta_d * p
   float* x = nullptr;               // [Mpad][hidden] residual stream

@@ -45,13 +45,16 @@ __global__ void k_zero(u32x4* p, size_t n) {
 // Prompt keys/values -> caches.  One thread per rotary pair of one slot of one
 // kv head.  Keys are rotated with the model's positions (Eq. rope-3d with the
 // axis assignment of Eq. axis-assign for the target; the slot index for the
-// draft, Eq. flatrope-proj); values are stored transposed ([head_dim][cap]).
+// draft, Eq. flatrope-proj); values are stored transposed.  Slot s lives in
+// page pt[s / kAttnChunk] at offset s % kAttnChunk; a page holds keys
+// [nkv][kAttnChunk][D] and values [nkv][D][kAttnChunk].
 // ---------------------------------------------------------------------------
 struct PrefixArgs {
   const bf16_t* k_pre;   // [P][nkv][D]
   const bf16_t* v;       // [P][nkv][D]
-  bf16_t* kc;            // this layer & sequence: [nkv][cap][D]
-  bf16_t* vt;            // [nkv][D][cap]
+  bf16_t* kc;            // this layer's key pool
+  bf16_t* vt;            // this layer's value pool
+  const int32_t* pt;     // this sequence's page table
   const int32_t* pos3;   // this sequence: [3][cap]
   const float2* cs;      // [cap][D/2]
   const int8_t* axis;    // [D/2]
@@ -71,9 +74,11 @@ __global__ void k_prefix_kv(PrefixArgs a) {
     const int p = a.flat ? s : a.pos3[a.axis[d] * a.cap + s];
     const float2 c = a.cs[(size_t)p * half + d];
     const float re = e * c.x - o * c.y, ro = e * c.y + o * c.x;
-    *reinterpret_cast<uint32_t*>(a.kc + ((size_t)h * a.cap + s) * a.D + 2 * d) = pack2(re, ro);
-    a.vt[((size_t)h * a.D + 2 * d) * a.cap + s] = a.v[src];
-    a.vt[((size_t)h * a.D + 2 * d + 1) * a.cap + s] = a.v[src + 1];
+    const size_t pg = (size_t)a.pt[s / kAttnChunk] * a.nkv + h;
+    const int off = s % kAttnChunk;
+    *reinterpret_cast<uint32_t*>(a.kc + (pg * kAttnChunk + off) * a.D + 2 * d) = pack2(re, ro);
+    a.vt[(pg * a.D + 2 * d) * kAttnChunk + off] = a.v[src];
+    a.vt[(pg * a.D + 2 * d + 1) * kAttnChunk + off] = a.v[src + 1];
   }
 }
 
@@ -217,9 +222,10 @@ struct GemvArgs {
   float* out;            // EPI_STORE: [splits][M][N]
   // EPI_ROPE
   bf16_t* q;             // [M][nq*D]
-  bf16_t *kc, *vt;       // layer bases [B][nkv][cap][D], [B][nkv][D][cap]
+  bf16_t *kc, *vt;       // layer bases of the paged key / value pools
+  const int32_t* pt;     // [B][pps] page tables
   const float2* rcs;     // [Mpad][D/2] (cos, sin) per row
-  int nq, nkv, D, cap;
+  int nq, nkv, D, pps;
   // EPI_RESID
   float* x32;            // [M][N] residual stream
   const bf16_t* gain;    // [N] gain of the next RMSNorm
@@ -371,15 +377,15 @@ __global__ __launch_bounds__(NW * 64) void k_gemv(GemvArgs a) {
         if (head < a.nq) {
           *reinterpret_cast<uint32_t*>(a.q + ((size_t)m * a.nq + head) * a.D + 2 * d) = pack2(re, ro);
         } else {
-          const int h = head - a.nq;
-          *reinterpret_cast<uint32_t*>(a.kc + (((size_t)b * a.nkv + h) * a.cap + slot) * a.D + 2 * d) =
+          const size_t pg = (size_t)a.pt[b * a.pps + slot / kAttnChunk] * a.nkv + (head - a.nq);
+          *reinterpret_cast<uint32_t*>(a.kc + (pg * kAttnChunk + slot % kAttnChunk) * a.D + 2 * d) =
               pack2(re, ro);
         }
       } else {
-        const int h = head - a.nq - a.nkv;
-        bf16_t* vp = a.vt + (((size_t)b * a.nkv + h) * a.D + 2 * d) * a.cap + slot;
+        const size_t pg = (size_t)a.pt[b * a.pps + slot / kAttnChunk] * a.nkv + (head - a.nq - a.nkv);
+        bf16_t* vp = a.vt + (pg * a.D + 2 * d) * kAttnChunk + slot % kAttnChunk;
         vp[0] = f2bf(e);
-        vp[a.cap] = f2bf(o);
+        vp[kAttnChunk] = f2bf(o);
       }
     }
   } else if constexpr (EPI == EPI_RESID) {
@@ -659,8 +665,8 @@ __global__ __launch_bounds__(256) void k_down_finish(FinishArgs p) {
 //
 // grid (splits, kv_heads * row_blocks, B); a workgroup owns one kv head, up to
 // 64 query rows (row = j*G + g: new row j, q head kvh*G + g) and the key range
-// [split*chunk, (split+1)*chunk) clipped to the keys that exist.  Wave w owns
-// query rows 16w..16w+15.
+// [split*chunk, (split+1)*chunk) clipped to the keys that exist: one cache
+// page (chunk = kAttnChunk).  Wave w owns query rows 16w..16w+15.
 //
 // Scores are computed transposed, S^T = K Q^T, so that lane l owns query row
 // l&15: A = K tile (lane: key kb + (l&15), 8 dims), B = Q^T (lane: row l&15,
@@ -675,12 +681,13 @@ __global__ __launch_bounds__(256) void k_down_finish(FinishArgs p) {
 struct AttnArgs {
   const SeqState* st;
   const bf16_t* q;       // [Mpad][nq][D]
-  const bf16_t* kc;      // layer base [B][nkv][cap][D]
-  const bf16_t* vt;      // layer base [B][nkv][D][cap]
+  const bf16_t* kc;      // layer base of the key pool [pages][nkv][kAttnChunk][D]
+  const bf16_t* vt;      // layer base of the value pool [pages][nkv][D][kAttnChunk]
+  const int32_t* pt;     // [B][pps] page tables
   float* op;             // [splits][B][nq][R][D]
   float* mp;             // [splits][B][nq][R]
   float* lp;
-  int nq, nkv, G, R, B, cap, chunk, row_blocks;
+  int nq, nkv, G, R, B, pps, chunk, row_blocks;
   float scale_log2;      // log2(e) / sqrt(D)
 };
 
@@ -735,9 +742,10 @@ __global__ __launch_bounds__(256) void k_attn(AttnArgs a) {
   bf16_t* Ks = reinterpret_cast<bf16_t*>(lds);
   bf16_t* Vs = Ks + (size_t)a.chunk * kst;
   {
-    constexpr int PER_T = kMaxAttnChunk * D / 8 / 256;   // 16-byte vectors per thread and operand
-    const bf16_t* Kb = a.kc + ((size_t)b * a.nkv + kvh) * a.cap * D;
-    const bf16_t* Vb = a.vt + ((size_t)b * a.nkv + kvh) * D * a.cap;
+    constexpr int PER_T = kAttnChunk * D / 8 / 256;   // 16-byte vectors per thread and operand
+    const size_t pg = (size_t)a.pt[b * a.pps + split] * a.nkv + kvh;
+    const bf16_t* Kb = a.kc + pg * kAttnChunk * D;
+    const bf16_t* Vb = a.vt + pg * D * kAttnChunk;
     const int nvec = a.chunk * (D / 8);                   // per operand
     const int per_row = a.chunk / 8;
     u32x4 kr[PER_T], vr[PER_T];
@@ -745,10 +753,10 @@ __global__ __launch_bounds__(256) void k_attn(AttnArgs a) {
     for (int u = 0; u < PER_T; ++u) {
       const int i = threadIdx.x + 256 * u;
       const int key = i / (D / 8), c8 = i % (D / 8);
-      kr[u] = (i < nvec && k0 + key < k1) ? ld16(Kb + (size_t)(k0 + key) * D + 8 * c8) : u32x4{0, 0, 0, 0};
+      kr[u] = (i < nvec && k0 + key < k1) ? ld16(Kb + (size_t)key * D + 8 * c8) : u32x4{0, 0, 0, 0};
       const int d = i / per_row, v8 = i % per_row;
       const int slot = k0 + 8 * v8;
-      vr[u] = (i < nvec && slot < k1) ? ld16(Vb + (size_t)d * a.cap + slot) : u32x4{0, 0, 0, 0};
+      vr[u] = (i < nvec && slot < k1) ? ld16(Vb + (size_t)d * kAttnChunk + 8 * v8) : u32x4{0, 0, 0, 0};
     }
 #pragma unroll
     for (int u = 0; u < PER_T; ++u) {
@@ -1184,14 +1192,15 @@ hipError_t run_layer(Ctx& c, Model& m, int li, const bf16_t* next_gain, bool sel
     g.nq = nq;
     g.nkv = nkv;
     g.D = D;
-    g.cap = c.cap;
+    g.pt = c.pt;
+    g.pps = c.pps;
     CK((gemv_launch<EPI_ROPE, 1>(c, g, SPEC_KERNEL_QKV, gemv_bytes(g.N, H, M, 2.0))));
   }
   // attention
   {
     const int G = nq / nkv;
     const int rb = (c.R * G + 63) / 64;
-    AttnArgs p{c.st, c.q, kc, vt, c.op, c.mp, c.lp, nq, nkv, G, c.R, c.B, c.cap, c.attn_chunk, rb,
+    AttnArgs p{c.st, c.q, kc, vt, c.pt, c.op, c.mp, c.lp, nq, nkv, G, c.R, c.B, c.pps, c.attn_chunk, rb,
                kLog2e / sqrtf((float)D)};
     dim3 grid(c.attn_splits, nkv * rb, c.B);
     {
@@ -1286,9 +1295,9 @@ void init_kernel_attributes() {
   done = true;
   pass_set_attributes(gemv_lds_limit());
   (void)hipFuncSetAttribute(reinterpret_cast<const void*>(&k_attn<128>), hipFuncAttributeMaxDynamicSharedMemorySize,
-                            (int)attn_lds_bytes(kMaxAttnChunk, 128));
+                            (int)attn_lds_bytes(kAttnChunk, 128));
   (void)hipFuncSetAttribute(reinterpret_cast<const void*>(&k_attn<64>), hipFuncAttributeMaxDynamicSharedMemorySize,
-                            (int)attn_lds_bytes(kMaxAttnChunk, 64));
+                            (int)attn_lds_bytes(kAttnChunk, 64));
   set_lds_limit_p<EPI_STORE, 1>();
   set_lds_limit_p<EPI_STORE, 2>();
   set_lds_limit_p<EPI_STORE, 3>();
@@ -1417,11 +1426,11 @@ hipError_t launch_prefix_kv(Ctx& c, Model& m, int layer, int b, int prefix_len, 
                             const bf16_t* v) {
   const spec_dims& d = m.d;
   const size_t kvl = m.kv_layer;
-  const size_t per_seq = (size_t)d.kv_heads * c.cap * d.head_dim;
   PrefixArgs p{k_pre,
                v,
-               m.kc + kvl * layer + per_seq * b,
-               m.vt + kvl * layer + per_seq * b,
+               m.kc + kvl * layer,
+               m.vt + kvl * layer,
+               c.pt + (size_t)b * c.pps,
                c.pos3 + (size_t)b * 3 * c.cap,
                c.cs,
                m.axis,
@@ -1458,7 +1467,8 @@ PassArgs pass_args(Ctx& c, Model& m, bool draft) {
   a.B = c.B;
   a.rps = c.R;
   a.mpad = c.Mpad;
-  a.cap = c.cap;
+  a.pt = c.pt;
+  a.pps = c.pps;
   a.eps = d.rms_eps;
   a.scale_log2 = kLog2e / sqrtf((float)d.head_dim);
   a.lw = m.lw_dev;

@@ -35,14 +35,15 @@ enum { kJobQkv = 0, kJobO = 1, kJobGateUp = 2, kJobDown = 3 };
 struct PassArgs {
   SeqState* st;
   int layers, H, nq, nkv, D, F;
-  int M, R, B, rps, mpad, cap;
+  int M, R, B, rps, mpad, pps;
   float eps, scale_log2;
   const LayerW* lw;          // [layers] device copy of the layer weight pointers
   const GemvJob* jobs;       // [layers][kPassJobs]
   const bf16_t* final_norm;
   int select_last;           // draft pass: the last layer keeps each sequence's last row only
-  // caches (layer 0 bases; kv_layer elements per layer)
+  // paged caches (layer 0 bases; kv_layer elements per layer) and page tables
   bf16_t *kc, *vt;
+  const int32_t* pt;         // [B][pps]
   size_t kv_layer;
   const float2* rcs;         // [Mpad][D/2] per-row (cos, sin)
   // activations: x is shared; the others are per layer (stride in elements)

@@ -350,14 +350,14 @@ __device__ __forceinline__ void gemv_phase(const PassArgs& a, const GemvJob& j, 
           if (head < a.nq) {
             st_u32(j.q + ((size_t)m * a.nq + head) * D + 2 * d, pack2(re, ro));
           } else {
-            const int h = head - a.nq;
-            st_u32(j.kc + (((size_t)b * a.nkv + h) * a.cap + slot) * D + 2 * d, pack2(re, ro));
+            const size_t pg = (size_t)ldg(a.pt + b * a.pps + slot / kAttnChunk) * a.nkv + (head - a.nq);
+            st_u32(j.kc + (pg * kAttnChunk + slot % kAttnChunk) * D + 2 * d, pack2(re, ro));
           }
         } else {
-          const int h = head - a.nq - a.nkv;
-          bf16_t* vp = j.vt + (((size_t)b * a.nkv + h) * D + 2 * d) * a.cap + slot;
+          const size_t pg = (size_t)ldg(a.pt + b * a.pps + slot / kAttnChunk) * a.nkv + (head - a.nq - a.nkv);
+          bf16_t* vp = j.vt + (pg * D + 2 * d) * kAttnChunk + slot % kAttnChunk;
           st_u16(vp, f2bf(e));
-          st_u16(vp + a.cap, f2bf(o));
+          st_u16(vp + kAttnChunk, f2bf(o));
         }
       }
     } else if constexpr (EPI == PE_RESID) {
@@ -490,18 +490,19 @@ __device__ __forceinline__ void attn_phase(const PassArgs& a, const bf16_t* q, c
       // all of the thread's key and value loads are issued before its first
       // LDS store, so their latencies overlap
       constexpr int PER_T = kAttnChunk * D / 8 / 256;
-      const bf16_t* Kb = kc + ((size_t)b * a.nkv + kvh) * a.cap * D;
-      const bf16_t* Vb = vt + ((size_t)b * a.nkv + kvh) * D * a.cap;
+      const size_t pg = (size_t)ldg(a.pt + b * a.pps + split) * a.nkv + kvh;
+      const bf16_t* Kb = kc + pg * kAttnChunk * D;
+      const bf16_t* Vb = vt + pg * D * kAttnChunk;
       const int per_row = kAttnChunk / 8;
       u32x4 rk[PER_T], rv[PER_T];
 #pragma unroll
       for (int u = 0; u < PER_T; ++u) {
         const int i = gt + 256 * u;
         const int key = i / (D / 8), c8 = i % (D / 8);
-        rk[u] = k0 + key < k1 ? ldg16(Kb + (size_t)(k0 + key) * D + 8 * c8) : u32x4{0, 0, 0, 0};
+        rk[u] = k0 + key < k1 ? ldg16(Kb + (size_t)key * D + 8 * c8) : u32x4{0, 0, 0, 0};
         const int d = i / per_row, v8 = i % per_row;
         const int slot = k0 + 8 * v8;
-        rv[u] = slot < k1 ? ldg16(Vb + (size_t)d * a.cap + slot) : u32x4{0, 0, 0, 0};
+        rv[u] = slot < k1 ? ldg16(Vb + (size_t)d * kAttnChunk + 8 * v8) : u32x4{0, 0, 0, 0};
       }
 #pragma unroll
       for (int u = 0; u < PER_T; ++u) {

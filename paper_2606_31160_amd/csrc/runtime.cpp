@@ -69,6 +69,11 @@ bool check_dims(const spec_dims& d, bool is_target, std::string& err, const char
   return true;
 }
 
+// KV pages of one sequence (include/spec.h, spec_seq_pages).
+int seq_pages(const spec_config* cfg, const spec_seq_init& s) {
+  return (int)((align_up((size_t)s.prefix_len + cfg->max_new_tokens + cfg->K + 2, kAttnChunk)) / kAttnChunk);
+}
+
 bool check_config(const spec_config* cfg, const spec_seq_init* seqs, bool has_draft, std::string& err) {
   if (!cfg || !seqs) {
     err = "null config or sequences";
@@ -168,6 +173,37 @@ bool check_config(const spec_config* cfg, const spec_seq_init* seqs, bool has_dr
         }
     }
   }
+  // page tables: all or none; together a permutation of the pool's pages
+  int given = 0;
+  long long pool = 0;
+  for (int b = 0; b < cfg->batch; ++b) {
+    given += seqs[b].page_table != nullptr;
+    pool += seq_pages(cfg, seqs[b]);
+  }
+  if (given != 0 && given != cfg->batch) {
+    err = "either every sequence gives a page_table or none does";
+    return false;
+  }
+  if (pool >= (1ll << 31) / kAttnChunk) {
+    err = "too many KV pages";
+    return false;
+  }
+  if (given) {
+    std::vector<char> used((size_t)pool, 0);
+    for (int b = 0; b < cfg->batch; ++b) {
+      const int n = seq_pages(cfg, seqs[b]);
+      for (int i = 0; i < n; ++i) {
+        const int32_t p = seqs[b].page_table[i];
+        if (p < 0 || p >= pool || used[p]) {
+          char buf[160];
+          snprintf(buf, sizeof buf, "sequence %d: page_table[%d] = %d is out of range or used twice", b, i, p);
+          err = buf;
+          return false;
+        }
+        used[p] = 1;
+      }
+    }
+  }
   return true;
 }
 
@@ -194,8 +230,9 @@ bool check_weights(const spec_model_weights* w, const spec_dims& d, std::string&
 // ---- layout -------------------------------------------------------------------
 
 struct Layout {
-  int B, K, R, M, Mpad, V, cap, chunk, splits;
+  int B, K, R, M, Mpad, V, cap, chunk, splits, pool;
 };
+
 
 Layout make_layout(const spec_config* cfg, const spec_seq_init* seqs) {
   Layout L{};
@@ -207,13 +244,11 @@ Layout make_layout(const spec_config* cfg, const spec_seq_init* seqs) {
   L.V = cfg->vocab;
   int maxP = 0;
   for (int b = 0; b < L.B; ++b) maxP = std::max(maxP, seqs[b].prefix_len);
-  L.cap = (int)align_up((size_t)maxP + cfg->max_new_tokens + cfg->K + 2, 64);
+  L.cap = (int)align_up((size_t)maxP + cfg->max_new_tokens + cfg->K + 2, kAttnChunk);
   L.chunk = kAttnChunk;
-  if (const char* e = getenv("SPECDEC_ATTN_CHUNK")) {
-    const int v = atoi(e);
-    if (v >= 32 && v <= kMaxAttnChunk && v % 32 == 0) L.chunk = v;
-  }
-  L.splits = (L.cap + L.chunk - 1) / L.chunk;
+  L.splits = L.cap / L.chunk;
+  L.pool = 0;
+  for (int b = 0; b < L.B; ++b) L.pool += seq_pages(cfg, seqs[b]);
   return L;
 }
 
@@ -278,6 +313,8 @@ size_t carve(Ctx& c, const spec_config* cfg, const spec_seq_init* seqs, bool has
   c.Mpad = L.Mpad;
   c.V = L.V;
   c.cap = L.cap;
+  c.pps = L.splits;
+  c.pool = L.pool;
   c.attn_chunk = L.chunk;
   c.ncu = num_cus();
   c.attn_splits = L.splits;
@@ -309,6 +346,7 @@ size_t carve(Ctx& c, const spec_config* cfg, const spec_seq_init* seqs, bool has
   Carver cv{base};
   c.st = cv.take<SeqState>(L.B);
   c.hist = cv.take<int32_t>((size_t)L.B * L.cap);
+  c.pt = cv.take<int32_t>((size_t)L.B * L.splits);
   c.pos3 = cv.take<int32_t>((size_t)L.B * 3 * L.cap);
   c.cs = cv.take<float2>((size_t)L.cap * (D / 2));
   c.tgt.axis = cv.take<int8_t>(D / 2);
@@ -329,11 +367,11 @@ size_t carve(Ctx& c, const spec_config* cfg, const spec_seq_init* seqs, bool has
   c.amax_v = cv.take<float>((size_t)(L.V / kTile) * L.Mpad);
   c.amax_i = cv.take<int32_t>((size_t)(L.V / kTile) * L.Mpad);
   c.logits = cv.take<bf16_t>((size_t)L.Mpad * L.V);
-  c.tgt.kv_layer = (size_t)L.B * t.kv_heads * L.cap * D;
+  c.tgt.kv_layer = (size_t)L.pool * t.kv_heads * kAttnChunk * D;
   c.tgt.kc = cv.take<bf16_t>(c.tgt.kv_layer * t.layers);
   c.tgt.vt = cv.take<bf16_t>(c.tgt.kv_layer * t.layers);
   if (has_draft) {
-    c.drf.kv_layer = (size_t)L.B * cfg->draft.kv_heads * L.cap * D;
+    c.drf.kv_layer = (size_t)L.pool * cfg->draft.kv_heads * kAttnChunk * D;
     c.drf.kc = cv.take<bf16_t>(c.drf.kv_layer * cfg->draft.layers);
     c.drf.vt = cv.take<bf16_t>(c.drf.kv_layer * cfg->draft.layers);
   }
@@ -510,6 +548,11 @@ spec_status guarded(spec_ctx* ctx, F f) {
 
 extern "C" {
 
+int32_t spec_seq_pages(const spec_config* cfg, const spec_seq_init* seq) {
+  if (!cfg || !seq || seq->prefix_len < 1 || cfg->max_new_tokens < 1 || cfg->K < 0) return -1;
+  return seq_pages(cfg, *seq);
+}
+
 spec_status spec_workspace_bytes(const spec_config* cfg, const spec_seq_init* seqs, size_t* bytes) {
   if (!cfg || !seqs || !bytes) return SPEC_E_INVAL;
   try {
@@ -614,6 +657,15 @@ spec_status spec_init(const spec_config* cfg, const void* embed, const spec_mode
     std::vector<int8_t> ax_t(half), ax_d(half);
     build_axis(cfg->target, false, ax_t.data());
     build_axis(cfg->draft, true, ax_d.data());
+    c.pt_host.assign((size_t)c.B * c.pps, 0);
+    c.npages.assign(c.B, 0);
+    for (int b = 0, next = 0; b < c.B; ++b) {
+      const int n = seq_pages(cfg, seqs[b]);
+      c.npages[b] = n;
+      for (int i = 0; i < n; ++i)
+        c.pt_host[(size_t)b * c.pps + i] = seqs[b].page_table ? seqs[b].page_table[i] : next + i;
+      next += n;
+    }
     std::vector<SeqState> st(c.B);
     std::vector<int32_t> hist((size_t)c.B * c.cap, 0);
     for (int b = 0; b < c.B; ++b) {
@@ -634,6 +686,8 @@ spec_status spec_init(const spec_config* cfg, const void* embed, const spec_mode
     hipError_t e;
     if ((e = launch_zero(c, workspace, need)) != hipSuccess) return hip_fail(e, "workspace clear");
     if ((e = hipMemcpyAsync(c.pos3, pos.data(), pos.size() * 4, hipMemcpyHostToDevice, stream)) != hipSuccess ||
+        (e = hipMemcpyAsync(c.pt, c.pt_host.data(), c.pt_host.size() * 4, hipMemcpyHostToDevice, stream)) !=
+            hipSuccess ||
         (e = hipMemcpyAsync(c.cs, cs.data(), cs.size() * sizeof(float2), hipMemcpyHostToDevice, stream)) !=
             hipSuccess ||
         (e = hipMemcpyAsync(c.tgt.axis, ax_t.data(), half, hipMemcpyHostToDevice, stream)) != hipSuccess ||
@@ -812,26 +866,27 @@ spec_status spec_debug_kv(spec_ctx* ctx, int32_t b, int32_t model, int32_t layer
     if (model != 0 && !(model == 1 && c.has_draft)) return set_err(c, SPEC_E_INVAL, "bad model");
     Model& m = model == 0 ? c.tgt : c.drf;
     if (b < 0 || b >= c.B || layer < 0 || layer >= m.d.layers || (which != 0 && which != 1) || pos0 < 0 ||
-        npos < 0 || pos0 + npos > c.cap || !host_out)
+        npos < 0 || pos0 + npos > c.npages[b] * kAttnChunk || !host_out)
       return set_err(c, SPEC_E_INVAL, "bad arguments");
     HIPCHK(c, hipStreamSynchronize(c.stream), "sync");
     const int nkv = m.d.kv_heads, D = m.d.head_dim;
     bf16_t* out = static_cast<bf16_t*>(host_out);
-    const size_t per_seq = (size_t)nkv * c.cap * D;
-    std::vector<bf16_t> tmp((size_t)npos * D);
-    for (int h = 0; h < nkv; ++h) {
-      if (which == 0) {
-        const bf16_t* src = m.kc + m.kv_layer * layer + per_seq * b + ((size_t)h * c.cap + pos0) * D;
-        HIPCHK(c, hipMemcpy(tmp.data(), src, tmp.size() * 2, hipMemcpyDeviceToHost), "kv read");
-        for (int s = 0; s < npos; ++s) memcpy(out + ((size_t)s * nkv + h) * D, tmp.data() + (size_t)s * D, D * 2);
-      } else {
-        const bf16_t* src = m.vt + m.kv_layer * layer + per_seq * b + (size_t)h * D * c.cap + pos0;
-        HIPCHK(c, hipMemcpy2D(tmp.data(), (size_t)npos * 2, src, (size_t)c.cap * 2, (size_t)npos * 2, D,
-                              hipMemcpyDeviceToHost),
-               "kv read");
-        for (int s = 0; s < npos; ++s)
-          for (int d = 0; d < D; ++d) out[((size_t)s * nkv + h) * D + d] = tmp[(size_t)d * npos + s];
-      }
+    // one page (all kv heads) at a time: keys [nkv][page][D], values [nkv][D][page]
+    const size_t page_elems = (size_t)nkv * kAttnChunk * D;
+    std::vector<bf16_t> tmp(page_elems);
+    for (int s = pos0; s < pos0 + npos;) {
+      const int pi = s / kAttnChunk, off = s % kAttnChunk;
+      const int n = std::min(kAttnChunk - off, pos0 + npos - s);
+      const bf16_t* src = (which == 0 ? m.kc : m.vt) + m.kv_layer * layer +
+                          (size_t)c.pt_host[(size_t)b * c.pps + pi] * page_elems;
+      HIPCHK(c, hipMemcpy(tmp.data(), src, page_elems * 2, hipMemcpyDeviceToHost), "kv read");
+      for (int i = 0; i < n; ++i)
+        for (int h = 0; h < nkv; ++h)
+          for (int d = 0; d < D; ++d)
+            out[((size_t)(s - pos0 + i) * nkv + h) * D + d] =
+                which == 0 ? tmp[((size_t)h * kAttnChunk + off + i) * D + d]
+                           : tmp[((size_t)h * D + d) * kAttnChunk + off + i];
+      s += n;
     }
     return SPEC_OK;
   });

@@ -25,11 +25,14 @@ class Session:
 
     source='host'   weights drawn with numpy on the host (small shapes)
     source='device' weights drawn on the GPU with torch's seeded generator
+    page_seed       None: each sequence's KV pages follow the previous
+                    sequence's; an int: a seeded random permutation of the
+                    page pool is handed over as the sequences' page tables
     """
 
     def __init__(self, w, source: str = "host", flags: int = 0, with_draft: bool = True,
                  K: Optional[int] = None, max_new_tokens: Optional[int] = None, stop_token: Optional[int] = None,
-                 provider=None):
+                 provider=None, page_seed: Optional[int] = None):
         torch = _require_gpu()
         import workloads as W
         self.torch = torch
@@ -88,6 +91,18 @@ class Session:
             if self.has_draft:
                 s.drf_k, s.drf_v = arr(kv["draft"][0]), arr(kv["draft"][1])
             self._keep += [blocks, s.tgt_k, s.tgt_v]
+        if page_seed is not None:
+            import ctypes
+            npg = [B.spec_seq_pages(cfg, seqs[b]) for b in range(self.B)]
+            perm = np.random.default_rng(page_seed).permutation(sum(npg)).astype(np.int32)
+            self.page_tables = []
+            off = 0
+            for b in range(self.B):
+                arr = (ctypes.c_int32 * npg[b])(*perm[off:off + npg[b]].tolist())
+                off += npg[b]
+                seqs[b].page_table = arr
+                self.page_tables.append(arr)
+            self._keep += self.page_tables
         self.seqs = seqs
         self.ws_bytes = B.spec_workspace_bytes(cfg, seqs)
         self.ws = torch.empty(self.ws_bytes, dtype=torch.uint8, device=self.dev)

@@ -31,7 +31,7 @@ def test_struct_sizes_match_c_layout():
     # 64-bit SysV layout of the header's structs
     assert ctypes.sizeof(B.spec_dims) == 48
     assert ctypes.sizeof(B.spec_config) == 120
-    assert ctypes.sizeof(B.spec_seq_init) == 56
+    assert ctypes.sizeof(B.spec_seq_init) == 64
     assert ctypes.sizeof(B.spec_layer_weights) == 72
 
 
@@ -163,3 +163,35 @@ def test_calls_on_null_context():
     assert L.spec_commit(None, None, None, None, None) == 1
     assert L.spec_sync(None, None) == 1
     L.spec_destroy(None)
+
+
+def test_page_tables_validated_on_host():
+    w = W.get("C1")
+    cfg = _cfg(w, batch=2)
+    seqs, keep = _seqs(w, cfg, blocks=_blocks(w))
+    n = B.spec_seq_pages(cfg, seqs[0])
+    # prompt + token budget + K + 2 slots, in pages of 64
+    assert n == -(-(w.seqs[0].prefix_len + 20 + w.K + 2) // 64)
+    plain = B.spec_workspace_bytes(cfg, seqs)
+
+    def tables(t0, t1):
+        a0 = (ctypes.c_int32 * len(t0))(*t0)
+        a1 = (ctypes.c_int32 * len(t1))(*t1)
+        keep.extend([a0, a1])
+        seqs[0].page_table, seqs[1].page_table = a0, a1
+
+    perm = list(range(2 * n))[::-1]
+    tables(perm[:n], perm[n:])
+    assert B.spec_workspace_bytes(cfg, seqs) == plain     # same pool, another order
+    for t0, t1, needle in [(perm[:n], perm[:n], "used twice"),
+                           (perm[:n - 1] + [2 * n], perm[n:], "out of range"),
+                           (perm[:n - 1] + [-1], perm[n:], "out of range")]:
+        tables(t0, t1)
+        with pytest.raises(B.SpecError) as e:
+            B.spec_workspace_bytes(cfg, seqs)
+        assert needle in str(e.value)
+    tables(perm[:n], perm[n:])
+    seqs[1].page_table = None
+    with pytest.raises(B.SpecError) as e:
+        B.spec_workspace_bytes(cfg, seqs)
+    assert "every sequence" in str(e.value)

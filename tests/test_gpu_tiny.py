@@ -311,6 +311,26 @@ def test_batch_of_two(c1):
     S.check_argmax_rows(spec[1], z)
 
 
+def test_shuffled_page_tables(c1):
+    """Caches in a seeded random permutation of the page pool (caller page
+    tables) give the same tokens and bit-identical cached keys and values as
+    the default in-order pages."""
+    w = c1[0]
+    lay2 = W.SeqLayout(260, (W.VisionBlock(20, 2, 8, 8),))
+    wb = w.with_(seqs=(w.seqs[0], lay2), p_accept=(0.8, 0.8))
+    plain, paged = _session(wb), _session(wb, page_seed=5)
+    assert run_batch(plain, "draft") == run_batch(paged, "draft")
+    for b in range(wb.batch):
+        st = plain.state(b)
+        assert st == paged.state(b)
+        for model, shape, n in ((0, wb.target, st["seq_len"]), (1, wb.draft, st["draft_len"])):
+            for li in range(shape.layers):
+                for which in (0, 1):
+                    assert np.array_equal(plain.kv(b, model, li, which, 0, n), paged.kv(b, model, li, which, 0, n))
+    plain.close()
+    paged.close()
+
+
 def test_block_of_16_with_two_row_blocks(c1):
     # K = 16 (M = 17 rows, two 16-row MFMA blocks in every GEMV) and 4 q heads
     # per kv head (68 query rows per kv head: two attention row blocks).
