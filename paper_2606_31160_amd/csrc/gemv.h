@@ -1,0 +1,67 @@
+// Arguments of the weight-streaming GEMV kernels (kernels.hip) and of the
+// batched-row GEMM (gemm.hip), and the consumer steps their epilogues fuse.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "ctx.h"
+
+namespace specdec {
+
+enum {
+  EPI_STORE = 0,   // out[split][m][n]: k-split partial sums (down projection)
+  EPI_ROPE = 1,    // y/rms; rotation of q/k at the row's position, q store, K / V^T cache append (QKV)
+  EPI_RESID = 2,   // x += y; xg = bf16(x * g); sums of x^2 (O projection)
+  EPI_SWIGLU = 3,  // y/rms; half-tiles (8 gate rows, 8 up rows): u = silu(gate) * up (gate/up)
+  EPI_ARGMAX = 4   // y/rms; per-tile (max, index) of the logits, optional bf16 logits (LM head)
+};
+
+struct GemvArgs {
+  const bf16_t* w[3];
+  int row0[3];           // first output row of each weight segment (multiples of 16)
+  int nseg;
+  int N, Kd;
+  const bf16_t* x;       // [M][ldx]
+  int ldx, M, splits;
+  const SeqState* st;
+  int rps;               // rows per sequence
+  int mpad;              // row stride of ss / amax
+  const float* ss_in;    // [H/16][mpad] sums of x^2 of the input rows (ROPE, SWIGLU, ARGMAX)
+  int H;                 // row length those sums cover
+  float eps;
+  float* out;            // EPI_STORE: [splits][M][N]
+  // EPI_ROPE
+  bf16_t* q;             // [M][nq*D]
+  bf16_t *kc, *vt;       // layer bases of the paged key / value pools
+  const int32_t* pt;     // [B][pps] page tables
+  const float2* rcs;     // [Mpad][D/2] (cos, sin) per row
+  int nq, nkv, D, pps;
+  // EPI_RESID
+  float* x32;            // [M][N] residual stream
+  const bf16_t* gain;    // [N] gain of the next RMSNorm
+  bf16_t* xg;            // [M][N] bf16(x * gain)
+  float* ss_out;         // [N/16][mpad] sums of x^2
+  // EPI_SWIGLU
+  bf16_t* u;             // [M][N/2]
+  // EPI_ARGMAX
+  float* amax_v;         // [N/16][mpad]
+  int32_t* amax_i;
+  bf16_t* logits;        // [M][N]
+  int allow_logits;
+};
+
+// Passes of up to kThinRows rows use the thin GEMV kernels (kernels.hip);
+// larger passes (up to SPEC_MAX_ROWS) the batched-row GEMM (gemm.hip).
+constexpr int kThinRows = 64;
+constexpr int kGemmWaves = 4;   // waves per GEMM workgroup, one 16-column output tile each
+
+// Dynamic LDS bytes of a GEMM launch over M rows.
+size_t gemm_lds_bytes(int M);
+// y = x W^T over g.M rows (kThinRows < M <= SPEC_MAX_ROWS) with epilogue
+// `epi`; grid (ceil(N / 64), g.splits).  Only EPI_STORE may use k-splits.
+hipError_t gemm_launch(int epi, const GemvArgs& g, hipStream_t s, hipEvent_t e0, hipEvent_t e1);
+// k-splits of an EPI_STORE GEMM (the down projection) over N outputs and Kd inputs.
+int gemm_down_splits(int N, int Kd, int ncu);
+
+}  // namespace specdec

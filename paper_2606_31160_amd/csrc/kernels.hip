@@ -18,6 +18,7 @@
 
 #include "ctx.h"
 #include "device.h"
+#include "gemv.h"
 #include "pass.h"
 
 namespace specdec {
@@ -198,48 +199,6 @@ __global__ __launch_bounds__(1024) void k_embed(EmbedArgs p) {
 // consumers of a normalised input scale y by 1/rms(x), a per-row scalar
 // (RMSNorm(x) g W^T = (x g) W^T / rms(x)).
 // ---------------------------------------------------------------------------
-enum {
-  EPI_STORE = 0,   // out[split][m][n]: k-split partial sums (down projection)
-  EPI_ROPE = 1,    // y/rms; rotation of q/k at the row's position, q store, K / V^T cache append (QKV)
-  EPI_RESID = 2,   // x += y; xg = bf16(x * g); sums of x^2 (O projection)
-  EPI_SWIGLU = 3,  // y/rms; half-tiles (8 gate rows, 8 up rows): u = silu(gate) * up (gate/up)
-  EPI_ARGMAX = 4   // y/rms; per-tile (max, index) of the logits, optional bf16 logits (LM head)
-};
-
-struct GemvArgs {
-  const bf16_t* w[3];
-  int row0[3];           // first output row of each weight segment (multiples of 16)
-  int nseg;
-  int N, Kd;
-  const bf16_t* x;       // [M][ldx]
-  int ldx, M, splits;
-  const SeqState* st;
-  int rps;               // rows per sequence
-  int mpad;              // row stride of ss / amax
-  const float* ss_in;    // [H/16][mpad] sums of x^2 of the input rows (ROPE, SWIGLU, ARGMAX)
-  int H;                 // row length those sums cover
-  float eps;
-  float* out;            // EPI_STORE: [splits][M][N]
-  // EPI_ROPE
-  bf16_t* q;             // [M][nq*D]
-  bf16_t *kc, *vt;       // layer bases of the paged key / value pools
-  const int32_t* pt;     // [B][pps] page tables
-  const float2* rcs;     // [Mpad][D/2] (cos, sin) per row
-  int nq, nkv, D, pps;
-  // EPI_RESID
-  float* x32;            // [M][N] residual stream
-  const bf16_t* gain;    // [N] gain of the next RMSNorm
-  bf16_t* xg;            // [M][N] bf16(x * gain)
-  float* ss_out;         // [N/16][mpad] sums of x^2
-  // EPI_SWIGLU
-  bf16_t* u;             // [M][N/2]
-  // EPI_ARGMAX
-  float* amax_v;         // [N/16][mpad]
-  int32_t* amax_i;
-  bf16_t* logits;        // [M][N]
-  int allow_logits;
-};
-
 template <int MB, int NW, int SMAX, int TT, int EPI>
 __global__ __launch_bounds__(NW * 64) void k_gemv(GemvArgs a) {
   extern __shared__ __align__(16) unsigned char lds[];
@@ -1146,6 +1105,12 @@ GemvArgs gemv_base(Ctx& c, int M, int rps) {
   return g;
 }
 
+// Passes of more than kThinRows rows: the batched-row GEMM (gemm.hip).
+hipError_t gemm_run(Ctx& c, int epi, const GemvArgs& g, int kind, double bytes) {
+  Timed t(c, kind, bytes);
+  return gemm_launch(epi, g, S(c), t.e0, t.e1);
+}
+
 #define CK(x)                               \
   do {                                      \
     hipError_t e_ = (x);                    \
@@ -1194,7 +1159,10 @@ hipError_t run_layer(Ctx& c, Model& m, int li, const bf16_t* next_gain, bool sel
     g.D = D;
     g.pt = c.pt;
     g.pps = c.pps;
-    CK((gemv_launch<EPI_ROPE, 1>(c, g, SPEC_KERNEL_QKV, gemv_bytes(g.N, H, M, 2.0))));
+    if (M > kThinRows)
+      CK(gemm_run(c, EPI_ROPE, g, SPEC_KERNEL_QKV, gemv_bytes(g.N, H, M, 2.0)));
+    else
+      CK((gemv_launch<EPI_ROPE, 1>(c, g, SPEC_KERNEL_QKV, gemv_bytes(g.N, H, M, 2.0))));
   }
   // attention
   {
@@ -1235,7 +1203,10 @@ hipError_t run_layer(Ctx& c, Model& m, int li, const bf16_t* next_gain, bool sel
     g.gain = w.ffn_norm;
     g.xg = c.xg;
     g.ss_out = c.ss;
-    CK((gemv_launch<EPI_RESID, 1>(c, g, SPEC_KERNEL_O, gemv_bytes(H, nq * D, M, 10.0))));
+    if (M > kThinRows)
+      CK(gemm_run(c, EPI_RESID, g, SPEC_KERNEL_O, gemv_bytes(H, nq * D, M, 10.0)));
+    else
+      CK((gemv_launch<EPI_RESID, 1>(c, g, SPEC_KERNEL_O, gemv_bytes(H, nq * D, M, 10.0))));
   }
   // gate/up (+ 1/rms of the FFN norm) + SwiGLU
   if (m.ljobs_dev) {
@@ -1256,7 +1227,11 @@ hipError_t run_layer(Ctx& c, Model& m, int li, const bf16_t* next_gain, bool sel
     g.H = H;
     g.eps = d.rms_eps;
     g.u = c.u;
-    CK(gemv_launch_p<EPI_SWIGLU>(c, g, std::min(c.ncu, 2 * F / kTile), SPEC_KERNEL_GATEUP, gemv_bytes(2 * F, H, M, 1.0)));
+    if (M > kThinRows)
+      CK(gemm_run(c, EPI_SWIGLU, g, SPEC_KERNEL_GATEUP, gemv_bytes(2 * F, H, M, 1.0)));
+    else
+      CK(gemv_launch_p<EPI_SWIGLU>(c, g, std::min(c.ncu, 2 * F / kTile), SPEC_KERNEL_GATEUP,
+                                   gemv_bytes(2 * F, H, M, 1.0)));
   }
   // down projection (k-split partials) -> residual + the next norm's input
   {
@@ -1276,8 +1251,12 @@ hipError_t run_layer(Ctx& c, Model& m, int li, const bf16_t* next_gain, bool sel
       g.ldx = F;
       g.splits = m.s_down;
       g.out = c.part;
-      const int per_split = std::max(1, std::min(c.ncu / m.s_down, H / kTile));
-      CK(gemv_launch_p<EPI_STORE>(c, g, per_split * m.s_down, SPEC_KERNEL_DOWN, gemv_bytes(H, F, M, 4.0 * m.s_down)));
+      if (M > kThinRows) {
+        CK(gemm_run(c, EPI_STORE, g, SPEC_KERNEL_DOWN, gemv_bytes(H, F, M, 4.0 * m.s_down)));
+      } else {
+        const int per_split = std::max(1, std::min(c.ncu / m.s_down, H / kTile));
+        CK(gemv_launch_p<EPI_STORE>(c, g, per_split * m.s_down, SPEC_KERNEL_DOWN, gemv_bytes(H, F, M, 4.0 * m.s_down)));
+      }
     }
     FinishArgs p{c.st, c.part, S_down, M, c.R, H, c.Mpad, select_last ? 1 : 0, c.x, next_gain, c.xg, c.ss};
     Timed t(c, SPEC_KERNEL_OTHER, 0);
@@ -1557,7 +1536,10 @@ hipError_t launch_forward(Ctx& c, PassMode mode) {
     g.logits = c.logits;
     g.allow_logits = draft ? 0 : 1;
     const double bytes = gemv_bytes(c.V, d.hidden, g.M, 0.0) + 8.0 * (c.V / kTile) * g.M;
-    CK(gemv_launch_p<EPI_ARGMAX>(c, g, std::min(c.ncu, c.V / kTile), SPEC_KERNEL_LMHEAD, bytes));
+    if (g.M > kThinRows)
+      CK(gemm_run(c, EPI_ARGMAX, g, SPEC_KERNEL_LMHEAD, bytes));
+    else
+      CK(gemv_launch_p<EPI_ARGMAX>(c, g, std::min(c.ncu, c.V / kTile), SPEC_KERNEL_LMHEAD, bytes));
   }
   const int ntiles = c.V / kTile;
   Timed t(c, SPEC_KERNEL_OTHER, 0);

@@ -13,6 +13,7 @@
 #include <vector>
 
 #include "ctx.h"
+#include "gemv.h"
 #include "pass.h"
 
 using namespace specdec;
@@ -87,8 +88,8 @@ bool check_config(const spec_config* cfg, const spec_seq_init* seqs, bool has_dr
     err = "K out of range";
     return false;
   }
-  if (cfg->batch * (cfg->K + 1) > 64) {
-    err = "batch*(K+1) rows per pass must not exceed 64";
+  if (cfg->batch * (cfg->K + 1) > SPEC_MAX_ROWS) {
+    err = "batch*(K+1) rows per pass must not exceed SPEC_MAX_ROWS";
     return false;
   }
   if (cfg->vocab < 16 || cfg->vocab % 16) {
@@ -252,7 +253,9 @@ Layout make_layout(const spec_config* cfg, const spec_seq_init* seqs) {
   return L;
 }
 
-void set_splits(Model& m, int M) { m.s_down = down_splits(M, m.d.ffn, num_cus()); }
+void set_splits(Model& m, int M) {
+  m.s_down = M > kThinRows ? gemm_down_splits(m.d.hidden, m.d.ffn, num_cus()) : down_splits(M, m.d.ffn, num_cus());
+}
 
 // Down-projection k-splits of the persistent pass for one model: the fewest
 // that divide the grid (one workgroup per CU) while every worker wave streams
@@ -289,6 +292,7 @@ size_t part_elems_for(const Model& m, int M) { return (size_t)m.s_down * M * m.d
 // (one k-split): their x rows for the full reduction length must fit in LDS,
 // and each wave streams at most kGemvSteps steps.
 bool check_fits(const spec_dims& d, int M, std::string& err, const char* who) {
+  if (M > kThinRows) return true;   // the batched-row GEMM streams x through LDS in chunks
   const int Ks[2] = {d.hidden, d.q_heads * d.head_dim};
   for (int Kd : Ks) {
     const int T = (Kd + 31) / 32;

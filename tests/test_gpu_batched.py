@@ -1,0 +1,156 @@
+"""GPU parity of passes over many sequences at once: more than 64 rows per
+pass run on the batched-row GEMM, with caches in shuffled KV pages.
+
+  * 16 tiny scenes of different prompt lengths, K = 4 (80 rows): one verify's
+    logits, accept lengths, commits and new K/V rows against the oracle, then
+    the speculative loop to the token budget, every committed token checked
+    against the oracle's logits over the sequence's own history;
+  * 8 tiny scenes with K = 16 and 4 q heads per kv head (136 rows, two
+    attention row blocks);
+  * 16 scenes of the 16-scene workload's prompt structure (prompts of
+    2048..8192 tokens, four camera grids each) at the 7B-class width through
+    one target layer, 144 rows: logits of every sequence against the oracle.
+"""
+import dataclasses
+
+import numpy as np
+import pytest
+
+import workloads as W
+from oracle import numerics as ON
+from oracle import spec as OS
+from tests import _support as S
+
+pytestmark = pytest.mark.gpu
+
+
+def _session(w, **kw):
+    from paper_2606_31160_amd.harness import Session
+    return Session(w, **kw)
+
+
+def _scenes(w, n, lo, hi, seed):
+    # four (2, h, 16) camera grids fill about 85% of each prompt (lo >= 430)
+    lens = np.random.default_rng(seed).integers(lo, hi + 1, size=n)
+    seqs = tuple(W.c5_layout(int(p)) for p in lens)
+    assert all(max(b.start + b.ntok for b in q.blocks) <= q.prefix_len for q in seqs)
+    return w.with_(seqs=seqs, p_accept=tuple([0.8] * n))
+
+
+def _verify_against_oracle(w, s, T, seed, check_kv=(0,)):
+    """One verify of explicit drafts (the oracle's first greedy token, then
+    random ids) for every sequence, with logits, against the oracle."""
+    rng = np.random.default_rng(seed)
+    seqs, drafts = [], np.zeros((w.batch, w.K), dtype=np.int32)
+    for b in range(w.batch):
+        probe = S.oracle_sequence(w, b, T, None, with_draft=False)
+        d = rng.integers(0, w.vocab, size=w.K).astype(np.int32)
+        d[:1] = OS.greedy_trace(probe, 1)
+        drafts[b] = d
+        seqs.append(S.oracle_sequence(w, b, T, None, with_draft=False))
+    s.verify(drafts, logits=True)
+    s.commit()
+    coms, acc, fin = s.committed()
+    gl = s.logits.float().cpu().numpy()
+    for b in range(w.batch):
+        ref = seqs[b].verify(drafts[b])
+        for j in range(w.K + 1):
+            assert S.normwise_err(gl[b, j], ref.logits[j]) <= S.LOGIT_RTOL, (b, j)
+        l = int(acc[b])
+        pinned = S.margin(ref.logits) > S.MARGIN
+        if pinned[:ref.accept_len + 1].all():
+            assert l == ref.accept_len and coms[b] == ref.committed, b
+        assert coms[b][:l] == list(drafts[b][:l])
+        S.check_argmax_rows(coms[b][l:l + 1], ref.logits[l:l + 1])
+        st = s.state(b)
+        assert st["seq_len"] == w.seqs[b].prefix_len + l + 1 and st["pending"] == coms[b][-1]
+        if b in check_kv:
+            P = w.seqs[b].prefix_len
+            for li in range(w.target.layers):
+                for which, cache in ((0, seqs[b].tc.k[li]), (1, seqs[b].tc.v[li])):
+                    got = ON.decode(s.kv(b, 0, li, which, P, w.K + 1))
+                    assert S.normwise_err(got, cache[P:P + w.K + 1]) <= S.LOGIT_RTOL, (b, li, which)
+
+
+def _loop(s, max_rounds=100):
+    outs = [[] for _ in range(s.B)]
+    done = [False] * s.B
+    for _ in range(max_rounds):
+        for _ in range(s.K):
+            s.draft_step()
+        s.verify(None)
+        s.commit()
+        coms, acc, fin = s.committed()
+        for b in range(s.B):
+            if not done[b]:
+                outs[b] += [int(t) for t in coms[b]]
+                done[b] = bool(fin[b])
+            else:
+                assert coms[b] == []
+        if all(done):
+            break
+    assert s.sync() == s.B
+    return outs
+
+
+def _check_history(w, T, outs):
+    """Each committed token is the oracle's greedy token after the tokens
+    committed before it (pinned rows), or within the tolerance of its top-1."""
+    for b, toks in enumerate(outs):
+        assert len(toks) == w.max_new_tokens
+        seq = S.oracle_sequence(w, b, T, None, with_draft=False)
+        P = w.seqs[b].prefix_len
+        rows = [seq.pending] + toks[:-1]
+        z = T.forward(rows, list(range(P, P + len(rows))), seq.tc)
+        S.check_argmax_rows(toks, z)
+
+
+@pytest.fixture(scope="module")
+def tiny16():
+    w = _scenes(W.get("C1"), 16, 430, 700, seed=3)
+    hp = W.HostWeights(w)
+    T, _ = S.oracle_decoders(w, hp)
+    return w, hp, T
+
+
+def test_sixteen_scenes_one_verify(tiny16):
+    w, hp, T = tiny16
+    assert w.batch * (w.K + 1) == 80
+    s = _session(w, page_seed=11)
+    _verify_against_oracle(w, s, T, seed=5, check_kv=(0, 9, 15))
+    s.close()
+
+
+def test_sixteen_scenes_spec_loop(tiny16):
+    w, hp, T = tiny16
+    s = _session(w, page_seed=12)
+    outs = _loop(s)
+    s.close()
+    _check_history(w, T, outs)
+
+
+def test_block_of_16_eight_scenes():
+    base = W.get("C1")
+    w = _scenes(base, 8, 430, 600, seed=4).with_(
+        K=16, target=dataclasses.replace(base.target, q_heads=8, kv_heads=2),
+        draft=dataclasses.replace(base.draft, q_heads=8, kv_heads=2))
+    assert w.batch * (w.K + 1) == 136
+    T, _ = S.oracle_decoders(w, W.HostWeights(w))
+    s = _session(w, page_seed=13)
+    _verify_against_oracle(w, s, T, seed=6, check_kv=(3,))
+    s.close()
+    s = _session(w)
+    outs = _loop(s)
+    s.close()
+    _check_history(w, T, outs)
+
+
+def test_sixteen_scenes_7b_width_one_layer():
+    c5 = W.get("C5")
+    w = W.get("C2").with_(seqs=c5.seqs, p_accept=c5.p_accept, draft=None)
+    assert w.batch * (w.K + 1) == 144 and w.target.hidden == 3584
+    hp = W.HostWeights(w)
+    T, _ = S.oracle_decoders(w, hp, cache_weights=True)
+    s = _session(w, provider=hp, page_seed=14)
+    _verify_against_oracle(w, s, T, seed=7, check_kv=(0, 15))
+    s.close()
