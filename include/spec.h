@@ -79,6 +79,10 @@ typedef struct spec_dims {
                                       shapes allow it (else one kernel per layer step) */
 #define SPEC_FLAG_PASS_TIMELINE 4  /* the persistent pass kernel records per-phase wall-clock stamps
                                       (see spec_debug_pass_timeline); adds a small cost */
+#define SPEC_FLAG_ROWMAJOR 8       /* stream the caller's row-major weights directly.  Without it, passes
+                                      of at most 16 rows (batch*(K+1) <= 16) on the layered path stream a
+                                      tile-packed copy of every weight matrix that spec_init writes into
+                                      the workspace (its size is part of spec_workspace_bytes) */
 
 typedef struct spec_config {
   spec_dims target;          /* deliberative reasoner (3D M-RoPE) */
@@ -223,6 +227,15 @@ spec_status spec_debug_state(spec_ctx* ctx, int32_t b, int32_t* host_out);
  * host_out [npos][kv_heads][head_dim] bf16. */
 spec_status spec_debug_kv(spec_ctx* ctx, int32_t b, int32_t model, int32_t layer, int32_t which,
                           int32_t pos0, int32_t npos, void* host_out);
+
+/* Execution path of the context's passes into *path:
+ * SPEC_PATH_ROWMAJOR (one kernel per layer step over the caller's row-major weights),
+ * SPEC_PATH_PACKED (one kernel per layer step over the tile-packed weight copy),
+ * SPEC_PATH_PERSISTENT (the persistent pass kernel). */
+#define SPEC_PATH_ROWMAJOR 0
+#define SPEC_PATH_PACKED 1
+#define SPEC_PATH_PERSISTENT 2
+spec_status spec_debug_path(const spec_ctx* ctx, int32_t* path);
 
 /* Wall-clock stamps of the most recent persistent pass (context created with
  * SPEC_FLAG_PASS_TIMELINE; synchronising).  host_out receives

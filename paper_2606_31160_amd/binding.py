@@ -23,6 +23,7 @@ SPEC_KV_PAGE = 64
 SPEC_FLAG_NO_GRAPHS = 1
 SPEC_FLAG_PERSISTENT = 2
 SPEC_FLAG_PASS_TIMELINE = 4
+SPEC_FLAG_ROWMAJOR = 8
 STATUS = {0: "SPEC_OK", 1: "SPEC_E_INVAL", 2: "SPEC_E_STATE", 3: "SPEC_E_CAPACITY", 5: "SPEC_E_HIP",
           6: "SPEC_E_NUMERIC"}
 KERNEL_KINDS = {"qkv": 0, "o": 1, "gateup": 2, "down": 3, "lmhead": 4, "attn": 5, "other": 6,
@@ -91,6 +92,7 @@ def lib():
             "spec_timing_read": [P, c_int32, POINTER(c_int64), POINTER(c_double), POINTER(c_double)],
             "spec_debug_pass_timeline": [P, c_int32, P, c_int64, POINTER(c_int32), POINTER(c_int32),
                                          POINTER(c_double)],
+            "spec_debug_path": [P, POINTER(c_int32)],
         }
         for name, args in sig.items():
             f = getattr(L, name)
@@ -185,6 +187,15 @@ def spec_debug_kv(ctx, b: int, model: int, layer: int, which: int, pos0: int, np
     out = np.zeros((npos, kv_heads, head_dim), dtype=np.uint16)
     _check(lib().spec_debug_kv(ctx, b, model, layer, which, pos0, npos, out.ctypes.data), "spec_debug_kv", ctx)
     return out
+
+
+PATHS = {0: "rowmajor", 1: "packed", 2: "persistent"}
+
+
+def spec_debug_path(ctx) -> str:
+    p = c_int32(-1)
+    _check(lib().spec_debug_path(ctx, ctypes.byref(p)), "spec_debug_path", ctx)
+    return PATHS[p.value]
 
 
 def spec_timing(ctx, enable: bool) -> None:

@@ -15,6 +15,7 @@ namespace specdec {
 typedef uint16_t bf16_t;
 struct PassArgs;
 struct GemvJob;
+struct SgJob;
 
 constexpr int kMaxRows = SPEC_MAX_K + 1;     // rows per sequence in one pass
 constexpr int kTile = 16;                    // output rows per GEMV tile (one MFMA block)
@@ -72,6 +73,11 @@ struct Model {
   PassArgs* largs_dev = nullptr;       // layered path: arguments of the one-phase GEMV kernels
   GemvJob* ljobs_dev = nullptr;        // layered path: [layers][kPassJobs] (gate/up and down used)
   size_t kv_layer = 0;              // elements of one layer's key (or value) cache
+  // tile-packed weights (sgemv.h) of every layer: q/k/v, o, gate/up pairs, down
+  bf16_t* pk = nullptr;
+  size_t pk_layer = 0, pk_o = 0, pk_gu = 0, pk_dn = 0;   // elements per layer; offsets inside a layer
+  std::vector<SgJob> sg_host;       // [layers][4] (q/k/v, o, gate/up, down) + the LM head
+  SgJob* sg_dev = nullptr;          // device copy
 };
 
 struct TimingRec {
@@ -117,6 +123,14 @@ struct Ctx {
 
   const bf16_t* embed = nullptr;
   Model tgt, drf;
+
+  // packed-weight path (passes of at most 16 rows)
+  bool sg = false;
+  bf16_t* pk_head = nullptr;        // tile-packed LM head (shared by both models)
+  float* sg_part = nullptr;         // partial tiles of split units
+  unsigned* sg_cnt = nullptr;       // arrival counters
+  size_t sg_part_floats = 0;
+  int sg_units = 0;
   bool has_draft = false;
 
   // persistent pass (pass.hip): per-layer activations, barrier words
@@ -165,6 +179,12 @@ hipError_t launch_forward(Ctx& c, PassMode mode);   // embed .. accept / draft p
 hipError_t launch_draft_out(Ctx& c, int32_t* d_tokens);
 hipError_t launch_commit(Ctx& c, int32_t* acc, int32_t* committed, int32_t* ncommit, int32_t* fin);
 hipError_t launch_logits_out(Ctx& c, void* d_logits);
+// Packed-weight path: plans (and, with fill, points) every GEMV job of a model;
+// false if a shape does not fit.  Packs a model's weights / the LM head.
+bool sg_build_jobs(Ctx& c, Model& m, bool draft, bool fill);
+hipError_t sg_pack_model(Ctx& c, Model& m);
+hipError_t sg_pack_head(Ctx& c);
+hipError_t sg_upload_jobs(Ctx& c, Model& m);
 
 // Dynamic LDS bytes one GEMV workgroup needs (TT tiles, M rows, span k-steps)
 // and the device limit; k-splits of a GEMV whose workgroups cannot hold all

@@ -20,6 +20,7 @@
 #include "device.h"
 #include "gemv.h"
 #include "pass.h"
+#include "sgemv.h"
 
 namespace specdec {
 
@@ -1121,6 +1122,60 @@ hipError_t gemm_run(Ctx& c, int epi, const GemvArgs& g, int kind, double bytes) 
 // the shapes allow it; measured per projection on the 7B-class verify.
 constexpr bool kQkvAsJob = false, kOAsJob = false, kDownAsJob = false;
 
+// Split-KV attention of one layer + the combine of its splits.
+hipError_t launch_attention(Ctx& c, Model& m, int li) {
+  const spec_dims& d = m.d;
+  const int D = d.head_dim, nq = d.q_heads, nkv = d.kv_heads;
+  bf16_t* kc = m.kc + m.kv_layer * li;
+  bf16_t* vt = m.vt + m.kv_layer * li;
+  const int G = nq / nkv;
+  const int rb = (c.R * G + 63) / 64;
+  AttnArgs p{c.st, c.q, kc, vt, c.pt, c.op, c.mp, c.lp, nq, nkv, G, c.R, c.B, c.pps, c.attn_chunk, rb,
+             kLog2e / sqrtf((float)D)};
+  dim3 grid(c.attn_splits, nkv * rb, c.B);
+  {
+    Timed t(c, SPEC_KERNEL_ATTN, 0);
+    if (D == 128)
+      hipExtLaunchKernelGGL(k_attn<128>, grid, dim3(256), attn_lds_bytes(c.attn_chunk, D), S(c), t.e0, t.e1, 0, p);
+    else
+      hipExtLaunchKernelGGL(k_attn<64>, grid, dim3(256), attn_lds_bytes(c.attn_chunk, D), S(c), t.e0, t.e1, 0, p);
+    CK(hipGetLastError());
+  }
+  CombineArgs cb{c.st, c.op, c.mp, c.lp, c.o, nq, D, c.R, c.B, c.attn_chunk};
+  Timed t2(c, SPEC_KERNEL_OTHER, 0);
+  hipExtLaunchKernelGGL(k_attn_combine, dim3(c.R, nq, c.B), dim3(256),
+                        (size_t)(((c.attn_splits + 3) & ~3) + 8 * D) * sizeof(float), S(c), t2.e0, t2.e1, 0, cb);
+  return hipGetLastError();
+}
+
+// One layer on the packed-weight path: q/k/v (+rotary, KV append),
+// attention, o (+residual), gate/up (+SwiGLU), down (+residual, next norm).
+hipError_t run_layer_sg(Ctx& c, Model& m, int li) {
+  const spec_dims& d = m.d;
+  const int H = d.hidden, D = d.head_dim, nq = d.q_heads, nkv = d.kv_heads, F = d.ffn;
+  const int M = c.M;
+  const SgJob* hj = m.sg_host.data() + (size_t)li * 4;
+  const SgJob* dj = m.sg_dev + (size_t)li * 4;
+  {
+    Timed t(c, SPEC_KERNEL_QKV, gemv_bytes((nq + 2 * nkv) * D, H, M, 2.0));
+    CK(sg_launch(SG_ROPE, hj[0], dj + 0, S(c), t.e0, t.e1));
+  }
+  CK(launch_attention(c, m, li));
+  {
+    Timed t(c, SPEC_KERNEL_O, gemv_bytes(H, nq * D, M, 10.0));
+    CK(sg_launch(SG_RESID, hj[1], dj + 1, S(c), t.e0, t.e1));
+  }
+  {
+    Timed t(c, SPEC_KERNEL_GATEUP, gemv_bytes(2 * F, H, M, 1.0));
+    CK(sg_launch(SG_SWIGLU, hj[2], dj + 2, S(c), t.e0, t.e1));
+  }
+  {
+    Timed t(c, SPEC_KERNEL_DOWN, gemv_bytes(H, F, M, 10.0));
+    CK(sg_launch(SG_DOWN, hj[3], dj + 3, S(c), t.e0, t.e1));
+  }
+  return hipSuccess;
+}
+
 hipError_t run_layer(Ctx& c, Model& m, int li, const bf16_t* next_gain, bool select_last) {
   const spec_dims& d = m.d;
   const int H = d.hidden, D = d.head_dim, nq = d.q_heads, nkv = d.kv_heads, F = d.ffn;
@@ -1164,28 +1219,7 @@ hipError_t run_layer(Ctx& c, Model& m, int li, const bf16_t* next_gain, bool sel
     else
       CK((gemv_launch<EPI_ROPE, 1>(c, g, SPEC_KERNEL_QKV, gemv_bytes(g.N, H, M, 2.0))));
   }
-  // attention
-  {
-    const int G = nq / nkv;
-    const int rb = (c.R * G + 63) / 64;
-    AttnArgs p{c.st, c.q, kc, vt, c.pt, c.op, c.mp, c.lp, nq, nkv, G, c.R, c.B, c.pps, c.attn_chunk, rb,
-               kLog2e / sqrtf((float)D)};
-    dim3 grid(c.attn_splits, nkv * rb, c.B);
-    {
-      Timed t(c, SPEC_KERNEL_ATTN, 0);
-      if (D == 128)
-        hipExtLaunchKernelGGL(k_attn<128>, grid, dim3(256), attn_lds_bytes(c.attn_chunk, D), S(c), t.e0, t.e1, 0, p);
-      else
-        hipExtLaunchKernelGGL(k_attn<64>, grid, dim3(256), attn_lds_bytes(c.attn_chunk, D), S(c), t.e0, t.e1, 0, p);
-      CK(hipGetLastError());
-    }
-    CombineArgs cb{c.st, c.op, c.mp, c.lp, c.o, nq, D, c.R, c.B, c.attn_chunk};
-    Timed t2(c, SPEC_KERNEL_OTHER, 0);
-    hipExtLaunchKernelGGL(k_attn_combine, dim3(c.R, nq, c.B), dim3(256),
-                          (size_t)(((c.attn_splits + 3) & ~3) + 8 * D) * sizeof(float), S(c), t2.e0, t2.e1, 0,
-                       cb);
-    CK(hipGetLastError());
-  }
+  CK(launch_attention(c, m, li));
   // o projection + residual; bf16(x * g_ffn) and sums of x^2 for the FFN norm
   if (m.ljobs_dev && kOAsJob) {
     Timed t(c, SPEC_KERNEL_O, gemv_bytes(H, nq * D, M, 10.0));
@@ -1273,6 +1307,7 @@ void init_kernel_attributes() {
   if (done) return;
   done = true;
   pass_set_attributes(gemv_lds_limit());
+  sg_set_attributes(gemv_lds_limit());
   (void)hipFuncSetAttribute(reinterpret_cast<const void*>(&k_attn<128>), hipFuncAttributeMaxDynamicSharedMemorySize,
                             (int)attn_lds_bytes(kAttnChunk, 128));
   (void)hipFuncSetAttribute(reinterpret_cast<const void*>(&k_attn<64>), hipFuncAttributeMaxDynamicSharedMemorySize,
@@ -1389,6 +1424,155 @@ hipError_t upload_layered_jobs(Ctx& c, Model& m, bool draft) {
   hipError_t e = hipMemcpyAsync(m.largs_dev, &a, sizeof a, hipMemcpyHostToDevice, c.stream);
   if (e == hipSuccess)
     e = hipMemcpyAsync(m.ljobs_dev, jobs.data(), jobs.size() * sizeof(GemvJob), hipMemcpyHostToDevice, c.stream);
+  if (e == hipSuccess) e = hipStreamSynchronize(c.stream);
+  return e;
+}
+
+// ---------------------------------------------------------------------------
+// Packed-weight path: job tables and weight packing
+// ---------------------------------------------------------------------------
+namespace {
+int steps_of(int Kd) { return (Kd + 31) / 32; }
+}  // namespace
+
+bool sg_build_jobs(Ctx& c, Model& m, bool draft, bool fill) {
+  const spec_dims& d = m.d;
+  const int H = d.hidden, D = d.head_dim, nq = d.q_heads, nkv = d.kv_heads, F = d.ffn;
+  const int ncu = c.ncu, lim = gemv_lds_limit();
+  const int nqkv = (nq + 2 * nkv) * D;
+  // packed elements per layer and offsets of o, gate/up, down inside a layer
+  m.pk_o = sg_packed_elems(nqkv / kTile, steps_of(H));
+  m.pk_gu = m.pk_o + sg_packed_elems(H / kTile, steps_of(nq * D));
+  m.pk_dn = m.pk_gu + sg_packed_elems(2 * F / kTile, steps_of(H));
+  m.pk_layer = m.pk_dn + sg_packed_elems(H / kTile, steps_of(F));
+  m.sg_host.assign((size_t)d.layers * 4 + 1, SgJob{});
+  auto base = [&](SgJob& j, int ntiles, int Kd, const bf16_t* x) {
+    j.ntiles = ntiles;
+    j.T = steps_of(Kd);
+    j.Kd = Kd;
+    j.ldx = Kd;
+    j.x = x;
+    j.M = c.M;
+    j.rps = c.R;
+    j.mpad = c.Mpad;
+    j.eps = d.rms_eps;
+    j.st = c.st;
+    j.part = c.sg_part;
+    j.cnt = c.sg_cnt;
+  };
+  for (int li = 0; li < d.layers; ++li) {
+    SgJob* j = m.sg_host.data() + (size_t)li * 4;
+    bf16_t* pk = m.pk ? m.pk + m.pk_layer * li : nullptr;
+    const bool last = li + 1 == d.layers;
+    base(j[0], nqkv / kTile, H, c.xg);
+    j[0].w = pk;
+    j[0].ss_in = c.ss;
+    j[0].Hn = H;
+    j[0].q = c.q;
+    j[0].kc = m.kc ? m.kc + m.kv_layer * li : nullptr;
+    j[0].vt = m.vt ? m.vt + m.kv_layer * li : nullptr;
+    j[0].pt = c.pt;
+    j[0].pps = c.pps;
+    j[0].rcs = c.rcs;
+    j[0].nq = nq;
+    j[0].nkv = nkv;
+    j[0].D = D;
+    base(j[1], H / kTile, nq * D, c.o);
+    j[1].w = pk ? pk + m.pk_o : nullptr;
+    j[1].x32 = c.x;
+    j[1].H = H;
+    j[1].gain = fill ? m.L[li].ffn_norm : nullptr;
+    j[1].xg = c.xg;
+    j[1].ss_out = c.ss;
+    base(j[2], 2 * F / kTile, H, c.xg);
+    j[2].w = pk ? pk + m.pk_gu : nullptr;
+    j[2].ss_in = c.ss;
+    j[2].Hn = H;
+    j[2].u = c.u;
+    base(j[3], H / kTile, F, c.u);
+    j[3].w = pk ? pk + m.pk_dn : nullptr;
+    j[3].x32 = c.x;
+    j[3].H = H;
+    j[3].gain = fill ? (last ? m.final_norm : m.L[li + 1].attn_norm) : nullptr;
+    j[3].xg = c.xg;
+    j[3].ss_out = c.ss;
+    j[3].select_last = (draft && last) ? 1 : 0;
+    const int epis[4] = {SG_ROPE, SG_RESID, SG_SWIGLU, SG_DOWN};
+    for (int k = 0; k < 4; ++k)
+      if (!sg_plan(j[k], epis[k], ncu, lim)) return false;
+  }
+  SgJob& h = m.sg_host[(size_t)d.layers * 4];
+  base(h, c.V / kTile, H, c.xg);
+  h.w = c.pk_head;
+  h.M = draft ? c.B : c.M;
+  h.rps = draft ? 1 : c.R;
+  h.ss_in = c.ss;
+  h.Hn = H;
+  h.amax_v = c.amax_v;
+  h.amax_i = c.amax_i;
+  h.logits = c.logits;
+  h.allow_logits = draft ? 0 : 1;
+  return sg_plan(h, SG_ARGMAX, ncu, lim);
+}
+
+hipError_t sg_pack_model(Ctx& c, Model& m) {
+  const spec_dims& d = m.d;
+  const int H = d.hidden, D = d.head_dim, nq = d.q_heads, nkv = d.kv_heads, F = d.ffn;
+  for (int li = 0; li < d.layers; ++li) {
+    const LayerW& w = m.L[li];
+    bf16_t* pk = m.pk + m.pk_layer * li;
+    PackSrc a{};
+    a.seg[0] = w.wq;
+    a.seg[1] = w.wk;
+    a.seg[2] = w.wv;
+    a.row0[1] = nq * D;
+    a.row0[2] = (nq + nkv) * D;
+    a.nseg = 3;
+    a.Kd = H;
+    a.ntiles = (nq + 2 * nkv) * D / kTile;
+    a.T = steps_of(H);
+    CK(sg_pack(pk, a, c.stream));
+    PackSrc o{};
+    o.seg[0] = w.wo;
+    o.nseg = 1;
+    o.Kd = nq * D;
+    o.ntiles = H / kTile;
+    o.T = steps_of(nq * D);
+    CK(sg_pack(pk + m.pk_o, o, c.stream));
+    PackSrc g{};
+    g.seg[0] = w.wg;
+    g.seg[1] = w.wu;
+    g.nseg = 2;
+    g.pair = 1;
+    g.Kd = H;
+    g.ntiles = 2 * F / kTile;
+    g.T = steps_of(H);
+    CK(sg_pack(pk + m.pk_gu, g, c.stream));
+    PackSrc dn{};
+    dn.seg[0] = w.wd;
+    dn.nseg = 1;
+    dn.Kd = F;
+    dn.ntiles = H / kTile;
+    dn.T = steps_of(F);
+    CK(sg_pack(pk + m.pk_dn, dn, c.stream));
+  }
+  return hipSuccess;
+}
+
+hipError_t sg_pack_head(Ctx& c) {
+  PackSrc e{};
+  e.seg[0] = c.embed;
+  e.nseg = 1;
+  e.Kd = c.tgt.d.hidden;
+  e.ntiles = c.V / kTile;
+  e.T = steps_of(e.Kd);
+  return sg_pack(c.pk_head, e, c.stream);
+}
+
+hipError_t sg_upload_jobs(Ctx& c, Model& m) {
+  hipError_t e = hipMemcpyAsync(m.sg_dev, m.sg_host.data(), m.sg_host.size() * sizeof(SgJob), hipMemcpyHostToDevice,
+                                c.stream);
+  // the host table must stay put until the copy is done
   if (e == hipSuccess) e = hipStreamSynchronize(c.stream);
   return e;
 }
@@ -1512,6 +1696,8 @@ hipError_t launch_forward(Ctx& c, PassMode mode) {
   const bool draft = mode == PASS_DRAFT;
   if (persistent) {
     CK(run_layers_persistent(c, m, draft));
+  } else if (c.sg) {
+    for (int li = 0; li < d.layers; ++li) CK(run_layer_sg(c, m, li));
   } else {
     for (int li = 0; li < d.layers; ++li) {
       const bool last = li + 1 == d.layers;
@@ -1520,7 +1706,13 @@ hipError_t launch_forward(Ctx& c, PassMode mode) {
   }
   // LM head (+ 1/rms of the final norm) with the fused per-tile argmax; the
   // draft proposes from each sequence's last row only (stored as row b)
-  {
+  if (c.sg) {
+    const int rows = draft ? c.B : M;
+    const double bytes = gemv_bytes(c.V, d.hidden, rows, 0.0) + 8.0 * (c.V / kTile) * rows;
+    Timed t(c, SPEC_KERNEL_LMHEAD, bytes);
+    const size_t hi = (size_t)d.layers * 4;
+    CK(sg_launch(SG_ARGMAX, m.sg_host[hi], m.sg_dev + hi, S(c), t.e0, t.e1));
+  } else {
     GemvArgs g = gemv_base(c, draft ? c.B : M, draft ? 1 : c.R);
     g.w[0] = c.embed;
     g.nseg = 1;

@@ -15,6 +15,7 @@
 #include "ctx.h"
 #include "gemv.h"
 #include "pass.h"
+#include "sgemv.h"
 
 using namespace specdec;
 
@@ -447,6 +448,30 @@ size_t carve(Ctx& c, const spec_config* cfg, const spec_seq_init* seqs, bool has
     }
     c.pass_lds = lds;
   }
+  // packed-weight path: passes of at most 16 rows on the layered path
+  c.sg = false;
+  if (!(cfg->flags & SPEC_FLAG_ROWMAJOR) && !c.use_pass && L.M <= kSgMaxRows &&
+      sg_build_jobs(c, c.tgt, false, false) && (!has_draft || sg_build_jobs(c, c.drf, true, false))) {
+    size_t pf = 0;
+    int units = 0;
+    for (int k = 0; k < (has_draft ? 2 : 1); ++k)
+      for (const SgJob& j : (k ? c.drf : c.tgt).sg_host) {
+        pf = std::max(pf, sg_part_floats(j));
+        units = std::max(units, j.units);
+      }
+    c.sg = true;
+    c.sg_part_floats = pf;
+    c.sg_units = units;
+    c.sg_part = cv.take<float>(pf);
+    c.sg_cnt = cv.take<unsigned>((size_t)units);
+    c.pk_head = cv.take<bf16_t>(sg_packed_elems(L.V / kTile, (H + 31) / 32));
+    c.tgt.pk = cv.take<bf16_t>(c.tgt.pk_layer * t.layers);
+    c.tgt.sg_dev = cv.take<SgJob>(c.tgt.sg_host.size());
+    if (has_draft) {
+      c.drf.pk = cv.take<bf16_t>(c.drf.pk_layer * cfg->draft.layers);
+      c.drf.sg_dev = cv.take<SgJob>(c.drf.sg_host.size());
+    }
+  }
   return align_up(cv.off, kAlign);
 }
 
@@ -709,6 +734,17 @@ spec_status spec_init(const spec_config* cfg, const void* embed, const spec_mode
           (has_draft && (e = upload_pass_tables(c, c.drf, true)) != hipSuccess))
         return hip_fail(e, "layer table upload");
     }
+    if (c.sg) {
+      if (!sg_build_jobs(c, c.tgt, false, true) || (has_draft && !sg_build_jobs(c, c.drf, true, true))) {
+        g_init_error = "packed GEMV plan changed between sizing and init";
+        delete ctx;
+        return SPEC_E_INVAL;
+      }
+      if ((e = sg_pack_head(c)) != hipSuccess || (e = sg_pack_model(c, c.tgt)) != hipSuccess ||
+          (has_draft && (e = sg_pack_model(c, c.drf)) != hipSuccess) || (e = sg_upload_jobs(c, c.tgt)) != hipSuccess ||
+          (has_draft && (e = sg_upload_jobs(c, c.drf)) != hipSuccess))
+        return hip_fail(e, "weight packing");
+    }
     if (c.tgt.ljobs_dev) {
       if ((e = upload_layered_jobs(c, c.tgt, false)) != hipSuccess ||
           (has_draft && (e = upload_layered_jobs(c, c.drf, true)) != hipSuccess))
@@ -839,6 +875,13 @@ spec_status spec_debug_state(spec_ctx* ctx, int32_t b, int32_t* host_out) {
     memcpy(host_out, v, sizeof v);
     return SPEC_OK;
   });
+}
+
+spec_status spec_debug_path(const spec_ctx* ctx, int32_t* path) {
+  if (!ctx || !path) return SPEC_E_INVAL;
+  const Ctx& c = ctx->c;
+  *path = c.use_pass ? SPEC_PATH_PERSISTENT : (c.sg ? SPEC_PATH_PACKED : SPEC_PATH_ROWMAJOR);
+  return SPEC_OK;
 }
 
 spec_status spec_debug_pass_timeline(spec_ctx* ctx, int32_t model, unsigned long long* host_out, int64_t capacity,

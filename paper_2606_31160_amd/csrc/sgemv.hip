@@ -1,0 +1,514 @@
+// Balanced weight-streaming GEMV on gfx950 for passes of at most 16 rows.
+//
+// y[m][n] = sum_k x[m][k] W[n][k] over tile-packed weights (sgemv.h): each
+// 16-row x 32-column MFMA operand block is 1 KB contiguous, so every wave
+// load reads 1 KB of consecutive memory and a tile is one contiguous run.
+//
+// Work split.  Whole units (a 16-row tile, or a gate/up tile pair) are dealt
+// round-robin to the G workgroups of a k-slice (unit r*G + g in round r, the
+// last round ragged), so at any moment the workgroups stream neighbouring
+// tiles.  A tile's k-steps (of its slice) are cut into 15 chunks, one per
+// worker wave.
+//
+// Waves.  Waves 1..15 stream weights: each keeps its share of one tile (up to
+// 8 loads of 16 bytes per lane) in flight through a rolling register buffer
+// and multiplies it against x staged once in LDS; a step a wave does not own
+// reads a buffer offset past the matrix, which returns zeros without touching
+// memory, so the step loop has no branches and the workers issue no other
+// memory operation.  Wave 0 (control) sums the 15 partial tiles in a fixed
+// order through double-buffered LDS, one workgroup barrier per tile, and runs
+// the epilogue while the workers already stream the next tile.
+//
+// k-sliced reductions (the down projection, whose input row does not fit in
+// LDS) are finished by the workgroup that arrives last at a tile: each slice's
+// workgroup stores its partial tile, makes it visible with a release fence and
+// counts itself in; the last one reads the partials back in slice order, adds
+// them and runs the epilogue, and resets the counter for the next launch.
+// Sums are therefore deterministic.
+//
+// Epilogues (RMSNorm is applied as a per-row 1/rms from the producer's
+// per-16-column sums of squares):
+//   SG_ROPE    q/k/v: rotation of q and k pairs at each row's position
+//              (Eq. rope-3d / Eq. flatrope-proj via the per-row (cos, sin)),
+//              query store, K and V^T cache append
+//   SG_RESID   o: residual add, bf16(x * g) and sums of x^2 for the next norm
+//   SG_SWIGLU  gate/up tile pairs: silu(gate) * up
+//   SG_DOWN    down: as SG_RESID; on a draft pass's last layer only each
+//              sequence's last live row, stored as row b
+//   SG_ARGMAX  LM head: per-tile (max, index), optional bf16 logits
+#include <hip/hip_runtime.h>
+#include <hip/hip_ext.h>
+
+#include <algorithm>
+#include <cmath>
+
+#include "ctx.h"
+#include "device.h"
+#include "sgemv.h"
+
+namespace specdec {
+
+namespace {
+
+#define SG_GLOBAL __attribute__((address_space(1)))
+
+constexpr int kOut = 0x7FFFFF00;          // buffer offset past every packed matrix (they are < kOut bytes)
+constexpr int kRsrcWord3 = 0x00020000;    // raw buffer resource, 32-bit data
+constexpr int kSsParts = kSgWaves * 64 / 16;   // partial sums of squares per row
+
+__device__ __forceinline__ f32x4 ld_coh(const float* p) {
+  const SG_GLOBAL uint64_t* q = (const SG_GLOBAL uint64_t*)(p);
+  const uint64_t a = __hip_atomic_load(q, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  const uint64_t b = __hip_atomic_load(q + 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  return f32x4{__uint_as_float((uint32_t)a), __uint_as_float((uint32_t)(a >> 32)), __uint_as_float((uint32_t)b),
+               __uint_as_float((uint32_t)(b >> 32))};
+}
+
+// Workgroup barrier that waits for this wave's LDS operations only (global
+// loads and stores stay in flight).  The memory clobber keeps the compiler
+// from moving LDS accesses across it.
+__device__ __forceinline__ void lds_barrier() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
+
+// Per-lane row facts the control wave needs (lane's row m = lane & 15).
+struct RowInfo {
+  bool live;       // row m < M and inside its sequence's current row count
+  int b, jr;       // sequence and row within it
+  int count;       // that sequence's row count
+  int slot, page;  // SG_ROPE: cache slot and its page
+  int want_logits;
+  float inv_rms;
+};
+
+template <int EPI>
+__device__ __forceinline__ void epilogue(const SgJob& j, const RowInfo& ri, int u, f32x4 ya, f32x4 yb, f32x4 pa,
+                                         u32x2 pb) {
+  const int lane = threadIdx.x & 63, m = lane & 15, grp = lane >> 4;
+  const int M = j.M;
+  if constexpr (EPI == SG_ROPE) {
+    if (ri.live) {
+      const int D = j.D, n0 = 16 * u, head = n0 / D, d0 = (n0 % D) / 2 + 2 * grp;
+      const float s = ri.inv_rms;
+      const float e0 = ya.x * s, o0 = ya.y * s, e1 = ya.z * s, o1 = ya.w * s;
+      const int off = ri.slot % kAttnChunk;
+      if (head < j.nq + j.nkv) {
+        const uint32_t w0 = pack2(e0 * pa.x - o0 * pa.y, e0 * pa.y + o0 * pa.x);
+        const uint32_t w1 = pack2(e1 * pa.z - o1 * pa.w, e1 * pa.w + o1 * pa.z);
+        if (head < j.nq) {
+          *reinterpret_cast<u32x2*>(j.q + ((size_t)m * j.nq + head) * D + 2 * d0) = u32x2{w0, w1};
+        } else {
+          const size_t pg = (size_t)ri.page * j.nkv + (head - j.nq);
+          *reinterpret_cast<u32x2*>(j.kc + (pg * kAttnChunk + off) * D + 2 * d0) = u32x2{w0, w1};
+        }
+      } else {
+        const size_t pg = (size_t)ri.page * j.nkv + (head - j.nq - j.nkv);
+        bf16_t* vp = j.vt + (pg * D + 2 * d0) * kAttnChunk + off;
+        vp[0] = f2bf(e0);
+        vp[kAttnChunk] = f2bf(o0);
+        vp[2 * kAttnChunk] = f2bf(e1);
+        vp[3 * kAttnChunk] = f2bf(o1);
+      }
+    }
+  } else if constexpr (EPI == SG_RESID || EPI == SG_DOWN) {
+    const int n = 16 * u + 4 * grp;
+    f32x4 xn = pa;
+    if (ri.live) {
+      xn += ya;
+      *reinterpret_cast<f32x4*>(j.x32 + (size_t)m * j.H + n) = xn;
+    }
+    float sq = xn.x * xn.x + xn.y * xn.y + xn.z * xn.z + xn.w * xn.w;
+    sq += __shfl_xor(sq, 16);
+    sq += __shfl_xor(sq, 32);
+    bool write = m < M;
+    int out = m;
+    if (EPI == SG_DOWN && j.select_last) {
+      write = ri.live && ri.jr == ri.count - 1;
+      out = ri.b;
+    }
+    if (write) {
+      const float g0 = __uint_as_float(pb.x << 16), g1 = __uint_as_float(pb.x & 0xffff0000u);
+      const float g2 = __uint_as_float(pb.y << 16), g3 = __uint_as_float(pb.y & 0xffff0000u);
+      *reinterpret_cast<u32x2*>(j.xg + (size_t)out * j.H + n) =
+          u32x2{pack2(xn.x * g0, xn.y * g1), pack2(xn.z * g2, xn.w * g3)};
+      if (grp == 0) j.ss_out[(size_t)u * j.mpad + out] = sq;
+    }
+  } else if constexpr (EPI == SG_SWIGLU) {
+    if (m < M) {
+      const float s = ri.inv_rms;
+      const f32x4 g = ya * s, up = yb * s;
+      float r[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) r[i] = g[i] / (1.f + expf(-g[i])) * up[i];
+      const int F = j.ntiles * 8;
+      *reinterpret_cast<u32x2*>(j.u + (size_t)m * F + 16 * u + 4 * grp) = u32x2{pack2(r[0], r[1]), pack2(r[2], r[3])};
+    }
+  } else {   // SG_ARGMAX
+    const f32x4 y = ya * ri.inv_rms;
+    const int N = j.ntiles * 16, n = 16 * u + 4 * grp;
+    if (j.allow_logits && m < M && ri.want_logits)
+      *reinterpret_cast<u32x2*>(j.logits + (size_t)m * N + n) = u32x2{pack2(y.x, y.y), pack2(y.z, y.w)};
+    float best = -INFINITY;
+    int bi = n;
+    int nan = 0;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      float v = y[i];
+      if (v != v) {
+        nan = 1;
+        v = -INFINITY;
+      }
+      if (v > best) {
+        best = v;
+        bi = n + i;
+      }
+    }
+#pragma unroll
+    for (int o = 16; o <= 32; o <<= 1) {
+      const float v2 = __shfl_xor(best, o);
+      const int i2 = __shfl_xor(bi, o);
+      nan |= __shfl_xor(nan, o);
+      amax_merge(best, bi, v2, i2);
+    }
+    if (grp == 0 && m < M) {
+      j.amax_v[(size_t)u * j.mpad + m] = best;
+      j.amax_i[(size_t)u * j.mpad + m] = bi;
+      if (nan) atomicOr(const_cast<int32_t*>(&j.st[ri.b].err), ERR_NUMERIC);
+    }
+  }
+}
+
+// Epilogue inputs of unit u that come from memory: the (cos, sin) of the
+// lane's two rotary pairs, or the residual and the norm gain of its 4 columns.
+template <int EPI>
+__device__ __forceinline__ void epilogue_inputs(const SgJob& j, const RowInfo& ri, int u, f32x4& pa, u32x2& pb) {
+  const int lane = threadIdx.x & 63, m = lane & 15, grp = lane >> 4;
+  pa = f32x4{0.f, 0.f, 0.f, 0.f};
+  pb = u32x2{0u, 0u};
+  if constexpr (EPI == SG_ROPE) {
+    const int D = j.D, n0 = 16 * u, head = n0 / D, d0 = (n0 % D) / 2 + 2 * grp;
+    if (ri.live && head < j.nq + j.nkv)
+      pa = *reinterpret_cast<const f32x4*>(reinterpret_cast<const float*>(j.rcs + (size_t)m * (D / 2) + d0));
+  } else if constexpr (EPI == SG_RESID || EPI == SG_DOWN) {
+    const int n = 16 * u + 4 * grp;
+    if (m < j.M) {
+      pa = *reinterpret_cast<const f32x4*>(j.x32 + (size_t)m * j.H + n);
+      pb = *reinterpret_cast<const u32x2*>(j.gain + n);
+    }
+  }
+}
+
+template <int EPI>
+__global__ __launch_bounds__(kSgWaves * 64) void k_sgemv(const SgJob* __restrict__ jp) {
+  extern __shared__ __align__(16) unsigned char lds[];
+  constexpr bool kPair = EPI == SG_SWIGLU;
+  constexpr int TPU = kPair ? 2 : 1;   // tiles per unit
+  constexpr bool kNorm = EPI == SG_ROPE || EPI == SG_SWIGLU || EPI == SG_ARGMAX;
+  const SgJob& j = *jp;
+  const int wave = __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6));
+  const int lane = threadIdx.x & 63;
+  const int S = j.S, G = j.G, T = j.T, M = j.M;
+  const int sl = blockIdx.x / G, gi = blockIdx.x - sl * G;
+  const int k0 = sl * T / S, k1 = (sl + 1) * T / S, span = k1 - k0;
+  // Units (a tile, or a gate/up tile pair) are dealt round-robin: this
+  // workgroup takes units gi, gi + G, gi + 2G, ... (the last round ragged), so
+  // at any moment the workgroups stream neighbouring tiles.
+  const int units = j.ntiles / TPU;
+  const int n_it = (units / G + (gi < units % G ? 1 : 0)) * TPU;   // tiles of this workgroup
+  auto tile_of = [&](int it) { return ((it / TPU) * G + gi) * TPU + it % TPU; };
+  const int per_row = span * 4, xst = per_row + 1;
+  u32x4* xs = reinterpret_cast<u32x4*>(lds);
+  f32x4* red = reinterpret_cast<f32x4*>(lds + (size_t)M * xst * 16);                        // [2][workers][64]
+  int* pend = reinterpret_cast<int*>(lds + (size_t)M * xst * 16 + 2 * kSgWorkers * 64 * 16);   // [kSgPendMax + 4]
+  float* ssp = reinterpret_cast<float*>(pend + kSgPendMax + 4);                                // [kSsParts][16]
+
+  // live rows: lane b reads sequence b's row count, then an OR across lanes
+  uint32_t live = 0;
+  {
+    const int nseq = (M + j.rps - 1) / j.rps;
+    if (lane < nseq) {
+      const int n = min(j.st[lane].count, j.rps);
+      if (n > 0) live = ((1u << n) - 1u) << (lane * j.rps);
+    }
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) live |= (uint32_t)__shfl_xor((int)live, o);
+    live = (uint32_t)__builtin_amdgcn_readfirstlane((int)live) & ((1u << M) - 1u);
+  }
+
+  // workers: the first tile's weights into the rolling buffer
+  const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(const_cast<bf16_t*>(j.w), 0,
+                                                                      j.ntiles * T * 1024, kRsrcWord3);
+  const int wi = wave - 1;
+  int ws0 = 0, nst = 0;
+  if (wave > 0) {
+    ws0 = k0 + span * wi / kSgWorkers;
+    nst = k0 + span * (wi + 1) / kSgWorkers - ws0;
+  }
+  const int lane_off = lane * 16;
+  u32x4 wv[kSgDepth];
+  if (wave > 0 && n_it > 0) {
+    const int v = (tile_of(0) * T + ws0) * 1024 + lane_off;
+#pragma unroll
+    for (int i = 0; i < kSgDepth; ++i)
+      wv[i] = __builtin_amdgcn_raw_buffer_load_b128(rs, i < nst ? v + 1024 * i : kOut, 0, 0);
+  }
+
+  // x rows of this slice -> LDS (dead rows and columns past Kd as zeros);
+  // rows are padded by 16 bytes so the 16 rows of one MFMA operand spread
+  // over the LDS banks.  Each thread issues a batch of loads before its
+  // first store so that their latencies overlap.
+  {
+    constexpr int XB = 8;
+    const int nvec = M * per_row;
+    for (int c0 = threadIdx.x; c0 < nvec; c0 += XB * kSgWaves * 64) {   // workgroup-uniform trip count
+      u32x4 v[XB];
+#pragma unroll
+      for (int b = 0; b < XB; ++b) {
+        const int c = c0 + b * kSgWaves * 64;
+        const int m = c / per_row, qq = c - m * per_row;
+        const int k = k0 * 32 + qq * 8;
+        v[b] = (c < nvec && ((live >> m) & 1) && k < j.Kd)
+                   ? *reinterpret_cast<const u32x4*>(j.x + (size_t)m * j.ldx + k)
+                   : u32x4{0, 0, 0, 0};
+      }
+#pragma unroll
+      for (int b = 0; b < XB; ++b) {
+        const int c = c0 + b * kSgWaves * 64;
+        const int m = c / per_row, qq = c - m * per_row;
+        if (c < nvec) xs[m * xst + qq] = v[b];
+      }
+    }
+  }
+  // normalised inputs: per-row partial sums of the producer's sums of squares,
+  // kSsParts parts per row (every wave adds them in a fixed order)
+  if constexpr (kNorm) {
+    const int r = threadIdx.x & 15, p = threadIdx.x >> 4;
+    const int ntt = j.Hn / kTile;
+    float v = 0.f;
+    for (int t0 = p; t0 < ntt; t0 += kSsParts * 8) {
+      float tmp[8];
+#pragma unroll
+      for (int b = 0; b < 8; ++b) {
+        const int tt = t0 + kSsParts * b;
+        tmp[b] = tt < ntt ? j.ss_in[(size_t)tt * j.mpad + r] : 0.f;
+      }
+#pragma unroll
+      for (int b = 0; b < 8; ++b) v += tmp[b];
+    }
+    ssp[p * 16 + r] = v;
+  }
+
+  // per-row facts (every wave: all of them may finish split units)
+  RowInfo ri{};
+  {
+    const int m = lane & 15;
+    ri.live = m < M && ((live >> m) & 1);
+    ri.b = m < M ? m / j.rps : 0;
+    ri.jr = m - ri.b * j.rps;
+    ri.count = j.st[ri.b].count;
+    ri.want_logits = j.st[ri.b].want_logits;
+    ri.inv_rms = 1.f;
+    if constexpr (EPI == SG_ROPE) {
+      if (ri.live) {
+        ri.slot = j.st[ri.b].base + ri.jr;
+        ri.page = j.pt[ri.b * j.pps + ri.slot / kAttnChunk];
+      }
+    }
+  }
+  __syncthreads();
+  if constexpr (kNorm) {
+    float v = 0.f;
+    for (int p = 0; p < kSsParts; ++p) v += ssp[p * 16 + (lane & 15)];
+    ri.inv_rms = rsqrtf(v / j.Hn + j.eps);
+  }
+
+  const int m = lane & 15;
+  const bool mok = m < M;
+  const u32x4* xrow = xs + (mok ? m : 0) * xst + (ws0 - k0) * 4 + (lane >> 4);
+  int npend = 0;
+  f32x4 ya = f32x4{0.f, 0.f, 0.f, 0.f}, yb = ya;
+  // The workers and the control wave run separate loops (the branch is on a
+  // wave-uniform value) with one workgroup barrier per tile each, so that
+  // the workers' code holds nothing but weight loads and MFMAs.  The barrier
+  // waits for LDS traffic only: the control wave's stores stay in flight.
+  if (wave > 0) {
+    for (int it = 0; it < n_it; ++it) {
+      const bool na = it + 1 < n_it;
+      const int vn = (tile_of(it + 1) * T + ws0) * 1024 + lane_off;
+      f32x4 acc = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int i = 0; i < kSgDepth; ++i) {
+        const bool on = i < nst;
+        const u32x4 xr = xrow[4 * (on ? i : 0)];
+        const u32x4 xv = (on && mok) ? xr : u32x4{0, 0, 0, 0};
+        acc = mfma16x16x32(wv[i], xv, acc);
+        wv[i] = __builtin_amdgcn_raw_buffer_load_b128(rs, (na && on) ? vn + 1024 * i : kOut, 0, 0);
+      }
+      red[((it & 1) * kSgWorkers + wi) * 64 + lane] = acc;
+      lds_barrier();
+    }
+  } else {
+    for (int it = 0; it < n_it; ++it) {
+      const int t = tile_of(it);
+      f32x4 pa;
+      u32x2 pb;
+      epilogue_inputs<EPI>(j, ri, t / TPU, pa, pb);   // in flight while the workers stream tile t
+      lds_barrier();
+      f32x4 y = red[((it & 1) * kSgWorkers) * 64 + lane];
+#pragma unroll
+      for (int w = 1; w < kSgWorkers; ++w) y += red[((it & 1) * kSgWorkers + w) * 64 + lane];
+      const int u = t / TPU, half = t - u * TPU;
+      if (half == 0) {
+        ya = y;
+        yb = f32x4{0.f, 0.f, 0.f, 0.f};
+      } else {
+        yb = y;
+      }
+      if (half == TPU - 1 || it == n_it - 1) {
+        if (S == 1) {
+          epilogue<EPI>(j, ri, u, ya, yb, pa, pb);
+        } else {
+          const int k = it / TPU;   // partial slot: this workgroup's k-th unit
+          float* pp = j.part + (((size_t)blockIdx.x * j.kmax + k) * 2) * 256;
+          *reinterpret_cast<f32x4*>(pp + lane * 4) = ya;
+          if (kPair) *reinterpret_cast<f32x4*>(pp + 256 + lane * 4) = yb;
+          if (lane == 0) pend[npend] = u;
+          ++npend;
+        }
+        ya = f32x4{0.f, 0.f, 0.f, 0.f};
+      }
+    }
+  }
+
+  // k-sliced reductions: unit u's partials come from workgroup u % G of every
+  // slice, slot u / G.  The control wave counts this workgroup in on all of
+  // its units at once (one atomic per lane); the units it completes last are
+  // then finished by all waves in parallel, each adding the partials of its
+  // unit in slice order.
+  if (wave == 0 && lane == 0) pend[kSgPendMax] = npend;
+  __syncthreads();
+  const int np = pend[kSgPendMax];
+  if (np > 0) {
+    constexpr int kMine = 1 << 30;
+    if (wave == 0) {
+      __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");   // partial stores reach memory first
+      for (int p = lane; p < np; p += 64) {
+        const int u = pend[p];
+        const unsigned old = __hip_atomic_fetch_add(j.cnt + u, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        if (old + 1 == (unsigned)S) pend[p] = u | kMine;
+      }
+    }
+    __syncthreads();
+    for (int p = wave; p < np; p += kSgWaves) {
+      const int e = pend[p];
+      if (!(e & kMine)) continue;
+      const int u = e & ~kMine;
+      f32x4 pa;
+      u32x2 pb;
+      epilogue_inputs<EPI>(j, ri, u, pa, pb);
+      f32x4 sa = f32x4{0.f, 0.f, 0.f, 0.f}, sb = sa;
+      for (int s2 = 0; s2 < S; ++s2) {
+        const float* pp = j.part + (((size_t)(s2 * G + u % G) * j.kmax + u / G) * 2) * 256;
+        sa += ld_coh(pp + lane * 4);
+        if (kPair) sb += ld_coh(pp + 256 + lane * 4);
+      }
+      if (lane == 0) __hip_atomic_store(j.cnt + u, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      epilogue<EPI>(j, ri, u, sa, sb, pa, pb);
+    }
+  }
+}
+
+// Packs row-major weights into the tile layout; one thread per 16-byte block.
+__global__ void k_pack(bf16_t* dst, PackSrc p) {
+  const size_t nvec = (size_t)p.ntiles * p.T * 64;
+  for (size_t v = (size_t)blockIdx.x * blockDim.x + threadIdx.x; v < nvec; v += (size_t)gridDim.x * blockDim.x) {
+    const int lane = (int)(v & 63);
+    const size_t ts = v >> 6;
+    const int step = (int)(ts % p.T), tile = (int)(ts / p.T);
+    const int r = lane & 15, k = step * 32 + 8 * (lane >> 4);
+    const bf16_t* row;
+    if (p.pair) {
+      row = p.seg[tile & 1] + (size_t)((tile >> 1) * 16 + r) * p.Kd;
+    } else {
+      const int n = tile * 16 + r;
+      int sg = 0;
+      for (int i = 1; i < 3; ++i)
+        if (i < p.nseg && n >= p.row0[i]) sg = i;
+      row = p.seg[sg] + (size_t)(n - p.row0[sg]) * p.Kd;
+    }
+    u32x4 val = u32x4{0, 0, 0, 0};
+    if (k < p.Kd) val = *reinterpret_cast<const u32x4*>(row + k);
+    *reinterpret_cast<u32x4*>(dst + v * 8) = val;
+  }
+}
+
+}  // namespace
+
+size_t sg_packed_elems(int ntiles, int T) { return (size_t)ntiles * T * 64 * 8; }
+
+size_t sg_lds_bytes(const SgJob& j) {
+  const int span = (j.T + j.S - 1) / j.S;
+  return (size_t)j.M * (span * 4 + 1) * 16 + 2 * kSgWorkers * 64 * 16 + (kSgPendMax + 4) * sizeof(int) +
+         kSsParts * 16 * sizeof(float);
+}
+
+size_t sg_part_floats(const SgJob& j) { return (size_t)j.S * j.G * j.kmax * 2 * 256; }
+
+bool sg_plan(SgJob& j, int epi, int ncu, int lds_limit) {
+  const int tpu = epi == SG_SWIGLU ? 2 : 1;
+  if (j.ntiles < 1 || j.ntiles % tpu || j.M < 1 || j.M > kSgMaxRows || j.T < 1 || j.rps < 1 || ncu < 1) return false;
+  if ((long long)j.ntiles * j.T * 1024 >= kOut) return false;
+  const int smin = (j.T + kSgMaxSpan - 1) / kSgMaxSpan;
+  int S = smin;
+  for (int s = smin; s <= 2 * smin; ++s)
+    if (ncu % s == 0) {
+      S = s;
+      break;
+    }
+  for (;; ++S) {
+    if (S > j.T) return false;
+    j.S = S;
+    if (sg_lds_bytes(j) <= (size_t)lds_limit) break;
+  }
+  j.units = j.ntiles / tpu;
+  j.G = std::max(1, std::min(ncu / S, j.units));
+  // partial slots (k-sliced reductions): one per unit of a workgroup
+  const int kmax = S > 1 ? (j.units + j.G - 1) / j.G : 1;
+  if (kmax > kSgPendMax) return false;
+  j.kmax = kmax;
+  return true;
+}
+
+hipError_t sg_launch(int epi, const SgJob& h, const SgJob* dev, hipStream_t s, hipEvent_t e0, hipEvent_t e1) {
+  const dim3 grid(h.S * h.G), block(kSgWaves * 64);
+  const uint32_t lds = (uint32_t)sg_lds_bytes(h);
+  switch (epi) {
+    case SG_ROPE: hipExtLaunchKernelGGL(k_sgemv<SG_ROPE>, grid, block, lds, s, e0, e1, 0, dev); break;
+    case SG_RESID: hipExtLaunchKernelGGL(k_sgemv<SG_RESID>, grid, block, lds, s, e0, e1, 0, dev); break;
+    case SG_SWIGLU: hipExtLaunchKernelGGL(k_sgemv<SG_SWIGLU>, grid, block, lds, s, e0, e1, 0, dev); break;
+    case SG_DOWN: hipExtLaunchKernelGGL(k_sgemv<SG_DOWN>, grid, block, lds, s, e0, e1, 0, dev); break;
+    case SG_ARGMAX: hipExtLaunchKernelGGL(k_sgemv<SG_ARGMAX>, grid, block, lds, s, e0, e1, 0, dev); break;
+    default: return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
+
+hipError_t sg_pack(bf16_t* dst, const PackSrc& src, hipStream_t s) {
+  const size_t nvec = (size_t)src.ntiles * src.T * 64;
+  const int blocks = (int)std::min<size_t>((nvec + 255) / 256, 16384);
+  hipLaunchKernelGGL(k_pack, dim3(blocks), dim3(256), 0, s, dst, src);
+  return hipGetLastError();
+}
+
+void sg_set_attributes(int lds_limit) {
+  (void)hipFuncSetAttribute(reinterpret_cast<const void*>(&k_sgemv<SG_ROPE>),
+                            hipFuncAttributeMaxDynamicSharedMemorySize, lds_limit);
+  (void)hipFuncSetAttribute(reinterpret_cast<const void*>(&k_sgemv<SG_RESID>),
+                            hipFuncAttributeMaxDynamicSharedMemorySize, lds_limit);
+  (void)hipFuncSetAttribute(reinterpret_cast<const void*>(&k_sgemv<SG_SWIGLU>),
+                            hipFuncAttributeMaxDynamicSharedMemorySize, lds_limit);
+  (void)hipFuncSetAttribute(reinterpret_cast<const void*>(&k_sgemv<SG_DOWN>),
+                            hipFuncAttributeMaxDynamicSharedMemorySize, lds_limit);
+  (void)hipFuncSetAttribute(reinterpret_cast<const void*>(&k_sgemv<SG_ARGMAX>),
+                            hipFuncAttributeMaxDynamicSharedMemorySize, lds_limit);
+}
+
+}  // namespace specdec

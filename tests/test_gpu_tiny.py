@@ -22,12 +22,13 @@ from tests import _support as S
 pytestmark = pytest.mark.gpu
 
 
-# Every test runs on both execution paths of the library: the persistent
-# pass kernel and one kernel per layer step.
+# Every test runs on the three execution paths of the library: the persistent
+# pass kernel, and one kernel per layer step over the tile-packed weight copy
+# or over the caller's row-major weights.
 _PATH = {"flags": 0}
 
 
-@pytest.fixture(autouse=True, params=["persistent", "layered"])
+@pytest.fixture(autouse=True, params=["persistent", "packed", "rowmajor"])
 def path(request):
     _PATH["flags"] = S.PATH_FLAGS[request.param]
     yield request.param
@@ -394,6 +395,7 @@ def test_requested_execution_path_runs(c1, path):
     n_qkv, _, _ = B.spec_timing_read(s.ctx, "qkv")
     B.spec_timing(s.ctx, False)
     assert s.sync() == 0
+    assert B.spec_debug_path(s.ctx) == path
     if path == "persistent":
         assert (n_pt, n_pd, n_qkv) == (1, w.K, 0)
     else:
