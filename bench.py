@@ -72,8 +72,8 @@ def draft_step_bytes(w, n_ctx):
 CSRC = os.path.join(ROOT, "paper_2606_31160_amd", "csrc")
 TRAFFIC_PASS = os.path.join(ROOT, "profiles", "k_pass_7b_verify_hbm_traffic.txt")
 PASS_SOURCES = [os.path.join(CSRC, f) for f in ("pass.hip", "pass.h", "device.h", "ctx.h")]
-TRAFFIC_GATEUP = os.path.join(ROOT, "profiles", "k_gemv_job_swiglu_7b_verify_hbm_traffic.txt")
-GATEUP_SOURCES = [os.path.join(CSRC, f) for f in ("pass.hip", "pass.h", "device.h", "ctx.h")]
+TRAFFIC_GATEUP = os.path.join(ROOT, "profiles", "k_sgemv_swiglu_7b_verify_hbm_traffic.txt")
+GATEUP_SOURCES = [os.path.join(CSRC, f) for f in ("sgemv.hip", "sgemv.h", "device.h", "ctx.h")]
 
 
 def sources_digest(files):
@@ -354,8 +354,9 @@ def main():
         dom_traffic = measured_traffic(TRAFFIC_PASS, PASS_SOURCES)
     else:
         dom = kernels["gateup"]
-        dom_name = ("k_gemv_job SWIGLU: fused gate/up projection + SwiGLU (gate/up tile pairs, rolling "
-                    "16-step weight buffer), 2x18944x3584 bf16 weights")
+        dom_name = ("k_sgemv<SG_SWIGLU>: fused gate/up projection + SwiGLU over tile-packed weights "
+                    "(gate/up tile pairs dealt round-robin, 15 load-only worker waves + a control wave), "
+                    "2x18944x3584 bf16 weights")
         dom_traffic = measured_traffic(TRAFFIC_GATEUP, GATEUP_SOURCES)
     log("per-kernel timing: " + json.dumps(kernels))
 

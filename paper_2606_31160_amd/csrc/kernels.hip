@@ -1733,7 +1733,9 @@ hipError_t launch_forward(Ctx& c, PassMode mode) {
     else
       CK(gemv_launch_p<EPI_ARGMAX>(c, g, std::min(c.ncu, c.V / kTile), SPEC_KERNEL_LMHEAD, bytes));
   }
-  const int ntiles = c.V / kTile;
+  // (max, index) entries per row the LM head left: one per tile, or one per
+  // workgroup on the packed path
+  const int ntiles = c.sg ? m.sg_host[(size_t)d.layers * 4].amax_n : c.V / kTile;
   Timed t(c, SPEC_KERNEL_OTHER, 0);
   AmaxArgs p{c.st, c.amax_v, c.amax_i, ntiles, c.Mpad, draft ? 1 : c.R, draft ? 1 : 0};
   hipExtLaunchKernelGGL(k_argmax_rows, dim3(draft ? 1 : c.R, c.B), dim3(1024), 0, c.stream, t.e0, t.e1, 0, p);

@@ -67,8 +67,9 @@ struct SgJob {
   // SG_SWIGLU
   bf16_t* u;              // [M][ntiles*8]
   // SG_ARGMAX
-  float* amax_v;          // [ntiles][mpad]
+  float* amax_v;          // [amax_n][mpad] (max, index) of each row per workgroup (per tile when k-sliced)
   int32_t* amax_i;
+  int amax_n;
   bf16_t* logits;         // [M][ntiles*16]
   int allow_logits;
 };

@@ -35,7 +35,8 @@
 //   SG_SWIGLU  gate/up tile pairs: silu(gate) * up
 //   SG_DOWN    down: as SG_RESID; on a draft pass's last layer only each
 //              sequence's last live row, stored as row b
-//   SG_ARGMAX  LM head: per-tile (max, index), optional bf16 logits
+//   SG_ARGMAX  LM head: optional bf16 logits, and the (max, index) of each row
+//              over the workgroup's tiles (per tile when k-sliced)
 #include <hip/hip_runtime.h>
 #include <hip/hip_ext.h>
 
@@ -77,10 +78,14 @@ struct RowInfo {
   int slot, page;  // SG_ROPE: cache slot and its page
   int want_logits;
   float inv_rms;
+  // SG_ARGMAX without k-slices: running (max, index) of the row over this
+  // workgroup's tiles, and whether a NaN was seen
+  float best;
+  int bi, nan;
 };
 
 template <int EPI>
-__device__ __forceinline__ void epilogue(const SgJob& j, const RowInfo& ri, int u, f32x4 ya, f32x4 yb, f32x4 pa,
+__device__ __forceinline__ void epilogue(const SgJob& j, RowInfo& ri, int u, f32x4 ya, f32x4 yb, f32x4 pa,
                                          u32x2 pb) {
   const int lane = threadIdx.x & 63, m = lane & 15, grp = lane >> 4;
   const int M = j.M;
@@ -168,7 +173,12 @@ __device__ __forceinline__ void epilogue(const SgJob& j, const RowInfo& ri, int 
       nan |= __shfl_xor(nan, o);
       amax_merge(best, bi, v2, i2);
     }
-    if (grp == 0 && m < M) {
+    if (j.S == 1) {
+      // one workgroup finishes all of its tiles: keep the row's running best
+      // (ties to the lower index, so the order of tiles does not matter)
+      amax_merge(ri.best, ri.bi, best, bi);
+      ri.nan |= nan;
+    } else if (grp == 0 && m < M) {
       j.amax_v[(size_t)u * j.mpad + m] = best;
       j.amax_i[(size_t)u * j.mpad + m] = bi;
       if (nan) atomicOr(const_cast<int32_t*>(&j.st[ri.b].err), ERR_NUMERIC);
@@ -306,6 +316,9 @@ __global__ __launch_bounds__(kSgWaves * 64) void k_sgemv(const SgJob* __restrict
     ri.count = j.st[ri.b].count;
     ri.want_logits = j.st[ri.b].want_logits;
     ri.inv_rms = 1.f;
+    ri.best = -INFINITY;
+    ri.bi = 0x7fffffff;
+    ri.nan = 0;
     if constexpr (EPI == SG_ROPE) {
       if (ri.live) {
         ri.slot = j.st[ri.b].base + ri.jr;
@@ -375,6 +388,15 @@ __global__ __launch_bounds__(kSgWaves * 64) void k_sgemv(const SgJob* __restrict
         }
         ya = f32x4{0.f, 0.f, 0.f, 0.f};
       }
+    }
+  }
+
+  if constexpr (EPI == SG_ARGMAX) {
+    const int m = lane & 15;
+    if (wave == 0 && S == 1 && lane < 16 && m < M) {   // lanes 0..15 hold rows 0..15
+      j.amax_v[(size_t)gi * j.mpad + m] = ri.best;
+      j.amax_i[(size_t)gi * j.mpad + m] = ri.bi;
+      if (ri.nan) atomicOr(const_cast<int32_t*>(&j.st[ri.b].err), ERR_NUMERIC);
     }
   }
 
@@ -474,6 +496,7 @@ bool sg_plan(SgJob& j, int epi, int ncu, int lds_limit) {
   const int kmax = S > 1 ? (j.units + j.G - 1) / j.G : 1;
   if (kmax > kSgPendMax) return false;
   j.kmax = kmax;
+  j.amax_n = S == 1 ? j.G : j.ntiles;
   return true;
 }
 
