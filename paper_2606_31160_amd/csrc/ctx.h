@@ -77,7 +77,6 @@ struct Model {
   bf16_t* pk = nullptr;
   size_t pk_layer = 0, pk_o = 0, pk_gu = 0, pk_dn = 0;   // elements per layer; offsets inside a layer
   std::vector<SgJob> sg_host;       // [layers][4] (q/k/v, o, gate/up, down) + the LM head
-  SgJob* sg_dev = nullptr;          // device copy
 };
 
 struct TimingRec {
@@ -184,7 +183,6 @@ hipError_t launch_logits_out(Ctx& c, void* d_logits);
 bool sg_build_jobs(Ctx& c, Model& m, bool draft, bool fill);
 hipError_t sg_pack_model(Ctx& c, Model& m);
 hipError_t sg_pack_head(Ctx& c);
-hipError_t sg_upload_jobs(Ctx& c, Model& m);
 
 // Dynamic LDS bytes one GEMV workgroup needs (TT tiles, M rows, span k-steps)
 // and the device limit; k-splits of a GEMV whose workgroups cannot hold all

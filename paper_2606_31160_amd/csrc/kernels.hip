@@ -659,8 +659,13 @@ __global__ __launch_bounds__(256) void k_attn(AttnArgs a) {
   const int b = blockIdx.z;
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int g4 = lane >> 4;
+  // The page of this split is read together with the sequence state (it
+  // depends on the split only; table entries past a sequence's pages name
+  // page 0), so the key and value loads wait for one round trip, not two.
+  const int page = a.pt[b * a.pps + split];
   const SeqState& s = a.st[b];
   const int count = s.count, base = s.base;
+  asm volatile("" ::"s"(page), "s"(count), "s"(base));   // both loads issued before either is awaited
   const int rows = count * a.G;
   const int wrow0 = rb * 64 + wave * 16;
   const int qr = wrow0 + (lane & 15);
@@ -703,7 +708,7 @@ __global__ __launch_bounds__(256) void k_attn(AttnArgs a) {
   bf16_t* Vs = Ks + (size_t)a.chunk * kst;
   {
     constexpr int PER_T = kAttnChunk * D / 8 / 256;   // 16-byte vectors per thread and operand
-    const size_t pg = (size_t)a.pt[b * a.pps + split] * a.nkv + kvh;
+    const size_t pg = (size_t)page * a.nkv + kvh;
     const bf16_t* Kb = a.kc + pg * kAttnChunk * D;
     const bf16_t* Vb = a.vt + pg * D * kAttnChunk;
     const int nvec = a.chunk * (D / 8);                   // per operand
@@ -1155,23 +1160,22 @@ hipError_t run_layer_sg(Ctx& c, Model& m, int li) {
   const int H = d.hidden, D = d.head_dim, nq = d.q_heads, nkv = d.kv_heads, F = d.ffn;
   const int M = c.M;
   const SgJob* hj = m.sg_host.data() + (size_t)li * 4;
-  const SgJob* dj = m.sg_dev + (size_t)li * 4;
   {
     Timed t(c, SPEC_KERNEL_QKV, gemv_bytes((nq + 2 * nkv) * D, H, M, 2.0));
-    CK(sg_launch(SG_ROPE, hj[0], dj + 0, S(c), t.e0, t.e1));
+    CK(sg_launch(SG_ROPE, hj[0], S(c), t.e0, t.e1));
   }
   CK(launch_attention(c, m, li));
   {
     Timed t(c, SPEC_KERNEL_O, gemv_bytes(H, nq * D, M, 10.0));
-    CK(sg_launch(SG_RESID, hj[1], dj + 1, S(c), t.e0, t.e1));
+    CK(sg_launch(SG_RESID, hj[1], S(c), t.e0, t.e1));
   }
   {
     Timed t(c, SPEC_KERNEL_GATEUP, gemv_bytes(2 * F, H, M, 1.0));
-    CK(sg_launch(SG_SWIGLU, hj[2], dj + 2, S(c), t.e0, t.e1));
+    CK(sg_launch(SG_SWIGLU, hj[2], S(c), t.e0, t.e1));
   }
   {
     Timed t(c, SPEC_KERNEL_DOWN, gemv_bytes(H, F, M, 10.0));
-    CK(sg_launch(SG_DOWN, hj[3], dj + 3, S(c), t.e0, t.e1));
+    CK(sg_launch(SG_DOWN, hj[3], S(c), t.e0, t.e1));
   }
   return hipSuccess;
 }
@@ -1569,14 +1573,6 @@ hipError_t sg_pack_head(Ctx& c) {
   return sg_pack(c.pk_head, e, c.stream);
 }
 
-hipError_t sg_upload_jobs(Ctx& c, Model& m) {
-  hipError_t e = hipMemcpyAsync(m.sg_dev, m.sg_host.data(), m.sg_host.size() * sizeof(SgJob), hipMemcpyHostToDevice,
-                                c.stream);
-  // the host table must stay put until the copy is done
-  if (e == hipSuccess) e = hipStreamSynchronize(c.stream);
-  return e;
-}
-
 hipError_t launch_zero(Ctx& c, void* p, size_t bytes) {
   const size_t n = bytes / 16;
   if (n == 0) return hipSuccess;
@@ -1711,7 +1707,7 @@ hipError_t launch_forward(Ctx& c, PassMode mode) {
     const double bytes = gemv_bytes(c.V, d.hidden, rows, 0.0) + 8.0 * (c.V / kTile) * rows;
     Timed t(c, SPEC_KERNEL_LMHEAD, bytes);
     const size_t hi = (size_t)d.layers * 4;
-    CK(sg_launch(SG_ARGMAX, m.sg_host[hi], m.sg_dev + hi, S(c), t.e0, t.e1));
+    CK(sg_launch(SG_ARGMAX, m.sg_host[hi], S(c), t.e0, t.e1));
   } else {
     GemvArgs g = gemv_base(c, draft ? c.B : M, draft ? 1 : c.R);
     g.w[0] = c.embed;

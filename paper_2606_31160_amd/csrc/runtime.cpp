@@ -466,10 +466,8 @@ size_t carve(Ctx& c, const spec_config* cfg, const spec_seq_init* seqs, bool has
     c.sg_cnt = cv.take<unsigned>((size_t)units);
     c.pk_head = cv.take<bf16_t>(sg_packed_elems(L.V / kTile, (H + 31) / 32));
     c.tgt.pk = cv.take<bf16_t>(c.tgt.pk_layer * t.layers);
-    c.tgt.sg_dev = cv.take<SgJob>(c.tgt.sg_host.size());
     if (has_draft) {
       c.drf.pk = cv.take<bf16_t>(c.drf.pk_layer * cfg->draft.layers);
-      c.drf.sg_dev = cv.take<SgJob>(c.drf.sg_host.size());
     }
   }
   return align_up(cv.off, kAlign);
@@ -741,8 +739,7 @@ spec_status spec_init(const spec_config* cfg, const void* embed, const spec_mode
         return SPEC_E_INVAL;
       }
       if ((e = sg_pack_head(c)) != hipSuccess || (e = sg_pack_model(c, c.tgt)) != hipSuccess ||
-          (has_draft && (e = sg_pack_model(c, c.drf)) != hipSuccess) || (e = sg_upload_jobs(c, c.tgt)) != hipSuccess ||
-          (has_draft && (e = sg_upload_jobs(c, c.drf)) != hipSuccess))
+          (has_draft && (e = sg_pack_model(c, c.drf)) != hipSuccess))
         return hip_fail(e, "weight packing");
     }
     if (c.tgt.ljobs_dev) {

@@ -34,8 +34,8 @@ struct PackSrc {
   int ntiles, T;          // packed tiles and steps
 };
 
-// One projection of one layer (built on the host, read by the kernel from
-// device memory).
+// One projection of one layer (built on the host at set-up, passed to the
+// kernel by value).
 struct SgJob {
   const bf16_t* w;        // packed weights [ntiles][T] blocks
   int ntiles, T;
@@ -80,8 +80,7 @@ bool sg_plan(SgJob& j, int epi, int ncu, int lds_limit);
 size_t sg_lds_bytes(const SgJob& j);
 size_t sg_part_floats(const SgJob& j);
 size_t sg_packed_elems(int ntiles, int T);
-hipError_t sg_launch(int epi, const SgJob& host_job, const SgJob* dev_job, hipStream_t s, hipEvent_t e0,
-                     hipEvent_t e1);
+hipError_t sg_launch(int epi, const SgJob& job, hipStream_t s, hipEvent_t e0, hipEvent_t e1);
 hipError_t sg_pack(bf16_t* dst, const PackSrc& src, hipStream_t s);
 void sg_set_attributes(int lds_limit);
 

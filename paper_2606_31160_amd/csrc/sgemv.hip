@@ -12,7 +12,8 @@
 //
 // Waves.  Waves 1..15 stream weights: each keeps its share of one tile (up to
 // 8 loads of 16 bytes per lane) in flight through a rolling register buffer
-// and multiplies it against x staged once in LDS; a step a wave does not own
+// and multiplies it against the x operands of its k-steps, which it loads
+// once into registers (the same for every tile); a step a wave does not own
 // reads a buffer offset past the matrix, which returns zeros without touching
 // memory, so the step loop has no branches and the workers issue no other
 // memory operation.  Wave 0 (control) sums the 15 partial tiles in a fixed
@@ -55,7 +56,6 @@ namespace {
 
 constexpr int kOut = 0x7FFFFF00;          // buffer offset past every packed matrix (they are < kOut bytes)
 constexpr int kRsrcWord3 = 0x00020000;    // raw buffer resource, 32-bit data
-constexpr int kSsParts = kSgWaves * 64 / 16;   // partial sums of squares per row
 
 __device__ __forceinline__ f32x4 ld_coh(const float* p) {
   const SG_GLOBAL uint64_t* q = (const SG_GLOBAL uint64_t*)(p);
@@ -206,13 +206,15 @@ __device__ __forceinline__ void epilogue_inputs(const SgJob& j, const RowInfo& r
   }
 }
 
+// The job is a kernel argument (not a pointer to it) so that its fields
+// arrive with the launch: the weight and activation loads do not wait for a
+// memory round trip to fetch their addresses first.
 template <int EPI>
-__global__ __launch_bounds__(kSgWaves * 64) void k_sgemv(const SgJob* __restrict__ jp) {
+__global__ __launch_bounds__(kSgWaves * 64) void k_sgemv(const SgJob j) {
   extern __shared__ __align__(16) unsigned char lds[];
   constexpr bool kPair = EPI == SG_SWIGLU;
   constexpr int TPU = kPair ? 2 : 1;   // tiles per unit
   constexpr bool kNorm = EPI == SG_ROPE || EPI == SG_SWIGLU || EPI == SG_ARGMAX;
-  const SgJob& j = *jp;
   const int wave = __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6));
   const int lane = threadIdx.x & 63;
   const int S = j.S, G = j.G, T = j.T, M = j.M;
@@ -224,94 +226,66 @@ __global__ __launch_bounds__(kSgWaves * 64) void k_sgemv(const SgJob* __restrict
   const int units = j.ntiles / TPU;
   const int n_it = (units / G + (gi < units % G ? 1 : 0)) * TPU;   // tiles of this workgroup
   auto tile_of = [&](int it) { return ((it / TPU) * G + gi) * TPU + it % TPU; };
-  const int per_row = span * 4, xst = per_row + 1;
-  u32x4* xs = reinterpret_cast<u32x4*>(lds);
-  f32x4* red = reinterpret_cast<f32x4*>(lds + (size_t)M * xst * 16);                        // [2][workers][64]
-  int* pend = reinterpret_cast<int*>(lds + (size_t)M * xst * 16 + 2 * kSgWorkers * 64 * 16);   // [kSgPendMax + 4]
-  float* ssp = reinterpret_cast<float*>(pend + kSgPendMax + 4);                                // [kSsParts][16]
+  f32x4* red = reinterpret_cast<f32x4*>(lds);                                          // [2][workers][64]
+  int* pend = reinterpret_cast<int*>(lds + 2 * kSgWorkers * 64 * 16);                  // [kSgPendMax + 4]
+  float* rms_sh = reinterpret_cast<float*>(pend + kSgPendMax + 4);                     // [16] 1/rms per row
 
-  // live rows: lane b reads sequence b's row count, then an OR across lanes
-  uint32_t live = 0;
-  {
-    const int nseq = (M + j.rps - 1) / j.rps;
-    if (lane < nseq) {
-      const int n = min(j.st[lane].count, j.rps);
-      if (n > 0) live = ((1u << n) - 1u) << (lane * j.rps);
-    }
-#pragma unroll
-    for (int o = 1; o < 64; o <<= 1) live |= (uint32_t)__shfl_xor((int)live, o);
-    live = (uint32_t)__builtin_amdgcn_readfirstlane((int)live) & ((1u << M) - 1u);
-  }
-
-  // workers: the first tile's weights into the rolling buffer
-  const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(const_cast<bf16_t*>(j.w), 0,
-                                                                      j.ntiles * T * 1024, kRsrcWord3);
+  // Worker w owns k-steps [ws0, ws0 + nst) of every tile of this slice.
   const int wi = wave - 1;
   int ws0 = 0, nst = 0;
   if (wave > 0) {
     ws0 = k0 + span * wi / kSgWorkers;
     nst = k0 + span * (wi + 1) / kSgWorkers - ws0;
   }
+  const int m = lane & 15, grp = lane >> 4;
+  const bool mok = m < M;
+
+  // Issue order (vector memory returns in order per wave): a worker first
+  // loads its x operands (the same for every tile, so they stay in registers:
+  // lane (m, g) holds x[m][32 s + 8 g .. +8] of its step s), then the first
+  // tile's weights, so that the MFMAs can start as soon as weights arrive.
+  // Rows of dead sequences are zeroed once the live mask is known.
+  u32x4 xv[kSgDepth];
+  const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(const_cast<bf16_t*>(j.w), 0,
+                                                                      j.ntiles * T * 1024, kRsrcWord3);
   const int lane_off = lane * 16;
   u32x4 wv[kSgDepth];
-  if (wave > 0 && n_it > 0) {
-    const int v = (tile_of(0) * T + ws0) * 1024 + lane_off;
+  if (wave > 0) {
 #pragma unroll
-    for (int i = 0; i < kSgDepth; ++i)
-      wv[i] = __builtin_amdgcn_raw_buffer_load_b128(rs, i < nst ? v + 1024 * i : kOut, 0, 0);
+    for (int i = 0; i < kSgDepth; ++i) {
+      const int k = (ws0 + i) * 32 + 8 * grp;
+      xv[i] = (i < nst && mok && k < j.Kd) ? *reinterpret_cast<const u32x4*>(j.x + (size_t)m * j.ldx + k)
+                                             : u32x4{0, 0, 0, 0};
+    }
+    if (n_it > 0) {
+      const int v = (tile_of(0) * T + ws0) * 1024 + lane_off;
+#pragma unroll
+      for (int i = 0; i < kSgDepth; ++i)
+        wv[i] = __builtin_amdgcn_raw_buffer_load_b128(rs, i < nst ? v + 1024 * i : kOut, 0, 0);
+    }
   }
 
-  // x rows of this slice -> LDS (dead rows and columns past Kd as zeros);
-  // rows are padded by 16 bytes so the 16 rows of one MFMA operand spread
-  // over the LDS banks.  Each thread issues a batch of loads before its
-  // first store so that their latencies overlap.
+  // live rows: sequence b's rows are live below its row count (scalar loads)
+  uint32_t live = 0;
   {
-    constexpr int XB = 8;
-    const int nvec = M * per_row;
-    for (int c0 = threadIdx.x; c0 < nvec; c0 += XB * kSgWaves * 64) {   // workgroup-uniform trip count
-      u32x4 v[XB];
-#pragma unroll
-      for (int b = 0; b < XB; ++b) {
-        const int c = c0 + b * kSgWaves * 64;
-        const int m = c / per_row, qq = c - m * per_row;
-        const int k = k0 * 32 + qq * 8;
-        v[b] = (c < nvec && ((live >> m) & 1) && k < j.Kd)
-                   ? *reinterpret_cast<const u32x4*>(j.x + (size_t)m * j.ldx + k)
-                   : u32x4{0, 0, 0, 0};
-      }
-#pragma unroll
-      for (int b = 0; b < XB; ++b) {
-        const int c = c0 + b * kSgWaves * 64;
-        const int m = c / per_row, qq = c - m * per_row;
-        if (c < nvec) xs[m * xst + qq] = v[b];
-      }
+    const int nseq = (M + j.rps - 1) / j.rps;
+    for (int b = 0; b < nseq; ++b) {
+      const int n = min(j.st[b].count, j.rps);
+      if (n > 0) live |= ((1u << n) - 1u) << (b * j.rps);
     }
+    live &= (1u << M) - 1u;
   }
-  // normalised inputs: per-row partial sums of the producer's sums of squares,
-  // kSsParts parts per row (every wave adds them in a fixed order)
-  if constexpr (kNorm) {
-    const int r = threadIdx.x & 15, p = threadIdx.x >> 4;
-    const int ntt = j.Hn / kTile;
-    float v = 0.f;
-    for (int t0 = p; t0 < ntt; t0 += kSsParts * 8) {
-      float tmp[8];
+  if (wave > 0 && !((live >> m) & 1)) {
 #pragma unroll
-      for (int b = 0; b < 8; ++b) {
-        const int tt = t0 + kSsParts * b;
-        tmp[b] = tt < ntt ? j.ss_in[(size_t)tt * j.mpad + r] : 0.f;
-      }
-#pragma unroll
-      for (int b = 0; b < 8; ++b) v += tmp[b];
-    }
-    ssp[p * 16 + r] = v;
+    for (int i = 0; i < kSgDepth; ++i) xv[i] = u32x4{0, 0, 0, 0};
   }
 
-  // per-row facts (every wave: all of them may finish split units)
+  // per-row facts of the lane's row m (the control wave now; the other waves
+  // fill theirs before finishing split units)
   RowInfo ri{};
-  {
-    const int m = lane & 15;
-    ri.live = m < M && ((live >> m) & 1);
-    ri.b = m < M ? m / j.rps : 0;
+  auto row_info = [&]() {
+    ri.live = mok && ((live >> m) & 1);
+    ri.b = mok ? m / j.rps : 0;
     ri.jr = m - ri.b * j.rps;
     ri.count = j.st[ri.b].count;
     ri.want_logits = j.st[ri.b].want_logits;
@@ -325,17 +299,47 @@ __global__ __launch_bounds__(kSgWaves * 64) void k_sgemv(const SgJob* __restrict
         ri.page = j.pt[ri.b * j.pps + ri.slot / kAttnChunk];
       }
     }
-  }
-  __syncthreads();
-  if constexpr (kNorm) {
-    float v = 0.f;
-    for (int p = 0; p < kSsParts; ++p) v += ssp[p * 16 + (lane & 15)];
-    ri.inv_rms = rsqrtf(v / j.Hn + j.eps);
+  };
+  if (wave == 0) {
+    row_info();
+    // normalised inputs: 1/rms of row m from the producer's per-16-column
+    // sums of squares; lane (m, g) adds the sums t = g, g + 4, ... and the
+    // four lane groups are added in a fixed order
+    if constexpr (kNorm) {
+      // lane (t, q) reads rows 4q..4q+3 of sum t = lane / 4, 16 sums per
+      // load; the 16 lanes of each q are then added by an xor butterfly,
+      // which gives every lane bit-identical totals
+      const int ntt = j.Hn / kTile;
+      const int q = lane & 3;
+      f32x4 acc4 = f32x4{0.f, 0.f, 0.f, 0.f};
+      for (int t0 = lane >> 2; t0 < ntt; t0 += 16 * 8) {
+        f32x4 tmp[8];
+#pragma unroll
+        for (int b = 0; b < 8; ++b) {
+          const int tt = t0 + 16 * b;
+          tmp[b] = tt < ntt ? *reinterpret_cast<const f32x4*>(j.ss_in + (size_t)tt * j.mpad + 4 * q)
+                            : f32x4{0.f, 0.f, 0.f, 0.f};
+        }
+#pragma unroll
+        for (int b = 0; b < 8; ++b) acc4 += tmp[b];
+      }
+#pragma unroll
+      for (int o = 4; o < 64; o <<= 1) {
+        acc4.x += __shfl_xor(acc4.x, o);
+        acc4.y += __shfl_xor(acc4.y, o);
+        acc4.z += __shfl_xor(acc4.z, o);
+        acc4.w += __shfl_xor(acc4.w, o);
+      }
+      const int src = m >> 2;
+      const float c0 = __shfl(acc4.x, src), c1 = __shfl(acc4.y, src), c2 = __shfl(acc4.z, src),
+                  c3 = __shfl(acc4.w, src);
+      const int c = m & 3;
+      const float sum = c == 0 ? c0 : c == 1 ? c1 : c == 2 ? c2 : c3;
+      ri.inv_rms = rsqrtf(sum / j.Hn + j.eps);
+      if (lane < 16) rms_sh[lane] = ri.inv_rms;
+    }
   }
 
-  const int m = lane & 15;
-  const bool mok = m < M;
-  const u32x4* xrow = xs + (mok ? m : 0) * xst + (ws0 - k0) * 4 + (lane >> 4);
   int npend = 0;
   f32x4 ya = f32x4{0.f, 0.f, 0.f, 0.f}, yb = ya;
   // The workers and the control wave run separate loops (the branch is on a
@@ -350,9 +354,7 @@ __global__ __launch_bounds__(kSgWaves * 64) void k_sgemv(const SgJob* __restrict
 #pragma unroll
       for (int i = 0; i < kSgDepth; ++i) {
         const bool on = i < nst;
-        const u32x4 xr = xrow[4 * (on ? i : 0)];
-        const u32x4 xv = (on && mok) ? xr : u32x4{0, 0, 0, 0};
-        acc = mfma16x16x32(wv[i], xv, acc);
+        acc = mfma16x16x32(wv[i], xv[i], acc);
         wv[i] = __builtin_amdgcn_raw_buffer_load_b128(rs, (na && on) ? vn + 1024 * i : kOut, 0, 0);
       }
       red[((it & 1) * kSgWorkers + wi) * 64 + lane] = acc;
@@ -419,6 +421,10 @@ __global__ __launch_bounds__(kSgWaves * 64) void k_sgemv(const SgJob* __restrict
       }
     }
     __syncthreads();
+    if (wave > 0) {
+      row_info();
+      if constexpr (kNorm) ri.inv_rms = rms_sh[m];
+    }
     for (int p = wave; p < np; p += kSgWaves) {
       const int e = pend[p];
       if (!(e & kMine)) continue;
@@ -426,11 +432,25 @@ __global__ __launch_bounds__(kSgWaves * 64) void k_sgemv(const SgJob* __restrict
       f32x4 pa;
       u32x2 pb;
       epilogue_inputs<EPI>(j, ri, u, pa, pb);
+      // The partials of up to kBatch slices are loaded together, then added
+      // in slice order: one memory round trip per batch, not per slice.
+      constexpr int kBatch = kPair ? 4 : 8;
       f32x4 sa = f32x4{0.f, 0.f, 0.f, 0.f}, sb = sa;
-      for (int s2 = 0; s2 < S; ++s2) {
-        const float* pp = j.part + (((size_t)(s2 * G + u % G) * j.kmax + u / G) * 2) * 256;
-        sa += ld_coh(pp + lane * 4);
-        if (kPair) sb += ld_coh(pp + 256 + lane * 4);
+      for (int s0 = 0; s0 < S; s0 += kBatch) {
+        f32x4 va[kBatch], vb[kBatch];
+#pragma unroll
+        for (int i = 0; i < kBatch; ++i) {
+          const int s2 = min(s0 + i, S - 1);
+          const float* pp = j.part + (((size_t)(s2 * G + u % G) * j.kmax + u / G) * 2) * 256;
+          va[i] = ld_coh(pp + lane * 4);
+          if (kPair) vb[i] = ld_coh(pp + 256 + lane * 4);
+        }
+#pragma unroll
+        for (int i = 0; i < kBatch; ++i)
+          if (s0 + i < S) {
+            sa += va[i];
+            if (kPair) sb += vb[i];
+          }
       }
       if (lane == 0) __hip_atomic_store(j.cnt + u, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
       epilogue<EPI>(j, ri, u, sa, sb, pa, pb);
@@ -466,10 +486,8 @@ __global__ void k_pack(bf16_t* dst, PackSrc p) {
 
 size_t sg_packed_elems(int ntiles, int T) { return (size_t)ntiles * T * 64 * 8; }
 
-size_t sg_lds_bytes(const SgJob& j) {
-  const int span = (j.T + j.S - 1) / j.S;
-  return (size_t)j.M * (span * 4 + 1) * 16 + 2 * kSgWorkers * 64 * 16 + (kSgPendMax + 4) * sizeof(int) +
-         kSsParts * 16 * sizeof(float);
+size_t sg_lds_bytes(const SgJob&) {
+  return 2 * kSgWorkers * 64 * 16 + (kSgPendMax + 4) * sizeof(int) + 16 * sizeof(float);
 }
 
 size_t sg_part_floats(const SgJob& j) { return (size_t)j.S * j.G * j.kmax * 2 * 256; }
@@ -500,15 +518,15 @@ bool sg_plan(SgJob& j, int epi, int ncu, int lds_limit) {
   return true;
 }
 
-hipError_t sg_launch(int epi, const SgJob& h, const SgJob* dev, hipStream_t s, hipEvent_t e0, hipEvent_t e1) {
+hipError_t sg_launch(int epi, const SgJob& h, hipStream_t s, hipEvent_t e0, hipEvent_t e1) {
   const dim3 grid(h.S * h.G), block(kSgWaves * 64);
   const uint32_t lds = (uint32_t)sg_lds_bytes(h);
   switch (epi) {
-    case SG_ROPE: hipExtLaunchKernelGGL(k_sgemv<SG_ROPE>, grid, block, lds, s, e0, e1, 0, dev); break;
-    case SG_RESID: hipExtLaunchKernelGGL(k_sgemv<SG_RESID>, grid, block, lds, s, e0, e1, 0, dev); break;
-    case SG_SWIGLU: hipExtLaunchKernelGGL(k_sgemv<SG_SWIGLU>, grid, block, lds, s, e0, e1, 0, dev); break;
-    case SG_DOWN: hipExtLaunchKernelGGL(k_sgemv<SG_DOWN>, grid, block, lds, s, e0, e1, 0, dev); break;
-    case SG_ARGMAX: hipExtLaunchKernelGGL(k_sgemv<SG_ARGMAX>, grid, block, lds, s, e0, e1, 0, dev); break;
+    case SG_ROPE: hipExtLaunchKernelGGL(k_sgemv<SG_ROPE>, grid, block, lds, s, e0, e1, 0, h); break;
+    case SG_RESID: hipExtLaunchKernelGGL(k_sgemv<SG_RESID>, grid, block, lds, s, e0, e1, 0, h); break;
+    case SG_SWIGLU: hipExtLaunchKernelGGL(k_sgemv<SG_SWIGLU>, grid, block, lds, s, e0, e1, 0, h); break;
+    case SG_DOWN: hipExtLaunchKernelGGL(k_sgemv<SG_DOWN>, grid, block, lds, s, e0, e1, 0, h); break;
+    case SG_ARGMAX: hipExtLaunchKernelGGL(k_sgemv<SG_ARGMAX>, grid, block, lds, s, e0, e1, 0, h); break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();
