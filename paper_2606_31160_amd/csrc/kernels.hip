@@ -634,17 +634,19 @@ __global__ __launch_bounds__(256) void k_down_finish(FinishArgs p) {
 // Two 16-key tiles give lane l the 8 keys {4g..4g+3, 16+4g..16+4g+3}
 // (g = l>>4) of its row, which is exactly a B operand P^T for O^T = V^T P^T
 // when the 32 k-slots are mapped to keys in that order; the A operand V^T is
-// read from the transposed value cache as two 8-byte loads per lane.  Online
-// softmax statistics are per lane (its row); the row max crosses the four lane
-// groups with two xor-shuffles.
+// read from the transposed value cache as two 8-byte loads per lane.  The
+// softmax statistics of the chunk are per lane (its row); the row max crosses
+// the four lane groups with two xor-shuffles.  Partial outputs are stored
+// unnormalised in bf16, with the chunk's max and sum in fp32, for the combine.
 // ---------------------------------------------------------------------------
+
 struct AttnArgs {
   const SeqState* st;
   const bf16_t* q;       // [Mpad][nq][D]
   const bf16_t* kc;      // layer base of the key pool [pages][nkv][kAttnChunk][D]
   const bf16_t* vt;      // layer base of the value pool [pages][nkv][D][kAttnChunk]
   const int32_t* pt;     // [B][pps] page tables
-  float* op;             // [splits][B][nq][R][D]
+  bf16_t* op;            // [splits][B][nq][R][D] unnormalised partial outputs (bf16)
   float* mp;             // [splits][B][nq][R]
   float* lp;
   int nq, nkv, G, R, B, pps, chunk, row_blocks;
@@ -685,54 +687,59 @@ __global__ __launch_bounds__(256) void k_attn(AttnArgs a) {
       a.lp[oi] = 0.f;
     }
     if (rvalid) {
-      float* op = a.op + oi * D;
-      for (int d = g4 * 4; d < D; d += 16) *reinterpret_cast<f32x4*>(op + d) = f32x4{0.f, 0.f, 0.f, 0.f};
+      bf16_t* op = a.op + oi * D;
+      for (int d = g4 * 4; d < D; d += 16) *reinterpret_cast<u32x2*>(op + d) = u32x2{0u, 0u};
     }
     return;
   }
 
-  // This wave's query rows; issued first so their latency overlaps the staging.
+  // This wave's query rows; issued first so their latency overlaps the
+  // staging.  Loads are unconditional (an invalid lane reads row 0 of its
+  // head): a lane's scores only reach its own row, and those of invalid rows
+  // are masked below.
   u32x4 qf[D / 32];
   {
     const bf16_t* qp = a.q + ((size_t)(b * a.R + j) * a.nq + hq) * D + 8 * g4;
 #pragma unroll
-    for (int t = 0; t < D / 32; ++t) qf[t] = (rvalid && wrow0 < rows) ? ld16(qp + 32 * t) : u32x4{0, 0, 0, 0};
+    for (int t = 0; t < D / 32; ++t) qf[t] = ld16(qp + 32 * t);
   }
 
   // Stage the chunk once for all waves: keys [chunk][D + 8] and values
-  // transposed [D][chunk + 8] (the pads spread rows over the LDS banks).
-  // Keys at or past k1 are stored as zeros.  Every load of the thread is
-  // issued before the first LDS store so that their latencies overlap.
+  // transposed [D][chunk + 8] (the pads spread rows over the LDS banks).  The
+  // whole page is loaded (its slots past k1 hold stale data): keys there only
+  // meet masked scores, values there are stored as zeros.  Every load of the
+  // thread is issued before the first LDS store so that their latencies
+  // overlap, and unconditionally so that no branch splits them.
   const int kst = D + 8, vst = a.chunk + 8;
   bf16_t* Ks = reinterpret_cast<bf16_t*>(lds);
   bf16_t* Vs = Ks + (size_t)a.chunk * kst;
   {
     constexpr int PER_T = kAttnChunk * D / 8 / 256;   // 16-byte vectors per thread and operand
+    static_assert(PER_T * 256 * 8 == kAttnChunk * D, "the threads cover the page exactly");
     const size_t pg = (size_t)page * a.nkv + kvh;
     const bf16_t* Kb = a.kc + pg * kAttnChunk * D;
     const bf16_t* Vb = a.vt + pg * D * kAttnChunk;
-    const int nvec = a.chunk * (D / 8);                   // per operand
-    const int per_row = a.chunk / 8;
+    constexpr int per_row = kAttnChunk / 8;
     u32x4 kr[PER_T], vr[PER_T];
 #pragma unroll
     for (int u = 0; u < PER_T; ++u) {
       const int i = threadIdx.x + 256 * u;
       const int key = i / (D / 8), c8 = i % (D / 8);
-      kr[u] = (i < nvec && k0 + key < k1) ? ld16(Kb + (size_t)key * D + 8 * c8) : u32x4{0, 0, 0, 0};
+      kr[u] = ld16(Kb + (size_t)key * D + 8 * c8);
       const int d = i / per_row, v8 = i % per_row;
-      const int slot = k0 + 8 * v8;
-      vr[u] = (i < nvec && slot < k1) ? ld16(Vb + (size_t)d * kAttnChunk + 8 * v8) : u32x4{0, 0, 0, 0};
+      vr[u] = ld16(Vb + (size_t)d * kAttnChunk + 8 * v8);
     }
 #pragma unroll
     for (int u = 0; u < PER_T; ++u) {
       const int i = threadIdx.x + 256 * u;
-      if (i >= nvec) break;
       const int key = i / (D / 8), c8 = i % (D / 8);
       *reinterpret_cast<u32x4*>(Ks + (size_t)key * kst + 8 * c8) = kr[u];
       const int d = i / per_row, v8 = i % per_row;
       const int slot = k0 + 8 * v8;
       u32x4 v = vr[u];
-      if (slot < k1 && slot + 8 > k1) {             // ragged end of the valid keys
+      if (slot >= k1) {
+        v = u32x4{0, 0, 0, 0};
+      } else if (slot + 8 > k1) {                   // ragged end of the valid keys
         uint32_t w[4] = {v.x, v.y, v.z, v.w};
 #pragma unroll
         for (int e = 0; e < 8; ++e)
@@ -745,63 +752,70 @@ __global__ __launch_bounds__(256) void k_attn(AttnArgs a) {
   __syncthreads();
   if (wrow0 >= rows) return;                        // wave-uniform; no barrier follows
 
-  float m_run = -INFINITY, l_run = 0.f;
+  // The whole chunk (kAttnChunk = 64 keys) in one step: S^T = K Q^T for the
+  // four 16-key groups (lanes own query rows; lane group g4 holds keys
+  // 16h + 4 g4 + i), one softmax over the chunk in log2 units, then
+  // O^T = V^T P^T over the two 32-key halves.  Within a half the key order of
+  // the P^T operand (keys 4 g4 + i and 16 + 4 g4 + i) is the one the V^T
+  // operand is read in, so the contraction is exact.
+  static_assert(kAttnChunk == 4 * 16, "one step covers four 16-key groups");
+  f32x4 sc[4];
+#pragma unroll
+  for (int h = 0; h < 4; ++h) {
+    const bf16_t* kp = Ks + (size_t)(16 * h + (lane & 15)) * kst + 8 * g4;
+    f32x4 acc = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int t = 0; t < D / 32; ++t) acc = mfma16x16x32(*reinterpret_cast<const u32x4*>(kp + 32 * t), qf[t], acc);
+    sc[h] = acc;
+  }
+  // V^T operands of both halves, read while the softmax runs
+  u32x4 va[2][D / 16];
+#pragma unroll
+  for (int hb = 0; hb < 2; ++hb)
+#pragma unroll
+    for (int dt = 0; dt < D / 16; ++dt) {
+      const bf16_t* vp = Vs + (size_t)(16 * dt + (lane & 15)) * vst + 32 * hb + 4 * g4;
+      const u32x2 lo = *reinterpret_cast<const u32x2*>(vp), hi = *reinterpret_cast<const u32x2*>(vp + 16);
+      va[hb][dt] = u32x4{lo.x, lo.y, hi.x, hi.y};
+    }
+  float p[16];
+  float m_run = -INFINITY;
+#pragma unroll
+  for (int h = 0; h < 4; ++h)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int key = k0 + 16 * h + 4 * g4 + i;
+      const bool ok = rvalid && key < k1 && key < vis_end;
+      const float v = ok ? sc[h][i] * a.scale_log2 : -INFINITY;
+      p[h * 4 + i] = v;
+      m_run = fmaxf(m_run, v);
+    }
+  m_run = fmaxf(m_run, __shfl_xor(m_run, 16));
+  m_run = fmaxf(m_run, __shfl_xor(m_run, 32));
+  float l_run = 0.f;
+#pragma unroll
+  for (int i = 0; i < 16; ++i) {
+    p[i] = (p[i] == -INFINITY) ? 0.f : exp2f(p[i] - m_run);
+    l_run += p[i];
+  }
   f32x4 o[D / 16];
 #pragma unroll
   for (int dt = 0; dt < D / 16; ++dt) o[dt] = f32x4{0.f, 0.f, 0.f, 0.f};
-
-  // One 32-key block: S^T = K Q^T (lanes own query rows), online softmax in
-  // log2 units, then O^T += V^T P^T.  The key order inside the block is the
-  // same permutation on the P^T and V^T operands, so the contraction is exact.
-  for (int kb = 0; kb < k1 - k0; kb += kKeyBlock) {
-    f32x4 sc[2];
 #pragma unroll
-    for (int h2 = 0; h2 < 2; ++h2) {
-      const bf16_t* kp = Ks + (size_t)(kb + 16 * h2 + (lane & 15)) * kst + 8 * g4;
-      f32x4 acc = f32x4{0.f, 0.f, 0.f, 0.f};
+  for (int hb = 0; hb < 2; ++hb) {
+    const float* ph = p + 8 * hb;
+    const u32x4 pb = u32x4{pack2(ph[0], ph[1]), pack2(ph[2], ph[3]), pack2(ph[4], ph[5]), pack2(ph[6], ph[7])};
 #pragma unroll
-      for (int t = 0; t < D / 32; ++t)
-        acc = mfma16x16x32(*reinterpret_cast<const u32x4*>(kp + 32 * t), qf[t], acc);
-      sc[h2] = acc;
-    }
-    float p[8];
-    float bm = -INFINITY;
-#pragma unroll
-    for (int h2 = 0; h2 < 2; ++h2)
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int key = k0 + kb + 16 * h2 + 4 * g4 + i;
-        const bool ok = rvalid && key < k1 && key < vis_end;
-        const float v = ok ? sc[h2][i] * a.scale_log2 : -INFINITY;
-        p[h2 * 4 + i] = v;
-        bm = fmaxf(bm, v);
-      }
-    bm = fmaxf(bm, __shfl_xor(bm, 16));
-    bm = fmaxf(bm, __shfl_xor(bm, 32));
-    const float m_new = fmaxf(m_run, bm);
-    const float alpha = (m_run == -INFINITY) ? 0.f : exp2f(m_run - m_new);
-    float ps = 0.f;
-#pragma unroll
-    for (int i = 0; i < 8; ++i) {
-      p[i] = (p[i] == -INFINITY) ? 0.f : exp2f(p[i] - m_new);
-      ps += p[i];
-    }
-    l_run = l_run * alpha + ps;
-    m_run = m_new;
-    const u32x4 pb = u32x4{pack2(p[0], p[1]), pack2(p[2], p[3]), pack2(p[4], p[5]), pack2(p[6], p[7])};
-#pragma unroll
-    for (int dt = 0; dt < D / 16; ++dt) {
-      const bf16_t* vp = Vs + (size_t)(16 * dt + (lane & 15)) * vst + kb + 4 * g4;
-      const u32x2 lo = *reinterpret_cast<const u32x2*>(vp), hi = *reinterpret_cast<const u32x2*>(vp + 16);
-      o[dt] = mfma16x16x32(u32x4{lo.x, lo.y, hi.x, hi.y}, pb, o[dt] * alpha);
-    }
+    for (int dt = 0; dt < D / 16; ++dt) o[dt] = mfma16x16x32(va[hb][dt], pb, o[dt]);
   }
   l_run += __shfl_xor(l_run, 16);
   l_run += __shfl_xor(l_run, 32);
   if (rvalid) {
-    float* op = a.op + oi * D;
+    bf16_t* op = a.op + oi * D;
 #pragma unroll
-    for (int dt = 0; dt < D / 16; ++dt) *reinterpret_cast<f32x4*>(op + 16 * dt + 4 * g4) = o[dt];
+    for (int dt = 0; dt < D / 16; ++dt)
+      *reinterpret_cast<u32x2*>(op + 16 * dt + 4 * g4) =
+          u32x2{pack2(o[dt].x, o[dt].y), pack2(o[dt].z, o[dt].w)};
     if (g4 == 0) {
       a.mp[oi] = m_run;
       a.lp[oi] = l_run;
@@ -817,7 +831,8 @@ size_t attn_lds_bytes(int chunk, int D) {
 // 2^(m_s - M) l_s.  grid (R, q_heads, B), 256 threads: 8 groups of splits x 32 groups of 4 columns.
 struct CombineArgs {
   const SeqState* st;
-  const float *op, *mp, *lp;
+  const bf16_t* op;      // bf16 partial outputs
+  const float *mp, *lp;
   bf16_t* o;             // [Mpad][nq*D]
   int nq, D, R, B, chunk;
 };
@@ -852,10 +867,15 @@ __global__ __launch_bounds__(256) void k_attn_combine(CombineArgs a) {
   const int c4 = threadIdx.x & 31, sg = threadIdx.x >> 5;
   f32x4 v = f32x4{0.f, 0.f, 0.f, 0.f};
   if (4 * c4 < a.D) {
-    const float* src = a.op + row * a.D + 4 * c4;
+    const bf16_t* src = a.op + row * a.D + 4 * c4;
     const size_t ostride = sstride * a.D;
 #pragma unroll 4
-    for (int sp = sg; sp < ns; sp += 8) v += coef[sp] * *reinterpret_cast<const f32x4*>(src + sp * ostride);
+    for (int sp = sg; sp < ns; sp += 8) {
+      const u32x2 w = *reinterpret_cast<const u32x2*>(src + sp * ostride);
+      const f32x4 ov = f32x4{__uint_as_float(w.x << 16), __uint_as_float(w.x & 0xffff0000u),
+                             __uint_as_float(w.y << 16), __uint_as_float(w.y & 0xffff0000u)};
+      v += coef[sp] * ov;
+    }
     *reinterpret_cast<f32x4*>(part + sg * a.D + 4 * c4) = v;
   }
   __syncthreads();
@@ -1135,7 +1155,7 @@ hipError_t launch_attention(Ctx& c, Model& m, int li) {
   bf16_t* vt = m.vt + m.kv_layer * li;
   const int G = nq / nkv;
   const int rb = (c.R * G + 63) / 64;
-  AttnArgs p{c.st, c.q, kc, vt, c.pt, c.op, c.mp, c.lp, nq, nkv, G, c.R, c.B, c.pps, c.attn_chunk, rb,
+  AttnArgs p{c.st, c.q, kc, vt, c.pt, reinterpret_cast<bf16_t*>(c.op), c.mp, c.lp, nq, nkv, G, c.R, c.B, c.pps, c.attn_chunk, rb,
              kLog2e / sqrtf((float)D)};
   dim3 grid(c.attn_splits, nkv * rb, c.B);
   {
@@ -1146,7 +1166,7 @@ hipError_t launch_attention(Ctx& c, Model& m, int li) {
       hipExtLaunchKernelGGL(k_attn<64>, grid, dim3(256), attn_lds_bytes(c.attn_chunk, D), S(c), t.e0, t.e1, 0, p);
     CK(hipGetLastError());
   }
-  CombineArgs cb{c.st, c.op, c.mp, c.lp, c.o, nq, D, c.R, c.B, c.attn_chunk};
+  CombineArgs cb{c.st, reinterpret_cast<const bf16_t*>(c.op), c.mp, c.lp, c.o, nq, D, c.R, c.B, c.attn_chunk};
   Timed t2(c, SPEC_KERNEL_OTHER, 0);
   hipExtLaunchKernelGGL(k_attn_combine, dim3(c.R, nq, c.B), dim3(256),
                         (size_t)(((c.attn_splits + 3) & ~3) + 8 * D) * sizeof(float), S(c), t2.e0, t2.e1, 0, cb);
