@@ -14,6 +14,10 @@ namespace specdec {
 constexpr int kSgWorkers = 15;                // weight-streaming waves per workgroup
 constexpr int kSgWaves = kSgWorkers + 1;      // + the control wave
 constexpr int kSgDepth = 8;                   // k-steps each worker keeps in flight (one tile's share)
+#ifndef SG_DEPTH_XS
+#define SG_DEPTH_XS 8
+#endif
+constexpr int kSgDepthXs = SG_DEPTH_XS;       // k-steps in flight per worker when x is streamed
 constexpr int kSgMaxRows = 16;                // rows of one MFMA block
 constexpr int kSgMaxSpan = kSgWorkers * kSgDepth;   // k-steps of one tile slice
 constexpr int kSgPendMax = 64;                // units one workgroup may have to finish
@@ -40,6 +44,7 @@ struct SgJob {
   const bf16_t* w;        // packed weights [ntiles][T] blocks
   int ntiles, T;
   int S, G;               // k-slices of T; workgroups per slice (grid = S*G)
+  int xs;                 // x streamed with the weights (long k-ranges) instead of held in registers
   int kmax;               // partial slots per workgroup
   int units;              // fixup units (tiles, or gate/up tile pairs)
   const bf16_t* x;        // input rows [M][ldx], Kd valid columns

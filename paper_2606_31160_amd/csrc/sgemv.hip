@@ -20,8 +20,13 @@
 // order through double-buffered LDS, one workgroup barrier per tile, and runs
 // the epilogue while the workers already stream the next tile.
 //
-// k-sliced reductions (the down projection, whose input row does not fit in
-// LDS) are finished by the workgroup that arrives last at a tile: each slice's
+// Long k-ranges (the down projection: its input rows are 18944 wide) stream
+// x with the weights: a worker's k-steps are taken eight at a time, each slot
+// of the rolling buffer holding one weight block and the matching x operand
+// (read from L2), so a tile is never cut across workgroups.
+//
+// k-sliced reductions (S > 1, kept for shapes that ask for them) are finished
+// by the workgroup that arrives last at a tile: each slice's
 // workgroup stores its partial tile, makes it visible with a release fence and
 // counts itself in; the last one reads the partials back in slice order, adds
 // them and runs the epilogue, and resets the counter for the next launch.
@@ -209,8 +214,9 @@ __device__ __forceinline__ void epilogue_inputs(const SgJob& j, const RowInfo& r
 // The job is a kernel argument (not a pointer to it) so that its fields
 // arrive with the launch: the weight and activation loads do not wait for a
 // memory round trip to fetch their addresses first.
-template <int EPI>
+template <int EPI, bool XS>
 __global__ __launch_bounds__(kSgWaves * 64) void k_sgemv(const SgJob j) {
+  constexpr int DEP = XS ? kSgDepthXs : kSgDepth;   // rolling-buffer slots per worker
   extern __shared__ __align__(16) unsigned char lds[];
   constexpr bool kPair = EPI == SG_SWIGLU;
   constexpr int TPU = kPair ? 2 : 1;   // tiles per unit
@@ -245,22 +251,32 @@ __global__ __launch_bounds__(kSgWaves * 64) void k_sgemv(const SgJob j) {
   // lane (m, g) holds x[m][32 s + 8 g .. +8] of its step s), then the first
   // tile's weights, so that the MFMAs can start as soon as weights arrive.
   // Rows of dead sequences are zeroed once the live mask is known.
-  u32x4 xv[kSgDepth];
+  u32x4 xv[DEP];
   const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(const_cast<bf16_t*>(j.w), 0,
                                                                       j.ntiles * T * 1024, kRsrcWord3);
+  // x rows as a buffer (streamed x): an offset past it reads zeros
+  const __amdgpu_buffer_rsrc_t rsx = __builtin_amdgcn_make_buffer_rsrc(const_cast<bf16_t*>(j.x), 0,
+                                                                       M * j.ldx * 2, kRsrcWord3);
+  auto x_off = [&](int step) {   // byte offset of lane (m, grp)'s x operand of a k-step, or kOut
+    const int k = step * 32 + 8 * grp;
+    return (mok && k < j.Kd) ? (m * j.ldx + k) * 2 : kOut;
+  };
   const int lane_off = lane * 16;
-  u32x4 wv[kSgDepth];
+  u32x4 wv[DEP];
   if (wave > 0) {
 #pragma unroll
-    for (int i = 0; i < kSgDepth; ++i) {
+    for (int i = 0; i < DEP; ++i) {
       const int k = (ws0 + i) * 32 + 8 * grp;
-      xv[i] = (i < nst && mok && k < j.Kd) ? *reinterpret_cast<const u32x4*>(j.x + (size_t)m * j.ldx + k)
-                                             : u32x4{0, 0, 0, 0};
+      if constexpr (XS)
+        xv[i] = __builtin_amdgcn_raw_buffer_load_b128(rsx, i < nst ? x_off(ws0 + i) : kOut, 0, 0);
+      else
+        xv[i] = (i < nst && mok && k < j.Kd) ? *reinterpret_cast<const u32x4*>(j.x + (size_t)m * j.ldx + k)
+                                               : u32x4{0, 0, 0, 0};
     }
     if (n_it > 0) {
       const int v = (tile_of(0) * T + ws0) * 1024 + lane_off;
 #pragma unroll
-      for (int i = 0; i < kSgDepth; ++i)
+      for (int i = 0; i < DEP; ++i)
         wv[i] = __builtin_amdgcn_raw_buffer_load_b128(rs, i < nst ? v + 1024 * i : kOut, 0, 0);
     }
   }
@@ -275,9 +291,10 @@ __global__ __launch_bounds__(kSgWaves * 64) void k_sgemv(const SgJob j) {
     }
     live &= (1u << M) - 1u;
   }
-  if (wave > 0 && !((live >> m) & 1)) {
+  const bool xok = (live >> m) & 1;
+  if (!XS && wave > 0 && !xok) {
 #pragma unroll
-    for (int i = 0; i < kSgDepth; ++i) xv[i] = u32x4{0, 0, 0, 0};
+    for (int i = 0; i < DEP; ++i) xv[i] = u32x4{0, 0, 0, 0};
   }
 
   // per-row facts of the lane's row m (the control wave now; the other waves
@@ -346,13 +363,37 @@ __global__ __launch_bounds__(kSgWaves * 64) void k_sgemv(const SgJob j) {
   // wave-uniform value) with one workgroup barrier per tile each, so that
   // the workers' code holds nothing but weight loads and MFMAs.  The barrier
   // waits for LDS traffic only: the control wave's stores stay in flight.
-  if (wave > 0) {
+  if (wave > 0 && XS) {
+    // streamed x: a tile's steps are taken DEP at a time; slot i holds
+    // step g * DEP + i of the worker's range, and is refilled (weights and
+    // x) with the same slot of the next group, or of the next tile's first
+    const int NG = (nst + DEP - 1) / DEP;
+    for (int it = 0; it < n_it; ++it) {
+      f32x4 acc = f32x4{0.f, 0.f, 0.f, 0.f};
+      for (int g = 0; g < NG; ++g) {
+        const bool lastg = g + 1 == NG;
+        const int nit = lastg ? it + 1 : it, ng = lastg ? 0 : g + 1;
+        const bool nv = nit < n_it;
+        const int vn = (tile_of(nv ? nit : it) * T + ws0 + ng * DEP) * 1024 + lane_off;
+#pragma unroll
+        for (int i = 0; i < DEP; ++i) {
+          acc = mfma16x16x32(wv[i], xok ? xv[i] : u32x4{0, 0, 0, 0}, acc);
+          const int sn = ng * DEP + i;
+          const bool on = nv && sn < nst;
+          wv[i] = __builtin_amdgcn_raw_buffer_load_b128(rs, on ? vn + 1024 * i : kOut, 0, 0);
+          xv[i] = __builtin_amdgcn_raw_buffer_load_b128(rsx, on ? x_off(ws0 + sn) : kOut, 0, 0);
+        }
+      }
+      red[((it & 1) * kSgWorkers + wi) * 64 + lane] = acc;
+      lds_barrier();
+    }
+  } else if (wave > 0) {
     for (int it = 0; it < n_it; ++it) {
       const bool na = it + 1 < n_it;
       const int vn = (tile_of(it + 1) * T + ws0) * 1024 + lane_off;
       f32x4 acc = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-      for (int i = 0; i < kSgDepth; ++i) {
+      for (int i = 0; i < DEP; ++i) {
         const bool on = i < nst;
         acc = mfma16x16x32(wv[i], xv[i], acc);
         wv[i] = __builtin_amdgcn_raw_buffer_load_b128(rs, (na && on) ? vn + 1024 * i : kOut, 0, 0);
@@ -495,8 +536,12 @@ size_t sg_part_floats(const SgJob& j) { return (size_t)j.S * j.G * j.kmax * 2 * 
 bool sg_plan(SgJob& j, int epi, int ncu, int lds_limit) {
   const int tpu = epi == SG_SWIGLU ? 2 : 1;
   if (j.ntiles < 1 || j.ntiles % tpu || j.M < 1 || j.M > kSgMaxRows || j.T < 1 || j.rps < 1 || ncu < 1) return false;
-  if ((long long)j.ntiles * j.T * 1024 >= kOut) return false;
-  const int smin = (j.T + kSgMaxSpan - 1) / kSgMaxSpan;
+  if ((long long)j.ntiles * j.T * 1024 >= kOut || (long long)j.M * j.ldx * 2 >= kOut) return false;
+  // A k-range longer than the workers can hold x for is streamed (x loaded
+  // with the weights, step by step) rather than cut into k-slices: no
+  // partial tiles and no cross-workgroup fixup.
+  j.xs = j.T > kSgMaxSpan ? 1 : 0;
+  const int smin = j.xs ? 1 : (j.T + kSgMaxSpan - 1) / kSgMaxSpan;
   int S = smin;
   for (int s = smin; s <= 2 * smin; ++s)
     if (ncu % s == 0) {
@@ -521,14 +566,22 @@ bool sg_plan(SgJob& j, int epi, int ncu, int lds_limit) {
 hipError_t sg_launch(int epi, const SgJob& h, hipStream_t s, hipEvent_t e0, hipEvent_t e1) {
   const dim3 grid(h.S * h.G), block(kSgWaves * 64);
   const uint32_t lds = (uint32_t)sg_lds_bytes(h);
+#define SG_CASE(E)                                                                             \
+  case E:                                                                                      \
+    if (h.xs)                                                                                  \
+      hipExtLaunchKernelGGL(k_sgemv<E, true>, grid, block, lds, s, e0, e1, 0, h);             \
+    else                                                                                       \
+      hipExtLaunchKernelGGL(k_sgemv<E, false>, grid, block, lds, s, e0, e1, 0, h);            \
+    break;
   switch (epi) {
-    case SG_ROPE: hipExtLaunchKernelGGL(k_sgemv<SG_ROPE>, grid, block, lds, s, e0, e1, 0, h); break;
-    case SG_RESID: hipExtLaunchKernelGGL(k_sgemv<SG_RESID>, grid, block, lds, s, e0, e1, 0, h); break;
-    case SG_SWIGLU: hipExtLaunchKernelGGL(k_sgemv<SG_SWIGLU>, grid, block, lds, s, e0, e1, 0, h); break;
-    case SG_DOWN: hipExtLaunchKernelGGL(k_sgemv<SG_DOWN>, grid, block, lds, s, e0, e1, 0, h); break;
-    case SG_ARGMAX: hipExtLaunchKernelGGL(k_sgemv<SG_ARGMAX>, grid, block, lds, s, e0, e1, 0, h); break;
+    SG_CASE(SG_ROPE)
+    SG_CASE(SG_RESID)
+    SG_CASE(SG_SWIGLU)
+    SG_CASE(SG_DOWN)
+    SG_CASE(SG_ARGMAX)
     default: return hipErrorInvalidValue;
   }
+#undef SG_CASE
   return hipGetLastError();
 }
 
@@ -540,16 +593,13 @@ hipError_t sg_pack(bf16_t* dst, const PackSrc& src, hipStream_t s) {
 }
 
 void sg_set_attributes(int lds_limit) {
-  (void)hipFuncSetAttribute(reinterpret_cast<const void*>(&k_sgemv<SG_ROPE>),
-                            hipFuncAttributeMaxDynamicSharedMemorySize, lds_limit);
-  (void)hipFuncSetAttribute(reinterpret_cast<const void*>(&k_sgemv<SG_RESID>),
-                            hipFuncAttributeMaxDynamicSharedMemorySize, lds_limit);
-  (void)hipFuncSetAttribute(reinterpret_cast<const void*>(&k_sgemv<SG_SWIGLU>),
-                            hipFuncAttributeMaxDynamicSharedMemorySize, lds_limit);
-  (void)hipFuncSetAttribute(reinterpret_cast<const void*>(&k_sgemv<SG_DOWN>),
-                            hipFuncAttributeMaxDynamicSharedMemorySize, lds_limit);
-  (void)hipFuncSetAttribute(reinterpret_cast<const void*>(&k_sgemv<SG_ARGMAX>),
-                            hipFuncAttributeMaxDynamicSharedMemorySize, lds_limit);
+  const void* fns[] = {
+      reinterpret_cast<const void*>(&k_sgemv<SG_ROPE, false>),   reinterpret_cast<const void*>(&k_sgemv<SG_ROPE, true>),
+      reinterpret_cast<const void*>(&k_sgemv<SG_RESID, false>),  reinterpret_cast<const void*>(&k_sgemv<SG_RESID, true>),
+      reinterpret_cast<const void*>(&k_sgemv<SG_SWIGLU, false>), reinterpret_cast<const void*>(&k_sgemv<SG_SWIGLU, true>),
+      reinterpret_cast<const void*>(&k_sgemv<SG_DOWN, false>),   reinterpret_cast<const void*>(&k_sgemv<SG_DOWN, true>),
+      reinterpret_cast<const void*>(&k_sgemv<SG_ARGMAX, false>), reinterpret_cast<const void*>(&k_sgemv<SG_ARGMAX, true>)};
+  for (const void* f : fns) (void)hipFuncSetAttribute(f, hipFuncAttributeMaxDynamicSharedMemorySize, lds_limit);
 }
 
 }  // namespace specdec
