@@ -30,6 +30,11 @@ __device__ __forceinline__ uint32_t pack2(float lo, float hi) { return f2bf_bits
 
 __device__ __forceinline__ u32x4 ld16(const bf16_t* p) { return *reinterpret_cast<const u32x4*>(p); }
 __device__ __forceinline__ u32x2 ld8(const bf16_t* p) { return *reinterpret_cast<const u32x2*>(p); }
+// Non-temporal 16-byte load, for weights (read once per pass): streamed with
+// the nt hint they do not displace data that is reused.
+__device__ __forceinline__ u32x4 ld16_nt(const bf16_t* p) {
+  return __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(p));
+}
 
 __device__ __forceinline__ f32x4 mfma16x16x32(u32x4 a, u32x4 b, f32x4 c) {
   return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, a), __builtin_bit_cast(bf16x8, b), c,

@@ -102,7 +102,7 @@ __global__ __launch_bounds__(kGemmWaves * 64) void k_gemm(GemvArgs a) {
 #pragma unroll
     for (int st = 0; st < 2; ++st) {
       const int k = kc + 32 * st + kq;
-      wr[st] = (wtile && k < kend) ? ld16(wp + k) : u32x4{0, 0, 0, 0};
+      wr[st] = (wtile && k < kend) ? ld16_nt(wp + k) : u32x4{0, 0, 0, 0};
     }
   };
 

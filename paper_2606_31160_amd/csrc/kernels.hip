@@ -238,7 +238,7 @@ __global__ __launch_bounds__(NW * 64) void k_gemv(GemvArgs a) {
 #pragma unroll
     for (int i = 0; i < SMAX; ++i) {
       const int k = (w0 + i) << 5;
-      wv[tt][i] = (w0 + i < w1 && k + kq < Kd) ? ld16(wp + k) : u32x4{0, 0, 0, 0};
+      wv[tt][i] = (w0 + i < w1 && k + kq < Kd) ? ld16_nt(wp + k) : u32x4{0, 0, 0, 0};
     }
   }
 
@@ -454,7 +454,7 @@ __global__ __launch_bounds__(NW * 64) void k_gemv_p(GemvArgs a) {
 #pragma unroll
     for (int i = 0; i < SMAX; ++i) {
       const int k = (w0 + i) << 5;
-      wv[i] = (w0 + i < w1 && k + kq < Kd) ? ld16(wp + k) : u32x4{0, 0, 0, 0};
+      wv[i] = (w0 + i < w1 && k + kq < Kd) ? ld16_nt(wp + k) : u32x4{0, 0, 0, 0};
     }
   };
 

@@ -61,6 +61,10 @@ namespace {
 
 constexpr int kOut = 0x7FFFFF00;          // buffer offset past every packed matrix (they are < kOut bytes)
 constexpr int kRsrcWord3 = 0x00020000;    // raw buffer resource, 32-bit data
+// Cache policy of the weight loads: non-temporal.  Each weight byte is read
+// once per pass, and streaming it with the nt hint measured 6.4-6.8 TB/s on
+// the large projections against 5.7-6.1 TB/s for default-policy loads.
+constexpr int kNt = 2;
 
 __device__ __forceinline__ f32x4 ld_coh(const float* p) {
   const SG_GLOBAL uint64_t* q = (const SG_GLOBAL uint64_t*)(p);
@@ -277,7 +281,7 @@ __global__ __launch_bounds__(kSgWaves * 64) void k_sgemv(const SgJob j) {
       const int v = (tile_of(0) * T + ws0) * 1024 + lane_off;
 #pragma unroll
       for (int i = 0; i < DEP; ++i)
-        wv[i] = __builtin_amdgcn_raw_buffer_load_b128(rs, i < nst ? v + 1024 * i : kOut, 0, 0);
+        wv[i] = __builtin_amdgcn_raw_buffer_load_b128(rs, i < nst ? v + 1024 * i : kOut, 0, kNt);
     }
   }
 
@@ -380,7 +384,7 @@ __global__ __launch_bounds__(kSgWaves * 64) void k_sgemv(const SgJob j) {
           acc = mfma16x16x32(wv[i], xok ? xv[i] : u32x4{0, 0, 0, 0}, acc);
           const int sn = ng * DEP + i;
           const bool on = nv && sn < nst;
-          wv[i] = __builtin_amdgcn_raw_buffer_load_b128(rs, on ? vn + 1024 * i : kOut, 0, 0);
+          wv[i] = __builtin_amdgcn_raw_buffer_load_b128(rs, on ? vn + 1024 * i : kOut, 0, kNt);
           xv[i] = __builtin_amdgcn_raw_buffer_load_b128(rsx, on ? x_off(ws0 + sn) : kOut, 0, 0);
         }
       }
@@ -396,7 +400,7 @@ __global__ __launch_bounds__(kSgWaves * 64) void k_sgemv(const SgJob j) {
       for (int i = 0; i < DEP; ++i) {
         const bool on = i < nst;
         acc = mfma16x16x32(wv[i], xv[i], acc);
-        wv[i] = __builtin_amdgcn_raw_buffer_load_b128(rs, (na && on) ? vn + 1024 * i : kOut, 0, 0);
+        wv[i] = __builtin_amdgcn_raw_buffer_load_b128(rs, (na && on) ? vn + 1024 * i : kOut, 0, kNt);
       }
       red[((it & 1) * kSgWorkers + wi) * 64 + lane] = acc;
       lds_barrier();
