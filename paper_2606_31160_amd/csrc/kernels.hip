@@ -1514,6 +1514,9 @@ bool sg_build_jobs(Ctx& c, Model& m, bool draft, bool fill) {
     j[2].Hn = H;
     j[2].u = c.u;
     base(j[3], H / kTile, F, c.u);
+    // the down projection streams x; its input is written step-major so that
+    // the rows of one k-step are a single contiguous run
+    j[2].upk = j[3].xpk = F > 32 * kSgMaxSpan ? 1 : 0;
     j[3].w = pk ? pk + m.pk_dn : nullptr;
     j[3].x32 = c.x;
     j[3].H = H;

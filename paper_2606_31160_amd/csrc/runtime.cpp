@@ -359,7 +359,7 @@ size_t carve(Ctx& c, const spec_config* cfg, const spec_seq_init* seqs, bool has
   c.x = cv.take<float>((size_t)L.Mpad * H);
   c.q = cv.take<bf16_t>((size_t)L.Mpad * nqD);
   c.o = cv.take<bf16_t>((size_t)L.Mpad * nqD);
-  c.u = cv.take<bf16_t>((size_t)L.Mpad * F);
+  c.u = cv.take<bf16_t>((size_t)L.Mpad * align_up(F, 32));   // row-major, or step-major for the packed path
   c.xg = cv.take<bf16_t>((size_t)L.Mpad * H);
   c.ss = cv.take<float>((size_t)(H / kTile) * L.Mpad);
   c.rcs = cv.take<float2>((size_t)L.Mpad * (D / 2));

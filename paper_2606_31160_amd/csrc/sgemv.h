@@ -47,7 +47,8 @@ struct SgJob {
   int xs;                 // x streamed with the weights (long k-ranges) instead of held in registers
   int kmax;               // partial slots per workgroup
   int units;              // fixup units (tiles, or gate/up tile pairs)
-  const bf16_t* x;        // input rows [M][ldx], Kd valid columns
+  const bf16_t* x;        // input rows [M][ldx], Kd valid columns; or step-major (xpk)
+  int xpk;                // x step-major: [ceil(Kd/32)][M][32], so a step's rows are one contiguous run
   int ldx, Kd, M, rps;    // rows; rows per sequence
   const float* ss_in;     // normalised input: [Hn/16][mpad] sums of squares, else null
   int Hn, mpad;
@@ -70,7 +71,8 @@ struct SgJob {
   float* ss_out;          // [H/16][mpad]
   int select_last;        // SG_DOWN of a draft pass's last layer: each sequence's last live row as row b
   // SG_SWIGLU
-  bf16_t* u;              // [M][ntiles*8]
+  bf16_t* u;              // [M][ntiles*8], or step-major [ntiles/4][M][32] (upk)
+  int upk;
   // SG_ARGMAX
   float* amax_v;          // [amax_n][mpad] (max, index) of each row per workgroup (per tile when k-sliced)
   int32_t* amax_i;

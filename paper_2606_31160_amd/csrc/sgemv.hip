@@ -152,8 +152,9 @@ __device__ __forceinline__ void epilogue(const SgJob& j, RowInfo& ri, int u, f32
       float r[4];
 #pragma unroll
       for (int i = 0; i < 4; ++i) r[i] = g[i] / (1.f + expf(-g[i])) * up[i];
-      const int F = j.ntiles * 8;
-      *reinterpret_cast<u32x2*>(j.u + (size_t)m * F + 16 * u + 4 * grp) = u32x2{pack2(r[0], r[1]), pack2(r[2], r[3])};
+      const int F = j.ntiles * 8, n = 16 * u + 4 * grp;
+      const size_t at = j.upk ? ((size_t)(n >> 5) * M + m) * 32 + (n & 31) : (size_t)m * F + n;
+      *reinterpret_cast<u32x2*>(j.u + at) = u32x2{pack2(r[0], r[1]), pack2(r[2], r[3])};
     }
   } else {   // SG_ARGMAX
     const f32x4 y = ya * ri.inv_rms;
@@ -259,11 +260,12 @@ __global__ __launch_bounds__(kSgWaves * 64) void k_sgemv(const SgJob j) {
   const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(const_cast<bf16_t*>(j.w), 0,
                                                                       j.ntiles * T * 1024, kRsrcWord3);
   // x rows as a buffer (streamed x): an offset past it reads zeros
-  const __amdgpu_buffer_rsrc_t rsx = __builtin_amdgcn_make_buffer_rsrc(const_cast<bf16_t*>(j.x), 0,
-                                                                       M * j.ldx * 2, kRsrcWord3);
+  const __amdgpu_buffer_rsrc_t rsx = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<bf16_t*>(j.x), 0, j.xpk ? T * M * 64 : M * j.ldx * 2, kRsrcWord3);
+  bool xrow = mok;               // lane's x row is loaded (narrowed to live rows once they are known)
   auto x_off = [&](int step) {   // byte offset of lane (m, grp)'s x operand of a k-step, or kOut
     const int k = step * 32 + 8 * grp;
-    return (mok && k < j.Kd) ? (m * j.ldx + k) * 2 : kOut;
+    return (xrow && k < j.Kd) ? (j.xpk ? ((step * M + m) * 32 + 8 * grp) * 2 : (m * j.ldx + k) * 2) : kOut;
   };
   const int lane_off = lane * 16;
   u32x4 wv[DEP];
@@ -296,6 +298,7 @@ __global__ __launch_bounds__(kSgWaves * 64) void k_sgemv(const SgJob j) {
     live &= (1u << M) - 1u;
   }
   const bool xok = (live >> m) & 1;
+  xrow = mok && xok;   // streamed x: rows of dead sequences are not read at all
   if (!XS && wave > 0 && !xok) {
 #pragma unroll
     for (int i = 0; i < DEP; ++i) xv[i] = u32x4{0, 0, 0, 0};
