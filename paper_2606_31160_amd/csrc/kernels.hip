@@ -129,6 +129,7 @@ struct EmbedArgs {
   const float2* cs;      // [cap][D/2]
   const int8_t* axis;    // [D/2]
   int H, R, cap, mode, mpad, D, flat;
+  int V;                 // vocabulary size: a token outside [0, V) is reported and read as 0
 };
 
 __global__ __launch_bounds__(1024) void k_embed(EmbedArgs p) {
@@ -158,6 +159,10 @@ __global__ __launch_bounds__(1024) void k_embed(EmbedArgs p) {
   }
   const size_t r = (size_t)b * p.R + j;
   const bool live = j < count;
+  if (tok < 0 || tok >= p.V) {   // never from a valid pass; guards the gather below
+    if (live && threadIdx.x == 0) atomicOr(&p.st[b].err, ERR_TOKEN);
+    tok = 0;
+  }
   const bf16_t* er = p.E + (size_t)tok * p.H;
   for (int n = threadIdx.x; n < p.H; n += blockDim.x) {
     const float v = live ? bf2f(er[n]) : 0.f;
@@ -1707,7 +1712,7 @@ hipError_t launch_forward(Ctx& c, PassMode mode) {
     EmbedArgs p{c.st,    c.hist, c.embed,      m.L[0].attn_norm, c.x, persistent ? c.p_xa : c.xg,
                 persistent ? c.p_ssa : c.ss,  c.rcs,
                 c.pos3,  c.cs,   m.axis,       d.hidden,         c.R, c.cap,    (int)mode, c.Mpad,
-                d.head_dim, m.flat ? 1 : 0};
+                d.head_dim, m.flat ? 1 : 0, c.V};
     Timed t(c, SPEC_KERNEL_OTHER, 0);
     hipExtLaunchKernelGGL(k_embed, dim3(c.R, c.B), dim3(1024), (size_t)d.hidden * sizeof(float), c.stream, t.e0, t.e1, 0, p);
     CK(hipGetLastError());
