@@ -42,7 +42,8 @@ struct SeqState {
   int32_t want_logits;  // the current verify copies bf16 logits out
   int32_t base;         // slot of row 0 of the current pass
   int32_t count;        // valid rows of the current pass (0 when idle)
-  int32_t pad[2];
+  int32_t dcall;        // draft_step calls this round (the output column of the next one)
+  int32_t pad;
   int32_t vtok[kMaxRows];       // verify rows: pending, d_1..d_K
   int32_t rstar[kMaxRows];      // greedy token of each verify row
   int32_t committed[kMaxRows];  // tokens of the last verify to commit
@@ -151,7 +152,11 @@ struct Ctx {
 
   // graphs
   bool use_graphs = true;
-  hipGraphExec_t g_verify = nullptr, g_draft = nullptr;
+  hipGraphExec_t g_verify = nullptr, g_draft = nullptr, g_commit = nullptr;
+  int32_t* draft_out = nullptr;                  // draft_step's output array (baked into the draft graph)
+  int32_t* g_draft_out = nullptr;                // ... the one the current draft graph writes
+  int32_t* commit_out[4] = {};                   // spec_commit's outputs (baked into the commit graph)
+  int32_t* g_commit_out[4] = {};
 
   // timing
   bool timing = false;
@@ -175,7 +180,6 @@ hipError_t launch_prefix_kv(Ctx& c, Model& m, int layer, int b, int prefix_len,
                             const bf16_t* k_pre, const bf16_t* v);
 hipError_t launch_stage_verify(Ctx& c, const int32_t* d_override, int want_logits);
 hipError_t launch_forward(Ctx& c, PassMode mode);   // embed .. accept / draft pick
-hipError_t launch_draft_out(Ctx& c, int32_t* d_tokens);
 hipError_t launch_commit(Ctx& c, int32_t* acc, int32_t* committed, int32_t* ncommit, int32_t* fin);
 hipError_t launch_logits_out(Ctx& c, void* d_logits);
 // Packed-weight path: plans (and, with fill, points) every GEMV job of a model;

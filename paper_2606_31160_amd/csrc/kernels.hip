@@ -905,6 +905,8 @@ struct AmaxArgs {
   const float* amax_v;
   const int32_t* amax_i;
   int ntiles, mpad, rps, draft;
+  int32_t* out;          // draft: [B][K] proposals, column = draft calls so far (-1 when none); or null
+  int K;
 };
 
 __global__ __launch_bounds__(1024) void k_argmax_rows(AmaxArgs p) {
@@ -912,7 +914,13 @@ __global__ __launch_bounds__(1024) void k_argmax_rows(AmaxArgs p) {
   __shared__ int shi[1024];
   const int j = blockIdx.x, b = blockIdx.y;
   SeqState& s = p.st[b];
-  if (s.count == 0) return;
+  if (s.count == 0) {
+    if (p.draft && threadIdx.x == 0) {   // nothing proposed this call
+      if (p.out && s.dcall < p.K) p.out[b * p.K + s.dcall] = -1;
+      s.dcall += 1;
+    }
+    return;
+  }
   const int row = b * p.rps + j;
   float v = -INFINITY;
   int i = 0x7fffffff;
@@ -948,13 +956,10 @@ __global__ __launch_bounds__(1024) void k_argmax_rows(AmaxArgs p) {
       s.props[s.dstep] = shi[0];
       s.draft_len = s.base + s.count;
       s.dstep += 1;
+      if (p.out && s.dcall < p.K) p.out[b * p.K + s.dcall] = shi[0];
+      s.dcall += 1;
     }
   }
-}
-
-__global__ void k_draft_out(const SeqState* st, int32_t* out, int K, int col) {
-  const SeqState& s = st[blockIdx.x];
-  out[blockIdx.x * K + col] = (s.count > 0 && s.dstep == col + 1) ? s.props[col] : -1;
 }
 
 // Accept + commit (Eq. accept, Eq. commit): l = longest prefix of the verify's
@@ -998,6 +1003,7 @@ __global__ void k_commit(SeqState* st, int32_t* hist, int cap, int K, int stop, 
     s.n_commit = c;
   }
   s.dstep = 0;
+  s.dcall = 0;
   if (o_acc) o_acc[b] = l;
   if (o_n) o_n[b] = c;
   if (o_fin) o_fin[b] = s.finished;
@@ -1761,14 +1767,8 @@ hipError_t launch_forward(Ctx& c, PassMode mode) {
   // workgroup on the packed path
   const int ntiles = c.sg ? m.sg_host[(size_t)d.layers * 4].amax_n : c.V / kTile;
   Timed t(c, SPEC_KERNEL_OTHER, 0);
-  AmaxArgs p{c.st, c.amax_v, c.amax_i, ntiles, c.Mpad, draft ? 1 : c.R, draft ? 1 : 0};
+  AmaxArgs p{c.st, c.amax_v, c.amax_i, ntiles, c.Mpad, draft ? 1 : c.R, draft ? 1 : 0, draft ? c.draft_out : nullptr, c.K};
   hipExtLaunchKernelGGL(k_argmax_rows, dim3(draft ? 1 : c.R, c.B), dim3(1024), 0, c.stream, t.e0, t.e1, 0, p);
-  return hipGetLastError();
-}
-
-hipError_t launch_draft_out(Ctx& c, int32_t* d_tokens) {
-  if (!d_tokens) return hipSuccess;
-  hipLaunchKernelGGL(k_draft_out, dim3(c.B), dim3(1), 0, c.stream, c.st, d_tokens, c.K, c.dsteps);
   return hipGetLastError();
 }
 

@@ -521,16 +521,10 @@ spec_status set_err(Ctx& c, spec_status s, const char* msg) {
     if (e_ != hipSuccess) return fail_hip(c, e_, where); \
   } while (0)
 
-// Runs one pass either directly or through its captured graph.
-spec_status run_pass(Ctx& c, PassMode mode) {
-  const bool graphs = c.use_graphs && !c.timing;
-  if (!graphs) {
-    // timing mode: a head start so the timed kernels run back to back
-    if (c.timing) HIPCHK(c, launch_hold(c, mode == PASS_VERIFY ? 4.0 : 1.0), "timing hold");
-    HIPCHK(c, launch_forward(c, mode), "forward pass");
-    return SPEC_OK;
-  }
-  hipGraphExec_t& ge = mode == PASS_VERIFY ? c.g_verify : c.g_draft;
+// Captures `launch` into `ge` on the capture stream (once; `ge` is reset by
+// the caller when what the graph bakes in changes) and launches it.
+template <class Launch>
+spec_status run_graph(Ctx& c, hipGraphExec_t& ge, Launch&& launch) {
   if (!ge) {
     if (!c.cap_stream) HIPCHK(c, hipStreamCreateWithFlags(&c.cap_stream, hipStreamNonBlocking), "capture stream");
     hipStream_t user = c.stream;
@@ -539,7 +533,7 @@ spec_status run_pass(Ctx& c, PassMode mode) {
     hipError_t e = hipStreamBeginCapture(c.cap_stream, hipStreamCaptureModeThreadLocal);
     hipError_t el = hipSuccess;
     if (e == hipSuccess) {
-      el = launch_forward(c, mode);
+      el = launch();
       e = hipStreamEndCapture(c.cap_stream, &g);
     }
     c.stream = user;
@@ -554,6 +548,42 @@ spec_status run_pass(Ctx& c, PassMode mode) {
   }
   HIPCHK(c, hipGraphLaunch(ge, c.stream), "graph launch");
   return SPEC_OK;
+}
+
+// Runs one pass either directly or through its captured graph.  A draft
+// pass's graph also writes the proposals to the caller's array, so it is
+// captured again when that array changes.
+spec_status run_pass(Ctx& c, PassMode mode) {
+  const bool graphs = c.use_graphs && !c.timing;
+  if (!graphs) {
+    // timing mode: a head start so the timed kernels run back to back
+    if (c.timing) HIPCHK(c, launch_hold(c, mode == PASS_VERIFY ? 4.0 : 1.0), "timing hold");
+    HIPCHK(c, launch_forward(c, mode), "forward pass");
+    return SPEC_OK;
+  }
+  if (mode == PASS_DRAFT && c.g_draft && c.g_draft_out != c.draft_out) {
+    (void)hipGraphExecDestroy(c.g_draft);
+    c.g_draft = nullptr;
+  }
+  if (mode == PASS_DRAFT) c.g_draft_out = c.draft_out;
+  return run_graph(c, mode == PASS_VERIFY ? c.g_verify : c.g_draft, [&] { return launch_forward(c, mode); });
+}
+
+// The commit kernel runs through a graph of its own too: launched directly
+// right after the verify graph it started about 8 us late on MI355X, while a
+// graph after a graph starts at once.  Its output pointers are baked in.
+spec_status run_commit(Ctx& c) {
+  if (!c.use_graphs || c.timing) {
+    HIPCHK(c, launch_commit(c, c.commit_out[0], c.commit_out[1], c.commit_out[2], c.commit_out[3]), "commit");
+    return SPEC_OK;
+  }
+  if (c.g_commit && !std::equal(c.commit_out, c.commit_out + 4, c.g_commit_out)) {
+    (void)hipGraphExecDestroy(c.g_commit);
+    c.g_commit = nullptr;
+  }
+  std::copy(c.commit_out, c.commit_out + 4, c.g_commit_out);
+  return run_graph(c, c.g_commit,
+                   [&] { return launch_commit(c, c.commit_out[0], c.commit_out[1], c.commit_out[2], c.commit_out[3]); });
 }
 
 template <class F>
@@ -780,9 +810,9 @@ spec_status draft_step(spec_ctx* ctx, int32_t* d_draft_tokens) {
     if (c.K < 1) return set_err(c, SPEC_E_STATE, "draft_step: K is 0");
     if (c.phase == Ctx::VERIFIED) return set_err(c, SPEC_E_STATE, "draft_step: commit the last verify first");
     if (c.dsteps >= c.K) return set_err(c, SPEC_E_STATE, "draft_step: K steps already taken this round");
+    c.draft_out = d_draft_tokens;
     spec_status s = run_pass(c, PASS_DRAFT);
     if (s != SPEC_OK) return s;
-    HIPCHK(c, launch_draft_out(c, d_draft_tokens), "draft output");
     c.dsteps += 1;
     c.phase = Ctx::DRAFTING;
     return SPEC_OK;
@@ -807,7 +837,12 @@ spec_status spec_commit(spec_ctx* ctx, int32_t* d_accept_len, int32_t* d_committ
                         int32_t* d_finished) {
   return guarded(ctx, [&](Ctx& c) -> spec_status {
     if (c.phase != Ctx::VERIFIED) return set_err(c, SPEC_E_STATE, "spec_commit: no verify to commit");
-    HIPCHK(c, launch_commit(c, d_accept_len, d_committed, d_n_committed, d_finished), "commit");
+    c.commit_out[0] = d_accept_len;
+    c.commit_out[1] = d_committed;
+    c.commit_out[2] = d_n_committed;
+    c.commit_out[3] = d_finished;
+    spec_status s = run_commit(c);
+    if (s != SPEC_OK) return s;
     c.phase = Ctx::READY;
     c.dsteps = 0;
     return SPEC_OK;
@@ -840,6 +875,7 @@ void spec_destroy(spec_ctx* ctx) {
   if (c.stream) (void)hipStreamSynchronize(c.stream);
   if (c.g_verify) (void)hipGraphExecDestroy(c.g_verify);
   if (c.g_draft) (void)hipGraphExecDestroy(c.g_draft);
+  if (c.g_commit) (void)hipGraphExecDestroy(c.g_commit);
   if (c.cap_stream) (void)hipStreamDestroy(c.cap_stream);
   for (hipEvent_t e : c.ev_pool) (void)hipEventDestroy(e);
   delete ctx;
