@@ -296,8 +296,7 @@ def main():
     def round_(r, evs=None):
         if evs:
             evs[0].record()
-        for _ in range(K):
-            B.draft_step(s.ctx, s.dtok.data_ptr())
+        B.draft_steps(s.ctx, K, s.dtok.data_ptr())
         if evs:
             evs[1].record()
         B.spec_verify(s.ctx, drafts[r].data_ptr(), 0)

@@ -178,6 +178,12 @@ spec_status spec_init(const spec_config* cfg, const void* embed,
  * State: READY or DRAFTING with fewer than K steps taken -> DRAFTING. */
 spec_status draft_step(spec_ctx* ctx, int32_t* d_draft_tokens);
 
+/* n draft steps in one call: the same as n calls of draft_step (columns j..j+n-1
+ * of d_draft_tokens), issued as one launch sequence so that the steps follow
+ * each other on the device without a gap between them.  1 <= n <= K minus the
+ * steps already taken this round; the state rules are those of draft_step. */
+spec_status draft_steps(spec_ctx* ctx, int32_t n, int32_t* d_draft_tokens);
+
 /* One verify pass (Eq. verify, Eq. accept).  Rows [pending, d_1..d_K] of every
  * sequence go through the target in one forward pass; row j's greedy token is
  * r*_{j+1} (argmax over fp32 logits, lowest index on ties, NaN as -inf).

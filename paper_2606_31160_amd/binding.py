@@ -82,6 +82,7 @@ def lib():
             "spec_init": [POINTER(spec_config), P, POINTER(spec_model_weights), POINTER(spec_model_weights),
                           POINTER(spec_seq_init), P, c_size_t, P, POINTER(P)],
             "draft_step": [P, P],
+            "draft_steps": [P, c_int32, P],
             "spec_verify": [P, P, P],
             "spec_commit": [P, P, P, P, P],
             "spec_sync": [P, POINTER(c_int32)],
@@ -143,6 +144,10 @@ def spec_init(cfg: spec_config, embed: int, target: spec_model_weights, draft, s
 
 def draft_step(ctx, d_draft_tokens: int = 0) -> None:
     _check(lib().draft_step(ctx, c_void_p(d_draft_tokens or None)), "draft_step", ctx)
+
+
+def draft_steps(ctx, n: int, d_draft_tokens: int = 0) -> None:
+    _check(lib().draft_steps(ctx, n, c_void_p(d_draft_tokens or None)), "draft_steps", ctx)
 
 
 def spec_verify(ctx, d_draft_tokens: int = 0, d_logits: int = 0) -> None:

@@ -155,6 +155,9 @@ struct Ctx {
   hipGraphExec_t g_verify = nullptr, g_draft = nullptr, g_commit = nullptr;
   int32_t* draft_out = nullptr;                  // draft_step's output array (baked into the draft graph)
   int32_t* g_draft_out = nullptr;                // ... the one the current draft graph writes
+  hipGraphExec_t g_drafts = nullptr;             // n draft passes in one graph (draft_steps)
+  int g_drafts_n = 0;
+  int32_t* g_drafts_out = nullptr;
   int32_t* commit_out[4] = {};                   // spec_commit's outputs (baked into the commit graph)
   int32_t* g_commit_out[4] = {};
 

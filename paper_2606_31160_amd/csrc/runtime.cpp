@@ -819,6 +819,40 @@ spec_status draft_step(spec_ctx* ctx, int32_t* d_draft_tokens) {
   });
 }
 
+spec_status draft_steps(spec_ctx* ctx, int32_t n, int32_t* d_draft_tokens) {
+  return guarded(ctx, [&](Ctx& c) -> spec_status {
+    if (!c.has_draft) return set_err(c, SPEC_E_STATE, "draft_steps: no draft model");
+    if (c.K < 1) return set_err(c, SPEC_E_STATE, "draft_steps: K is 0");
+    if (c.phase == Ctx::VERIFIED) return set_err(c, SPEC_E_STATE, "draft_steps: commit the last verify first");
+    if (n < 1 || n > c.K - c.dsteps) return set_err(c, SPEC_E_STATE, "draft_steps: n must be 1..K minus the steps taken");
+    c.draft_out = d_draft_tokens;
+    if (n == 1 || !c.use_graphs || c.timing) {
+      for (int i = 0; i < n; ++i) {
+        spec_status s = run_pass(c, PASS_DRAFT);
+        if (s != SPEC_OK) return s;
+      }
+    } else {
+      if (c.g_drafts && (c.g_drafts_n != n || c.g_drafts_out != d_draft_tokens)) {
+        (void)hipGraphExecDestroy(c.g_drafts);
+        c.g_drafts = nullptr;
+      }
+      c.g_drafts_n = n;
+      c.g_drafts_out = d_draft_tokens;
+      spec_status s = run_graph(c, c.g_drafts, [&]() -> hipError_t {
+        for (int i = 0; i < n; ++i) {
+          const hipError_t e = launch_forward(c, PASS_DRAFT);
+          if (e != hipSuccess) return e;
+        }
+        return hipSuccess;
+      });
+      if (s != SPEC_OK) return s;
+    }
+    c.dsteps += n;
+    c.phase = Ctx::DRAFTING;
+    return SPEC_OK;
+  });
+}
+
 spec_status spec_verify(spec_ctx* ctx, const int32_t* d_draft_tokens, void* d_logits) {
   return guarded(ctx, [&](Ctx& c) -> spec_status {
     if (c.phase == Ctx::VERIFIED) return set_err(c, SPEC_E_STATE, "spec_verify: commit the last verify first");
@@ -876,6 +910,7 @@ void spec_destroy(spec_ctx* ctx) {
   if (c.g_verify) (void)hipGraphExecDestroy(c.g_verify);
   if (c.g_draft) (void)hipGraphExecDestroy(c.g_draft);
   if (c.g_commit) (void)hipGraphExecDestroy(c.g_commit);
+  if (c.g_drafts) (void)hipGraphExecDestroy(c.g_drafts);
   if (c.cap_stream) (void)hipStreamDestroy(c.cap_stream);
   for (hipEvent_t e : c.ev_pool) (void)hipEventDestroy(e);
   delete ctx;

@@ -160,6 +160,9 @@ class Session:
     def draft_step(self, out=None):
         B.draft_step(self.ctx, (out if out is not None else self.dtok).data_ptr())
 
+    def draft_steps(self, n: int, out=None):
+        B.draft_steps(self.ctx, n, (out if out is not None else self.dtok).data_ptr())
+
     def verify(self, drafts=None, logits: bool = False):
         """drafts: None (the draft's own proposals), or [B][K] ints (host or device)."""
         ptr = 0

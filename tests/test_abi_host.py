@@ -159,6 +159,7 @@ def test_init_rejects_before_touching_the_device():
 def test_calls_on_null_context():
     L = B.lib()
     assert L.draft_step(None, None) == 1
+    assert L.draft_steps(None, 1, None) == 1
     assert L.spec_verify(None, None, None) == 1
     assert L.spec_commit(None, None, None, None, None) == 1
     assert L.spec_sync(None, None) == 1

@@ -245,8 +245,12 @@ def test_call_order_enforced(c1):
         s.commit()                      # nothing verified
     with pytest.raises(B.SpecError):
         s.verify(None)                  # no proposals yet
-    for _ in range(w.K):
-        s.draft_step()
+    with pytest.raises(B.SpecError):
+        s.draft_steps(0)                # n must be at least 1
+    s.draft_step()
+    with pytest.raises(B.SpecError):
+        s.draft_steps(w.K)              # more than the K - 1 steps left
+    s.draft_steps(w.K - 1)
     with pytest.raises(B.SpecError):
         s.draft_step()                  # K steps already taken
     s.verify(None)
@@ -271,6 +275,35 @@ def test_graphs_and_direct_launches_agree(c1):
         outs.append((o, lg))
     assert outs[0][0] == outs[1][0]
     assert bool((outs[0][1] == outs[1][1]).all())
+
+
+def test_draft_steps_equals_single_steps(c1):
+    """draft_steps(n) is n draft_step calls issued as one launch sequence: the
+    same proposals (columns of the output), the same state, over several
+    rounds that include verifier overrides, and a split of K into 1 + (K - 1)."""
+    w, hp, T, D, trace = c1
+    runs = []
+    for how in ("single", "batched", "split"):
+        s = _session(w)
+        props, states = [], []
+        for _ in range(4):
+            if how == "single":
+                for _ in range(w.K):
+                    s.draft_step()
+            elif how == "batched":
+                s.draft_steps(w.K)
+            else:
+                s.draft_step()
+                s.draft_steps(w.K - 1)
+            props.append(s.dtok.cpu().numpy().copy())
+            s.verify(None)
+            s.commit()
+            states.append(s.state(0))
+        runs.append((props, states))
+    for other in runs[1:]:
+        for a, b in zip(runs[0][0], other[0]):
+            assert np.array_equal(a, b)
+        assert runs[0][1] == other[1]
 
 
 def run_batch(s, mode, max_rounds=100):
