@@ -659,8 +659,7 @@ struct AttnArgs {
 };
 
 template <int D>
-__global__ __launch_bounds__(256) void k_attn(AttnArgs a) {
-  extern __shared__ __align__(16) unsigned char lds[];
+__device__ __forceinline__ void attn_partials(const AttnArgs& a, unsigned char* lds) {
   const int split = blockIdx.x;
   const int kvh = blockIdx.y / a.row_blocks, rb = blockIdx.y % a.row_blocks;
   const int b = blockIdx.z;
@@ -828,6 +827,13 @@ __global__ __launch_bounds__(256) void k_attn(AttnArgs a) {
   }
 }
 
+template <int D>
+__global__ __launch_bounds__(256) void k_attn(AttnArgs a) {
+  extern __shared__ __align__(16) unsigned char lds[];
+  attn_partials<D>(a, lds);
+}
+
+
 size_t attn_lds_bytes(int chunk, int D) {
   return ((size_t)chunk * (D + 8) + (size_t)D * (chunk + 8)) * sizeof(bf16_t);
 }
@@ -842,9 +848,9 @@ struct CombineArgs {
   int nq, D, R, B, chunk;
 };
 
-__global__ __launch_bounds__(256) void k_attn_combine(CombineArgs a) {
-  extern __shared__ float coef[];   // [ns] weights, then [8][D] partial sums
-  const int j = blockIdx.x, h = blockIdx.y, b = blockIdx.z;
+// One (row j, q head h, sequence b) of the combine; coef is LDS of at least
+// ((splits + 3) & ~3) + 8 * D floats.  Called by all threads of a workgroup.
+__device__ __forceinline__ void combine_unit(const CombineArgs& a, int j, int h, int b, float* coef) {
   const SeqState& s = a.st[b];
   if (j >= s.count) return;
   const int vis_end = s.base + j + 1;
@@ -891,6 +897,11 @@ __global__ __launch_bounds__(256) void k_attn_combine(CombineArgs a) {
     for (int g = 0; g < 8; ++g) t += part[g * a.D + d];
     a.o[(size_t)(b * a.R + j) * a.nq * a.D + h * a.D + d] = f2bf(t);
   }
+}
+
+__global__ __launch_bounds__(256) void k_attn_combine(CombineArgs a) {
+  extern __shared__ float coef[];   // [ns] weights, then [8][D] partial sums
+  combine_unit(a, blockIdx.x, blockIdx.y, blockIdx.z, coef);
 }
 
 // ---------------------------------------------------------------------------
@@ -1169,6 +1180,8 @@ hipError_t launch_attention(Ctx& c, Model& m, int li) {
   AttnArgs p{c.st, c.q, kc, vt, c.pt, reinterpret_cast<bf16_t*>(c.op), c.mp, c.lp, nq, nkv, G, c.R, c.B, c.pps, c.attn_chunk, rb,
              kLog2e / sqrtf((float)D)};
   dim3 grid(c.attn_splits, nkv * rb, c.B);
+  CombineArgs cb{c.st, reinterpret_cast<const bf16_t*>(c.op), c.mp, c.lp, c.o, nq, D, c.R, c.B, c.attn_chunk};
+  const size_t comb_lds = (size_t)(((c.attn_splits + 3) & ~3) + 8 * D) * sizeof(float);
   {
     Timed t(c, SPEC_KERNEL_ATTN, 0);
     if (D == 128)
@@ -1177,10 +1190,8 @@ hipError_t launch_attention(Ctx& c, Model& m, int li) {
       hipExtLaunchKernelGGL(k_attn<64>, grid, dim3(256), attn_lds_bytes(c.attn_chunk, D), S(c), t.e0, t.e1, 0, p);
     CK(hipGetLastError());
   }
-  CombineArgs cb{c.st, reinterpret_cast<const bf16_t*>(c.op), c.mp, c.lp, c.o, nq, D, c.R, c.B, c.attn_chunk};
   Timed t2(c, SPEC_KERNEL_OTHER, 0);
-  hipExtLaunchKernelGGL(k_attn_combine, dim3(c.R, nq, c.B), dim3(256),
-                        (size_t)(((c.attn_splits + 3) & ~3) + 8 * D) * sizeof(float), S(c), t2.e0, t2.e1, 0, cb);
+  hipExtLaunchKernelGGL(k_attn_combine, dim3(c.R, nq, c.B), dim3(256), comb_lds, S(c), t2.e0, t2.e1, 0, cb);
   return hipGetLastError();
 }
 

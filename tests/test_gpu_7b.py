@@ -55,8 +55,12 @@ def c2():
     return w, hp, T
 
 
-def test_one_layer_verify_against_oracle(c2):
+@pytest.mark.parametrize("K", [8, 15])
+def test_one_layer_verify_against_oracle(c2, K):
+    # K = 15: 16 verify rows, a full MFMA row block (every row of the packed
+    # kernels' operands live, the streamed down-projection input at 16 rows)
     w, hp, T = c2
+    w = w.with_(K=K)
     s = _session(w, provider=hp)
     P = w.seqs[0].prefix_len
     L = P + w.K + 1
