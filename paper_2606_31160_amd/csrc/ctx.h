@@ -147,6 +147,7 @@ struct Ctx {
   // host state machine
   enum Phase { READY = 0, DRAFTING = 1, VERIFIED = 2 } phase = READY;
   int dsteps = 0;
+  bool gemm_rows = false;              // layered row-major passes run on the batched-row GEMM
   bool poisoned = false;
   std::string err;
 

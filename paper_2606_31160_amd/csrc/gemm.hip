@@ -1,5 +1,6 @@
 // Batched-row GEMM on MFMA for passes of more than kThinRows rows (several
-// sequences verified together): y[m][n] = sum_k x[m][k] W[n][k] for up to
+// sequences verified together), and of 17..kThinRows rows whose width the
+// thin GEMV cannot stage (one sequence with K = 16 at hidden 4096): y[m][n] = sum_k x[m][k] W[n][k] for up to
 // SPEC_MAX_ROWS rows, with the same fused epilogues as the thin GEMV kernels
 // (1/rms row scale, rotary + paged KV append, residual + next-norm input,
 // SwiGLU, per-tile argmax, or k-split partial sums).
@@ -273,6 +274,9 @@ hipError_t launch_mb(const GemvArgs& g, hipStream_t s, hipEvent_t e0, hipEvent_t
   const dim3 grid((g.N + kGemmWaves * kTile - 1) / (kGemmWaves * kTile), g.splits), block(kGemmWaves * 64);
   const size_t lds = gemm_lds_bytes(g.M);
   switch (mb) {
+    case 2: hipExtLaunchKernelGGL((k_gemm<2, EPI>), grid, block, lds, s, e0, e1, 0, g); break;
+    case 3: hipExtLaunchKernelGGL((k_gemm<3, EPI>), grid, block, lds, s, e0, e1, 0, g); break;
+    case 4: hipExtLaunchKernelGGL((k_gemm<4, EPI>), grid, block, lds, s, e0, e1, 0, g); break;
     case 5: hipExtLaunchKernelGGL((k_gemm<5, EPI>), grid, block, lds, s, e0, e1, 0, g); break;
     case 6: hipExtLaunchKernelGGL((k_gemm<6, EPI>), grid, block, lds, s, e0, e1, 0, g); break;
     case 7: hipExtLaunchKernelGGL((k_gemm<7, EPI>), grid, block, lds, s, e0, e1, 0, g); break;
@@ -292,7 +296,7 @@ size_t gemm_lds_bytes(int M) {
 }
 
 hipError_t gemm_launch(int epi, const GemvArgs& g, hipStream_t s, hipEvent_t e0, hipEvent_t e1) {
-  if (g.M <= kThinRows || g.M > SPEC_MAX_ROWS || g.splits < 1 || (epi != EPI_STORE && g.splits != 1) ||
+  if (g.M <= kSgMaxRowsGemm || g.M > SPEC_MAX_ROWS || g.splits < 1 || (epi != EPI_STORE && g.splits != 1) ||
       g.N % kTile != 0 || g.Kd % 8 != 0)
     return hipErrorInvalidValue;
   switch (epi) {

@@ -54,6 +54,7 @@ struct GemvArgs {
 // Passes of up to kThinRows rows use the thin GEMV kernels (kernels.hip);
 // larger passes (up to SPEC_MAX_ROWS) the batched-row GEMM (gemm.hip).
 constexpr int kThinRows = 64;
+constexpr int kSgMaxRowsGemm = 16;   // the GEMM takes passes of more rows than one MFMA block
 constexpr int kGemmWaves = 4;   // waves per GEMM workgroup, one 16-column output tile each
 
 // Dynamic LDS bytes of a GEMM launch over M rows.

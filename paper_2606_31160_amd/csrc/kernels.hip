@@ -1042,9 +1042,11 @@ int gemv_lds_limit() {
   static int lim = -1;
   if (lim < 0) {
     int dev = 0, v = 0;
+    // without a device to ask (host-side validation), gfx950's 160 KB: the
+    // library is built for that target only
     if (hipGetDevice(&dev) != hipSuccess ||
         hipDeviceGetAttribute(&v, hipDeviceAttributeMaxSharedMemoryPerBlock, dev) != hipSuccess || v <= 0)
-      v = 65536;
+      v = 160 * 1024;
     lim = std::min(v, 160 * 1024) - 256;   // room for the small static arrays
   }
   return lim;
@@ -1260,7 +1262,7 @@ hipError_t run_layer(Ctx& c, Model& m, int li, const bf16_t* next_gain, bool sel
     g.D = D;
     g.pt = c.pt;
     g.pps = c.pps;
-    if (M > kThinRows)
+    if (c.gemm_rows)
       CK(gemm_run(c, EPI_ROPE, g, SPEC_KERNEL_QKV, gemv_bytes(g.N, H, M, 2.0)));
     else
       CK((gemv_launch<EPI_ROPE, 1>(c, g, SPEC_KERNEL_QKV, gemv_bytes(g.N, H, M, 2.0))));
@@ -1283,7 +1285,7 @@ hipError_t run_layer(Ctx& c, Model& m, int li, const bf16_t* next_gain, bool sel
     g.gain = w.ffn_norm;
     g.xg = c.xg;
     g.ss_out = c.ss;
-    if (M > kThinRows)
+    if (c.gemm_rows)
       CK(gemm_run(c, EPI_RESID, g, SPEC_KERNEL_O, gemv_bytes(H, nq * D, M, 10.0)));
     else
       CK((gemv_launch<EPI_RESID, 1>(c, g, SPEC_KERNEL_O, gemv_bytes(H, nq * D, M, 10.0))));
@@ -1307,7 +1309,7 @@ hipError_t run_layer(Ctx& c, Model& m, int li, const bf16_t* next_gain, bool sel
     g.H = H;
     g.eps = d.rms_eps;
     g.u = c.u;
-    if (M > kThinRows)
+    if (c.gemm_rows)
       CK(gemm_run(c, EPI_SWIGLU, g, SPEC_KERNEL_GATEUP, gemv_bytes(2 * F, H, M, 1.0)));
     else
       CK(gemv_launch_p<EPI_SWIGLU>(c, g, std::min(c.ncu, 2 * F / kTile), SPEC_KERNEL_GATEUP,
@@ -1331,7 +1333,7 @@ hipError_t run_layer(Ctx& c, Model& m, int li, const bf16_t* next_gain, bool sel
       g.ldx = F;
       g.splits = m.s_down;
       g.out = c.part;
-      if (M > kThinRows) {
+      if (c.gemm_rows) {
         CK(gemm_run(c, EPI_STORE, g, SPEC_KERNEL_DOWN, gemv_bytes(H, F, M, 4.0 * m.s_down)));
       } else {
         const int per_split = std::max(1, std::min(c.ncu / m.s_down, H / kTile));
@@ -1769,7 +1771,7 @@ hipError_t launch_forward(Ctx& c, PassMode mode) {
     g.logits = c.logits;
     g.allow_logits = draft ? 0 : 1;
     const double bytes = gemv_bytes(c.V, d.hidden, g.M, 0.0) + 8.0 * (c.V / kTile) * g.M;
-    if (g.M > kThinRows)
+    if (g.M > kThinRows || (!draft && c.gemm_rows))
       CK(gemm_run(c, EPI_ARGMAX, g, SPEC_KERNEL_LMHEAD, bytes));
     else
       CK(gemv_launch_p<EPI_ARGMAX>(c, g, std::min(c.ncu, c.V / kTile), SPEC_KERNEL_LMHEAD, bytes));

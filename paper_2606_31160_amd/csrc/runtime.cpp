@@ -254,8 +254,8 @@ Layout make_layout(const spec_config* cfg, const spec_seq_init* seqs) {
   return L;
 }
 
-void set_splits(Model& m, int M) {
-  m.s_down = M > kThinRows ? gemm_down_splits(m.d.hidden, m.d.ffn, num_cus()) : down_splits(M, m.d.ffn, num_cus());
+void set_splits(Model& m, int M, bool gemm_rows) {
+  m.s_down = gemm_rows ? gemm_down_splits(m.d.hidden, m.d.ffn, num_cus()) : down_splits(M, m.d.ffn, num_cus());
 }
 
 // Down-projection k-splits of the persistent pass for one model: the fewest
@@ -292,20 +292,37 @@ size_t part_elems_for(const Model& m, int M) { return (size_t)m.s_down * M * m.d
 // The q/k/v, o, gate/up and LM-head GEMVs keep a workgroup's whole reduction
 // (one k-split): their x rows for the full reduction length must fit in LDS,
 // and each wave streams at most kGemvSteps steps.
-bool check_fits(const spec_dims& d, int M, std::string& err, const char* who) {
-  if (M > kThinRows) return true;   // the batched-row GEMM streams x through LDS in chunks
+// Whether the thin GEMV kernels can stage M rows of every input width of a model.
+bool thin_fits(const spec_dims& d, int M, int* bad_width = nullptr) {
   const int Ks[2] = {d.hidden, d.q_heads * d.head_dim};
   for (int Kd : Ks) {
     const int T = (Kd + 31) / 32;
     if (T > kGemvWaves * kGemvSteps || gemv_p_lds_bytes(M, T) > (size_t)gemv_lds_limit()) {
-      char buf[200];
-      snprintf(buf, sizeof buf, "%s: %d rows per pass (batch*(K+1)) with width %d exceed one GEMV workgroup", who, M,
-               Kd);
-      err = buf;
+      if (bad_width) *bad_width = Kd;
       return false;
     }
   }
   return true;
+}
+
+bool check_fits(const spec_dims& d, int M, std::string& err, const char* who) {
+  // more rows than one MFMA block: the batched-row GEMM, which streams x
+  // through LDS in chunks, takes what the thin kernels cannot stage
+  if (M > kSgMaxRowsGemm) return true;
+  int Kd = 0;
+  if (!thin_fits(d, M, &Kd)) {
+    char buf[200];
+    snprintf(buf, sizeof buf, "%s: %d rows per pass (batch*(K+1)) with width %d exceed one GEMV workgroup", who, M, Kd);
+    err = buf;
+    return false;
+  }
+  return true;
+}
+
+// Layered passes of this many rows run on the batched-row GEMM.
+bool gemm_rows_for(const spec_config* cfg, bool has_draft, int M) {
+  if (M > kThinRows) return true;
+  return M > kSgMaxRowsGemm && (!thin_fits(cfg->target, M) || (has_draft && !thin_fits(cfg->draft, M)));
 }
 
 // Carves the workspace (base == nullptr only measures).  Returns total bytes.
@@ -325,11 +342,12 @@ size_t carve(Ctx& c, const spec_config* cfg, const spec_seq_init* seqs, bool has
   c.attn_splits = L.splits;
   c.tgt.d = cfg->target;
   c.tgt.flat = false;
-  set_splits(c.tgt, L.M);
+  c.gemm_rows = gemm_rows_for(cfg, has_draft, L.M);
+  set_splits(c.tgt, L.M, c.gemm_rows);
   if (has_draft) {
     c.drf.d = cfg->draft;
     c.drf.flat = true;
-    set_splits(c.drf, L.M);
+    set_splits(c.drf, L.M, c.gemm_rows);
   }
   const spec_dims& t = cfg->target;
   const int H = t.hidden, D = t.head_dim;

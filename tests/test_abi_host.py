@@ -85,6 +85,17 @@ def test_workspace_query_on_host():
     assert B.spec_workspace_bytes(cfg, seqs) > n1
 
 
+@pytest.mark.parametrize("name", ["C3", "C6"])
+def test_benchmark_and_paper_configs_validate_on_host(name):
+    # the 7B-class benchmark configuration, and the paper's backbone at K = 16
+    # (17 verify rows, interleaved axis assignment)
+    w = W.get(name)
+    cfg = _cfg(w)
+    seqs, keep = _seqs(w, cfg, blocks=_blocks(w))
+    n = B.spec_workspace_bytes(cfg, seqs)
+    assert n > 0 and n % 256 == 0
+
+
 @pytest.mark.parametrize("mutate,needle", [
     (lambda c, s: setattr(c, "K", 17), "K out of range"),
     (lambda c, s: setattr(c, "batch", 0), "batch"),

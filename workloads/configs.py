@@ -5,7 +5,7 @@ holds none of the method's arithmetic: position ids, rotations, the forward pass
 and the accept/commit rule live in the oracle and, independently, in the HIP
 library.
 
-The five workloads follow the synthetic stand-ins for the paper's Alpamayo-R1
+The workloads follow the synthetic stand-ins for the paper's Alpamayo-R1
 clips (Sec. 5: prompts dominated by visual tokens, chain-of-causation outputs of
 15-20 tokens, greedy verification), sized after a Qwen2.5-VL-7B-class backbone.
 """
@@ -93,6 +93,16 @@ QWEN7B_LAYER = ModelShape(layers=28, hidden=3584, q_heads=28, kv_heads=4, head_d
                           ffn=18944, mrope_section=(16, 24, 24))
 QWEN7B_DRAFT = replace(QWEN7B_LAYER, layers=2)
 
+# The paper's own target backbone (Sec. 5): 36 decoder layers and 32 attention
+# heads, as stated there; the remaining widths (hidden 4096, 8 kv heads, SwiGLU
+# 12288, vocabulary 151936) are those of that backbone's public configuration.
+# Its rotary axis assignment is the interleaved form of Eq. axis-assign.  The
+# draft is one FlatRoPE layer of the same width (the paper's autoregressive draft
+# is a single layer).
+PAPER_BACKBONE = ModelShape(layers=36, hidden=4096, q_heads=32, kv_heads=8, head_dim=128,
+                            ffn=12288, mrope_section=(24, 20, 20), interleaved=True)
+PAPER_DRAFT = replace(PAPER_BACKBONE, layers=1, interleaved=False)
+
 
 def _c1() -> Workload:
     # 1x16x16 vision grid at index 0, then 64 trajectory/text tokens.
@@ -134,8 +144,16 @@ def _c5(seed: int = 1000) -> Workload:
                     p_accept=tuple(float(p) for p in ps), max_new_tokens=20)
 
 
+def _c6() -> Workload:
+    # The paper's verification width: K = 16 proposals (17 verify rows) against
+    # its 36-layer backbone, over the 4096-token vision-dominated prompt of C3.
+    lay = SeqLayout(4096, (VisionBlock(0, 4, 28, 32),))
+    return Workload("C6-paper-backbone-K16", PAPER_BACKBONE, PAPER_DRAFT, vocab=151936, K=16,
+                    seqs=(lay,), p_accept=(0.75,))
+
+
 def get(name: str) -> Workload:
-    table = {"C1": _c1, "C2": _c2, "C3": _c3, "C5": _c5}
+    table = {"C1": _c1, "C2": _c2, "C3": _c3, "C5": _c5, "C6": _c6}
     return table[name]()
 
 
