@@ -12,7 +12,9 @@ Modules
   model      the decoder stack evaluated on new rows against a KV cache
   spec       Eq. stage1 (greedy), Eq. propose, Eq. verify, Eq. accept, Eq. commit
   report     Eq. L-and-speedup and the cost ratio of Sec. 5.1
+  budget     the attention-budget readout of Sec. 4.2 (mass per token class,
+             entropy within trajectory/text)
 
 Every function with no independent pin says "parity unpinned" in its docstring.
 """
-from . import numerics, positions, rope, model, spec, report  # noqa: F401
+from . import numerics, positions, rope, budget, model, spec, report  # noqa: F401

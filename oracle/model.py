@@ -24,7 +24,7 @@ from typing import Callable, Dict, Optional, Sequence
 
 import numpy as np
 
-from . import numerics, rope
+from . import budget, numerics, rope
 
 ROTARY_MROPE = "mrope"
 ROTARY_FLAT = "flat"
@@ -103,6 +103,12 @@ class Decoder:
         self.lm_chunk = lm_chunk
         self._layers: Dict[int, Dict[str, np.ndarray]] = {}
         self._embed: Optional[np.ndarray] = None
+        # attention budget readout (budget.budget): when readout_layer is set,
+        # forward() stores the [M, n_q, 4] readout of that layer's attention
+        # over slots classified by readout_classes in self.readout
+        self.readout_layer: Optional[int] = None
+        self.readout_classes: Optional[np.ndarray] = None
+        self.readout: Optional[np.ndarray] = None
 
     # -- weights -----------------------------------------------------------
     def layer(self, li: int) -> Dict[str, np.ndarray]:
@@ -182,6 +188,8 @@ class Decoder:
             v = self._r(v)
             cache.k[li][slots] = k
             cache.v[li][slots] = v
+            if li == self.readout_layer:
+                self.readout = budget.budget(q, cache.k[li], slots, self.readout_classes)
             o = self._r(attend(q, cache.k[li], cache.v[li], slots).reshape(M, nq * D))
             x = x + o @ W["wo"].T
             b = self._r(rmsnorm(x, W["ffn_norm"], s.rms_eps))
