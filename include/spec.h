@@ -68,7 +68,8 @@ typedef struct spec_dims {
   int32_t head_dim;          /* 64 or 128 */
   int32_t ffn;               /* SwiGLU inner width; multiple of 16 */
   int32_t mrope_section[3];  /* (s_T, s_H, s_W) rotary pairs per axis, summing to
-                                head_dim/2 (Eq. rope-3d); ignored by the draft */
+                                head_dim/2 (Eq. rope-3d); ignored by the draft unless
+                                SPEC_FLAG_DRAFT_MROPE */
   int32_t interleaved;       /* 0: blocked axis assignment, 1: d mod 3 (Eq. axis-assign) */
   float rope_base;           /* theta_d = rope_base^(-2d/head_dim) (Eq. mrope-phase) */
   float rms_eps;             /* RMSNorm epsilon */
@@ -83,6 +84,9 @@ typedef struct spec_dims {
                                       of at most 16 rows (batch*(K+1) <= 16) on the layered path stream a
                                       tile-packed copy of every weight matrix that spec_init writes into
                                       the workspace (its size is part of spec_workspace_bytes) */
+#define SPEC_FLAG_DRAFT_MROPE 16   /* the draft rotates with 3D M-RoPE (its own mrope_section and
+                                      interleaved, validated as the target's) instead of FlatRoPE: the
+                                      comparison arm of the attention-budget readout (Sec. 4.2) */
 
 typedef struct spec_config {
   spec_dims target;          /* deliberative reasoner (3D M-RoPE) */
@@ -203,6 +207,25 @@ spec_status spec_verify(spec_ctx* ctx, const int32_t* d_draft_tokens, void* d_lo
  * State: VERIFIED -> READY. */
 spec_status spec_commit(spec_ctx* ctx, int32_t* d_accept_len, int32_t* d_committed,
                         int32_t* d_n_committed, int32_t* d_finished);
+
+/* Attention-budget readout (Sec. 4.2, Table attn-budget): arms the next pass
+ * of `model` (0: the target, i.e. the next spec_verify; 1: the draft, i.e. the
+ * next draft step) to also report where attention layer `layer` (0-based) puts
+ * its softmax mass.  Cache slots are classed as visual (inside a vision
+ * block), trajectory/text (any other prompt slot) or generated (index >=
+ * prefix_len).  For every row j < the pass's row count of sequence b and
+ * every query head h of that model, the pass writes d_out[((b*(K+1) + j) *
+ * q_heads + h)*4 + c] (device float32, 16-byte aligned):
+ *   c = 0, 1, 2  attention mass on visual / trajectory-text / generated slots
+ *                (the three sum to 1 up to rounding);
+ *   c = 3        entropy of the attention restricted to trajectory/text slots
+ *                and renormalised, divided by ln(number of those slots)
+ *                (0 when the prompt has at most one such slot).
+ * Rows a pass does not run (finished sequences, rows past a draft pass's
+ * count) are left unchanged.  The armed pass is launched kernel by kernel
+ * (no graph replay); the readout then disarms.  d_out = NULL disarms.
+ * Not available on the persistent pass kernel (SPEC_E_STATE).  Any state. */
+spec_status spec_attn_readout(spec_ctx* ctx, int32_t model, int32_t layer, float* d_out);
 
 /* Synchronising: waits for the stream, then reports how many sequences have
  * finished (*n_finished, may be NULL) and returns SPEC_E_INVAL / SPEC_E_NUMERIC

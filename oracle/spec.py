@@ -88,7 +88,11 @@ class Sequence:
         self.finished = False
         self.history: List[int] = []              # accept length per verify
         if draft is not None:
-            self.dc = draft.new_cache(capacity, positions.flat_positions(capacity))
+            # FlatRoPE draft: every slot at its 1D index; an M-RoPE draft (the
+            # comparison arm of the attention-budget readout, Sec. 4.2) uses
+            # the target's 3D positions
+            dpos = self.tpos if draft.rotary == M.ROTARY_MROPE else positions.flat_positions(capacity)
+            self.dc = draft.new_cache(capacity, dpos)
             for li in range(draft.s.layers):
                 k, v = drf_prefix_kv(li)
                 draft.fill_prefix(self.dc, li, k, v)

@@ -24,6 +24,7 @@ SPEC_FLAG_NO_GRAPHS = 1
 SPEC_FLAG_PERSISTENT = 2
 SPEC_FLAG_PASS_TIMELINE = 4
 SPEC_FLAG_ROWMAJOR = 8
+SPEC_FLAG_DRAFT_MROPE = 16
 STATUS = {0: "SPEC_OK", 1: "SPEC_E_INVAL", 2: "SPEC_E_STATE", 3: "SPEC_E_CAPACITY", 5: "SPEC_E_HIP",
           6: "SPEC_E_NUMERIC"}
 KERNEL_KINDS = {"qkv": 0, "o": 1, "gateup": 2, "down": 3, "lmhead": 4, "attn": 5, "other": 6,
@@ -85,6 +86,7 @@ def lib():
             "draft_steps": [P, c_int32, P],
             "spec_verify": [P, P, P],
             "spec_commit": [P, P, P, P, P],
+            "spec_attn_readout": [P, c_int32, c_int32, P],
             "spec_sync": [P, POINTER(c_int32)],
             "spec_debug_positions": [P, c_int32, P, c_int32],
             "spec_debug_state": [P, c_int32, P],
@@ -158,6 +160,10 @@ def spec_commit(ctx, d_accept_len: int = 0, d_committed: int = 0, d_n_committed:
                 d_finished: int = 0) -> None:
     _check(lib().spec_commit(ctx, *(c_void_p(p or None) for p in (d_accept_len, d_committed, d_n_committed,
                                                                     d_finished))), "spec_commit", ctx)
+
+
+def spec_attn_readout(ctx, model: int, layer: int, d_out: int = 0) -> None:
+    _check(lib().spec_attn_readout(ctx, model, layer, c_void_p(d_out or None)), "spec_attn_readout", ctx)
 
 
 def spec_sync(ctx) -> int:

@@ -120,6 +120,8 @@ struct Ctx {
   float* amax_v = nullptr;          // [vocab/16][Mpad] per-tile maximum logit
   int32_t* amax_i = nullptr;        // [vocab/16][Mpad] its index
   bf16_t* logits = nullptr;         // [Mpad][vocab] bf16 logits of the last verify
+  int8_t* cls = nullptr;            // [B][cap] class of every slot: 0 visual, 1 trajectory/text, 2 generated
+  float* rp = nullptr;              // [splits][B][q_heads][R][4] attention-budget readout partials
 
   const bf16_t* embed = nullptr;
   Model tgt, drf;
@@ -161,6 +163,15 @@ struct Ctx {
   int32_t* g_drafts_out = nullptr;
   int32_t* commit_out[4] = {};                   // spec_commit's outputs (baked into the commit graph)
   int32_t* g_commit_out[4] = {};
+
+  // attention-budget readout: armed by spec_attn_readout, active during the
+  // one pass it applies to
+  float ro_inv_ln[SPEC_MAX_BATCH] = {};   // 1 / ln(trajectory/text slots) per sequence, 0 if <= 1
+  int ro_arm_model = -1, ro_arm_layer = 0;
+  float* ro_arm_out = nullptr;
+  const Model* ro_m = nullptr;
+  int ro_layer = 0;
+  float* ro_out = nullptr;
 
   // timing
   bool timing = false;

@@ -643,6 +643,13 @@ __global__ __launch_bounds__(256) void k_down_finish(FinishArgs p) {
 // softmax statistics of the chunk are per lane (its row); the row max crosses
 // the four lane groups with two xor-shuffles.  Partial outputs are stored
 // unnormalised in bf16, with the chunk's max and sum in fp32, for the combine.
+//
+// The readout variant (RO) also writes, per (row, q head, split), the sums of
+// 2^(s - m) over the split's visible keys of each token class (visual,
+// trajectory/text, generated; s = score in log2 units, m = the split's max)
+// and E = sum over trajectory/text keys of 2^(s - m) (s - m): the terms from
+// which the combine forms the attention mass per class and the entropy within
+// trajectory/text (Sec. 4.2, Table attn-budget).
 // ---------------------------------------------------------------------------
 
 struct AttnArgs {
@@ -656,9 +663,12 @@ struct AttnArgs {
   float* lp;
   int nq, nkv, G, R, B, pps, chunk, row_blocks;
   float scale_log2;      // log2(e) / sqrt(D)
+  const int8_t* cls;     // readout: [B][cap] class of every slot (0 visual, 1 trajectory/text, 2 generated)
+  float* rp;             // readout: [splits][B][nq][R][4] class sums and trajectory E term
+  int cap;
 };
 
-template <int D>
+template <int D, bool RO>
 __device__ __forceinline__ void attn_partials(const AttnArgs& a, unsigned char* lds) {
   const int split = blockIdx.x;
   const int kvh = blockIdx.y / a.row_blocks, rb = blockIdx.y % a.row_blocks;
@@ -693,6 +703,7 @@ __device__ __forceinline__ void attn_partials(const AttnArgs& a, unsigned char* 
     if (rvalid) {
       bf16_t* op = a.op + oi * D;
       for (int d = g4 * 4; d < D; d += 16) *reinterpret_cast<u32x2*>(op + d) = u32x2{0u, 0u};
+      if (RO && g4 == 0) *reinterpret_cast<f32x4*>(a.rp + oi * 4) = f32x4{0.f, 0.f, 0.f, 0.f};
     }
     return;
   }
@@ -706,6 +717,14 @@ __device__ __forceinline__ void attn_partials(const AttnArgs& a, unsigned char* 
     const bf16_t* qp = a.q + ((size_t)(b * a.R + j) * a.nq + hq) * D + 8 * g4;
 #pragma unroll
     for (int t = 0; t < D / 32; ++t) qf[t] = ld16(qp + 32 * t);
+  }
+  // readout: classes of this lane's 16 keys, 4 consecutive slots per word
+  // (byte i of word h: slot k0 + 16 h + 4 g4 + i; k0 + 63 < cap)
+  uint32_t cw[4] = {0u, 0u, 0u, 0u};
+  if (RO) {
+    const int8_t* cp = a.cls + (size_t)b * a.cap + k0 + 4 * g4;
+#pragma unroll
+    for (int h = 0; h < 4; ++h) cw[h] = *reinterpret_cast<const uint32_t*>(cp + 16 * h);
   }
 
   // Stage the chunk once for all waves: keys [chunk][D + 8] and values
@@ -797,10 +816,19 @@ __device__ __forceinline__ void attn_partials(const AttnArgs& a, unsigned char* 
   m_run = fmaxf(m_run, __shfl_xor(m_run, 16));
   m_run = fmaxf(m_run, __shfl_xor(m_run, 32));
   float l_run = 0.f;
+  float rs[4] = {0.f, 0.f, 0.f, 0.f};   // readout: class sums, then the trajectory E term
 #pragma unroll
   for (int i = 0; i < 16; ++i) {
-    p[i] = (p[i] == -INFINITY) ? 0.f : exp2f(p[i] - m_run);
+    const float v = p[i];
+    p[i] = (v == -INFINITY) ? 0.f : exp2f(v - m_run);
     l_run += p[i];
+    if (RO) {
+      const uint32_t cl = (cw[i >> 2] >> (8 * (i & 3))) & 0xffu;
+      rs[0] += cl == 0 ? p[i] : 0.f;
+      rs[1] += cl == 1 ? p[i] : 0.f;
+      rs[2] += cl == 2 ? p[i] : 0.f;
+      rs[3] += (cl == 1 && v != -INFINITY) ? p[i] * (v - m_run) : 0.f;
+    }
   }
   f32x4 o[D / 16];
 #pragma unroll
@@ -814,6 +842,14 @@ __device__ __forceinline__ void attn_partials(const AttnArgs& a, unsigned char* 
   }
   l_run += __shfl_xor(l_run, 16);
   l_run += __shfl_xor(l_run, 32);
+  if (RO) {
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      rs[r] += __shfl_xor(rs[r], 16);
+      rs[r] += __shfl_xor(rs[r], 32);
+    }
+    if (rvalid && g4 == 0) *reinterpret_cast<f32x4*>(a.rp + oi * 4) = f32x4{rs[0], rs[1], rs[2], rs[3]};
+  }
   if (rvalid) {
     bf16_t* op = a.op + oi * D;
 #pragma unroll
@@ -827,10 +863,10 @@ __device__ __forceinline__ void attn_partials(const AttnArgs& a, unsigned char* 
   }
 }
 
-template <int D>
+template <int D, bool RO>
 __global__ __launch_bounds__(256) void k_attn(AttnArgs a) {
   extern __shared__ __align__(16) unsigned char lds[];
-  attn_partials<D>(a, lds);
+  attn_partials<D, RO>(a, lds);
 }
 
 
@@ -840,16 +876,27 @@ size_t attn_lds_bytes(int chunk, int D) {
 
 // Merge the splits of each (row, q head): o = sum_s 2^(m_s - M) O_s / sum_s
 // 2^(m_s - M) l_s.  grid (R, q_heads, B), 256 threads: 8 groups of splits x 32 groups of 4 columns.
+//
+// Readout (RO): with w_s = 2^(m_s - M), L = sum_s w_s l_s, the mass of class c
+// is sum_s w_s C_c,s / L, and E = sum_s w_s (E_s + (m_s - M) C_1,s) is the
+// trajectory term relative to M, so that for q_k = 2^(s_k - M) / C_1 over the
+// trajectory/text keys, H(q) = ln C_1 - ln 2 * E / C_1 (C_1 = sum_s w_s C_1,s).
 struct CombineArgs {
   const SeqState* st;
   const bf16_t* op;      // bf16 partial outputs
   const float *mp, *lp;
   bf16_t* o;             // [Mpad][nq*D]
   int nq, D, R, B, chunk;
+  const float* rp;       // readout: [splits][B][nq][R][4] partial class sums and E terms
+  float* ro;             // readout: [B][R][nq][4] masses (visual, trajectory/text, generated), entropy
+  float inv_ln[SPEC_MAX_BATCH];   // readout: 1 / ln(trajectory/text slots) of each sequence, 0 if <= 1
 };
 
 // One (row j, q head h, sequence b) of the combine; coef is LDS of at least
 // ((splits + 3) & ~3) + 8 * D floats.  Called by all threads of a workgroup.
+constexpr float kLn2 = 0.6931471805599453f;
+
+template <bool RO>
 __device__ __forceinline__ void combine_unit(const CombineArgs& a, int j, int h, int b, float* coef) {
   const SeqState& s = a.st[b];
   if (j >= s.count) return;
@@ -863,14 +910,34 @@ __device__ __forceinline__ void combine_unit(const CombineArgs& a, int j, int h,
     for (int sp = l; sp < ns; sp += 64) M = fmaxf(M, a.mp[sp * sstride + row]);
     for (int o = 32; o > 0; o >>= 1) M = fmaxf(M, __shfl_xor(M, o));
     float L = 0.f;
+    float r[4] = {0.f, 0.f, 0.f, 0.f};
     for (int sp = l; sp < ns; sp += 64) {
-      const float w = exp2f(a.mp[sp * sstride + row] - M);
+      const float ms = a.mp[sp * sstride + row];   // finite: split sp holds a key the row sees
+      const float w = exp2f(ms - M);
       coef[sp] = w;
       L += w * a.lp[sp * sstride + row];
+      if (RO) {
+        const f32x4 c = *reinterpret_cast<const f32x4*>(a.rp + (sp * sstride + row) * 4);
+        r[0] += w * c.x;
+        r[1] += w * c.y;
+        r[2] += w * c.z;
+        r[3] += w * (c.w + (ms - M) * c.y);
+      }
     }
     for (int o = 32; o > 0; o >>= 1) L += __shfl_xor(L, o);
     const float inv = 1.f / L;
     for (int sp = l; sp < ns; sp += 64) coef[sp] *= inv;
+    if (RO) {
+#pragma unroll
+      for (int k = 0; k < 4; ++k)
+        for (int o = 32; o > 0; o >>= 1) r[k] += __shfl_xor(r[k], o);
+      if (l == 0) {
+        const float il = a.inv_ln[b];
+        const float hn = (il > 0.f && r[1] > 0.f) ? (logf(r[1]) - kLn2 * r[3] / r[1]) * il : 0.f;
+        *reinterpret_cast<f32x4*>(a.ro + (((size_t)b * a.R + j) * a.nq + h) * 4) =
+            f32x4{r[0] * inv, r[1] * inv, r[2] * inv, hn};
+      }
+    }
   }
   __syncthreads();
   // thread = (split group sg of 8, 4-wide column group c4); D / 4 <= 32 groups
@@ -899,9 +966,10 @@ __device__ __forceinline__ void combine_unit(const CombineArgs& a, int j, int h,
   }
 }
 
+template <bool RO>
 __global__ __launch_bounds__(256) void k_attn_combine(CombineArgs a) {
   extern __shared__ float coef[];   // [ns] weights, then [8][D] partial sums
-  combine_unit(a, blockIdx.x, blockIdx.y, blockIdx.z, coef);
+  combine_unit<RO>(a, blockIdx.x, blockIdx.y, blockIdx.z, coef);
 }
 
 // ---------------------------------------------------------------------------
@@ -1171,7 +1239,8 @@ hipError_t gemm_run(Ctx& c, int epi, const GemvArgs& g, int kind, double bytes) 
 // the shapes allow it; measured per projection on the 7B-class verify.
 constexpr bool kQkvAsJob = false, kOAsJob = false, kDownAsJob = false;
 
-// Split-KV attention of one layer + the combine of its splits.
+// Split-KV attention of one layer + the combine of its splits; on the layer
+// an armed readout names, the readout variants of both kernels.
 hipError_t launch_attention(Ctx& c, Model& m, int li) {
   const spec_dims& d = m.d;
   const int D = d.head_dim, nq = d.q_heads, nkv = d.kv_heads;
@@ -1179,21 +1248,26 @@ hipError_t launch_attention(Ctx& c, Model& m, int li) {
   bf16_t* vt = m.vt + m.kv_layer * li;
   const int G = nq / nkv;
   const int rb = (c.R * G + 63) / 64;
+  const bool ro = c.ro_out && c.ro_m == &m && c.ro_layer == li;
   AttnArgs p{c.st, c.q, kc, vt, c.pt, reinterpret_cast<bf16_t*>(c.op), c.mp, c.lp, nq, nkv, G, c.R, c.B, c.pps, c.attn_chunk, rb,
-             kLog2e / sqrtf((float)D)};
+             kLog2e / sqrtf((float)D), c.cls, c.rp, c.cap};
   dim3 grid(c.attn_splits, nkv * rb, c.B);
-  CombineArgs cb{c.st, reinterpret_cast<const bf16_t*>(c.op), c.mp, c.lp, c.o, nq, D, c.R, c.B, c.attn_chunk};
+  CombineArgs cb{c.st, reinterpret_cast<const bf16_t*>(c.op), c.mp, c.lp, c.o, nq, D, c.R, c.B, c.attn_chunk, c.rp,
+                 ro ? c.ro_out : nullptr, {}};
+  for (int b = 0; b < c.B && b < SPEC_MAX_BATCH; ++b) cb.inv_ln[b] = c.ro_inv_ln[b];
   const size_t comb_lds = (size_t)(((c.attn_splits + 3) & ~3) + 8 * D) * sizeof(float);
+  const size_t lds = attn_lds_bytes(c.attn_chunk, D);
   {
     Timed t(c, SPEC_KERNEL_ATTN, 0);
     if (D == 128)
-      hipExtLaunchKernelGGL(k_attn<128>, grid, dim3(256), attn_lds_bytes(c.attn_chunk, D), S(c), t.e0, t.e1, 0, p);
+      hipExtLaunchKernelGGL(ro ? k_attn<128, true> : k_attn<128, false>, grid, dim3(256), lds, S(c), t.e0, t.e1, 0, p);
     else
-      hipExtLaunchKernelGGL(k_attn<64>, grid, dim3(256), attn_lds_bytes(c.attn_chunk, D), S(c), t.e0, t.e1, 0, p);
+      hipExtLaunchKernelGGL(ro ? k_attn<64, true> : k_attn<64, false>, grid, dim3(256), lds, S(c), t.e0, t.e1, 0, p);
     CK(hipGetLastError());
   }
   Timed t2(c, SPEC_KERNEL_OTHER, 0);
-  hipExtLaunchKernelGGL(k_attn_combine, dim3(c.R, nq, c.B), dim3(256), comb_lds, S(c), t2.e0, t2.e1, 0, cb);
+  hipExtLaunchKernelGGL(ro ? k_attn_combine<true> : k_attn_combine<false>, dim3(c.R, nq, c.B), dim3(256), comb_lds,
+                        S(c), t2.e0, t2.e1, 0, cb);
   return hipGetLastError();
 }
 
@@ -1356,10 +1430,11 @@ void init_kernel_attributes() {
   done = true;
   pass_set_attributes(gemv_lds_limit());
   sg_set_attributes(gemv_lds_limit());
-  (void)hipFuncSetAttribute(reinterpret_cast<const void*>(&k_attn<128>), hipFuncAttributeMaxDynamicSharedMemorySize,
-                            (int)attn_lds_bytes(kAttnChunk, 128));
-  (void)hipFuncSetAttribute(reinterpret_cast<const void*>(&k_attn<64>), hipFuncAttributeMaxDynamicSharedMemorySize,
-                            (int)attn_lds_bytes(kAttnChunk, 64));
+  const void* attn[4] = {reinterpret_cast<const void*>(&k_attn<128, false>), reinterpret_cast<const void*>(&k_attn<128, true>),
+                         reinterpret_cast<const void*>(&k_attn<64, false>), reinterpret_cast<const void*>(&k_attn<64, true>)};
+  for (int i = 0; i < 4; ++i)
+    (void)hipFuncSetAttribute(attn[i], hipFuncAttributeMaxDynamicSharedMemorySize,
+                              (int)attn_lds_bytes(kAttnChunk, i < 2 ? 128 : 64));
   set_lds_limit_p<EPI_STORE, 1>();
   set_lds_limit_p<EPI_STORE, 2>();
   set_lds_limit_p<EPI_STORE, 3>();

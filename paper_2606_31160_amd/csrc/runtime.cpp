@@ -107,7 +107,7 @@ bool check_config(const spec_config* cfg, const spec_seq_init* seqs, bool has_dr
   }
   if (!check_dims(cfg->target, true, err, "target")) return false;
   if (has_draft) {
-    if (!check_dims(cfg->draft, false, err, "draft")) return false;
+    if (!check_dims(cfg->draft, (cfg->flags & SPEC_FLAG_DRAFT_MROPE) != 0, err, "draft")) return false;
     if (cfg->draft.hidden != cfg->target.hidden || cfg->draft.head_dim != cfg->target.head_dim ||
         cfg->draft.rope_base != cfg->target.rope_base) {
       err = "draft hidden, head_dim and rope_base must equal the target's";
@@ -346,7 +346,7 @@ size_t carve(Ctx& c, const spec_config* cfg, const spec_seq_init* seqs, bool has
   set_splits(c.tgt, L.M, c.gemm_rows);
   if (has_draft) {
     c.drf.d = cfg->draft;
-    c.drf.flat = true;
+    c.drf.flat = (cfg->flags & SPEC_FLAG_DRAFT_MROPE) == 0;
     set_splits(c.drf, L.M, c.gemm_rows);
   }
   const spec_dims& t = cfg->target;
@@ -390,6 +390,8 @@ size_t carve(Ctx& c, const spec_config* cfg, const spec_seq_init* seqs, bool has
   c.amax_v = cv.take<float>((size_t)(L.V / kTile) * L.Mpad);
   c.amax_i = cv.take<int32_t>((size_t)(L.V / kTile) * L.Mpad);
   c.logits = cv.take<bf16_t>((size_t)L.Mpad * L.V);
+  c.cls = cv.take<int8_t>((size_t)L.B * L.cap);
+  c.rp = cv.take<float>(attn_rows * 4);
   c.tgt.kv_layer = (size_t)L.pool * t.kv_heads * kAttnChunk * D;
   c.tgt.kc = cv.take<bf16_t>(c.tgt.kv_layer * t.layers);
   c.tgt.vt = cv.take<bf16_t>(c.tgt.kv_layer * t.layers);
@@ -572,6 +574,21 @@ spec_status run_graph(Ctx& c, hipGraphExec_t& ge, Launch&& launch) {
 // pass's graph also writes the proposals to the caller's array, so it is
 // captured again when that array changes.
 spec_status run_pass(Ctx& c, PassMode mode) {
+  const int mi = mode == PASS_VERIFY ? 0 : 1;
+  if (c.ro_arm_out && c.ro_arm_model == mi) {
+    // an armed readout: this pass is launched kernel by kernel with the
+    // readout variants on its layer; graphs and later passes are unaffected
+    c.ro_m = mi ? &c.drf : &c.tgt;
+    c.ro_layer = c.ro_arm_layer;
+    c.ro_out = c.ro_arm_out;
+    c.ro_arm_out = nullptr;
+    c.ro_arm_model = -1;
+    const hipError_t e = launch_forward(c, mode);
+    c.ro_m = nullptr;
+    c.ro_out = nullptr;
+    HIPCHK(c, e, "forward pass with readout");
+    return SPEC_OK;
+  }
   const bool graphs = c.use_graphs && !c.timing;
   if (!graphs) {
     // timing mode: a head start so the timed kernels run back to back
@@ -731,7 +748,7 @@ spec_status spec_init(const spec_config* cfg, const void* embed, const spec_mode
       }
     std::vector<int8_t> ax_t(half), ax_d(half);
     build_axis(cfg->target, false, ax_t.data());
-    build_axis(cfg->draft, true, ax_d.data());
+    build_axis(cfg->draft, c.drf.flat, ax_d.data());
     c.pt_host.assign((size_t)c.B * c.pps, 0);
     c.npages.assign(c.B, 0);
     for (int b = 0, next = 0; b < c.B; ++b) {
@@ -740,6 +757,21 @@ spec_status spec_init(const spec_config* cfg, const void* embed, const spec_mode
       for (int i = 0; i < n; ++i)
         c.pt_host[(size_t)b * c.pps + i] = seqs[b].page_table ? seqs[b].page_table[i] : next + i;
       next += n;
+    }
+    // token class of every slot for the attention-budget readout (Sec. 4.2):
+    // vision-block slots, other prompt slots, generated slots
+    std::vector<int8_t> cls((size_t)c.B * c.cap, 2);
+    for (int b = 0; b < c.B; ++b) {
+      int8_t* cb = cls.data() + (size_t)b * c.cap;
+      std::fill(cb, cb + seqs[b].prefix_len, (int8_t)1);
+      int ntraj = seqs[b].prefix_len;
+      for (int i = 0; i < seqs[b].n_blocks; ++i) {
+        const spec_vision_block& v = seqs[b].blocks[i];
+        const int n = v.t * v.h * v.w;
+        std::fill(cb + v.start, cb + v.start + n, (int8_t)0);
+        ntraj -= n;
+      }
+      c.ro_inv_ln[b] = ntraj > 1 ? (float)(1.0 / std::log((double)ntraj)) : 0.f;
     }
     std::vector<SeqState> st(c.B);
     std::vector<int32_t> hist((size_t)c.B * c.cap, 0);
@@ -769,7 +801,8 @@ spec_status spec_init(const spec_config* cfg, const void* embed, const spec_mode
         (e = hipMemcpyAsync(c.drf.axis, ax_d.data(), half, hipMemcpyHostToDevice, stream)) != hipSuccess ||
         (e = hipMemcpyAsync(c.st, st.data(), st.size() * sizeof(SeqState), hipMemcpyHostToDevice, stream)) !=
             hipSuccess ||
-        (e = hipMemcpyAsync(c.hist, hist.data(), hist.size() * 4, hipMemcpyHostToDevice, stream)) != hipSuccess)
+        (e = hipMemcpyAsync(c.hist, hist.data(), hist.size() * 4, hipMemcpyHostToDevice, stream)) != hipSuccess ||
+        (e = hipMemcpyAsync(c.cls, cls.data(), cls.size(), hipMemcpyHostToDevice, stream)) != hipSuccess)
       return hip_fail(e, "table upload");
     if (c.use_pass) {
       if ((e = hipMemcpyAsync(c.tgt.lw_dev, c.tgt.L.data(), c.tgt.L.size() * sizeof(LayerW), hipMemcpyHostToDevice,
@@ -844,7 +877,7 @@ spec_status draft_steps(spec_ctx* ctx, int32_t n, int32_t* d_draft_tokens) {
     if (c.phase == Ctx::VERIFIED) return set_err(c, SPEC_E_STATE, "draft_steps: commit the last verify first");
     if (n < 1 || n > c.K - c.dsteps) return set_err(c, SPEC_E_STATE, "draft_steps: n must be 1..K minus the steps taken");
     c.draft_out = d_draft_tokens;
-    if (n == 1 || !c.use_graphs || c.timing) {
+    if (n == 1 || !c.use_graphs || c.timing || (c.ro_arm_out && c.ro_arm_model == 1)) {
       for (int i = 0; i < n; ++i) {
         spec_status s = run_pass(c, PASS_DRAFT);
         if (s != SPEC_OK) return s;
@@ -897,6 +930,27 @@ spec_status spec_commit(spec_ctx* ctx, int32_t* d_accept_len, int32_t* d_committ
     if (s != SPEC_OK) return s;
     c.phase = Ctx::READY;
     c.dsteps = 0;
+    return SPEC_OK;
+  });
+}
+
+spec_status spec_attn_readout(spec_ctx* ctx, int32_t model, int32_t layer, float* d_out) {
+  return guarded(ctx, [&](Ctx& c) -> spec_status {
+    if (!d_out) {
+      c.ro_arm_out = nullptr;
+      c.ro_arm_model = -1;
+      return SPEC_OK;
+    }
+    if (model != 0 && model != 1) return set_err(c, SPEC_E_INVAL, "spec_attn_readout: model must be 0 or 1");
+    if (model == 1 && !c.has_draft) return set_err(c, SPEC_E_STATE, "spec_attn_readout: no draft model");
+    const Model& m = model ? c.drf : c.tgt;
+    if (layer < 0 || layer >= m.d.layers) return set_err(c, SPEC_E_INVAL, "spec_attn_readout: layer out of range");
+    if (!aligned16(d_out)) return set_err(c, SPEC_E_INVAL, "spec_attn_readout: d_out must be 16-byte aligned");
+    if (c.use_pass)
+      return set_err(c, SPEC_E_STATE, "spec_attn_readout: not available on the persistent pass kernel");
+    c.ro_arm_model = model;
+    c.ro_arm_layer = layer;
+    c.ro_arm_out = d_out;
     return SPEC_OK;
   });
 }

@@ -175,6 +175,17 @@ class Session:
     def commit(self):
         B.spec_commit(self.ctx, self.acc.data_ptr(), self.com.data_ptr(), self.ncom.data_ptr(), self.fin.data_ptr())
 
+    def attn_readout(self, model: int, layer: int):
+        """Arms the attention-budget readout of `layer` for the next pass of
+        `model` (0 target, 1 draft); returns the float32 [B, K+1, q_heads, 4]
+        device tensor that pass fills (NaN where it writes nothing)."""
+        shape = self.w.target if model == 0 else self.w.draft
+        out = self.torch.full((self.B, self.K + 1, shape.q_heads, 4), float("nan"), dtype=self.torch.float32,
+                              device=self.dev)
+        self._readout = out
+        B.spec_attn_readout(self.ctx, model, layer, out.data_ptr())
+        return out
+
     def sync(self) -> int:
         return B.spec_sync(self.ctx)
 

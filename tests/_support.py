@@ -23,12 +23,13 @@ def capacity_for(w: W.Workload, b: int) -> int:
     return w.seqs[b].prefix_len + w.max_new_tokens + w.K + 2
 
 
-def oracle_decoders(w: W.Workload, provider, mirror: bool = False, cache_weights: bool = True):
+def oracle_decoders(w: W.Workload, provider, mirror: bool = False, cache_weights: bool = True,
+                    draft_rotary: str = OM.ROTARY_FLAT):
     T = OM.Decoder(provider, "target", w.target, w.vocab, OM.ROTARY_MROPE, mirror=mirror,
                    cache_weights=cache_weights)
     D = None
     if w.draft is not None:
-        D = OM.Decoder(provider, "draft", w.draft, w.vocab, OM.ROTARY_FLAT, mirror=mirror,
+        D = OM.Decoder(provider, "draft", w.draft, w.vocab, draft_rotary, mirror=mirror,
                        cache_weights=cache_weights)
     return T, D
 

@@ -107,6 +107,9 @@ def test_benchmark_and_paper_configs_validate_on_host(name):
     (lambda c, s: setattr(c.target, "q_heads", 3), "q_heads"),
     (lambda c, s: setattr(c.target, "ffn", 680), "ffn"),
     (lambda c, s: setattr(c.draft, "hidden", 128), "draft"),
+    # an M-RoPE draft's sections are validated like the target's
+    (lambda c, s: (setattr(c, "flags", B.SPEC_FLAG_DRAFT_MROPE), c.draft.mrope_section.__setitem__(0, 9)),
+     "draft: mrope_section"),
     (lambda c, s: setattr(s[0], "pending_token", 1024), "pending_token"),
     (lambda c, s: setattr(s[0], "prefix_len", 0), "prefix_len"),
 ])
@@ -171,10 +174,19 @@ def test_calls_on_null_context():
     L = B.lib()
     assert L.draft_step(None, None) == 1
     assert L.draft_steps(None, 1, None) == 1
+    assert L.spec_attn_readout(None, 0, 0, None) == 1
     assert L.spec_verify(None, None, None) == 1
     assert L.spec_commit(None, None, None, None, None) == 1
     assert L.spec_sync(None, None) == 1
     L.spec_destroy(None)
+
+
+def test_flatrope_draft_ignores_its_sections():
+    w = W.get("C1")
+    cfg = _cfg(w)
+    seqs, keep = _seqs(w, cfg, blocks=_blocks(w))
+    cfg.draft.mrope_section[0] = 9
+    assert B.spec_workspace_bytes(cfg, seqs) > 0
 
 
 def test_page_tables_validated_on_host():

@@ -207,3 +207,21 @@ def test_iid_expected_L_by_enumeration():
         assert e == pytest.approx(report.iid_expected_L(p, K), rel=1e-12)
         assert e == pytest.approx((1 - p ** (K + 1)) / (1 - p), rel=1e-12)
     assert report.mean_accepted_length([3, 0, 8]) == pytest.approx(14 / 3)
+
+
+def test_mrope_draft_reduces_to_flatrope_on_text_and_differs_on_vision():
+    # An M-RoPE draft gives every text slot (i, i, i), whose rotation is the 1D
+    # one at i (Eq. rope-3d with equal axes), so on a prompt without vision
+    # blocks it proposes exactly what the FlatRoPE draft does; with a vision
+    # block the two see different key positions.
+    for blocks, same in (((), True), ((W.VisionBlock(0, 1, 5, 6),), False)):
+        w = _tiny(vocab=256).with_(seqs=(W.SeqLayout(48, blocks),))
+        hp = W.HostWeights(w)
+        outs = []
+        for rot in (M.ROTARY_FLAT, M.ROTARY_MROPE):
+            T, D = S.oracle_decoders(w, hp, draft_rotary=rot)
+            seq = S.oracle_sequence(w, 0, T, D)
+            d, z = seq.draft_step()
+            outs.append((d, z, seq.dc.k[0][:48].copy()))
+        assert np.allclose(outs[0][1], outs[1][1], rtol=1e-12, atol=1e-12) == same
+        assert np.allclose(outs[0][2], outs[1][2], rtol=1e-12, atol=1e-12) == same

@@ -21,7 +21,9 @@ class ModelShape:
 
     `mrope_section` is (s_T, s_H, s_W) in rotary pairs and must sum to
     head_dim/2 (Sec. 3.3, Eq. rope-3d).  `interleaved` selects the axis
-    assignment of Eq. axis-assign.  The draft ignores both (FlatRoPE, Sec. 4.2).
+    assignment of Eq. axis-assign.  The draft ignores both (FlatRoPE, Sec. 4.2)
+    unless it runs with M-RoPE as the comparison arm of the attention-budget
+    readout.
     """
     layers: int
     hidden: int
