@@ -199,6 +199,119 @@ def calibration_copy():
     log(f"calibration copy: {a.numel() * 2} bytes read, {b.numel() * 2} written")
 
 
+def copy_peak_gbs(reps=10):
+    """Bytes moved per second (read + write) by a plain 1 GiB device copy: the
+    streaming rate a kernel on this machine can reach in practice."""
+    import torch
+    a = torch.empty(1 << 29, dtype=torch.int16, device="cuda").fill_(1)
+    b = torch.empty_like(a)
+    for _ in range(3):
+        b.copy_(a)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    e0.record()
+    for _ in range(reps):
+        b.copy_(a)
+    e1.record()
+    torch.cuda.synchronize()
+    gbs = 2 * a.numel() * 2 * reps / (e0.elapsed_time(e1) * 1e-3) / 1e9
+    del a, b
+    torch.cuda.empty_cache()
+    return gbs
+
+
+def batched_scenes(src, K):
+    """The 16-scene workload end to end: 16 independent scenes (prompts of
+    2048..8192 tokens, four camera grids each, shuffled KV pages), each
+    emitting 20 tokens through draft K=8 -> verify -> commit rounds with the
+    scene's own draft match rate p in [0.5, 0.9], against greedy decoding
+    (K = 0) of the same scenes in the same run.  Every pass of the rounds
+    covers all 16 scenes (144 verify rows).  The first round of each loop
+    (graph capture) is not timed."""
+    import torch
+    import workloads as W
+    from paper_2606_31160_amd import binding as B
+    from paper_2606_31160_amd.harness import Session
+    w = W.get("C5")
+    nb, T = w.batch, w.max_new_tokens
+
+    # greedy decoding (K = 0): the AR rate
+    ar = Session(w, source="device", provider=src, K=0, with_draft=False, page_seed=5)
+    e = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+    for i in range(T):
+        if i == 1:
+            e[0].record()
+        B.spec_verify(ar.ctx, 0, 0)
+        B.spec_commit(ar.ctx, 0, 0, 0, 0)
+    e[1].record()
+    torch.cuda.synchronize()
+    ar_ms = e[0].elapsed_time(e[1])
+    assert all(ar.state(b)["n_gen"] == T for b in range(nb))
+    ar.close()
+    del ar
+
+    # the target's greedy continuation at the speculative passes' shape (144
+    # rows run on the batched GEMM, whose sums are grouped differently from
+    # the 16-row kernels of greedy decoding): rounds with random drafts commit
+    # only the target's own greedy tokens
+    rng = np.random.default_rng(11)
+    g = Session(w, source="device", provider=src, page_seed=5)
+    tr = [[] for _ in range(nb)]
+    while min(len(t) for t in tr) < T:
+        g.verify(rng.integers(0, w.vocab, size=(nb, K)).astype(np.int32))
+        g.commit()
+        coms, _, _ = g.committed()
+        for b in range(nb):
+            tr[b] += [int(t) for t in coms[b]]
+    g.close()
+    del g
+    tr = np.array([t[:T] for t in tr], dtype=np.int32)
+
+    # every round's drafts and commit counts, planned on the host
+    synth = [W.DraftSynth(w, b) for b in range(nb)]
+    pos = [0] * nb
+    plan, toks, active = [], [], []
+    while min(pos) < T:
+        d = np.zeros((nb, K), dtype=np.int32)
+        n = 0
+        active.append(sum(1 for b in range(nb) if pos[b] < T))
+        for b in range(nb):
+            if pos[b] >= T:
+                continue
+            d[b] = synth[b].propose(tr[b, pos[b]:], K)
+            c = min(lcp(d[b], tr[b, pos[b]:pos[b] + K]) + 1, T - pos[b])
+            pos[b] += c
+            n += c
+        plan.append(d)
+        toks.append(n)
+    drafts = torch.tensor(np.stack(plan), dtype=torch.int32, device="cuda")
+
+    s = Session(w, source="device", provider=src, page_seed=5)
+    e = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+    for r in range(len(plan)):
+        if r == 1:
+            e[0].record()
+        B.draft_steps(s.ctx, K, s.dtok.data_ptr())
+        B.spec_verify(s.ctx, drafts[r].data_ptr(), 0)
+        B.spec_commit(s.ctx, s.acc.data_ptr(), 0, s.ncom.data_ptr(), s.fin.data_ptr())
+    e[1].record()
+    torch.cuda.synchronize()
+    spec_ms = e[0].elapsed_time(e[1])
+    assert all(s.state(b)["n_gen"] == T and s.state(b)["finished"] for b in range(nb))
+    s.close()
+    del s
+    torch.cuda.empty_cache()
+    lens = [q.prefix_len for q in w.seqs]
+    return {"workload": "16 scenes x 20 tokens, prompts %d..%d (85%% vision, 4 cameras x (2,h,16) grids), "
+                        "K=8, p in [0.5, 0.9], paged KV (shuffled pages); 144-row verify passes" % (min(lens), max(lens)),
+            "tokens_per_s": round(sum(toks[1:]) / (spec_ms * 1e-3), 1),
+            "ar_tokens_per_s": round(nb * (T - 1) / (ar_ms * 1e-3), 1),
+            "rounds": len(plan),
+            "mean_accepted_L": round(nb * T / sum(active), 3),
+            "ms_per_round": round(spec_ms / (len(plan) - 1), 3),
+            "ar_ms_per_step": round(ar_ms / (T - 1), 3)}
+
+
 def pmc_pass(rounds, K):
     """Rounds of the timed workload, launched kernel by kernel, for counter
     collection; prints one line per round."""
@@ -228,6 +341,7 @@ def main():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-batched", action="store_true", help="skip the 16-scene side figure")
     ap.add_argument("--calibration-copy", action="store_true",
                     help="end with a plain 1 GiB device copy (reference for HBM byte counters)")
     ap.add_argument("--pmc-pass", type=int, default=0, metavar="R",
@@ -320,6 +434,7 @@ def main():
     total_ms = start.elapsed_time(stop)
     draft_ms = [e[0].elapsed_time(e[1]) for e in evs]
     verify_ms = [e[1].elapsed_time(e[2]) for e in evs]
+    round_ms = [e[0].elapsed_time(e[3]) for e in evs]
     st = s.state(0)
     expect = sum(commits[:args.warmup + args.steps])
     assert st["n_gen"] == expect, (st, expect)
@@ -399,6 +514,14 @@ def main():
                      "launches": dom["launches"], "avg_launch_us": dom["avg_us"],
                      "bytes_per_launch": dom["bytes_per_launch"]},
     }
+    out["verify_us_p10_p50_p90"] = [round(float(np.percentile(verify_ms, q)) * 1e3, 1) for q in (10, 50, 90)]
+    out["round_ms_p10_p50_p90"] = [round(float(np.percentile(round_ms, q)), 3) for q in (10, 50, 90)]
+    if not args.no_batched:
+        log("16-scene workload ...")
+        out["batched_16_scenes"] = batched_scenes(src, K)
+    cp = copy_peak_gbs()
+    out["copy_peak_gbs"] = round(cp, 1)
+    out["verify_frac_of_copy_peak"] = round(v_bytes / (v_us * 1e-6) / 1e9 / cp, 4)
     if not args.no_cpu_baseline:
         log("timing the oracle on a bounded sample ...")
         out["cpu_baseline"] = cpu_baseline(w, src, L, K)

@@ -81,9 +81,10 @@ typedef struct spec_dims {
 #define SPEC_FLAG_PASS_TIMELINE 4  /* the persistent pass kernel records per-phase wall-clock stamps
                                       (see spec_debug_pass_timeline); adds a small cost */
 #define SPEC_FLAG_ROWMAJOR 8       /* stream the caller's row-major weights directly.  Without it, passes
-                                      of at most 16 rows (batch*(K+1) <= 16) on the layered path stream a
-                                      tile-packed copy of every weight matrix that spec_init writes into
-                                      the workspace (its size is part of spec_workspace_bytes) */
+                                      on the layered path of at most 16 rows (batch*(K+1) <= 16), or of
+                                      rows the batched-row GEMM takes, stream a tile-packed copy of every
+                                      weight matrix that spec_init writes into the workspace (its size is
+                                      part of spec_workspace_bytes) */
 #define SPEC_FLAG_DRAFT_MROPE 16   /* the draft rotates with 3D M-RoPE (its own mrope_section and
                                       interleaved, validated as the target's) instead of FlatRoPE: the
                                       comparison arm of the attention-budget readout (Sec. 4.2) */

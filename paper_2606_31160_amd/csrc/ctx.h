@@ -67,6 +67,7 @@ struct Model {
   bf16_t* vt = nullptr;             // [layers][pool pages][kv_heads][head_dim][kAttnChunk], values transposed
   int8_t* axis = nullptr;           // [head_dim/2] axis (0 T, 1 H, 2 W) of each rotary pair
   int s_down = 1;                  // k-splits of the down projection
+  int s_o = 1;                     // k-splits of the o projection on the batched-row GEMM
   int pass_splits = 1;             // k-splits of the down projection in the persistent pass
   LayerW* lw_dev = nullptr;        // [layers] device copy of L (persistent pass)
   PassArgs* pass_args_dev = nullptr;   // device copy of this model's pass arguments
@@ -150,6 +151,7 @@ struct Ctx {
   enum Phase { READY = 0, DRAFTING = 1, VERIFIED = 2 } phase = READY;
   int dsteps = 0;
   bool gemm_rows = false;              // layered row-major passes run on the batched-row GEMM
+  bool gemm_pk = false;                // ... which streams the tile-packed weight copy
   bool poisoned = false;
   std::string err;
 
@@ -200,6 +202,8 @@ hipError_t launch_logits_out(Ctx& c, void* d_logits);
 // Packed-weight path: plans (and, with fill, points) every GEMV job of a model;
 // false if a shape does not fit.  Packs a model's weights / the LM head.
 bool sg_build_jobs(Ctx& c, Model& m, bool draft, bool fill);
+// Offsets of o, gate/up and down inside a layer of the tile-packed copy, and its elements per layer.
+void pk_offsets(Model& m);
 hipError_t sg_pack_model(Ctx& c, Model& m);
 hipError_t sg_pack_head(Ctx& c);
 

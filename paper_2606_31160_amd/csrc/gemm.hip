@@ -1,18 +1,30 @@
 // Batched-row GEMM on MFMA for passes of more than kThinRows rows (several
 // sequences verified together), and of 17..kThinRows rows whose width the
-// thin GEMV cannot stage (one sequence with K = 16 at hidden 4096): y[m][n] = sum_k x[m][k] W[n][k] for up to
-// SPEC_MAX_ROWS rows, with the same fused epilogues as the thin GEMV kernels
-// (1/rms row scale, rotary + paged KV append, residual + next-norm input,
-// SwiGLU, per-tile argmax, or k-split partial sums).
+// thin GEMV cannot stage (one sequence with K = 16 at hidden 4096): y[m][n] =
+// sum_k x[m][k] W[n][k] for up to SPEC_MAX_ROWS rows, with the same fused
+// epilogues as the thin GEMV kernels (1/rms row scale, rotary + paged KV
+// append, residual + next-norm input, SwiGLU, per-tile argmax, or k-split
+// partial sums).
 //
-// A workgroup of 4 waves owns 64 output columns (wave w: the 16-column tile
-// 4*blockIdx.x + w) and the k-range of split blockIdx.y.  The k-range is
-// walked in chunks of 64 columns (two 32-wide MFMA steps).  Every chunk's x
-// rows are staged once in LDS and shared by the 4 waves; each wave streams
-// its own 16 weight rows.  Loads run kStages chunks ahead: chunk c's x
-// vectors and weight fragments sit in registers while chunks c-1.. are
-// multiplied, then x goes to one of two LDS buffers.  Workgroup barriers wait
-// for LDS traffic only, never for the loads in flight.
+// A workgroup owns kGemmTiles = 4 output tiles of 16 columns and the k-range
+// of split blockIdx.y, walked in chunks of 32 * kSteps columns (kSteps
+// 32-wide MFMA steps; kSteps = 4 or 2 by the row count).  It has two kinds
+// of waves:
+//   * 2 * kSteps MFMA waves.  Wave w = 2q + p multiplies tile pair p (tiles
+//     2p, 2p+1) by step q of every chunk: each x operand it reads from LDS
+//     feeds two MFMAs, and the step groups split the k-range (their partial
+//     tiles are summed through LDS at the end).  They stream only weights,
+//     kStages chunks ahead.
+//   * 4 loader waves.  They stage every chunk's x rows (all rows) into one of
+//     two LDS buffers, loading kStages chunks ahead.
+// Loads complete in issue order per wave, so a wave that waited for x would
+// also wait for every weight load issued before it; with x in waves of its
+// own, the weight loads stay kStages chunks deep.  One workgroup barrier per
+// chunk hands a staged buffer to the MFMA waves; barriers wait for LDS
+// traffic only, never for loads in flight.  Both loops run a whole number of
+// kStages-chunk rounds with no early exit (chunks past the k-range load
+// nothing and add zeros): an exit inside the unrolled round would make the
+// compiler drain every load in flight at the loop head.
 //
 // v_mfma_f32_16x16x32_bf16 takes the weight fragment as A (lane l: row l&15,
 // k 8*(l>>4)..+8) and x^T as B (lane l: x row l&15, same k); lane l then
@@ -31,50 +43,100 @@ namespace specdec {
 
 namespace {
 
-constexpr int kChunk = 64;                    // k columns per stage
-constexpr int kStages = 3;                    // chunks of loads in flight
-constexpr int kXStride = kChunk + 8;          // bf16 per LDS x row (16-byte pad against bank conflicts)
-constexpr int kYStride = 17;                  // floats per row of a wave's output tile in LDS
+constexpr int kLoadWaves = 4;                 // waves that stage x
+constexpr int kOut = 0x7FFFFF00;              // buffer offset past every operand: the load returns zeros
+constexpr int kRsrcWord3 = 0x00020000;        // raw buffer resource, 32-bit data
+constexpr int kNt = 2;                        // non-temporal hint of the weight loads
+constexpr int NL = kLoadWaves * 64;           // loader threads
+constexpr int kYStride = 17;                  // floats per row of an output tile in LDS
 
-size_t x_lds_bytes(int rows) { return (size_t)2 * rows * kXStride * sizeof(bf16_t); }
-size_t y_lds_bytes(int rows) { return (size_t)kGemmWaves * rows * kYStride * sizeof(float); }
+// Step groups (32-wide k-steps per chunk, one MFMA wave pair each) and chunks
+// of loads in flight, by 16-row blocks: up to 5 blocks 4 groups and 5
+// chunks (12 waves, 168 registers each); from 6 blocks, whose accumulators
+// need more registers, 2 groups (8 waves, 256 registers each) and 8 chunks.
+// The compiler waits for all of a wave's loads once per round of kStages
+// chunks, so a deep round is what keeps enough bytes in flight per CU.
+constexpr int steps_for(int mb) { return mb >= 6 ? 2 : 4; }
+constexpr int stages_for(int mb) { return mb >= 6 ? 8 : 5; }
+constexpr int threads_for(int mb) { return (2 * steps_for(mb) + kLoadWaves) * 64; }
+constexpr int xstride_for(int mb) { return 32 * steps_for(mb) + 8; }   // bf16 per LDS x row (16-byte pad)
+static_assert(kGemmTiles == 4, "MFMA wave w = 2q + p: tile pair p, step group q");
+
+// two x buffers of 16 mb rows plus a spare row each (the target of loader
+// stores past the last row, so that no branch skips a store)
+size_t x_lds_bytes(int mb) { return (size_t)2 * (16 * mb + 1) * xstride_for(mb) * sizeof(bf16_t); }
+// output tiles, plus (4 step groups) the partial tiles of groups 2 and 3 while they are summed
+size_t y_lds_bytes(int mb) {
+  return (size_t)(steps_for(mb) == 4 ? 2 : 1) * kGemmTiles * (16 * mb) * kYStride * sizeof(float);
+}
 
 template <int MB, int EPI>
-__global__ __launch_bounds__(kGemmWaves * 64) void k_gemm(GemvArgs a) {
+__global__ __launch_bounds__(threads_for(MB)) void k_gemm(GemvArgs a) {
   constexpr int ROWS = MB * 16;
-  constexpr int XV = (ROWS * (kChunk / 8) + kGemmWaves * 64 - 1) / (kGemmWaves * 64);   // x vectors per thread
+  constexpr int kSteps = steps_for(MB), kStages = stages_for(MB), NT = threads_for(MB);
+  constexpr int kMfmaWaves = 2 * kSteps;
+  constexpr int kChunk = 32 * kSteps;                         // k columns per stage
+  constexpr int kXStride = xstride_for(MB);
+  constexpr int CV = kChunk / 8;                              // x vectors per row and chunk
+  constexpr int XV = (ROWS * CV + NL - 1) / NL;               // x vectors per loader thread and chunk
   constexpr bool kNorm = EPI == EPI_ROPE || EPI == EPI_SWIGLU || EPI == EPI_ARGMAX;
-  constexpr int NT = kGemmWaves * 64;
   extern __shared__ __align__(16) unsigned char lds[];
   __shared__ float inv_rms[ROWS];
   __shared__ int live_s[ROWS];
+  __shared__ float rms_part[kNorm ? NT : 1];
 
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const bool loader = wave >= kMfmaWaves;                    // wave-uniform role
+  const int pair = wave & 1, q = (wave >> 1) & (kSteps - 1);
+  const int lt = threadIdx.x - kMfmaWaves * 64;               // loader thread index
   const int split = blockIdx.y;
   const int Kd = a.Kd, M = a.M, N = a.N;
   const int T = (Kd + 31) >> 5;
   const int s0 = (int)((long long)split * T / a.splits);
   const int s1 = (int)((long long)(split + 1) * T / a.splits);
-  const int nch = (s1 - s0 + 1) >> 1;
+  const int nch = (s1 - s0 + kSteps - 1) / kSteps;
   const int kq = 8 * (lane >> 4);
-  const int n0 = (blockIdx.x * kGemmWaves + wave) * kTile;   // this wave's output columns
-  const bool wtile = n0 < N;
+  const int kend = min(s1 * 32, Kd);
 
-  // this lane's weight row
-  const bf16_t* wp = a.w[0];
-  if (wtile) {
+  // Weights are read through buffer resources, x through one over its rows:
+  // every load is issued unconditionally, and one that a lane does not need
+  // (past the split, a dead row, a tile past N) gets offset kOut and returns
+  // zeros without a memory access.  With no branch around a load, the
+  // compiler's wait counts stay exact and loads stay kStages chunks deep.
+  //
+  // MFMA waves, tile t of the pair: on the tile-packed copy, block (tile,
+  // step) is 1 KB at (tile * T + step) * 1 KB with lane l at 16 l; on
+  // row-major weights, lane l reads row l & 15 of the tile.  SwiGLU tiles
+  // come in pairs on both (tile 2c: gate rows 16c..16c+16, tile 2c+1: the up
+  // rows of the same features), so every tile is one load per step.
+  const bool packed = a.pw != nullptr;
+  __amdgpu_buffer_rsrc_t rw[2];
+  int wbase[2];          // byte offset of this lane's fragment at step 0 (kOut: tile unused)
+#pragma unroll
+  for (int t = 0; t < 2; ++t) {
+    const int tile = blockIdx.x * kGemmTiles + 2 * pair + t;
+    const int n0 = tile * kTile;
+    const bool on = !loader && n0 < N;
     const int r = lane & 15;
-    if constexpr (EPI == EPI_SWIGLU) {
-      // half-tile: rows 0-7 are gate rows n0/2 .. +8, rows 8-15 the matching up rows
-      wp = r < 8 ? a.w[0] + (size_t)(n0 / 2 + r) * Kd : a.w[1] + (size_t)(n0 / 2 + r - 8) * Kd;
+    if (packed) {
+      rw[t] = __builtin_amdgcn_make_buffer_rsrc(const_cast<bf16_t*>(a.pw), 0, (N / kTile) * T * 1024, kRsrcWord3);
+      wbase[t] = on ? tile * T * 1024 + 16 * lane : kOut;
+    } else if constexpr (EPI == EPI_SWIGLU) {
+      const int F = N / 2;
+      rw[t] = __builtin_amdgcn_make_buffer_rsrc(const_cast<bf16_t*>(a.w[tile & 1]), 0, F * Kd * 2, kRsrcWord3);
+      wbase[t] = on ? (((tile >> 1) * kTile + r) * Kd + kq) * 2 : kOut;
     } else {
       int sg = 0;
 #pragma unroll
       for (int i = 1; i < 3; ++i)
         if (i < a.nseg && n0 >= a.row0[i]) sg = i;
-      wp = a.w[sg] + (size_t)(n0 - a.row0[sg] + r) * Kd;
+      const int rows = (sg + 1 < a.nseg ? a.row0[sg + 1] : N) - a.row0[sg];
+      rw[t] = __builtin_amdgcn_make_buffer_rsrc(const_cast<bf16_t*>(a.w[sg]), 0, rows * Kd * 2, kRsrcWord3);
+      wbase[t] = on ? ((n0 - a.row0[sg] + r) * Kd + kq) * 2 : kOut;
     }
   }
+  const __amdgpu_buffer_rsrc_t rx =
+      __builtin_amdgcn_make_buffer_rsrc(const_cast<bf16_t*>(a.x), 0, M * a.ldx * 2, kRsrcWord3);
 
   // live rows: row m is row m % rps of sequence m / rps, live while below
   // that sequence's row count
@@ -88,98 +150,170 @@ __global__ __launch_bounds__(kGemmWaves * 64) void k_gemm(GemvArgs a) {
   }
   __syncthreads();
 
-  // stage c: x vector v (v < ROWS*8) is row v >> 3, columns 8*(v & 7) .. +8 of
-  // the chunk; dead rows, columns past the split or past Kd read as zeros
-  auto issue = [&](int c, u32x4 (&xr)[XV], u32x4 (&wr)[2]) {
-    const int kc = (s0 + 2 * c) * 32;
-    const int kend = min(s1 * 32, Kd);
+  // 1/rms of each live row from the per-16-column sums of squares, at the
+  // start.  ss_in is [H/16][mpad]: for one column group the rows are
+  // contiguous, so thread (part p, row m) sums groups p*per .. (p+1)*per - 1
+  // of row m with loads that are coalesced across the rows, all issued before
+  // the first add (one memory round trip per workgroup); the parts are then
+  // added in order.  inv_rms is read after the K loop's barriers.
+  if constexpr (kNorm) {
+    constexpr int P = NT / ROWS;              // parts per row (>= 3)
+    constexpr int LPT = 96;                   // loads per thread (H/16 <= LPT * P, checked on the host)
+    const int nt = a.H / kTile, per = (nt + P - 1) / P;
+    const int m = threadIdx.x % ROWS, p = threadIdx.x / ROWS;
+    float v[LPT];
+#pragma unroll
+    for (int j = 0; j < LPT; ++j) v[j] = a.ss_in[(size_t)min(p * per + j, nt - 1) * a.mpad + m];
+    float sum = 0.f;
+#pragma unroll
+    for (int j = 0; j < LPT; ++j) sum += (p < P && j < per && p * per + j < nt) ? v[j] : 0.f;
+    rms_part[threadIdx.x] = sum;
+    __syncthreads();
+    if (threadIdx.x < ROWS) {
+      float t = 0.f;
+      for (int q2 = 0; q2 < P; ++q2) t += rms_part[q2 * ROWS + threadIdx.x];
+      inv_rms[threadIdx.x] = live_s[threadIdx.x] ? rsqrtf(t / a.H + a.eps) : 0.f;
+    }
+  }
+
+  // Loader waves, chunk c: x vector v (v < ROWS*CV) is row v / CV, columns
+  // 8*(v % CV) .. +8 of the chunk.  MFMA waves, chunk c: step q of the chunk
+  // for both tiles.  Dead rows, columns past the split or past Kd read as
+  // zeros (Kd % 8 == 0, so a vector starting below the end lies inside).
+  auto issue_x = [&](int c, u32x4 (&xr)[XV]) {
+    const int kc = (s0 + kSteps * c) * 32;
 #pragma unroll
     for (int i = 0; i < XV; ++i) {
-      const int v = threadIdx.x + NT * i;
-      const int m = v >> 3, k = kc + 8 * (v & 7);
-      const bool ok = v < ROWS * 8 && m < M && live_s[m] && k < kend;
-      xr[i] = ok ? ld16(a.x + (size_t)m * a.ldx + k) : u32x4{0, 0, 0, 0};
-    }
-#pragma unroll
-    for (int st = 0; st < 2; ++st) {
-      const int k = kc + 32 * st + kq;
-      wr[st] = (wtile && k < kend) ? ld16_nt(wp + k) : u32x4{0, 0, 0, 0};
+      const int v = lt + NL * i;
+      const int m = v / CV, k = kc + 8 * (v % CV);
+      const int mm = m < ROWS ? m : ROWS - 1;   // (no branch around the LDS read)
+      const bool ok = (v < ROWS * CV) & (m < M) & (live_s[mm] != 0) & (k < kend);
+      xr[i] = __builtin_amdgcn_raw_buffer_load_b128(rx, ok ? (m * a.ldx + k) * 2 : kOut, 0, 0);
     }
   };
-
-  u32x4 xr[kStages][XV];
-  u32x4 wr[kStages][2];
+  auto issue_w = [&](int c, u32x4 (&wr)[2]) {
+    const int st = s0 + kSteps * c + q;
+    const bool ok = packed ? st < s1 : st * 32 + kq < kend;
+    const int step_bytes = packed ? 1024 : 64;
 #pragma unroll
-  for (int u = 0; u < kStages; ++u)
-    if (u < nch) issue(u, xr[u], wr[u]);
+    for (int t = 0; t < 2; ++t)
+      wr[t] = __builtin_amdgcn_raw_buffer_load_b128(rw[t], (ok && wbase[t] != kOut) ? wbase[t] + st * step_bytes : kOut,
+                                                    0, kNt);
+  };
 
-  f32x4 acc[MB];
-#pragma unroll
-  for (int mb = 0; mb < MB; ++mb) acc[mb] = f32x4{0.f, 0.f, 0.f, 0.f};
   bf16_t* xs = reinterpret_cast<bf16_t*>(lds);
-
-  for (int c0 = 0; c0 < nch; c0 += kStages) {   // workgroup-uniform
+  float* y = reinterpret_cast<float*>(lds);   // output tiles once the x buffers are free
+  // Both roles pass the same barriers: one per chunk, then the sums' (five
+  // with four step groups, three with two).
+  if (loader) {
+    u32x4 xr[kStages][XV];
 #pragma unroll
-    for (int u = 0; u < kStages; ++u) {
-      const int c = c0 + u;
-      if (c >= nch) break;
-      bf16_t* xb = xs + (size_t)(c & 1) * ROWS * kXStride;
+    for (int u = 0; u < kStages; ++u) issue_x(u, xr[u]);
+    for (int c0 = 0; c0 < nch; c0 += kStages) {   // workgroup-uniform
 #pragma unroll
-      for (int i = 0; i < XV; ++i) {
-        const int v = threadIdx.x + NT * i;
-        if (v < ROWS * 8) *reinterpret_cast<u32x4*>(xb + (v >> 3) * kXStride + 8 * (v & 7)) = xr[u][i];
-      }
-      // LDS stores visible to all waves; buffer c&1 was last read in chunk
-      // c-2, before every wave passed chunk c-1's barrier
-      __syncthreads();
-      const u32x4 w0 = wr[u][0], w1 = wr[u][1];
-      if (c + kStages < nch) issue(c + kStages, xr[u], wr[u]);
+      for (int u = 0; u < kStages; ++u) {
+        const int c = c0 + u;   // chunks past the last one load nothing and stage zeros
+        // buffer c&1 was last read in chunk c-2, before every wave passed
+        // chunk c-1's barrier
+        bf16_t* xb = xs + (size_t)(c & 1) * (ROWS + 1) * kXStride;
 #pragma unroll
-      for (int mb = 0; mb < MB; ++mb) {
-        const bf16_t* xp = xb + (mb * 16 + (lane & 15)) * kXStride + kq;
-        acc[mb] = mfma16x16x32(w0, *reinterpret_cast<const u32x4*>(xp), acc[mb]);
-        acc[mb] = mfma16x16x32(w1, *reinterpret_cast<const u32x4*>(xp + 32), acc[mb]);
+        for (int i = 0; i < XV; ++i) {
+          const int v = lt + NL * i;
+          const int row = v < ROWS * CV ? v / CV : ROWS;
+          *reinterpret_cast<u32x4*>(xb + row * kXStride + 8 * (v % CV)) = xr[u][i];
+        }
+        issue_x(c + kStages, xr[u]);   // past the last chunk: zeros, no memory access
+        __syncthreads();   // chunk c's x rows are visible to every wave
       }
     }
-  }
-
-  // 1/rms of each live row from the per-16-column sums of squares (fixed order)
-  if constexpr (kNorm) {
-    for (int m = wave; m < ROWS; m += kGemmWaves) {
-      float v = 0.f;
-      if (live_s[m])
-        for (int t = lane; t < a.H / kTile; t += 64) v += a.ss_in[(size_t)t * a.mpad + m];
-      for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
-      if (lane == 0) inv_rms[m] = live_s[m] ? rsqrtf(v / a.H + a.eps) : 0.f;
-    }
-  }
-  __syncthreads();   // x buffers are free; inv_rms is complete
-
-  // wave tiles -> LDS: yw[wave][m][c]
-  float* y = reinterpret_cast<float*>(lds);
-  {
-    float* yw = y + (size_t)wave * ROWS * kYStride;
+    for (int i = 0; i < (kSteps == 4 ? 5 : 3); ++i) __syncthreads();
+  } else {
+    u32x4 wr[kStages][2];
 #pragma unroll
-    for (int mb = 0; mb < MB; ++mb) {
+    for (int u = 0; u < kStages; ++u) issue_w(u, wr[u]);
+    f32x4 acc[2][MB];
+#pragma unroll
+    for (int t = 0; t < 2; ++t)
+#pragma unroll
+      for (int mb = 0; mb < MB; ++mb) acc[t][mb] = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int c0 = 0; c0 < nch; c0 += kStages) {   // workgroup-uniform
+#pragma unroll
+      for (int u = 0; u < kStages; ++u) {
+        const int c = c0 + u;   // chunks past the last one multiply zeros
+        const bf16_t* xb = xs + (size_t)(c & 1) * (ROWS + 1) * kXStride;
+        __syncthreads();   // chunk c's x rows are visible to every wave
+        const u32x4 w0 = wr[u][0], w1 = wr[u][1];
+        issue_w(c + kStages, wr[u]);   // past the last chunk: zeros, no memory access
+#pragma unroll
+        for (int mb = 0; mb < MB; ++mb) {
+          const u32x4 xv = *reinterpret_cast<const u32x4*>(xb + (mb * 16 + (lane & 15)) * kXStride + 32 * q + kq);
+          acc[0][mb] = mfma16x16x32(w0, xv, acc[0][mb]);
+          acc[1][mb] = mfma16x16x32(w1, xv, acc[1][mb]);
+        }
+      }
+    }
+    __syncthreads();   // 1: x buffers are free
+
+    // Sum the step groups' partial tiles in a fixed order, ((q0 + q2) + (q1 + q3))
+    // with four groups (2 and 3 store, 0 and 1 add; 1 stores, 0 adds) or
+    // q0 + q1 with two; group 0 scales by 1/rms and leaves the result in
+    // y[tile][m][c].
+    auto tile_at = [&](float* base, int t, int mb, int i) -> float& {
       const int m = mb * 16 + (lane & 15);
-      const float sc = kNorm ? inv_rms[m] : 1.f;
+      return base[((2 * pair + t) * ROWS + m) * kYStride + 4 * (lane >> 4) + i];
+    };
+    auto store = [&](float* dst) {
 #pragma unroll
-      for (int i = 0; i < 4; ++i) yw[m * kYStride + 4 * (lane >> 4) + i] = acc[mb][i] * sc;
+      for (int t = 0; t < 2; ++t)
+#pragma unroll
+        for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+          for (int i = 0; i < 4; ++i) tile_at(dst, t, mb, i) = acc[t][mb][i];
+    };
+    if constexpr (kSteps == 4) {
+      float* yp = y + (size_t)kGemmTiles * ROWS * kYStride;   // the upper partial tiles
+      if (q >= 2) store(q == 2 ? y : yp);
+      __syncthreads();   // 2
+      if (q < 2) {
+        float* src = q == 0 ? y : yp;
+#pragma unroll
+        for (int t = 0; t < 2; ++t)
+#pragma unroll
+          for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) acc[t][mb][i] += tile_at(src, t, mb, i);
+      }
+      __syncthreads();   // 3
     }
+    if (q == 1) store(y);
+    __syncthreads();   // 4 (two groups: 2)
+    if (q == 0) {
+#pragma unroll
+      for (int t = 0; t < 2; ++t)
+#pragma unroll
+        for (int mb = 0; mb < MB; ++mb) {
+          const float sc = kNorm ? inv_rms[mb * 16 + (lane & 15)] : 1.f;
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            float& d = tile_at(y, t, mb, i);
+            d = (acc[t][mb][i] + d) * sc;
+          }
+        }
+    }
+    __syncthreads();   // 5 (two groups: 3)
   }
-  __syncthreads();
 
-  // epilogues: items of (wave tile w, row m, column or pair)
+  // epilogues: items of (tile w, row m, column or pair)
   if constexpr (EPI == EPI_STORE) {
-    for (int idx = threadIdx.x; idx < kGemmWaves * ROWS * 16; idx += NT) {
+    for (int idx = threadIdx.x; idx < kGemmTiles * ROWS * 16; idx += NT) {
       const int w = idx / (ROWS * 16), r = idx % (ROWS * 16), m = r >> 4, cc = r & 15;
-      const int nw = (blockIdx.x * kGemmWaves + w) * kTile;
+      const int nw = (blockIdx.x * kGemmTiles + w) * kTile;
       if (nw < N && m < M) a.out[((size_t)split * M + m) * N + nw + cc] = y[(w * ROWS + m) * kYStride + cc];
     }
   } else if constexpr (EPI == EPI_ROPE) {
-    for (int idx = threadIdx.x; idx < kGemmWaves * ROWS * 8; idx += NT) {
+    for (int idx = threadIdx.x; idx < kGemmTiles * ROWS * 8; idx += NT) {
       const int w = idx / (ROWS * 8), r = idx % (ROWS * 8), m = r >> 3, pr = r & 7;
-      const int nw = (blockIdx.x * kGemmWaves + w) * kTile;
+      const int nw = (blockIdx.x * kGemmTiles + w) * kTile;
       if (nw >= N || m >= M || !live_s[m]) continue;
       const int b = m / a.rps, j = m - b * a.rps;
       const int slot = a.st[b].base + j;
@@ -205,9 +339,9 @@ __global__ __launch_bounds__(kGemmWaves * 64) void k_gemm(GemvArgs a) {
   } else if constexpr (EPI == EPI_RESID) {
     // 16 consecutive threads share (w, m): the row's sum of squares over the
     // tile is a 16-lane reduction
-    for (int idx = threadIdx.x; idx < kGemmWaves * ROWS * 16; idx += NT) {
+    for (int idx = threadIdx.x; idx < kGemmTiles * ROWS * 16; idx += NT) {
       const int w = idx / (ROWS * 16), r = idx % (ROWS * 16), m = r >> 4, cc = r & 15;
-      const int nw = (blockIdx.x * kGemmWaves + w) * kTile;
+      const int nw = (blockIdx.x * kGemmTiles + w) * kTile;
       const bool ok = nw < N && m < M;
       float xn = 0.f;
       if (ok) {
@@ -224,28 +358,28 @@ __global__ __launch_bounds__(kGemmWaves * 64) void k_gemm(GemvArgs a) {
       if (ok && cc == 0) a.ss_out[(size_t)(nw / kTile) * a.mpad + m] = sq;
     }
   } else if constexpr (EPI == EPI_SWIGLU) {
-    // columns 0-7 gate, 8-15 up of output features nw/2 .. nw/2 + 8
+    // tiles 2j, 2j+1: gate and up rows of features 16 j' .. +16, j' = 2 blockIdx.x + j
     const int F = N / 2;
-    for (int idx = threadIdx.x; idx < kGemmWaves * ROWS * 8; idx += NT) {
-      const int w = idx / (ROWS * 8), r = idx % (ROWS * 8), m = r >> 3, cc = r & 7;
-      const int nw = (blockIdx.x * kGemmWaves + w) * kTile;
-      if (nw >= N || m >= M) continue;
-      const float g = y[(w * ROWS + m) * kYStride + cc];
-      const float up = y[(w * ROWS + m) * kYStride + 8 + cc];
-      a.u[(size_t)m * F + nw / 2 + cc] = f2bf(g / (1.f + expf(-g)) * up);
+    for (int idx = threadIdx.x; idx < 2 * ROWS * 16; idx += NT) {
+      const int j = idx / (ROWS * 16), r = idx % (ROWS * 16), m = r >> 4, cc = r & 15;
+      const int f = (2 * blockIdx.x + j) * kTile + cc;
+      if (f >= F || m >= M) continue;
+      const float g = y[(2 * j * ROWS + m) * kYStride + cc];
+      const float up = y[((2 * j + 1) * ROWS + m) * kYStride + cc];
+      a.u[(size_t)m * F + f] = f2bf(g / (1.f + expf(-g)) * up);
     }
   } else {   // EPI_ARGMAX
     if (a.allow_logits) {
-      for (int idx = threadIdx.x; idx < kGemmWaves * ROWS * 16; idx += NT) {
+      for (int idx = threadIdx.x; idx < kGemmTiles * ROWS * 16; idx += NT) {
         const int w = idx / (ROWS * 16), r = idx % (ROWS * 16), m = r >> 4, cc = r & 15;
-        const int nw = (blockIdx.x * kGemmWaves + w) * kTile;
+        const int nw = (blockIdx.x * kGemmTiles + w) * kTile;
         if (nw < N && m < M && a.st[m / a.rps].want_logits)
           a.logits[(size_t)m * N + nw + cc] = f2bf(y[(w * ROWS + m) * kYStride + cc]);
       }
     }
-    for (int idx = threadIdx.x; idx < kGemmWaves * ROWS; idx += NT) {
+    for (int idx = threadIdx.x; idx < kGemmTiles * ROWS; idx += NT) {
       const int w = idx / ROWS, m = idx % ROWS;
-      const int nw = (blockIdx.x * kGemmWaves + w) * kTile;
+      const int nw = (blockIdx.x * kGemmTiles + w) * kTile;
       if (nw >= N || m >= M) continue;
       float best = -INFINITY;
       int bi = nw;
@@ -271,7 +405,7 @@ __global__ __launch_bounds__(kGemmWaves * 64) void k_gemm(GemvArgs a) {
 template <int EPI>
 hipError_t launch_mb(const GemvArgs& g, hipStream_t s, hipEvent_t e0, hipEvent_t e1) {
   const int mb = (g.M + 15) / 16;
-  const dim3 grid((g.N + kGemmWaves * kTile - 1) / (kGemmWaves * kTile), g.splits), block(kGemmWaves * 64);
+  const dim3 grid((g.N + kGemmTiles * kTile - 1) / (kGemmTiles * kTile), g.splits), block(threads_for(mb));
   const size_t lds = gemm_lds_bytes(g.M);
   switch (mb) {
     case 2: hipExtLaunchKernelGGL((k_gemm<2, EPI>), grid, block, lds, s, e0, e1, 0, g); break;
@@ -288,17 +422,50 @@ hipError_t launch_mb(const GemvArgs& g, hipStream_t s, hipEvent_t e0, hipEvent_t
   return hipGetLastError();
 }
 
+template <int MB>
+void set_mb_attributes(int limit) {
+  const int lds = (int)std::max(x_lds_bytes(MB), y_lds_bytes(MB));
+  if (lds > limit) return;   // such a launch is rejected by the host-side LDS check
+  const void* f[5] = {reinterpret_cast<const void*>(&k_gemm<MB, EPI_STORE>),
+                      reinterpret_cast<const void*>(&k_gemm<MB, EPI_ROPE>),
+                      reinterpret_cast<const void*>(&k_gemm<MB, EPI_RESID>),
+                      reinterpret_cast<const void*>(&k_gemm<MB, EPI_SWIGLU>),
+                      reinterpret_cast<const void*>(&k_gemm<MB, EPI_ARGMAX>)};
+  for (const void* p : f) (void)hipFuncSetAttribute(p, hipFuncAttributeMaxDynamicSharedMemorySize, lds);
+}
+
 }  // namespace
 
 size_t gemm_lds_bytes(int M) {
-  const int rows = 16 * ((M + 15) / 16);
-  return std::max(x_lds_bytes(rows), y_lds_bytes(rows));
+  const int mb = (M + 15) / 16;
+  return std::max(x_lds_bytes(mb), y_lds_bytes(mb));
+}
+
+void gemm_set_attributes(int limit) {
+  set_mb_attributes<2>(limit);
+  set_mb_attributes<3>(limit);
+  set_mb_attributes<4>(limit);
+  set_mb_attributes<5>(limit);
+  set_mb_attributes<6>(limit);
+  set_mb_attributes<7>(limit);
+  set_mb_attributes<8>(limit);
+  set_mb_attributes<9>(limit);
+  set_mb_attributes<10>(limit);
 }
 
 hipError_t gemm_launch(int epi, const GemvArgs& g, hipStream_t s, hipEvent_t e0, hipEvent_t e1) {
   if (g.M <= kSgMaxRowsGemm || g.M > SPEC_MAX_ROWS || g.splits < 1 || (epi != EPI_STORE && g.splits != 1) ||
       g.N % kTile != 0 || g.Kd % 8 != 0)
     return hipErrorInvalidValue;
+  // the 1/rms prologue reads at most 96 sums of squares per thread, in
+  // threads_for / rows parts per row
+  {
+    const int mb = (g.M + 15) / 16, parts = threads_for(mb) / (16 * mb);
+    if ((epi == EPI_ROPE || epi == EPI_SWIGLU || epi == EPI_ARGMAX) && (g.H < kTile || g.H / kTile > 96 * parts))
+      return hipErrorInvalidValue;
+  }
+  // every operand is addressed with 32-bit byte offsets below kOut
+  if ((long long)g.N * ((g.Kd + 31) / 32) * 64 >= kOut || (long long)g.M * g.ldx * 2 >= kOut) return hipErrorInvalidValue;
   switch (epi) {
     case EPI_STORE: return launch_mb<EPI_STORE>(g, s, e0, e1);
     case EPI_ROPE: return launch_mb<EPI_ROPE>(g, s, e0, e1);
@@ -312,10 +479,10 @@ hipError_t gemm_launch(int epi, const GemvArgs& g, hipStream_t s, hipEvent_t e0,
 // k-splits of the down projection over M > kThinRows rows: enough
 // workgroups to cover every CU once, at least two chunks per split.
 int gemm_down_splits(int N, int Kd, int ncu) {
-  const int groups = (N + kGemmWaves * kTile - 1) / (kGemmWaves * kTile);
+  const int groups = (N + kGemmTiles * kTile - 1) / (kGemmTiles * kTile);
   const int T = (Kd + 31) / 32;
   int s = std::max(1, (ncu + groups - 1) / groups);
-  return std::max(1, std::min(s, T / (2 * 2)));
+  return std::max(1, std::min(s, T / 8));   // at least 8 k-steps per split
 }
 
 }  // namespace specdec

@@ -21,6 +21,8 @@ struct GemvArgs {
   const bf16_t* w[3];
   int row0[3];           // first output row of each weight segment (multiples of 16)
   int nseg;
+  const bf16_t* pw;      // GEMM only: the tile-packed copy of these weights ([N/16][steps] blocks of
+                         // 1 KB, sgemv.h; gate/up as gate, up tile pairs), or null to read w
   int N, Kd;
   const bf16_t* x;       // [M][ldx]
   int ldx, M, splits;
@@ -55,10 +57,12 @@ struct GemvArgs {
 // larger passes (up to SPEC_MAX_ROWS) the batched-row GEMM (gemm.hip).
 constexpr int kThinRows = 64;
 constexpr int kSgMaxRowsGemm = 16;   // the GEMM takes passes of more rows than one MFMA block
-constexpr int kGemmWaves = 4;   // waves per GEMM workgroup, one 16-column output tile each
+constexpr int kGemmTiles = 4;   // 16-column output tiles per GEMM workgroup
 
 // Dynamic LDS bytes of a GEMM launch over M rows.
 size_t gemm_lds_bytes(int M);
+// Raises the dynamic LDS limit of every GEMM instantiation that fits `limit` bytes.
+void gemm_set_attributes(int limit);
 // y = x W^T over g.M rows (kThinRows < M <= SPEC_MAX_ROWS) with epilogue
 // `epi`; grid (ceil(N / 64), g.splits).  Only EPI_STORE may use k-splits.
 hipError_t gemm_launch(int epi, const GemvArgs& g, hipStream_t s, hipEvent_t e0, hipEvent_t e1);

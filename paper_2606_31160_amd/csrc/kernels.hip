@@ -1305,6 +1305,8 @@ hipError_t run_layer(Ctx& c, Model& m, int li, const bf16_t* next_gain, bool sel
   const LayerW& w = m.L[li];
   bf16_t* kc = m.kc + m.kv_layer * li;
   bf16_t* vt = m.vt + m.kv_layer * li;
+  // the GEMM streams this layer's tile-packed copy when there is one
+  const bf16_t* pk = (c.gemm_rows && c.gemm_pk) ? m.pk + m.pk_layer * li : nullptr;
 
   // q, k, v (+ 1/rms of the attention norm) + rotary + cache append
   if (m.ljobs_dev && kQkvAsJob) {
@@ -1336,6 +1338,7 @@ hipError_t run_layer(Ctx& c, Model& m, int li, const bf16_t* next_gain, bool sel
     g.D = D;
     g.pt = c.pt;
     g.pps = c.pps;
+    g.pw = pk;
     if (c.gemm_rows)
       CK(gemm_run(c, EPI_ROPE, g, SPEC_KERNEL_QKV, gemv_bytes(g.N, H, M, 2.0)));
     else
@@ -1359,10 +1362,21 @@ hipError_t run_layer(Ctx& c, Model& m, int li, const bf16_t* next_gain, bool sel
     g.gain = w.ffn_norm;
     g.xg = c.xg;
     g.ss_out = c.ss;
-    if (c.gemm_rows)
-      CK(gemm_run(c, EPI_RESID, g, SPEC_KERNEL_O, gemv_bytes(H, nq * D, M, 10.0)));
-    else
+    g.pw = pk ? pk + m.pk_o : nullptr;
+    if (c.gemm_rows) {
+      // k-split partial sums, so that enough workgroups stream the narrow
+      // matrix; the finishing kernel adds them to the residual stream and
+      // writes the FFN norm's input, as after the down projection
+      g.splits = m.s_o;
+      g.out = c.part;
+      CK(gemm_run(c, EPI_STORE, g, SPEC_KERNEL_O, gemv_bytes(H, nq * D, M, 4.0 * m.s_o)));
+      FinishArgs p{c.st, c.part, m.s_o, M, c.R, H, c.Mpad, 0, c.x, w.ffn_norm, c.xg, c.ss};
+      Timed t(c, SPEC_KERNEL_OTHER, 0);
+      hipExtLaunchKernelGGL(k_down_finish, dim3((H + 255) / 256, M), dim3(256), 0, S(c), t.e0, t.e1, 0, p);
+      CK(hipGetLastError());
+    } else {
       CK((gemv_launch<EPI_RESID, 1>(c, g, SPEC_KERNEL_O, gemv_bytes(H, nq * D, M, 10.0))));
+    }
   }
   // gate/up (+ 1/rms of the FFN norm) + SwiGLU
   if (m.ljobs_dev) {
@@ -1383,6 +1397,7 @@ hipError_t run_layer(Ctx& c, Model& m, int li, const bf16_t* next_gain, bool sel
     g.H = H;
     g.eps = d.rms_eps;
     g.u = c.u;
+    g.pw = pk ? pk + m.pk_gu : nullptr;
     if (c.gemm_rows)
       CK(gemm_run(c, EPI_SWIGLU, g, SPEC_KERNEL_GATEUP, gemv_bytes(2 * F, H, M, 1.0)));
     else
@@ -1407,6 +1422,7 @@ hipError_t run_layer(Ctx& c, Model& m, int li, const bf16_t* next_gain, bool sel
       g.ldx = F;
       g.splits = m.s_down;
       g.out = c.part;
+      g.pw = pk ? pk + m.pk_dn : nullptr;
       if (c.gemm_rows) {
         CK(gemm_run(c, EPI_STORE, g, SPEC_KERNEL_DOWN, gemv_bytes(H, F, M, 4.0 * m.s_down)));
       } else {
@@ -1430,6 +1446,7 @@ void init_kernel_attributes() {
   done = true;
   pass_set_attributes(gemv_lds_limit());
   sg_set_attributes(gemv_lds_limit());
+  gemm_set_attributes(gemv_lds_limit());
   const void* attn[4] = {reinterpret_cast<const void*>(&k_attn<128, false>), reinterpret_cast<const void*>(&k_attn<128, true>),
                          reinterpret_cast<const void*>(&k_attn<64, false>), reinterpret_cast<const void*>(&k_attn<64, true>)};
   for (int i = 0; i < 4; ++i)
@@ -1558,16 +1575,22 @@ namespace {
 int steps_of(int Kd) { return (Kd + 31) / 32; }
 }  // namespace
 
+void pk_offsets(Model& m) {
+  const spec_dims& d = m.d;
+  const int H = d.hidden, D = d.head_dim, nq = d.q_heads, nkv = d.kv_heads, F = d.ffn;
+  const int nqkv = (nq + 2 * nkv) * D;
+  m.pk_o = sg_packed_elems(nqkv / kTile, steps_of(H));
+  m.pk_gu = m.pk_o + sg_packed_elems(H / kTile, steps_of(nq * D));
+  m.pk_dn = m.pk_gu + sg_packed_elems(2 * F / kTile, steps_of(H));
+  m.pk_layer = m.pk_dn + sg_packed_elems(H / kTile, steps_of(F));
+}
+
 bool sg_build_jobs(Ctx& c, Model& m, bool draft, bool fill) {
   const spec_dims& d = m.d;
   const int H = d.hidden, D = d.head_dim, nq = d.q_heads, nkv = d.kv_heads, F = d.ffn;
   const int ncu = c.ncu, lim = gemv_lds_limit();
   const int nqkv = (nq + 2 * nkv) * D;
-  // packed elements per layer and offsets of o, gate/up, down inside a layer
-  m.pk_o = sg_packed_elems(nqkv / kTile, steps_of(H));
-  m.pk_gu = m.pk_o + sg_packed_elems(H / kTile, steps_of(nq * D));
-  m.pk_dn = m.pk_gu + sg_packed_elems(2 * F / kTile, steps_of(H));
-  m.pk_layer = m.pk_dn + sg_packed_elems(H / kTile, steps_of(F));
+  pk_offsets(m);
   m.sg_host.assign((size_t)d.layers * 4 + 1, SgJob{});
   auto base = [&](SgJob& j, int ntiles, int Kd, const bf16_t* x) {
     j.ntiles = ntiles;
@@ -1846,8 +1869,10 @@ hipError_t launch_forward(Ctx& c, PassMode mode) {
     g.logits = c.logits;
     g.allow_logits = draft ? 0 : 1;
     const double bytes = gemv_bytes(c.V, d.hidden, g.M, 0.0) + 8.0 * (c.V / kTile) * g.M;
-    if (g.M > kThinRows || (!draft && c.gemm_rows))
+    if (g.M > kThinRows || (!draft && c.gemm_rows)) {
+      g.pw = c.gemm_pk ? c.pk_head : nullptr;
       CK(gemm_run(c, EPI_ARGMAX, g, SPEC_KERNEL_LMHEAD, bytes));
+    }
     else
       CK(gemv_launch_p<EPI_ARGMAX>(c, g, std::min(c.ncu, c.V / kTile), SPEC_KERNEL_LMHEAD, bytes));
   }

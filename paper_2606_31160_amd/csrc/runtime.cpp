@@ -256,6 +256,7 @@ Layout make_layout(const spec_config* cfg, const spec_seq_init* seqs) {
 
 void set_splits(Model& m, int M, bool gemm_rows) {
   m.s_down = gemm_rows ? gemm_down_splits(m.d.hidden, m.d.ffn, num_cus()) : down_splits(M, m.d.ffn, num_cus());
+  m.s_o = gemm_rows ? gemm_down_splits(m.d.hidden, m.d.q_heads * m.d.head_dim, num_cus()) : 1;
 }
 
 // Down-projection k-splits of the persistent pass for one model: the fewest
@@ -287,7 +288,7 @@ int pass_splits_for(const spec_dims& d, const Layout& L, int ncu) {
   return 0;
 }
 
-size_t part_elems_for(const Model& m, int M) { return (size_t)m.s_down * M * m.d.hidden; }
+size_t part_elems_for(const Model& m, int M) { return (size_t)std::max(m.s_down, m.s_o) * M * m.d.hidden; }
 
 // The q/k/v, o, gate/up and LM-head GEMVs keep a workgroup's whole reduction
 // (one k-split): their x rows for the full reduction length must fit in LDS,
@@ -487,6 +488,19 @@ size_t carve(Ctx& c, const spec_config* cfg, const spec_seq_init* seqs, bool has
     c.pk_head = cv.take<bf16_t>(sg_packed_elems(L.V / kTile, (H + 31) / 32));
     c.tgt.pk = cv.take<bf16_t>(c.tgt.pk_layer * t.layers);
     if (has_draft) {
+      c.drf.pk = cv.take<bf16_t>(c.drf.pk_layer * cfg->draft.layers);
+    }
+  }
+  // passes on the batched-row GEMM stream the same tile-packed copy: every
+  // wave load is then 1 KB of consecutive memory instead of 16 row pieces
+  c.gemm_pk = false;
+  if (!c.sg && c.gemm_rows && !(cfg->flags & SPEC_FLAG_ROWMAJOR) && !c.use_pass) {
+    c.gemm_pk = true;
+    pk_offsets(c.tgt);
+    c.pk_head = cv.take<bf16_t>(sg_packed_elems(L.V / kTile, (H + 31) / 32));
+    c.tgt.pk = cv.take<bf16_t>(c.tgt.pk_layer * t.layers);
+    if (has_draft) {
+      pk_offsets(c.drf);
       c.drf.pk = cv.take<bf16_t>(c.drf.pk_layer * cfg->draft.layers);
     }
   }
@@ -823,6 +837,11 @@ spec_status spec_init(const spec_config* cfg, const void* embed, const spec_mode
           (has_draft && (e = sg_pack_model(c, c.drf)) != hipSuccess))
         return hip_fail(e, "weight packing");
     }
+    if (c.gemm_pk) {
+      if ((e = sg_pack_head(c)) != hipSuccess || (e = sg_pack_model(c, c.tgt)) != hipSuccess ||
+          (has_draft && (e = sg_pack_model(c, c.drf)) != hipSuccess))
+        return hip_fail(e, "weight packing");
+    }
     if (c.tgt.ljobs_dev) {
       if ((e = upload_layered_jobs(c, c.tgt, false)) != hipSuccess ||
           (has_draft && (e = upload_layered_jobs(c, c.drf, true)) != hipSuccess))
@@ -1020,7 +1039,7 @@ spec_status spec_debug_state(spec_ctx* ctx, int32_t b, int32_t* host_out) {
 spec_status spec_debug_path(const spec_ctx* ctx, int32_t* path) {
   if (!ctx || !path) return SPEC_E_INVAL;
   const Ctx& c = ctx->c;
-  *path = c.use_pass ? SPEC_PATH_PERSISTENT : (c.sg ? SPEC_PATH_PACKED : SPEC_PATH_ROWMAJOR);
+  *path = c.use_pass ? SPEC_PATH_PERSISTENT : ((c.sg || c.gemm_pk) ? SPEC_PATH_PACKED : SPEC_PATH_ROWMAJOR);
   return SPEC_OK;
 }
 

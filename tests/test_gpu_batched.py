@@ -37,17 +37,17 @@ def _scenes(w, n, lo, hi, seed):
     return w.with_(seqs=seqs, p_accept=tuple([0.8] * n))
 
 
-def _verify_against_oracle(w, s, T, seed, check_kv=(0,)):
+def _verify_against_oracle(w, s, T, seed, check_kv=(0,), kv=None):
     """One verify of explicit drafts (the oracle's first greedy token, then
     random ids) for every sequence, with logits, against the oracle."""
     rng = np.random.default_rng(seed)
     seqs, drafts = [], np.zeros((w.batch, w.K), dtype=np.int32)
     for b in range(w.batch):
-        probe = S.oracle_sequence(w, b, T, None, with_draft=False)
+        probe = S.oracle_sequence(w, b, T, None, kv=kv, with_draft=False)
         d = rng.integers(0, w.vocab, size=w.K).astype(np.int32)
         d[:1] = OS.greedy_trace(probe, 1)
         drafts[b] = d
-        seqs.append(S.oracle_sequence(w, b, T, None, with_draft=False))
+        seqs.append(S.oracle_sequence(w, b, T, None, kv=kv, with_draft=False))
     s.verify(drafts, logits=True)
     s.commit()
     coms, acc, fin = s.committed()
@@ -113,10 +113,15 @@ def tiny16():
     return w, hp, T
 
 
-def test_sixteen_scenes_one_verify(tiny16):
+@pytest.mark.parametrize("path", ["packed", "rowmajor"])
+def test_sixteen_scenes_one_verify(tiny16, path):
+    # the GEMM streams the tile-packed weight copy by default, the caller's
+    # row-major weights with SPEC_FLAG_ROWMAJOR
+    from paper_2606_31160_amd import binding as B
     w, hp, T = tiny16
     assert w.batch * (w.K + 1) == 80
-    s = _session(w, page_seed=11)
+    s = _session(w, page_seed=11, flags=S.PATH_FLAGS[path])
+    assert B.spec_debug_path(s.ctx) == path
     _verify_against_oracle(w, s, T, seed=5, check_kv=(0, 9, 15))
     s.close()
 
@@ -145,12 +150,13 @@ def test_block_of_16_eight_scenes():
     _check_history(w, T, outs)
 
 
-def test_sixteen_scenes_7b_width_one_layer():
+@pytest.mark.parametrize("path", ["packed", "rowmajor"])
+def test_sixteen_scenes_7b_width_one_layer(path):
     c5 = W.get("C5")
     w = W.get("C2").with_(seqs=c5.seqs, p_accept=c5.p_accept, draft=None)
     assert w.batch * (w.K + 1) == 144 and w.target.hidden == 3584
-    hp = W.HostWeights(w)
-    T, _ = S.oracle_decoders(w, hp, cache_weights=True)
-    s = _session(w, provider=hp, page_seed=14)
-    _verify_against_oracle(w, s, T, seed=7, check_kv=(0, 15))
+    src = W.DeviceWeights(w)
+    T, _ = S.oracle_decoders(w, src, cache_weights=True)
+    s = _session(w, source="device", provider=src, page_seed=14, flags=S.PATH_FLAGS[path])
+    _verify_against_oracle(w, s, T, seed=7, check_kv=(0, 15), kv=S.device_kv)
     s.close()
