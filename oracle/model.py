@@ -48,10 +48,11 @@ def softmax(s: np.ndarray) -> np.ndarray:
 
 
 def attend(q: np.ndarray, kc: np.ndarray, vc: np.ndarray, slots: Sequence[int]) -> np.ndarray:
-    """Causal grouped-query attention.
+    """Grouped-query attention over a cache prefix.
 
     q [M, n_q, D] (rotated), kc/vc [cap, n_kv, D] (keys rotated); row i sees
-    cache slots 0..slots[i].  Returns [M, n_q, D].
+    cache slots 0..slots[i] (its own slot for causal attention, a later one for
+    the rows of a block that see each other).  Returns [M, n_q, D].
     """
     M, nq, D = q.shape
     nkv = kc.shape[1]
@@ -165,13 +166,16 @@ class Decoder:
 
     # -- forward -----------------------------------------------------------
     def forward(self, tokens: Sequence[int], slots: Sequence[int], cache: KVCache,
-                want_hidden: bool = False):
+                want_hidden: bool = False, visible: Optional[Sequence[int]] = None):
         """Run the stack on rows (tokens[i] at slots[i]); writes their K/V into the
         cache and returns float64 logits [M, V] (and the final normalised hidden
-        rows if want_hidden)."""
+        rows if want_hidden).  Row i attends to slots 0..visible[i] (default
+        slots[i]: causal); every row's K/V of a layer is written before that
+        layer's attention, so a row may see later rows of the same call."""
         s = self.s
         M = len(tokens)
         slots = np.asarray(slots, dtype=np.int64)
+        vis = slots if visible is None else np.asarray(visible, dtype=np.int64)
         if M == 0:
             return np.zeros((0, self.vocab))
         D, nq, nkv = s.head_dim, s.q_heads, s.kv_heads
@@ -189,8 +193,8 @@ class Decoder:
             cache.k[li][slots] = k
             cache.v[li][slots] = v
             if li == self.readout_layer:
-                self.readout = budget.budget(q, cache.k[li], slots, self.readout_classes)
-            o = self._r(attend(q, cache.k[li], cache.v[li], slots).reshape(M, nq * D))
+                self.readout = budget.budget(q, cache.k[li], vis, self.readout_classes)
+            o = self._r(attend(q, cache.k[li], cache.v[li], vis).reshape(M, nq * D))
             x = x + o @ W["wo"].T
             b = self._r(rmsnorm(x, W["ffn_norm"], s.rms_eps))
             u = self._r(silu(b @ W["w_gate"].T) * (b @ W["w_up"].T))

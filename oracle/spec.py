@@ -175,6 +175,28 @@ class Sequence:
         K = self.K if K is None else K
         return [self.draft_step()[0] for _ in range(K)]
 
+    def block_propose(self, mask_token: int, K: Optional[int] = None):
+        """Eq. propose in a single forward (the block-diffusion draft family of
+        Sec. 4.1): rows [pending, MASK x K] at slots n..n+K, where the pending
+        row attends causally and every MASK row attends to the prefix and to
+        all rows of the block; MASK row i proposes d_i (greedy).  Committed
+        tokens the draft has not consumed with their own inputs (accepted
+        proposals, whose slots hold MASK rows' K/V) are first re-encoded
+        causally.  Afterwards only the pending row's slot holds a real input.
+        Returns (proposals, logits [K, V] of the MASK rows)."""
+        K = self.K if K is None else K
+        n = self.seq_len
+        if self.draft_len < n:
+            slots = list(range(self.draft_len, n))
+            self.D.forward([self.token_at(s) for s in slots], slots, self.dc)
+        rows = [self.pending] + [int(mask_token)] * K
+        slots = list(range(n, n + K + 1))
+        z = self.D.forward(rows, slots, self.dc, visible=[n] + [n + K] * K)
+        props = [int(t) for t in M.greedy_argmax(z[1:])]
+        self.props = props
+        self.draft_len = n + 1
+        return props, z[1:]
+
 
 def greedy_trace(seq: Sequence, max_tokens: Optional[int] = None) -> List[int]:
     """Greedy decoding until stop / budget; returns the generated tokens."""

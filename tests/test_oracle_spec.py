@@ -225,3 +225,62 @@ def test_mrope_draft_reduces_to_flatrope_on_text_and_differs_on_vision():
             outs.append((d, z, seq.dc.k[0][:48].copy()))
         assert np.allclose(outs[0][1], outs[1][1], rtol=1e-12, atol=1e-12) == same
         assert np.allclose(outs[0][2], outs[1][2], rtol=1e-12, atol=1e-12) == same
+
+
+# --- block proposal (single-forward draft, Eq. propose) ---------------------------
+
+def _block_seq(K=4, max_new=12):
+    w = _tiny(K=K, max_new=max_new)
+    hp = W.HostWeights(w)
+    T, D = S.oracle_decoders(w, hp)
+    return w, hp, T, D
+
+
+def test_block_visibility_rules():
+    w, hp, T, D = _block_seq()
+    mask = w.vocab - 1
+    seq = S.oracle_sequence(w, 0, T, D)
+    n, K = seq.seq_len, w.K
+    rows = [seq.pending] + [mask] * K
+    slots = list(range(n, n + K + 1))
+    ref = S.oracle_sequence(w, 0, T, D)
+    # visible = slots is the default causal pass, bit for bit
+    z_causal = ref.D.forward(rows, slots, ref.dc)
+    fresh = S.oracle_sequence(w, 0, T, D)
+    assert np.array_equal(fresh.D.forward(rows, slots, fresh.dc, visible=slots), z_causal)
+    z_block = seq.D.forward(rows, slots, seq.dc, visible=[n] + [n + K] * K)
+    # the pending row and the last MASK row see exactly what a causal pass shows them
+    assert np.array_equal(z_block[0], z_causal[0])
+    assert np.allclose(z_block[K], z_causal[K], rtol=1e-12, atol=1e-12)
+    # an earlier MASK row also sees the MASK rows after it
+    assert not np.allclose(z_block[1], z_causal[1], rtol=1e-6)
+
+
+def test_spec_loop_with_block_drafts_equals_greedy():
+    w, hp, T, D = _block_seq()
+    trace = OS.greedy_trace(S.oracle_sequence(w, 0, T, None, with_draft=False))
+    seq = S.oracle_sequence(w, 0, T, D)
+    out = OS.spec_loop(seq, lambda sq: sq.block_propose(w.vocab - 1)[0])
+    assert out == list(trace)
+
+
+def test_block_catch_up_reencodes_accepted_tokens():
+    # proposals that the verifier accepts were consumed as MASK inputs; the
+    # next block proposal re-encodes them, so the draft cache over the
+    # committed sequence equals a fresh causal pass over it
+    w, hp, T, D = _block_seq(K=4, max_new=20)
+    trace = OS.greedy_trace(S.oracle_sequence(w, 0, T, None, with_draft=False))
+    seq = S.oracle_sequence(w, 0, T, D)
+    P = seq.P
+    for _ in range(3):
+        seq.block_propose(w.vocab - 1)
+        i = len(seq.generated)
+        seq.verify(trace[i:i + w.K])          # all accepted (a bonus token too)
+    seq.block_propose(w.vocab - 1)            # re-encodes the accepted tokens
+    n = seq.seq_len
+    fresh = S.oracle_sequence(w, 0, T, D)
+    toks = [fresh.pending] + list(seq.generated)
+    fresh.D.forward(toks, list(range(P, P + len(toks))), fresh.dc)
+    for li in range(D.s.layers):
+        assert np.allclose(seq.dc.k[li][P:n + 1], fresh.dc.k[li][P:n + 1], rtol=1e-10, atol=1e-12)
+        assert np.allclose(seq.dc.v[li][P:n + 1], fresh.dc.v[li][P:n + 1], rtol=1e-10, atol=1e-12)
