@@ -441,6 +441,28 @@ def main():
     timed_tokens = sum(commits[args.warmup:args.warmup + args.steps])
     tok_s = timed_tokens / (total_ms / 1e3)
 
+    # 3b. the same rounds with the single-forward block proposal (the draft's
+    # catch-up of accepted tokens + one pass over [pending, MASK x K])
+    sb = Session(w, source="device", provider=src, flags=B.SPEC_FLAG_BLOCK_DRAFT)
+    evb = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(args.steps)]
+    for r in range(args.warmup + args.steps):
+        k = r - args.warmup
+        if k >= 0:
+            evb[k][0].record()
+        B.draft_steps(sb.ctx, K, sb.dtok.data_ptr())
+        if k >= 0:
+            evb[k][1].record()
+        B.spec_verify(sb.ctx, drafts[r].data_ptr(), 0)
+        B.spec_commit(sb.ctx, sb.acc.data_ptr(), 0, sb.ncom.data_ptr(), sb.fin.data_ptr())
+        if k >= 0:
+            evb[k][2].record()
+    torch.cuda.synchronize()
+    assert sb.state(0)["n_gen"] == expect
+    blk_ms = [e[0].elapsed_time(e[1]) for e in evb]
+    blk_round_ms = [e[0].elapsed_time(e[2]) for e in evb]
+    sb.close()
+    del sb
+
     # 4. per-kernel timing pass (events around every launch, no graph replay)
     B.spec_timing(s.ctx, True)
     for r in range(args.warmup + args.steps, rounds_total - 1):
@@ -514,6 +536,14 @@ def main():
                      "launches": dom["launches"], "avg_launch_us": dom["avg_us"],
                      "bytes_per_launch": dom["bytes_per_launch"]},
     }
+    b_us = float(np.median(blk_ms)) * 1e3
+    out["block_draft"] = {
+        "proposal_us": round(b_us, 1),
+        "cost_ratio_c": round(b_us / v_us, 4),
+        "theoretical_speedup_S": round(L / (1 + b_us / v_us), 3),
+        "tokens_per_s": round(timed_tokens / (sum(blk_round_ms) / 1e3), 2),
+        "note": "single-forward block proposal of K=8 with the same 2-layer draft (catch-up of accepted "
+                "tokens + one pass over [pending, MASK x 8]); same rounds and drafts as the main figure"}
     out["verify_us_p10_p50_p90"] = [round(float(np.percentile(verify_ms, q)) * 1e3, 1) for q in (10, 50, 90)]
     out["round_ms_p10_p50_p90"] = [round(float(np.percentile(round_ms, q)), 3) for q in (10, 50, 90)]
     if not args.no_batched:

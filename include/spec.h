@@ -85,6 +85,12 @@ typedef struct spec_dims {
                                       rows the batched-row GEMM takes, stream a tile-packed copy of every
                                       weight matrix that spec_init writes into the workspace (its size is
                                       part of spec_workspace_bytes) */
+#define SPEC_FLAG_BLOCK_DRAFT 32   /* draft_step proposes all K tokens in one forward of the draft (the
+                                      block-diffusion draft family, Sec. 4.1): rows [pending, MASK x K],
+                                      the pending row attending causally and every MASK row attending to
+                                      the prefix and the whole block; MASK row i proposes d_i.  Accepted
+                                      proposals of the previous round are first re-encoded causally.
+                                      Needs a draft; not with SPEC_FLAG_PERSISTENT. */
 #define SPEC_FLAG_DRAFT_MROPE 16   /* the draft rotates with 3D M-RoPE (its own mrope_section and
                                       interleaved, validated as the target's) instead of FlatRoPE: the
                                       comparison arm of the attention-budget readout (Sec. 4.2) */
@@ -100,6 +106,7 @@ typedef struct spec_config {
   int32_t max_new_tokens;    /* committed-token budget per sequence, >= 1 */
   int32_t stop_token;        /* committing this token ends a sequence; -1: none */
   int32_t flags;             /* SPEC_FLAG_* */
+  int32_t mask_token;        /* SPEC_FLAG_BLOCK_DRAFT: input token of the MASK rows, in [0, vocab) */
 } spec_config;
 
 /* Borrowed device pointers (bf16).  They must stay valid until spec_destroy. */
@@ -175,7 +182,9 @@ spec_status spec_init(const spec_config* cfg, const void* embed,
                       const spec_seq_init* seqs, void* workspace, size_t workspace_bytes,
                       hipStream_t stream, spec_ctx** out);
 
-/* One draft step (Eq. propose as a chain of single-token steps).  The draft
+/* One draft step (Eq. propose as a chain of single-token steps; with
+ * SPEC_FLAG_BLOCK_DRAFT the single-forward block proposal, which writes all K
+ * columns of d_draft_tokens and counts as the round's K steps).  The draft
  * first consumes the committed tokens it has not yet seen (one row normally,
  * up to K+1 after the verifier overrode its proposals), then proposes a token
  * from its last row with a greedy argmax.  Call j (0-based) of a round writes
@@ -188,6 +197,8 @@ spec_status draft_step(spec_ctx* ctx, int32_t* d_draft_tokens);
  * each other on the device without a gap between them.  1 <= n <= K minus the
  * steps already taken this round; the state rules are those of draft_step. */
 spec_status draft_steps(spec_ctx* ctx, int32_t n, int32_t* d_draft_tokens);
+/* (With SPEC_FLAG_BLOCK_DRAFT, draft_steps(ctx, K, out) is the block proposal
+ * and n must be K.) */
 
 /* One verify pass (Eq. verify, Eq. accept).  Rows [pending, d_1..d_K] of every
  * sequence go through the target in one forward pass; row j's greedy token is

@@ -25,6 +25,7 @@ SPEC_FLAG_PERSISTENT = 2
 SPEC_FLAG_PASS_TIMELINE = 4
 SPEC_FLAG_ROWMAJOR = 8
 SPEC_FLAG_DRAFT_MROPE = 16
+SPEC_FLAG_BLOCK_DRAFT = 32
 STATUS = {0: "SPEC_OK", 1: "SPEC_E_INVAL", 2: "SPEC_E_STATE", 3: "SPEC_E_CAPACITY", 5: "SPEC_E_HIP",
           6: "SPEC_E_NUMERIC"}
 KERNEL_KINDS = {"qkv": 0, "o": 1, "gateup": 2, "down": 3, "lmhead": 4, "attn": 5, "other": 6,
@@ -39,7 +40,8 @@ class spec_dims(Structure):
 
 class spec_config(Structure):
     _fields_ = [("target", spec_dims), ("draft", spec_dims), ("vocab", c_int32), ("K", c_int32),
-                ("batch", c_int32), ("max_new_tokens", c_int32), ("stop_token", c_int32), ("flags", c_int32)]
+                ("batch", c_int32), ("max_new_tokens", c_int32), ("stop_token", c_int32), ("flags", c_int32),
+                ("mask_token", c_int32)]
 
 
 class spec_layer_weights(Structure):

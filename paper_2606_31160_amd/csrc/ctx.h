@@ -43,7 +43,8 @@ struct SeqState {
   int32_t base;         // slot of row 0 of the current pass
   int32_t count;        // valid rows of the current pass (0 when idle)
   int32_t dcall;        // draft_step calls this round (the output column of the next one)
-  int32_t pad;
+  int32_t causal;       // rows 0..causal-1 of the current pass attend causally; the rest see
+                        // every row of the pass (a block proposal's MASK rows)
   int32_t vtok[kMaxRows];       // verify rows: pending, d_1..d_K
   int32_t rstar[kMaxRows];      // greedy token of each verify row
   int32_t committed[kMaxRows];  // tokens of the last verify to commit
@@ -52,7 +53,10 @@ struct SeqState {
 
 enum { ERR_TOKEN = 1, ERR_NUMERIC = 2, ERR_STATE = 4, ERR_SYNC = 8 };
 
-enum PassMode { PASS_VERIFY = 0, PASS_DRAFT = 1 };
+// Passes: the target's verify; one draft step (consume, propose from the last
+// row); for the single-forward block proposal, the draft's causal catch-up of
+// committed tokens it has not consumed (no LM head) and the block pass itself.
+enum PassMode { PASS_VERIFY = 0, PASS_DRAFT = 1, PASS_CATCHUP = 2, PASS_BLOCK = 3 };
 
 struct LayerW {
   const bf16_t *attn_norm, *wq, *wk, *wv, *wo, *ffn_norm, *wg, *wu, *wd;
@@ -79,6 +83,7 @@ struct Model {
   bf16_t* pk = nullptr;
   size_t pk_layer = 0, pk_o = 0, pk_gu = 0, pk_dn = 0;   // elements per layer; offsets inside a layer
   std::vector<SgJob> sg_host;       // [layers][4] (q/k/v, o, gate/up, down) + the LM head
+  std::vector<SgJob> sg_block;      // draft, block proposal: the last layer's down for every row, the LM head over all rows
 };
 
 struct TimingRec {
@@ -135,6 +140,8 @@ struct Ctx {
   size_t sg_part_floats = 0;
   int sg_units = 0;
   bool has_draft = false;
+  bool block_draft = false;          // SPEC_FLAG_BLOCK_DRAFT: draft_step proposes all K in one forward
+  int mask_token = 0;                // input token of the block's MASK rows
 
   // persistent pass (pass.hip): per-layer activations, barrier words
   bool use_pass = false;

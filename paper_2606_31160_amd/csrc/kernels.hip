@@ -130,17 +130,33 @@ struct EmbedArgs {
   const int8_t* axis;    // [D/2]
   int H, R, cap, mode, mpad, D, flat;
   int V;                 // vocabulary size: a token outside [0, V) is reported and read as 0
+  int mask;              // block pass: input token of the MASK rows
 };
 
 __global__ __launch_bounds__(1024) void k_embed(EmbedArgs p) {
   extern __shared__ float sq[];   // [H]
   const int j = blockIdx.x, b = blockIdx.y;
   const SeqState& s = p.st[b];
-  int base, count, tok = 0;
+  int base, count, tok = 0, causal = -1;
   if (p.mode == PASS_VERIFY) {
     base = s.seq_len;
     count = s.finished ? 0 : p.R;
     tok = s.vtok[j];
+  } else if (p.mode == PASS_CATCHUP) {
+    // committed tokens the draft has not consumed with their own inputs
+    base = s.draft_len;
+    count = s.finished ? 0 : s.seq_len - base;
+    if (count < 0 || count > p.R) {
+      if (!s.finished && j == 0 && threadIdx.x == 0) atomicOr(&p.st[b].err, ERR_STATE);
+      count = 0;
+    }
+    if (j < count) tok = p.hist[(size_t)b * p.cap + base + j];
+  } else if (p.mode == PASS_BLOCK) {
+    // [pending, MASK x (R-1)] at slots seq_len .. seq_len + R - 1
+    base = s.seq_len;
+    count = s.finished ? 0 : p.R;
+    causal = 1;
+    tok = j == 0 ? p.hist[(size_t)b * p.cap + base] : p.mask;
   } else {
     base = s.draft_len;
     const int last = s.seq_len + s.dstep;
@@ -156,6 +172,7 @@ __global__ __launch_bounds__(1024) void k_embed(EmbedArgs p) {
   if (j == 0 && threadIdx.x == 0) {
     p.st[b].base = base;
     p.st[b].count = count;
+    p.st[b].causal = causal < 0 ? count : causal;
   }
   const size_t r = (size_t)b * p.R + j;
   const bool live = j < count;
@@ -680,8 +697,8 @@ __device__ __forceinline__ void attn_partials(const AttnArgs& a, unsigned char* 
   // page 0), so the key and value loads wait for one round trip, not two.
   const int page = a.pt[b * a.pps + split];
   const SeqState& s = a.st[b];
-  const int count = s.count, base = s.base;
-  asm volatile("" ::"s"(page), "s"(count), "s"(base));   // both loads issued before either is awaited
+  const int count = s.count, base = s.base, causal = s.causal;
+  asm volatile("" ::"s"(page), "s"(count), "s"(base), "s"(causal));   // all loads issued before any is awaited
   const int rows = count * a.G;
   const int wrow0 = rb * 64 + wave * 16;
   const int qr = wrow0 + (lane & 15);
@@ -691,7 +708,7 @@ __device__ __forceinline__ void attn_partials(const AttnArgs& a, unsigned char* 
   const int kv_end = base + count;
   const int k0 = split * a.chunk;
   const int k1 = min(k0 + a.chunk, kv_end);
-  const int vis_end = base + j + 1;
+  const int vis_end = base + (j < causal ? j + 1 : count);   // rows past `causal` see the whole pass
   const size_t oi = (((size_t)split * a.B + b) * a.nq + hq) * a.R + j;
 
   if (k0 >= k1) {                                   // no keys in this split (workgroup-uniform)
@@ -900,7 +917,7 @@ template <bool RO>
 __device__ __forceinline__ void combine_unit(const CombineArgs& a, int j, int h, int b, float* coef) {
   const SeqState& s = a.st[b];
   if (j >= s.count) return;
-  const int vis_end = s.base + j + 1;
+  const int vis_end = s.base + (j < s.causal ? j + 1 : s.count);
   const int ns = (vis_end + a.chunk - 1) / a.chunk;   // splits holding keys this row sees
   const size_t row = ((size_t)b * a.nq + h) * a.R + j;
   const size_t sstride = (size_t)a.B * a.nq * a.R;
@@ -1090,6 +1107,29 @@ __global__ void k_commit(SeqState* st, int32_t* hist, int cap, int K, int stop, 
     for (int i = 0; i <= K; ++i) o_com[b * (K + 1) + i] = i < c ? s.committed[i] : -1;
 }
 
+// Block proposal (Eq. propose in one forward): MASK row i of the pass (row
+// i + 1) proposes d_i; the proposals go to the sequence's state and to the
+// caller's [B][K] array.  Only the pending row's slot now holds the draft K/V
+// of a real input.  grid B.
+__global__ void k_block_props(SeqState* st, int K, int32_t* out) {
+  const int b = blockIdx.x;
+  SeqState& s = st[b];
+  const bool live = s.count > 0;
+  for (int i = threadIdx.x; i < K; i += blockDim.x) {
+    const int d = live ? s.rstar[i + 1] : -1;
+    if (live) s.props[i] = d;
+    if (out) out[b * K + i] = d;
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    if (live) {
+      s.draft_len = s.base + 1;
+      s.dstep = K;
+    }
+    s.dcall = K;
+  }
+}
+
 // ---------------------------------------------------------------------------
 // host-side launch helpers
 // ---------------------------------------------------------------------------
@@ -1273,11 +1313,13 @@ hipError_t launch_attention(Ctx& c, Model& m, int li) {
 
 // One layer on the packed-weight path: q/k/v (+rotary, KV append),
 // attention, o (+residual), gate/up (+SwiGLU), down (+residual, next norm).
-hipError_t run_layer_sg(Ctx& c, Model& m, int li) {
+hipError_t run_layer_sg(Ctx& c, Model& m, int li, bool block) {
   const spec_dims& d = m.d;
   const int H = d.hidden, D = d.head_dim, nq = d.q_heads, nkv = d.kv_heads, F = d.ffn;
   const int M = c.M;
   const SgJob* hj = m.sg_host.data() + (size_t)li * 4;
+  // a block proposal's last layer writes the LM head input of every row
+  const SgJob& down = (block && li + 1 == d.layers) ? m.sg_block[0] : hj[3];
   {
     Timed t(c, SPEC_KERNEL_QKV, gemv_bytes((nq + 2 * nkv) * D, H, M, 2.0));
     CK(sg_launch(SG_ROPE, hj[0], S(c), t.e0, t.e1));
@@ -1293,7 +1335,7 @@ hipError_t run_layer_sg(Ctx& c, Model& m, int li) {
   }
   {
     Timed t(c, SPEC_KERNEL_DOWN, gemv_bytes(H, F, M, 10.0));
-    CK(sg_launch(SG_DOWN, hj[3], S(c), t.e0, t.e1));
+    CK(sg_launch(SG_DOWN, down, S(c), t.e0, t.e1));
   }
   return hipSuccess;
 }
@@ -1661,7 +1703,21 @@ bool sg_build_jobs(Ctx& c, Model& m, bool draft, bool fill) {
   h.amax_i = c.amax_i;
   h.logits = c.logits;
   h.allow_logits = draft ? 0 : 1;
-  return sg_plan(h, SG_ARGMAX, ncu, lim);
+  if (!sg_plan(h, SG_ARGMAX, ncu, lim)) return false;
+  // block proposal: the last layer's down writes every row's LM head input,
+  // and the LM head runs over all rows
+  m.sg_block.clear();
+  if (draft && c.block_draft) {
+    SgJob dn = m.sg_host[(size_t)(d.layers - 1) * 4 + 3];
+    dn.select_last = 0;
+    SgJob hd = h;
+    hd.M = c.M;
+    hd.rps = c.R;
+    hd.allow_logits = 0;
+    if (!sg_plan(dn, SG_DOWN, ncu, lim) || !sg_plan(hd, SG_ARGMAX, ncu, lim)) return false;
+    m.sg_block = {dn, hd};
+  }
+  return true;
 }
 
 hipError_t sg_pack_model(Ctx& c, Model& m) {
@@ -1829,22 +1885,25 @@ hipError_t launch_forward(Ctx& c, PassMode mode) {
     EmbedArgs p{c.st,    c.hist, c.embed,      m.L[0].attn_norm, c.x, persistent ? c.p_xa : c.xg,
                 persistent ? c.p_ssa : c.ss,  c.rcs,
                 c.pos3,  c.cs,   m.axis,       d.hidden,         c.R, c.cap,    (int)mode, c.Mpad,
-                d.head_dim, m.flat ? 1 : 0, c.V};
+                d.head_dim, m.flat ? 1 : 0, c.V, c.mask_token};
     Timed t(c, SPEC_KERNEL_OTHER, 0);
     hipExtLaunchKernelGGL(k_embed, dim3(c.R, c.B), dim3(1024), (size_t)d.hidden * sizeof(float), c.stream, t.e0, t.e1, 0, p);
     CK(hipGetLastError());
   }
-  const bool draft = mode == PASS_DRAFT;
+  // draft: a draft step, which proposes from each sequence's last row (stored
+  // as row b); a block pass runs the LM head over every row, as a verify does
+  const bool draft = mode == PASS_DRAFT, block = mode == PASS_BLOCK;
   if (persistent) {
     CK(run_layers_persistent(c, m, draft));
   } else if (c.sg) {
-    for (int li = 0; li < d.layers; ++li) CK(run_layer_sg(c, m, li));
+    for (int li = 0; li < d.layers; ++li) CK(run_layer_sg(c, m, li, block));
   } else {
     for (int li = 0; li < d.layers; ++li) {
       const bool last = li + 1 == d.layers;
       CK(run_layer(c, m, li, last ? m.final_norm : m.L[li + 1].attn_norm, last && draft));
     }
   }
+  if (mode == PASS_CATCHUP) return hipSuccess;   // consumes tokens only: no LM head
   // LM head (+ 1/rms of the final norm) with the fused per-tile argmax; the
   // draft proposes from each sequence's last row only (stored as row b)
   if (c.sg) {
@@ -1852,7 +1911,7 @@ hipError_t launch_forward(Ctx& c, PassMode mode) {
     const double bytes = gemv_bytes(c.V, d.hidden, rows, 0.0) + 8.0 * (c.V / kTile) * rows;
     Timed t(c, SPEC_KERNEL_LMHEAD, bytes);
     const size_t hi = (size_t)d.layers * 4;
-    CK(sg_launch(SG_ARGMAX, m.sg_host[hi], S(c), t.e0, t.e1));
+    CK(sg_launch(SG_ARGMAX, block ? m.sg_block[1] : m.sg_host[hi], S(c), t.e0, t.e1));
   } else {
     GemvArgs g = gemv_base(c, draft ? c.B : M, draft ? 1 : c.R);
     g.w[0] = c.embed;
@@ -1867,7 +1926,7 @@ hipError_t launch_forward(Ctx& c, PassMode mode) {
     g.amax_v = c.amax_v;
     g.amax_i = c.amax_i;
     g.logits = c.logits;
-    g.allow_logits = draft ? 0 : 1;
+    g.allow_logits = mode == PASS_VERIFY ? 1 : 0;
     const double bytes = gemv_bytes(c.V, d.hidden, g.M, 0.0) + 8.0 * (c.V / kTile) * g.M;
     if (g.M > kThinRows || (!draft && c.gemm_rows)) {
       g.pw = c.gemm_pk ? c.pk_head : nullptr;
@@ -1878,11 +1937,19 @@ hipError_t launch_forward(Ctx& c, PassMode mode) {
   }
   // (max, index) entries per row the LM head left: one per tile, or one per
   // workgroup on the packed path
-  const int ntiles = c.sg ? m.sg_host[(size_t)d.layers * 4].amax_n : c.V / kTile;
-  Timed t(c, SPEC_KERNEL_OTHER, 0);
-  AmaxArgs p{c.st, c.amax_v, c.amax_i, ntiles, c.Mpad, draft ? 1 : c.R, draft ? 1 : 0, draft ? c.draft_out : nullptr, c.K};
-  hipExtLaunchKernelGGL(k_argmax_rows, dim3(draft ? 1 : c.R, c.B), dim3(1024), 0, c.stream, t.e0, t.e1, 0, p);
-  return hipGetLastError();
+  const int ntiles = c.sg ? (block ? m.sg_block[1] : m.sg_host[(size_t)d.layers * 4]).amax_n : c.V / kTile;
+  {
+    Timed t(c, SPEC_KERNEL_OTHER, 0);
+    AmaxArgs p{c.st, c.amax_v, c.amax_i, ntiles, c.Mpad, draft ? 1 : c.R, draft ? 1 : 0, draft ? c.draft_out : nullptr, c.K};
+    hipExtLaunchKernelGGL(k_argmax_rows, dim3(draft ? 1 : c.R, c.B), dim3(1024), 0, c.stream, t.e0, t.e1, 0, p);
+    CK(hipGetLastError());
+  }
+  if (block) {
+    Timed t(c, SPEC_KERNEL_OTHER, 0);
+    hipExtLaunchKernelGGL(k_block_props, dim3(c.B), dim3(64), 0, c.stream, t.e0, t.e1, 0, c.st, c.K, c.draft_out);
+    CK(hipGetLastError());
+  }
+  return hipSuccess;
 }
 
 hipError_t launch_commit(Ctx& c, int32_t* acc, int32_t* committed, int32_t* ncommit, int32_t* fin) {

@@ -106,6 +106,20 @@ bool check_config(const spec_config* cfg, const spec_seq_init* seqs, bool has_dr
     return false;
   }
   if (!check_dims(cfg->target, true, err, "target")) return false;
+  if (cfg->flags & SPEC_FLAG_BLOCK_DRAFT) {
+    if (!has_draft || cfg->K < 1) {
+      err = "SPEC_FLAG_BLOCK_DRAFT needs a draft and K >= 1";
+      return false;
+    }
+    if (cfg->flags & SPEC_FLAG_PERSISTENT) {
+      err = "SPEC_FLAG_BLOCK_DRAFT runs on the layered path, not with SPEC_FLAG_PERSISTENT";
+      return false;
+    }
+    if (cfg->mask_token < 0 || cfg->mask_token >= cfg->vocab) {
+      err = "mask_token out of range";
+      return false;
+    }
+  }
   if (has_draft) {
     if (!check_dims(cfg->draft, (cfg->flags & SPEC_FLAG_DRAFT_MROPE) != 0, err, "draft")) return false;
     if (cfg->draft.hidden != cfg->target.hidden || cfg->draft.head_dim != cfg->target.head_dim ||
@@ -343,6 +357,8 @@ size_t carve(Ctx& c, const spec_config* cfg, const spec_seq_init* seqs, bool has
   c.attn_splits = L.splits;
   c.tgt.d = cfg->target;
   c.tgt.flat = false;
+  c.block_draft = has_draft && (cfg->flags & SPEC_FLAG_BLOCK_DRAFT) != 0;
+  c.mask_token = cfg->mask_token;
   c.gemm_rows = gemm_rows_for(cfg, has_draft, L.M);
   set_splits(c.tgt, L.M, c.gemm_rows);
   if (has_draft) {
@@ -475,11 +491,14 @@ size_t carve(Ctx& c, const spec_config* cfg, const spec_seq_init* seqs, bool has
       sg_build_jobs(c, c.tgt, false, false) && (!has_draft || sg_build_jobs(c, c.drf, true, false))) {
     size_t pf = 0;
     int units = 0;
-    for (int k = 0; k < (has_draft ? 2 : 1); ++k)
-      for (const SgJob& j : (k ? c.drf : c.tgt).sg_host) {
-        pf = std::max(pf, sg_part_floats(j));
-        units = std::max(units, j.units);
-      }
+    for (int k = 0; k < (has_draft ? 2 : 1); ++k) {
+      const Model& mm = k ? c.drf : c.tgt;
+      for (const std::vector<SgJob>* js : {&mm.sg_host, &mm.sg_block})
+        for (const SgJob& j : *js) {
+          pf = std::max(pf, sg_part_floats(j));
+          units = std::max(units, j.units);
+        }
+    }
     c.sg = true;
     c.sg_part_floats = pf;
     c.sg_units = units;
@@ -555,6 +574,14 @@ spec_status set_err(Ctx& c, spec_status s, const char* msg) {
     if (e_ != hipSuccess) return fail_hip(c, e_, where); \
   } while (0)
 
+// One pass; a block proposal is the draft's catch-up of accepted tokens and
+// the block pass.
+hipError_t launch_pass(Ctx& c, PassMode mode) {
+  if (mode != PASS_BLOCK) return launch_forward(c, mode);
+  const hipError_t e = launch_forward(c, PASS_CATCHUP);
+  return e != hipSuccess ? e : launch_forward(c, PASS_BLOCK);
+}
+
 // Captures `launch` into `ge` on the capture stream (once; `ge` is reset by
 // the caller when what the graph bakes in changes) and launches it.
 template <class Launch>
@@ -589,6 +616,7 @@ spec_status run_graph(Ctx& c, hipGraphExec_t& ge, Launch&& launch) {
 // captured again when that array changes.
 spec_status run_pass(Ctx& c, PassMode mode) {
   const int mi = mode == PASS_VERIFY ? 0 : 1;
+  const bool drafting = mode != PASS_VERIFY;
   if (c.ro_arm_out && c.ro_arm_model == mi) {
     // an armed readout: this pass is launched kernel by kernel with the
     // readout variants on its layer; graphs and later passes are unaffected
@@ -597,7 +625,7 @@ spec_status run_pass(Ctx& c, PassMode mode) {
     c.ro_out = c.ro_arm_out;
     c.ro_arm_out = nullptr;
     c.ro_arm_model = -1;
-    const hipError_t e = launch_forward(c, mode);
+    const hipError_t e = launch_pass(c, mode);
     c.ro_m = nullptr;
     c.ro_out = nullptr;
     HIPCHK(c, e, "forward pass with readout");
@@ -607,15 +635,15 @@ spec_status run_pass(Ctx& c, PassMode mode) {
   if (!graphs) {
     // timing mode: a head start so the timed kernels run back to back
     if (c.timing) HIPCHK(c, launch_hold(c, mode == PASS_VERIFY ? 4.0 : 1.0), "timing hold");
-    HIPCHK(c, launch_forward(c, mode), "forward pass");
+    HIPCHK(c, launch_pass(c, mode), "forward pass");
     return SPEC_OK;
   }
-  if (mode == PASS_DRAFT && c.g_draft && c.g_draft_out != c.draft_out) {
+  if (drafting && c.g_draft && c.g_draft_out != c.draft_out) {
     (void)hipGraphExecDestroy(c.g_draft);
     c.g_draft = nullptr;
   }
-  if (mode == PASS_DRAFT) c.g_draft_out = c.draft_out;
-  return run_graph(c, mode == PASS_VERIFY ? c.g_verify : c.g_draft, [&] { return launch_forward(c, mode); });
+  if (drafting) c.g_draft_out = c.draft_out;
+  return run_graph(c, mode == PASS_VERIFY ? c.g_verify : c.g_draft, [&] { return launch_pass(c, mode); });
 }
 
 // The commit kernel runs through a graph of its own too: launched directly
@@ -881,9 +909,9 @@ spec_status draft_step(spec_ctx* ctx, int32_t* d_draft_tokens) {
     if (c.phase == Ctx::VERIFIED) return set_err(c, SPEC_E_STATE, "draft_step: commit the last verify first");
     if (c.dsteps >= c.K) return set_err(c, SPEC_E_STATE, "draft_step: K steps already taken this round");
     c.draft_out = d_draft_tokens;
-    spec_status s = run_pass(c, PASS_DRAFT);
+    spec_status s = run_pass(c, c.block_draft ? PASS_BLOCK : PASS_DRAFT);
     if (s != SPEC_OK) return s;
-    c.dsteps += 1;
+    c.dsteps += c.block_draft ? c.K : 1;
     c.phase = Ctx::DRAFTING;
     return SPEC_OK;
   });
@@ -895,6 +923,15 @@ spec_status draft_steps(spec_ctx* ctx, int32_t n, int32_t* d_draft_tokens) {
     if (c.K < 1) return set_err(c, SPEC_E_STATE, "draft_steps: K is 0");
     if (c.phase == Ctx::VERIFIED) return set_err(c, SPEC_E_STATE, "draft_steps: commit the last verify first");
     if (n < 1 || n > c.K - c.dsteps) return set_err(c, SPEC_E_STATE, "draft_steps: n must be 1..K minus the steps taken");
+    if (c.block_draft) {
+      if (n != c.K) return set_err(c, SPEC_E_STATE, "draft_steps: the block proposal takes n = K");
+      c.draft_out = d_draft_tokens;
+      spec_status s = run_pass(c, PASS_BLOCK);
+      if (s != SPEC_OK) return s;
+      c.dsteps = c.K;
+      c.phase = Ctx::DRAFTING;
+      return SPEC_OK;
+    }
     c.draft_out = d_draft_tokens;
     if (n == 1 || !c.use_graphs || c.timing || (c.ro_arm_out && c.ro_arm_model == 1)) {
       for (int i = 0; i < n; ++i) {

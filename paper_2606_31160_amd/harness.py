@@ -32,7 +32,7 @@ class Session:
 
     def __init__(self, w, source: str = "host", flags: int = 0, with_draft: bool = True,
                  K: Optional[int] = None, max_new_tokens: Optional[int] = None, stop_token: Optional[int] = None,
-                 provider=None, page_seed: Optional[int] = None):
+                 provider=None, page_seed: Optional[int] = None, mask_token: Optional[int] = None):
         torch = _require_gpu()
         import workloads as W
         self.torch = torch
@@ -65,6 +65,7 @@ class Session:
         cfg.max_new_tokens = w.max_new_tokens if max_new_tokens is None else max_new_tokens
         cfg.stop_token = w.stop_token if stop_token is None else stop_token
         cfg.flags = flags
+        cfg.mask_token = w.vocab - 1 if mask_token is None else mask_token   # block proposal's MASK input
         self.cfg = cfg
 
         seqs = (B.spec_seq_init * self.B)()

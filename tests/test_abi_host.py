@@ -30,7 +30,7 @@ def test_library_loads_and_exports_every_declared_symbol():
 def test_struct_sizes_match_c_layout():
     # 64-bit SysV layout of the header's structs
     assert ctypes.sizeof(B.spec_dims) == 48
-    assert ctypes.sizeof(B.spec_config) == 120
+    assert ctypes.sizeof(B.spec_config) == 124
     assert ctypes.sizeof(B.spec_seq_init) == 64
     assert ctypes.sizeof(B.spec_layer_weights) == 72
 
@@ -112,6 +112,9 @@ def test_benchmark_and_paper_configs_validate_on_host(name):
      "draft: mrope_section"),
     (lambda c, s: setattr(s[0], "pending_token", 1024), "pending_token"),
     (lambda c, s: setattr(s[0], "prefix_len", 0), "prefix_len"),
+    (lambda c, s: (setattr(c, "flags", B.SPEC_FLAG_BLOCK_DRAFT), setattr(c, "mask_token", 1024)), "mask_token"),
+    (lambda c, s: setattr(c, "flags", B.SPEC_FLAG_BLOCK_DRAFT | B.SPEC_FLAG_PERSISTENT), "PERSISTENT"),
+    (lambda c, s: (setattr(c, "flags", B.SPEC_FLAG_BLOCK_DRAFT), setattr(c, "K", 0)), "BLOCK_DRAFT"),
 ])
 def test_invalid_config_rejected_on_host(mutate, needle):
     w = W.get("C1")
