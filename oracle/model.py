@@ -110,6 +110,12 @@ class Decoder:
         self.readout_layer: Optional[int] = None
         self.readout_classes: Optional[np.ndarray] = None
         self.readout: Optional[np.ndarray] = None
+        # conditioning on another stack's hidden states: input_hook(x, slots)
+        # replaces the embedded rows before layer 0; capture_layers names the
+        # layers whose output residual rows forward() keeps in self.captured
+        self.input_hook: Optional[Callable[[np.ndarray, np.ndarray], np.ndarray]] = None
+        self.capture_layers: Sequence[int] = ()
+        self.captured: Dict[int, np.ndarray] = {}
 
     # -- weights -----------------------------------------------------------
     def layer(self, li: int) -> Dict[str, np.ndarray]:
@@ -181,6 +187,9 @@ class Decoder:
         D, nq, nkv = s.head_dim, s.q_heads, s.kv_heads
         pos = cache.pos3[:, slots]
         x = self.embed_rows(tokens)
+        if self.input_hook is not None:
+            x = self.input_hook(x, slots)
+        self.captured = {}
         for li in range(s.layers):
             W = self.layer(li)
             a = self._r(rmsnorm(x, W["attn_norm"], s.rms_eps))
@@ -199,6 +208,8 @@ class Decoder:
             b = self._r(rmsnorm(x, W["ffn_norm"], s.rms_eps))
             u = self._r(silu(b @ W["w_gate"].T) * (b @ W["w_up"].T))
             x = x + u @ W["w_down"].T
+            if li in self.capture_layers:
+                self.captured[li] = self._r(x)
         h = self._r(rmsnorm(x, self.final_norm(), s.rms_eps))
         z = self.lm_head(h)
         return (z, h) if want_hidden else z

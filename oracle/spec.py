@@ -29,6 +29,7 @@ from typing import Callable, List, Optional
 import numpy as np
 
 from . import model as M
+from . import numerics
 from . import positions
 
 
@@ -65,12 +66,46 @@ class VerifyResult:
     finished: bool
 
 
+class Conditioning:
+    """The draft conditioned on target hidden states (Sec. 4.1: the target's
+    hidden states from several layers feed the draft; fused EAGLE-3 style,
+    Sec. 5).  Reading:
+
+      f_t = W_fuse [h_a(t); h_b(t); h_c(t)]       (3H -> H)
+      x_t = e(token_t) + W_in [e(token_t); f_{t-1}]  (2H -> H), the draft's layer-0 input
+
+    where h_l(t) is the target's residual stream after layer l at slot t, taken
+    from verify rows whose inputs are committed; f is zero where the target has
+    not verified the slot (prompt slots, since prefill is not part of the
+    path, and the draft's own proposal rows)."""
+
+    def __init__(self, layers, w_fuse: np.ndarray, w_in: np.ndarray, mirror: bool = False):
+        self.layers = tuple(int(l) for l in layers)
+        self.w_fuse = np.asarray(w_fuse, dtype=np.float64)
+        self.w_in = np.asarray(w_in, dtype=np.float64)
+        self.mirror = mirror
+
+    def fuse(self, captured, j: int) -> np.ndarray:
+        h = np.concatenate([captured[l][j] for l in self.layers])
+        f = self.w_fuse @ h
+        return numerics.mirror(f) if self.mirror else f
+
+    def input(self, x: np.ndarray, slots, feat) -> np.ndarray:
+        H = x.shape[1]
+        out = np.empty_like(x)
+        for i, t in enumerate(slots):
+            f = feat.get(int(t) - 1, np.zeros(H))
+            out[i] = x[i] + self.w_in @ np.concatenate([x[i], f])
+        return out
+
+
 class Sequence:
     """One scene: target (and optionally draft) caches plus committed tokens."""
 
     def __init__(self, target: M.Decoder, draft: Optional[M.Decoder], prefix_len: int, blocks,
                  pending_token: int, capacity: int, tgt_prefix_kv, drf_prefix_kv=None,
-                 K: int = 4, max_new_tokens: int = 20, stop_token: int = -1):
+                 K: int = 4, max_new_tokens: int = 20, stop_token: int = -1,
+                 cond: Optional[Conditioning] = None):
         """tgt_prefix_kv(layer) -> (k_bits, v_bits) [P, n_kv, D] uint16; likewise
         drf_prefix_kv for the draft.  `blocks` are (start, t, h, w) grids."""
         self.T, self.D = target, draft
@@ -84,6 +119,8 @@ class Sequence:
         for li in range(target.s.layers):
             k, v = tgt_prefix_kv(li)
             target.fill_prefix(self.tc, li, k, v)
+        self.cond = cond
+        self.feat = {}                            # slot -> fused target feature (conditioning)
         self.committed = [int(pending_token)]     # tokens at indices P, P+1, ...
         self.finished = False
         self.history: List[int] = []              # accept length per verify
@@ -124,11 +161,19 @@ class Sequence:
         K = len(drafts)
         rows = [self.pending] + [int(d) for d in drafts]
         slots = list(range(n, n + K + 1))
+        if self.cond is not None:
+            self.T.capture_layers = self.cond.layers
         z = self.T.forward(rows, slots, self.tc)
+        self.T.capture_layers = ()
         rstar = M.greedy_argmax(z)
         l = accept_length(drafts, rstar)
         budget = self.max_new - len(self.generated)
         toks, fin = commit_tokens(drafts, rstar, l, self.stop, budget)
+        if self.cond is not None:
+            # rows 0..len(toks)-1 had committed inputs (the pending token and
+            # the accepted proposals): their features are final
+            for j in range(len(toks)):
+                self.feat[n + j] = self.cond.fuse(self.T.captured, j)
         self._commit(n, toks)
         self.finished = fin
         self.history.append(l)
@@ -151,6 +196,14 @@ class Sequence:
         return self.verify([]).committed[0]
 
     # draft -------------------------------------------------------------------
+    def _draft_forward(self, tokens, slots, visible=None):
+        if self.cond is not None:
+            self.D.input_hook = lambda x, sl: self.cond.input(x, sl, self.feat)
+        try:
+            return self.D.forward(tokens, slots, self.dc, visible=visible)
+        finally:
+            self.D.input_hook = None
+
     def draft_input(self, s: int) -> int:
         n = self.seq_len
         if s <= n:
@@ -164,7 +217,7 @@ class Sequence:
         last = n + len(self.props)
         slots = list(range(self.draft_len, last + 1))
         toks = [self.draft_input(s) for s in slots]
-        z = self.D.forward(toks, slots, self.dc)
+        z = self._draft_forward(toks, slots)
         d = int(M.greedy_argmax(z[-1:])[0])
         self.props.append(d)
         self.draft_len = last + 1
@@ -188,10 +241,10 @@ class Sequence:
         n = self.seq_len
         if self.draft_len < n:
             slots = list(range(self.draft_len, n))
-            self.D.forward([self.token_at(s) for s in slots], slots, self.dc)
+            self._draft_forward([self.token_at(s) for s in slots], slots)
         rows = [self.pending] + [int(mask_token)] * K
         slots = list(range(n, n + K + 1))
-        z = self.D.forward(rows, slots, self.dc, visible=[n] + [n + K] * K)
+        z = self._draft_forward(rows, slots, visible=[n] + [n + K] * K)
         props = [int(t) for t in M.greedy_argmax(z[1:])]
         self.props = props
         self.draft_len = n + 1

@@ -48,8 +48,16 @@ def device_kv(w: W.Workload, b: int, model: str):
                        bits(W.prefix_kv_device(w, b, model, li, "v")))
 
 
+def conditioning(w: W.Workload, provider, layers, mirror: bool = False):
+    """The oracle's target-hidden-state conditioning with the workload's seeded
+    fusion weights."""
+    from oracle import numerics as ON
+    return OS.Conditioning(layers, ON.decode(provider.get("draft", -1, "w_fuse")),
+                           ON.decode(provider.get("draft", -1, "w_in")), mirror=mirror)
+
+
 def oracle_sequence(w: W.Workload, b: int, T, D, kv=None, capacity=None, pending=None,
-                    with_draft: bool = True):
+                    with_draft: bool = True, cond=None):
     lay = w.seqs[b]
     cap = capacity or capacity_for(w, b)
     blocks = [(bl.start, bl.t, bl.h, bl.w) for bl in lay.blocks]
@@ -58,7 +66,7 @@ def oracle_sequence(w: W.Workload, b: int, T, D, kv=None, capacity=None, pending
     dd = D if with_draft else None
     return OS.Sequence(T, dd, lay.prefix_len, blocks, pend, cap, kv(w, b, "target"),
                        kv(w, b, "draft") if dd is not None else None,
-                       K=w.K, max_new_tokens=w.max_new_tokens, stop_token=w.stop_token)
+                       K=w.K, max_new_tokens=w.max_new_tokens, stop_token=w.stop_token, cond=cond)
 
 
 def margin(z: np.ndarray) -> np.ndarray:

@@ -284,3 +284,61 @@ def test_block_catch_up_reencodes_accepted_tokens():
     for li in range(D.s.layers):
         assert np.allclose(seq.dc.k[li][P:n + 1], fresh.dc.k[li][P:n + 1], rtol=1e-10, atol=1e-12)
         assert np.allclose(seq.dc.v[li][P:n + 1], fresh.dc.v[li][P:n + 1], rtol=1e-10, atol=1e-12)
+
+
+# --- conditioning on target hidden states -----------------------------------------
+
+def test_conditioning_with_zero_input_weights_is_the_plain_draft():
+    w, hp, T, D = _block_seq()
+    cond = S.conditioning(w, hp, (0, 1, 1))
+    cond.w_in[:] = 0.0
+    a = S.oracle_sequence(w, 0, T, D, cond=cond)
+    b = S.oracle_sequence(w, 0, T, D)
+    for _ in range(2):
+        da, za = a.draft_step()
+        db, zb = b.draft_step()
+        assert np.array_equal(za, zb)
+    trace = OS.greedy_trace(S.oracle_sequence(w, 0, T, None, with_draft=False))
+    a.verify(trace[:2] + [0, 0])
+    b.verify(trace[:2] + [0, 0])
+    assert a.feat and set(a.feat) == set(range(a.P, a.seq_len))
+    assert np.array_equal(a.draft_step()[1], b.draft_step()[1])
+
+
+def test_captured_last_layer_reproduces_the_logits():
+    # the residual stream after the last layer, normalised and projected on
+    # the tied embedding, is the forward pass's own logits
+    w, hp, T, D = _block_seq()
+    seq = S.oracle_sequence(w, 0, T, None, with_draft=False)
+    L = T.s.layers
+    T.capture_layers = (L - 1,)
+    z = T.forward([seq.pending, 5, 9], [seq.P, seq.P + 1, seq.P + 2], seq.tc)
+    T.capture_layers = ()
+    h = M.rmsnorm(T.captured[L - 1], T.final_norm(), T.s.rms_eps)
+    assert np.allclose(T.lm_head(h), z, rtol=1e-12, atol=1e-12)
+
+
+def test_features_of_a_verify_equal_sequential_single_row_features():
+    # a verify of K+1 rows yields, for each committed row, the feature that
+    # one-row verifies of the same tokens yield (the target is causal)
+    w, hp, T, D = _block_seq()
+    cond = S.conditioning(w, hp, (0, 1, 1))
+    trace = OS.greedy_trace(S.oracle_sequence(w, 0, T, None, with_draft=False))
+    a = S.oracle_sequence(w, 0, T, None, with_draft=False, cond=cond)
+    a.verify(trace[:w.K])                       # all accepted: K+1 committed rows
+    b = S.oracle_sequence(w, 0, T, None, with_draft=False, cond=cond)
+    for _ in range(w.K + 1):
+        b.verify([])
+    assert set(a.feat) == set(b.feat)
+    for t in a.feat:
+        assert np.allclose(a.feat[t], b.feat[t], rtol=1e-9, atol=1e-9)
+
+
+def test_conditioned_spec_loop_equals_greedy():
+    w, hp, T, D = _block_seq()
+    cond = S.conditioning(w, hp, (0, 1, 1))
+    trace = OS.greedy_trace(S.oracle_sequence(w, 0, T, None, with_draft=False))
+    seq = S.oracle_sequence(w, 0, T, D, cond=cond)
+    assert OS.spec_loop(seq, lambda sq: sq.propose()) == list(trace)
+    seq = S.oracle_sequence(w, 0, T, D, cond=cond)
+    assert OS.spec_loop(seq, lambda sq: sq.block_propose(w.vocab - 1)[0]) == list(trace)

@@ -26,7 +26,10 @@ from .configs import ModelShape, Workload
 
 MODEL_IDS = {"target": 0, "draft": 1, "global": 2}
 LAYER_TENSORS = ("attn_norm", "wq", "wk", "wv", "wo", "ffn_norm", "w_gate", "w_up", "w_down")
-NAME_IDS = {n: i for i, n in enumerate(LAYER_TENSORS + ("final_norm", "embed", "k_prefix", "v_prefix"))}
+# (w_fuse, w_in: the draft's conditioning on target hidden states, appended so
+# that earlier keys keep their streams)
+NAME_IDS = {n: i for i, n in enumerate(LAYER_TENSORS + ("final_norm", "embed", "k_prefix", "v_prefix",
+                                                        "w_fuse", "w_in"))}
 
 
 def bf16_bits_from_f32(x: np.ndarray) -> np.ndarray:
@@ -45,6 +48,7 @@ def tensor_shape(shape: ModelShape, vocab: int, name: str) -> Tuple[int, ...]:
         "wo": (H, shape.q_heads * D),
         "w_gate": (shape.ffn, H), "w_up": (shape.ffn, H), "w_down": (H, shape.ffn),
         "embed": (vocab, H),
+        "w_fuse": (H, 3 * H), "w_in": (H, 2 * H),
     }[name]
 
 
