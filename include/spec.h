@@ -91,6 +91,14 @@ typedef struct spec_dims {
                                       the prefix and the whole block; MASK row i proposes d_i.  Accepted
                                       proposals of the previous round are first re-encoded causally.
                                       Needs a draft; not with SPEC_FLAG_PERSISTENT. */
+#define SPEC_FLAG_COND 64          /* the draft is conditioned on target hidden states (Sec. 4.1; fused
+                                      EAGLE-3 style, Sec. 5): every verify keeps the target's residual
+                                      stream after layers cond_layers[0..2]; for the rows whose inputs get
+                                      committed, f = w_fuse [h0; h1; h2] (3*hidden -> hidden) becomes the
+                                      slot's feature, and a draft row at slot t takes the layer-0 input
+                                      e + w_in [e; f(t-1)] (2*hidden -> hidden; f = 0 where no verified
+                                      feature exists: prompt slots and the draft's proposal rows).
+                                      Needs a draft with w_fuse and w_in; not with SPEC_FLAG_PERSISTENT. */
 #define SPEC_FLAG_DRAFT_MROPE 16   /* the draft rotates with 3D M-RoPE (its own mrope_section and
                                       interleaved, validated as the target's) instead of FlatRoPE: the
                                       comparison arm of the attention-budget readout (Sec. 4.2) */
@@ -107,6 +115,7 @@ typedef struct spec_config {
   int32_t stop_token;        /* committing this token ends a sequence; -1: none */
   int32_t flags;             /* SPEC_FLAG_* */
   int32_t mask_token;        /* SPEC_FLAG_BLOCK_DRAFT: input token of the MASK rows, in [0, vocab) */
+  int32_t cond_layers[3];    /* SPEC_FLAG_COND: target layers (0-based) whose output is fused */
 } spec_config;
 
 /* Borrowed device pointers (bf16).  They must stay valid until spec_destroy. */
@@ -125,6 +134,8 @@ typedef struct spec_layer_weights {
 typedef struct spec_model_weights {
   const spec_layer_weights* layers;  /* host array of dims.layers entries */
   const void* final_norm;            /* [hidden] bf16, device */
+  const void* w_fuse;                /* draft, SPEC_FLAG_COND: [hidden][3*hidden] bf16; else ignored */
+  const void* w_in;                  /* draft, SPEC_FLAG_COND: [hidden][2*hidden] bf16; else ignored */
 } spec_model_weights;
 
 /* A (t, h, w) grid of vision patches occupying sequence indices
@@ -268,6 +279,10 @@ spec_status spec_debug_state(spec_ctx* ctx, int32_t b, int32_t* host_out);
  * host_out [npos][kv_heads][head_dim] bf16. */
 spec_status spec_debug_kv(spec_ctx* ctx, int32_t b, int32_t model, int32_t layer, int32_t which,
                           int32_t pos0, int32_t npos, void* host_out);
+
+/* SPEC_FLAG_COND: the fused target features of sequence b's slots [slot0,
+ * slot0+n) into host_out [n][hidden] bf16 (zero for slots never verified). */
+spec_status spec_debug_feature(spec_ctx* ctx, int32_t b, int32_t slot0, int32_t n, void* host_out);
 
 /* Execution path of the context's passes into *path:
  * SPEC_PATH_ROWMAJOR (one kernel per layer step over the caller's row-major weights),

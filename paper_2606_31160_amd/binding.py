@@ -26,6 +26,7 @@ SPEC_FLAG_PASS_TIMELINE = 4
 SPEC_FLAG_ROWMAJOR = 8
 SPEC_FLAG_DRAFT_MROPE = 16
 SPEC_FLAG_BLOCK_DRAFT = 32
+SPEC_FLAG_COND = 64
 STATUS = {0: "SPEC_OK", 1: "SPEC_E_INVAL", 2: "SPEC_E_STATE", 3: "SPEC_E_CAPACITY", 5: "SPEC_E_HIP",
           6: "SPEC_E_NUMERIC"}
 KERNEL_KINDS = {"qkv": 0, "o": 1, "gateup": 2, "down": 3, "lmhead": 4, "attn": 5, "other": 6,
@@ -41,7 +42,7 @@ class spec_dims(Structure):
 class spec_config(Structure):
     _fields_ = [("target", spec_dims), ("draft", spec_dims), ("vocab", c_int32), ("K", c_int32),
                 ("batch", c_int32), ("max_new_tokens", c_int32), ("stop_token", c_int32), ("flags", c_int32),
-                ("mask_token", c_int32)]
+                ("mask_token", c_int32), ("cond_layers", c_int32 * 3)]
 
 
 class spec_layer_weights(Structure):
@@ -50,7 +51,8 @@ class spec_layer_weights(Structure):
 
 
 class spec_model_weights(Structure):
-    _fields_ = [("layers", POINTER(spec_layer_weights)), ("final_norm", c_void_p)]
+    _fields_ = [("layers", POINTER(spec_layer_weights)), ("final_norm", c_void_p), ("w_fuse", c_void_p),
+                ("w_in", c_void_p)]
 
 
 class spec_vision_block(Structure):
@@ -98,6 +100,7 @@ def lib():
             "spec_debug_pass_timeline": [P, c_int32, P, c_int64, POINTER(c_int32), POINTER(c_int32),
                                          POINTER(c_double)],
             "spec_debug_path": [P, POINTER(c_int32)],
+            "spec_debug_feature": [P, c_int32, c_int32, c_int32, P],
         }
         for name, args in sig.items():
             f = getattr(L, name)
@@ -203,6 +206,14 @@ def spec_debug_kv(ctx, b: int, model: int, layer: int, which: int, pos0: int, np
 
 
 PATHS = {0: "rowmajor", 1: "packed", 2: "persistent"}
+
+
+def spec_debug_feature(ctx, b: int, slot0: int, n: int, hidden: int):
+    """Fused target features of slots [slot0, slot0+n) as bf16 bits [n][hidden]."""
+    import numpy as np
+    out = np.zeros((n, hidden), dtype=np.uint16)
+    _check(lib().spec_debug_feature(ctx, b, slot0, n, out.ctypes.data_as(c_void_p)), "spec_debug_feature", ctx)
+    return out
 
 
 def spec_debug_path(ctx) -> str:

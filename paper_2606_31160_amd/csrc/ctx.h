@@ -53,6 +53,8 @@ struct SeqState {
 
 enum { ERR_TOKEN = 1, ERR_NUMERIC = 2, ERR_STATE = 4, ERR_SYNC = 8 };
 
+constexpr int kCondSplits = 4;   // k-splits of the feature fusion (3H inputs) and of the input projection
+
 // Passes: the target's verify; one draft step (consume, propose from the last
 // row); for the single-forward block proposal, the draft's causal catch-up of
 // committed tokens it has not consumed (no LM head) and the block pass itself.
@@ -142,6 +144,15 @@ struct Ctx {
   bool has_draft = false;
   bool block_draft = false;          // SPEC_FLAG_BLOCK_DRAFT: draft_step proposes all K in one forward
   int mask_token = 0;                // input token of the block's MASK rows
+  // SPEC_FLAG_COND: the draft conditioned on target hidden states
+  bool cond = false;
+  int cond_layers[3] = {};
+  const bf16_t* w_fuse = nullptr;    // [H][3H]
+  const bf16_t* w_in = nullptr;      // [H][2H]
+  bf16_t* cat3 = nullptr;            // [Mpad][3H] verify rows' residual streams after cond_layers
+  float* fusedp = nullptr;           // [kCondSplits][M][H] k-split partial sums of w_fuse . cat3
+  bf16_t* feat = nullptr;            // [B][cap][H] fused feature of every verified slot
+  bf16_t* cat2 = nullptr;            // [Mpad][2H] draft rows' [embedding; feature of the previous slot]
 
   // persistent pass (pass.hip): per-layer activations, barrier words
   bool use_pass = false;

@@ -131,6 +131,8 @@ struct EmbedArgs {
   int H, R, cap, mode, mpad, D, flat;
   int V;                 // vocabulary size: a token outside [0, V) is reported and read as 0
   int mask;              // block pass: input token of the MASK rows
+  bf16_t* cat2;          // conditioned draft: [Mpad][2H] rows [embedding; feature of the previous slot], or null
+  const bf16_t* feat;    // [B][cap][H] fused target features
 };
 
 __global__ __launch_bounds__(1024) void k_embed(EmbedArgs p) {
@@ -186,6 +188,18 @@ __global__ __launch_bounds__(1024) void k_embed(EmbedArgs p) {
     p.x[r * p.H + n] = v;
     p.xg[r * p.H + n] = f2bf(v * bf2f(p.g[n]));
     sq[n] = v * v;
+  }
+  if (p.cat2) {
+    // the input projection's operand: [embedding; feature of slot - 1], the
+    // feature zero where the target has not verified that slot
+    const int prev = base + j - 1;
+    const bool hasf = live && prev >= s.prefix_len && prev < s.seq_len;
+    const bf16_t* fr = p.feat + ((size_t)b * p.cap + (hasf ? prev : 0)) * p.H;
+    bf16_t* cr = p.cat2 + r * 2 * p.H;
+    for (int n = threadIdx.x; n < p.H; n += blockDim.x) {
+      cr[n] = live ? er[n] : (bf16_t)0;
+      cr[p.H + n] = hasf ? fr[n] : (bf16_t)0;
+    }
   }
   if (live && threadIdx.x < p.D / 2) {
     const int slot = base + j, d = threadIdx.x;
@@ -1130,6 +1144,30 @@ __global__ void k_block_props(SeqState* st, int K, int32_t* out) {
   }
 }
 
+// Conditioning: keep the verify rows' residual stream after a chosen target
+// layer as column block `part` of cat3 (bf16).  grid (H/256, M).
+__global__ void k_capture(const float* x, bf16_t* cat3, int H, int part) {
+  const int m = blockIdx.y, n = blockIdx.x * 256 + threadIdx.x;
+  if (n < H) cat3[(size_t)m * 3 * H + (size_t)part * H + n] = f2bf(x[(size_t)m * H + n]);
+}
+
+// After a commit: the fused features (sum of the k-split partials) of the
+// rows whose inputs were committed become the features of their slots.
+// grid (rows per sequence, B), 256 threads.
+__global__ void k_feat_commit(const SeqState* st, const float* part, int S, int M, int rps, int H, bf16_t* feat,
+                              int cap) {
+  const int j = blockIdx.x, b = blockIdx.y;
+  const SeqState& s = st[b];
+  if (s.count == 0 || j >= s.n_commit) return;   // no verify rows, or row j not committed
+  const int slot = s.seq_len - s.n_commit + j;
+  const size_t m = (size_t)b * rps + j;
+  for (int n = threadIdx.x; n < H; n += blockDim.x) {
+    float v = 0.f;
+    for (int sp = 0; sp < S; ++sp) v += part[((size_t)sp * M + m) * H + n];
+    feat[((size_t)b * cap + slot) * H + n] = f2bf(v);
+  }
+}
+
 // ---------------------------------------------------------------------------
 // host-side launch helpers
 // ---------------------------------------------------------------------------
@@ -1875,6 +1913,42 @@ hipError_t run_layers_persistent(Ctx& c, Model& m, bool draft) {
   return pass_launch(m.pass_args_dev, d.head_dim, draft, c.ncu, c.pass_lds, S(c), t.e0, t.e1);
 }
 
+// A k-split GEMV y = W x over the pass's rows (partial sums into `out`),
+// on the thin kernels or, for the GEMM's row counts, on the batched GEMM.
+hipError_t cond_gemv(Ctx& c, const bf16_t* w, const bf16_t* x, int N, int Kd, int S, float* out) {
+  GemvArgs g = gemv_base(c, c.M, c.R);
+  g.w[0] = w;
+  g.nseg = 1;
+  g.N = N;
+  g.Kd = Kd;
+  g.x = x;
+  g.ldx = Kd;
+  g.splits = S;
+  g.out = out;
+  const double bytes = gemv_bytes(N, Kd, c.M, 4.0 * S);
+  if (c.gemm_rows) return gemm_run(c, EPI_STORE, g, SPEC_KERNEL_OTHER, bytes);
+  const int per_split = std::max(1, std::min(c.ncu / S, N / kTile));
+  return gemv_launch_p<EPI_STORE>(c, g, per_split * S, SPEC_KERNEL_OTHER, bytes);
+}
+
+// Conditioned draft pass: x = e + W_in [e; f] before layer 0, the layer-0
+// norm input rewritten by the finishing kernel of the down projection.
+hipError_t launch_cond_input(Ctx& c, Model& m) {
+  const int H = m.d.hidden;
+  CK(cond_gemv(c, c.w_in, c.cat2, H, 2 * H, kCondSplits, c.part));
+  FinishArgs p{c.st, c.part, kCondSplits, c.M, c.R, H, c.Mpad, 0, c.x, m.L[0].attn_norm, c.xg, c.ss};
+  Timed t(c, SPEC_KERNEL_OTHER, 0);
+  hipExtLaunchKernelGGL(k_down_finish, dim3((H + 255) / 256, c.M), dim3(256), 0, S(c), t.e0, t.e1, 0, p);
+  return hipGetLastError();
+}
+
+// Verify pass: w_fuse [h0; h1; h2] of every row, as k-split partials (the
+// commit keeps the committed rows').
+hipError_t launch_cond_fuse(Ctx& c) {
+  const int H = c.tgt.d.hidden;
+  return cond_gemv(c, c.w_fuse, c.cat3, H, 3 * H, kCondSplits, c.fusedp);
+}
+
 hipError_t launch_forward(Ctx& c, PassMode mode) {
   Model& m = mode == PASS_VERIFY ? c.tgt : c.drf;
   const spec_dims& d = m.d;
@@ -1885,7 +1959,8 @@ hipError_t launch_forward(Ctx& c, PassMode mode) {
     EmbedArgs p{c.st,    c.hist, c.embed,      m.L[0].attn_norm, c.x, persistent ? c.p_xa : c.xg,
                 persistent ? c.p_ssa : c.ss,  c.rcs,
                 c.pos3,  c.cs,   m.axis,       d.hidden,         c.R, c.cap,    (int)mode, c.Mpad,
-                d.head_dim, m.flat ? 1 : 0, c.V, c.mask_token};
+                d.head_dim, m.flat ? 1 : 0, c.V, c.mask_token,
+                (c.cond && mode != PASS_VERIFY) ? c.cat2 : nullptr, c.feat};
     Timed t(c, SPEC_KERNEL_OTHER, 0);
     hipExtLaunchKernelGGL(k_embed, dim3(c.R, c.B), dim3(1024), (size_t)d.hidden * sizeof(float), c.stream, t.e0, t.e1, 0, p);
     CK(hipGetLastError());
@@ -1893,16 +1968,33 @@ hipError_t launch_forward(Ctx& c, PassMode mode) {
   // draft: a draft step, which proposes from each sequence's last row (stored
   // as row b); a block pass runs the LM head over every row, as a verify does
   const bool draft = mode == PASS_DRAFT, block = mode == PASS_BLOCK;
+  if (c.cond && mode != PASS_VERIFY) CK(launch_cond_input(c, m));
+  auto capture = [&](int li) -> hipError_t {   // conditioning: the verify keeps chosen layers' output
+    if (!c.cond || mode != PASS_VERIFY) return hipSuccess;
+    for (int i = 0; i < 3; ++i)
+      if (c.cond_layers[i] == li) {
+        Timed t(c, SPEC_KERNEL_OTHER, 0);
+        hipExtLaunchKernelGGL(k_capture, dim3((d.hidden + 255) / 256, M), dim3(256), 0, S(c), t.e0, t.e1, 0, c.x,
+                              c.cat3, d.hidden, i);
+        CK(hipGetLastError());
+      }
+    return hipSuccess;
+  };
   if (persistent) {
     CK(run_layers_persistent(c, m, draft));
   } else if (c.sg) {
-    for (int li = 0; li < d.layers; ++li) CK(run_layer_sg(c, m, li, block));
+    for (int li = 0; li < d.layers; ++li) {
+      CK(run_layer_sg(c, m, li, block));
+      CK(capture(li));
+    }
   } else {
     for (int li = 0; li < d.layers; ++li) {
       const bool last = li + 1 == d.layers;
       CK(run_layer(c, m, li, last ? m.final_norm : m.L[li + 1].attn_norm, last && draft));
+      CK(capture(li));
     }
   }
+  if (c.cond && mode == PASS_VERIFY) CK(launch_cond_fuse(c));
   if (mode == PASS_CATCHUP) return hipSuccess;   // consumes tokens only: no LM head
   // LM head (+ 1/rms of the final norm) with the fused per-tile argmax; the
   // draft proposes from each sequence's last row only (stored as row b)
@@ -1953,10 +2045,19 @@ hipError_t launch_forward(Ctx& c, PassMode mode) {
 }
 
 hipError_t launch_commit(Ctx& c, int32_t* acc, int32_t* committed, int32_t* ncommit, int32_t* fin) {
-  Timed t(c, SPEC_KERNEL_OTHER, 0);
-  hipExtLaunchKernelGGL(k_commit, dim3(c.B), dim3(1), 0, c.stream, t.e0, t.e1, 0, c.st, c.hist, c.cap, c.K, c.cfg.stop_token,
-                     c.cfg.max_new_tokens, acc, committed, ncommit, fin);
-  return hipGetLastError();
+  {
+    Timed t(c, SPEC_KERNEL_OTHER, 0);
+    hipExtLaunchKernelGGL(k_commit, dim3(c.B), dim3(1), 0, c.stream, t.e0, t.e1, 0, c.st, c.hist, c.cap, c.K,
+                          c.cfg.stop_token, c.cfg.max_new_tokens, acc, committed, ncommit, fin);
+    CK(hipGetLastError());
+  }
+  if (c.cond) {
+    Timed t(c, SPEC_KERNEL_OTHER, 0);
+    hipExtLaunchKernelGGL(k_feat_commit, dim3(c.R, c.B), dim3(256), 0, c.stream, t.e0, t.e1, 0, c.st, c.fusedp,
+                          kCondSplits, c.M, c.R, c.tgt.d.hidden, c.feat, c.cap);
+    CK(hipGetLastError());
+  }
+  return hipSuccess;
 }
 
 hipError_t launch_logits_out(Ctx& c, void* d_logits) {

@@ -106,6 +106,17 @@ bool check_config(const spec_config* cfg, const spec_seq_init* seqs, bool has_dr
     return false;
   }
   if (!check_dims(cfg->target, true, err, "target")) return false;
+  if (cfg->flags & SPEC_FLAG_COND) {
+    if (!has_draft || (cfg->flags & SPEC_FLAG_PERSISTENT)) {
+      err = "SPEC_FLAG_COND needs a draft and runs on the layered path, not with SPEC_FLAG_PERSISTENT";
+      return false;
+    }
+    for (int i = 0; i < 3; ++i)
+      if (cfg->cond_layers[i] < 0 || cfg->cond_layers[i] >= cfg->target.layers) {
+        err = "cond_layers out of range";
+        return false;
+      }
+  }
   if (cfg->flags & SPEC_FLAG_BLOCK_DRAFT) {
     if (!has_draft || cfg->K < 1) {
       err = "SPEC_FLAG_BLOCK_DRAFT needs a draft and K >= 1";
@@ -302,7 +313,9 @@ int pass_splits_for(const spec_dims& d, const Layout& L, int ncu) {
   return 0;
 }
 
-size_t part_elems_for(const Model& m, int M) { return (size_t)std::max(m.s_down, m.s_o) * M * m.d.hidden; }
+size_t part_elems_for(const Model& m, int M) {
+  return (size_t)std::max({m.s_down, m.s_o, kCondSplits}) * M * m.d.hidden;
+}
 
 // The q/k/v, o, gate/up and LM-head GEMVs keep a workgroup's whole reduction
 // (one k-split): their x rows for the full reduction length must fit in LDS,
@@ -359,6 +372,8 @@ size_t carve(Ctx& c, const spec_config* cfg, const spec_seq_init* seqs, bool has
   c.tgt.flat = false;
   c.block_draft = has_draft && (cfg->flags & SPEC_FLAG_BLOCK_DRAFT) != 0;
   c.mask_token = cfg->mask_token;
+  c.cond = has_draft && (cfg->flags & SPEC_FLAG_COND) != 0;
+  for (int i = 0; i < 3; ++i) c.cond_layers[i] = cfg->cond_layers[i];
   c.gemm_rows = gemm_rows_for(cfg, has_draft, L.M);
   set_splits(c.tgt, L.M, c.gemm_rows);
   if (has_draft) {
@@ -409,6 +424,12 @@ size_t carve(Ctx& c, const spec_config* cfg, const spec_seq_init* seqs, bool has
   c.logits = cv.take<bf16_t>((size_t)L.Mpad * L.V);
   c.cls = cv.take<int8_t>((size_t)L.B * L.cap);
   c.rp = cv.take<float>(attn_rows * 4);
+  if (c.cond) {
+    c.cat3 = cv.take<bf16_t>((size_t)L.Mpad * 3 * H);
+    c.fusedp = cv.take<float>((size_t)kCondSplits * L.M * H);
+    c.feat = cv.take<bf16_t>((size_t)L.B * L.cap * H);
+    c.cat2 = cv.take<bf16_t>((size_t)L.Mpad * 2 * H);
+  }
   c.tgt.kv_layer = (size_t)L.pool * t.kv_heads * kAttnChunk * D;
   c.tgt.kc = cv.take<bf16_t>(c.tgt.kv_layer * t.layers);
   c.tgt.vt = cv.take<bf16_t>(c.tgt.kv_layer * t.layers);
@@ -729,7 +750,10 @@ spec_status spec_init(const spec_config* cfg, const void* embed, const spec_mode
     return SPEC_E_INVAL;
   }
   if (!check_weights(target, cfg->target, err, "target") ||
-      (has_draft && !check_weights(draft, cfg->draft, err, "draft"))) {
+      (has_draft && !check_weights(draft, cfg->draft, err, "draft")) ||
+      ((cfg->flags & SPEC_FLAG_COND) && has_draft &&
+       (!draft->w_fuse || !draft->w_in || !aligned16(draft->w_fuse) || !aligned16(draft->w_in)) &&
+       (err = "SPEC_FLAG_COND: draft w_fuse / w_in null or misaligned", true))) {
     g_init_error = err;
     return SPEC_E_INVAL;
   }
@@ -774,6 +798,10 @@ spec_status spec_init(const spec_config* cfg, const void* embed, const spec_mode
     };
     load_model(c.tgt, target);
     if (has_draft) load_model(c.drf, draft);
+    if (c.cond) {
+      c.w_fuse = static_cast<const bf16_t*>(draft->w_fuse);
+      c.w_in = static_cast<const bf16_t*>(draft->w_in);
+    }
     if (hipGetDevice(&c.device) != hipSuccess) c.device = 0;
     init_kernel_attributes();
 
@@ -1069,6 +1097,20 @@ spec_status spec_debug_state(spec_ctx* ctx, int32_t b, int32_t* host_out) {
     HIPCHK(c, hipMemcpy(&s, c.st + b, sizeof s, hipMemcpyDeviceToHost), "state read");
     const int32_t v[8] = {s.seq_len, s.draft_len, s.pending, s.n_gen, s.finished, s.accept_len, s.n_commit, s.err};
     memcpy(host_out, v, sizeof v);
+    return SPEC_OK;
+  });
+}
+
+spec_status spec_debug_feature(spec_ctx* ctx, int32_t b, int32_t slot0, int32_t n, void* host_out) {
+  return guarded(ctx, [&](Ctx& c) -> spec_status {
+    if (!c.cond) return set_err(c, SPEC_E_STATE, "spec_debug_feature: the draft is not conditioned");
+    if (b < 0 || b >= c.B || slot0 < 0 || n < 0 || slot0 + n > c.cap || (n > 0 && !host_out))
+      return set_err(c, SPEC_E_INVAL, "bad arguments");
+    HIPCHK(c, hipStreamSynchronize(c.stream), "sync");
+    const size_t H = c.tgt.d.hidden;
+    HIPCHK(c, hipMemcpy(host_out, c.feat + ((size_t)b * c.cap + slot0) * H, (size_t)n * H * sizeof(bf16_t),
+                        hipMemcpyDeviceToHost),
+           "feature copy");
     return SPEC_OK;
   });
 }

@@ -32,7 +32,8 @@ class Session:
 
     def __init__(self, w, source: str = "host", flags: int = 0, with_draft: bool = True,
                  K: Optional[int] = None, max_new_tokens: Optional[int] = None, stop_token: Optional[int] = None,
-                 provider=None, page_seed: Optional[int] = None, mask_token: Optional[int] = None):
+                 provider=None, page_seed: Optional[int] = None, mask_token: Optional[int] = None,
+                 cond_layers=None):
         torch = _require_gpu()
         import workloads as W
         self.torch = torch
@@ -66,6 +67,14 @@ class Session:
         cfg.stop_token = w.stop_token if stop_token is None else stop_token
         cfg.flags = flags
         cfg.mask_token = w.vocab - 1 if mask_token is None else mask_token   # block proposal's MASK input
+        if cond_layers is not None:   # the draft conditioned on these target layers' hidden states
+            cfg.flags |= B.SPEC_FLAG_COND
+            for i in range(3):
+                cfg.cond_layers[i] = int(cond_layers[i])
+            self.w_fuse = self._tensor("draft", -1, "w_fuse")
+            self.w_in = self._tensor("draft", -1, "w_in")
+            self.drf_struct.w_fuse = self.w_fuse.data_ptr()
+            self.drf_struct.w_in = self.w_in.data_ptr()
         self.cfg = cfg
 
         seqs = (B.spec_seq_init * self.B)()
@@ -195,6 +204,9 @@ class Session:
 
     def positions(self, b: int, length: int):
         return B.spec_debug_positions(self.ctx, b, length)
+
+    def feature(self, b, slot0, n):
+        return B.spec_debug_feature(self.ctx, b, slot0, n, self.w.target.hidden)
 
     def kv(self, b, model, layer, which, pos0, npos):
         shape = self.w.target if model == 0 else self.w.draft

@@ -30,7 +30,7 @@ def test_library_loads_and_exports_every_declared_symbol():
 def test_struct_sizes_match_c_layout():
     # 64-bit SysV layout of the header's structs
     assert ctypes.sizeof(B.spec_dims) == 48
-    assert ctypes.sizeof(B.spec_config) == 124
+    assert ctypes.sizeof(B.spec_config) == 136
     assert ctypes.sizeof(B.spec_seq_init) == 64
     assert ctypes.sizeof(B.spec_layer_weights) == 72
 
