@@ -312,6 +312,42 @@ def batched_scenes(src, K):
             "ar_ms_per_step": round(ar_ms / (T - 1), 3)}
 
 
+def tp4_shard(K, steps=10):
+    """One GPU's share of a 4-way tensor-parallel verify of the same target:
+    7 q heads + 1 kv head, SwiGLU 4736 and 38016 vocabulary rows per GPU, the
+    hidden size unchanged (the all-reduces and the argmax all-gather are not
+    part of it).  Times the shard's verify and its HBM fraction."""
+    import dataclasses
+    import torch
+    import workloads as W
+    from paper_2606_31160_amd import binding as B
+    from paper_2606_31160_amd.harness import Session
+    base = W.get("C3")
+    t = dataclasses.replace(base.target, q_heads=7, kv_heads=1, ffn=4736)
+    w = base.with_(target=t, draft=None, vocab=38016, max_new_tokens=(steps + 4) * (K + 1) + 4)
+    s = Session(w, source="device", provider=W.DeviceWeights(w), with_draft=False)
+    rng = np.random.default_rng(9)
+    dr = torch.tensor(rng.integers(0, w.vocab, size=(steps + 2, K)), dtype=torch.int32, device="cuda")
+    e = [torch.cuda.Event(enable_timing=True) for _ in range(2 * steps)]
+    for r in range(steps + 2):
+        k = r - 2
+        if k >= 0:
+            e[2 * k].record()
+        B.spec_verify(s.ctx, dr[r].data_ptr(), 0)
+        if k >= 0:
+            e[2 * k + 1].record()
+        B.spec_commit(s.ctx, 0, 0, 0, 0)
+    torch.cuda.synchronize()
+    v_us = float(np.median([e[2 * k].elapsed_time(e[2 * k + 1]) for k in range(steps)])) * 1e3
+    n_ctx = w.seqs[0].prefix_len + (steps // 2 + 2)
+    by = verify_bytes(w, n_ctx)
+    s.close()
+    return {"shard": "7/1 heads, FFN 4736, vocab 38016 of 28/4, 18944, 152064 (TP=4), hidden 3584, 28 layers, "
+                     "9 rows, prompt 4096",
+            "verify_us": round(v_us, 1), "bytes": int(by),
+            "hbm_frac": round(by / (v_us * 1e-6) / 1e9 / PEAK_HBM_GBS, 4)}
+
+
 def pmc_pass(rounds, K):
     """Rounds of the timed workload, launched kernel by kernel, for counter
     collection; prints one line per round."""
@@ -582,6 +618,9 @@ def main():
     if not args.no_batched:
         log("16-scene workload ...")
         out["batched_16_scenes"] = batched_scenes(src, K)
+    if not args.no_batched:
+        log("tensor-parallel shard ...")
+        out["tp4_shard"] = tp4_shard(K)
     cp = copy_peak_gbs()
     out["copy_peak_gbs"] = round(cp, 1)
     out["verify_frac_of_copy_peak"] = round(v_bytes / (v_us * 1e-6) / 1e9 / cp, 4)
