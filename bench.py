@@ -174,10 +174,17 @@ def cpu_baseline(w, src, tokens_per_round, K):
         return t_sample * (f_layers * layers_full / layers_sample + (1 - f_layers) * frac_v)
 
     round_s = K * scaled(t_draft, dl, w.draft.layers, w.draft) + scaled(t_verify, tl, w.target.layers, w.target)
+    model = "unknown"
+    try:
+        with open("/proc/cpuinfo") as f:
+            model = next((ln.split(":", 1)[1].strip() for ln in f if ln.startswith("model name")), model)
+    except OSError:
+        pass
     return {
         "value": tokens_per_round / round_s,
         "unit": "tokens/s",
         "cores": int(threads),
+        "cpu": model,
         "kind": "oracle",
         "sample": (f"float64 numpy oracle: one verify of {K + 1} rows over the {lay.prefix_len}-token prompt through "
                    f"{tl} of {w.target.layers} target layers + 1/{frac_v} of the LM head ({t_verify:.2f} s), one "
