@@ -51,16 +51,20 @@ constexpr int NL = kLoadWaves * 64;           // loader threads
 constexpr int kYStride = 17;                  // floats per row of an output tile in LDS
 
 // Step groups (32-wide k-steps per chunk, one MFMA wave pair each) and chunks
-// of loads in flight, by 16-row blocks: up to 5 blocks 4 groups and 5
-// chunks (12 waves, 168 registers each); from 6 blocks, whose accumulators
-// need more registers, 2 groups (8 waves, 256 registers each) and 8 chunks.
+// of loads in flight, by 16-row blocks: up to 3 blocks 2 groups and 8 chunks
+// (8 waves of at most 128 registers: two workgroups per CU); 4-5 blocks 4
+// groups and 5 chunks (12 waves, 168 registers each); from 6 blocks, whose
+// accumulators need more registers, 2 groups and 8 chunks (8 waves of 256).
 // The compiler waits for all of a wave's loads once per round of kStages
 // chunks, so a deep round is what keeps enough bytes in flight per CU.
-constexpr int steps_for(int mb) { return mb >= 6 ? 2 : 4; }
-constexpr int stages_for(int mb) { return mb >= 6 ? 8 : 5; }
+constexpr int steps_for(int mb) { return (mb >= 6 || mb <= 3) ? 2 : 4; }
+constexpr int stages_for(int mb) { return (mb >= 6 || mb <= 3) ? 8 : 5; }
 constexpr int threads_for(int mb) { return (2 * steps_for(mb) + kLoadWaves) * 64; }
 constexpr int xstride_for(int mb) { return 32 * steps_for(mb) + 8; }   // bf16 per LDS x row (16-byte pad)
 static_assert(kGemmTiles == 4, "MFMA wave w = 2q + p: tile pair p, step group q");
+// Sums of squares each thread of the 1/rms prologue loads, with `parts`
+// threads per row: enough for hidden 8192 (512 sums) where registers allow.
+constexpr int lpt_for(int parts) { return (512 + parts - 1) / parts < 96 ? (512 + parts - 1) / parts : 96; }
 
 // two x buffers of 16 mb rows plus a spare row each (the target of loader
 // stores past the last row, so that no branch skips a store)
@@ -158,7 +162,7 @@ __global__ __launch_bounds__(threads_for(MB)) void k_gemm(GemvArgs a) {
   // added in order.  inv_rms is read after the K loop's barriers.
   if constexpr (kNorm) {
     constexpr int P = NT / ROWS;              // parts per row (>= 3)
-    constexpr int LPT = 96;                   // loads per thread (H/16 <= LPT * P, checked on the host)
+    constexpr int LPT = lpt_for(P);           // loads per thread (H/16 <= LPT * P, checked on the host)
     const int nt = a.H / kTile, per = (nt + P - 1) / P;
     const int m = threadIdx.x % ROWS, p = threadIdx.x / ROWS;
     float v[LPT];
@@ -457,11 +461,12 @@ hipError_t gemm_launch(int epi, const GemvArgs& g, hipStream_t s, hipEvent_t e0,
   if (g.M <= kSgMaxRowsGemm || g.M > SPEC_MAX_ROWS || g.splits < 1 || (epi != EPI_STORE && g.splits != 1) ||
       g.N % kTile != 0 || g.Kd % 8 != 0)
     return hipErrorInvalidValue;
-  // the 1/rms prologue reads at most 96 sums of squares per thread, in
-  // threads_for / rows parts per row
+  // the 1/rms prologue reads at most lpt_for(parts) sums of squares per
+  // thread, in threads_for / rows parts per row
   {
     const int mb = (g.M + 15) / 16, parts = threads_for(mb) / (16 * mb);
-    if ((epi == EPI_ROPE || epi == EPI_SWIGLU || epi == EPI_ARGMAX) && (g.H < kTile || g.H / kTile > 96 * parts))
+    if ((epi == EPI_ROPE || epi == EPI_SWIGLU || epi == EPI_ARGMAX) &&
+        (g.H < kTile || g.H / kTile > lpt_for(parts) * parts))
       return hipErrorInvalidValue;
   }
   // every operand is addressed with 32-bit byte offsets below kOut
