@@ -490,4 +490,35 @@ int gemm_down_splits(int N, int Kd, int ncu) {
   return std::max(1, std::min(s, T / 8));   // at least 8 k-steps per split
 }
 
+int gemm_wgs_per_cu(int M) {
+  // only the 8-wave shape of up to three row blocks is sized for two
+  // workgroups per CU; the wider ones keep one, so that their (larger) k-split
+  // partials do not double
+  const int mb = (M + 15) / 16;
+  const void* f = nullptr;
+  switch (mb) {
+    case 2: f = reinterpret_cast<const void*>(&k_gemm<2, EPI_STORE>); break;
+    case 3: f = reinterpret_cast<const void*>(&k_gemm<3, EPI_STORE>); break;
+    default: return 1;
+  }
+  int n = 0;
+  const size_t lds = gemm_lds_bytes(M);
+  if (hipFuncSetAttribute(f, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds) != hipSuccess ||
+      hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, f, threads_for(mb), lds) != hipSuccess) {
+    (void)hipGetLastError();
+    return 1;
+  }
+  return std::max(1, std::min(n, 2));
+}
+
+int gemm_qkv_splits(int N, int Kd, int M, int ncu) {
+  const int groups = (N + kGemmTiles * kTile - 1) / (kGemmTiles * kTile);
+  if (2 * groups >= ncu) return 1;
+  // one workgroup per CU: measured faster here than filling both slots, as
+  // the doubled partials outweigh the extra streams
+  const int s = gemm_down_splits(N, Kd, ncu);
+  // 2 * s * M * N fp32 partial bytes <= (N * Kd bf16 weight bytes) / 10
+  return (long long)40 * s * M <= Kd ? s : 1;
+}
+
 }  // namespace specdec

@@ -68,5 +68,14 @@ void gemm_set_attributes(int limit);
 hipError_t gemm_launch(int epi, const GemvArgs& g, hipStream_t s, hipEvent_t e0, hipEvent_t e1);
 // k-splits of an EPI_STORE GEMM (the down projection) over N outputs and Kd inputs.
 int gemm_down_splits(int N, int Kd, int ncu);
+// Workgroups of the k-split GEMM over M rows resident per CU: the runtime's
+// occupancy for the shapes of up to three row blocks (at most 2), else 1;
+// the o and down projections split to fill every resident slot once.
+int gemm_wgs_per_cu(int M);
+// k-splits of the q/k/v GEMM over M rows: 1 (one launch with the fused rotary
+// epilogue) unless its workgroups cover under half the CUs and the fp32
+// partials it writes and reads back stay under a tenth of its weight bytes;
+// a split launch is finished by k_qkv_finish (kernels.hip).
+int gemm_qkv_splits(int N, int Kd, int M, int ncu);
 
 }  // namespace specdec

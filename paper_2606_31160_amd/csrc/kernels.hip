@@ -656,6 +656,66 @@ __global__ __launch_bounds__(256) void k_down_finish(FinishArgs p) {
   if ((n & 15) == 0) p.ss[(size_t)(n >> 4) * p.mpad + out] = sq;
 }
 
+// Finish of a k-split q/k/v GEMM: per live row m and column pair (2i, 2i+1),
+// the split partials are added, scaled by the row's 1/rms (the attention
+// RMSNorm, whose gain is already in the bf16 input), rotated by the row's
+// (cos, sin) when the pair belongs to a q or k head (Sec. 3.3, Eq. rope-3d),
+// and stored as the fused rotary epilogue stores them: q rows, key pages and
+// transposed value pages.  grid (ceil(N/2 / 256), M), 256 threads.
+struct QkvFinishArgs {
+  const SeqState* st;
+  const float* part;     // [S][M][N]
+  int S, M, N, rps, mpad, H;
+  float eps;
+  const float* ss;       // [H/16][mpad] sums of x^2 of the input rows
+  const float2* rcs;     // [Mpad][D/2]
+  const int32_t* pt;     // [B][pps]
+  int nq, nkv, D, pps;
+  bf16_t* q;             // [M][nq*D]
+  bf16_t *kc, *vt;       // layer bases of the paged key / value pools
+};
+
+__global__ __launch_bounds__(256) void k_qkv_finish(QkvFinishArgs a) {
+  __shared__ float inv_rms;
+  const int m = blockIdx.y;
+  const int b = m / a.rps, j = m - b * a.rps;
+  if (j >= a.st[b].count) return;                 // uniform over the workgroup
+  if (threadIdx.x < 64) {
+    float v = 0.f;
+    for (int t = threadIdx.x; t < a.H / kTile; t += 64) v += a.ss[(size_t)t * a.mpad + m];
+    for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
+    if (threadIdx.x == 0) inv_rms = rsqrtf(v / a.H + a.eps);
+  }
+  __syncthreads();
+  const int pr = blockIdx.x * 256 + threadIdx.x;
+  if (pr >= a.N / 2) return;
+  float e = 0.f, o = 0.f;
+  for (int sp = 0; sp < a.S; ++sp) {
+    const float2 v = *reinterpret_cast<const float2*>(a.part + ((size_t)sp * a.M + m) * a.N + 2 * pr);
+    e += v.x;
+    o += v.y;
+  }
+  e *= inv_rms;
+  o *= inv_rms;
+  const int n = 2 * pr, head = n / a.D, d = (n % a.D) >> 1;
+  const int slot = a.st[b].base + j;
+  if (head < a.nq + a.nkv) {
+    const float2 cs = a.rcs[(size_t)m * (a.D / 2) + d];
+    const float re = e * cs.x - o * cs.y, ro = e * cs.y + o * cs.x;
+    if (head < a.nq) {
+      *reinterpret_cast<uint32_t*>(a.q + ((size_t)m * a.nq + head) * a.D + 2 * d) = pack2(re, ro);
+    } else {
+      const size_t pg = (size_t)a.pt[b * a.pps + slot / kAttnChunk] * a.nkv + (head - a.nq);
+      *reinterpret_cast<uint32_t*>(a.kc + (pg * kAttnChunk + slot % kAttnChunk) * a.D + 2 * d) = pack2(re, ro);
+    }
+  } else {
+    const size_t pg = (size_t)a.pt[b * a.pps + slot / kAttnChunk] * a.nkv + (head - a.nq - a.nkv);
+    bf16_t* vp = a.vt + (pg * a.D + 2 * d) * kAttnChunk + slot % kAttnChunk;
+    vp[0] = f2bf(e);
+    vp[kAttnChunk] = f2bf(o);
+  }
+}
+
 // ---------------------------------------------------------------------------
 // Split-KV causal grouped-query attention on MFMA.
 //
@@ -1419,7 +1479,19 @@ hipError_t run_layer(Ctx& c, Model& m, int li, const bf16_t* next_gain, bool sel
     g.pt = c.pt;
     g.pps = c.pps;
     g.pw = pk;
-    if (c.gemm_rows)
+    const int sq = c.gemm_rows ? gemm_qkv_splits(g.N, H, M, c.ncu) : 1;
+    if (sq > 1) {
+      // too few 64-column workgroups to stream the matrix at full rate: k-split
+      // partial sums, then the norm, rotation and cache append in k_qkv_finish
+      g.splits = sq;
+      g.out = c.part;
+      CK(gemm_run(c, EPI_STORE, g, SPEC_KERNEL_QKV, gemv_bytes(g.N, H, M, 4.0 * sq)));
+      QkvFinishArgs p{c.st, c.part, sq, M, g.N, c.R, c.Mpad, H, d.rms_eps, c.ss, c.rcs, c.pt,
+                      nq, nkv, D, c.pps, c.q, kc, vt};
+      Timed t(c, SPEC_KERNEL_OTHER, 0);
+      hipExtLaunchKernelGGL(k_qkv_finish, dim3((g.N / 2 + 255) / 256, M), dim3(256), 0, S(c), t.e0, t.e1, 0, p);
+      CK(hipGetLastError());
+    } else if (c.gemm_rows)
       CK(gemm_run(c, EPI_ROPE, g, SPEC_KERNEL_QKV, gemv_bytes(g.N, H, M, 2.0)));
     else
       CK((gemv_launch<EPI_ROPE, 1>(c, g, SPEC_KERNEL_QKV, gemv_bytes(g.N, H, M, 2.0))));

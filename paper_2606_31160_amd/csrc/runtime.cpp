@@ -280,8 +280,9 @@ Layout make_layout(const spec_config* cfg, const spec_seq_init* seqs) {
 }
 
 void set_splits(Model& m, int M, bool gemm_rows) {
-  m.s_down = gemm_rows ? gemm_down_splits(m.d.hidden, m.d.ffn, num_cus()) : down_splits(M, m.d.ffn, num_cus());
-  m.s_o = gemm_rows ? gemm_down_splits(m.d.hidden, m.d.q_heads * m.d.head_dim, num_cus()) : 1;
+  const int slots = gemm_rows ? num_cus() * gemm_wgs_per_cu(M) : num_cus();
+  m.s_down = gemm_rows ? gemm_down_splits(m.d.hidden, m.d.ffn, slots) : down_splits(M, m.d.ffn, num_cus());
+  m.s_o = gemm_rows ? gemm_down_splits(m.d.hidden, m.d.q_heads * m.d.head_dim, slots) : 1;
 }
 
 // Down-projection k-splits of the persistent pass for one model: the fewest
@@ -314,7 +315,14 @@ int pass_splits_for(const spec_dims& d, const Layout& L, int ncu) {
 }
 
 size_t part_elems_for(const Model& m, int M) {
-  return (size_t)std::max({m.s_down, m.s_o, kCondSplits}) * M * m.d.hidden;
+  // a pass of fewer rows may split the q/k/v GEMM where one of M rows does not
+  const int nqkv = (m.d.q_heads + 2 * m.d.kv_heads) * m.d.head_dim;
+  size_t qkv = 0;
+  for (int r = 1; r <= M; ++r) {
+    const int sq = gemm_qkv_splits(nqkv, m.d.hidden, r, num_cus());
+    if (sq > 1) qkv = std::max(qkv, (size_t)sq * r * nqkv);
+  }
+  return std::max((size_t)std::max({m.s_down, m.s_o, kCondSplits}) * M * m.d.hidden, qkv);
 }
 
 // The q/k/v, o, gate/up and LM-head GEMVs keep a workgroup's whole reduction
