@@ -9,7 +9,9 @@ are re-encoded causally in the next round.
     K/V, and a second round after accepted proposals (the catch-up);
   * the speculative loop with block proposals commits exactly greedy decoding
     (tiny, and 16 tiny scenes whose 80-row passes run on the batched GEMM);
-  * the 2-layer draft at 7B width over the 3328-token prompt against the oracle.
+  * the 2-layer draft at 7B width over the 3328-token prompt against the oracle;
+  * three scenes at the paper backbone's width with K = 16: the speculative loop
+    with block proposals commits exactly greedy decoding.
 """
 import numpy as np
 import pytest
@@ -131,6 +133,38 @@ def test_block_sixteen_scenes_gemm_equals_greedy():
                 done[b] = bool(fin[b])
     ref.close()
     s = _session(w, provider=hp, page_seed=21)
+    spec = _loop(s)
+    s.close()
+    assert spec == outs
+
+
+def test_block_paper_width_three_scenes_equals_greedy():
+    """Hidden 4096, 32/8 heads, K = 16, three scenes: the 51-row verify and block
+    passes keep the q/k/v GEMM in one split, while passes of 17..34 rows would
+    take its k-split route (too few workgroups), so its partial buffer must
+    cover pass row counts below the context's largest.  The greedy reference is
+    taken at the verify's pass shape, as above."""
+    import dataclasses
+    base = W.get("C6")
+    w = base.with_(target=dataclasses.replace(base.target, layers=2), vocab=2048, max_new_tokens=24,
+                   seqs=tuple(W.c5_layout(p) for p in (1100, 1400, 1700)), p_accept=(0.8, 0.8, 0.8))
+    src = W.DeviceWeights(w)
+    from paper_2606_31160_amd.harness import Session
+    ref = Session(w, source="device", provider=src, page_seed=21)
+    rng = np.random.default_rng(5)
+    outs = [[] for _ in range(w.batch)]
+    done = [False] * w.batch
+    while not all(done):
+        ref.verify(rng.integers(0, w.vocab, size=(w.batch, w.K)).astype(np.int32))
+        ref.commit()
+        coms, acc, fin = ref.committed()
+        for b in range(w.batch):
+            if not done[b]:
+                outs[b] += [int(t) for t in coms[b]]
+                done[b] = bool(fin[b])
+    ref.close()
+    assert all(len(o) == w.max_new_tokens for o in outs)
+    s = _session(w, source="device", provider=src, page_seed=21)
     spec = _loop(s)
     s.close()
     assert spec == outs
