@@ -44,22 +44,6 @@ def verify_bytes(w, n_ctx):
     return t.layers * layer_w + 2 * w.vocab * t.hidden + (n_ctx + w.K + 1) * kv_row + (w.K + 1) * kv_row
 
 
-def pass_layers_bytes(w, n_ctx):
-    """Algorithmic HBM bytes of the persistent kernel of one verify (every
-    layer, no LM head): all layer weights once, the cached K/V of n_ctx slots
-    read once, K+1 new K/V rows written, the M activation rows in and out of
-    every projection."""
-    t = w.target
-    D = t.head_dim
-    M = w.K + 1
-    layer_w = 2 * (t.hidden * (t.q_heads + 2 * t.kv_heads) * D + t.q_heads * D * t.hidden
-                   + 3 * t.hidden * t.ffn + 2 * t.hidden)
-    acts = 2 * M * (t.hidden + (t.q_heads + 2 * t.kv_heads) * D + t.q_heads * D + t.hidden
-                    + t.hidden + 2 * t.ffn + t.ffn + t.hidden)
-    kv_row = t.kv_heads * D * 2 * 2
-    return t.layers * (layer_w + acts + (n_ctx + M) * kv_row)
-
-
 def draft_step_bytes(w, n_ctx):
     d = w.draft
     D = d.head_dim
@@ -70,8 +54,6 @@ def draft_step_bytes(w, n_ctx):
 
 
 CSRC = os.path.join(ROOT, "paper_2606_31160_amd", "csrc")
-TRAFFIC_PASS = os.path.join(ROOT, "profiles", "k_pass_7b_verify_hbm_traffic.txt")
-PASS_SOURCES = [os.path.join(CSRC, f) for f in ("pass.hip", "pass.h", "device.h", "ctx.h")]
 TRAFFIC_GATEUP = os.path.join(ROOT, "profiles", "k_sgemv_swiglu_7b_verify_hbm_traffic.txt")
 GATEUP_SOURCES = [os.path.join(CSRC, f) for f in ("sgemv.hip", "sgemv.h", "device.h", "ctx.h")]
 
@@ -568,12 +550,12 @@ def main():
     for r in range(args.warmup + args.steps, rounds_total - 1):
         round_(r)
     kernels = {}
-    for kind in ("pass_target", "pass_draft", "qkv", "o", "gateup", "down", "lmhead", "attn", "other"):
+    for kind in ("qkv", "o", "gateup", "down", "lmhead", "attn", "other"):
         n, ms, by = B.spec_timing_read(s.ctx, kind)
         if n == 0:
             continue
         kernels[kind] = {"launches": int(n), "avg_us": round(ms * 1e3 / n, 2)}
-        if by > 0 and not kind.startswith("pass"):
+        if by > 0:
             kernels[kind]["bytes_per_launch"] = round(by / n)
             kernels[kind]["gbs"] = round(by / (ms * 1e-3) / 1e9, 1)
     B.spec_timing(s.ctx, False)
@@ -581,19 +563,11 @@ def main():
     # context length of the timing pass's verifies (slots read by attention)
     t_rounds = range(args.warmup + args.steps, rounds_total - 1)
     ctx_t = [n_prompt + sum(commits[:r]) for r in t_rounds]
-    if "pass_target" in kernels:
-        dom = kernels["pass_target"]
-        dom["bytes_per_launch"] = round(float(np.mean([pass_layers_bytes(w, n) for n in ctx_t])))
-        dom["gbs"] = round(dom["bytes_per_launch"] / (dom["avg_us"] * 1e-6) / 1e9, 1)
-        dom_name = ("k_pass (persistent verify: all 28 target layers in one launch; weight streaming GEMVs with "
-                    "fused norm/rotary/SwiGLU/residual, split-KV attention)")
-        dom_traffic = measured_traffic(TRAFFIC_PASS, PASS_SOURCES)
-    else:
-        dom = kernels["gateup"]
-        dom_name = ("k_sgemv<SG_SWIGLU>: fused gate/up projection + SwiGLU over tile-packed weights "
-                    "(gate/up tile pairs dealt round-robin, 15 load-only worker waves + a control wave), "
-                    "2x18944x3584 bf16 weights")
-        dom_traffic = measured_traffic(TRAFFIC_GATEUP, GATEUP_SOURCES)
+    dom = kernels["gateup"]
+    dom_name = ("k_sgemv<SG_SWIGLU>: fused gate/up projection + SwiGLU over tile-packed weights "
+                "(gate/up tile pairs dealt round-robin, 15 load-only worker waves + a control wave), "
+                "2x18944x3584 bf16 weights")
+    dom_traffic = measured_traffic(TRAFFIC_GATEUP, GATEUP_SOURCES)
     log("per-kernel timing: " + json.dumps(kernels))
 
     n_ctx = n_prompt + expect // 2

@@ -76,10 +76,7 @@ typedef struct spec_dims {
 } spec_dims;
 
 #define SPEC_FLAG_NO_GRAPHS 1      /* launch kernels one by one instead of replaying HIP graphs */
-#define SPEC_FLAG_PERSISTENT 2     /* run all layers of a pass in the persistent pass kernel when the
-                                      shapes allow it (else one kernel per layer step) */
-#define SPEC_FLAG_PASS_TIMELINE 4  /* the persistent pass kernel records per-phase wall-clock stamps
-                                      (see spec_debug_pass_timeline); adds a small cost */
+/* (values 2 and 4 are not used; unknown flag bits are rejected with SPEC_E_INVAL) */
 #define SPEC_FLAG_ROWMAJOR 8       /* stream the caller's row-major weights directly.  Without it, passes
                                       on the layered path of at most 16 rows (batch*(K+1) <= 16), or of
                                       rows the batched-row GEMM takes, stream a tile-packed copy of every
@@ -90,7 +87,7 @@ typedef struct spec_dims {
                                       the pending row attending causally and every MASK row attending to
                                       the prefix and the whole block; MASK row i proposes d_i.  Accepted
                                       proposals of the previous round are first re-encoded causally.
-                                      Needs a draft; not with SPEC_FLAG_PERSISTENT. */
+                                      Needs a draft. */
 #define SPEC_FLAG_COND 64          /* the draft is conditioned on target hidden states (Sec. 4.1; fused
                                       EAGLE-3 style, Sec. 5): every verify keeps the target's residual
                                       stream after layers cond_layers[0..2]; for the rows whose inputs get
@@ -98,7 +95,7 @@ typedef struct spec_dims {
                                       slot's feature, and a draft row at slot t takes the layer-0 input
                                       e + w_in [e; f(t-1)] (2*hidden -> hidden; f = 0 where no verified
                                       feature exists: prompt slots and the draft's proposal rows).
-                                      Needs a draft with w_fuse and w_in; not with SPEC_FLAG_PERSISTENT. */
+                                      Needs a draft with w_fuse and w_in. */
 #define SPEC_FLAG_DRAFT_MROPE 16   /* the draft rotates with 3D M-RoPE (its own mrope_section and
                                       interleaved, validated as the target's) instead of FlatRoPE: the
                                       comparison arm of the attention-budget readout (Sec. 4.2) */
@@ -247,7 +244,7 @@ spec_status spec_commit(spec_ctx* ctx, int32_t* d_accept_len, int32_t* d_committ
  * Rows a pass does not run (finished sequences, rows past a draft pass's
  * count) are left unchanged.  The armed pass is launched kernel by kernel
  * (no graph replay); the readout then disarms.  d_out = NULL disarms.
- * Not available on the persistent pass kernel (SPEC_E_STATE).  Any state. */
+ * Any state. */
 spec_status spec_attn_readout(spec_ctx* ctx, int32_t model, int32_t layer, float* d_out);
 
 /* Synchronising: waits for the stream, then reports how many sequences have
@@ -286,22 +283,10 @@ spec_status spec_debug_feature(spec_ctx* ctx, int32_t b, int32_t slot0, int32_t 
 
 /* Execution path of the context's passes into *path:
  * SPEC_PATH_ROWMAJOR (one kernel per layer step over the caller's row-major weights),
- * SPEC_PATH_PACKED (one kernel per layer step over the tile-packed weight copy),
- * SPEC_PATH_PERSISTENT (the persistent pass kernel). */
+ * SPEC_PATH_PACKED (one kernel per layer step over the tile-packed weight copy). */
 #define SPEC_PATH_ROWMAJOR 0
 #define SPEC_PATH_PACKED 1
-#define SPEC_PATH_PERSISTENT 2
 spec_status spec_debug_path(const spec_ctx* ctx, int32_t* path);
-
-/* Wall-clock stamps of the most recent persistent pass (context created with
- * SPEC_FLAG_PASS_TIMELINE; synchronising).  host_out receives
- * [events][workgroups] unsigned 64-bit ticks of the device's constant-rate
- * clock (*tick_hz per second); events = 1 + 12 * layers of the pass's model:
- * the start, then for each layer and phase (QKV, attention, combine, O,
- * gate/up, down) the workgroup's work done and its next barrier passed.
- * *n_events and *n_workgroups describe the layout; capacity is in elements. */
-spec_status spec_debug_pass_timeline(spec_ctx* ctx, int32_t model, unsigned long long* host_out, int64_t capacity,
-                                     int32_t* n_events, int32_t* n_workgroups, double* tick_hz);
 
 /* Per-kernel timing with HIP events on the context's stream.  While enabled,
  * calls launch kernels one by one (no graph replay), each through
@@ -320,9 +305,7 @@ enum spec_kernel_kind {
   SPEC_KERNEL_LMHEAD = 4,    /* tied LM head with the fused per-tile argmax */
   SPEC_KERNEL_ATTN = 5,      /* split-KV attention */
   SPEC_KERNEL_OTHER = 6,     /* embed, attention combine, down reduction, accept, commit */
-  SPEC_KERNEL_PASS_TARGET = 7, /* persistent kernel running every layer of a verify pass */
-  SPEC_KERNEL_PASS_DRAFT = 8,  /* persistent kernel running every layer of a draft step */
-  SPEC_KERNEL_KINDS = 9
+  SPEC_KERNEL_KINDS = 7
 };
 spec_status spec_timing(spec_ctx* ctx, int32_t enable);
 spec_status spec_timing_read(spec_ctx* ctx, int32_t kind, int64_t* launches, double* ms, double* bytes);

@@ -21,16 +21,13 @@ SPEC_MAX_BATCH = 16
 SPEC_MAX_ROWS = 160
 SPEC_KV_PAGE = 64
 SPEC_FLAG_NO_GRAPHS = 1
-SPEC_FLAG_PERSISTENT = 2
-SPEC_FLAG_PASS_TIMELINE = 4
 SPEC_FLAG_ROWMAJOR = 8
 SPEC_FLAG_DRAFT_MROPE = 16
 SPEC_FLAG_BLOCK_DRAFT = 32
 SPEC_FLAG_COND = 64
 STATUS = {0: "SPEC_OK", 1: "SPEC_E_INVAL", 2: "SPEC_E_STATE", 3: "SPEC_E_CAPACITY", 5: "SPEC_E_HIP",
           6: "SPEC_E_NUMERIC"}
-KERNEL_KINDS = {"qkv": 0, "o": 1, "gateup": 2, "down": 3, "lmhead": 4, "attn": 5, "other": 6,
-                "pass_target": 7, "pass_draft": 8}
+KERNEL_KINDS = {"qkv": 0, "o": 1, "gateup": 2, "down": 3, "lmhead": 4, "attn": 5, "other": 6}
 
 
 class spec_dims(Structure):
@@ -97,8 +94,6 @@ def lib():
             "spec_debug_kv": [P, c_int32, c_int32, c_int32, c_int32, c_int32, c_int32, P],
             "spec_timing": [P, c_int32],
             "spec_timing_read": [P, c_int32, POINTER(c_int64), POINTER(c_double), POINTER(c_double)],
-            "spec_debug_pass_timeline": [P, c_int32, P, c_int64, POINTER(c_int32), POINTER(c_int32),
-                                         POINTER(c_double)],
             "spec_debug_path": [P, POINTER(c_int32)],
             "spec_debug_feature": [P, c_int32, c_int32, c_int32, P],
         }
@@ -205,7 +200,7 @@ def spec_debug_kv(ctx, b: int, model: int, layer: int, which: int, pos0: int, np
     return out
 
 
-PATHS = {0: "rowmajor", 1: "packed", 2: "persistent"}
+PATHS = {0: "rowmajor", 1: "packed"}
 
 
 def spec_debug_feature(ctx, b: int, slot0: int, n: int, hidden: int):
@@ -231,19 +226,6 @@ def spec_timing_read(ctx, kind: str):
     _check(lib().spec_timing_read(ctx, KERNEL_KINDS[kind], ctypes.byref(n), ctypes.byref(ms), ctypes.byref(by)),
            "spec_timing_read", ctx)
     return n.value, ms.value, by.value
-
-
-def spec_debug_pass_timeline(ctx, model: int):
-    """Stamps of the last persistent pass of `model` (0 target, 1 draft):
-    (uint64 array [events][workgroups], ticks per second)."""
-    import numpy as np
-    ne, nw, hz = c_int32(0), c_int32(0), c_double(0)
-    _check(lib().spec_debug_pass_timeline(ctx, model, None, 0, ctypes.byref(ne), ctypes.byref(nw), ctypes.byref(hz)),
-           "spec_debug_pass_timeline", ctx)
-    out = np.zeros((ne.value, nw.value), dtype=np.uint64)
-    _check(lib().spec_debug_pass_timeline(ctx, model, out.ctypes.data, out.size, None, None, None),
-           "spec_debug_pass_timeline", ctx)
-    return out, hz.value
 
 
 def dims(shape, layers=None) -> spec_dims:

@@ -13,8 +13,6 @@
 namespace specdec {
 
 typedef uint16_t bf16_t;
-struct PassArgs;
-struct GemvJob;
 struct SgJob;
 
 constexpr int kMaxRows = SPEC_MAX_K + 1;     // rows per sequence in one pass
@@ -51,7 +49,7 @@ struct SeqState {
   int32_t props[kMaxRows];      // the draft's own proposals this round
 };
 
-enum { ERR_TOKEN = 1, ERR_NUMERIC = 2, ERR_STATE = 4, ERR_SYNC = 8 };
+enum { ERR_TOKEN = 1, ERR_NUMERIC = 2, ERR_STATE = 4 };
 
 constexpr int kCondSplits = 4;   // k-splits of the feature fusion (3H inputs) and of the input projection
 
@@ -74,12 +72,6 @@ struct Model {
   int8_t* axis = nullptr;           // [head_dim/2] axis (0 T, 1 H, 2 W) of each rotary pair
   int s_down = 1;                  // k-splits of the down projection
   int s_o = 1;                     // k-splits of the o projection on the batched-row GEMM
-  int pass_splits = 1;             // k-splits of the down projection in the persistent pass
-  LayerW* lw_dev = nullptr;        // [layers] device copy of L (persistent pass)
-  PassArgs* pass_args_dev = nullptr;   // device copy of this model's pass arguments
-  GemvJob* jobs_dev = nullptr;         // [layers][kPassJobs] GEMV phases of the pass
-  PassArgs* largs_dev = nullptr;       // layered path: arguments of the one-phase GEMV kernels
-  GemvJob* ljobs_dev = nullptr;        // layered path: [layers][kPassJobs] (gate/up and down used)
   size_t kv_layer = 0;              // elements of one layer's key (or value) cache
   // tile-packed weights (sgemv.h) of every layer: q/k/v, o, gate/up pairs, down
   bf16_t* pk = nullptr;
@@ -102,7 +94,7 @@ struct Ctx {
   int pool = 0;                      // cache pages per layer
   std::vector<int32_t> pt_host;      // [B][pps] physical page of each sequence page
   std::vector<int32_t> npages;       // [B] pages each sequence owns
-  int ncu = 256;                     // compute units of the device (persistent GEMV grids)
+  int ncu = 256;                     // compute units of the device (GEMV grids)
   hipStream_t stream = nullptr;      // caller's stream
   hipStream_t cap_stream = nullptr;  // private stream used only for graph capture
   int device = 0;
@@ -154,17 +146,6 @@ struct Ctx {
   bf16_t* feat = nullptr;            // [B][cap][H] fused feature of every verified slot
   bf16_t* cat2 = nullptr;            // [Mpad][2H] draft rows' [embedding; feature of the previous slot]
 
-  // persistent pass (pass.hip): per-layer activations, barrier words
-  bool use_pass = false;
-  size_t pass_lds = 0;
-  size_t ljob_lds = 0;              // dynamic LDS of the layered path's one-phase GEMV kernels
-  int pass_layers = 0;              // max layers over the models
-  bf16_t *p_xa = nullptr, *p_xf = nullptr, *p_q = nullptr, *p_o = nullptr, *p_u = nullptr;
-  float *p_ssa = nullptr, *p_ssf = nullptr, *p_part = nullptr;
-  unsigned* p_bar = nullptr;
-  size_t p_x_layer = 0, p_ss_layer = 0, p_q_layer = 0, p_u_layer = 0;
-  unsigned long long* p_timeline = nullptr;   // SPEC_FLAG_PASS_TIMELINE
-
   // host state machine
   enum Phase { READY = 0, DRAFTING = 1, VERIFIED = 2 } phase = READY;
   int dsteps = 0;
@@ -206,10 +187,6 @@ struct Ctx {
 // Each returns hipSuccess or the launch error.
 
 hipError_t launch_zero(Ctx& c, void* p, size_t bytes);
-// Uploads the persistent pass's arguments and GEMV jobs of one model (init).
-hipError_t upload_pass_tables(Ctx& c, Model& m, bool draft);
-// Uploads the layered path's one-phase GEMV arguments and jobs of one model.
-hipError_t upload_layered_jobs(Ctx& c, Model& m, bool draft);
 hipError_t launch_hold(Ctx& c, double ms);   // bounded device-side wait (timing mode)
 hipError_t launch_prefix_kv(Ctx& c, Model& m, int layer, int b, int prefix_len,
                             const bf16_t* k_pre, const bf16_t* v);

@@ -1,4 +1,4 @@
-// Device-side helpers shared by the gfx950 kernels (kernels.hip, pass.hip):
+// Device-side helpers shared by the gfx950 kernels (kernels.hip, sgemv.hip, gemm.hip):
 // vector types, bfloat16 conversion, 16x16x32 bf16 MFMA, reductions.
 #pragma once
 

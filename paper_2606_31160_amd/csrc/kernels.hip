@@ -19,7 +19,6 @@
 #include "ctx.h"
 #include "device.h"
 #include "gemv.h"
-#include "pass.h"
 #include "sgemv.h"
 
 namespace specdec {
@@ -1373,10 +1372,6 @@ hipError_t gemm_run(Ctx& c, int epi, const GemvArgs& g, int kind, double bytes) 
     if (e_ != hipSuccess) return e_;        \
   } while (0)
 
-// Which layered projections run as one-phase GEMV kernels (pass.hip) when
-// the shapes allow it; measured per projection on the 7B-class verify.
-constexpr bool kQkvAsJob = false, kOAsJob = false, kDownAsJob = false;
-
 // Split-KV attention of one layer + the combine of its splits; on the layer
 // an armed readout names, the readout variants of both kernels.
 hipError_t launch_attention(Ctx& c, Model& m, int li) {
@@ -1449,11 +1444,7 @@ hipError_t run_layer(Ctx& c, Model& m, int li, const bf16_t* next_gain, bool sel
   const bf16_t* pk = (c.gemm_rows && c.gemm_pk) ? m.pk + m.pk_layer * li : nullptr;
 
   // q, k, v (+ 1/rms of the attention norm) + rotary + cache append
-  if (m.ljobs_dev && kQkvAsJob) {
-    Timed t(c, SPEC_KERNEL_QKV, gemv_bytes((nq + 2 * nkv) * D, H, M, 2.0));
-    CK(gemv_job_launch(kJobQkv, gemv_job_steps(H, 1), m.largs_dev, m.ljobs_dev + (size_t)li * kPassJobs + kJobQkv,
-                       c.ncu, c.ljob_lds, S(c), t.e0, t.e1));
-  } else {
+  {
     GemvArgs g = gemv_base(c, M, c.R);
     g.w[0] = w.wq;
     g.w[1] = w.wk;
@@ -1498,11 +1489,7 @@ hipError_t run_layer(Ctx& c, Model& m, int li, const bf16_t* next_gain, bool sel
   }
   CK(launch_attention(c, m, li));
   // o projection + residual; bf16(x * g_ffn) and sums of x^2 for the FFN norm
-  if (m.ljobs_dev && kOAsJob) {
-    Timed t(c, SPEC_KERNEL_O, gemv_bytes(H, nq * D, M, 10.0));
-    CK(gemv_job_launch(kJobO, gemv_job_steps(nq * D, 1), m.largs_dev, m.ljobs_dev + (size_t)li * kPassJobs + kJobO,
-                       c.ncu, c.ljob_lds, S(c), t.e0, t.e1));
-  } else {
+  {
     GemvArgs g = gemv_base(c, M, c.R);
     g.w[0] = w.wo;
     g.nseg = 1;
@@ -1531,11 +1518,7 @@ hipError_t run_layer(Ctx& c, Model& m, int li, const bf16_t* next_gain, bool sel
     }
   }
   // gate/up (+ 1/rms of the FFN norm) + SwiGLU
-  if (m.ljobs_dev) {
-    Timed t(c, SPEC_KERNEL_GATEUP, gemv_bytes(2 * F, H, M, 1.0));
-    CK(gemv_job_launch(kJobGateUp, gemv_job_steps(H, 1), m.largs_dev, m.ljobs_dev + (size_t)li * kPassJobs + kJobGateUp,
-                       c.ncu, c.ljob_lds, S(c), t.e0, t.e1));
-  } else {
+  {
     GemvArgs g = gemv_base(c, M, c.R);
     g.w[0] = w.wg;
     g.w[1] = w.wu;
@@ -1558,13 +1541,8 @@ hipError_t run_layer(Ctx& c, Model& m, int li, const bf16_t* next_gain, bool sel
   }
   // down projection (k-split partials) -> residual + the next norm's input
   {
-    int S_down = m.s_down;
-    if (m.ljobs_dev && kDownAsJob) {
-      S_down = m.pass_splits;
-      Timed t(c, SPEC_KERNEL_DOWN, gemv_bytes(H, F, M, 4.0 * S_down));
-      CK(gemv_job_launch(kJobDown, gemv_job_steps(F, S_down), m.largs_dev,
-                         m.ljobs_dev + (size_t)li * kPassJobs + kJobDown, c.ncu, c.ljob_lds, S(c), t.e0, t.e1));
-    } else {
+    const int S_down = m.s_down;
+    {
       GemvArgs g = gemv_base(c, M, c.R);
       g.w[0] = w.wd;
       g.nseg = 1;
@@ -1596,7 +1574,6 @@ void init_kernel_attributes() {
   static bool done = false;
   if (done) return;
   done = true;
-  pass_set_attributes(gemv_lds_limit());
   sg_set_attributes(gemv_lds_limit());
   gemm_set_attributes(gemv_lds_limit());
   const void* attn[4] = {reinterpret_cast<const void*>(&k_attn<128, false>), reinterpret_cast<const void*>(&k_attn<128, true>),
@@ -1645,79 +1622,6 @@ hipError_t launch_hold(Ctx& c, double ms) {
   ms = std::min(std::max(ms, 0.0), 100.0);
   hipLaunchKernelGGL(k_hold, dim3(1), dim3(1), 0, c.stream, (long long)(ms * khz));
   return hipGetLastError();
-}
-
-PassArgs pass_args(Ctx& c, Model& m, bool draft);
-
-hipError_t upload_pass_tables(Ctx& c, Model& m, bool draft) {
-  const PassArgs a = pass_args(c, m, draft);
-  std::vector<GemvJob> jobs((size_t)m.d.layers * kPassJobs);
-  pass_build_jobs(a, m.L.data(), m.final_norm, jobs.data());
-  hipError_t e = hipMemcpyAsync(m.pass_args_dev, &a, sizeof a, hipMemcpyHostToDevice, c.stream);
-  if (e == hipSuccess)
-    e = hipMemcpyAsync(m.jobs_dev, jobs.data(), jobs.size() * sizeof(GemvJob), hipMemcpyHostToDevice, c.stream);
-  // the host copies are local: wait for the uploads before they go away
-  if (e == hipSuccess) e = hipStreamSynchronize(c.stream);
-  return e;
-}
-
-hipError_t upload_layered_jobs(Ctx& c, Model& m, bool draft) {
-  PassArgs a = pass_args(c, m, draft);
-  a.part = c.part;                    // down partials for k_down_finish
-  a.down_splits = m.pass_splits;
-  std::vector<GemvJob> jobs((size_t)m.d.layers * kPassJobs);
-  const spec_dims& d = m.d;
-  for (int li = 0; li < d.layers; ++li) {
-    const LayerW& w = m.L[li];
-    GemvJob* j = jobs.data() + (size_t)li * kPassJobs;
-    j[kJobQkv] = GemvJob{};
-    j[kJobQkv].w[0] = w.wq;
-    j[kJobQkv].w[1] = w.wk;
-    j[kJobQkv].w[2] = w.wv;
-    j[kJobQkv].row0[1] = d.q_heads * d.head_dim;
-    j[kJobQkv].row0[2] = (d.q_heads + d.kv_heads) * d.head_dim;
-    j[kJobQkv].nseg = 3;
-    j[kJobQkv].N = (d.q_heads + 2 * d.kv_heads) * d.head_dim;
-    j[kJobQkv].Kd = d.hidden;
-    j[kJobQkv].splits = 1;
-    j[kJobQkv].x = c.xg;
-    j[kJobQkv].ss_in = c.ss;
-    j[kJobQkv].q = c.q;
-    j[kJobQkv].kc = m.kc + m.kv_layer * li;
-    j[kJobQkv].vt = m.vt + m.kv_layer * li;
-    j[kJobO] = GemvJob{};
-    j[kJobO].w[0] = j[kJobO].w[1] = j[kJobO].w[2] = w.wo;
-    j[kJobO].nseg = 1;
-    j[kJobO].N = d.hidden;
-    j[kJobO].Kd = d.q_heads * d.head_dim;
-    j[kJobO].splits = 1;
-    j[kJobO].x = c.o;
-    j[kJobO].gain = w.ffn_norm;
-    j[kJobO].xg_out = c.xg;
-    j[kJobO].ss_out = c.ss;
-    j[kJobGateUp] = GemvJob{};
-    j[kJobGateUp].w[0] = w.wg;
-    j[kJobGateUp].w[1] = j[kJobGateUp].w[2] = w.wu;
-    j[kJobGateUp].nseg = 2;
-    j[kJobGateUp].N = 2 * d.ffn;
-    j[kJobGateUp].Kd = d.hidden;
-    j[kJobGateUp].splits = 1;
-    j[kJobGateUp].x = c.xg;
-    j[kJobGateUp].ss_in = c.ss;
-    j[kJobGateUp].u = c.u;
-    j[kJobDown] = GemvJob{};
-    j[kJobDown].w[0] = j[kJobDown].w[1] = j[kJobDown].w[2] = w.wd;
-    j[kJobDown].nseg = 1;
-    j[kJobDown].N = d.hidden;
-    j[kJobDown].Kd = d.ffn;
-    j[kJobDown].splits = m.pass_splits;
-    j[kJobDown].x = c.u;
-  }
-  hipError_t e = hipMemcpyAsync(m.largs_dev, &a, sizeof a, hipMemcpyHostToDevice, c.stream);
-  if (e == hipSuccess)
-    e = hipMemcpyAsync(m.ljobs_dev, jobs.data(), jobs.size() * sizeof(GemvJob), hipMemcpyHostToDevice, c.stream);
-  if (e == hipSuccess) e = hipStreamSynchronize(c.stream);
-  return e;
 }
 
 // ---------------------------------------------------------------------------
@@ -1921,70 +1825,6 @@ hipError_t launch_stage_verify(Ctx& c, const int32_t* d_override, int want_logit
   return hipGetLastError();
 }
 
-// Arguments of the persistent pass for one model.
-PassArgs pass_args(Ctx& c, Model& m, bool draft) {
-  const spec_dims& d = m.d;
-  PassArgs a{};
-  a.st = c.st;
-  a.layers = d.layers;
-  a.H = d.hidden;
-  a.nq = d.q_heads;
-  a.nkv = d.kv_heads;
-  a.D = d.head_dim;
-  a.F = d.ffn;
-  a.M = c.M;
-  a.R = c.R;
-  a.B = c.B;
-  a.rps = c.R;
-  a.mpad = c.Mpad;
-  a.pt = c.pt;
-  a.pps = c.pps;
-  a.eps = d.rms_eps;
-  a.scale_log2 = kLog2e / sqrtf((float)d.head_dim);
-  a.lw = m.lw_dev;
-  a.jobs = m.jobs_dev;
-  a.final_norm = m.final_norm;
-  a.select_last = draft ? 1 : 0;
-  a.kc = m.kc;
-  a.vt = m.vt;
-  a.kv_layer = m.kv_layer;
-  a.rcs = c.rcs;
-  a.x = c.x;
-  a.xa = c.p_xa;
-  a.xf = c.p_xf;
-  a.ssa = c.p_ssa;
-  a.ssf = c.p_ssf;
-  a.q = c.p_q;
-  a.o = c.p_o;
-  a.u = c.p_u;
-  a.x_layer = c.p_x_layer;
-  a.ss_layer = c.p_ss_layer;
-  a.q_layer = c.p_q_layer;
-  a.u_layer = c.p_u_layer;
-  a.xg_final = c.xg;
-  a.ss_final = c.ss;
-  a.op = c.op;
-  a.mp = c.mp;
-  a.lp = c.lp;
-  a.attn_chunk = c.attn_chunk;
-  a.attn_splits = c.attn_splits;
-  a.down_splits = m.pass_splits;
-  a.part = c.p_part;
-  a.bar = c.p_bar;
-  a.timeline = c.p_timeline;
-  return a;
-}
-
-// Every layer of a pass in the persistent kernel (pass.hip).
-hipError_t run_layers_persistent(Ctx& c, Model& m, bool draft) {
-  const spec_dims& d = m.d;
-  const int H = d.hidden, D = d.head_dim, nq = d.q_heads, nkv = d.kv_heads, F = d.ffn;
-  const double per_layer = gemv_bytes((nq + 2 * nkv) * D, H, c.M, 2.0) + gemv_bytes(H, nq * D, c.M, 10.0) +
-                           gemv_bytes(2 * F, H, c.M, 1.0) + gemv_bytes(H, F, c.M, 4.0 * m.pass_splits);
-  Timed t(c, draft ? SPEC_KERNEL_PASS_DRAFT : SPEC_KERNEL_PASS_TARGET, per_layer * d.layers);
-  return pass_launch(m.pass_args_dev, d.head_dim, draft, c.ncu, c.pass_lds, S(c), t.e0, t.e1);
-}
-
 // A k-split GEMV y = W x over the pass's rows (partial sums into `out`),
 // on the thin kernels or, for the GEMM's row counts, on the batched GEMM.
 hipError_t cond_gemv(Ctx& c, const bf16_t* w, const bf16_t* x, int N, int Kd, int S, float* out) {
@@ -2025,11 +1865,9 @@ hipError_t launch_forward(Ctx& c, PassMode mode) {
   Model& m = mode == PASS_VERIFY ? c.tgt : c.drf;
   const spec_dims& d = m.d;
   const int M = c.M;
-  const bool persistent = c.use_pass;
   {
-    // the persistent pass reads layer 0's norm input from its per-layer buffers
-    EmbedArgs p{c.st,    c.hist, c.embed,      m.L[0].attn_norm, c.x, persistent ? c.p_xa : c.xg,
-                persistent ? c.p_ssa : c.ss,  c.rcs,
+    EmbedArgs p{c.st,    c.hist, c.embed,      m.L[0].attn_norm, c.x, c.xg,
+                c.ss,  c.rcs,
                 c.pos3,  c.cs,   m.axis,       d.hidden,         c.R, c.cap,    (int)mode, c.Mpad,
                 d.head_dim, m.flat ? 1 : 0, c.V, c.mask_token,
                 (c.cond && mode != PASS_VERIFY) ? c.cat2 : nullptr, c.feat};
@@ -2052,9 +1890,7 @@ hipError_t launch_forward(Ctx& c, PassMode mode) {
       }
     return hipSuccess;
   };
-  if (persistent) {
-    CK(run_layers_persistent(c, m, draft));
-  } else if (c.sg) {
+  if (c.sg) {
     for (int li = 0; li < d.layers; ++li) {
       CK(run_layer_sg(c, m, li, block));
       CK(capture(li));

@@ -14,7 +14,6 @@
 
 #include "ctx.h"
 #include "gemv.h"
-#include "pass.h"
 #include "sgemv.h"
 
 using namespace specdec;
@@ -28,6 +27,8 @@ namespace {
 thread_local std::string g_init_error;
 
 constexpr size_t kAlign = 256;
+constexpr int32_t kKnownFlags = SPEC_FLAG_NO_GRAPHS | SPEC_FLAG_ROWMAJOR | SPEC_FLAG_BLOCK_DRAFT | SPEC_FLAG_COND |
+                                SPEC_FLAG_DRAFT_MROPE;
 
 size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 
@@ -105,10 +106,14 @@ bool check_config(const spec_config* cfg, const spec_seq_init* seqs, bool has_dr
     err = "stop_token out of range";
     return false;
   }
+  if (cfg->flags & ~kKnownFlags) {
+    err = "unknown bits in flags";
+    return false;
+  }
   if (!check_dims(cfg->target, true, err, "target")) return false;
   if (cfg->flags & SPEC_FLAG_COND) {
-    if (!has_draft || (cfg->flags & SPEC_FLAG_PERSISTENT)) {
-      err = "SPEC_FLAG_COND needs a draft and runs on the layered path, not with SPEC_FLAG_PERSISTENT";
+    if (!has_draft) {
+      err = "SPEC_FLAG_COND needs a draft";
       return false;
     }
     for (int i = 0; i < 3; ++i)
@@ -120,10 +125,6 @@ bool check_config(const spec_config* cfg, const spec_seq_init* seqs, bool has_dr
   if (cfg->flags & SPEC_FLAG_BLOCK_DRAFT) {
     if (!has_draft || cfg->K < 1) {
       err = "SPEC_FLAG_BLOCK_DRAFT needs a draft and K >= 1";
-      return false;
-    }
-    if (cfg->flags & SPEC_FLAG_PERSISTENT) {
-      err = "SPEC_FLAG_BLOCK_DRAFT runs on the layered path, not with SPEC_FLAG_PERSISTENT";
       return false;
     }
     if (cfg->mask_token < 0 || cfg->mask_token >= cfg->vocab) {
@@ -285,35 +286,6 @@ void set_splits(Model& m, int M, bool gemm_rows) {
   m.s_o = gemm_rows ? gemm_down_splits(m.d.hidden, m.d.q_heads * m.d.head_dim, slots) : 1;
 }
 
-// Down-projection k-splits of the persistent pass for one model: the fewest
-// that divide the grid (one workgroup per CU) while every worker wave streams
-// at most kPassSteps k-steps per tile and every phase fits in LDS; 0 when the
-// shapes do not fit the persistent kernel.
-int pass_splits_for(const spec_dims& d, const Layout& L, int ncu) {
-  if (L.M > 16 || (d.head_dim != 64 && d.head_dim != 128) || L.chunk != kAttnChunk) return 0;
-  // gate/up rows are read with plain loads: whole 32-wide steps per row; the
-  // other projections use 32-bit buffer offsets: segments below 2 GiB
-  if (d.hidden % 32 != 0) return 0;
-  const long long seg = std::max({(long long)d.q_heads * d.head_dim, (long long)d.ffn}) * d.hidden * 2;
-  if (seg >= (1ll << 31)) return 0;
-  PassArgs a{};
-  a.H = d.hidden;
-  a.nq = d.q_heads;
-  a.nkv = d.kv_heads;
-  a.D = d.head_dim;
-  a.F = d.ffn;
-  a.M = L.M;
-  a.attn_chunk = L.chunk;
-  a.attn_splits = L.splits;
-  const int T = (d.ffn + 31) / 32;
-  for (int s = 1; s <= std::min(ncu, T); ++s) {
-    if (ncu % s) continue;
-    a.down_splits = s;
-    if (pass_steps(a) <= kPassSteps && pass_lds_bytes(a) <= (size_t)gemv_lds_limit()) return s;
-  }
-  return 0;
-}
-
 size_t part_elems_for(const Model& m, int M) {
   // a pass of fewer rows may split the q/k/v GEMM where one of M rows does not
   const int nqkv = (m.d.q_heads + 2 * m.d.kv_heads) * m.d.head_dim;
@@ -399,13 +371,6 @@ size_t carve(Ctx& c, const spec_config* cfg, const spec_seq_init* seqs, bool has
     nq = std::max(nq, cfg->draft.q_heads);
     part = std::max(part, part_elems_for(c.drf, L.M));
   }
-  const bool want_pass = (cfg->flags & SPEC_FLAG_PERSISTENT) != 0;
-  c.tgt.pass_splits = pass_splits_for(cfg->target, L, c.ncu);
-  c.drf.pass_splits = has_draft ? pass_splits_for(cfg->draft, L, c.ncu) : 0;
-  const bool eligible = c.tgt.pass_splits > 0 && (!has_draft || c.drf.pass_splits > 0);
-  c.use_pass = want_pass && eligible;
-  if (eligible)
-    part = std::max(part, (size_t)std::max(c.tgt.pass_splits, c.drf.pass_splits) * L.M * H);
   Carver cv{base};
   c.st = cv.take<SeqState>(L.B);
   c.hist = cv.take<int32_t>((size_t)L.B * L.cap);
@@ -446,77 +411,9 @@ size_t carve(Ctx& c, const spec_config* cfg, const spec_seq_init* seqs, bool has
     c.drf.kc = cv.take<bf16_t>(c.drf.kv_layer * cfg->draft.layers);
     c.drf.vt = cv.take<bf16_t>(c.drf.kv_layer * cfg->draft.layers);
   }
-  if (eligible) {
-    c.tgt.largs_dev = cv.take<PassArgs>(1);
-    c.tgt.ljobs_dev = cv.take<GemvJob>((size_t)t.layers * kPassJobs);
-    if (has_draft) {
-      c.drf.largs_dev = cv.take<PassArgs>(1);
-      c.drf.ljobs_dev = cv.take<GemvJob>((size_t)cfg->draft.layers * kPassJobs);
-    }
-    PassArgs a{};
-    a.H = H;
-    a.M = L.M;
-    a.attn_chunk = L.chunk;
-    a.attn_splits = L.splits;
-    size_t lds = 0;
-    for (int k = 0; k < (has_draft ? 2 : 1); ++k) {
-      const spec_dims& d = k ? cfg->draft : t;
-      a.nq = d.q_heads;
-      a.nkv = d.kv_heads;
-      a.D = d.head_dim;
-      a.F = d.ffn;
-      a.down_splits = k ? c.drf.pass_splits : c.tgt.pass_splits;
-      lds = std::max(lds, pass_gemv_lds_bytes(a));
-    }
-    c.ljob_lds = lds;
-  }
-  if (c.use_pass) {
-    const int nl = std::max(t.layers, has_draft ? cfg->draft.layers : 0);
-    const int S = std::max(c.tgt.pass_splits, c.drf.pass_splits);
-    c.pass_layers = nl;
-    c.p_x_layer = (size_t)L.Mpad * H;
-    c.p_ss_layer = (size_t)(H / kTile) * L.Mpad;
-    c.p_q_layer = (size_t)L.Mpad * nqD;
-    c.p_u_layer = (size_t)L.Mpad * F;
-    c.p_xa = cv.take<bf16_t>(c.p_x_layer * (nl + 1));
-    c.p_xf = cv.take<bf16_t>(c.p_x_layer * nl);
-    c.p_ssa = cv.take<float>(c.p_ss_layer * (nl + 1));
-    c.p_ssf = cv.take<float>(c.p_ss_layer * nl);
-    c.p_q = cv.take<bf16_t>(c.p_q_layer * nl);
-    c.p_o = cv.take<bf16_t>(c.p_q_layer * nl);
-    c.p_u = cv.take<bf16_t>(c.p_u_layer * nl);
-    c.p_part = cv.take<float>((size_t)S * L.M * H);
-    c.p_bar = cv.take<unsigned>(kPassBarWords);
-    if (cfg->flags & SPEC_FLAG_PASS_TIMELINE)
-      c.p_timeline = cv.take<unsigned long long>((size_t)pass_timeline_events(nl) * c.ncu);
-    c.tgt.lw_dev = cv.take<LayerW>(t.layers);
-    c.tgt.pass_args_dev = cv.take<PassArgs>(1);
-    c.tgt.jobs_dev = cv.take<GemvJob>((size_t)t.layers * kPassJobs);
-    if (has_draft) {
-      c.drf.lw_dev = cv.take<LayerW>(cfg->draft.layers);
-      c.drf.pass_args_dev = cv.take<PassArgs>(1);
-      c.drf.jobs_dev = cv.take<GemvJob>((size_t)cfg->draft.layers * kPassJobs);
-    }
-    PassArgs a{};
-    a.H = H;
-    a.M = L.M;
-    a.attn_chunk = L.chunk;
-    a.attn_splits = L.splits;
-    size_t lds = 0;
-    for (int k = 0; k < (has_draft ? 2 : 1); ++k) {
-      const spec_dims& d = k ? cfg->draft : t;
-      a.nq = d.q_heads;
-      a.nkv = d.kv_heads;
-      a.D = d.head_dim;
-      a.F = d.ffn;
-      a.down_splits = k ? c.drf.pass_splits : c.tgt.pass_splits;
-      lds = std::max(lds, pass_lds_bytes(a));
-    }
-    c.pass_lds = lds;
-  }
   // packed-weight path: passes of at most 16 rows on the layered path
   c.sg = false;
-  if (!(cfg->flags & SPEC_FLAG_ROWMAJOR) && !c.use_pass && L.M <= kSgMaxRows &&
+  if (!(cfg->flags & SPEC_FLAG_ROWMAJOR) && L.M <= kSgMaxRows &&
       sg_build_jobs(c, c.tgt, false, false) && (!has_draft || sg_build_jobs(c, c.drf, true, false))) {
     size_t pf = 0;
     int units = 0;
@@ -542,7 +439,7 @@ size_t carve(Ctx& c, const spec_config* cfg, const spec_seq_init* seqs, bool has
   // passes on the batched-row GEMM stream the same tile-packed copy: every
   // wave load is then 1 KB of consecutive memory instead of 16 row pieces
   c.gemm_pk = false;
-  if (!c.sg && c.gemm_rows && !(cfg->flags & SPEC_FLAG_ROWMAJOR) && !c.use_pass) {
+  if (!c.sg && c.gemm_rows && !(cfg->flags & SPEC_FLAG_ROWMAJOR)) {
     c.gemm_pk = true;
     pk_offsets(c.tgt);
     c.pk_head = cv.take<bf16_t>(sg_packed_elems(L.V / kTile, (H + 31) / 32));
@@ -882,15 +779,6 @@ spec_status spec_init(const spec_config* cfg, const void* embed, const spec_mode
         (e = hipMemcpyAsync(c.hist, hist.data(), hist.size() * 4, hipMemcpyHostToDevice, stream)) != hipSuccess ||
         (e = hipMemcpyAsync(c.cls, cls.data(), cls.size(), hipMemcpyHostToDevice, stream)) != hipSuccess)
       return hip_fail(e, "table upload");
-    if (c.use_pass) {
-      if ((e = hipMemcpyAsync(c.tgt.lw_dev, c.tgt.L.data(), c.tgt.L.size() * sizeof(LayerW), hipMemcpyHostToDevice,
-                              stream)) != hipSuccess ||
-          (has_draft && (e = hipMemcpyAsync(c.drf.lw_dev, c.drf.L.data(), c.drf.L.size() * sizeof(LayerW),
-                                            hipMemcpyHostToDevice, stream)) != hipSuccess) ||
-          (e = upload_pass_tables(c, c.tgt, false)) != hipSuccess ||
-          (has_draft && (e = upload_pass_tables(c, c.drf, true)) != hipSuccess))
-        return hip_fail(e, "layer table upload");
-    }
     if (c.sg) {
       if (!sg_build_jobs(c, c.tgt, false, true) || (has_draft && !sg_build_jobs(c, c.drf, true, true))) {
         g_init_error = "packed GEMV plan changed between sizing and init";
@@ -905,11 +793,6 @@ spec_status spec_init(const spec_config* cfg, const void* embed, const spec_mode
       if ((e = sg_pack_head(c)) != hipSuccess || (e = sg_pack_model(c, c.tgt)) != hipSuccess ||
           (has_draft && (e = sg_pack_model(c, c.drf)) != hipSuccess))
         return hip_fail(e, "weight packing");
-    }
-    if (c.tgt.ljobs_dev) {
-      if ((e = upload_layered_jobs(c, c.tgt, false)) != hipSuccess ||
-          (has_draft && (e = upload_layered_jobs(c, c.drf, true)) != hipSuccess))
-        return hip_fail(e, "GEMV job upload");
     }
     for (int b = 0; b < c.B; ++b) {
       for (int l = 0; l < c.tgt.d.layers; ++l)
@@ -1038,8 +921,6 @@ spec_status spec_attn_readout(spec_ctx* ctx, int32_t model, int32_t layer, float
     const Model& m = model ? c.drf : c.tgt;
     if (layer < 0 || layer >= m.d.layers) return set_err(c, SPEC_E_INVAL, "spec_attn_readout: layer out of range");
     if (!aligned16(d_out)) return set_err(c, SPEC_E_INVAL, "spec_attn_readout: d_out must be 16-byte aligned");
-    if (c.use_pass)
-      return set_err(c, SPEC_E_STATE, "spec_attn_readout: not available on the persistent pass kernel");
     c.ro_arm_model = model;
     c.ro_arm_layer = layer;
     c.ro_arm_out = d_out;
@@ -1062,7 +943,6 @@ spec_status spec_sync(spec_ctx* ctx, int32_t* n_finished) {
     if (err & ERR_NUMERIC) return set_err(c, SPEC_E_NUMERIC, "NaN logits seen on the device");
     if (err & ERR_TOKEN) return set_err(c, SPEC_E_INVAL, "a draft token id was out of range (replaced by 0)");
     if (err & ERR_STATE) return set_err(c, SPEC_E_STATE, "draft catch-up exceeded K+1 rows");
-    if (err & ERR_SYNC) return set_err(c, SPEC_E_HIP, "a device-wide barrier of the persistent pass timed out");
     return SPEC_OK;
   });
 }
@@ -1126,31 +1006,8 @@ spec_status spec_debug_feature(spec_ctx* ctx, int32_t b, int32_t slot0, int32_t 
 spec_status spec_debug_path(const spec_ctx* ctx, int32_t* path) {
   if (!ctx || !path) return SPEC_E_INVAL;
   const Ctx& c = ctx->c;
-  *path = c.use_pass ? SPEC_PATH_PERSISTENT : ((c.sg || c.gemm_pk) ? SPEC_PATH_PACKED : SPEC_PATH_ROWMAJOR);
+  *path = (c.sg || c.gemm_pk) ? SPEC_PATH_PACKED : SPEC_PATH_ROWMAJOR;
   return SPEC_OK;
-}
-
-spec_status spec_debug_pass_timeline(spec_ctx* ctx, int32_t model, unsigned long long* host_out, int64_t capacity,
-                                     int32_t* n_events, int32_t* n_workgroups, double* tick_hz) {
-  return guarded(ctx, [&](Ctx& c) -> spec_status {
-    if (!c.p_timeline) return set_err(c, SPEC_E_STATE, "the context was created without SPEC_FLAG_PASS_TIMELINE");
-    if (model != 0 && !(model == 1 && c.has_draft)) return set_err(c, SPEC_E_INVAL, "bad model");
-    const int ev = pass_timeline_events((model == 0 ? c.tgt : c.drf).d.layers);
-    const size_t n = (size_t)ev * c.ncu;
-    if (n_events) *n_events = ev;
-    if (n_workgroups) *n_workgroups = c.ncu;
-    if (tick_hz) {
-      int khz = 0;
-      if (hipDeviceGetAttribute(&khz, hipDeviceAttributeWallClockRate, c.device) != hipSuccess || khz <= 0)
-        khz = 100000;
-      *tick_hz = khz * 1e3;
-    }
-    if (!host_out) return SPEC_OK;
-    if (capacity < (int64_t)n) return set_err(c, SPEC_E_CAPACITY, "timeline buffer too small");
-    HIPCHK(c, hipStreamSynchronize(c.stream), "sync");
-    HIPCHK(c, hipMemcpy(host_out, c.p_timeline, n * sizeof(unsigned long long), hipMemcpyDeviceToHost), "timeline");
-    return SPEC_OK;
-  });
 }
 
 spec_status spec_debug_kv(spec_ctx* ctx, int32_t b, int32_t model, int32_t layer, int32_t which, int32_t pos0,

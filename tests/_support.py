@@ -16,7 +16,7 @@ MARGIN = 2e-2
 
 
 # Session flags selecting the library's execution path (see include/spec.h).
-PATH_FLAGS = {"persistent": 2, "packed": 0, "rowmajor": 8}
+PATH_FLAGS = {"packed": 0, "rowmajor": 8}
 
 
 def capacity_for(w: W.Workload, b: int) -> int:

@@ -113,7 +113,8 @@ def test_benchmark_and_paper_configs_validate_on_host(name):
     (lambda c, s: setattr(s[0], "pending_token", 1024), "pending_token"),
     (lambda c, s: setattr(s[0], "prefix_len", 0), "prefix_len"),
     (lambda c, s: (setattr(c, "flags", B.SPEC_FLAG_BLOCK_DRAFT), setattr(c, "mask_token", 1024)), "mask_token"),
-    (lambda c, s: setattr(c, "flags", B.SPEC_FLAG_BLOCK_DRAFT | B.SPEC_FLAG_PERSISTENT), "PERSISTENT"),
+    (lambda c, s: setattr(c, "flags", 2), "unknown bits in flags"),
+    (lambda c, s: setattr(c, "flags", 4 | B.SPEC_FLAG_ROWMAJOR), "unknown bits in flags"),
     (lambda c, s: (setattr(c, "flags", B.SPEC_FLAG_BLOCK_DRAFT), setattr(c, "K", 0)), "BLOCK_DRAFT"),
 ])
 def test_invalid_config_rejected_on_host(mutate, needle):

@@ -25,13 +25,13 @@ from tests import _support as S
 pytestmark = pytest.mark.gpu
 
 
-# Every test runs on the three execution paths of the library: the persistent
-# pass kernel, and one kernel per layer step over the tile-packed weight copy
-# or over the caller's row-major weights.
+# Every test runs on both execution paths of the library: one kernel per
+# layer step over the tile-packed weight copy or over the caller's row-major
+# weights.
 _PATH = {"flags": 0}
 
 
-@pytest.fixture(autouse=True, params=["persistent", "packed", "rowmajor"])
+@pytest.fixture(autouse=True, params=["packed", "rowmajor"])
 def path(request):
     _PATH["flags"] = S.PATH_FLAGS[request.param]
     yield request.param

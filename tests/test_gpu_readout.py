@@ -120,15 +120,9 @@ def test_readout_pass_is_a_plain_pass_and_arms_once(c1):
     assert c0[0] == c1_[0] and list(c0[1]) == list(c1_[1])
 
 
-def test_readout_rejected_on_persistent_pass_and_bad_arguments(c1):
+def test_readout_rejects_bad_arguments(c1):
     from paper_2606_31160_amd import binding as B
     w, hp = c1
-    s = _session(w, provider=hp, flags=S.PATH_FLAGS["persistent"])
-    if B.spec_debug_path(s.ctx) == "persistent":
-        with pytest.raises(B.SpecError) as e:
-            s.attn_readout(0, 0)
-        assert e.value.status == 2
-    s.close()
     s = _session(w, provider=hp)
     for model, layer in ((0, 2), (0, -1), (1, 1), (2, 0)):
         with pytest.raises(B.SpecError) as e:

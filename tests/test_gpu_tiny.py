@@ -22,13 +22,13 @@ from tests import _support as S
 pytestmark = pytest.mark.gpu
 
 
-# Every test runs on the three execution paths of the library: the persistent
-# pass kernel, and one kernel per layer step over the tile-packed weight copy
-# or over the caller's row-major weights.
+# Every test runs on both execution paths of the library: one kernel per
+# layer step over the tile-packed weight copy or over the caller's row-major
+# weights.
 _PATH = {"flags": 0}
 
 
-@pytest.fixture(autouse=True, params=["persistent", "packed", "rowmajor"])
+@pytest.fixture(autouse=True, params=["packed", "rowmajor"])
 def path(request):
     _PATH["flags"] = S.PATH_FLAGS[request.param]
     yield request.param
@@ -412,8 +412,8 @@ def test_interleaved_axis_assignment_rotation():
 
 
 def test_requested_execution_path_runs(c1, path):
-    """The persistent pass kernel runs every layer when it is selected, and
-    the per-layer kernels run otherwise (counted by the library's timing)."""
+    """The requested weight layout is the one the per-layer kernels stream,
+    one launch per layer step (counted by the library's timing)."""
     from paper_2606_31160_amd import binding as B
     w = c1[0]
     s = _session(w)
@@ -423,14 +423,9 @@ def test_requested_execution_path_runs(c1, path):
         s.draft_step()
     s.verify(None)
     s.commit()
-    n_pt, _, _ = B.spec_timing_read(s.ctx, "pass_target")
-    n_pd, _, _ = B.spec_timing_read(s.ctx, "pass_draft")
     n_qkv, _, _ = B.spec_timing_read(s.ctx, "qkv")
     B.spec_timing(s.ctx, False)
     assert s.sync() == 0
     assert B.spec_debug_path(s.ctx) == path
-    if path == "persistent":
-        assert (n_pt, n_pd, n_qkv) == (1, w.K, 0)
-    else:
-        assert (n_pt, n_pd) == (0, 0) and n_qkv == w.target.layers + w.K * w.draft.layers
+    assert n_qkv == w.target.layers + w.K * w.draft.layers
     s.close()

@@ -191,3 +191,29 @@ def test_zero_output_projections_leave_residual_stream():
 def test_greedy_argmax_ties_and_nan():
     z = np.array([[1.0, 3.0, 3.0, 2.0], [np.nan, 0.5, np.nan, 0.5], [-1.0, -2.0, np.nan, -1.0]])
     assert list(M.greedy_argmax(z)) == [1, 1, 0]
+
+
+def test_softmax_rows_sum_to_one_and_are_shift_invariant():
+    rng = np.random.default_rng(12)
+    s = rng.standard_normal((5, 37)) * 30
+    p = M.softmax(s)
+    assert np.allclose(p.sum(axis=-1), 1.0, rtol=0, atol=1e-14)
+    assert np.all(p >= 0)
+    assert np.allclose(M.softmax(s + 1234.5), p, rtol=1e-12, atol=1e-15)
+    assert np.allclose(p, scipy.special.softmax(s, axis=-1), rtol=1e-12, atol=1e-15)
+
+
+def test_chunked_lm_head_equals_one_product():
+    # the LM head over vocabulary chunks (used for the 152064-row head) equals
+    # one product with the whole decoded embedding, ragged last chunk included
+    w = _tiny(vocab=1000)
+    hp = W.HostWeights(w)
+    E = numerics.decode(hp.get("global", -1, "embed"))
+    h = np.random.default_rng(13).standard_normal((3, w.target.hidden))
+    whole = M.Decoder(hp, "target", w.target, w.vocab, M.ROTARY_MROPE)
+    assert whole.vocab <= whole.lm_chunk
+    chunked = M.Decoder(hp, "target", w.target, w.vocab, M.ROTARY_MROPE, cache_weights=False, lm_chunk=96)
+    ref = h @ E.T
+    assert np.allclose(whole.lm_head(h), ref, rtol=1e-13, atol=1e-13)
+    assert np.allclose(chunked.lm_head(h), ref, rtol=1e-13, atol=1e-13)
+    assert chunked.lm_head(h).shape == (3, 1000)

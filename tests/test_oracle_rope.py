@@ -122,3 +122,40 @@ def test_flat_adjacent_tokens_differ_in_every_pair():
     y = R.flatrope(x, np.array([40, 41]))
     diff_pairs = np.all(y[0].reshape(2, 64, 2) != y[1].reshape(2, 64, 2), axis=2)
     assert diff_pairs.all()
+
+
+def _rotate_half_split(x, phi):
+    """The half-split convention of public rotary code: pair d is
+    (x_d, x_{d + D/2}), i.e. x * [cos, cos] + [-x2, x1] * [sin, sin]."""
+    D = x.shape[-1]
+    x1, x2 = x[..., :D // 2], x[..., D // 2:]
+    c = np.concatenate([np.cos(phi), np.cos(phi)], axis=-1)[:, None, :]
+    s = np.concatenate([np.sin(phi), np.sin(phi)], axis=-1)[:, None, :]
+    return x * c + np.concatenate([-x2, x1], axis=-1) * s
+
+
+@pytest.mark.parametrize("inter", [False, True])
+def test_adjacent_pairs_equal_half_split_under_a_row_permutation(inter):
+    # Reading of Eq. rope-1d: adjacent pairs (2d, 2d+1).  A half-split model is
+    # the same model with the rows of W_q and W_k permuted so that half-split
+    # dimension d lands on 2d and d + D/2 on 2d + 1: rotated vectors agree up
+    # to that permutation and attention scores agree exactly.
+    rng = np.random.default_rng(11)
+    D, n = 64, 6
+    perm = np.empty(D, dtype=np.int64)           # adjacent index -> half-split index
+    perm[0::2] = np.arange(D // 2)
+    perm[1::2] = np.arange(D // 2) + D // 2
+    pos3 = rng.integers(0, 500, size=(3, n))
+    phi = R.phases(pos3, D, (8, 12, 12), inter)
+    q_half = rng.standard_normal((n, 2, D))
+    k_half = rng.standard_normal((n, 2, D))
+    rq_half = _rotate_half_split(q_half, phi)
+    rk_half = _rotate_half_split(k_half, phi)
+    rq_adj = R.mrope(q_half[..., perm], pos3, (8, 12, 12), inter)
+    rk_adj = R.mrope(k_half[..., perm], pos3, (8, 12, 12), inter)
+    assert np.allclose(rq_adj, rq_half[..., perm], rtol=0, atol=1e-12)
+    s_half = np.einsum("ihd,jhd->hij", rq_half, rk_half)
+    s_adj = np.einsum("ihd,jhd->hij", rq_adj, rk_adj)
+    assert np.allclose(s_adj, s_half, rtol=1e-12, atol=1e-12)
+    # without the permutation the two conventions differ
+    assert not np.allclose(R.mrope(q_half, pos3, (8, 12, 12), inter), rq_half, atol=1e-3)
