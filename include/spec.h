@@ -217,6 +217,34 @@ spec_status draft_steps(spec_ctx* ctx, int32_t n, int32_t* d_draft_tokens);
  * State: READY (with d_draft_tokens, or K == 0) or DRAFTING after K steps -> VERIFIED. */
 spec_status spec_verify(spec_ctx* ctx, const int32_t* d_draft_tokens, void* d_logits);
 
+/* ---- verify without allocation ------------------------------------------- */
+
+#define SPEC_SCRATCH_BYTES (32u << 20)   /* size of the library's static scratch array per GPU */
+
+/* For callers that cannot allocate or instantiate anything while they run:
+ * code under HIP stream capture (this call can be captured into the caller's
+ * own graph), tight serving loops, harnesses that forbid allocation.
+ * Same arguments, state rules, device outputs and results as spec_verify, with
+ * two differences:
+ *   - the pass's scratch (split-KV attention partials, partial tiles and
+ *     k-split sums of the projections, the per-workgroup argmax pairs of the LM
+ *     head, their arrival counters and the bf16 logits staging) lives in one
+ *     static device array of SPEC_SCRATCH_BYTES bytes that the library holds
+ *     on each GPU it runs on until the process ends (its address is looked up
+ *     in spec_init), not in the context's workspace;
+ *   - every kernel is launched directly on the context's stream: no HIP graph
+ *     is captured, instantiated or launched.
+ * It calls no hipMalloc, hipFree or other allocating routine.  The counters
+ * that must start at zero are cleared by a fill kernel at the start of the
+ * call.  Every call on one GPU, from any context, shares that GPU's array,
+ * which keeps the last call's contents: calls on one GPU that overlap in time
+ * (other streams or threads) race and give wrong results, so serialise them.
+ * Returns SPEC_E_CAPACITY, with nothing enqueued and the context unchanged,
+ * when the context's verify needs more than SPEC_SCRATCH_BYTES of scratch (the
+ * error text gives the need; it grows with batch*(K+1) rows, query heads,
+ * sequence capacity and vocabulary).  Any other error is spec_verify's. */
+spec_status spec_verify_scratch(spec_ctx* ctx, const int32_t* d_draft_tokens, void* d_logits);
+
 /* Commit (Eq. commit): appends (d_1..d_l, r*_{l+1}), cut after a stop token
  * or at the token budget, to each unfinished sequence; the target keeps KV
  * slots up to the new length and the draft keeps the slots whose inputs still

@@ -20,6 +20,7 @@ SPEC_MAX_K = 16
 SPEC_MAX_BATCH = 16
 SPEC_MAX_ROWS = 160
 SPEC_KV_PAGE = 64
+SPEC_SCRATCH_BYTES = 32 << 20
 SPEC_FLAG_NO_GRAPHS = 1
 SPEC_FLAG_ROWMAJOR = 8
 SPEC_FLAG_DRAFT_MROPE = 16
@@ -86,6 +87,7 @@ def lib():
             "draft_step": [P, P],
             "draft_steps": [P, c_int32, P],
             "spec_verify": [P, P, P],
+            "spec_verify_scratch": [P, P, P],
             "spec_commit": [P, P, P, P, P],
             "spec_attn_readout": [P, c_int32, c_int32, P],
             "spec_sync": [P, POINTER(c_int32)],
@@ -154,6 +156,11 @@ def draft_steps(ctx, n: int, d_draft_tokens: int = 0) -> None:
 
 def spec_verify(ctx, d_draft_tokens: int = 0, d_logits: int = 0) -> None:
     _check(lib().spec_verify(ctx, c_void_p(d_draft_tokens or None), c_void_p(d_logits or None)), "spec_verify", ctx)
+
+
+def spec_verify_scratch(ctx, d_draft_tokens: int = 0, d_logits: int = 0) -> None:
+    _check(lib().spec_verify_scratch(ctx, c_void_p(d_draft_tokens or None), c_void_p(d_logits or None)),
+           "spec_verify_scratch", ctx)
 
 
 def spec_commit(ctx, d_accept_len: int = 0, d_committed: int = 0, d_n_committed: int = 0,

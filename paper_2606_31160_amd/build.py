@@ -7,7 +7,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "libspecdec.so")
-SOURCES = ["kernels.hip", "gemm.hip", "sgemv.hip", "runtime.cpp"]
+SOURCES = ["kernels.hip", "gemm.hip", "sgemv.hip", "scratch.hip", "runtime.cpp"]
 
 # Packed-FP32 VALU forms are turned off for all device code.
 HIPCC_FLAGS = [

@@ -114,7 +114,8 @@ struct Ctx {
   float2* rcs = nullptr;            // [Mpad][head_dim/2] (cos, sin) of each row's rotary pairs
   float* part = nullptr;            // GEMV k-split partial sums
   size_t part_elems = 0;
-  float* op = nullptr;              // [splits][B][q_heads][R][head_dim] attention partials
+  bf16_t* op = nullptr;             // [splits][B][q_heads][R][head_dim] attention partials (unnormalised)
+  size_t attn_rows = 0;             // splits * B * q_heads * R (max over the models)
   float* mp = nullptr;              // [splits][B][q_heads][R] running max (log2 units)
   float* lp = nullptr;              // [splits][B][q_heads][R] running sum
   float* amax_v = nullptr;          // [vocab/16][Mpad] per-tile maximum logit
@@ -201,6 +202,12 @@ bool sg_build_jobs(Ctx& c, Model& m, bool draft, bool fill);
 void pk_offsets(Model& m);
 hipError_t sg_pack_model(Ctx& c, Model& m);
 hipError_t sg_pack_head(Ctx& c);
+
+// The library's static per-device scratch array (scratch.hip): its device
+// address on the current device, resolved once per device (spec_init).
+hipError_t scratch_resolve(int device);
+void* scratch_device_ptr(int device);
+size_t scratch_capacity();
 
 // Dynamic LDS bytes one GEMV workgroup needs (TT tiles, M rows, span k-steps)
 // and the device limit; k-splits of a GEMV whose workgroups cannot hold all

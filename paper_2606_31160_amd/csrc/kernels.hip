@@ -1382,10 +1382,10 @@ hipError_t launch_attention(Ctx& c, Model& m, int li) {
   const int G = nq / nkv;
   const int rb = (c.R * G + 63) / 64;
   const bool ro = c.ro_out && c.ro_m == &m && c.ro_layer == li;
-  AttnArgs p{c.st, c.q, kc, vt, c.pt, reinterpret_cast<bf16_t*>(c.op), c.mp, c.lp, nq, nkv, G, c.R, c.B, c.pps, c.attn_chunk, rb,
+  AttnArgs p{c.st, c.q, kc, vt, c.pt, c.op, c.mp, c.lp, nq, nkv, G, c.R, c.B, c.pps, c.attn_chunk, rb,
              kLog2e / sqrtf((float)D), c.cls, c.rp, c.cap};
   dim3 grid(c.attn_splits, nkv * rb, c.B);
-  CombineArgs cb{c.st, reinterpret_cast<const bf16_t*>(c.op), c.mp, c.lp, c.o, nq, D, c.R, c.B, c.attn_chunk, c.rp,
+  CombineArgs cb{c.st, c.op, c.mp, c.lp, c.o, nq, D, c.R, c.B, c.attn_chunk, c.rp,
                  ro ? c.ro_out : nullptr, {}};
   for (int b = 0; b < c.B && b < SPEC_MAX_BATCH; ++b) cb.inv_ln[b] = c.ro_inv_ln[b];
   const size_t comb_lds = (size_t)(((c.attn_splits + 3) & ~3) + 8 * D) * sizeof(float);
@@ -1404,6 +1404,22 @@ hipError_t launch_attention(Ctx& c, Model& m, int li) {
   return hipGetLastError();
 }
 
+// A packed-GEMV job with the context's current partial-tile, counter,
+// argmax and logits buffers: the planned jobs keep the workspace's, and a
+// call that moves those buffers elsewhere (spec_verify_scratch) swaps the
+// context's pointers for its duration.
+SgJob sg_job(const Ctx& c, const SgJob& j) {
+  SgJob r = j;
+  r.part = c.sg_part;
+  r.cnt = c.sg_cnt;
+  if (r.amax_v) {
+    r.amax_v = c.amax_v;
+    r.amax_i = c.amax_i;
+    r.logits = c.logits;
+  }
+  return r;
+}
+
 // One layer on the packed-weight path: q/k/v (+rotary, KV append),
 // attention, o (+residual), gate/up (+SwiGLU), down (+residual, next norm).
 hipError_t run_layer_sg(Ctx& c, Model& m, int li, bool block) {
@@ -1415,20 +1431,20 @@ hipError_t run_layer_sg(Ctx& c, Model& m, int li, bool block) {
   const SgJob& down = (block && li + 1 == d.layers) ? m.sg_block[0] : hj[3];
   {
     Timed t(c, SPEC_KERNEL_QKV, gemv_bytes((nq + 2 * nkv) * D, H, M, 2.0));
-    CK(sg_launch(SG_ROPE, hj[0], S(c), t.e0, t.e1));
+    CK(sg_launch(SG_ROPE, sg_job(c, hj[0]), S(c), t.e0, t.e1));
   }
   CK(launch_attention(c, m, li));
   {
     Timed t(c, SPEC_KERNEL_O, gemv_bytes(H, nq * D, M, 10.0));
-    CK(sg_launch(SG_RESID, hj[1], S(c), t.e0, t.e1));
+    CK(sg_launch(SG_RESID, sg_job(c, hj[1]), S(c), t.e0, t.e1));
   }
   {
     Timed t(c, SPEC_KERNEL_GATEUP, gemv_bytes(2 * F, H, M, 1.0));
-    CK(sg_launch(SG_SWIGLU, hj[2], S(c), t.e0, t.e1));
+    CK(sg_launch(SG_SWIGLU, sg_job(c, hj[2]), S(c), t.e0, t.e1));
   }
   {
     Timed t(c, SPEC_KERNEL_DOWN, gemv_bytes(H, F, M, 10.0));
-    CK(sg_launch(SG_DOWN, down, S(c), t.e0, t.e1));
+    CK(sg_launch(SG_DOWN, sg_job(c, down), S(c), t.e0, t.e1));
   }
   return hipSuccess;
 }
@@ -1911,7 +1927,7 @@ hipError_t launch_forward(Ctx& c, PassMode mode) {
     const double bytes = gemv_bytes(c.V, d.hidden, rows, 0.0) + 8.0 * (c.V / kTile) * rows;
     Timed t(c, SPEC_KERNEL_LMHEAD, bytes);
     const size_t hi = (size_t)d.layers * 4;
-    CK(sg_launch(SG_ARGMAX, block ? m.sg_block[1] : m.sg_host[hi], S(c), t.e0, t.e1));
+    CK(sg_launch(SG_ARGMAX, sg_job(c, block ? m.sg_block[1] : m.sg_host[hi]), S(c), t.e0, t.e1));
   } else {
     GemvArgs g = gemv_base(c, draft ? c.B : M, draft ? 1 : c.R);
     g.w[0] = c.embed;

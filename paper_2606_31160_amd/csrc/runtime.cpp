@@ -389,7 +389,8 @@ size_t carve(Ctx& c, const spec_config* cfg, const spec_seq_init* seqs, bool has
   c.part = cv.take<float>(part);
   c.part_elems = part;
   const size_t attn_rows = (size_t)L.splits * L.B * nq * L.R;
-  c.op = cv.take<float>(attn_rows * D);
+  c.attn_rows = attn_rows;
+  c.op = cv.take<bf16_t>(attn_rows * D);
   c.mp = cv.take<float>(attn_rows);
   c.lp = cv.take<float>(attn_rows);
   c.amax_v = cv.take<float>((size_t)(L.V / kTile) * L.Mpad);
@@ -589,6 +590,79 @@ spec_status run_commit(Ctx& c) {
                    [&] { return launch_commit(c, c.commit_out[0], c.commit_out[1], c.commit_out[2], c.commit_out[3]); });
 }
 
+// Where spec_verify_scratch puts a verify's scratch inside the static array:
+// the buffers spec_verify takes from the workspace for the duration of one
+// pass (attention partials, partial sums and tiles, arrival counters, argmax
+// pairs, logits staging).  Offsets are 256-byte aligned.
+struct ScratchPlan {
+  size_t op = 0, mp = 0, lp = 0, rp = 0, part = 0, sg_part = 0, sg_cnt = 0, amax_v = 0, amax_i = 0, logits = 0;
+  size_t cnt_bytes = 0;   // counters to clear (a multiple of 16)
+  size_t bytes = 0;
+};
+
+ScratchPlan scratch_plan(const Ctx& c) {
+  ScratchPlan p;
+  size_t off = 0;
+  auto take = [&](size_t n) {
+    off = align_up(off, kAlign);
+    const size_t at = off;
+    off += n;
+    return at;
+  };
+  const int D = c.tgt.d.head_dim;
+  const size_t amax = (size_t)(c.V / kTile) * c.Mpad;
+  p.op = take(c.attn_rows * D * sizeof(bf16_t));
+  p.mp = take(c.attn_rows * sizeof(float));
+  p.lp = take(c.attn_rows * sizeof(float));
+  p.rp = take(c.attn_rows * 4 * sizeof(float));
+  p.part = take(c.part_elems * sizeof(float));
+  p.sg_part = take(c.sg ? c.sg_part_floats * sizeof(float) : 0);
+  p.cnt_bytes = c.sg ? align_up((size_t)c.sg_units * sizeof(unsigned), 16) : 0;
+  p.sg_cnt = take(p.cnt_bytes);
+  p.amax_v = take(amax * sizeof(float));
+  p.amax_i = take(amax * sizeof(int32_t));
+  p.logits = take((size_t)c.Mpad * c.V * sizeof(bf16_t));
+  p.bytes = align_up(off, kAlign);
+  return p;
+}
+
+// Points the context's scratch buffers into the static array for the
+// lifetime of the object, then restores the workspace's.
+struct ScratchSwap {
+  Ctx& c;
+  bf16_t* op;
+  float *mp, *lp, *rp, *part, *sg_part, *amax_v;
+  unsigned* sg_cnt;
+  int32_t* amax_i;
+  bf16_t* logits;
+  ScratchSwap(Ctx& ctx, char* base, const ScratchPlan& p)
+      : c(ctx), op(ctx.op), mp(ctx.mp), lp(ctx.lp), rp(ctx.rp), part(ctx.part), sg_part(ctx.sg_part),
+        amax_v(ctx.amax_v), sg_cnt(ctx.sg_cnt), amax_i(ctx.amax_i), logits(ctx.logits) {
+    c.op = reinterpret_cast<bf16_t*>(base + p.op);
+    c.mp = reinterpret_cast<float*>(base + p.mp);
+    c.lp = reinterpret_cast<float*>(base + p.lp);
+    c.rp = reinterpret_cast<float*>(base + p.rp);
+    c.part = reinterpret_cast<float*>(base + p.part);
+    c.sg_part = c.sg ? reinterpret_cast<float*>(base + p.sg_part) : nullptr;
+    c.sg_cnt = c.sg ? reinterpret_cast<unsigned*>(base + p.sg_cnt) : nullptr;
+    c.amax_v = reinterpret_cast<float*>(base + p.amax_v);
+    c.amax_i = reinterpret_cast<int32_t*>(base + p.amax_i);
+    c.logits = reinterpret_cast<bf16_t*>(base + p.logits);
+  }
+  ~ScratchSwap() {
+    c.op = op;
+    c.mp = mp;
+    c.lp = lp;
+    c.rp = rp;
+    c.part = part;
+    c.sg_part = sg_part;
+    c.sg_cnt = sg_cnt;
+    c.amax_v = amax_v;
+    c.amax_i = amax_i;
+    c.logits = logits;
+  }
+};
+
 template <class F>
 spec_status guarded(spec_ctx* ctx, F f) {
   if (!ctx) return SPEC_E_INVAL;
@@ -709,6 +783,15 @@ spec_status spec_init(const spec_config* cfg, const void* embed, const spec_mode
     }
     if (hipGetDevice(&c.device) != hipSuccess) c.device = 0;
     init_kernel_attributes();
+    {
+      // the static scratch array's address on this device (spec_verify_scratch)
+      const hipError_t e = scratch_resolve(c.device);
+      if (e != hipSuccess) {
+        g_init_error = std::string("scratch symbol lookup: ") + hipGetErrorString(e);
+        delete ctx;
+        return SPEC_E_HIP;
+      }
+    }
 
     // host-built tables
     const int D = cfg->target.head_dim, half = D / 2;
@@ -887,6 +970,47 @@ spec_status spec_verify(spec_ctx* ctx, const int32_t* d_draft_tokens, void* d_lo
     HIPCHK(c, launch_stage_verify(c, c.K > 0 ? d_draft_tokens : nullptr, d_logits ? 1 : 0), "verify staging");
     spec_status s = run_pass(c, PASS_VERIFY);
     if (s != SPEC_OK) return s;
+    HIPCHK(c, launch_logits_out(c, d_logits), "logits copy");
+    c.phase = Ctx::VERIFIED;
+    return SPEC_OK;
+  });
+}
+
+spec_status spec_verify_scratch(spec_ctx* ctx, const int32_t* d_draft_tokens, void* d_logits) {
+  return guarded(ctx, [&](Ctx& c) -> spec_status {
+    if (c.phase == Ctx::VERIFIED)
+      return set_err(c, SPEC_E_STATE, "spec_verify_scratch: commit the last verify first");
+    if (!d_draft_tokens && c.K > 0 && c.dsteps != c.K)
+      return set_err(c, SPEC_E_STATE,
+                     "spec_verify_scratch: no draft tokens given and fewer than K draft steps taken");
+    const ScratchPlan plan = scratch_plan(c);
+    if (plan.bytes > scratch_capacity()) {
+      char buf[200];
+      snprintf(buf, sizeof buf,
+               "spec_verify_scratch: this context's verify needs %zu bytes of scratch, more than the %zu-byte "
+               "static array (SPEC_SCRATCH_BYTES)",
+               plan.bytes, scratch_capacity());
+      return set_err(c, SPEC_E_CAPACITY, buf);
+    }
+    char* base = static_cast<char*>(scratch_device_ptr(c.device));
+    if (!base) return set_err(c, SPEC_E_STATE, "spec_verify_scratch: scratch address not resolved on this device");
+    ScratchSwap swap(c, base, plan);
+    // arrival counters start at zero (every launch leaves them at zero, but
+    // the array is shared with every other context on this GPU)
+    if (plan.cnt_bytes) HIPCHK(c, launch_zero(c, c.sg_cnt, plan.cnt_bytes), "scratch counter clear");
+    HIPCHK(c, launch_stage_verify(c, c.K > 0 ? d_draft_tokens : nullptr, d_logits ? 1 : 0), "verify staging");
+    if (c.ro_arm_out && c.ro_arm_model == 0) {
+      c.ro_m = &c.tgt;
+      c.ro_layer = c.ro_arm_layer;
+      c.ro_out = c.ro_arm_out;
+      c.ro_arm_out = nullptr;
+      c.ro_arm_model = -1;
+    }
+    if (c.timing) HIPCHK(c, launch_hold(c, 4.0), "timing hold");
+    const hipError_t e = launch_pass(c, PASS_VERIFY);
+    c.ro_m = nullptr;
+    c.ro_out = nullptr;
+    HIPCHK(c, e, "forward pass");
     HIPCHK(c, launch_logits_out(c, d_logits), "logits copy");
     c.phase = Ctx::VERIFIED;
     return SPEC_OK;
