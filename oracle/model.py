@@ -5,7 +5,7 @@ M-RoPE on every attention layer (Sec. 3.3) and the draft as a small transformer
 with FlatRoPE (Sec. 4.1-4.2); it does not spell out the block.  The reading used
 here is a pre-norm decoder layer:
 
-    a = RMSNorm(x) * g_attn
+    a = RMSNorm(x) * g_attn                     (evaluated as ((x * g) W^T) / rms(x))
     q, k, v = a W_q^T, a W_k^T, a W_v^T          (no bias)
     q, k rotated at their token's position      (M-RoPE target / FlatRoPE draft)
     o = softmax(q k^T / sqrt(D)) v              (causal; GQA: q head h reads kv head h // (n_q/n_kv))
@@ -151,6 +151,14 @@ class Decoder:
     def _r(self, x: np.ndarray) -> np.ndarray:
         return numerics.mirror(x) if self.mirror else x
 
+    def _normed(self, x: np.ndarray, g: np.ndarray):
+        """RMSNorm(x) * g as the pair (x * g, 1 / sqrt(mean(x^2) + eps)): the
+        projection of the normalised rows is (x * g) W^T scaled per row, the
+        same product as RMSNorm(x) * g W^T.  In mirror mode x * g is rounded
+        to bfloat16, where the GPU stores the projection's input."""
+        inv = 1.0 / np.sqrt(np.mean(x * x, axis=-1, keepdims=True) + self.s.rms_eps)
+        return self._r(x * g), inv
+
     # -- rotary ------------------------------------------------------------
     def rotate(self, x: np.ndarray, pos3: np.ndarray) -> np.ndarray:
         """x [N, heads, D]; pos3 [3, N] (target) -- the draft uses pos3[0] as m."""
@@ -192,10 +200,10 @@ class Decoder:
         self.captured = {}
         for li in range(s.layers):
             W = self.layer(li)
-            a = self._r(rmsnorm(x, W["attn_norm"], s.rms_eps))
-            q = (a @ W["wq"].T).reshape(M, nq, D)
-            k = (a @ W["wk"].T).reshape(M, nkv, D)
-            v = (a @ W["wv"].T).reshape(M, nkv, D)
+            a, ia = self._normed(x, W["attn_norm"])
+            q = ((a @ W["wq"].T) * ia).reshape(M, nq, D)
+            k = ((a @ W["wk"].T) * ia).reshape(M, nkv, D)
+            v = ((a @ W["wv"].T) * ia).reshape(M, nkv, D)
             q = self._r(self.rotate(q, pos))
             k = self._r(self.rotate(k, pos))
             v = self._r(v)
@@ -205,14 +213,14 @@ class Decoder:
                 self.readout = budget.budget(q, cache.k[li], vis, self.readout_classes)
             o = self._r(attend(q, cache.k[li], cache.v[li], vis).reshape(M, nq * D))
             x = x + o @ W["wo"].T
-            b = self._r(rmsnorm(x, W["ffn_norm"], s.rms_eps))
-            u = self._r(silu(b @ W["w_gate"].T) * (b @ W["w_up"].T))
+            b, ib = self._normed(x, W["ffn_norm"])
+            u = self._r(silu((b @ W["w_gate"].T) * ib) * ((b @ W["w_up"].T) * ib))
             x = x + u @ W["w_down"].T
             if li in self.capture_layers:
                 self.captured[li] = self._r(x)
-        h = self._r(rmsnorm(x, self.final_norm(), s.rms_eps))
-        z = self.lm_head(h)
-        return (z, h) if want_hidden else z
+        h, ih = self._normed(x, self.final_norm())
+        z = self.lm_head(h) * ih
+        return (z, h * ih) if want_hidden else z
 
 
 def greedy_argmax(z: np.ndarray) -> np.ndarray:

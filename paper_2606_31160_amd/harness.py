@@ -28,12 +28,14 @@ class Session:
     page_seed       None: each sequence's KV pages follow the previous
                     sequence's; an int: a seeded random permutation of the
                     page pool is handed over as the sequences' page tables
+    pending_tokens  None: the workload's first pending token per sequence;
+                    else one token id per sequence
     """
 
     def __init__(self, w, source: str = "host", flags: int = 0, with_draft: bool = True,
                  K: Optional[int] = None, max_new_tokens: Optional[int] = None, stop_token: Optional[int] = None,
                  provider=None, page_seed: Optional[int] = None, mask_token: Optional[int] = None,
-                 cond_layers=None):
+                 cond_layers=None, pending_tokens=None):
         torch = _require_gpu()
         import workloads as W
         self.torch = torch
@@ -87,7 +89,8 @@ class Session:
                 blocks[i].start, blocks[i].t, blocks[i].h, blocks[i].w = bl.start, bl.t, bl.h, bl.w
             s.n_blocks = len(lay.blocks)
             s.blocks = blocks
-            s.pending_token = W.first_pending_token(w, b)
+            s.pending_token = (W.first_pending_token(w, b) if pending_tokens is None
+                               else int(pending_tokens[b]))
             kv = {}
             for model, shape in (("target", w.target), ("draft", w.draft if self.has_draft else None)):
                 if shape is None:

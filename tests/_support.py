@@ -96,3 +96,46 @@ def check_argmax_rows(gpu_tokens, oracle_logits, tol: float = MARGIN):
         else:
             assert top - z[j, int(t)] <= tol * abs(top), f"row {j}: gpu {t} not near-max"
     return pinned
+
+
+def pending_candidates(w: W.Workload, b: int, n: int = 8):
+    """The workload's own first pending token, then seeded alternatives."""
+    rng = np.random.default_rng([w.seed + 77, b])
+    return [W.first_pending_token(w, b)] + [int(t) for t in rng.integers(0, w.vocab, size=n - 1)]
+
+
+def pinned_greedy_drafts(w: W.Workload, b: int, T, k: int, kv=None, seed: int = 0):
+    """Reseed the pending token until the oracle's greedy continuation has its
+    first k+1 rows pinned (top-1/top-2 margin above MARGIN), then build K
+    drafts = the first k greedy tokens followed by tokens that differ from the
+    greedy token at position k+1, so that l = k exactly.  Returns
+    (pending, drafts [K] int32, greedy trace [k+1], oracle logits of those rows)."""
+    rng = np.random.default_rng(seed)
+    for p in pending_candidates(w, b):
+        seq = oracle_sequence(w, b, T, None, kv=kv, with_draft=False, pending=p)
+        trace, rows = [], []
+        for _ in range(k + 1):
+            res = seq.verify([])
+            if margin(res.logits)[0] <= MARGIN:
+                break
+            trace.append(int(res.committed[0]))
+            rows.append(res.logits[0])
+        if len(trace) < k + 1:
+            continue
+        d = rng.integers(0, w.vocab, size=w.K).astype(np.int32)
+        d[:k] = trace[:k]
+        if k < w.K and d[k] == trace[k]:
+            d[k] = (trace[k] + 1) % w.vocab
+        return p, d, trace, np.stack(rows)
+    raise AssertionError("no candidate pending token gives pinned greedy rows")
+
+
+def assert_verify_matches(ref, drafts, coms, acc, k):
+    """Bit-exact accept length and committed tokens against the oracle's
+    verify, whose rows 0..k must be pinned (asserted, not assumed)."""
+    pinned = margin(ref.logits) > MARGIN
+    assert pinned[:ref.accept_len + 1].all(), "oracle rows 0..l not pinned"
+    assert ref.accept_len == k, (ref.accept_len, k)
+    assert int(acc) == ref.accept_len, (int(acc), ref.accept_len)
+    assert list(coms) == list(ref.committed), (list(coms), ref.committed)
+    assert list(coms[:k]) == [int(t) for t in drafts[:k]]

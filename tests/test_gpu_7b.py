@@ -6,10 +6,14 @@ benchmark times (batch 1, K = 8, 9 verify rows).
     (logits, greedy tokens, accept length, new K/V rows, position ids);
   * the 2-layer FlatRoPE draft at that width, against the oracle;
   * 4 target layers with the full 152064-token tied head over the 4096-token
-    prompt, against the oracle;
-  * the full 28-layer verify: the speculative output equals greedy decoding
-    bit for bit (a property that holds at any size; the oracle would need
-    minutes for 28 layers).
+    prompt, against the oracle (l = 2 and the bonus token bit for bit);
+  * the full 28-layer verify over the 4096-token prompt against the oracle
+    (logits of every row, l and commits bit for bit, first and last layers'
+    new K/V rows);
+  * the full 28-layer speculative loop equals greedy decoding bit for bit.
+
+Wherever l and the committed tokens are compared, the pending token is
+reseeded until the oracle's rows 0..l are pinned, and that is asserted.
 """
 import dataclasses
 
@@ -58,20 +62,18 @@ def c2():
 @pytest.mark.parametrize("K", [8, 15])
 def test_one_layer_verify_against_oracle(c2, K):
     # K = 15: 16 verify rows, a full MFMA row block (every row of the packed
-    # kernels' operands live, the streamed down-projection input at 16 rows)
+    # kernels' operands live, the streamed down-projection input at 16 rows).
+    # The pending token is reseeded until the oracle's first four greedy rows
+    # are pinned; the drafts copy three greedy tokens, so l = 3 is asserted
+    # bit for bit together with the bonus token.
     w, hp, T = c2
     w = w.with_(K=K)
-    s = _session(w, provider=hp)
+    pend, drafts, trace, _ = S.pinned_greedy_drafts(w, 0, T, k=3, seed=21)
+    s = _session(w, provider=hp, pending_tokens=[pend])
     P = w.seqs[0].prefix_len
     L = P + w.K + 1
     assert np.array_equal(s.positions(0, L), OP.target_positions(L, _blocks(w)))
-    rng = np.random.default_rng(21)
-    drafts = rng.integers(0, w.vocab, size=w.K).astype(np.int32)
-    seq = S.oracle_sequence(w, 0, T, None, with_draft=False)
-    # make the first three drafts the oracle's own greedy tokens so l > 0 is exercised
-    probe = S.oracle_sequence(w, 0, T, None, with_draft=False)
-    greedy = OS.greedy_trace(probe, 3)
-    drafts[:3] = greedy
+    seq = S.oracle_sequence(w, 0, T, None, with_draft=False, pending=pend)
     s.verify(drafts[None, :], logits=True)
     s.commit()
     ref = seq.verify(drafts)
@@ -79,11 +81,10 @@ def test_one_layer_verify_against_oracle(c2, K):
     for j in range(w.K + 1):
         assert S.normwise_err(gl[j], ref.logits[j]) <= S.LOGIT_RTOL, j
     coms, acc, fin = s.committed()
-    l = int(acc[0])
-    pinned = S.margin(ref.logits) > S.MARGIN
-    if pinned[:ref.accept_len + 1].all():
-        assert l == ref.accept_len and coms[0] == ref.committed
-    assert coms[0][:l] == list(drafts[:l])
+    S.assert_verify_matches(ref, drafts, coms[0], acc[0], k=3)
+    assert coms[0] == trace
+    st = s.state(0)
+    assert st["seq_len"] == P + 4 and st["pending"] == trace[3]
     for li in range(w.target.layers):
         for which, ref_c in ((0, seq.tc.k[li]), (1, seq.tc.v[li])):
             got = ON.decode(s.kv(0, 0, li, which, P, w.K + 1))
@@ -120,14 +121,15 @@ def test_two_layer_flatrope_draft_against_oracle():
 
 
 def test_four_layers_with_full_vocabulary_against_oracle():
+    # full 152064-token head: the pending token is reseeded until the oracle's
+    # first three greedy rows are pinned, so l = 2 and the bonus are asserted
     base = W.get("C3")
     w = base.with_(target=dataclasses.replace(base.target, layers=4), draft=None)
     src = W.DeviceWeights(w)
-    s = _session(w, source="device", provider=src)
-    T, _ = S.oracle_decoders(w, src, cache_weights=False)
-    seq = S.oracle_sequence(w, 0, T, None, kv=S.device_kv, with_draft=False)
-    rng = np.random.default_rng(31)
-    drafts = rng.integers(0, w.vocab, size=w.K).astype(np.int32)
+    T, _ = S.oracle_decoders(w, src, cache_weights=True)
+    pend, drafts, trace, _ = S.pinned_greedy_drafts(w, 0, T, k=2, kv=S.device_kv, seed=31)
+    s = _session(w, source="device", provider=src, pending_tokens=[pend])
+    seq = S.oracle_sequence(w, 0, T, None, kv=S.device_kv, with_draft=False, pending=pend)
     s.verify(drafts[None, :], logits=True)
     s.commit()
     ref = seq.verify(drafts)
@@ -135,9 +137,86 @@ def test_four_layers_with_full_vocabulary_against_oracle():
     for j in range(w.K + 1):
         assert S.normwise_err(gl[j], ref.logits[j]) <= S.LOGIT_RTOL, j
     coms, acc, fin = s.committed()
-    l = int(acc[0])
-    assert coms[0][:l] == list(drafts[:l])
-    S.check_argmax_rows(coms[0][l:l + 1], ref.logits[l:l + 1])
+    S.assert_verify_matches(ref, drafts, coms[0], acc[0], k=2)
+    assert coms[0] == trace
+    s.close()
+
+
+@pytest.fixture(scope="module")
+def c3_oracle():
+    """The oracle's verify of the 28-layer workload with random drafts, for a
+    pending token whose row 0 is pinned (shared by both execution paths).
+
+    Tolerance at this depth.  Any implementation that stores activations in
+    bf16 (the projections' inputs, q/k/v and the KV cache, the attention and
+    SwiGLU outputs) departs from exact arithmetic by the rounding noise of
+    that format, and through 28 layers this noise alone exceeds 2e-2: the
+    oracle's own mirror mode (bf16 at those points, float64 elsewhere) differs
+    from the plain float64 oracle by d_fmt ~ 2.7e-2 on these rows.  (Rounding
+    flips make it chaotic: a 1e-7 change of the input moves the mirror
+    oracle's logits by ~2.8e-2, the plain oracle's by 7.6e-7.)  So the bar
+    here is tau = max(2e-2, 1.5 d_fmt), computed from the oracle in this test,
+    and a row is pinned when its top-1/top-2 margin exceeds tau."""
+    import psutil
+    w = W.get("C3").with_(draft=None)
+    src = W.DeviceWeights(w)
+    # the float64 layer cache (about 57 GB) only where the host has room
+    big = psutil.virtual_memory().available > 150 * 2**30
+    T, _ = S.oracle_decoders(w, src, cache_weights=big)
+    rng = np.random.default_rng(41)
+    drafts = rng.integers(0, w.vocab, size=w.K).astype(np.int32)
+
+    def verify(pend, mirror):
+        T.mirror = mirror
+        try:
+            seq = S.oracle_sequence(w, 0, T, None, kv=S.device_kv, with_draft=False, pending=pend)
+            return seq, seq.verify(drafts)
+        finally:
+            T.mirror = False
+
+    for pend in S.pending_candidates(w, 0, n=6):
+        seq, ref = verify(pend, False)
+        _, fmt = verify(pend, True)
+        d_fmt = max(S.normwise_err(fmt.logits[j], ref.logits[j]) for j in range(w.K + 1))
+        tau = max(S.LOGIT_RTOL, 1.5 * d_fmt)
+        mg = S.margin(ref.logits)[0]
+        print(f"pending {pend}: row-0 margin {mg:.4f}, d_fmt {d_fmt:.3e}, tau {tau:.3e}, l = {ref.accept_len}",
+              flush=True)
+        if mg > tau and ref.accept_len == 0:
+            break
+    else:
+        raise AssertionError("no candidate pending token gives a row 0 pinned at tau")
+    P = w.seqs[0].prefix_len
+    kv = {(li, which): c[P:P + w.K + 1].copy() for li in (0, w.target.layers - 1)
+          for which, c in ((0, seq.tc.k[li]), (1, seq.tc.v[li]))}
+    return w, src, pend, drafts, ref, kv, tau
+
+
+def test_full_28_layer_verify_against_oracle(c3_oracle):
+    """The timed verify itself: 28 layers, the 152064-token head, the
+    4096-token prompt, 9 rows, against the plain float64 oracle.  Logits of
+    every row within tau (see c3_oracle), l and the committed tokens bit for
+    bit (the pending token is reseeded until the oracle's row 0 is pinned at
+    tau), the first layer's new K/V rows within 2e-2 and the last layer's
+    within tau."""
+    w, src, pend, drafts, ref, kv, tau = c3_oracle
+    s = _session(w, source="device", provider=src, pending_tokens=[pend])
+    s.verify(drafts[None, :], logits=True)
+    s.commit()
+    gl = s.logits[0].float().cpu().numpy()
+    errs = [S.normwise_err(gl[j], ref.logits[j]) for j in range(w.K + 1)]
+    print(f"28 layers: logit error max {max(errs):.3e} (tau {tau:.3e})", flush=True)
+    for j in range(w.K + 1):
+        assert errs[j] <= tau, (j, errs[j], tau)
+    coms, acc, fin = s.committed()
+    assert S.margin(ref.logits)[0] > tau
+    assert int(acc[0]) == ref.accept_len == 0
+    assert list(coms[0]) == list(ref.committed)
+    P = w.seqs[0].prefix_len
+    for (li, which), want in kv.items():
+        got = ON.decode(s.kv(0, 0, li, which, P, w.K + 1))
+        bar = S.LOGIT_RTOL if li == 0 else tau
+        assert S.normwise_err(got, want) <= bar, (li, which)
     s.close()
 
 

@@ -429,3 +429,92 @@ def test_requested_execution_path_runs(c1, path):
     assert B.spec_debug_path(s.ctx) == path
     assert n_qkv == w.target.layers + w.K * w.draft.layers
     s.close()
+
+
+class _EditedEmbed:
+    """The workload's weights with the tied embedding edited by `edit`."""
+
+    def __init__(self, base, edit):
+        self.base, self.edit = base, edit
+
+    def get(self, model, layer, name):
+        a = self.base.get(model, layer, name)
+        return self.edit(a.copy()) if name == "embed" else a
+
+
+@pytest.mark.parametrize("direction", ["copy_up", "copy_down"])
+def test_exact_argmax_tie_goes_to_the_lowest_index(c1, direction):
+    """Eq. verify's greedy argmax on exact ties (reading: lowest index wins).
+    Copying the embedding row of row 0's greedy token v into another row u
+    makes logits z[v] and z[u] bit-equal on both sides; the committed bonus
+    token must then be min(u, v), with u in another LM-head tile and
+    workgroup, above or below v."""
+    w, hp = c1[0], c1[1]
+    rng = np.random.default_rng(51)
+    drafts = None
+    for pend in S.pending_candidates(w, 0):
+        T, _ = S.oracle_decoders(w, hp)
+        z0 = S.oracle_sequence(w, 0, T, None, with_draft=False, pending=pend).verify([]).logits[0]
+        v = int(np.argmax(z0))
+        if S.margin(z0[None, :])[0] <= S.MARGIN:
+            continue
+        u = (v + 16 * 7 + 3) % w.vocab if direction == "copy_up" else (v - 16 * 7 - 3) % w.vocab
+        if pend == u or (direction == "copy_up") != (u > v):
+            continue
+        drafts = rng.integers(0, w.vocab, size=w.K).astype(np.int32)
+        drafts[drafts == u] = (u + 1) % w.vocab
+        drafts[drafts == v] = (v + 1) % w.vocab
+        break
+    assert drafts is not None
+
+    def edit(E):
+        E[u] = E[v]
+        return E
+
+    prov = _EditedEmbed(hp, edit)
+    T, _ = S.oracle_decoders(w, prov)
+    ref = S.oracle_sequence(w, 0, T, None, with_draft=False, pending=pend).verify(drafts)
+    assert ref.logits[0, u] == ref.logits[0, v]
+    want = min(u, v)
+    assert ref.rstar[0] == want and ref.accept_len == 0
+    s = _session(w, provider=prov, pending_tokens=[pend])
+    s.verify(drafts[None, :], logits=True)
+    s.commit()
+    zb = s.logits[0, 0].view(s.torch.int16).cpu().numpy()
+    assert zb[u] == zb[v]
+    coms, acc, fin = s.committed()
+    assert int(acc[0]) == 0 and coms[0] == [want], (coms[0], u, v)
+    assert s.sync() == 0
+    s.close()
+
+
+def test_nan_logits_are_reported_and_skipped(c1):
+    """NaN logits count as -inf in the argmax and set SPEC_E_NUMERIC, which
+    spec_sync reports (reading of Eq. verify's argmax on invalid values)."""
+    from paper_2606_31160_amd import binding as B
+    w, hp = c1[0], c1[1]
+    pend = W.first_pending_token(w, 0)
+    rng = np.random.default_rng(52)
+    drafts = rng.integers(0, w.vocab, size=w.K).astype(np.int32)
+    jn = next(j for j in range(w.vocab - 1, 0, -1) if j != pend and j not in set(drafts.tolist()))
+
+    def edit(E):
+        E[jn] = 0x7FC0            # a quiet NaN in every column of one row
+        return E
+
+    prov = _EditedEmbed(hp, edit)
+    T, _ = S.oracle_decoders(w, prov)
+    ref = S.oracle_sequence(w, 0, T, None, with_draft=False, pending=pend).verify(drafts)
+    assert np.isnan(ref.logits[:, jn]).all() and not np.isnan(np.delete(ref.logits, jn, axis=1)).any()
+    s = _session(w, provider=prov)
+    s.verify(drafts[None, :])
+    s.commit()
+    with pytest.raises(B.SpecError) as e:
+        s.sync()
+    assert e.value.status == 6
+    coms, acc, fin = s.committed()
+    z = np.delete(ref.logits, jn, axis=1)
+    if S.margin(z[:1])[0] > S.MARGIN:
+        assert coms[0][-1] == ref.committed[-1] and int(acc[0]) == ref.accept_len
+    assert jn not in coms[0]
+    s.close()

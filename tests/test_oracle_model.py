@@ -42,6 +42,20 @@ def test_rmsnorm_unit_rms_and_scale_invariance():
     assert np.allclose(M.rmsnorm(x, g, 0.0), y * g, rtol=1e-13)
 
 
+def test_normed_pair_is_rmsnorm_times_gain():
+    # the (x * g, 1/rms) pair the forward pass projects equals RMSNorm(x) * g
+    w = _tiny()
+    T, _ = S.oracle_decoders(w, W.HostWeights(w))
+    rng = np.random.default_rng(14)
+    x = rng.standard_normal((3, w.target.hidden)) * 5
+    g = 1 + 0.1 * rng.standard_normal(w.target.hidden)
+    a, inv = T._normed(x, g)
+    assert np.allclose(a * inv, M.rmsnorm(x, g, w.target.rms_eps), rtol=1e-13, atol=1e-15)
+    T.mirror = True
+    am, _ = T._normed(x, g)
+    assert np.array_equal(am, numerics.mirror(x * g))
+
+
 def test_silu_is_x_times_logistic():
     x = np.linspace(-30, 30, 101)
     assert np.allclose(M.silu(x), x * scipy.special.expit(x), rtol=1e-13, atol=1e-300)

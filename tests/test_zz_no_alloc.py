@@ -92,12 +92,13 @@ def test_scratch_verify_equals_verify_on_two_calls_then_a_smaller_one():
 
 
 def test_scratch_verify_refuses_a_pass_larger_than_the_array():
-    # 16 sequences of the two-frame 3328-token prompt at 7B width, 144 rows:
-    # the split-KV partials alone exceed the static array
+    # 16 sequences of the two-frame 3328-token prompt at 7B width with the
+    # 152064-token head, 144 rows: the logits staging alone (144 x 152064
+    # bf16) exceeds the static array
     from paper_2606_31160_amd import binding as B
     from paper_2606_31160_amd.harness import Session
     c2 = W.get("C2")
-    w = c2.with_(draft=None, seqs=tuple([c2.seqs[0]] * 16), p_accept=tuple([0.75] * 16))
+    w = c2.with_(draft=None, vocab=152064, seqs=tuple([c2.seqs[0]] * 16), p_accept=tuple([0.75] * 16))
     assert w.batch * (w.K + 1) == 144
     s = Session(w, source="device", provider=W.DeviceWeights(w))
     with pytest.raises(B.SpecError) as e:
