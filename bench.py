@@ -364,7 +364,7 @@ def paper_backbone(steps=10):
     path = B.spec_debug_path(s.ctx)
     s.close()
     return {"workload": "36 layers, hidden 4096, 32/8 heads, SwiGLU 12288, vocab 151936, interleaved M-RoPE, "
-                        "K=16 (17 rows), prompt 4096", "path": path + " (batched-row GEMM)",
+                        "K=16 (17 rows), prompt 4096", "path": path + " (two 16-row MFMA blocks per weight block)",
             "verify_us": round(v_us, 1), "bytes": int(by),
             "hbm_frac": round(by / (v_us * 1e-6) / 1e9 / PEAK_HBM_GBS, 4)}
 

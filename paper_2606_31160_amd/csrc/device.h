@@ -41,6 +41,39 @@ __device__ __forceinline__ f32x4 mfma16x16x32(u32x4 a, u32x4 b, f32x4 c) {
                                                  0, 0, 0);
 }
 
+// Device-coherent accesses for data handed between workgroups of one launch
+// (possibly on different XCDs): relaxed agent-scope atomic loads and stores,
+// which go to the device's coherence point instead of the XCD's L2.  A writer
+// waits for its stores to complete (s_waitcnt) before it signals; a reader
+// that saw the signal reads with ld_coh*.  No cache-wide writeback or
+// invalidate is involved.
+#define SD_GLOBAL __attribute__((address_space(1)))
+__device__ __forceinline__ f32x4 ld_coh4(const float* p) {
+  const SD_GLOBAL uint64_t* q = (const SD_GLOBAL uint64_t*)(p);
+  const uint64_t a = __hip_atomic_load(q, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  const uint64_t b = __hip_atomic_load(q + 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  return f32x4{__uint_as_float((uint32_t)a), __uint_as_float((uint32_t)(a >> 32)), __uint_as_float((uint32_t)b),
+               __uint_as_float((uint32_t)(b >> 32))};
+}
+__device__ __forceinline__ float2 ld_coh2(const float* p) {
+  const uint64_t a =
+      __hip_atomic_load((const SD_GLOBAL uint64_t*)(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  return make_float2(__uint_as_float((uint32_t)a), __uint_as_float((uint32_t)(a >> 32)));
+}
+__device__ __forceinline__ void st_coh4(float* p, f32x4 v) {
+  SD_GLOBAL uint64_t* q = (SD_GLOBAL uint64_t*)(p);
+  __hip_atomic_store(q, (uint64_t)__float_as_uint(v.x) | ((uint64_t)__float_as_uint(v.y) << 32), __ATOMIC_RELAXED,
+                     __HIP_MEMORY_SCOPE_AGENT);
+  __hip_atomic_store(q + 1, (uint64_t)__float_as_uint(v.z) | ((uint64_t)__float_as_uint(v.w) << 32),
+                     __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ void st_coh2(float* p, float x, float y) {
+  __hip_atomic_store((SD_GLOBAL uint64_t*)(p), (uint64_t)__float_as_uint(x) | ((uint64_t)__float_as_uint(y) << 32),
+                     __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+// Waits until every vector memory access of the wave has completed.
+__device__ __forceinline__ void wait_vmem() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
+
 // Block-wide sum of one float per thread (blockDim.x a multiple of 64, <= 1024),
 // in a fixed order.
 __device__ float block_sum(float v, float* sh) {

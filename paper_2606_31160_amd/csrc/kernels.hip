@@ -1000,10 +1000,10 @@ __global__ __launch_bounds__(256) void k_attn(AttnArgs a) {
 }
 
 // Cache pages per attention split: one while the one-page grid has at most
-// about kAttnWgs workgroups, else enough pages per split to bring the grid
+// ATTN_TARGET_WGS workgroups, else enough pages per split to bring the grid
 // down to about that size (fewer partials to write and merge).
 #ifndef ATTN_TARGET_WGS
-#define ATTN_TARGET_WGS 256
+#define ATTN_TARGET_WGS 2048
 #endif
 int attn_pages_per_split(size_t one_page_workgroups) {
   return (int)std::max<size_t>(1, one_page_workgroups / ATTN_TARGET_WGS);

@@ -349,9 +349,9 @@ size_t carve(Ctx& c, const spec_config* cfg, const spec_seq_init* seqs, bool has
   c.ncu = num_cus();
   {
     // attention splits of np cache pages each (the target's grid decides)
-    const int G = cfg->target.q_heads / cfg->target.kv_heads;
-    const int rb = (L.R * G + 63) / 64;
-    c.attn_np = attn_pages_per_split((size_t)L.splits * cfg->target.kv_heads * rb * L.B);
+    // from the sequence count and cache size only, not the pass's row count, so
+    // that a row's attention sum is grouped the same way for every K
+    c.attn_np = attn_pages_per_split((size_t)L.splits * cfg->target.kv_heads * L.B);
     c.attn_splits = (L.splits + c.attn_np - 1) / c.attn_np;
   }
   c.tgt.d = cfg->target;

@@ -1,5 +1,5 @@
 // Balanced weight-streaming GEMV over tile-packed weights (sgemv.hip) for
-// passes of at most 16 rows: one kernel per projection, with the consumer's
+// passes of at most 32 rows (one or two MFMA row blocks): one kernel per projection, with the consumer's
 // elementwise step and, for the down projection, the k-slice reduction,
 // residual and next-norm input fused in.
 #pragma once
@@ -14,11 +14,12 @@ namespace specdec {
 constexpr int kSgWorkers = 15;                // weight-streaming waves per workgroup
 constexpr int kSgWaves = kSgWorkers + 1;      // + the control wave
 constexpr int kSgDepth = 8;                   // k-steps each worker keeps in flight (one tile's share)
+constexpr int kSgDepthMax = 9;                // ... for inputs of up to 15 * 9 steps (4096 wide)
 #ifndef SG_DEPTH_XS
 #define SG_DEPTH_XS 8
 #endif
 constexpr int kSgDepthXs = SG_DEPTH_XS;       // k-steps in flight per worker when x is streamed
-constexpr int kSgMaxRows = 16;                // rows of one MFMA block
+constexpr int kSgMaxRows = 32;                // rows of a pass: two MFMA row blocks
 constexpr int kSgMaxSpan = kSgWorkers * kSgDepth;   // k-steps of one tile slice
 constexpr int kSgPendMax = 64;                // units one workgroup may have to finish
 
@@ -45,6 +46,7 @@ struct SgJob {
   int ntiles, T;
   int S, G;               // k-slices of T; workgroups per slice (grid = S*G)
   int xs;                 // x streamed with the weights (long k-ranges) instead of held in registers
+  int dep9;               // x in registers, 9 steps per worker (inputs of 121..135 steps)
   int kmax;               // partial slots per workgroup
   int units;              // fixup units (tiles, or gate/up tile pairs)
   const bf16_t* x;        // input rows [M][ldx], Kd valid columns; or step-major (xpk)
@@ -54,7 +56,7 @@ struct SgJob {
   int Hn, mpad;
   float eps;
   const SeqState* st;
-  float* part;            // partial tiles [S*G][kmax][2][64] x float4
+  float* part;            // partial tiles [S*G][kmax][row blocks][2][64] x float4
   unsigned* cnt;          // [units] arrival counters, zero between launches
   // SG_ROPE: rotation at each row's position, queries, K and V^T cache append
   bf16_t* q;

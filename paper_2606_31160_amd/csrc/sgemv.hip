@@ -1,4 +1,4 @@
-// Balanced weight-streaming GEMV on gfx950 for passes of at most 16 rows.
+// Balanced weight-streaming GEMV on gfx950 for passes of at most 32 rows.
 //
 // y[m][n] = sum_k x[m][k] W[n][k] over tile-packed weights (sgemv.h): each
 // 16-row x 32-column MFMA operand block is 1 KB contiguous, so every wave
@@ -57,8 +57,6 @@ namespace specdec {
 
 namespace {
 
-#define SG_GLOBAL __attribute__((address_space(1)))
-
 constexpr int kOut = 0x7FFFFF00;          // buffer offset past every packed matrix (they are < kOut bytes)
 constexpr int kRsrcWord3 = 0x00020000;    // raw buffer resource, 32-bit data
 // Cache policy of the weight loads: non-temporal.  Each weight byte is read
@@ -66,20 +64,14 @@ constexpr int kRsrcWord3 = 0x00020000;    // raw buffer resource, 32-bit data
 // the large projections against 5.7-6.1 TB/s for default-policy loads.
 constexpr int kNt = 2;
 
-__device__ __forceinline__ f32x4 ld_coh(const float* p) {
-  const SG_GLOBAL uint64_t* q = (const SG_GLOBAL uint64_t*)(p);
-  const uint64_t a = __hip_atomic_load(q, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-  const uint64_t b = __hip_atomic_load(q + 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-  return f32x4{__uint_as_float((uint32_t)a), __uint_as_float((uint32_t)(a >> 32)), __uint_as_float((uint32_t)b),
-               __uint_as_float((uint32_t)(b >> 32))};
-}
 
 // Workgroup barrier that waits for this wave's LDS operations only (global
 // loads and stores stay in flight).  The memory clobber keeps the compiler
 // from moving LDS accesses across it.
 __device__ __forceinline__ void lds_barrier() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
 
-// Per-lane row facts the control wave needs (lane's row m = lane & 15).
+// Per-lane row facts the control wave needs (lane's row m = lane % 16 + 16 rb
+// in row block rb).
 struct RowInfo {
   bool live;       // row m < M and inside its sequence's current row count
   int b, jr;       // sequence and row within it
@@ -94,9 +86,9 @@ struct RowInfo {
 };
 
 template <int EPI>
-__device__ __forceinline__ void epilogue(const SgJob& j, RowInfo& ri, int u, f32x4 ya, f32x4 yb, f32x4 pa,
+__device__ __forceinline__ void epilogue(const SgJob& j, RowInfo& ri, int rb, int u, f32x4 ya, f32x4 yb, f32x4 pa,
                                          u32x2 pb) {
-  const int lane = threadIdx.x & 63, m = lane & 15, grp = lane >> 4;
+  const int lane = threadIdx.x & 63, m = (lane & 15) + 16 * rb, grp = lane >> 4;
   const int M = j.M;
   if constexpr (EPI == SG_ROPE) {
     if (ri.live) {
@@ -199,8 +191,9 @@ __device__ __forceinline__ void epilogue(const SgJob& j, RowInfo& ri, int u, f32
 // Epilogue inputs of unit u that come from memory: the (cos, sin) of the
 // lane's two rotary pairs, or the residual and the norm gain of its 4 columns.
 template <int EPI>
-__device__ __forceinline__ void epilogue_inputs(const SgJob& j, const RowInfo& ri, int u, f32x4& pa, u32x2& pb) {
-  const int lane = threadIdx.x & 63, m = lane & 15, grp = lane >> 4;
+__device__ __forceinline__ void epilogue_inputs(const SgJob& j, const RowInfo& ri, int rb, int u, f32x4& pa,
+                                                u32x2& pb) {
+  const int lane = threadIdx.x & 63, m = (lane & 15) + 16 * rb, grp = lane >> 4;
   pa = f32x4{0.f, 0.f, 0.f, 0.f};
   pb = u32x2{0u, 0u};
   if constexpr (EPI == SG_ROPE) {
@@ -219,9 +212,14 @@ __device__ __forceinline__ void epilogue_inputs(const SgJob& j, const RowInfo& r
 // The job is a kernel argument (not a pointer to it) so that its fields
 // arrive with the launch: the weight and activation loads do not wait for a
 // memory round trip to fetch their addresses first.
-template <int EPI, bool XS>
+//
+// MB row blocks of 16 rows (passes of up to 16 * MB rows): every weight block
+// a worker loads feeds one MFMA per row block, and each output's sum is formed
+// exactly as with one row block (the same k-step chunks per worker, the same
+// order of the partial tiles), so a row's result does not depend on MB.
+template <int EPI, bool XS, int MB, int DEPN>
 __global__ __launch_bounds__(kSgWaves * 64) void k_sgemv(const SgJob j) {
-  constexpr int DEP = XS ? kSgDepthXs : kSgDepth;   // rolling-buffer slots per worker
+  constexpr int DEP = XS ? kSgDepthXs : DEPN;   // rolling-buffer slots per worker (x in registers: steps per worker)
   extern __shared__ __align__(16) unsigned char lds[];
   constexpr bool kPair = EPI == SG_SWIGLU;
   constexpr int TPU = kPair ? 2 : 1;   // tiles per unit
@@ -237,9 +235,9 @@ __global__ __launch_bounds__(kSgWaves * 64) void k_sgemv(const SgJob j) {
   const int units = j.ntiles / TPU;
   const int n_it = (units / G + (gi < units % G ? 1 : 0)) * TPU;   // tiles of this workgroup
   auto tile_of = [&](int it) { return ((it / TPU) * G + gi) * TPU + it % TPU; };
-  f32x4* red = reinterpret_cast<f32x4*>(lds);                                          // [2][workers][64]
-  int* pend = reinterpret_cast<int*>(lds + 2 * kSgWorkers * 64 * 16);                  // [kSgPendMax + 4]
-  float* rms_sh = reinterpret_cast<float*>(pend + kSgPendMax + 4);                     // [16] 1/rms per row
+  f32x4* red = reinterpret_cast<f32x4*>(lds);                                   // [2][MB][workers][64]
+  int* pend = reinterpret_cast<int*>(lds + 2 * MB * kSgWorkers * 64 * 16);      // [kSgPendMax + 4]
+  float* rms_sh = reinterpret_cast<float*>(pend + kSgPendMax + 4);              // [16 MB] 1/rms per row
 
   // Worker w owns k-steps [ws0, ws0 + nst) of every tile of this slice.
   const int wi = wave - 1;
@@ -248,37 +246,35 @@ __global__ __launch_bounds__(kSgWaves * 64) void k_sgemv(const SgJob j) {
     ws0 = k0 + span * wi / kSgWorkers;
     nst = k0 + span * (wi + 1) / kSgWorkers - ws0;
   }
-  const int m = lane & 15, grp = lane >> 4;
-  const bool mok = m < M;
+  const int m0 = lane & 15, grp = lane >> 4;
 
   // Issue order (vector memory returns in order per wave): a worker first
   // loads its x operands (the same for every tile, so they stay in registers:
   // lane (m, g) holds x[m][32 s + 8 g .. +8] of its step s), then the first
   // tile's weights, so that the MFMAs can start as soon as weights arrive.
   // Rows of dead sequences are zeroed once the live mask is known.
-  u32x4 xv[DEP];
+  u32x4 xv[MB][DEP];
   const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(const_cast<bf16_t*>(j.w), 0,
                                                                       j.ntiles * T * 1024, kRsrcWord3);
   // x rows as a buffer (streamed x): an offset past it reads zeros
   const __amdgpu_buffer_rsrc_t rsx = __builtin_amdgcn_make_buffer_rsrc(
       const_cast<bf16_t*>(j.x), 0, j.xpk ? T * M * 64 : M * j.ldx * 2, kRsrcWord3);
-  bool xrow = mok;               // lane's x row is loaded (narrowed to live rows once they are known)
-  auto x_off = [&](int step) {   // byte offset of lane (m, grp)'s x operand of a k-step, or kOut
-    const int k = step * 32 + 8 * grp;
-    return (xrow && k < j.Kd) ? (j.xpk ? ((step * M + m) * 32 + 8 * grp) * 2 : (m * j.ldx + k) * 2) : kOut;
+  bool xrow[MB];                 // lane's x row of each block is loaded (narrowed to live rows once known)
+#pragma unroll
+  for (int rb = 0; rb < MB; ++rb) xrow[rb] = m0 + 16 * rb < M;
+  auto x_off = [&](int rb, int step) {   // byte offset of lane (m, grp)'s x operand of a k-step, or kOut
+    const int k = step * 32 + 8 * grp, m = m0 + 16 * rb;
+    return (xrow[rb] && k < j.Kd) ? (j.xpk ? ((step * M + m) * 32 + 8 * grp) * 2 : (m * j.ldx + k) * 2) : kOut;
   };
   const int lane_off = lane * 16;
   u32x4 wv[DEP];
   if (wave > 0) {
 #pragma unroll
-    for (int i = 0; i < DEP; ++i) {
-      const int k = (ws0 + i) * 32 + 8 * grp;
-      if constexpr (XS)
-        xv[i] = __builtin_amdgcn_raw_buffer_load_b128(rsx, i < nst ? x_off(ws0 + i) : kOut, 0, 0);
-      else
-        xv[i] = (i < nst && mok && k < j.Kd) ? *reinterpret_cast<const u32x4*>(j.x + (size_t)m * j.ldx + k)
-                                               : u32x4{0, 0, 0, 0};
-    }
+    for (int rb = 0; rb < MB; ++rb)
+#pragma unroll
+      for (int i = 0; i < DEP; ++i) {
+        xv[rb][i] = __builtin_amdgcn_raw_buffer_load_b128(rsx, i < nst ? x_off(rb, ws0 + i) : kOut, 0, 0);
+      }
     if (n_it > 0) {
       const int v = (tile_of(0) * T + ws0) * 1024 + lane_off;
 #pragma unroll
@@ -295,77 +291,49 @@ __global__ __launch_bounds__(kSgWaves * 64) void k_sgemv(const SgJob j) {
       const int n = min(j.st[b].count, j.rps);
       if (n > 0) live |= ((1u << n) - 1u) << (b * j.rps);
     }
-    live &= (1u << M) - 1u;
+    if (M < 32) live &= (1u << M) - 1u;
   }
-  const bool xok = (live >> m) & 1;
-  xrow = mok && xok;   // streamed x: rows of dead sequences are not read at all
-  if (!XS && wave > 0 && !xok) {
+  bool xok[MB];
 #pragma unroll
-    for (int i = 0; i < DEP; ++i) xv[i] = u32x4{0, 0, 0, 0};
+  for (int rb = 0; rb < MB; ++rb) {
+    xok[rb] = (live >> (m0 + 16 * rb)) & 1;
+    xrow[rb] = xrow[rb] && xok[rb];   // streamed x: rows of dead sequences are not read at all
+  }
+  if (!XS && wave > 0) {
+#pragma unroll
+    for (int rb = 0; rb < MB; ++rb)
+      if (!xok[rb]) {
+#pragma unroll
+        for (int i = 0; i < DEP; ++i) xv[rb][i] = u32x4{0, 0, 0, 0};
+      }
   }
 
-  // per-row facts of the lane's row m (the control wave now; the other waves
-  // fill theirs before finishing split units)
-  RowInfo ri{};
-  auto row_info = [&]() {
-    ri.live = mok && ((live >> m) & 1);
-    ri.b = mok ? m / j.rps : 0;
-    ri.jr = m - ri.b * j.rps;
-    ri.count = j.st[ri.b].count;
-    ri.want_logits = j.st[ri.b].want_logits;
-    ri.inv_rms = 1.f;
-    ri.best = -INFINITY;
-    ri.bi = 0x7fffffff;
-    ri.nan = 0;
-    if constexpr (EPI == SG_ROPE) {
-      if (ri.live) {
-        ri.slot = j.st[ri.b].base + ri.jr;
-        ri.page = j.pt[ri.b * j.pps + ri.slot / kAttnChunk];
+  // per-row facts of the lane's rows (the control wave before its tile loop;
+  // every wave before finishing split units)
+  auto row_info = [&](RowInfo* ri) {
+#pragma unroll
+    for (int rb = 0; rb < MB; ++rb) {
+      RowInfo& r = ri[rb];
+      const int m = m0 + 16 * rb;
+      const bool mok = m < M;
+      r.live = mok && ((live >> m) & 1);
+      r.b = mok ? m / j.rps : 0;
+      r.jr = m - r.b * j.rps;
+      r.count = j.st[r.b].count;
+      r.want_logits = j.st[r.b].want_logits;
+      r.inv_rms = 1.f;
+      r.best = -INFINITY;
+      r.bi = 0x7fffffff;
+      r.nan = 0;
+      if constexpr (EPI == SG_ROPE) {
+        if (r.live) {
+          r.slot = j.st[r.b].base + r.jr;
+          r.page = j.pt[r.b * j.pps + r.slot / kAttnChunk];
+        }
       }
     }
   };
-  if (wave == 0) {
-    row_info();
-    // normalised inputs: 1/rms of row m from the producer's per-16-column
-    // sums of squares; lane (m, g) adds the sums t = g, g + 4, ... and the
-    // four lane groups are added in a fixed order
-    if constexpr (kNorm) {
-      // lane (t, q) reads rows 4q..4q+3 of sum t = lane / 4, 16 sums per
-      // load; the 16 lanes of each q are then added by an xor butterfly,
-      // which gives every lane bit-identical totals
-      const int ntt = j.Hn / kTile;
-      const int q = lane & 3;
-      f32x4 acc4 = f32x4{0.f, 0.f, 0.f, 0.f};
-      for (int t0 = lane >> 2; t0 < ntt; t0 += 16 * 8) {
-        f32x4 tmp[8];
-#pragma unroll
-        for (int b = 0; b < 8; ++b) {
-          const int tt = t0 + 16 * b;
-          tmp[b] = tt < ntt ? *reinterpret_cast<const f32x4*>(j.ss_in + (size_t)tt * j.mpad + 4 * q)
-                            : f32x4{0.f, 0.f, 0.f, 0.f};
-        }
-#pragma unroll
-        for (int b = 0; b < 8; ++b) acc4 += tmp[b];
-      }
-#pragma unroll
-      for (int o = 4; o < 64; o <<= 1) {
-        acc4.x += __shfl_xor(acc4.x, o);
-        acc4.y += __shfl_xor(acc4.y, o);
-        acc4.z += __shfl_xor(acc4.z, o);
-        acc4.w += __shfl_xor(acc4.w, o);
-      }
-      const int src = m >> 2;
-      const float c0 = __shfl(acc4.x, src), c1 = __shfl(acc4.y, src), c2 = __shfl(acc4.z, src),
-                  c3 = __shfl(acc4.w, src);
-      const int c = m & 3;
-      const float sum = c == 0 ? c0 : c == 1 ? c1 : c == 2 ? c2 : c3;
-      ri.inv_rms = rsqrtf(sum / j.Hn + j.eps);
-      if (lane < 16) rms_sh[lane] = ri.inv_rms;
-    }
-  }
-
   int npend = 0;
-  f32x4 ya = f32x4{0.f, 0.f, 0.f, 0.f}, yb = ya;
   // The workers and the control wave run separate loops (the branch is on a
   // wave-uniform value) with one workgroup barrier per tile each, so that
   // the workers' code holds nothing but weight loads and MFMAs.  The barrier
@@ -376,7 +344,9 @@ __global__ __launch_bounds__(kSgWaves * 64) void k_sgemv(const SgJob j) {
     // x) with the same slot of the next group, or of the next tile's first
     const int NG = (nst + DEP - 1) / DEP;
     for (int it = 0; it < n_it; ++it) {
-      f32x4 acc = f32x4{0.f, 0.f, 0.f, 0.f};
+      f32x4 acc[MB];
+#pragma unroll
+      for (int rb = 0; rb < MB; ++rb) acc[rb] = f32x4{0.f, 0.f, 0.f, 0.f};
       for (int g = 0; g < NG; ++g) {
         const bool lastg = g + 1 == NG;
         const int nit = lastg ? it + 1 : it, ng = lastg ? 0 : g + 1;
@@ -384,71 +354,137 @@ __global__ __launch_bounds__(kSgWaves * 64) void k_sgemv(const SgJob j) {
         const int vn = (tile_of(nv ? nit : it) * T + ws0 + ng * DEP) * 1024 + lane_off;
 #pragma unroll
         for (int i = 0; i < DEP; ++i) {
-          acc = mfma16x16x32(wv[i], xok ? xv[i] : u32x4{0, 0, 0, 0}, acc);
+#pragma unroll
+          for (int rb = 0; rb < MB; ++rb) acc[rb] = mfma16x16x32(wv[i], xok[rb] ? xv[rb][i] : u32x4{0, 0, 0, 0}, acc[rb]);
           const int sn = ng * DEP + i;
           const bool on = nv && sn < nst;
           wv[i] = __builtin_amdgcn_raw_buffer_load_b128(rs, on ? vn + 1024 * i : kOut, 0, kNt);
-          xv[i] = __builtin_amdgcn_raw_buffer_load_b128(rsx, on ? x_off(ws0 + sn) : kOut, 0, 0);
+#pragma unroll
+          for (int rb = 0; rb < MB; ++rb)
+            xv[rb][i] = __builtin_amdgcn_raw_buffer_load_b128(rsx, on ? x_off(rb, ws0 + sn) : kOut, 0, 0);
         }
       }
-      red[((it & 1) * kSgWorkers + wi) * 64 + lane] = acc;
+#pragma unroll
+      for (int rb = 0; rb < MB; ++rb) red[(((it & 1) * MB + rb) * kSgWorkers + wi) * 64 + lane] = acc[rb];
       lds_barrier();
     }
   } else if (wave > 0) {
     for (int it = 0; it < n_it; ++it) {
       const bool na = it + 1 < n_it;
       const int vn = (tile_of(it + 1) * T + ws0) * 1024 + lane_off;
-      f32x4 acc = f32x4{0.f, 0.f, 0.f, 0.f};
+      f32x4 acc[MB];
+#pragma unroll
+      for (int rb = 0; rb < MB; ++rb) acc[rb] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
       for (int i = 0; i < DEP; ++i) {
         const bool on = i < nst;
-        acc = mfma16x16x32(wv[i], xv[i], acc);
+#pragma unroll
+        for (int rb = 0; rb < MB; ++rb) acc[rb] = mfma16x16x32(wv[i], xv[rb][i], acc[rb]);
         wv[i] = __builtin_amdgcn_raw_buffer_load_b128(rs, (na && on) ? vn + 1024 * i : kOut, 0, kNt);
       }
-      red[((it & 1) * kSgWorkers + wi) * 64 + lane] = acc;
+#pragma unroll
+      for (int rb = 0; rb < MB; ++rb) red[(((it & 1) * MB + rb) * kSgWorkers + wi) * 64 + lane] = acc[rb];
       lds_barrier();
     }
   } else {
+    RowInfo ri[MB];
+    row_info(ri);
+    // normalised inputs: 1/rms of each row from the producer's per-16-column
+    // sums of squares: lane (t, q) reads rows 16 rb + 4q .. +3 of sum t =
+    // lane / 4, 16 sums per load; the 16 lanes of each q are then added by an
+    // xor butterfly, which gives every lane bit-identical totals
+    if constexpr (kNorm) {
+      const int ntt = j.Hn / kTile;
+      const int q = lane & 3;
+#pragma unroll
+      for (int rb = 0; rb < MB; ++rb) {
+        f32x4 acc4 = f32x4{0.f, 0.f, 0.f, 0.f};
+        for (int t0 = lane >> 2; t0 < ntt; t0 += 16 * 8) {
+          f32x4 tmp[8];
+#pragma unroll
+          for (int b = 0; b < 8; ++b) {
+            const int tt = t0 + 16 * b;
+            tmp[b] = tt < ntt ? *reinterpret_cast<const f32x4*>(j.ss_in + (size_t)tt * j.mpad + 16 * rb + 4 * q)
+                              : f32x4{0.f, 0.f, 0.f, 0.f};
+          }
+#pragma unroll
+          for (int b = 0; b < 8; ++b) acc4 += tmp[b];
+        }
+#pragma unroll
+        for (int o = 4; o < 64; o <<= 1) {
+          acc4.x += __shfl_xor(acc4.x, o);
+          acc4.y += __shfl_xor(acc4.y, o);
+          acc4.z += __shfl_xor(acc4.z, o);
+          acc4.w += __shfl_xor(acc4.w, o);
+        }
+        const int src = m0 >> 2;
+        const float c0 = __shfl(acc4.x, src), c1 = __shfl(acc4.y, src), c2 = __shfl(acc4.z, src),
+                    c3 = __shfl(acc4.w, src);
+        const int c = m0 & 3;
+        const float sum = c == 0 ? c0 : c == 1 ? c1 : c == 2 ? c2 : c3;
+        ri[rb].inv_rms = rsqrtf(sum / j.Hn + j.eps);
+        if (lane < 16) rms_sh[16 * rb + lane] = ri[rb].inv_rms;
+      }
+    }
+    f32x4 ya[MB], yb[MB];
+#pragma unroll
+    for (int rb = 0; rb < MB; ++rb) ya[rb] = yb[rb] = f32x4{0.f, 0.f, 0.f, 0.f};
     for (int it = 0; it < n_it; ++it) {
       const int t = tile_of(it);
-      f32x4 pa;
-      u32x2 pb;
-      epilogue_inputs<EPI>(j, ri, t / TPU, pa, pb);   // in flight while the workers stream tile t
-      lds_barrier();
-      f32x4 y = red[((it & 1) * kSgWorkers) * 64 + lane];
+      f32x4 pa[MB];
+      u32x2 pb[MB];
 #pragma unroll
-      for (int w = 1; w < kSgWorkers; ++w) y += red[((it & 1) * kSgWorkers + w) * 64 + lane];
+      for (int rb = 0; rb < MB; ++rb)
+        epilogue_inputs<EPI>(j, ri[rb], rb, t / TPU, pa[rb], pb[rb]);   // in flight while the workers stream tile t
+      lds_barrier();
       const int u = t / TPU, half = t - u * TPU;
-      if (half == 0) {
-        ya = y;
-        yb = f32x4{0.f, 0.f, 0.f, 0.f};
-      } else {
-        yb = y;
+#pragma unroll
+      for (int rb = 0; rb < MB; ++rb) {
+        const f32x4* rr = red + ((it & 1) * MB + rb) * kSgWorkers * 64 + lane;
+        f32x4 y = rr[0];
+#pragma unroll
+        for (int w = 1; w < kSgWorkers; ++w) y += rr[w * 64];
+        if (half == 0) {
+          ya[rb] = y;
+          yb[rb] = f32x4{0.f, 0.f, 0.f, 0.f};
+        } else {
+          yb[rb] = y;
+        }
       }
       if (half == TPU - 1 || it == n_it - 1) {
         if (S == 1) {
-          epilogue<EPI>(j, ri, u, ya, yb, pa, pb);
+#pragma unroll
+          for (int rb = 0; rb < MB; ++rb) epilogue<EPI>(j, ri[rb], rb, u, ya[rb], yb[rb], pa[rb], pb[rb]);
         } else {
           const int k = it / TPU;   // partial slot: this workgroup's k-th unit
-          float* pp = j.part + (((size_t)blockIdx.x * j.kmax + k) * 2) * 256;
-          *reinterpret_cast<f32x4*>(pp + lane * 4) = ya;
-          if (kPair) *reinterpret_cast<f32x4*>(pp + 256 + lane * 4) = yb;
+#pragma unroll
+          for (int rb = 0; rb < MB; ++rb) {
+            float* pp = j.part + ((((size_t)blockIdx.x * j.kmax + k) * MB + rb) * 2) * 256;
+            *reinterpret_cast<f32x4*>(pp + lane * 4) = ya[rb];
+            if (kPair) *reinterpret_cast<f32x4*>(pp + 256 + lane * 4) = yb[rb];
+          }
           if (lane == 0) pend[npend] = u;
           ++npend;
         }
-        ya = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int rb = 0; rb < MB; ++rb) ya[rb] = f32x4{0.f, 0.f, 0.f, 0.f};
+      }
+    }
+    if constexpr (EPI == SG_ARGMAX) {
+      if (S == 1 && lane < 16) {   // lanes 0..15 hold rows 16 rb .. 16 rb + 15
+#pragma unroll
+        for (int rb = 0; rb < MB; ++rb) {
+          const int m = lane + 16 * rb;
+          if (m < M) {
+            j.amax_v[(size_t)gi * j.mpad + m] = ri[rb].best;
+            j.amax_i[(size_t)gi * j.mpad + m] = ri[rb].bi;
+            if (ri[rb].nan) atomicOr(const_cast<int32_t*>(&j.st[ri[rb].b].err), ERR_NUMERIC);
+          }
+        }
       }
     }
   }
 
-  if constexpr (EPI == SG_ARGMAX) {
-    const int m = lane & 15;
-    if (wave == 0 && S == 1 && lane < 16 && m < M) {   // lanes 0..15 hold rows 0..15
-      j.amax_v[(size_t)gi * j.mpad + m] = ri.best;
-      j.amax_i[(size_t)gi * j.mpad + m] = ri.bi;
-      if (ri.nan) atomicOr(const_cast<int32_t*>(&j.st[ri.b].err), ERR_NUMERIC);
-    }
-  }
 
   // k-sliced reductions: unit u's partials come from workgroup u % G of every
   // slice, slot u / G.  The control wave counts this workgroup in on all of
@@ -469,39 +505,44 @@ __global__ __launch_bounds__(kSgWaves * 64) void k_sgemv(const SgJob j) {
       }
     }
     __syncthreads();
-    if (wave > 0) {
-      row_info();
-      if constexpr (kNorm) ri.inv_rms = rms_sh[m];
+    RowInfo ri[MB];
+    row_info(ri);
+    if constexpr (kNorm) {
+#pragma unroll
+      for (int rb = 0; rb < MB; ++rb) ri[rb].inv_rms = rms_sh[16 * rb + m0];
     }
     for (int p = wave; p < np; p += kSgWaves) {
       const int e = pend[p];
       if (!(e & kMine)) continue;
       const int u = e & ~kMine;
-      f32x4 pa;
-      u32x2 pb;
-      epilogue_inputs<EPI>(j, ri, u, pa, pb);
-      // The partials of up to kBatch slices are loaded together, then added
-      // in slice order: one memory round trip per batch, not per slice.
-      constexpr int kBatch = kPair ? 4 : 8;
-      f32x4 sa = f32x4{0.f, 0.f, 0.f, 0.f}, sb = sa;
-      for (int s0 = 0; s0 < S; s0 += kBatch) {
-        f32x4 va[kBatch], vb[kBatch];
 #pragma unroll
-        for (int i = 0; i < kBatch; ++i) {
-          const int s2 = min(s0 + i, S - 1);
-          const float* pp = j.part + (((size_t)(s2 * G + u % G) * j.kmax + u / G) * 2) * 256;
-          va[i] = ld_coh(pp + lane * 4);
-          if (kPair) vb[i] = ld_coh(pp + 256 + lane * 4);
-        }
+      for (int rb = 0; rb < MB; ++rb) {
+        f32x4 pa;
+        u32x2 pb;
+        epilogue_inputs<EPI>(j, ri[rb], rb, u, pa, pb);
+        // The partials of up to kBatch slices are loaded together, then added
+        // in slice order: one memory round trip per batch, not per slice.
+        constexpr int kBatch = kPair ? 4 : 8;
+        f32x4 sa = f32x4{0.f, 0.f, 0.f, 0.f}, sb = sa;
+        for (int s0 = 0; s0 < S; s0 += kBatch) {
+          f32x4 va[kBatch], vb[kBatch];
 #pragma unroll
-        for (int i = 0; i < kBatch; ++i)
-          if (s0 + i < S) {
-            sa += va[i];
-            if (kPair) sb += vb[i];
+          for (int i = 0; i < kBatch; ++i) {
+            const int s2 = min(s0 + i, S - 1);
+            const float* pp = j.part + ((((size_t)(s2 * G + u % G) * j.kmax + u / G) * MB + rb) * 2) * 256;
+            va[i] = ld_coh4(pp + lane * 4);
+            if (kPair) vb[i] = ld_coh4(pp + 256 + lane * 4);
           }
+#pragma unroll
+          for (int i = 0; i < kBatch; ++i)
+            if (s0 + i < S) {
+              sa += va[i];
+              if (kPair) sb += vb[i];
+            }
+        }
+        epilogue<EPI>(j, ri[rb], rb, u, sa, sb, pa, pb);
       }
       if (lane == 0) __hip_atomic_store(j.cnt + u, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      epilogue<EPI>(j, ri, u, sa, sb, pa, pb);
     }
   }
 }
@@ -534,11 +575,15 @@ __global__ void k_pack(bf16_t* dst, PackSrc p) {
 
 size_t sg_packed_elems(int ntiles, int T) { return (size_t)ntiles * T * 64 * 8; }
 
-size_t sg_lds_bytes(const SgJob&) {
-  return 2 * kSgWorkers * 64 * 16 + (kSgPendMax + 4) * sizeof(int) + 16 * sizeof(float);
+// Row blocks of 16 rows of a job.
+int sg_row_blocks(const SgJob& j) { return (j.M + 15) / 16; }
+
+size_t sg_lds_bytes(const SgJob& j) {
+  const int MB = sg_row_blocks(j);
+  return 2 * (size_t)MB * kSgWorkers * 64 * 16 + (kSgPendMax + 4) * sizeof(int) + 16 * MB * sizeof(float);
 }
 
-size_t sg_part_floats(const SgJob& j) { return (size_t)j.S * j.G * j.kmax * 2 * 256; }
+size_t sg_part_floats(const SgJob& j) { return (size_t)j.S * j.G * j.kmax * sg_row_blocks(j) * 2 * 256; }
 
 bool sg_plan(SgJob& j, int epi, int ncu, int lds_limit) {
   const int tpu = epi == SG_SWIGLU ? 2 : 1;
@@ -547,8 +592,12 @@ bool sg_plan(SgJob& j, int epi, int ncu, int lds_limit) {
   // A k-range longer than the workers can hold x for is streamed (x loaded
   // with the weights, step by step) rather than cut into k-slices: no
   // partial tiles and no cross-workgroup fixup.
-  j.xs = j.T > kSgMaxSpan ? 1 : 0;
-  const int smin = j.xs ? 1 : (j.T + kSgMaxSpan - 1) / kSgMaxSpan;
+  // x is held in registers while every worker's share of a tile's steps fits
+  // its buffer (8 steps, or 9 for the 4096-wide inputs of the paper's
+  // backbone); a row's sum is formed the same way in every variant
+  j.xs = j.T > kSgWorkers * kSgDepthMax ? 1 : 0;
+  j.dep9 = (!j.xs && j.T > kSgMaxSpan) ? 1 : 0;
+  const int smin = 1;
   int S = smin;
   for (int s = smin; s <= 2 * smin; ++s)
     if (ncu % s == 0) {
@@ -573,12 +622,17 @@ bool sg_plan(SgJob& j, int epi, int ncu, int lds_limit) {
 hipError_t sg_launch(int epi, const SgJob& h, hipStream_t s, hipEvent_t e0, hipEvent_t e1) {
   const dim3 grid(h.S * h.G), block(kSgWaves * 64);
   const uint32_t lds = (uint32_t)sg_lds_bytes(h);
-#define SG_CASE(E)                                                                             \
-  case E:                                                                                      \
-    if (h.xs)                                                                                  \
-      hipExtLaunchKernelGGL(k_sgemv<E, true>, grid, block, lds, s, e0, e1, 0, h);             \
-    else                                                                                       \
-      hipExtLaunchKernelGGL(k_sgemv<E, false>, grid, block, lds, s, e0, e1, 0, h);            \
+  const bool two = sg_row_blocks(h) == 2;
+#define SG_PICK(E, XS_, D)                                                                              \
+  hipExtLaunchKernelGGL(two ? k_sgemv<E, XS_, 2, D> : k_sgemv<E, XS_, 1, D>, grid, block, lds, s, e0, e1, 0, h)
+#define SG_CASE(E)                                  \
+  case E:                                           \
+    if (h.xs)                                       \
+      SG_PICK(E, true, kSgDepth);                   \
+    else if (h.dep9)                                \
+      SG_PICK(E, false, kSgDepthMax);               \
+    else                                            \
+      SG_PICK(E, false, kSgDepth);                  \
     break;
   switch (epi) {
     SG_CASE(SG_ROPE)
@@ -589,6 +643,7 @@ hipError_t sg_launch(int epi, const SgJob& h, hipStream_t s, hipEvent_t e0, hipE
     default: return hipErrorInvalidValue;
   }
 #undef SG_CASE
+#undef SG_PICK
   return hipGetLastError();
 }
 
@@ -599,14 +654,23 @@ hipError_t sg_pack(bf16_t* dst, const PackSrc& src, hipStream_t s) {
   return hipGetLastError();
 }
 
-void sg_set_attributes(int lds_limit) {
-  const void* fns[] = {
-      reinterpret_cast<const void*>(&k_sgemv<SG_ROPE, false>),   reinterpret_cast<const void*>(&k_sgemv<SG_ROPE, true>),
-      reinterpret_cast<const void*>(&k_sgemv<SG_RESID, false>),  reinterpret_cast<const void*>(&k_sgemv<SG_RESID, true>),
-      reinterpret_cast<const void*>(&k_sgemv<SG_SWIGLU, false>), reinterpret_cast<const void*>(&k_sgemv<SG_SWIGLU, true>),
-      reinterpret_cast<const void*>(&k_sgemv<SG_DOWN, false>),   reinterpret_cast<const void*>(&k_sgemv<SG_DOWN, true>),
-      reinterpret_cast<const void*>(&k_sgemv<SG_ARGMAX, false>), reinterpret_cast<const void*>(&k_sgemv<SG_ARGMAX, true>)};
+template <int E>
+void sg_set_attr(int lds_limit) {
+  const void* fns[] = {reinterpret_cast<const void*>(&k_sgemv<E, false, 1, kSgDepth>),
+                       reinterpret_cast<const void*>(&k_sgemv<E, true, 1, kSgDepth>),
+                       reinterpret_cast<const void*>(&k_sgemv<E, false, 2, kSgDepth>),
+                       reinterpret_cast<const void*>(&k_sgemv<E, true, 2, kSgDepth>),
+                       reinterpret_cast<const void*>(&k_sgemv<E, false, 1, kSgDepthMax>),
+                       reinterpret_cast<const void*>(&k_sgemv<E, false, 2, kSgDepthMax>)};
   for (const void* f : fns) (void)hipFuncSetAttribute(f, hipFuncAttributeMaxDynamicSharedMemorySize, lds_limit);
+}
+
+void sg_set_attributes(int lds_limit) {
+  sg_set_attr<SG_ROPE>(lds_limit);
+  sg_set_attr<SG_RESID>(lds_limit);
+  sg_set_attr<SG_SWIGLU>(lds_limit);
+  sg_set_attr<SG_DOWN>(lds_limit);
+  sg_set_attr<SG_ARGMAX>(lds_limit);
 }
 
 }  // namespace specdec
