@@ -89,8 +89,7 @@ struct TimingRec {
 struct Ctx {
   spec_config cfg{};
   int B = 1, K = 0, R = 1, M = 1, Mpad = 16, V = 0, cap = 0;
-  int attn_chunk = kAttnChunk, attn_splits = 1;   // attention splits per sequence
-  int attn_np = 1;                   // cache pages per attention split
+  int attn_chunk = kAttnChunk, attn_splits = 1;
   int pps = 1;                       // page-table entries per sequence (cap / kAttnChunk)
   int pool = 0;                      // cache pages per layer
   std::vector<int32_t> pt_host;      // [B][pps] physical page of each sequence page
@@ -115,7 +114,7 @@ struct Ctx {
   float2* rcs = nullptr;            // [Mpad][head_dim/2] (cos, sin) of each row's rotary pairs
   float* part = nullptr;            // GEMV k-split partial sums
   size_t part_elems = 0;
-  float* op = nullptr;              // [splits][B][q_heads][R][head_dim] attention partials (unnormalised)
+  bf16_t* op = nullptr;             // [splits][B][q_heads][R][head_dim] attention partials (unnormalised)
   size_t attn_rows = 0;             // splits * B * q_heads * R (max over the models)
   float* mp = nullptr;              // [splits][B][q_heads][R] running max (log2 units)
   float* lp = nullptr;              // [splits][B][q_heads][R] running sum
@@ -214,8 +213,6 @@ size_t scratch_capacity();
 // and the device limit; k-splits of a GEMV whose workgroups cannot hold all
 // of x.
 size_t gemv_lds_bytes(int TT, int M, int span_steps);
-// Pages per attention split for this many workgroups of one-page splits.
-int attn_pages_per_split(size_t one_page_workgroups);
 int gemv_lds_limit();
 size_t gemv_p_lds_bytes(int M, int span_steps);
 int down_splits(int M, int Kd, int ncu);

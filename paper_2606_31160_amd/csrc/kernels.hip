@@ -748,26 +748,16 @@ struct AttnArgs {
   const bf16_t* kc;      // layer base of the key pool [pages][nkv][kAttnChunk][D]
   const bf16_t* vt;      // layer base of the value pool [pages][nkv][D][kAttnChunk]
   const int32_t* pt;     // [B][pps] page tables
-  float* op;             // [splits][B][nq][R][D] unnormalised partial outputs
-  float* mp;             // [splits][B][nq][R] running max (log2 units)
-  float* lp;             // [splits][B][nq][R] running sum
-  int nq, nkv, G, R, B, pps, np, row_blocks;   // np: cache pages per split
+  bf16_t* op;            // [splits][B][nq][R][D] unnormalised partial outputs (bf16)
+  float* mp;             // [splits][B][nq][R]
+  float* lp;
+  int nq, nkv, G, R, B, pps, chunk, row_blocks;
   float scale_log2;      // log2(e) / sqrt(D)
   const int8_t* cls;     // readout: [B][cap] class of every slot (0 visual, 1 trajectory/text, 2 generated)
   float* rp;             // readout: [splits][B][nq][R][4] class sums and trajectory E term
   int cap;
 };
 
-// One split-KV partial: the workgroup (split, kv head x row block, sequence)
-// runs the online softmax of its 64 query rows (row = pass row j x the G
-// query heads of the kv head) over the np cache pages of its split, one page
-// (64 keys) at a time.  Each page's keys [64][D] and values V^T [D][64] are
-// staged in LDS, the next page's loads in flight while the current one is
-// multiplied (two LDS buffers).  Per page: S^T = K Q^T on MFMA, the page max
-// merged into the running max (rescaling the running sum and output), then
-// O^T += V^T P^T.  P enters the MFMA as a bf16 pair hi + lo (hi = bf16(p),
-// lo = bf16(p - hi)), so the product keeps about 16 significant bits of p,
-// and the partial output, max and sum are stored in fp32.
 template <int D, bool RO>
 __device__ __forceinline__ void attn_partials(const AttnArgs& a, unsigned char* lds) {
   const int split = blockIdx.x;
@@ -775,41 +765,40 @@ __device__ __forceinline__ void attn_partials(const AttnArgs& a, unsigned char* 
   const int b = blockIdx.z;
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int g4 = lane >> 4;
+  // The page of this split is read together with the sequence state (it
+  // depends on the split only; table entries past a sequence's pages name
+  // page 0), so the key and value loads wait for one round trip, not two.
+  const int page = a.pt[b * a.pps + split];
   const SeqState& s = a.st[b];
   const int count = s.count, base = s.base, causal = s.causal;
-  const int p0 = split * a.np;
-  // the first page's table entry is read with the sequence state, so the key
-  // and value loads wait for one round trip, not two
-  const int page0 = a.pt[b * a.pps + p0];
-  asm volatile("" ::"s"(page0), "s"(count), "s"(base), "s"(causal));
+  asm volatile("" ::"s"(page), "s"(count), "s"(base), "s"(causal));   // all loads issued before any is awaited
   const int rows = count * a.G;
   const int wrow0 = rb * 64 + wave * 16;
-  const bool active = wrow0 < rows;                 // wave-uniform
   const int qr = wrow0 + (lane & 15);
   const bool rvalid = qr < rows;
   const int j = rvalid ? qr / a.G : 0;
   const int hq = kvh * a.G + (rvalid ? qr % a.G : 0);
   const int kv_end = base + count;
-  const int k0 = p0 * kAttnChunk;
-  const int npg = min(a.np, (kv_end - k0 + kAttnChunk - 1) / kAttnChunk);   // pages of the split with keys
+  const int k0 = split * a.chunk;
+  const int k1 = min(k0 + a.chunk, kv_end);
   const int vis_end = base + (j < causal ? j + 1 : count);   // rows past `causal` see the whole pass
   const size_t oi = (((size_t)split * a.B + b) * a.nq + hq) * a.R + j;
 
-  if (npg <= 0) {                                   // no keys in this split (workgroup-uniform)
-    if (!active) return;
+  if (k0 >= k1) {                                   // no keys in this split (workgroup-uniform)
+    if (wrow0 >= rows) return;
     if (rvalid && g4 == 0) {
       a.mp[oi] = -INFINITY;
       a.lp[oi] = 0.f;
     }
     if (rvalid) {
-      float* op = a.op + oi * D;
-      for (int d = g4 * 4; d < D; d += 16) *reinterpret_cast<f32x4*>(op + d) = f32x4{0.f, 0.f, 0.f, 0.f};
+      bf16_t* op = a.op + oi * D;
+      for (int d = g4 * 4; d < D; d += 16) *reinterpret_cast<u32x2*>(op + d) = u32x2{0u, 0u};
       if (RO && g4 == 0) *reinterpret_cast<f32x4*>(a.rp + oi * 4) = f32x4{0.f, 0.f, 0.f, 0.f};
     }
     return;
   }
 
-  // This wave's query rows, issued first so their latency overlaps the
+  // This wave's query rows; issued first so their latency overlaps the
   // staging.  Loads are unconditional (an invalid lane reads row 0 of its
   // head): a lane's scores only reach its own row, and those of invalid rows
   // are masked below.
@@ -819,37 +808,47 @@ __device__ __forceinline__ void attn_partials(const AttnArgs& a, unsigned char* 
 #pragma unroll
     for (int t = 0; t < D / 32; ++t) qf[t] = ld16(qp + 32 * t);
   }
+  // readout: classes of this lane's 16 keys, 4 consecutive slots per word
+  // (byte i of word h: slot k0 + 16 h + 4 g4 + i; k0 + 63 < cap)
+  uint32_t cw[4] = {0u, 0u, 0u, 0u};
+  if (RO) {
+    const int8_t* cp = a.cls + (size_t)b * a.cap + k0 + 4 * g4;
+#pragma unroll
+    for (int h = 0; h < 4; ++h) cw[h] = *reinterpret_cast<const uint32_t*>(cp + 16 * h);
+  }
 
-  const int kst = D + 8, vst = kAttnChunk + 8;      // the pads spread rows over the LDS banks
-  constexpr int kBuf = kAttnChunk * (D + 8) + D * (kAttnChunk + 8);   // bf16 elements of one page buffer
-  constexpr int PER_T = kAttnChunk * D / 8 / 256;   // 16-byte vectors per thread and operand
-  static_assert(PER_T * 256 * 8 == kAttnChunk * D, "the threads cover the page exactly");
-  constexpr int per_row = kAttnChunk / 8;
-  u32x4 kr[PER_T], vr[PER_T];
-  // Global loads of page i of the split into registers (the whole page: its
-  // slots past the pass's keys hold stale data; keys there only meet masked
-  // scores and values there are stored as zeros).
-  auto load_page = [&](int page) {
+  // Stage the chunk once for all waves: keys [chunk][D + 8] and values
+  // transposed [D][chunk + 8] (the pads spread rows over the LDS banks).  The
+  // whole page is loaded (its slots past k1 hold stale data): keys there only
+  // meet masked scores, values there are stored as zeros.  Every load of the
+  // thread is issued before the first LDS store so that their latencies
+  // overlap, and unconditionally so that no branch splits them.
+  const int kst = D + 8, vst = a.chunk + 8;
+  bf16_t* Ks = reinterpret_cast<bf16_t*>(lds);
+  bf16_t* Vs = Ks + (size_t)a.chunk * kst;
+  {
+    constexpr int PER_T = kAttnChunk * D / 8 / 256;   // 16-byte vectors per thread and operand
+    static_assert(PER_T * 256 * 8 == kAttnChunk * D, "the threads cover the page exactly");
     const size_t pg = (size_t)page * a.nkv + kvh;
     const bf16_t* Kb = a.kc + pg * kAttnChunk * D;
     const bf16_t* Vb = a.vt + pg * D * kAttnChunk;
+    constexpr int per_row = kAttnChunk / 8;
+    u32x4 kr[PER_T], vr[PER_T];
 #pragma unroll
     for (int u = 0; u < PER_T; ++u) {
       const int i = threadIdx.x + 256 * u;
-      kr[u] = ld16(Kb + (size_t)(i / (D / 8)) * D + 8 * (i % (D / 8)));
-      vr[u] = ld16(Vb + (size_t)(i / per_row) * kAttnChunk + 8 * (i % per_row));
-    }
-  };
-  auto store_page = [&](int buf, int kp0) {
-    bf16_t* Ks = reinterpret_cast<bf16_t*>(lds) + buf * kBuf;
-    bf16_t* Vs = Ks + (size_t)kAttnChunk * kst;
-    const int k1 = min(kp0 + kAttnChunk, kv_end);
-#pragma unroll
-    for (int u = 0; u < PER_T; ++u) {
-      const int i = threadIdx.x + 256 * u;
-      *reinterpret_cast<u32x4*>(Ks + (size_t)(i / (D / 8)) * kst + 8 * (i % (D / 8))) = kr[u];
+      const int key = i / (D / 8), c8 = i % (D / 8);
+      kr[u] = ld16(Kb + (size_t)key * D + 8 * c8);
       const int d = i / per_row, v8 = i % per_row;
-      const int slot = kp0 + 8 * v8;
+      vr[u] = ld16(Vb + (size_t)d * kAttnChunk + 8 * v8);
+    }
+#pragma unroll
+    for (int u = 0; u < PER_T; ++u) {
+      const int i = threadIdx.x + 256 * u;
+      const int key = i / (D / 8), c8 = i % (D / 8);
+      *reinterpret_cast<u32x4*>(Ks + (size_t)key * kst + 8 * c8) = kr[u];
+      const int d = i / per_row, v8 = i % per_row;
+      const int slot = k0 + 8 * v8;
       u32x4 v = vr[u];
       if (slot >= k1) {
         v = u32x4{0, 0, 0, 0};
@@ -862,116 +861,75 @@ __device__ __forceinline__ void attn_partials(const AttnArgs& a, unsigned char* 
       }
       *reinterpret_cast<u32x4*>(Vs + (size_t)d * vst + 8 * v8) = v;
     }
-  };
+  }
+  __syncthreads();
+  if (wrow0 >= rows) return;                        // wave-uniform; no barrier follows
 
-  float m_run = -INFINITY, l_run = 0.f;
+  // The whole chunk (kAttnChunk = 64 keys) in one step: S^T = K Q^T for the
+  // four 16-key groups (lanes own query rows; lane group g4 holds keys
+  // 16h + 4 g4 + i), one softmax over the chunk in log2 units, then
+  // O^T = V^T P^T over the two 32-key halves.  Within a half the key order of
+  // the P^T operand (keys 4 g4 + i and 16 + 4 g4 + i) is the one the V^T
+  // operand is read in, so the contraction is exact.
+  static_assert(kAttnChunk == 4 * 16, "one step covers four 16-key groups");
+  f32x4 sc[4];
+#pragma unroll
+  for (int h = 0; h < 4; ++h) {
+    const bf16_t* kp = Ks + (size_t)(16 * h + (lane & 15)) * kst + 8 * g4;
+    f32x4 acc = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int t = 0; t < D / 32; ++t) acc = mfma16x16x32(*reinterpret_cast<const u32x4*>(kp + 32 * t), qf[t], acc);
+    sc[h] = acc;
+  }
+  // V^T operands of both halves, read while the softmax runs
+  u32x4 va[2][D / 16];
+#pragma unroll
+  for (int hb = 0; hb < 2; ++hb)
+#pragma unroll
+    for (int dt = 0; dt < D / 16; ++dt) {
+      const bf16_t* vp = Vs + (size_t)(16 * dt + (lane & 15)) * vst + 32 * hb + 4 * g4;
+      const u32x2 lo = *reinterpret_cast<const u32x2*>(vp), hi = *reinterpret_cast<const u32x2*>(vp + 16);
+      va[hb][dt] = u32x4{lo.x, lo.y, hi.x, hi.y};
+    }
+  float p[16];
+  float m_run = -INFINITY;
+#pragma unroll
+  for (int h = 0; h < 4; ++h)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int key = k0 + 16 * h + 4 * g4 + i;
+      const bool ok = rvalid && key < k1 && key < vis_end;
+      const float v = ok ? sc[h][i] * a.scale_log2 : -INFINITY;
+      p[h * 4 + i] = v;
+      m_run = fmaxf(m_run, v);
+    }
+  m_run = fmaxf(m_run, __shfl_xor(m_run, 16));
+  m_run = fmaxf(m_run, __shfl_xor(m_run, 32));
+  float l_run = 0.f;
   float rs[4] = {0.f, 0.f, 0.f, 0.f};   // readout: class sums, then the trajectory E term
+#pragma unroll
+  for (int i = 0; i < 16; ++i) {
+    const float v = p[i];
+    p[i] = (v == -INFINITY) ? 0.f : exp2f(v - m_run);
+    l_run += p[i];
+    if (RO) {
+      const uint32_t cl = (cw[i >> 2] >> (8 * (i & 3))) & 0xffu;
+      rs[0] += cl == 0 ? p[i] : 0.f;
+      rs[1] += cl == 1 ? p[i] : 0.f;
+      rs[2] += cl == 2 ? p[i] : 0.f;
+      rs[3] += (cl == 1 && v != -INFINITY) ? p[i] * (v - m_run) : 0.f;
+    }
+  }
   f32x4 o[D / 16];
 #pragma unroll
   for (int dt = 0; dt < D / 16; ++dt) o[dt] = f32x4{0.f, 0.f, 0.f, 0.f};
-
-  load_page(page0);
-  store_page(0, k0);
-  for (int i = 0; i < npg; ++i) {
-    const bool more = i + 1 < npg;
-    if (more) load_page(a.pt[b * a.pps + p0 + i + 1]);   // in flight while page i is multiplied
-    __syncthreads();                                       // page i is in buffer i & 1
-    const int kp0 = k0 + i * kAttnChunk;
-    const int k1 = min(kp0 + kAttnChunk, kv_end);
-    if (active) {
-      const bf16_t* Ks = reinterpret_cast<const bf16_t*>(lds) + (i & 1) * kBuf;
-      const bf16_t* Vs = Ks + (size_t)kAttnChunk * kst;
-      // S^T = K Q^T for the four 16-key groups (lane group g4 holds keys
-      // 16h + 4 g4 + i of the lane's query row)
-      f32x4 sc[4];
 #pragma unroll
-      for (int h = 0; h < 4; ++h) {
-        const bf16_t* kp = Ks + (size_t)(16 * h + (lane & 15)) * kst + 8 * g4;
-        f32x4 acc = f32x4{0.f, 0.f, 0.f, 0.f};
+  for (int hb = 0; hb < 2; ++hb) {
+    const float* ph = p + 8 * hb;
+    const u32x4 pb = u32x4{pack2(ph[0], ph[1]), pack2(ph[2], ph[3]), pack2(ph[4], ph[5]), pack2(ph[6], ph[7])};
 #pragma unroll
-        for (int t = 0; t < D / 32; ++t)
-          acc = mfma16x16x32(*reinterpret_cast<const u32x4*>(kp + 32 * t), qf[t], acc);
-        sc[h] = acc;
-      }
-      // V^T operands of both 32-key halves, read while the softmax runs;
-      // within a half the key order (keys 4 g4 + i and 16 + 4 g4 + i) is the
-      // one of the P^T operand below, so the contraction is exact
-      u32x4 va[2][D / 16];
-#pragma unroll
-      for (int hb = 0; hb < 2; ++hb)
-#pragma unroll
-        for (int dt = 0; dt < D / 16; ++dt) {
-          const bf16_t* vp = Vs + (size_t)(16 * dt + (lane & 15)) * vst + 32 * hb + 4 * g4;
-          const u32x2 lo = *reinterpret_cast<const u32x2*>(vp), hi = *reinterpret_cast<const u32x2*>(vp + 16);
-          va[hb][dt] = u32x4{lo.x, lo.y, hi.x, hi.y};
-        }
-      float p[16];
-      float m_p = -INFINITY;
-#pragma unroll
-      for (int h = 0; h < 4; ++h)
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          const int key = kp0 + 16 * h + 4 * g4 + e;
-          const bool ok = rvalid && key < k1 && key < vis_end;
-          const float v = ok ? sc[h][e] * a.scale_log2 : -INFINITY;
-          p[h * 4 + e] = v;
-          m_p = fmaxf(m_p, v);
-        }
-      m_p = fmaxf(m_p, __shfl_xor(m_p, 16));
-      m_p = fmaxf(m_p, __shfl_xor(m_p, 32));
-      const float m_new = fmaxf(m_run, m_p);
-      const float scale = m_new == -INFINITY ? 0.f : exp2f(m_run - m_new);   // 0 while m_run is -inf
-      if (RO) {
-        const float dm = m_run == -INFINITY ? 0.f : m_run - m_new;
-        rs[3] = scale * (rs[3] + dm * rs[1]);
-        rs[0] *= scale;
-        rs[1] *= scale;
-        rs[2] *= scale;
-      }
-      l_run *= scale;
-#pragma unroll
-      for (int dt = 0; dt < D / 16; ++dt) o[dt] *= scale;
-      uint32_t cw[4] = {0u, 0u, 0u, 0u};
-      if (RO) {   // classes of this lane's 16 keys, 4 consecutive slots per word (kp0 + 63 < cap)
-        const int8_t* cp = a.cls + (size_t)b * a.cap + kp0 + 4 * g4;
-#pragma unroll
-        for (int h = 0; h < 4; ++h) cw[h] = *reinterpret_cast<const uint32_t*>(cp + 16 * h);
-      }
-#pragma unroll
-      for (int e = 0; e < 16; ++e) {
-        const float v = p[e];
-        p[e] = (v == -INFINITY) ? 0.f : exp2f(v - m_new);
-        l_run += p[e];
-        if (RO) {
-          const uint32_t cl = (cw[e >> 2] >> (8 * (e & 3))) & 0xffu;
-          rs[0] += cl == 0 ? p[e] : 0.f;
-          rs[1] += cl == 1 ? p[e] : 0.f;
-          rs[2] += cl == 2 ? p[e] : 0.f;
-          rs[3] += (cl == 1 && v != -INFINITY) ? p[e] * (v - m_new) : 0.f;
-        }
-      }
-      m_run = m_new;
-#pragma unroll
-      for (int hb = 0; hb < 2; ++hb) {
-        const float* ph = p + 8 * hb;
-        uint32_t hw[4], lw[4];
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          hw[e] = pack2(ph[2 * e], ph[2 * e + 1]);
-          const float h0 = __uint_as_float(hw[e] << 16), h1 = __uint_as_float(hw[e] & 0xffff0000u);
-          lw[e] = pack2(ph[2 * e] - h0, ph[2 * e + 1] - h1);
-        }
-        const u32x4 phi = u32x4{hw[0], hw[1], hw[2], hw[3]}, plo = u32x4{lw[0], lw[1], lw[2], lw[3]};
-#pragma unroll
-        for (int dt = 0; dt < D / 16; ++dt) {
-          o[dt] = mfma16x16x32(va[hb][dt], phi, o[dt]);
-          o[dt] = mfma16x16x32(va[hb][dt], plo, o[dt]);
-        }
-      }
-    }
-    if (more) store_page((i + 1) & 1, kp0 + kAttnChunk);   // the other buffer: its readers passed the barrier
+    for (int dt = 0; dt < D / 16; ++dt) o[dt] = mfma16x16x32(va[hb][dt], pb, o[dt]);
   }
-  if (!active) return;
   l_run += __shfl_xor(l_run, 16);
   l_run += __shfl_xor(l_run, 32);
   if (RO) {
@@ -983,9 +941,11 @@ __device__ __forceinline__ void attn_partials(const AttnArgs& a, unsigned char* 
     if (rvalid && g4 == 0) *reinterpret_cast<f32x4*>(a.rp + oi * 4) = f32x4{rs[0], rs[1], rs[2], rs[3]};
   }
   if (rvalid) {
-    float* op = a.op + oi * D;
+    bf16_t* op = a.op + oi * D;
 #pragma unroll
-    for (int dt = 0; dt < D / 16; ++dt) *reinterpret_cast<f32x4*>(op + 16 * dt + 4 * g4) = o[dt];
+    for (int dt = 0; dt < D / 16; ++dt)
+      *reinterpret_cast<u32x2*>(op + 16 * dt + 4 * g4) =
+          u32x2{pack2(o[dt].x, o[dt].y), pack2(o[dt].z, o[dt].w)};
     if (g4 == 0) {
       a.mp[oi] = m_run;
       a.lp[oi] = l_run;
@@ -999,21 +959,9 @@ __global__ __launch_bounds__(256) void k_attn(AttnArgs a) {
   attn_partials<D, RO>(a, lds);
 }
 
-// Cache pages per attention split: one while the one-page grid has at most
-// ATTN_TARGET_WGS workgroups, else enough pages per split to bring the grid
-// down to about that size (fewer partials to write and merge).
-#ifndef ATTN_TARGET_WGS
-#define ATTN_TARGET_WGS 2048
-#endif
-int attn_pages_per_split(size_t one_page_workgroups) {
-  return (int)std::max<size_t>(1, one_page_workgroups / ATTN_TARGET_WGS);
-}
 
-// LDS of one attention workgroup: one page buffer, or two when a split holds
-// more than one page.
-size_t attn_lds_bytes(int np, int D) {
-  const size_t one = ((size_t)kAttnChunk * (D + 8) + (size_t)D * (kAttnChunk + 8)) * sizeof(bf16_t);
-  return np > 1 ? 2 * one : one;
+size_t attn_lds_bytes(int chunk, int D) {
+  return ((size_t)chunk * (D + 8) + (size_t)D * (chunk + 8)) * sizeof(bf16_t);
 }
 
 // Merge the splits of each (row, q head): o = sum_s 2^(m_s - M) O_s / sum_s
@@ -1025,10 +973,10 @@ size_t attn_lds_bytes(int np, int D) {
 // trajectory/text keys, H(q) = ln C_1 - ln 2 * E / C_1 (C_1 = sum_s w_s C_1,s).
 struct CombineArgs {
   const SeqState* st;
-  const float* op;       // fp32 partial outputs
+  const bf16_t* op;      // bf16 partial outputs
   const float *mp, *lp;
   bf16_t* o;             // [Mpad][nq*D]
-  int nq, D, R, B, span; // span: keys per split (np pages)
+  int nq, D, R, B, chunk;
   const float* rp;       // readout: [splits][B][nq][R][4] partial class sums and E terms
   float* ro;             // readout: [B][R][nq][4] masses (visual, trajectory/text, generated), entropy
   float inv_ln[SPEC_MAX_BATCH];   // readout: 1 / ln(trajectory/text slots) of each sequence, 0 if <= 1
@@ -1043,7 +991,7 @@ __device__ __forceinline__ void combine_unit(const CombineArgs& a, int j, int h,
   const SeqState& s = a.st[b];
   if (j >= s.count) return;
   const int vis_end = s.base + (j < s.causal ? j + 1 : s.count);
-  const int ns = (vis_end + a.span - 1) / a.span;     // splits holding keys this row sees
+  const int ns = (vis_end + a.chunk - 1) / a.chunk;   // splits holding keys this row sees
   const size_t row = ((size_t)b * a.nq + h) * a.R + j;
   const size_t sstride = (size_t)a.B * a.nq * a.R;
   if (threadIdx.x < 64) {
@@ -1087,10 +1035,15 @@ __device__ __forceinline__ void combine_unit(const CombineArgs& a, int j, int h,
   const int c4 = threadIdx.x & 31, sg = threadIdx.x >> 5;
   f32x4 v = f32x4{0.f, 0.f, 0.f, 0.f};
   if (4 * c4 < a.D) {
-    const float* src = a.op + row * a.D + 4 * c4;
+    const bf16_t* src = a.op + row * a.D + 4 * c4;
     const size_t ostride = sstride * a.D;
 #pragma unroll 4
-    for (int sp = sg; sp < ns; sp += 8) v += coef[sp] * *reinterpret_cast<const f32x4*>(src + sp * ostride);
+    for (int sp = sg; sp < ns; sp += 8) {
+      const u32x2 w = *reinterpret_cast<const u32x2*>(src + sp * ostride);
+      const f32x4 ov = f32x4{__uint_as_float(w.x << 16), __uint_as_float(w.x & 0xffff0000u),
+                             __uint_as_float(w.y << 16), __uint_as_float(w.y & 0xffff0000u)};
+      v += coef[sp] * ov;
+    }
     *reinterpret_cast<f32x4*>(part + sg * a.D + 4 * c4) = v;
   }
   __syncthreads();
@@ -1429,14 +1382,14 @@ hipError_t launch_attention(Ctx& c, Model& m, int li) {
   const int G = nq / nkv;
   const int rb = (c.R * G + 63) / 64;
   const bool ro = c.ro_out && c.ro_m == &m && c.ro_layer == li;
-  AttnArgs p{c.st, c.q, kc, vt, c.pt, c.op, c.mp, c.lp, nq, nkv, G, c.R, c.B, c.pps, c.attn_np, rb,
+  AttnArgs p{c.st, c.q, kc, vt, c.pt, c.op, c.mp, c.lp, nq, nkv, G, c.R, c.B, c.pps, c.attn_chunk, rb,
              kLog2e / sqrtf((float)D), c.cls, c.rp, c.cap};
   dim3 grid(c.attn_splits, nkv * rb, c.B);
-  CombineArgs cb{c.st, c.op, c.mp, c.lp, c.o, nq, D, c.R, c.B, c.attn_np * kAttnChunk, c.rp,
+  CombineArgs cb{c.st, c.op, c.mp, c.lp, c.o, nq, D, c.R, c.B, c.attn_chunk, c.rp,
                  ro ? c.ro_out : nullptr, {}};
   for (int b = 0; b < c.B && b < SPEC_MAX_BATCH; ++b) cb.inv_ln[b] = c.ro_inv_ln[b];
   const size_t comb_lds = (size_t)(((c.attn_splits + 3) & ~3) + 8 * D) * sizeof(float);
-  const size_t lds = attn_lds_bytes(c.attn_np, D);
+  const size_t lds = attn_lds_bytes(c.attn_chunk, D);
   {
     Timed t(c, SPEC_KERNEL_ATTN, 0);
     if (D == 128)
@@ -1643,7 +1596,7 @@ void init_kernel_attributes() {
                          reinterpret_cast<const void*>(&k_attn<64, false>), reinterpret_cast<const void*>(&k_attn<64, true>)};
   for (int i = 0; i < 4; ++i)
     (void)hipFuncSetAttribute(attn[i], hipFuncAttributeMaxDynamicSharedMemorySize,
-                              (int)attn_lds_bytes(2, i < 2 ? 128 : 64));
+                              (int)attn_lds_bytes(kAttnChunk, i < 2 ? 128 : 64));
   set_lds_limit_p<EPI_STORE, 1>();
   set_lds_limit_p<EPI_STORE, 2>();
   set_lds_limit_p<EPI_STORE, 3>();

@@ -347,13 +347,7 @@ size_t carve(Ctx& c, const spec_config* cfg, const spec_seq_init* seqs, bool has
   c.pool = L.pool;
   c.attn_chunk = L.chunk;
   c.ncu = num_cus();
-  {
-    // attention splits of np cache pages each (the target's grid decides)
-    // from the sequence count and cache size only, not the pass's row count, so
-    // that a row's attention sum is grouped the same way for every K
-    c.attn_np = attn_pages_per_split((size_t)L.splits * cfg->target.kv_heads * L.B);
-    c.attn_splits = (L.splits + c.attn_np - 1) / c.attn_np;
-  }
+  c.attn_splits = L.splits;
   c.tgt.d = cfg->target;
   c.tgt.flat = false;
   c.block_draft = has_draft && (cfg->flags & SPEC_FLAG_BLOCK_DRAFT) != 0;
@@ -394,9 +388,9 @@ size_t carve(Ctx& c, const spec_config* cfg, const spec_seq_init* seqs, bool has
   c.rcs = cv.take<float2>((size_t)L.Mpad * (D / 2));
   c.part = cv.take<float>(part);
   c.part_elems = part;
-  const size_t attn_rows = (size_t)c.attn_splits * L.B * nq * L.R;
+  const size_t attn_rows = (size_t)L.splits * L.B * nq * L.R;
   c.attn_rows = attn_rows;
-  c.op = cv.take<float>(attn_rows * D);
+  c.op = cv.take<bf16_t>(attn_rows * D);
   c.mp = cv.take<float>(attn_rows);
   c.lp = cv.take<float>(attn_rows);
   c.amax_v = cv.take<float>((size_t)(L.V / kTile) * L.Mpad);
@@ -617,7 +611,7 @@ ScratchPlan scratch_plan(const Ctx& c) {
   };
   const int D = c.tgt.d.head_dim;
   const size_t amax = (size_t)(c.V / kTile) * c.Mpad;
-  p.op = take(c.attn_rows * D * sizeof(float));
+  p.op = take(c.attn_rows * D * sizeof(bf16_t));
   p.mp = take(c.attn_rows * sizeof(float));
   p.lp = take(c.attn_rows * sizeof(float));
   p.rp = take(c.attn_rows * 4 * sizeof(float));
@@ -636,14 +630,15 @@ ScratchPlan scratch_plan(const Ctx& c) {
 // lifetime of the object, then restores the workspace's.
 struct ScratchSwap {
   Ctx& c;
-  float *op, *mp, *lp, *rp, *part, *sg_part, *amax_v;
+  bf16_t* op;
+  float *mp, *lp, *rp, *part, *sg_part, *amax_v;
   unsigned* sg_cnt;
   int32_t* amax_i;
   bf16_t* logits;
   ScratchSwap(Ctx& ctx, char* base, const ScratchPlan& p)
       : c(ctx), op(ctx.op), mp(ctx.mp), lp(ctx.lp), rp(ctx.rp), part(ctx.part), sg_part(ctx.sg_part),
         amax_v(ctx.amax_v), sg_cnt(ctx.sg_cnt), amax_i(ctx.amax_i), logits(ctx.logits) {
-    c.op = reinterpret_cast<float*>(base + p.op);
+    c.op = reinterpret_cast<bf16_t*>(base + p.op);
     c.mp = reinterpret_cast<float*>(base + p.mp);
     c.lp = reinterpret_cast<float*>(base + p.lp);
     c.rp = reinterpret_cast<float*>(base + p.rp);
