@@ -336,6 +336,17 @@ enum spec_kernel_kind {
   SPEC_KERNEL_KINDS = 7
 };
 spec_status spec_timing(spec_ctx* ctx, int32_t enable);
+
+/* Read-only streaming reference (no context): reads `bytes` (a multiple of
+ * 16) of device memory at d_buf (16-byte aligned) once with non-temporal
+ * 16-byte loads, each wave taking 8 KB chunks (eight 1 KB loads in flight),
+ * in sink_words / 4 workgroups of 256 threads, and writes one checksum word
+ * per wave to d_sink [sink_words]
+ * (device; sink_words a positive multiple of 4).  Enqueued on `stream`.  Used
+ * to measure the HBM read rate a kernel reaches on this device and to
+ * calibrate byte counters against a known read volume. */
+spec_status spec_stream_read(const void* d_buf, size_t bytes, uint32_t* d_sink, int32_t sink_words,
+                             hipStream_t stream);
 spec_status spec_timing_read(spec_ctx* ctx, int32_t kind, int64_t* launches, double* ms, double* bytes);
 
 #ifdef __cplusplus

@@ -95,6 +95,7 @@ def lib():
             "spec_debug_state": [P, c_int32, P],
             "spec_debug_kv": [P, c_int32, c_int32, c_int32, c_int32, c_int32, c_int32, P],
             "spec_timing": [P, c_int32],
+            "spec_stream_read": [P, ctypes.c_size_t, P, c_int32, P],
             "spec_timing_read": [P, c_int32, POINTER(c_int64), POINTER(c_double), POINTER(c_double)],
             "spec_debug_path": [P, POINTER(c_int32)],
             "spec_debug_feature": [P, c_int32, c_int32, c_int32, P],
@@ -222,6 +223,11 @@ def spec_debug_path(ctx) -> str:
     p = c_int32(-1)
     _check(lib().spec_debug_path(ctx, ctypes.byref(p)), "spec_debug_path", ctx)
     return PATHS[p.value]
+
+
+def spec_stream_read(d_buf: int, nbytes: int, d_sink: int, sink_words: int, stream: int) -> None:
+    _check(lib().spec_stream_read(c_void_p(d_buf), nbytes, c_void_p(d_sink), sink_words, c_void_p(stream or None)),
+           "spec_stream_read")
 
 
 def spec_timing(ctx, enable: bool) -> None:

@@ -188,6 +188,7 @@ struct Ctx {
 // Each returns hipSuccess or the launch error.
 
 hipError_t launch_zero(Ctx& c, void* p, size_t bytes);
+hipError_t launch_stream_read(const void* p, size_t bytes, uint32_t* sink, int sink_words, hipStream_t s);
 hipError_t launch_hold(Ctx& c, double ms);   // bounded device-side wait (timing mode)
 hipError_t launch_prefix_kv(Ctx& c, Model& m, int layer, int b, int prefix_len,
                             const bf16_t* k_pre, const bf16_t* v);

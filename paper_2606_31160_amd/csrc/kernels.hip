@@ -36,6 +36,31 @@ __global__ void k_hold(long long ticks) {
   while (wall_clock64() - t0 < ticks) __builtin_amdgcn_s_sleep(16);
 }
 
+// Read-only streaming: every 16-byte element of p once, non-temporal.  Each
+// wave reads 8 KB chunks (eight consecutive 1 KB loads, all in flight), the
+// chunks dealt round-robin over the waves of the grid; each wave writes the
+// xor of what it read.
+__global__ __launch_bounds__(256) void k_stream_read(const u32x4* p, size_t n, uint32_t* sink) {
+  const size_t nw = (size_t)gridDim.x * (blockDim.x / 64);
+  const size_t wid = (size_t)blockIdx.x * (blockDim.x / 64) + (threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63;
+  constexpr int kChunk = 8 * 64;   // 16-byte elements per chunk
+  u32x4 acc = u32x4{0, 0, 0, 0};
+  const size_t nchunks = n / kChunk;
+  for (size_t c = wid; c < nchunks; c += nw) {
+    const u32x4* q = p + c * kChunk + lane;
+    u32x4 v[8];
+#pragma unroll
+    for (int k = 0; k < 8; ++k) v[k] = __builtin_nontemporal_load(q + 64 * k);
+#pragma unroll
+    for (int k = 0; k < 8; ++k) acc ^= v[k];
+  }
+  for (size_t i = nchunks * kChunk + wid * 64 + lane; i < n; i += nw * 64) acc ^= __builtin_nontemporal_load(p + i);
+  uint32_t x = acc.x ^ acc.y ^ acc.z ^ acc.w;
+  for (int o = 32; o > 0; o >>= 1) x ^= __shfl_xor(x, o);
+  if (lane == 0) sink[wid] = x;
+}
+
 __global__ void k_zero(u32x4* p, size_t n) {
   size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
   const size_t stride = (size_t)gridDim.x * blockDim.x;
@@ -1802,6 +1827,12 @@ hipError_t sg_pack_head(Ctx& c) {
   e.ntiles = c.V / kTile;
   e.T = steps_of(e.Kd);
   return sg_pack(c.pk_head, e, c.stream);
+}
+
+hipError_t launch_stream_read(const void* p, size_t bytes, uint32_t* sink, int sink_words, hipStream_t s) {
+  hipLaunchKernelGGL(k_stream_read, dim3(sink_words / 4), dim3(256), 0, s, reinterpret_cast<const u32x4*>(p), bytes / 16,
+                     sink);
+  return hipGetLastError();
 }
 
 hipError_t launch_zero(Ctx& c, void* p, size_t bytes) {

@@ -1166,6 +1166,13 @@ spec_status spec_debug_kv(spec_ctx* ctx, int32_t b, int32_t model, int32_t layer
   });
 }
 
+spec_status spec_stream_read(const void* d_buf, size_t bytes, uint32_t* d_sink, int32_t sink_words,
+                            hipStream_t stream) {
+  if (!d_buf || !d_sink || bytes == 0 || bytes % 16 || !aligned16(d_buf) || sink_words < 4 || sink_words % 4)
+    return SPEC_E_INVAL;
+  return launch_stream_read(d_buf, bytes, d_sink, sink_words, stream) == hipSuccess ? SPEC_OK : SPEC_E_HIP;
+}
+
 spec_status spec_timing(spec_ctx* ctx, int32_t enable) {
   return guarded(ctx, [&](Ctx& c) -> spec_status {
     HIPCHK(c, hipStreamSynchronize(c.stream), "sync");
