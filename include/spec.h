@@ -96,6 +96,12 @@ typedef struct spec_dims {
                                       e + w_in [e; f(t-1)] (2*hidden -> hidden; f = 0 where no verified
                                       feature exists: prompt slots and the draft's proposal rows).
                                       Needs a draft with w_fuse and w_in. */
+#define SPEC_FLAG_FULL_DRAFT_ROWS 128  /* every draft step runs the pass of batch*(K+1) rows.  Without it,
+                                      a chained draft step after the first of a round (each live sequence
+                                      then consumes exactly one token, its previous proposal) runs as a
+                                      pass of one row per sequence on the tile-packed GEMV, when the
+                                      batch is at most 32, a packed weight copy exists and neither
+                                      SPEC_FLAG_BLOCK_DRAFT nor SPEC_FLAG_COND is set */
 #define SPEC_FLAG_DRAFT_MROPE 16   /* the draft rotates with 3D M-RoPE (its own mrope_section and
                                       interleaved, validated as the target's) instead of FlatRoPE: the
                                       comparison arm of the attention-budget readout (Sec. 4.2) */

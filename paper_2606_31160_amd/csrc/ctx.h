@@ -78,6 +78,7 @@ struct Model {
   size_t pk_layer = 0, pk_o = 0, pk_gu = 0, pk_dn = 0;   // elements per layer; offsets inside a layer
   std::vector<SgJob> sg_host;       // [layers][4] (q/k/v, o, gate/up, down) + the LM head
   std::vector<SgJob> sg_block;      // draft, block proposal: the last layer's down for every row, the LM head over all rows
+  std::vector<SgJob> sg_one;        // draft, steps after the first of a round: the sg_host jobs for one row per sequence
 };
 
 struct TimingRec {
@@ -150,6 +151,8 @@ struct Ctx {
   // host state machine
   enum Phase { READY = 0, DRAFTING = 1, VERIFIED = 2 } phase = READY;
   int dsteps = 0;
+  bool one_rows = false;             // draft steps after a round's first run as passes of one row per sequence
+  int Mpad1 = 16;                    // ... whose row count B is padded to this
   bool gemm_rows = false;              // layered row-major passes run on the batched-row GEMM
   bool gemm_pk = false;                // ... which streams the tile-packed weight copy
   bool poisoned = false;
@@ -158,10 +161,12 @@ struct Ctx {
   // graphs
   bool use_graphs = true;
   hipGraphExec_t g_verify = nullptr, g_draft = nullptr, g_commit = nullptr;
+  hipGraphExec_t g_draft1 = nullptr;             // the one-row-per-sequence draft pass
   int32_t* draft_out = nullptr;                  // draft_step's output array (baked into the draft graph)
   int32_t* g_draft_out = nullptr;                // ... the one the current draft graph writes
   hipGraphExec_t g_drafts = nullptr;             // n draft passes in one graph (draft_steps)
   int g_drafts_n = 0;
+  bool g_drafts_first = false;                   // ... its first pass is a round's first (full rows)
   int32_t* g_drafts_out = nullptr;
   int32_t* commit_out[4] = {};                   // spec_commit's outputs (baked into the commit graph)
   int32_t* g_commit_out[4] = {};

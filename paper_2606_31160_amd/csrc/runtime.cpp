@@ -28,7 +28,7 @@ thread_local std::string g_init_error;
 
 constexpr size_t kAlign = 256;
 constexpr int32_t kKnownFlags = SPEC_FLAG_NO_GRAPHS | SPEC_FLAG_ROWMAJOR | SPEC_FLAG_BLOCK_DRAFT | SPEC_FLAG_COND |
-                                SPEC_FLAG_DRAFT_MROPE;
+                                SPEC_FLAG_DRAFT_MROPE | SPEC_FLAG_FULL_DRAFT_ROWS;
 
 size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 
@@ -333,6 +333,26 @@ bool gemm_rows_for(const spec_config* cfg, bool has_draft, int M) {
   return M > kSgMaxRowsGemm && (!thin_fits(cfg->target, M) || (has_draft && !thin_fits(cfg->draft, M)));
 }
 
+// The draft's packed-GEMV jobs for a pass of one row per sequence (B rows),
+// kept in drf.sg_one; the context's pass shape is untouched on return.
+bool sg_build_one(Ctx& c, bool fill) {
+  const int R = c.R, M = c.M, Mpad = c.Mpad;
+  c.R = 1;
+  c.M = c.B;
+  c.Mpad = c.Mpad1;
+  std::vector<SgJob> host, block;
+  host.swap(c.drf.sg_host);
+  block.swap(c.drf.sg_block);
+  const bool ok = sg_build_jobs(c, c.drf, true, fill);
+  c.drf.sg_one.swap(c.drf.sg_host);
+  c.drf.sg_host.swap(host);
+  c.drf.sg_block.swap(block);
+  c.R = R;
+  c.M = M;
+  c.Mpad = Mpad;
+  return ok;
+}
+
 // Carves the workspace (base == nullptr only measures).  Returns total bytes.
 size_t carve(Ctx& c, const spec_config* cfg, const spec_seq_init* seqs, bool has_draft, char* base) {
   const Layout L = make_layout(cfg, seqs);
@@ -412,36 +432,41 @@ size_t carve(Ctx& c, const spec_config* cfg, const spec_seq_init* seqs, bool has
     c.drf.kc = cv.take<bf16_t>(c.drf.kv_layer * cfg->draft.layers);
     c.drf.vt = cv.take<bf16_t>(c.drf.kv_layer * cfg->draft.layers);
   }
-  // packed-weight path: passes of at most 16 rows on the layered path
+  // packed-weight path: passes of at most 32 rows on the layered path
   c.sg = false;
-  if (!(cfg->flags & SPEC_FLAG_ROWMAJOR) && L.M <= kSgMaxRows &&
-      sg_build_jobs(c, c.tgt, false, false) && (!has_draft || sg_build_jobs(c, c.drf, true, false))) {
+  const bool sg_ok = !(cfg->flags & SPEC_FLAG_ROWMAJOR) && L.M <= kSgMaxRows && sg_build_jobs(c, c.tgt, false, false) &&
+                     (!has_draft || sg_build_jobs(c, c.drf, true, false));
+  // passes on the batched-row GEMM stream the same tile-packed copy: every
+  // wave load is then 1 KB of consecutive memory instead of 16 row pieces
+  c.gemm_pk = !sg_ok && c.gemm_rows && !(cfg->flags & SPEC_FLAG_ROWMAJOR);
+  // live-row compaction of chained draft steps (one row per sequence)
+  c.Mpad1 = (int)align_up(L.B, 16);
+  c.one_rows = has_draft && !c.block_draft && !c.cond && L.R > 1 && L.B <= kSgMaxRows && (sg_ok || c.gemm_pk) &&
+               !(cfg->flags & SPEC_FLAG_FULL_DRAFT_ROWS) && sg_build_one(c, false);
+  if (sg_ok || c.one_rows) {
     size_t pf = 0;
     int units = 0;
-    for (int k = 0; k < (has_draft ? 2 : 1); ++k) {
-      const Model& mm = k ? c.drf : c.tgt;
-      for (const std::vector<SgJob>* js : {&mm.sg_host, &mm.sg_block})
-        for (const SgJob& j : *js) {
-          pf = std::max(pf, sg_part_floats(j));
-          units = std::max(units, j.units);
-        }
+    auto fold = [&](const std::vector<SgJob>& js) {
+      for (const SgJob& j : js) {
+        pf = std::max(pf, sg_part_floats(j));
+        units = std::max(units, j.units);
+      }
+    };
+    if (sg_ok) {
+      for (int k = 0; k < (has_draft ? 2 : 1); ++k) {
+        const Model& mm = k ? c.drf : c.tgt;
+        fold(mm.sg_host);
+        fold(mm.sg_block);
+      }
     }
-    c.sg = true;
+    if (c.one_rows) fold(c.drf.sg_one);
     c.sg_part_floats = pf;
     c.sg_units = units;
     c.sg_part = cv.take<float>(pf);
     c.sg_cnt = cv.take<unsigned>((size_t)units);
-    c.pk_head = cv.take<bf16_t>(sg_packed_elems(L.V / kTile, (H + 31) / 32));
-    c.tgt.pk = cv.take<bf16_t>(c.tgt.pk_layer * t.layers);
-    if (has_draft) {
-      c.drf.pk = cv.take<bf16_t>(c.drf.pk_layer * cfg->draft.layers);
-    }
   }
-  // passes on the batched-row GEMM stream the same tile-packed copy: every
-  // wave load is then 1 KB of consecutive memory instead of 16 row pieces
-  c.gemm_pk = false;
-  if (!c.sg && c.gemm_rows && !(cfg->flags & SPEC_FLAG_ROWMAJOR)) {
-    c.gemm_pk = true;
+  if (sg_ok || c.gemm_pk) {
+    c.sg = sg_ok;
     pk_offsets(c.tgt);
     c.pk_head = cv.take<bf16_t>(sg_packed_elems(L.V / kTile, (H + 31) / 32));
     c.tgt.pk = cv.take<bf16_t>(c.tgt.pk_layer * t.layers);
@@ -503,7 +528,35 @@ spec_status set_err(Ctx& c, spec_status s, const char* msg) {
 
 // One pass; a block proposal is the draft's catch-up of accepted tokens and
 // the block pass.
-hipError_t launch_pass(Ctx& c, PassMode mode) {
+// A chained draft step after the first of a round, as a pass of one row per
+// sequence on the packed GEMV: every live sequence consumes exactly its
+// previous proposal then (draft_len == seq_len + dstep), so the rows
+// b*(K+1)+1.. of the full pass would all be idle.
+struct OneRowPass {
+  Ctx& c;
+  int R, M, Mpad;
+  bool sg;
+  explicit OneRowPass(Ctx& ctx) : c(ctx), R(ctx.R), M(ctx.M), Mpad(ctx.Mpad), sg(ctx.sg) {
+    c.R = 1;
+    c.M = c.B;
+    c.Mpad = c.Mpad1;
+    c.sg = true;
+    c.drf.sg_host.swap(c.drf.sg_one);
+  }
+  ~OneRowPass() {
+    c.R = R;
+    c.M = M;
+    c.Mpad = Mpad;
+    c.sg = sg;
+    c.drf.sg_host.swap(c.drf.sg_one);
+  }
+};
+
+hipError_t launch_pass(Ctx& c, PassMode mode, bool one_row = false) {
+  if (one_row) {
+    OneRowPass shape(c);
+    return launch_forward(c, PASS_DRAFT);
+  }
   if (mode != PASS_BLOCK) return launch_forward(c, mode);
   const hipError_t e = launch_forward(c, PASS_CATCHUP);
   return e != hipSuccess ? e : launch_forward(c, PASS_BLOCK);
@@ -558,19 +611,24 @@ spec_status run_pass(Ctx& c, PassMode mode) {
     HIPCHK(c, e, "forward pass with readout");
     return SPEC_OK;
   }
+  const bool one = c.one_rows && mode == PASS_DRAFT && c.dsteps > 0;
   const bool graphs = c.use_graphs && !c.timing;
   if (!graphs) {
     // timing mode: a head start so the timed kernels run back to back
     if (c.timing) HIPCHK(c, launch_hold(c, mode == PASS_VERIFY ? 4.0 : 1.0), "timing hold");
-    HIPCHK(c, launch_pass(c, mode), "forward pass");
+    HIPCHK(c, launch_pass(c, mode, one), "forward pass");
     return SPEC_OK;
   }
-  if (drafting && c.g_draft && c.g_draft_out != c.draft_out) {
-    (void)hipGraphExecDestroy(c.g_draft);
-    c.g_draft = nullptr;
+  if (drafting && c.g_draft_out != c.draft_out) {
+    for (hipGraphExec_t* g : {&c.g_draft, &c.g_draft1})
+      if (*g) {
+        (void)hipGraphExecDestroy(*g);
+        *g = nullptr;
+      }
   }
   if (drafting) c.g_draft_out = c.draft_out;
-  return run_graph(c, mode == PASS_VERIFY ? c.g_verify : c.g_draft, [&] { return launch_pass(c, mode); });
+  return run_graph(c, mode == PASS_VERIFY ? c.g_verify : (one ? c.g_draft1 : c.g_draft),
+                   [&] { return launch_pass(c, mode, one); });
 }
 
 // The commit kernel runs through a graph of its own too: launched directly
@@ -872,6 +930,11 @@ spec_status spec_init(const spec_config* cfg, const void* embed, const spec_mode
           (has_draft && (e = sg_pack_model(c, c.drf)) != hipSuccess))
         return hip_fail(e, "weight packing");
     }
+    if (c.one_rows && !sg_build_one(c, true)) {
+      g_init_error = "packed GEMV plan of the one-row draft pass changed between sizing and init";
+      delete ctx;
+      return SPEC_E_INVAL;
+    }
     if (c.gemm_pk) {
       if ((e = sg_pack_head(c)) != hipSuccess || (e = sg_pack_model(c, c.tgt)) != hipSuccess ||
           (has_draft && (e = sg_pack_model(c, c.drf)) != hipSuccess))
@@ -939,24 +1002,27 @@ spec_status draft_steps(spec_ctx* ctx, int32_t n, int32_t* d_draft_tokens) {
       for (int i = 0; i < n; ++i) {
         spec_status s = run_pass(c, PASS_DRAFT);
         if (s != SPEC_OK) return s;
+        c.dsteps += 1;
       }
     } else {
-      if (c.g_drafts && (c.g_drafts_n != n || c.g_drafts_out != d_draft_tokens)) {
+      const bool first = c.dsteps == 0;
+      if (c.g_drafts && (c.g_drafts_n != n || c.g_drafts_out != d_draft_tokens || c.g_drafts_first != first)) {
         (void)hipGraphExecDestroy(c.g_drafts);
         c.g_drafts = nullptr;
       }
       c.g_drafts_n = n;
       c.g_drafts_out = d_draft_tokens;
+      c.g_drafts_first = first;
       spec_status s = run_graph(c, c.g_drafts, [&]() -> hipError_t {
         for (int i = 0; i < n; ++i) {
-          const hipError_t e = launch_forward(c, PASS_DRAFT);
+          const hipError_t e = launch_pass(c, PASS_DRAFT, c.one_rows && (!first || i > 0));
           if (e != hipSuccess) return e;
         }
         return hipSuccess;
       });
       if (s != SPEC_OK) return s;
+      c.dsteps += n;
     }
-    c.dsteps += n;
     c.phase = Ctx::DRAFTING;
     return SPEC_OK;
   });
@@ -1077,6 +1143,7 @@ void spec_destroy(spec_ctx* ctx) {
   if (c.stream) (void)hipStreamSynchronize(c.stream);
   if (c.g_verify) (void)hipGraphExecDestroy(c.g_verify);
   if (c.g_draft) (void)hipGraphExecDestroy(c.g_draft);
+  if (c.g_draft1) (void)hipGraphExecDestroy(c.g_draft1);
   if (c.g_commit) (void)hipGraphExecDestroy(c.g_commit);
   if (c.g_drafts) (void)hipGraphExecDestroy(c.g_drafts);
   if (c.cap_stream) (void)hipStreamDestroy(c.cap_stream);

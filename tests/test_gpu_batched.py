@@ -9,7 +9,9 @@ pass run on the batched-row GEMM, with caches in shuffled KV pages.
     attention row blocks);
   * 16 scenes of the 16-scene workload's prompt structure (prompts of
     2048..8192 tokens, four camera grids each) at the 7B-class width through
-    one target layer, 144 rows: logits of every sequence against the oracle.
+    one target layer, 144 rows: logits of every sequence against the oracle;
+  * chained draft steps compacted to one row per sequence: the 16-scene loop
+    with and without compaction, and bit-equal proposals on the packed path.
 """
 import dataclasses
 
@@ -126,12 +128,45 @@ def test_sixteen_scenes_one_verify(tiny16, path):
     s.close()
 
 
-def test_sixteen_scenes_spec_loop(tiny16):
+@pytest.mark.parametrize("rows", ["one_row", "full"])
+def test_sixteen_scenes_spec_loop(tiny16, rows):
+    # chained draft steps after a round's first run as 16-row passes on the
+    # packed GEMV (live-row compaction), or, with SPEC_FLAG_FULL_DRAFT_ROWS,
+    # as the 80-row pass on the GEMM
+    from paper_2606_31160_amd import binding as B
     w, hp, T = tiny16
-    s = _session(w, page_seed=12)
+    s = _session(w, page_seed=12, flags=B.SPEC_FLAG_FULL_DRAFT_ROWS if rows == "full" else 0)
     outs = _loop(s)
     s.close()
     _check_history(w, T, outs)
+
+
+def _proposal_rounds(w, flags, rounds=3):
+    s = _session(w, page_seed=4, flags=flags)
+    props, coms = [], []
+    for _ in range(rounds):
+        for _ in range(s.K):
+            s.draft_step()
+        props.append(s.dtok.cpu().numpy().copy())
+        s.verify(None)
+        s.commit()
+        coms.append(s.committed()[0])
+    s.sync()
+    s.close()
+    return props, coms
+
+
+def test_one_row_draft_steps_equal_full_row_steps():
+    # 3 scenes, K = 4: 15-row passes on the packed GEMV.  A draft row's
+    # result does not depend on the pass's row count there, so compacted
+    # draft steps propose exactly what the full passes propose.
+    from paper_2606_31160_amd import binding as B
+    w = _scenes(W.get("C1"), 3, 430, 520, seed=8).with_(max_new_tokens=64)
+    a = _proposal_rounds(w, 0)
+    b = _proposal_rounds(w, B.SPEC_FLAG_FULL_DRAFT_ROWS)
+    for pa, pb in zip(a[0], b[0]):
+        np.testing.assert_array_equal(pa, pb)
+    assert a[1] == b[1]
 
 
 def test_block_of_16_eight_scenes():
