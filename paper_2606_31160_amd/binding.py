@@ -14,7 +14,9 @@ import os
 from ctypes import POINTER, Structure, c_char_p, c_double, c_float, c_int32, c_int64, c_size_t, c_void_p
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(_HERE, "libspecdec.so")
+# SPECDEC_LIBRARY: another build of the same library (the host-sanitizer
+# build of the ABI tests); by default the in-tree build.
+LIB_PATH = os.environ.get("SPECDEC_LIBRARY") or os.path.join(_HERE, "libspecdec.so")
 
 SPEC_MAX_K = 16
 SPEC_MAX_BATCH = 16

@@ -24,10 +24,22 @@ def hipcc() -> str:
     return "hipcc"
 
 
-def build(verbose: bool = False) -> str:
+# Host-side AddressSanitizer + UndefinedBehaviorSanitizer (device code is
+# built as usual); the sanitizer runtime is linked as a shared library, which
+# a host process preloads (LD_PRELOAD) before loading this build.
+SANITIZE_FLAGS = [
+    "-Xarch_host", "-fsanitize=address", "-Xarch_host", "-fsanitize=undefined",
+    "-Xarch_host", "-fno-sanitize-recover=undefined", "-Xarch_host", "-fno-omit-frame-pointer",
+    "-shared-libsan", "-g",
+]
+
+
+def build(verbose: bool = False, sanitize: bool = False, out: str = LIB) -> str:
+    dest = out
     srcs = [os.path.join(CSRC, s) for s in SOURCES]
-    tmp = LIB + ".tmp"
-    cmd = [hipcc(), *HIPCC_FLAGS, "-I", os.path.join(ROOT, "include"), *srcs, "-o", tmp]
+    tmp = dest + ".tmp"
+    extra = SANITIZE_FLAGS if sanitize else []
+    cmd = [hipcc(), *HIPCC_FLAGS, *extra, "-I", os.path.join(ROOT, "include"), *srcs, "-o", tmp]
     if verbose:
         print(" ".join(cmd), flush=True)
     r = subprocess.run(cmd, capture_output=True, text=True)
@@ -37,8 +49,17 @@ def build(verbose: bool = False) -> str:
         raise RuntimeError(f"hipcc failed ({r.returncode}):\n{out}")
     if out.strip() and verbose:
         print(out)
-    os.replace(tmp, LIB)
-    return LIB
+    os.replace(tmp, dest)
+    return dest
+
+
+def sanitizer_runtime() -> str:
+    """Path of the compiler's shared AddressSanitizer runtime."""
+    r = subprocess.run([hipcc(), "-print-file-name=libclang_rt.asan-x86_64.so"], capture_output=True, text=True)
+    path = r.stdout.strip()
+    if r.returncode != 0 or not os.path.isabs(path) or not os.path.exists(path):
+        raise RuntimeError(f"no shared AddressSanitizer runtime next to {hipcc()}")
+    return path
 
 
 if __name__ == "__main__":
