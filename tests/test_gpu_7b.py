@@ -4,6 +4,8 @@ benchmark times (batch 1, K = 8, 9 verify rows).
 
   * one target layer over the 3328-token two-frame prompt, against the oracle
     (logits, greedy tokens, accept length, new K/V rows, position ids);
+  * the same layer with two sequences (18 rows: the two-row-block GEMV, and
+    on the row-major path the GEMM's k-split q/k/v route), against the oracle;
   * the 2-layer FlatRoPE draft at that width, against the oracle;
   * 4 target layers with the full 152064-token tied head over the 4096-token
     prompt, against the oracle (l = 2 and the bonus token bit for bit);
@@ -89,6 +91,36 @@ def test_one_layer_verify_against_oracle(c2, K):
         for which, ref_c in ((0, seq.tc.k[li]), (1, seq.tc.v[li])):
             got = ON.decode(s.kv(0, 0, li, which, P, w.K + 1))
             assert S.normwise_err(got, ref_c[P:P + w.K + 1]) <= S.LOGIT_RTOL
+    s.close()
+
+
+def test_one_layer_two_sequences_18_rows_against_oracle(c2, path):
+    # batch 2, K = 8: 18 rows per pass.  Packed: the two-row-block GEMV.
+    # Row-major: 18 rows of a 3584-wide input do not fit the thin GEMV's LDS,
+    # so the pass runs on the batched GEMM, whose q/k/v launch would cover
+    # too few CUs in one split and takes the k-split route (partial sums, then
+    # the rotary and cache-append finish).  Each sequence's pending token is
+    # reseeded until its first three greedy rows are pinned (l = 2 each).
+    w, hp, T = c2
+    w = w.with_(seqs=(w.seqs[0], w.seqs[0]), p_accept=(0.75, 0.75))
+    assert w.batch * (w.K + 1) == 18
+    picks = [S.pinned_greedy_drafts(w, b, T, k=2, seed=31 + b) for b in range(2)]
+    s = _session(w, provider=hp, pending_tokens=[p[0] for p in picks])
+    P = w.seqs[0].prefix_len
+    drafts = np.stack([p[1] for p in picks])
+    s.verify(drafts, logits=True)
+    s.commit()
+    coms, acc, fin = s.committed()
+    gl = s.logits.float().cpu().numpy()
+    for b in range(2):
+        seq = S.oracle_sequence(w, b, T, None, with_draft=False, pending=picks[b][0])
+        ref = seq.verify(drafts[b])
+        for j in range(w.K + 1):
+            assert S.normwise_err(gl[b, j], ref.logits[j]) <= S.LOGIT_RTOL, (b, j)
+        S.assert_verify_matches(ref, drafts[b], coms[b], acc[b], k=2)
+        for which, ref_c in ((0, seq.tc.k[0]), (1, seq.tc.v[0])):
+            got = ON.decode(s.kv(b, 0, 0, which, P, w.K + 1))
+            assert S.normwise_err(got, ref_c[P:P + w.K + 1]) <= S.LOGIT_RTOL, (b, which)
     s.close()
 
 

@@ -139,11 +139,10 @@ def test_block_sixteen_scenes_gemm_equals_greedy():
 
 
 def test_block_paper_width_three_scenes_equals_greedy():
-    """Hidden 4096, 32/8 heads, K = 16, three scenes: the 51-row verify and block
-    passes keep the q/k/v GEMM in one split, while passes of 17..34 rows would
-    take its k-split route (too few workgroups), so its partial buffer must
-    cover pass row counts below the context's largest.  The greedy reference is
-    taken at the verify's pass shape, as above."""
+    """Hidden 4096, 32/8 heads, K = 16, three scenes: every pass (verify,
+    catch-up and block) has 51 rows and runs on the batched GEMM with q/k/v in
+    one split.  The greedy reference is taken at the verify's pass shape, as
+    above."""
     import dataclasses
     base = W.get("C6")
     w = base.with_(target=dataclasses.replace(base.target, layers=2), vocab=2048, max_new_tokens=24,

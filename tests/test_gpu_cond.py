@@ -10,6 +10,7 @@ at slot t takes the input e + W_in [e; f(t-1)].
     the block proposal;
   * the speculative loop with a conditioned draft commits exactly greedy
     decoding;
+  * a 3-layer tiny target capturing three distinct layers (0, 1, 2);
   * one target layer at 7B width with the 2-layer draft: features and
     proposals against the oracle.
 """
@@ -86,6 +87,22 @@ def test_conditioned_draft_against_oracle(c1, path, block):
     s = _session(w, provider=hp, flags=flags, cond_layers=LAYERS_TINY)
     seq = S.oracle_sequence(w, 0, T, D, cond=S.conditioning(w, hp, LAYERS_TINY))
     _rounds(w, s, seq, trace, block)
+    s.close()
+
+
+def test_conditioned_draft_three_distinct_target_layers():
+    # a 3-layer tiny target capturing layers (0, 1, 2): every column block of
+    # the fused operand comes from a different layer, so a swapped block or a
+    # layer taken twice changes the features
+    import dataclasses
+    base = W.get("C1")
+    w = base.with_(target=dataclasses.replace(base.target, layers=3))
+    hp = W.HostWeights(w)
+    T, D = S.oracle_decoders(w, hp)
+    trace = OS.greedy_trace(S.oracle_sequence(w, 0, T, None, with_draft=False))
+    s = _session(w, provider=hp, cond_layers=(0, 1, 2))
+    seq = S.oracle_sequence(w, 0, T, D, cond=S.conditioning(w, hp, (0, 1, 2)))
+    _rounds(w, s, seq, trace, block=False)
     s.close()
 
 
