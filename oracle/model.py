@@ -116,6 +116,12 @@ class Decoder:
         self.input_hook: Optional[Callable[[np.ndarray, np.ndarray], np.ndarray]] = None
         self.capture_layers: Sequence[int] = ()
         self.captured: Dict[int, np.ndarray] = {}
+        # cross-attention conditioning (Sec. 4.1): layer cross_layer attends,
+        # instead of to keys of its own rows, to a context of keys and values
+        # that context_kv() computed from another stack's states; row i sees
+        # the context slots below both its own slot and cross_len
+        self.cross_layer: Optional[int] = None
+        self.cross_len: int = 0
 
     # -- weights -----------------------------------------------------------
     def layer(self, li: int) -> Dict[str, np.ndarray]:
@@ -178,6 +184,21 @@ class Decoder:
         cache.k[layer][:P] = self._r(self.rotate(k, cache.pos3[:, :P]))
         cache.v[layer][:P] = v
 
+    def context_kv(self, cache: KVCache, layer: int, f: np.ndarray, slots: Sequence[int]) -> None:
+        """Cross-attention context of `layer` at `slots` (Sec. 4.1: target
+        hidden states become the draft's attention keys and values): the rows
+        f [N, hidden] go through the layer's attention norm and its W_k, W_v;
+        the keys are rotated at each slot's position."""
+        s = self.s
+        slots = np.asarray(slots, dtype=np.int64)
+        N = len(slots)
+        W = self.layer(layer)
+        a, ia = self._normed(np.asarray(f, dtype=np.float64), W["attn_norm"])
+        k = ((a @ W["wk"].T) * ia).reshape(N, s.kv_heads, s.head_dim)
+        v = ((a @ W["wv"].T) * ia).reshape(N, s.kv_heads, s.head_dim)
+        cache.k[layer][slots] = self._r(self.rotate(k, cache.pos3[:, slots]))
+        cache.v[layer][slots] = self._r(v)
+
     # -- forward -----------------------------------------------------------
     def forward(self, tokens: Sequence[int], slots: Sequence[int], cache: KVCache,
                 want_hidden: bool = False, visible: Optional[Sequence[int]] = None):
@@ -202,16 +223,19 @@ class Decoder:
             W = self.layer(li)
             a, ia = self._normed(x, W["attn_norm"])
             q = ((a @ W["wq"].T) * ia).reshape(M, nq, D)
-            k = ((a @ W["wk"].T) * ia).reshape(M, nkv, D)
-            v = ((a @ W["wv"].T) * ia).reshape(M, nkv, D)
             q = self._r(self.rotate(q, pos))
-            k = self._r(self.rotate(k, pos))
-            v = self._r(v)
-            cache.k[li][slots] = k
-            cache.v[li][slots] = v
+            if li == self.cross_layer:
+                # the context only: slots before the row's own and before cross_len
+                lvis = np.minimum(slots - 1, self.cross_len - 1)
+            else:
+                k = ((a @ W["wk"].T) * ia).reshape(M, nkv, D)
+                v = ((a @ W["wv"].T) * ia).reshape(M, nkv, D)
+                cache.k[li][slots] = self._r(self.rotate(k, pos))
+                cache.v[li][slots] = self._r(v)
+                lvis = vis
             if li == self.readout_layer:
-                self.readout = budget.budget(q, cache.k[li], vis, self.readout_classes)
-            o = self._r(attend(q, cache.k[li], cache.v[li], vis).reshape(M, nq * D))
+                self.readout = budget.budget(q, cache.k[li], lvis, self.readout_classes)
+            o = self._r(attend(q, cache.k[li], cache.v[li], lvis).reshape(M, nq * D))
             x = x + o @ W["wo"].T
             b, ib = self._normed(x, W["ffn_norm"])
             u = self._r(silu((b @ W["w_gate"].T) * ib) * ((b @ W["w_up"].T) * ib))

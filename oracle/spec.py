@@ -77,13 +77,24 @@ class Conditioning:
     where h_l(t) is the target's residual stream after layer l at slot t, taken
     from verify rows whose inputs are committed; f is zero where the target has
     not verified the slot (prompt slots, since prefill is not part of the
-    path, and the draft's own proposal rows)."""
+    path, and the draft's own proposal rows).
 
-    def __init__(self, layers, w_fuse: np.ndarray, w_in: np.ndarray, mirror: bool = False):
+    cross=True is the form Sec. 4.1 states: the fused states are the draft's
+    cross-attention keys and values instead of an input term.  The draft's
+    layer 0 then attends only to a context whose slot s holds
+    k = rot_s(W_k RMSNorm(f_s)), v = W_v RMSNorm(f_s) (its own layer-0 norm
+    and projections), for the slots the target has verified, and the given
+    prompt keys and values for the prompt slots; a draft row at slot t sees
+    the context slots s < t that exist (s < seq_len), and its input is the
+    plain embedding (W_in is not used)."""
+
+    def __init__(self, layers, w_fuse: np.ndarray, w_in: Optional[np.ndarray], mirror: bool = False,
+                 cross: bool = False):
         self.layers = tuple(int(l) for l in layers)
         self.w_fuse = np.asarray(w_fuse, dtype=np.float64)
-        self.w_in = np.asarray(w_in, dtype=np.float64)
+        self.w_in = None if w_in is None else np.asarray(w_in, dtype=np.float64)
         self.mirror = mirror
+        self.cross = cross
 
     def fuse(self, captured, j: int) -> np.ndarray:
         h = np.concatenate([captured[l][j] for l in self.layers])
@@ -174,6 +185,9 @@ class Sequence:
             # the accepted proposals): their features are final
             for j in range(len(toks)):
                 self.feat[n + j] = self.cond.fuse(self.T.captured, j)
+            if self.cond.cross and self.D is not None:
+                slots_c = list(range(n, n + len(toks)))
+                self.D.context_kv(self.dc, 0, np.stack([self.feat[t] for t in slots_c]), slots_c)
         self._commit(n, toks)
         self.finished = fin
         self.history.append(l)
@@ -197,12 +211,15 @@ class Sequence:
 
     # draft -------------------------------------------------------------------
     def _draft_forward(self, tokens, slots, visible=None):
-        if self.cond is not None:
+        if self.cond is not None and self.cond.cross:
+            self.D.cross_layer, self.D.cross_len = 0, self.seq_len
+        elif self.cond is not None:
             self.D.input_hook = lambda x, sl: self.cond.input(x, sl, self.feat)
         try:
             return self.D.forward(tokens, slots, self.dc, visible=visible)
         finally:
             self.D.input_hook = None
+            self.D.cross_layer, self.D.cross_len = None, 0
 
     def draft_input(self, s: int) -> int:
         n = self.seq_len

@@ -48,12 +48,13 @@ def device_kv(w: W.Workload, b: int, model: str):
                        bits(W.prefix_kv_device(w, b, model, li, "v")))
 
 
-def conditioning(w: W.Workload, provider, layers, mirror: bool = False):
+def conditioning(w: W.Workload, provider, layers, mirror: bool = False, cross: bool = False):
     """The oracle's target-hidden-state conditioning with the workload's seeded
-    fusion weights."""
+    fusion weights (cross: as the draft's layer-0 cross-attention context)."""
     from oracle import numerics as ON
     return OS.Conditioning(layers, ON.decode(provider.get("draft", -1, "w_fuse")),
-                           ON.decode(provider.get("draft", -1, "w_in")), mirror=mirror)
+                           None if cross else ON.decode(provider.get("draft", -1, "w_in")), mirror=mirror,
+                           cross=cross)
 
 
 def oracle_sequence(w: W.Workload, b: int, T, D, kv=None, capacity=None, pending=None,

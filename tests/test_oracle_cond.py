@@ -129,3 +129,114 @@ def test_sequence_wires_features_to_committed_slots_and_draft_rows():
     for i, t in enumerate(slots):
         f = seq.feat.get(t - 1, np.zeros(w.target.hidden))
         assert np.allclose(x[i], 3.0 * e[i] + 7.0 * f, rtol=1e-12, atol=1e-12), t
+
+
+# --- the cross-attention form (Sec. 4.1: target states as the draft's K/V) ------------
+
+def _cross_seq(mirror=False):
+    w = _w()
+    hp = W.HostWeights(w)
+    T, D = S.oracle_decoders(w, hp)
+    cond = S.conditioning(w, hp, (2, 0, 1), cross=True)
+    trace = OS.greedy_trace(S.oracle_sequence(w, 0, T, None, with_draft=False))
+    seq = S.oracle_sequence(w, 0, T, D, cond=cond)
+    return w, T, D, seq, trace
+
+
+def test_cross_context_rows_are_the_draft_layer0_projections_of_the_features():
+    # after a verify that commits three rows, the draft's layer-0 cache holds,
+    # at exactly those slots, rot_s(W_k RMSNorm(f_s) g) and W_v RMSNorm(f_s) g;
+    # prompt slots keep the given keys and values, other slots stay untouched
+    from oracle import rope
+    w, T, D, seq, trace = _cross_seq()
+    n, P = seq.seq_len, seq.P
+    before_k, before_v = seq.dc.k[0].copy(), seq.dc.v[0].copy()
+    res = seq.verify([trace[0], trace[1], (trace[2] + 1) % w.vocab])
+    assert res.accept_len == 2
+    Wd = D.layer(0)
+    s = D.s
+    for t in (n, n + 1, n + 2):
+        a = M.rmsnorm(seq.feat[t], Wd["attn_norm"], s.rms_eps)
+        k = (Wd["wk"] @ a).reshape(1, s.kv_heads, s.head_dim)
+        want_k = rope.flatrope(k, np.array([t]), s.rope_base)[0]
+        want_v = (Wd["wv"] @ a).reshape(s.kv_heads, s.head_dim)
+        assert np.allclose(seq.dc.k[0][t], want_k, rtol=1e-10, atol=1e-12), t
+        assert np.allclose(seq.dc.v[0][t], want_v, rtol=1e-10, atol=1e-12), t
+    untouched = [i for i in range(seq.dc.cap) if i not in (n, n + 1, n + 2)]
+    assert np.array_equal(seq.dc.k[0][untouched], before_k[untouched])
+    assert np.array_equal(seq.dc.v[0][untouched], before_v[untouched])
+    assert np.any(before_k[:P] != 0)
+
+
+def test_cross_attention_with_zero_keys_averages_the_visible_context():
+    # zero W_k and W_q in the draft's layer 0 make every score 0, so each head's
+    # output is the plain mean of the values the row sees: the context slots
+    # s < min(t, seq_len).  With that layer's down projection zeroed the
+    # draft's final hidden row is RMSNorm(e + o W_o^T) g_final, a closed form
+    # of that visible set.
+    w, T, D, seq, trace = _cross_seq()
+    seq.verify([trace[0], (trace[1] + 1) % w.vocab, 0])        # l = 1: two rows committed
+    Wd = D.layer(0)
+    saved = {k: Wd[k].copy() for k in ("wq", "wk", "w_down")}
+    for k in saved:
+        Wd[k][:] = 0.0
+    try:
+        n = seq.seq_len
+        # the rows of the next draft step (catch-up rows before n, the pending row at n)
+        slots = list(range(seq.draft_len, n + 1))
+        toks = [seq.draft_input(t) for t in slots]
+        D.cross_layer, D.cross_len = 0, n
+        z, hid = D.forward(toks, slots, seq.dc, want_hidden=True)
+        D.cross_layer, D.cross_len = None, 0
+        s = D.s
+        G = s.q_heads // s.kv_heads
+        for i, t in enumerate(slots):
+            m = min(t, n)                                          # visible: 0 .. m-1
+            o = np.concatenate([seq.dc.v[0][:m, h // G, :].mean(axis=0) for h in range(s.q_heads)])
+            x = D.embed_rows([toks[i]])[0] + Wd["wo"] @ o
+            want = M.rmsnorm(x, D.final_norm(), s.rms_eps)
+            assert np.allclose(hid[i], want, rtol=1e-10, atol=1e-12), t
+    finally:
+        for k, v in saved.items():
+            Wd[k][:] = v
+
+
+def test_cross_row_sees_neither_its_own_slot_nor_unverified_slots():
+    w, T, D, seq, trace = _cross_seq()
+    seq.verify([trace[0], trace[1], (trace[2] + 1) % w.vocab])   # three rows committed
+    n = seq.seq_len
+
+    def run(slot_tok):
+        D.cross_layer, D.cross_len = 0, n
+        try:
+            return D.forward([slot_tok[1]], [slot_tok[0]], seq.dc)
+        finally:
+            D.cross_layer, D.cross_len = None, 0
+
+    t = n - 1                       # a catch-up row at a verified slot
+    row = (t, seq.token_at(t))
+    z0 = run(row)
+    for which in ("k", "v"):
+        c = getattr(seq.dc, which)[0]
+        keep = c.copy()
+        c[t] += 3.0                 # the row's own slot: not visible
+        assert np.array_equal(run(row), z0)
+        c[:] = keep
+        c[t - 1] += 3.0             # the slot before: visible
+        assert not np.allclose(run(row), z0)
+        c[:] = keep
+    # a proposal row beyond seq_len sees no context at or after seq_len
+    row = (n + 2, 5)
+    z1 = run(row)
+    c = seq.dc.v[0]
+    keep = c.copy()
+    c[n:n + 2] += 3.0
+    assert np.array_equal(run(row), z1)
+    c[n - 1] += 3.0
+    assert not np.allclose(run(row), z1)
+    c[:] = keep
+
+
+def test_cross_conditioned_spec_loop_equals_greedy():
+    w, T, D, seq, trace = _cross_seq()
+    assert OS.spec_loop(seq, lambda sq: sq.propose()) == list(trace)
