@@ -536,29 +536,33 @@ def main():
     del sb
 
     # 3c. the same rounds with the draft conditioned on target hidden states
-    # (layers 1, 14, 24 of 28 fused, EAGLE-3 style), K-step chain
-    sc = Session(w, source="device", provider=src, cond_layers=(1, 14, 24))
-    evc = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(args.steps)]
-    for r in range(args.warmup + args.steps):
-        k = r - args.warmup
-        if k >= 0:
-            evc[k][0].record()
-        B.draft_steps(sc.ctx, K, sc.dtok.data_ptr())
-        if k >= 0:
-            evc[k][1].record()
-        B.spec_verify(sc.ctx, drafts[r].data_ptr(), 0)
-        if k >= 0:
-            evc[k][2].record()
-        B.spec_commit(sc.ctx, sc.acc.data_ptr(), 0, sc.ncom.data_ptr(), sc.fin.data_ptr())
-        if k >= 0:
-            evc[k][3].record()
-    torch.cuda.synchronize()
-    assert sc.state(0)["n_gen"] == expect
-    cond_d = [e[0].elapsed_time(e[1]) for e in evc]
-    cond_v = [e[1].elapsed_time(e[2]) for e in evc]
-    cond_round = [e[0].elapsed_time(e[3]) for e in evc]
-    sc.close()
-    del sc
+    # (layers 1, 14, 24 of 28 fused, EAGLE-3 style), K-step chain: as the
+    # draft's input term, and as its layer-0 cross-attention context
+    def cond_rounds(cross):
+        sc = Session(w, source="device", provider=src, cond_layers=(1, 14, 24), cond_cross=cross)
+        evc = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(args.steps)]
+        for r in range(args.warmup + args.steps):
+            k = r - args.warmup
+            if k >= 0:
+                evc[k][0].record()
+            B.draft_steps(sc.ctx, K, sc.dtok.data_ptr())
+            if k >= 0:
+                evc[k][1].record()
+            B.spec_verify(sc.ctx, drafts[r].data_ptr(), 0)
+            if k >= 0:
+                evc[k][2].record()
+            B.spec_commit(sc.ctx, sc.acc.data_ptr(), 0, sc.ncom.data_ptr(), sc.fin.data_ptr())
+            if k >= 0:
+                evc[k][3].record()
+        torch.cuda.synchronize()
+        assert sc.state(0)["n_gen"] == expect
+        res = ([e[0].elapsed_time(e[1]) for e in evc], [e[1].elapsed_time(e[2]) for e in evc],
+               [e[2].elapsed_time(e[3]) for e in evc], [e[0].elapsed_time(e[3]) for e in evc])
+        sc.close()
+        return res
+
+    cond_d, cond_v, _, cond_round = cond_rounds(False)
+    cross_d, cross_v, cross_c, cross_round = cond_rounds(True)
 
     # 4. per-kernel timing pass (events around every launch, no graph replay)
     B.spec_timing(s.ctx, True)
@@ -648,6 +652,16 @@ def main():
         "tokens_per_s": round(timed_tokens / (sum(cond_round) / 1e3), 2),
         "note": "draft conditioned on target layers 1, 14, 24 (residual streams kept by the verify, committed "
                 "rows fused 3H->H per slot, draft input e + W_in[e; f]); K=8 step chain; same rounds and drafts"}
+    xd_us = float(np.median(cross_d)) * 1e3 / K
+    xv_us = float(np.median(cross_v)) * 1e3
+    out["cross_attention_draft"] = {
+        "verify_us": round(xv_us, 1), "draft_step_us": round(xd_us, 1),
+        "commit_us": round(float(np.median(cross_c)) * 1e3, 1),
+        "cost_ratio_c": round(K * xd_us / xv_us, 4),
+        "tokens_per_s": round(timed_tokens / (sum(cross_round) / 1e3), 2),
+        "note": "the same fused features as the draft's layer-0 cross-attention context (K/V of every committed "
+                "slot written by the commit through the draft's layer-0 projection; prompt slots keep the given "
+                "draft prompt K/V); K=8 step chain; same rounds and drafts"}
     out["verify_us_p10_p50_p90"] = [round(float(np.percentile(verify_ms, q)) * 1e3, 1) for q in (10, 50, 90)]
     out["round_ms_p10_p50_p90"] = [round(float(np.percentile(round_ms, q)), 3) for q in (10, 50, 90)]
     if not args.no_batched:

@@ -96,6 +96,15 @@ typedef struct spec_dims {
                                       e + w_in [e; f(t-1)] (2*hidden -> hidden; f = 0 where no verified
                                       feature exists: prompt slots and the draft's proposal rows).
                                       Needs a draft with w_fuse and w_in. */
+#define SPEC_FLAG_COND_CROSS 256   /* with SPEC_FLAG_COND: the fused features f are the draft's layer-0
+                                      cross-attention context (Sec. 4.1: target hidden states fed to the
+                                      draft as cross-attention K/V) instead of the input term.  After each
+                                      commit, every committed slot s gets k = rot_s(W_k RMSNorm(f_s)) and
+                                      v = W_v RMSNorm(f_s) (the draft's layer-0 norm and projections) in
+                                      the draft's layer-0 cache; the prompt slots keep the given draft
+                                      prompt K/V.  A draft row at slot t attends in layer 0 to the context
+                                      slots s < min(t, seq_len) only, and takes the plain embedding as
+                                      input (w_in may be null).  Not with SPEC_FLAG_BLOCK_DRAFT. */
 #define SPEC_FLAG_FULL_DRAFT_ROWS 128  /* every draft step runs the pass of batch*(K+1) rows.  Without it,
                                       a chained draft step after the first of a round (each live sequence
                                       then consumes exactly one token, its previous proposal) runs as a

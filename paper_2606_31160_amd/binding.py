@@ -29,6 +29,7 @@ SPEC_FLAG_DRAFT_MROPE = 16
 SPEC_FLAG_BLOCK_DRAFT = 32
 SPEC_FLAG_COND = 64
 SPEC_FLAG_FULL_DRAFT_ROWS = 128
+SPEC_FLAG_COND_CROSS = 256
 STATUS = {0: "SPEC_OK", 1: "SPEC_E_INVAL", 2: "SPEC_E_STATE", 3: "SPEC_E_CAPACITY", 5: "SPEC_E_HIP",
           6: "SPEC_E_NUMERIC"}
 KERNEL_KINDS = {"qkv": 0, "o": 1, "gateup": 2, "down": 3, "lmhead": 4, "attn": 5, "other": 6}

@@ -56,7 +56,7 @@ constexpr int kCondSplits = 4;   // k-splits of the feature fusion (3H inputs) a
 // Passes: the target's verify; one draft step (consume, propose from the last
 // row); for the single-forward block proposal, the draft's causal catch-up of
 // committed tokens it has not consumed (no LM head) and the block pass itself.
-enum PassMode { PASS_VERIFY = 0, PASS_DRAFT = 1, PASS_CATCHUP = 2, PASS_BLOCK = 3 };
+enum PassMode { PASS_VERIFY = 0, PASS_DRAFT = 1, PASS_CATCHUP = 2, PASS_BLOCK = 3, PASS_CTX = 4 };
 
 struct LayerW {
   const bf16_t *attn_norm, *wq, *wk, *wv, *wo, *ffn_norm, *wg, *wu, *wd;
@@ -147,6 +147,12 @@ struct Ctx {
   float* fusedp = nullptr;           // [kCondSplits][M][H] k-split partial sums of w_fuse . cat3
   bf16_t* feat = nullptr;            // [B][cap][H] fused feature of every verified slot
   bf16_t* cat2 = nullptr;            // [Mpad][2H] draft rows' [embedding; feature of the previous slot]
+  // SPEC_FLAG_COND_CROSS: the features are the draft's layer-0 cross-attention
+  // context instead of an input term; that layer's own K/V appends go to
+  // these unread pools (one draft layer's worth each)
+  bool cross = false;
+  bf16_t* junk_kc = nullptr;
+  bf16_t* junk_vt = nullptr;
 
   // host state machine
   enum Phase { READY = 0, DRAFTING = 1, VERIFIED = 2 } phase = READY;

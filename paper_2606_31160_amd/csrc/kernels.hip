@@ -132,6 +132,9 @@ __global__ void k_stage_verify(SeqState* st, const int32_t* over, int K, int V, 
 // ---------------------------------------------------------------------------
 // Row plan + embedding gather.  grid (R, B), 1024 threads.
 // Verify: rows at slots seq_len .. seq_len+K, tokens vtok.
+// Context (cross-attention conditioning, after a commit): rows at the
+// verify's committed slots, taking the slots' fused features instead of
+// embeddings.
 // Draft: rows at slots draft_len .. seq_len+dstep (catch-up), tokens from the
 // committed history up to seq_len and the draft's own proposals after it.
 // Writes the residual stream x, xg = bf16(x * g) with the first layer's
@@ -183,6 +186,12 @@ __global__ __launch_bounds__(1024) void k_embed(EmbedArgs p) {
     count = s.finished ? 0 : p.R;
     causal = 1;
     tok = j == 0 ? p.hist[(size_t)b * p.cap + base] : p.mask;
+  } else if (p.mode == PASS_CTX) {
+    // cross-attention context rows: the fused features of the slots whose
+    // inputs the last commit took from its verify (rows 0 .. n_commit-1 at
+    // the verify's slots)
+    base = s.base;
+    count = s.count > 0 ? s.n_commit : 0;
   } else {
     base = s.draft_len;
     const int last = s.seq_len + s.dstep;
@@ -206,7 +215,8 @@ __global__ __launch_bounds__(1024) void k_embed(EmbedArgs p) {
     if (live && threadIdx.x == 0) atomicOr(&p.st[b].err, ERR_TOKEN);
     tok = 0;
   }
-  const bf16_t* er = p.E + (size_t)tok * p.H;
+  const bf16_t* er = p.mode == PASS_CTX ? p.feat + ((size_t)b * p.cap + (live ? base + j : 0)) * p.H
+                                        : p.E + (size_t)tok * p.H;
   for (int n = threadIdx.x; n < p.H; n += blockDim.x) {
     const float v = live ? bf2f(er[n]) : 0.f;
     p.x[r * p.H + n] = v;
@@ -781,6 +791,7 @@ struct AttnArgs {
   const int8_t* cls;     // readout: [B][cap] class of every slot (0 visual, 1 trajectory/text, 2 generated)
   float* rp;             // readout: [splits][B][nq][R][4] class sums and trajectory E term
   int cap;
+  int cross;             // cross-attention context: row j sees the slots below min(base + j, seq_len)
 };
 
 template <int D, bool RO>
@@ -795,18 +806,21 @@ __device__ __forceinline__ void attn_partials(const AttnArgs& a, unsigned char* 
   // page 0), so the key and value loads wait for one round trip, not two.
   const int page = a.pt[b * a.pps + split];
   const SeqState& s = a.st[b];
-  const int count = s.count, base = s.base, causal = s.causal;
-  asm volatile("" ::"s"(page), "s"(count), "s"(base), "s"(causal));   // all loads issued before any is awaited
+  const int count = s.count, base = s.base, causal = s.causal, seq_len = s.seq_len;
+  asm volatile("" ::"s"(page), "s"(count), "s"(base), "s"(causal), "s"(seq_len));   // all loads issued before any is awaited
   const int rows = count * a.G;
   const int wrow0 = rb * 64 + wave * 16;
   const int qr = wrow0 + (lane & 15);
   const bool rvalid = qr < rows;
   const int j = rvalid ? qr / a.G : 0;
   const int hq = kvh * a.G + (rvalid ? qr % a.G : 0);
-  const int kv_end = base + count;
+  // keys [0, vis_end) of row j: causal (rows past `causal` see the whole
+  // pass), or, for a cross-attention context, the context slots before the
+  // row's own slot that exist (below seq_len)
+  const int kv_end = a.cross ? min(base + count - 1, seq_len) : base + count;
   const int k0 = split * a.chunk;
   const int k1 = min(k0 + a.chunk, kv_end);
-  const int vis_end = base + (j < causal ? j + 1 : count);   // rows past `causal` see the whole pass
+  const int vis_end = a.cross ? min(base + j, seq_len) : base + (j < causal ? j + 1 : count);
   const size_t oi = (((size_t)split * a.B + b) * a.nq + hq) * a.R + j;
 
   if (k0 >= k1) {                                   // no keys in this split (workgroup-uniform)
@@ -1005,6 +1019,7 @@ struct CombineArgs {
   const float* rp;       // readout: [splits][B][nq][R][4] partial class sums and E terms
   float* ro;             // readout: [B][R][nq][4] masses (visual, trajectory/text, generated), entropy
   float inv_ln[SPEC_MAX_BATCH];   // readout: 1 / ln(trajectory/text slots) of each sequence, 0 if <= 1
+  int cross;             // cross-attention context (as AttnArgs::cross)
 };
 
 // One (row j, q head h, sequence b) of the combine; coef is LDS of at least
@@ -1015,7 +1030,7 @@ template <bool RO>
 __device__ __forceinline__ void combine_unit(const CombineArgs& a, int j, int h, int b, float* coef) {
   const SeqState& s = a.st[b];
   if (j >= s.count) return;
-  const int vis_end = s.base + (j < s.causal ? j + 1 : s.count);
+  const int vis_end = a.cross ? min(s.base + j, s.seq_len) : s.base + (j < s.causal ? j + 1 : s.count);
   const int ns = (vis_end + a.chunk - 1) / a.chunk;   // splits holding keys this row sees
   const size_t row = ((size_t)b * a.nq + h) * a.R + j;
   const size_t sstride = (size_t)a.B * a.nq * a.R;
@@ -1407,11 +1422,12 @@ hipError_t launch_attention(Ctx& c, Model& m, int li) {
   const int G = nq / nkv;
   const int rb = (c.R * G + 63) / 64;
   const bool ro = c.ro_out && c.ro_m == &m && c.ro_layer == li;
+  const int cross = (c.cross && &m == &c.drf && li == 0) ? 1 : 0;
   AttnArgs p{c.st, c.q, kc, vt, c.pt, c.op, c.mp, c.lp, nq, nkv, G, c.R, c.B, c.pps, c.attn_chunk, rb,
-             kLog2e / sqrtf((float)D), c.cls, c.rp, c.cap};
+             kLog2e / sqrtf((float)D), c.cls, c.rp, c.cap, cross};
   dim3 grid(c.attn_splits, nkv * rb, c.B);
   CombineArgs cb{c.st, c.op, c.mp, c.lp, c.o, nq, D, c.R, c.B, c.attn_chunk, c.rp,
-                 ro ? c.ro_out : nullptr, {}};
+                 ro ? c.ro_out : nullptr, {}, cross};
   for (int b = 0; b < c.B && b < SPEC_MAX_BATCH; ++b) cb.inv_ln[b] = c.ro_inv_ln[b];
   const size_t comb_lds = (size_t)(((c.attn_splits + 3) & ~3) + 8 * D) * sizeof(float);
   const size_t lds = attn_lds_bytes(c.attn_chunk, D);
@@ -1474,9 +1490,62 @@ hipError_t run_layer_sg(Ctx& c, Model& m, int li, bool block) {
   return hipSuccess;
 }
 
+// q, k, v (+ 1/rms of the attention norm) + rotary + cache append of one
+// layer on the row-major path (thin GEMV or batched GEMM), appending K and
+// V^T to the given layer pools.
+hipError_t launch_qkv_rm(Ctx& c, Model& m, int li, bf16_t* kc, bf16_t* vt) {
+  const spec_dims& d = m.d;
+  const int H = d.hidden, D = d.head_dim, nq = d.q_heads, nkv = d.kv_heads;
+  const int M = c.M;
+  const LayerW& w = m.L[li];
+  const bf16_t* pk = (c.gemm_rows && c.gemm_pk) ? m.pk + m.pk_layer * li : nullptr;
+  GemvArgs g = gemv_base(c, M, c.R);
+  g.w[0] = w.wq;
+  g.w[1] = w.wk;
+  g.w[2] = w.wv;
+  g.row0[0] = 0;
+  g.row0[1] = nq * D;
+  g.row0[2] = (nq + nkv) * D;
+  g.nseg = 3;
+  g.N = (nq + 2 * nkv) * D;
+  g.Kd = H;
+  g.x = c.xg;
+  g.ldx = H;
+  g.ss_in = c.ss;
+  g.H = H;
+  g.eps = d.rms_eps;
+  g.q = c.q;
+  g.kc = kc;
+  g.vt = vt;
+  g.rcs = c.rcs;
+  g.nq = nq;
+  g.nkv = nkv;
+  g.D = D;
+  g.pt = c.pt;
+  g.pps = c.pps;
+  g.pw = pk;
+  const int sq = c.gemm_rows ? gemm_qkv_splits(g.N, H, M, c.ncu) : 1;
+  if (sq > 1) {
+    // too few 64-column workgroups to stream the matrix at full rate: k-split
+    // partial sums, then the norm, rotation and cache append in k_qkv_finish
+    g.splits = sq;
+    g.out = c.part;
+    CK(gemm_run(c, EPI_STORE, g, SPEC_KERNEL_QKV, gemv_bytes(g.N, H, M, 4.0 * sq)));
+    QkvFinishArgs p{c.st, c.part, sq, M, g.N, c.R, c.Mpad, H, d.rms_eps, c.ss, c.rcs, c.pt,
+                    nq, nkv, D, c.pps, c.q, kc, vt};
+    Timed t(c, SPEC_KERNEL_OTHER, 0);
+    hipExtLaunchKernelGGL(k_qkv_finish, dim3((g.N / 2 + 255) / 256, M), dim3(256), 0, S(c), t.e0, t.e1, 0, p);
+    CK(hipGetLastError());
+  } else if (c.gemm_rows)
+    CK(gemm_run(c, EPI_ROPE, g, SPEC_KERNEL_QKV, gemv_bytes(g.N, H, M, 2.0)));
+  else
+    CK((gemv_launch<EPI_ROPE, 1>(c, g, SPEC_KERNEL_QKV, gemv_bytes(g.N, H, M, 2.0))));
+  return hipSuccess;
+}
+
 hipError_t run_layer(Ctx& c, Model& m, int li, const bf16_t* next_gain, bool select_last) {
   const spec_dims& d = m.d;
-  const int H = d.hidden, D = d.head_dim, nq = d.q_heads, nkv = d.kv_heads, F = d.ffn;
+  const int H = d.hidden, D = d.head_dim, nq = d.q_heads, F = d.ffn;
   const int M = c.M;
   const LayerW& w = m.L[li];
   bf16_t* kc = m.kc + m.kv_layer * li;
@@ -1484,50 +1553,13 @@ hipError_t run_layer(Ctx& c, Model& m, int li, const bf16_t* next_gain, bool sel
   // the GEMM streams this layer's tile-packed copy when there is one
   const bf16_t* pk = (c.gemm_rows && c.gemm_pk) ? m.pk + m.pk_layer * li : nullptr;
 
-  // q, k, v (+ 1/rms of the attention norm) + rotary + cache append
-  {
-    GemvArgs g = gemv_base(c, M, c.R);
-    g.w[0] = w.wq;
-    g.w[1] = w.wk;
-    g.w[2] = w.wv;
-    g.row0[0] = 0;
-    g.row0[1] = nq * D;
-    g.row0[2] = (nq + nkv) * D;
-    g.nseg = 3;
-    g.N = (nq + 2 * nkv) * D;
-    g.Kd = H;
-    g.x = c.xg;
-    g.ldx = H;
-    g.ss_in = c.ss;
-    g.H = H;
-    g.eps = d.rms_eps;
-    g.q = c.q;
-    g.kc = kc;
-    g.vt = vt;
-    g.rcs = c.rcs;
-    g.nq = nq;
-    g.nkv = nkv;
-    g.D = D;
-    g.pt = c.pt;
-    g.pps = c.pps;
-    g.pw = pk;
-    const int sq = c.gemm_rows ? gemm_qkv_splits(g.N, H, M, c.ncu) : 1;
-    if (sq > 1) {
-      // too few 64-column workgroups to stream the matrix at full rate: k-split
-      // partial sums, then the norm, rotation and cache append in k_qkv_finish
-      g.splits = sq;
-      g.out = c.part;
-      CK(gemm_run(c, EPI_STORE, g, SPEC_KERNEL_QKV, gemv_bytes(g.N, H, M, 4.0 * sq)));
-      QkvFinishArgs p{c.st, c.part, sq, M, g.N, c.R, c.Mpad, H, d.rms_eps, c.ss, c.rcs, c.pt,
-                      nq, nkv, D, c.pps, c.q, kc, vt};
-      Timed t(c, SPEC_KERNEL_OTHER, 0);
-      hipExtLaunchKernelGGL(k_qkv_finish, dim3((g.N / 2 + 255) / 256, M), dim3(256), 0, S(c), t.e0, t.e1, 0, p);
-      CK(hipGetLastError());
-    } else if (c.gemm_rows)
-      CK(gemm_run(c, EPI_ROPE, g, SPEC_KERNEL_QKV, gemv_bytes(g.N, H, M, 2.0)));
-    else
-      CK((gemv_launch<EPI_ROPE, 1>(c, g, SPEC_KERNEL_QKV, gemv_bytes(g.N, H, M, 2.0))));
-  }
+  // q, k, v (+ 1/rms of the attention norm) + rotary + cache append; the
+  // draft's layer 0 under cross-attention conditioning appends nowhere
+  // visible (its cache holds the target context)
+  if (c.cross && &m == &c.drf && li == 0)
+    CK(launch_qkv_rm(c, m, li, c.junk_kc, c.junk_vt));
+  else
+    CK(launch_qkv_rm(c, m, li, kc, vt));
   CK(launch_attention(c, m, li));
   // o projection + residual; bf16(x * g_ffn) and sums of x^2 for the FFN norm
   {
@@ -1712,8 +1744,11 @@ bool sg_build_jobs(Ctx& c, Model& m, bool draft, bool fill) {
     j[0].ss_in = c.ss;
     j[0].Hn = H;
     j[0].q = c.q;
-    j[0].kc = m.kc ? m.kc + m.kv_layer * li : nullptr;
-    j[0].vt = m.vt ? m.vt + m.kv_layer * li : nullptr;
+    // the draft's layer 0 under cross-attention conditioning: its rows'
+    // own K/V go to the unread pools (that layer's cache is the context)
+    const bool junk = c.cross && draft && li == 0;
+    j[0].kc = junk ? c.junk_kc : (m.kc ? m.kc + m.kv_layer * li : nullptr);
+    j[0].vt = junk ? c.junk_vt : (m.vt ? m.vt + m.kv_layer * li : nullptr);
     j[0].pt = c.pt;
     j[0].pps = c.pps;
     j[0].rcs = c.rcs;
@@ -1917,7 +1952,7 @@ hipError_t launch_forward(Ctx& c, PassMode mode) {
                 c.ss,  c.rcs,
                 c.pos3,  c.cs,   m.axis,       d.hidden,         c.R, c.cap,    (int)mode, c.Mpad,
                 d.head_dim, m.flat ? 1 : 0, c.V, c.mask_token,
-                (c.cond && mode != PASS_VERIFY) ? c.cat2 : nullptr, c.feat};
+                (c.cond && !c.cross && mode != PASS_VERIFY) ? c.cat2 : nullptr, c.feat};
     Timed t(c, SPEC_KERNEL_OTHER, 0);
     hipExtLaunchKernelGGL(k_embed, dim3(c.R, c.B), dim3(1024), (size_t)d.hidden * sizeof(float), c.stream, t.e0, t.e1, 0, p);
     CK(hipGetLastError());
@@ -1925,7 +1960,7 @@ hipError_t launch_forward(Ctx& c, PassMode mode) {
   // draft: a draft step, which proposes from each sequence's last row (stored
   // as row b); a block pass runs the LM head over every row, as a verify does
   const bool draft = mode == PASS_DRAFT, block = mode == PASS_BLOCK;
-  if (c.cond && mode != PASS_VERIFY) CK(launch_cond_input(c, m));
+  if (c.cond && !c.cross && mode != PASS_VERIFY) CK(launch_cond_input(c, m));
   auto capture = [&](int li) -> hipError_t {   // conditioning: the verify keeps chosen layers' output
     if (!c.cond || mode != PASS_VERIFY) return hipSuccess;
     for (int i = 0; i < 3; ++i)
@@ -1999,6 +2034,33 @@ hipError_t launch_forward(Ctx& c, PassMode mode) {
   return hipSuccess;
 }
 
+// Cross-attention conditioning, after a commit (Sec. 4.1): the committed
+// slots' fused features become the draft's layer-0 context.  They take the
+// draft's layer-0 norm and q/k/v projection as a pass of their own: rows at
+// the verify's committed slots, keys rotated at those slots and appended with
+// the values to the layer's cache (the query output is not used).
+hipError_t launch_ctx_kv(Ctx& c) {
+  Model& m = c.drf;
+  const spec_dims& d = m.d;
+  {
+    EmbedArgs p{c.st,   c.hist, c.embed, m.L[0].attn_norm, c.x, c.xg, c.ss, c.rcs, c.pos3, c.cs, m.axis,
+                d.hidden, c.R, c.cap, (int)PASS_CTX, c.Mpad, d.head_dim, m.flat ? 1 : 0, c.V, c.mask_token,
+                nullptr, c.feat};
+    Timed t(c, SPEC_KERNEL_OTHER, 0);
+    hipExtLaunchKernelGGL(k_embed, dim3(c.R, c.B), dim3(1024), (size_t)d.hidden * sizeof(float), c.stream, t.e0,
+                          t.e1, 0, p);
+    CK(hipGetLastError());
+  }
+  if (c.sg) {
+    SgJob j = sg_job(c, m.sg_host[0]);
+    j.kc = m.kc;
+    j.vt = m.vt;
+    Timed t(c, SPEC_KERNEL_OTHER, 0);
+    return sg_launch(SG_ROPE, j, S(c), t.e0, t.e1);
+  }
+  return launch_qkv_rm(c, m, 0, m.kc, m.vt);
+}
+
 hipError_t launch_commit(Ctx& c, int32_t* acc, int32_t* committed, int32_t* ncommit, int32_t* fin) {
   {
     Timed t(c, SPEC_KERNEL_OTHER, 0);
@@ -2012,6 +2074,7 @@ hipError_t launch_commit(Ctx& c, int32_t* acc, int32_t* committed, int32_t* ncom
                           kCondSplits, c.M, c.R, c.tgt.d.hidden, c.feat, c.cap);
     CK(hipGetLastError());
   }
+  if (c.cross) CK(launch_ctx_kv(c));
   return hipSuccess;
 }
 

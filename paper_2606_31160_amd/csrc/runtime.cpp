@@ -28,7 +28,7 @@ thread_local std::string g_init_error;
 
 constexpr size_t kAlign = 256;
 constexpr int32_t kKnownFlags = SPEC_FLAG_NO_GRAPHS | SPEC_FLAG_ROWMAJOR | SPEC_FLAG_BLOCK_DRAFT | SPEC_FLAG_COND |
-                                SPEC_FLAG_DRAFT_MROPE | SPEC_FLAG_FULL_DRAFT_ROWS;
+                                SPEC_FLAG_DRAFT_MROPE | SPEC_FLAG_FULL_DRAFT_ROWS | SPEC_FLAG_COND_CROSS;
 
 size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 
@@ -121,6 +121,16 @@ bool check_config(const spec_config* cfg, const spec_seq_init* seqs, bool has_dr
         err = "cond_layers out of range";
         return false;
       }
+  }
+  if (cfg->flags & SPEC_FLAG_COND_CROSS) {
+    if (!(cfg->flags & SPEC_FLAG_COND)) {
+      err = "SPEC_FLAG_COND_CROSS needs SPEC_FLAG_COND";
+      return false;
+    }
+    if (cfg->flags & SPEC_FLAG_BLOCK_DRAFT) {
+      err = "SPEC_FLAG_COND_CROSS does not combine with SPEC_FLAG_BLOCK_DRAFT";
+      return false;
+    }
   }
   if (cfg->flags & SPEC_FLAG_BLOCK_DRAFT) {
     if (!has_draft || cfg->K < 1) {
@@ -373,6 +383,7 @@ size_t carve(Ctx& c, const spec_config* cfg, const spec_seq_init* seqs, bool has
   c.block_draft = has_draft && (cfg->flags & SPEC_FLAG_BLOCK_DRAFT) != 0;
   c.mask_token = cfg->mask_token;
   c.cond = has_draft && (cfg->flags & SPEC_FLAG_COND) != 0;
+  c.cross = c.cond && (cfg->flags & SPEC_FLAG_COND_CROSS) != 0;
   for (int i = 0; i < 3; ++i) c.cond_layers[i] = cfg->cond_layers[i];
   c.gemm_rows = gemm_rows_for(cfg, has_draft, L.M);
   set_splits(c.tgt, L.M, c.gemm_rows);
@@ -431,6 +442,10 @@ size_t carve(Ctx& c, const spec_config* cfg, const spec_seq_init* seqs, bool has
     c.drf.kv_layer = (size_t)L.pool * cfg->draft.kv_heads * kAttnChunk * D;
     c.drf.kc = cv.take<bf16_t>(c.drf.kv_layer * cfg->draft.layers);
     c.drf.vt = cv.take<bf16_t>(c.drf.kv_layer * cfg->draft.layers);
+    if (c.cross) {
+      c.junk_kc = cv.take<bf16_t>(c.drf.kv_layer);
+      c.junk_vt = cv.take<bf16_t>(c.drf.kv_layer);
+    }
   }
   // packed-weight path: passes of at most 32 rows on the layered path
   c.sg = false;
@@ -789,7 +804,8 @@ spec_status spec_init(const spec_config* cfg, const void* embed, const spec_mode
   if (!check_weights(target, cfg->target, err, "target") ||
       (has_draft && !check_weights(draft, cfg->draft, err, "draft")) ||
       ((cfg->flags & SPEC_FLAG_COND) && has_draft &&
-       (!draft->w_fuse || !draft->w_in || !aligned16(draft->w_fuse) || !aligned16(draft->w_in)) &&
+       (!draft->w_fuse || !aligned16(draft->w_fuse) ||
+        (!(cfg->flags & SPEC_FLAG_COND_CROSS) && (!draft->w_in || !aligned16(draft->w_in)))) &&
        (err = "SPEC_FLAG_COND: draft w_fuse / w_in null or misaligned", true))) {
     g_init_error = err;
     return SPEC_E_INVAL;

@@ -30,12 +30,14 @@ class Session:
                     page pool is handed over as the sequences' page tables
     pending_tokens  None: the workload's first pending token per sequence;
                     else one token id per sequence
+    cond_cross      with cond_layers: the features are the draft's layer-0
+                    cross-attention context (SPEC_FLAG_COND_CROSS)
     """
 
     def __init__(self, w, source: str = "host", flags: int = 0, with_draft: bool = True,
                  K: Optional[int] = None, max_new_tokens: Optional[int] = None, stop_token: Optional[int] = None,
                  provider=None, page_seed: Optional[int] = None, mask_token: Optional[int] = None,
-                 cond_layers=None, pending_tokens=None):
+                 cond_layers=None, pending_tokens=None, cond_cross: bool = False):
         torch = _require_gpu()
         import workloads as W
         self.torch = torch
@@ -70,13 +72,14 @@ class Session:
         cfg.flags = flags
         cfg.mask_token = w.vocab - 1 if mask_token is None else mask_token   # block proposal's MASK input
         if cond_layers is not None:   # the draft conditioned on these target layers' hidden states
-            cfg.flags |= B.SPEC_FLAG_COND
+            cfg.flags |= B.SPEC_FLAG_COND | (B.SPEC_FLAG_COND_CROSS if cond_cross else 0)
             for i in range(3):
                 cfg.cond_layers[i] = int(cond_layers[i])
             self.w_fuse = self._tensor("draft", -1, "w_fuse")
-            self.w_in = self._tensor("draft", -1, "w_in")
             self.drf_struct.w_fuse = self.w_fuse.data_ptr()
-            self.drf_struct.w_in = self.w_in.data_ptr()
+            if not cond_cross:        # the cross-attention form has no input projection
+                self.w_in = self._tensor("draft", -1, "w_in")
+                self.drf_struct.w_in = self.w_in.data_ptr()
         self.cfg = cfg
 
         seqs = (B.spec_seq_init * self.B)()

@@ -116,6 +116,9 @@ def test_benchmark_and_paper_configs_validate_on_host(name):
     (lambda c, s: setattr(c, "flags", 2), "unknown bits in flags"),
     (lambda c, s: setattr(c, "flags", 4 | B.SPEC_FLAG_ROWMAJOR), "unknown bits in flags"),
     (lambda c, s: (setattr(c, "flags", B.SPEC_FLAG_BLOCK_DRAFT), setattr(c, "K", 0)), "BLOCK_DRAFT"),
+    (lambda c, s: setattr(c, "flags", B.SPEC_FLAG_COND_CROSS), "needs SPEC_FLAG_COND"),
+    (lambda c, s: setattr(c, "flags", B.SPEC_FLAG_COND | B.SPEC_FLAG_COND_CROSS | B.SPEC_FLAG_BLOCK_DRAFT),
+     "does not combine with SPEC_FLAG_BLOCK_DRAFT"),
 ])
 def test_invalid_config_rejected_on_host(mutate, needle):
     w = W.get("C1")

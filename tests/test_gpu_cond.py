@@ -11,6 +11,9 @@ at slot t takes the input e + W_in [e; f(t-1)].
   * the speculative loop with a conditioned draft commits exactly greedy
     decoding;
   * a 3-layer tiny target capturing three distinct layers (0, 1, 2);
+  * the cross-attention form (SPEC_FLAG_COND_CROSS, Sec. 4.1): proposals,
+    features and the draft's layer-0 context K/V against the oracle on both
+    paths and at 7B width, greedy equivalence;
   * one target layer at 7B width with the 2-layer draft: features and
     proposals against the oracle.
 """
@@ -41,9 +44,11 @@ def c1():
     return w, hp, T, D, trace
 
 
-def _rounds(w, s, seq, trace, block, rounds=2):
+def _rounds(w, s, seq, trace, block, rounds=2, cross=False):
     """Drive GPU and oracle through the same rounds (greedy drafts, so that
-    proposals get accepted); check proposals and features."""
+    proposals get accepted); check proposals and features (and, for the
+    cross-attention form, the draft's layer-0 context K/V of the verified
+    slots)."""
     P = w.seqs[0].prefix_len
     same_history = True   # proposals are compared while both sides' draft histories agree
     for _ in range(rounds):
@@ -76,6 +81,11 @@ def _rounds(w, s, seq, trace, block, rounds=2):
         ref = np.stack([seq.feat[t] for t in range(P, n)])
         for r in range(n - P):
             assert S.normwise_err(got[r], ref[r]) <= S.LOGIT_RTOL, r
+        if cross:
+            for which, ref_c in ((0, seq.dc.k[0]), (1, seq.dc.v[0])):
+                ctx = ON.decode(s.kv(0, 1, 0, which, P, n - P))
+                for r in range(n - P):
+                    assert S.normwise_err(ctx[r], ref_c[P + r]) <= S.LOGIT_RTOL, (which, r)
 
 
 @pytest.mark.parametrize("block", [False, True])
@@ -106,6 +116,43 @@ def test_conditioned_draft_three_distinct_target_layers():
     s.close()
 
 
+@pytest.mark.parametrize("path", ["packed", "rowmajor"])
+def test_cross_attention_conditioned_draft_against_oracle(c1, path):
+    # Sec. 4.1's form: the fused features are the draft's layer-0
+    # cross-attention context; proposals, features and the context K/V of
+    # every verified slot against the oracle over three rounds
+    w, hp, T, D, trace = c1
+    s = _session(w, provider=hp, flags=S.PATH_FLAGS[path], cond_layers=LAYERS_TINY, cond_cross=True)
+    seq = S.oracle_sequence(w, 0, T, D, cond=S.conditioning(w, hp, LAYERS_TINY, cross=True))
+    _rounds(w, s, seq, trace, block=False, rounds=3, cross=True)
+    s.close()
+
+
+def test_cross_attention_spec_loop_equals_greedy(c1):
+    w, hp = c1[:2]
+    s = _session(w, provider=hp, cond_layers=LAYERS_TINY, cond_cross=True)
+    out = []
+    while True:
+        s.draft_steps(w.K)
+        s.verify(None)
+        s.commit()
+        coms, acc, fin = s.committed()
+        out += [int(t) for t in coms[0]]
+        if fin[0]:
+            break
+    s.close()
+    ar = _session(w, provider=hp, K=0, with_draft=False)
+    ref = []
+    while True:
+        ar.verify(None)
+        ar.commit()
+        coms, acc, fin = ar.committed()
+        ref += [int(t) for t in coms[0]]
+        if fin[0]:
+            break
+    assert out == ref and len(out) == w.max_new_tokens
+
+
 def test_conditioned_spec_loop_equals_greedy(c1):
     w, hp = c1[:2]
     s = _session(w, provider=hp, cond_layers=LAYERS_TINY)
@@ -129,6 +176,17 @@ def test_conditioned_spec_loop_equals_greedy(c1):
         if fin[0]:
             break
     assert out == ref and len(out) == w.max_new_tokens
+
+
+def test_cross_attention_conditioned_draft_7b_width():
+    w = W.get("C2")
+    src = W.DeviceWeights(w)
+    T, D = S.oracle_decoders(w, src, cache_weights=True)
+    trace = OS.greedy_trace(S.oracle_sequence(w, 0, T, None, kv=S.device_kv, with_draft=False), 2 * w.K + 4)
+    s = _session(w, source="device", provider=src, cond_layers=(0, 0, 0), cond_cross=True)
+    seq = S.oracle_sequence(w, 0, T, D, kv=S.device_kv, cond=S.conditioning(w, src, (0, 0, 0), cross=True))
+    _rounds(w, s, seq, trace, block=False, rounds=2, cross=True)
+    s.close()
 
 
 def test_conditioned_draft_7b_width():

@@ -14,6 +14,8 @@ on each mass and on the entropy; the three masses sum to 1 within 1e-5.
   * the draft's readout with FlatRoPE and with M-RoPE (SPEC_FLAG_DRAFT_MROPE),
     each against the oracle draft of that rotary, and the M-RoPE draft's
     speculative output still equals greedy decoding;
+  * the draft's layer-0 cross-attention (SPEC_FLAG_COND_CROSS), the layer the
+    paper's table reads, with FlatRoPE and with M-RoPE;
   * 7B-class width, one layer over the 3328-token two-frame prompt;
   * the paper backbone width (32 heads, interleaved M-RoPE), 17 verify rows.
 """
@@ -151,6 +153,38 @@ def test_draft_readout_flatrope_and_mrope(c1, rotary):
     assert np.all(np.isnan(got[1:]))
     _check(got[:1], D.readout)
     S.check_argmax_rows([tok], z[None, :])
+
+
+@pytest.mark.parametrize("rotary", [OM.ROTARY_FLAT, OM.ROTARY_MROPE])
+def test_draft_cross_attention_readout(c1, rotary):
+    # Table attn-budget reads the draft's layer-0 cross-attention: with
+    # SPEC_FLAG_COND_CROSS that layer attends to the target-state context
+    # (prompt slots and the slots a verify committed).  One verify with two
+    # accepted drafts, then the readout of the next draft step's rows.
+    from paper_2606_31160_amd import binding as B
+    w, hp = c1
+    layers = (0, 1, 1)
+    flags = B.SPEC_FLAG_DRAFT_MROPE if rotary == OM.ROTARY_MROPE else 0
+    T, D = S.oracle_decoders(w, hp, mirror=True, draft_rotary=rotary)
+    trace = OS.greedy_trace(S.oracle_sequence(w, 0, T, None, with_draft=False), 4)
+    drafts = np.array([trace[0], trace[1], (trace[2] + 1) % w.vocab, 0], dtype=np.int32)
+    s = _session(w, provider=hp, flags=flags, cond_layers=layers, cond_cross=True)
+    s.verify(drafts[None, :])
+    s.commit()
+    coms = s.committed()[0][0]
+    out = s.attn_readout(1, 0)
+    s.draft_step()
+    got = out[0].cpu().numpy()
+    s.close()
+    seq = S.oracle_sequence(w, 0, T, D, cond=S.conditioning(w, hp, layers, mirror=True, cross=True))
+    res = seq.verify(drafts)
+    assert list(coms) == list(res.committed) and res.accept_len == 2
+    D.readout_layer = 0
+    D.readout_classes = OB.slot_classes(w.seqs[0].prefix_len, _blocks(w), seq.cap)
+    seq.draft_step()
+    n = D.readout.shape[0]                      # the catch-up rows of the step
+    assert n >= 1 and np.all(np.isnan(got[n:]))
+    _check(got[:n], D.readout)
 
 
 def test_mrope_draft_keeps_greedy_output(c1):
