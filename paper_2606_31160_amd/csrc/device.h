@@ -71,6 +71,12 @@ __device__ __forceinline__ void st_coh2(float* p, float x, float y) {
   __hip_atomic_store((SD_GLOBAL uint64_t*)(p), (uint64_t)__float_as_uint(x) | ((uint64_t)__float_as_uint(y) << 32),
                      __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
+__device__ __forceinline__ void st_coh_u32(void* p, uint32_t v) {
+  __hip_atomic_store((SD_GLOBAL uint32_t*)(p), v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ uint32_t ld_coh_u32(const void* p) {
+  return __hip_atomic_load((const SD_GLOBAL uint32_t*)(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
 // Waits until every vector memory access of the wave has completed.
 __device__ __forceinline__ void wait_vmem() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
 

@@ -1988,12 +1988,21 @@ hipError_t launch_forward(Ctx& c, PassMode mode) {
   if (mode == PASS_CATCHUP) return hipSuccess;   // consumes tokens only: no LM head
   // LM head (+ 1/rms of the final norm) with the fused per-tile argmax; the
   // draft proposes from each sequence's last row only (stored as row b)
+  bool reduced = false;   // the LM head's last workgroup already reduced the rows (fused tail)
   if (c.sg) {
     const int rows = draft ? c.B : M;
     const double bytes = gemv_bytes(c.V, d.hidden, rows, 0.0) + 8.0 * (c.V / kTile) * rows;
     Timed t(c, SPEC_KERNEL_LMHEAD, bytes);
     const size_t hi = (size_t)d.layers * 4;
-    CK(sg_launch(SG_ARGMAX, sg_job(c, block ? m.sg_block[1] : m.sg_host[hi]), S(c), t.e0, t.e1));
+    SgJob h = sg_job(c, block ? m.sg_block[1] : m.sg_host[hi]);
+    if (h.S == 1) {
+      h.tail = draft ? 2 : 1;
+      h.tail_K = c.K;
+      h.tail_out = draft ? c.draft_out : nullptr;
+      h.tail_cnt = c.sg_cnt + c.sg_units;
+      reduced = true;
+    }
+    CK(sg_launch(SG_ARGMAX, h, S(c), t.e0, t.e1));
   } else {
     GemvArgs g = gemv_base(c, draft ? c.B : M, draft ? 1 : c.R);
     g.w[0] = c.embed;
@@ -2020,7 +2029,7 @@ hipError_t launch_forward(Ctx& c, PassMode mode) {
   // (max, index) entries per row the LM head left: one per tile, or one per
   // workgroup on the packed path
   const int ntiles = c.sg ? (block ? m.sg_block[1] : m.sg_host[(size_t)d.layers * 4]).amax_n : c.V / kTile;
-  {
+  if (!reduced) {
     Timed t(c, SPEC_KERNEL_OTHER, 0);
     AmaxArgs p{c.st, c.amax_v, c.amax_i, ntiles, c.Mpad, draft ? 1 : c.R, draft ? 1 : 0, draft ? c.draft_out : nullptr, c.K};
     hipExtLaunchKernelGGL(k_argmax_rows, dim3(draft ? 1 : c.R, c.B), dim3(1024), 0, c.stream, t.e0, t.e1, 0, p);

@@ -478,7 +478,7 @@ size_t carve(Ctx& c, const spec_config* cfg, const spec_seq_init* seqs, bool has
     c.sg_part_floats = pf;
     c.sg_units = units;
     c.sg_part = cv.take<float>(pf);
-    c.sg_cnt = cv.take<unsigned>((size_t)units);
+    c.sg_cnt = cv.take<unsigned>((size_t)units + 1);   // + the LM head's fused-argmax counter
   }
   if (sg_ok || c.gemm_pk) {
     c.sg = sg_ok;
@@ -690,7 +690,7 @@ ScratchPlan scratch_plan(const Ctx& c) {
   p.rp = take(c.attn_rows * 4 * sizeof(float));
   p.part = take(c.part_elems * sizeof(float));
   p.sg_part = take(c.sg ? c.sg_part_floats * sizeof(float) : 0);
-  p.cnt_bytes = c.sg ? align_up((size_t)c.sg_units * sizeof(unsigned), 16) : 0;
+  p.cnt_bytes = c.sg ? align_up((size_t)(c.sg_units + 1) * sizeof(unsigned), 16) : 0;
   p.sg_cnt = take(p.cnt_bytes);
   p.amax_v = take(amax * sizeof(float));
   p.amax_i = take(amax * sizeof(int32_t));

@@ -81,6 +81,15 @@ struct SgJob {
   int amax_n;
   bf16_t* logits;         // [M][ntiles*16]
   int allow_logits;
+  // SG_ARGMAX without k-slices: the workgroup that finishes last reduces the
+  // per-workgroup pairs of every row to its argmax (no separate launch).
+  // tail 1: r* of each row (verify and block passes); 2: a draft step's
+  // proposal, recorded in the sequence state and the caller's [B][tail_K]
+  // array tail_out; 0: pairs only
+  int tail;
+  int tail_K;
+  int32_t* tail_out;
+  unsigned* tail_cnt;     // arrival counter, zero between launches
 };
 
 // Fills the geometry of a job (S, G, kmax, units) for ncu compute units;

@@ -476,8 +476,15 @@ __global__ __launch_bounds__(kSgWaves * 64) void k_sgemv(const SgJob j) {
         for (int rb = 0; rb < MB; ++rb) {
           const int m = lane + 16 * rb;
           if (m < M) {
-            j.amax_v[(size_t)gi * j.mpad + m] = ri[rb].best;
-            j.amax_i[(size_t)gi * j.mpad + m] = ri[rb].bi;
+            float* pv = j.amax_v + (size_t)gi * j.mpad + m;
+            int32_t* pi = j.amax_i + (size_t)gi * j.mpad + m;
+            if (j.tail) {   // read by the last workgroup, possibly on another XCD
+              st_coh_u32(pv, __float_as_uint(ri[rb].best));
+              st_coh_u32(pi, (uint32_t)ri[rb].bi);
+            } else {
+              *pv = ri[rb].best;
+              *pi = ri[rb].bi;
+            }
             if (ri[rb].nan) atomicOr(const_cast<int32_t*>(&j.st[ri[rb].b].err), ERR_NUMERIC);
           }
         }
@@ -543,6 +550,53 @@ __global__ __launch_bounds__(kSgWaves * 64) void k_sgemv(const SgJob j) {
         epilogue<EPI>(j, ri[rb], rb, u, sa, sb, pa, pb);
       }
       if (lane == 0) __hip_atomic_store(j.cnt + u, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
+  }
+
+  if constexpr (EPI == SG_ARGMAX) {
+    if (S == 1 && j.tail) {
+      // The pairs of this workgroup are stored (coherently, awaited); the
+      // workgroup that arrives last reduces every row over all G pairs.
+      if (wave == 0) {
+        wait_vmem();
+        if (lane == 0) {
+          const unsigned t = __hip_atomic_fetch_add(j.tail_cnt, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+          pend[kSgPendMax + 1] = t + 1 == (unsigned)G ? 1 : 0;
+        }
+      }
+      __syncthreads();
+      if (pend[kSgPendMax + 1]) {
+        for (int m = wave; m < M; m += kSgWaves) {   // one row per wave
+          float best = -INFINITY;
+          int bi = 0x7fffffff;
+          for (int g = lane; g < G; g += 64)
+            amax_merge(best, bi, __uint_as_float(ld_coh_u32(j.amax_v + (size_t)g * j.mpad + m)),
+                       (int)ld_coh_u32(j.amax_i + (size_t)g * j.mpad + m));
+#pragma unroll
+          for (int o = 32; o > 0; o >>= 1) {
+            const float v2 = __shfl_xor(best, o);
+            const int i2 = __shfl_xor(bi, o);
+            amax_merge(best, bi, v2, i2);
+          }
+          if (lane == 0) {
+            SeqState& s = const_cast<SeqState*>(j.st)[m / j.rps];
+            const int jr = m % j.rps;
+            if (j.tail == 1) {
+              if (jr < s.count) s.rstar[jr] = bi;
+            } else if (s.count == 0) {   // a draft step that proposed nothing for this sequence
+              if (j.tail_out && s.dcall < j.tail_K) j.tail_out[(m / j.rps) * j.tail_K + s.dcall] = -1;
+              s.dcall += 1;
+            } else {
+              s.props[s.dstep] = bi;
+              s.draft_len = s.base + s.count;
+              s.dstep += 1;
+              if (j.tail_out && s.dcall < j.tail_K) j.tail_out[(m / j.rps) * j.tail_K + s.dcall] = bi;
+              s.dcall += 1;
+            }
+          }
+        }
+        if (threadIdx.x == 0) __hip_atomic_store(j.tail_cnt, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      }
     }
   }
 }
