@@ -197,27 +197,7 @@ def c3_oracle():
     T, _ = S.oracle_decoders(w, src, cache_weights=big)
     rng = np.random.default_rng(41)
     drafts = rng.integers(0, w.vocab, size=w.K).astype(np.int32)
-
-    def verify(pend, mirror):
-        T.mirror = mirror
-        try:
-            seq = S.oracle_sequence(w, 0, T, None, kv=S.device_kv, with_draft=False, pending=pend)
-            return seq, seq.verify(drafts)
-        finally:
-            T.mirror = False
-
-    for pend in S.pending_candidates(w, 0, n=6):
-        seq, ref = verify(pend, False)
-        _, fmt = verify(pend, True)
-        d_fmt = max(S.normwise_err(fmt.logits[j], ref.logits[j]) for j in range(w.K + 1))
-        tau = max(S.LOGIT_RTOL, 1.5 * d_fmt)
-        mg = S.margin(ref.logits)[0]
-        print(f"pending {pend}: row-0 margin {mg:.4f}, d_fmt {d_fmt:.3e}, tau {tau:.3e}, l = {ref.accept_len}",
-              flush=True)
-        if mg > tau and ref.accept_len == 0:
-            break
-    else:
-        raise AssertionError("no candidate pending token gives a row 0 pinned at tau")
+    pend, ref, seq, tau, _ = S.deep_verify_reference(w, 0, T, drafts, kv=S.device_kv)
     P = w.seqs[0].prefix_len
     kv = {(li, which): c[P:P + w.K + 1].copy() for li in (0, w.target.layers - 1)
           for which, c in ((0, seq.tc.k[li]), (1, seq.tc.v[li]))}

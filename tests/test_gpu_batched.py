@@ -10,6 +10,9 @@ pass run on the batched-row GEMM, with caches in shuffled KV pages.
   * 16 scenes of the 16-scene workload's prompt structure (prompts of
     2048..8192 tokens, four camera grids each) at the 7B-class width through
     one target layer, 144 rows: logits of every sequence against the oracle;
+  * the 16-scene workload at full size (28 layers, the 152064-token head,
+    one 144-row verify): its shortest- and longest-prompt scenes against the
+    oracle;
   * chained draft steps compacted to one row per sequence: the 16-scene loop
     with and without compaction, and bit-equal proposals on the packed path.
 """
@@ -139,6 +142,44 @@ def test_sixteen_scenes_spec_loop(tiny16, rows):
     outs = _loop(s)
     s.close()
     _check_history(w, T, outs)
+
+
+def test_sixteen_scenes_28_layer_verify_sampled_against_oracle():
+    """The 16-scene workload at full size: 28 layers, the 152064-token head,
+    prompts of 2048..8192 tokens in shuffled KV pages, one 144-row verify on
+    the batched GEMM.  The scenes with the shortest and the longest prompt are
+    checked against the plain float64 oracle: logits of their 9 rows within
+    tau (tests/_support.deep_verify_reference), l and the committed token bit
+    for bit (their pending tokens reseeded until row 0 is pinned at tau), and
+    their first and last layers' new K/V rows."""
+    import psutil
+    w = W.get("C5").with_(draft=None)
+    src = W.DeviceWeights(w)
+    T, _ = S.oracle_decoders(w, src, cache_weights=psutil.virtual_memory().available > 150 * 2**30)
+    drafts = np.random.default_rng(47).integers(0, w.vocab, size=(w.batch, w.K)).astype(np.int32)
+    lens = [q.prefix_len for q in w.seqs]
+    sample = sorted({int(np.argmin(lens)), int(np.argmax(lens))})
+    picks = {b: S.deep_verify_reference(w, b, T, drafts[b], kv=S.device_kv, n=4) for b in sample}
+    pend = [picks[b][0] if b in picks else W.first_pending_token(w, b) for b in range(w.batch)]
+    s = _session(w, source="device", provider=src, page_seed=5, pending_tokens=pend)
+    s.verify(drafts, logits=True)
+    s.commit()
+    gl = s.logits.float().cpu().numpy()
+    coms, acc, fin = s.committed()
+    for b in sample:
+        _, ref, seq, tau, _ = picks[b]
+        errs = [S.normwise_err(gl[b, j], ref.logits[j]) for j in range(w.K + 1)]
+        print(f"scene {b} (prompt {lens[b]}): logit error max {max(errs):.3e} (tau {tau:.3e})", flush=True)
+        assert max(errs) <= tau, b
+        assert int(acc[b]) == ref.accept_len == 0
+        assert list(coms[b]) == list(ref.committed)
+        P = w.seqs[b].prefix_len
+        for li in (0, w.target.layers - 1):
+            for which, cache in ((0, seq.tc.k[li]), (1, seq.tc.v[li])):
+                got = ON.decode(s.kv(b, 0, li, which, P, w.K + 1))
+                bar = S.LOGIT_RTOL if li == 0 else tau
+                assert S.normwise_err(got, cache[P:P + w.K + 1]) <= bar, (b, li, which)
+    s.close()
 
 
 def _proposal_rounds(w, flags, rounds=3):

@@ -5,6 +5,9 @@ interleaved M-RoPE axis assignment (Eq. axis-assign), and K = 16 proposals, so
 
   * one backbone layer over the 4096-token prompt, 17 rows, against the oracle
     (position ids, logits, greedy tokens, accept length, new K/V rows);
+  * the full 36-layer verify (17 rows, the 151936-token head) against the
+    oracle: logits within the bf16 format's own distance at that depth, l and
+    the committed token bit for bit, first and last layers' new K/V rows;
   * the full 36-layer target with its 1-layer FlatRoPE draft: speculative
     rounds with K = 16 commit exactly the library's K = 0 greedy decoding.
 """
@@ -54,6 +57,39 @@ def test_paper_backbone_layer_against_oracle():
     for which, ref_c in ((0, seq.tc.k[0]), (1, seq.tc.v[0])):
         got = ON.decode(s.kv(0, 0, 0, which, P, w.K + 1))
         assert S.normwise_err(got, ref_c[P:P + w.K + 1]) <= S.LOGIT_RTOL
+    s.close()
+
+
+def test_paper_backbone_full_36_layer_verify_against_oracle():
+    """The paper's own verification shape at full depth: 36 layers, hidden
+    4096, the 151936-token head, the 4096-token prompt, K = 16 (17 rows on the
+    two-row-block GEMV), against the plain float64 oracle.  Logits of every
+    row within tau (tests/_support.deep_verify_reference: the bf16 format's
+    own distance at this depth, derived here from the oracle), l and the
+    committed token bit for bit on a pending token whose row 0 is pinned at
+    tau, and the first and last layers' new K/V rows."""
+    import psutil
+    w = W.get("C6").with_(draft=None)
+    src = W.DeviceWeights(w)
+    T, _ = S.oracle_decoders(w, src, cache_weights=psutil.virtual_memory().available > 150 * 2**30)
+    drafts = np.random.default_rng(43).integers(0, w.vocab, size=w.K).astype(np.int32)
+    pend, ref, seq, tau, d_fmt = S.deep_verify_reference(w, 0, T, drafts, kv=S.device_kv)
+    s = _session(w, source="device", provider=src, pending_tokens=[pend])
+    s.verify(drafts[None, :], logits=True)
+    s.commit()
+    gl = s.logits[0].float().cpu().numpy()
+    errs = [S.normwise_err(gl[j], ref.logits[j]) for j in range(w.K + 1)]
+    print(f"36 layers, 17 rows: logit error max {max(errs):.3e} (tau {tau:.3e})", flush=True)
+    assert max(errs) <= tau
+    coms, acc, fin = s.committed()
+    assert int(acc[0]) == ref.accept_len == 0
+    assert list(coms[0]) == list(ref.committed)
+    P = w.seqs[0].prefix_len
+    for li in (0, w.target.layers - 1):
+        for which, cache in ((0, seq.tc.k[li]), (1, seq.tc.v[li])):
+            got = ON.decode(s.kv(0, 0, li, which, P, w.K + 1))
+            bar = S.LOGIT_RTOL if li == 0 else tau
+            assert S.normwise_err(got, cache[P:P + w.K + 1]) <= bar, (li, which)
     s.close()
 
 
