@@ -224,6 +224,34 @@ def read_peak_gbs(reps=10, nbytes=1 << 32):
     return gbs
 
 
+def stream_floor_us(sizes_mb=(8, 32, 128), reps=5):
+    """Duration of the library's read-only streaming kernel over buffers of a
+    few sizes, each read cold (a 1 GiB read in between evicts the caches),
+    median of `reps`: the cost of one launch that only reads its bytes, the
+    floor a projection of that size streams against."""
+    import torch
+    from paper_2606_31160_amd import binding as B
+    st = torch.cuda.current_stream().cuda_stream
+    big = torch.empty(1 << 31, dtype=torch.uint8, device="cuda").fill_(1)
+    sink = torch.empty(1024, dtype=torch.int32, device="cuda")
+    out = {}
+    for mb in sizes_mb:
+        n = mb << 20
+        ts = []
+        for _ in range(reps + 1):
+            B.spec_stream_read(big[1 << 30:].data_ptr(), 1 << 30, sink.data_ptr(), 1024, st)
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            B.spec_stream_read(big.data_ptr(), n, sink.data_ptr(), 1024, st)
+            e1.record()
+            torch.cuda.synchronize()
+            ts.append(e0.elapsed_time(e1) * 1e3)
+        out[f"{mb}MB"] = round(float(np.median(ts[1:])), 2)
+    del big, sink
+    torch.cuda.empty_cache()
+    return out
+
+
 def batched_scenes(src, K):
     """The 16-scene workload end to end: 16 independent scenes (prompts of
     2048..8192 tokens, four camera grids each, shuffled KV pages), each
@@ -674,6 +702,7 @@ def main():
         out["paper_backbone_k16"] = paper_backbone()
     rp = read_peak_gbs()
     out["read_peak_gbs"] = round(rp, 1)
+    out["stream_read_cold_us"] = stream_floor_us()
     out["verify_frac_of_read_peak"] = round(v_bytes / (v_us * 1e-6) / 1e9 / rp, 4)
     if not args.no_cpu_baseline:
         log("timing the oracle on a bounded sample ...")
