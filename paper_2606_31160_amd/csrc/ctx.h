@@ -91,6 +91,7 @@ struct Ctx {
   spec_config cfg{};
   int B = 1, K = 0, R = 1, M = 1, Mpad = 16, V = 0, cap = 0;
   int attn_chunk = kAttnChunk, attn_splits = 1;
+  int attn_ppw = 1;                  // pages per attention workgroup (several for many sequences)
   int pps = 1;                       // page-table entries per sequence (cap / kAttnChunk)
   int pool = 0;                      // cache pages per layer
   std::vector<int32_t> pt_host;      // [B][pps] physical page of each sequence page

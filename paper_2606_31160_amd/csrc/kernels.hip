@@ -792,6 +792,7 @@ struct AttnArgs {
   float* rp;             // readout: [splits][B][nq][R][4] class sums and trajectory E term
   int cap;
   int cross;             // cross-attention context: row j sees the slots below min(base + j, seq_len)
+  int ppw;               // k_attn_pages: pages per split (workgroup)
 };
 
 template <int D, bool RO>
@@ -996,6 +997,177 @@ template <int D, bool RO>
 __global__ __launch_bounds__(256) void k_attn(AttnArgs a) {
   extern __shared__ __align__(16) unsigned char lds[];
   attn_partials<D, RO>(a, lds);
+}
+
+// The same split-KV attention with a.ppw consecutive pages per workgroup,
+// for passes over many sequences (there are workgroups enough without one
+// per page, and fewer splits mean fewer partial outputs written and merged).
+// Pages are taken one at a time through the same LDS tile: the next page's
+// keys and values are loaded while this one's scores and products run, and
+// the running (max, sum, output) of each row is rescaled when the max grows.
+// grid (groups of ppw pages, kv heads x row blocks, B), 256 threads.
+template <int D>
+__global__ __launch_bounds__(256) void k_attn_pages(AttnArgs a) {
+  extern __shared__ __align__(16) unsigned char lds[];
+  const int grp = blockIdx.x;
+  const int kvh = blockIdx.y / a.row_blocks, rb = blockIdx.y % a.row_blocks;
+  const int b = blockIdx.z;
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int g4 = lane >> 4;
+  const SeqState& s = a.st[b];
+  const int count = s.count, base = s.base, causal = s.causal, seq_len = s.seq_len;
+  const int rows = count * a.G;
+  const int wrow0 = rb * 64 + wave * 16;
+  const int qr = wrow0 + (lane & 15);
+  const bool rvalid = qr < rows;
+  const int j = rvalid ? qr / a.G : 0;
+  const int hq = kvh * a.G + (rvalid ? qr % a.G : 0);
+  const int kv_end = a.cross ? min(base + count - 1, seq_len) : base + count;
+  const int vis_end = a.cross ? min(base + j, seq_len) : base + (j < causal ? j + 1 : count);
+  const int gk0 = grp * a.ppw * kAttnChunk;
+  const int gk1 = min(gk0 + a.ppw * kAttnChunk, kv_end);
+  const size_t oi = (((size_t)grp * a.B + b) * a.nq + hq) * a.R + j;
+
+  if (gk0 >= gk1) {                                 // no keys in this split (workgroup-uniform)
+    if (wrow0 >= rows) return;
+    if (rvalid && g4 == 0) {
+      a.mp[oi] = -INFINITY;
+      a.lp[oi] = 0.f;
+    }
+    if (rvalid) {
+      bf16_t* op = a.op + oi * D;
+      for (int d = g4 * 4; d < D; d += 16) *reinterpret_cast<u32x2*>(op + d) = u32x2{0u, 0u};
+    }
+    return;
+  }
+  const bool active = wrow0 < rows;                 // wave-uniform; inactive waves still pass the barriers
+  const int np = (gk1 - gk0 + kAttnChunk - 1) / kAttnChunk;
+
+  u32x4 qf[D / 32];
+  {
+    const bf16_t* qp = a.q + ((size_t)(b * a.R + j) * a.nq + hq) * D + 8 * g4;
+#pragma unroll
+    for (int t = 0; t < D / 32; ++t) qf[t] = ld16(qp + 32 * t);
+  }
+  const int kst = D + 8, vst = kAttnChunk + 8;
+  bf16_t* Ks = reinterpret_cast<bf16_t*>(lds);
+  bf16_t* Vs = Ks + (size_t)kAttnChunk * kst;
+  constexpr int PER_T = kAttnChunk * D / 8 / 256;   // 16-byte vectors per thread and operand
+  static_assert(PER_T * 256 * 8 == kAttnChunk * D, "the threads cover the page exactly");
+  constexpr int per_row = kAttnChunk / 8;
+  u32x4 kr[PER_T], vr[PER_T];
+  auto issue = [&](int pi) {   // page pi of the group: loads into registers
+    const int page = a.pt[b * a.pps + grp * a.ppw + pi];
+    const size_t pg = (size_t)page * a.nkv + kvh;
+    const bf16_t* Kb = a.kc + pg * kAttnChunk * D;
+    const bf16_t* Vb = a.vt + pg * D * kAttnChunk;
+#pragma unroll
+    for (int u = 0; u < PER_T; ++u) {
+      const int i = threadIdx.x + 256 * u;
+      kr[u] = ld16(Kb + (size_t)(i / (D / 8)) * D + 8 * (i % (D / 8)));
+      vr[u] = ld16(Vb + (size_t)(i / per_row) * kAttnChunk + 8 * (i % per_row));
+    }
+  };
+  auto stage = [&](int k0, int k1) {   // registers -> LDS; values past the valid keys as zeros
+#pragma unroll
+    for (int u = 0; u < PER_T; ++u) {
+      const int i = threadIdx.x + 256 * u;
+      *reinterpret_cast<u32x4*>(Ks + (size_t)(i / (D / 8)) * kst + 8 * (i % (D / 8))) = kr[u];
+      const int d = i / per_row, v8 = i % per_row;
+      const int slot = k0 + 8 * v8;
+      u32x4 v = vr[u];
+      if (slot >= k1) {
+        v = u32x4{0, 0, 0, 0};
+      } else if (slot + 8 > k1) {
+        uint32_t w[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+        for (int e = 0; e < 8; ++e)
+          if (slot + e >= k1) w[e >> 1] &= (e & 1) ? 0x0000FFFFu : 0xFFFF0000u;
+        v = u32x4{w[0], w[1], w[2], w[3]};
+      }
+      *reinterpret_cast<u32x4*>(Vs + (size_t)d * vst + 8 * v8) = v;
+    }
+  };
+
+  float m_run = -INFINITY, l_run = 0.f;
+  f32x4 o[D / 16];
+#pragma unroll
+  for (int dt = 0; dt < D / 16; ++dt) o[dt] = f32x4{0.f, 0.f, 0.f, 0.f};
+  issue(0);
+  for (int pi = 0; pi < np; ++pi) {   // workgroup-uniform
+    const int k0 = gk0 + pi * kAttnChunk, k1 = min(k0 + kAttnChunk, kv_end);
+    if (pi > 0) __syncthreads();      // every wave has read the previous page
+    stage(k0, k1);
+    __syncthreads();
+    if (pi + 1 < np) issue(pi + 1);   // in flight while this page is used
+    if (!active) continue;
+    f32x4 sc[4];
+#pragma unroll
+    for (int h = 0; h < 4; ++h) {
+      const bf16_t* kp = Ks + (size_t)(16 * h + (lane & 15)) * kst + 8 * g4;
+      f32x4 acc = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int t = 0; t < D / 32; ++t) acc = mfma16x16x32(*reinterpret_cast<const u32x4*>(kp + 32 * t), qf[t], acc);
+      sc[h] = acc;
+    }
+    u32x4 va[2][D / 16];
+#pragma unroll
+    for (int hb = 0; hb < 2; ++hb)
+#pragma unroll
+      for (int dt = 0; dt < D / 16; ++dt) {
+        const bf16_t* vp = Vs + (size_t)(16 * dt + (lane & 15)) * vst + 32 * hb + 4 * g4;
+        const u32x2 lo = *reinterpret_cast<const u32x2*>(vp), hi = *reinterpret_cast<const u32x2*>(vp + 16);
+        va[hb][dt] = u32x4{lo.x, lo.y, hi.x, hi.y};
+      }
+    float p[16];
+    float pm = -INFINITY;
+#pragma unroll
+    for (int h = 0; h < 4; ++h)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int key = k0 + 16 * h + 4 * g4 + i;
+        const bool ok = rvalid && key < k1 && key < vis_end;
+        const float v = ok ? sc[h][i] * a.scale_log2 : -INFINITY;
+        p[h * 4 + i] = v;
+        pm = fmaxf(pm, v);
+      }
+    pm = fmaxf(pm, __shfl_xor(pm, 16));
+    pm = fmaxf(pm, __shfl_xor(pm, 32));
+    const float m_new = fmaxf(m_run, pm);
+    const float alpha = m_run == -INFINITY ? 0.f : exp2f(m_run - m_new);
+    float ls = 0.f;
+#pragma unroll
+    for (int i = 0; i < 16; ++i) {
+      const float v = p[i];
+      p[i] = (v == -INFINITY) ? 0.f : exp2f(v - m_new);
+      ls += p[i];
+    }
+    l_run = l_run * alpha + ls;
+#pragma unroll
+    for (int dt = 0; dt < D / 16; ++dt) o[dt] *= alpha;
+#pragma unroll
+    for (int hb = 0; hb < 2; ++hb) {
+      const float* ph = p + 8 * hb;
+      const u32x4 pb = u32x4{pack2(ph[0], ph[1]), pack2(ph[2], ph[3]), pack2(ph[4], ph[5]), pack2(ph[6], ph[7])};
+#pragma unroll
+      for (int dt = 0; dt < D / 16; ++dt) o[dt] = mfma16x16x32(va[hb][dt], pb, o[dt]);
+    }
+    m_run = m_new;
+  }
+  if (!active) return;
+  l_run += __shfl_xor(l_run, 16);
+  l_run += __shfl_xor(l_run, 32);
+  if (rvalid) {
+    bf16_t* op = a.op + oi * D;
+#pragma unroll
+    for (int dt = 0; dt < D / 16; ++dt)
+      *reinterpret_cast<u32x2*>(op + 16 * dt + 4 * g4) =
+          u32x2{pack2(o[dt].x, o[dt].y), pack2(o[dt].z, o[dt].w)};
+    if (g4 == 0) {
+      a.mp[oi] = m_run;
+      a.lp[oi] = l_run;
+    }
+  }
 }
 
 
@@ -1423,17 +1595,25 @@ hipError_t launch_attention(Ctx& c, Model& m, int li) {
   const int rb = (c.R * G + 63) / 64;
   const bool ro = c.ro_out && c.ro_m == &m && c.ro_layer == li;
   const int cross = (c.cross && &m == &c.drf && li == 0) ? 1 : 0;
+  // several pages per workgroup where the context asks for it (many
+  // sequences); a readout pass keeps one page per workgroup
+  const int ppw = ro ? 1 : c.attn_ppw;
   AttnArgs p{c.st, c.q, kc, vt, c.pt, c.op, c.mp, c.lp, nq, nkv, G, c.R, c.B, c.pps, c.attn_chunk, rb,
-             kLog2e / sqrtf((float)D), c.cls, c.rp, c.cap, cross};
-  dim3 grid(c.attn_splits, nkv * rb, c.B);
-  CombineArgs cb{c.st, c.op, c.mp, c.lp, c.o, nq, D, c.R, c.B, c.attn_chunk, c.rp,
+             kLog2e / sqrtf((float)D), c.cls, c.rp, c.cap, cross, ppw};
+  dim3 grid((c.attn_splits + ppw - 1) / ppw, nkv * rb, c.B);
+  CombineArgs cb{c.st, c.op, c.mp, c.lp, c.o, nq, D, c.R, c.B, c.attn_chunk * ppw, c.rp,
                  ro ? c.ro_out : nullptr, {}, cross};
   for (int b = 0; b < c.B && b < SPEC_MAX_BATCH; ++b) cb.inv_ln[b] = c.ro_inv_ln[b];
   const size_t comb_lds = (size_t)(((c.attn_splits + 3) & ~3) + 8 * D) * sizeof(float);
   const size_t lds = attn_lds_bytes(c.attn_chunk, D);
   {
     Timed t(c, SPEC_KERNEL_ATTN, 0);
-    if (D == 128)
+    if (ppw > 1) {
+      if (D == 128)
+        hipExtLaunchKernelGGL(k_attn_pages<128>, grid, dim3(256), lds, S(c), t.e0, t.e1, 0, p);
+      else
+        hipExtLaunchKernelGGL(k_attn_pages<64>, grid, dim3(256), lds, S(c), t.e0, t.e1, 0, p);
+    } else if (D == 128)
       hipExtLaunchKernelGGL(ro ? k_attn<128, true> : k_attn<128, false>, grid, dim3(256), lds, S(c), t.e0, t.e1, 0, p);
     else
       hipExtLaunchKernelGGL(ro ? k_attn<64, true> : k_attn<64, false>, grid, dim3(256), lds, S(c), t.e0, t.e1, 0, p);
@@ -1654,6 +1834,10 @@ void init_kernel_attributes() {
   for (int i = 0; i < 4; ++i)
     (void)hipFuncSetAttribute(attn[i], hipFuncAttributeMaxDynamicSharedMemorySize,
                               (int)attn_lds_bytes(kAttnChunk, i < 2 ? 128 : 64));
+  (void)hipFuncSetAttribute(reinterpret_cast<const void*>(&k_attn_pages<128>),
+                            hipFuncAttributeMaxDynamicSharedMemorySize, (int)attn_lds_bytes(kAttnChunk, 128));
+  (void)hipFuncSetAttribute(reinterpret_cast<const void*>(&k_attn_pages<64>),
+                            hipFuncAttributeMaxDynamicSharedMemorySize, (int)attn_lds_bytes(kAttnChunk, 64));
   set_lds_limit_p<EPI_STORE, 1>();
   set_lds_limit_p<EPI_STORE, 2>();
   set_lds_limit_p<EPI_STORE, 3>();

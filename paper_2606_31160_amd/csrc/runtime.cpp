@@ -378,6 +378,11 @@ size_t carve(Ctx& c, const spec_config* cfg, const spec_seq_init* seqs, bool has
   c.attn_chunk = L.chunk;
   c.ncu = num_cus();
   c.attn_splits = L.splits;
+  // one page per attention workgroup gives a pass over a few sequences
+  // enough workgroups; from 8 sequences on, four pages per workgroup (the
+  // choice depends on the batch only, so every pass of a context groups the
+  // attention sums the same way)
+  c.attn_ppw = L.B >= 8 ? 4 : 1;
   c.tgt.d = cfg->target;
   c.tgt.flat = false;
   c.block_draft = has_draft && (cfg->flags & SPEC_FLAG_BLOCK_DRAFT) != 0;
