@@ -795,8 +795,9 @@ struct AttnArgs {
   int ppw;               // k_attn_pages: pages per split (workgroup)
 };
 
-template <int D, bool RO>
+template <int D, bool RO, int NW>
 __device__ __forceinline__ void attn_partials(const AttnArgs& a, unsigned char* lds) {
+  constexpr int NT = NW * 64;   // threads: NW waves of 16 query rows each
   const int split = blockIdx.x;
   const int kvh = blockIdx.y / a.row_blocks, rb = blockIdx.y % a.row_blocks;
   const int b = blockIdx.z;
@@ -810,7 +811,7 @@ __device__ __forceinline__ void attn_partials(const AttnArgs& a, unsigned char* 
   const int count = s.count, base = s.base, causal = s.causal, seq_len = s.seq_len;
   asm volatile("" ::"s"(page), "s"(count), "s"(base), "s"(causal), "s"(seq_len));   // all loads issued before any is awaited
   const int rows = count * a.G;
-  const int wrow0 = rb * 64 + wave * 16;
+  const int wrow0 = rb * (16 * NW) + wave * 16;
   const int qr = wrow0 + (lane & 15);
   const bool rvalid = qr < rows;
   const int j = rvalid ? qr / a.G : 0;
@@ -867,8 +868,8 @@ __device__ __forceinline__ void attn_partials(const AttnArgs& a, unsigned char* 
   bf16_t* Ks = reinterpret_cast<bf16_t*>(lds);
   bf16_t* Vs = Ks + (size_t)a.chunk * kst;
   {
-    constexpr int PER_T = kAttnChunk * D / 8 / 256;   // 16-byte vectors per thread and operand
-    static_assert(PER_T * 256 * 8 == kAttnChunk * D, "the threads cover the page exactly");
+    constexpr int PER_T = kAttnChunk * D / 8 / NT;    // 16-byte vectors per thread and operand
+    static_assert(PER_T * NT * 8 == kAttnChunk * D, "the threads cover the page exactly");
     const size_t pg = (size_t)page * a.nkv + kvh;
     const bf16_t* Kb = a.kc + pg * kAttnChunk * D;
     const bf16_t* Vb = a.vt + pg * D * kAttnChunk;
@@ -876,7 +877,7 @@ __device__ __forceinline__ void attn_partials(const AttnArgs& a, unsigned char* 
     u32x4 kr[PER_T], vr[PER_T];
 #pragma unroll
     for (int u = 0; u < PER_T; ++u) {
-      const int i = threadIdx.x + 256 * u;
+      const int i = threadIdx.x + NT * u;
       const int key = i / (D / 8), c8 = i % (D / 8);
       kr[u] = ld16(Kb + (size_t)key * D + 8 * c8);
       const int d = i / per_row, v8 = i % per_row;
@@ -884,7 +885,7 @@ __device__ __forceinline__ void attn_partials(const AttnArgs& a, unsigned char* 
     }
 #pragma unroll
     for (int u = 0; u < PER_T; ++u) {
-      const int i = threadIdx.x + 256 * u;
+      const int i = threadIdx.x + NT * u;
       const int key = i / (D / 8), c8 = i % (D / 8);
       *reinterpret_cast<u32x4*>(Ks + (size_t)key * kst + 8 * c8) = kr[u];
       const int d = i / per_row, v8 = i % per_row;
@@ -993,10 +994,10 @@ __device__ __forceinline__ void attn_partials(const AttnArgs& a, unsigned char* 
   }
 }
 
-template <int D, bool RO>
-__global__ __launch_bounds__(256) void k_attn(AttnArgs a) {
+template <int D, bool RO, int NW>
+__global__ __launch_bounds__(NW * 64) void k_attn(AttnArgs a) {
   extern __shared__ __align__(16) unsigned char lds[];
-  attn_partials<D, RO>(a, lds);
+  attn_partials<D, RO, NW>(a, lds);
 }
 
 // The same split-KV attention with a.ppw consecutive pages per workgroup,
@@ -1592,12 +1593,16 @@ hipError_t launch_attention(Ctx& c, Model& m, int li) {
   bf16_t* kc = m.kc + m.kv_layer * li;
   bf16_t* vt = m.vt + m.kv_layer * li;
   const int G = nq / nkv;
-  const int rb = (c.R * G + 63) / 64;
   const bool ro = c.ro_out && c.ro_m == &m && c.ro_layer == li;
   const int cross = (c.cross && &m == &c.drf && li == 0) ? 1 : 0;
   // several pages per workgroup where the context asks for it (many
   // sequences); a readout pass keeps one page per workgroup
   const int ppw = ro ? 1 : c.attn_ppw;
+  // query rows of one kv head (rows per sequence x q heads per kv head): up
+  // to 64 in one workgroup of 4 waves; more (e.g. 17 rows x 4 heads) in
+  // workgroups of 8 waves, so that each page is staged once for all of them
+  const int nw = (ppw == 1 && c.R * G > 64) ? 8 : 4;
+  const int rb = (c.R * G + 16 * nw - 1) / (16 * nw);
   AttnArgs p{c.st, c.q, kc, vt, c.pt, c.op, c.mp, c.lp, nq, nkv, G, c.R, c.B, c.pps, c.attn_chunk, rb,
              kLog2e / sqrtf((float)D), c.cls, c.rp, c.cap, cross, ppw};
   dim3 grid((c.attn_splits + ppw - 1) / ppw, nkv * rb, c.B);
@@ -1613,10 +1618,18 @@ hipError_t launch_attention(Ctx& c, Model& m, int li) {
         hipExtLaunchKernelGGL(k_attn_pages<128>, grid, dim3(256), lds, S(c), t.e0, t.e1, 0, p);
       else
         hipExtLaunchKernelGGL(k_attn_pages<64>, grid, dim3(256), lds, S(c), t.e0, t.e1, 0, p);
+    } else if (nw == 8) {
+      if (D == 128)
+        hipExtLaunchKernelGGL(ro ? k_attn<128, true, 8> : k_attn<128, false, 8>, grid, dim3(512), lds, S(c), t.e0, t.e1,
+                              0, p);
+      else
+        hipExtLaunchKernelGGL(ro ? k_attn<64, true, 8> : k_attn<64, false, 8>, grid, dim3(512), lds, S(c), t.e0, t.e1, 0,
+                              p);
     } else if (D == 128)
-      hipExtLaunchKernelGGL(ro ? k_attn<128, true> : k_attn<128, false>, grid, dim3(256), lds, S(c), t.e0, t.e1, 0, p);
+      hipExtLaunchKernelGGL(ro ? k_attn<128, true, 4> : k_attn<128, false, 4>, grid, dim3(256), lds, S(c), t.e0, t.e1, 0,
+                            p);
     else
-      hipExtLaunchKernelGGL(ro ? k_attn<64, true> : k_attn<64, false>, grid, dim3(256), lds, S(c), t.e0, t.e1, 0, p);
+      hipExtLaunchKernelGGL(ro ? k_attn<64, true, 4> : k_attn<64, false, 4>, grid, dim3(256), lds, S(c), t.e0, t.e1, 0, p);
     CK(hipGetLastError());
   }
   Timed t2(c, SPEC_KERNEL_OTHER, 0);
@@ -1829,11 +1842,14 @@ void init_kernel_attributes() {
   done = true;
   sg_set_attributes(gemv_lds_limit());
   gemm_set_attributes(gemv_lds_limit());
-  const void* attn[4] = {reinterpret_cast<const void*>(&k_attn<128, false>), reinterpret_cast<const void*>(&k_attn<128, true>),
-                         reinterpret_cast<const void*>(&k_attn<64, false>), reinterpret_cast<const void*>(&k_attn<64, true>)};
-  for (int i = 0; i < 4; ++i)
+  const void* attn[8] = {
+      reinterpret_cast<const void*>(&k_attn<128, false, 4>), reinterpret_cast<const void*>(&k_attn<128, true, 4>),
+      reinterpret_cast<const void*>(&k_attn<128, false, 8>), reinterpret_cast<const void*>(&k_attn<128, true, 8>),
+      reinterpret_cast<const void*>(&k_attn<64, false, 4>),  reinterpret_cast<const void*>(&k_attn<64, true, 4>),
+      reinterpret_cast<const void*>(&k_attn<64, false, 8>),  reinterpret_cast<const void*>(&k_attn<64, true, 8>)};
+  for (int i = 0; i < 8; ++i)
     (void)hipFuncSetAttribute(attn[i], hipFuncAttributeMaxDynamicSharedMemorySize,
-                              (int)attn_lds_bytes(kAttnChunk, i < 2 ? 128 : 64));
+                              (int)attn_lds_bytes(kAttnChunk, i < 4 ? 128 : 64));
   (void)hipFuncSetAttribute(reinterpret_cast<const void*>(&k_attn_pages<128>),
                             hipFuncAttributeMaxDynamicSharedMemorySize, (int)attn_lds_bytes(kAttnChunk, 128));
   (void)hipFuncSetAttribute(reinterpret_cast<const void*>(&k_attn_pages<64>),
