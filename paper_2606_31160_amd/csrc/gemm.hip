@@ -38,6 +38,7 @@
 #include "ctx.h"
 #include "device.h"
 #include "gemv.h"
+#include "sgemv.h"
 
 namespace specdec {
 
@@ -481,13 +482,16 @@ hipError_t gemm_launch(int epi, const GemvArgs& g, hipStream_t s, hipEvent_t e0,
   }
 }
 
-// k-splits of the down projection over M > kThinRows rows: enough
-// workgroups to cover every CU once, at least two chunks per split.
+// k-splits of the down projection over M > kThinRows rows: as many as fit
+// the resident workgroup slots in one round (a count that overflows them
+// leaves a second round for the few workgroups left over, which doubles the
+// projection's time: 56 groups x 5 splits = 280 workgroups on 256 slots),
+// at least 8 k-steps per split.
 int gemm_down_splits(int N, int Kd, int ncu) {
   const int groups = (N + kGemmTiles * kTile - 1) / (kGemmTiles * kTile);
   const int T = (Kd + 31) / 32;
-  int s = std::max(1, (ncu + groups - 1) / groups);
-  return std::max(1, std::min(s, T / 8));   // at least 8 k-steps per split
+  int s = std::max(1, ncu / groups);
+  return std::max(1, std::min(s, T / 8));
 }
 
 int gemm_wgs_per_cu(int M) {
@@ -517,8 +521,13 @@ int gemm_qkv_splits(int N, int Kd, int M, int ncu) {
   // one workgroup per CU: measured faster here than filling both slots, as
   // the doubled partials outweigh the extra streams
   const int s = gemm_down_splits(N, Kd, ncu);
-  // 2 * s * M * N fp32 partial bytes <= (N * Kd bf16 weight bytes) / 10
-  return (long long)40 * s * M <= Kd ? s : 1;
+  // Passes of more than 32 rows always split: such a GEMM is far from
+  // streaming its weights at full rate (the time goes into each workgroup's
+  // MFMA and x-operand work), so spreading it over s times the workgroups
+  // pays for the partials (144 rows: 72 workgroups -> 3 x 72).  Fewer rows
+  // split only while 2 * s * M * N fp32 partial bytes <= (N * Kd bf16 weight
+  // bytes) / 10.
+  return (M > kSgMaxRows || (long long)40 * s * M <= Kd) ? s : 1;
 }
 
 }  // namespace specdec
