@@ -18,15 +18,15 @@ constexpr float kLog2e = 1.4426950408889634f;
 
 __device__ __forceinline__ float bf2f(bf16_t h) { return __uint_as_float(((uint32_t)h) << 16); }
 
-// float -> bfloat16, round to nearest even; NaN stays NaN.
-__device__ __forceinline__ uint32_t f2bf_bits(float f) {
-  uint32_t u = __float_as_uint(f);
-  if ((u & 0x7fffffffu) > 0x7f800000u) return (u >> 16) | 0x40u;
-  u += 0x7fffu + ((u >> 16) & 1u);
-  return u >> 16;
+// float -> bfloat16, round to nearest even; NaN stays NaN.  The conversion
+// is gfx950's packed v_cvt_pk_bf16_f32 (one instruction for two values).
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+__device__ __forceinline__ uint32_t pack2(float lo, float hi) {
+  const bf16x2 v = {(__bf16)lo, (__bf16)hi};
+  return __builtin_bit_cast(uint32_t, v);
 }
+__device__ __forceinline__ uint32_t f2bf_bits(float f) { return pack2(f, 0.f) & 0xffffu; }
 __device__ __forceinline__ bf16_t f2bf(float f) { return (bf16_t)f2bf_bits(f); }
-__device__ __forceinline__ uint32_t pack2(float lo, float hi) { return f2bf_bits(lo) | (f2bf_bits(hi) << 16); }
 
 __device__ __forceinline__ u32x4 ld16(const bf16_t* p) { return *reinterpret_cast<const u32x4*>(p); }
 __device__ __forceinline__ u32x2 ld8(const bf16_t* p) { return *reinterpret_cast<const u32x2*>(p); }
