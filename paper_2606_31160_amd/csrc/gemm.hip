@@ -407,6 +407,258 @@ __global__ __launch_bounds__(threads_for(MB)) void k_gemm(GemvArgs a) {
   }
 }
 
+// ---------------------------------------------------------------------------
+// Wide-unit GEMM for the gate/up and LM-head projections of passes of 65 to
+// 160 rows over the tile-packed weights.  A workgroup owns kWideTiles = 16
+// output tiles (256 columns) and the whole k-range; its 4 waves own 4
+// consecutive tiles each and every row block, so each x operand read from LDS
+// feeds 4 MFMAs and each weight block MB of them.  Per 32-wide k-step the x
+// operands of all rows are staged by buffer-to-LDS loads straight in MFMA
+// operand order (block rb of a step: 16 rows x 32 columns, lane l's 16 bytes
+// at 16 l), kWideDepth steps ahead; weights go to registers the same depth
+// ahead.  One barrier per step; its wait counts are set by hand (the loads of
+// a step are x, then weights, in a fixed number per wave), so that every
+// step in flight stays in flight.  Steps past the end load the last step's x
+// again (finite values) and no weights (zeros).  Rows past M read past the
+// end of x; their outputs are never stored.
+// ---------------------------------------------------------------------------
+constexpr int kWideTiles = 16;
+constexpr int kWideWaves = 4;
+constexpr int kWideTpw = kWideTiles / kWideWaves;   // tiles per wave
+constexpr int kWideDepth = 3;
+constexpr int kWideSlice = 8;                       // sums of squares per partial of the 1/rms prologue
+
+__device__ __forceinline__ void lds_load16(__amdgpu_buffer_rsrc_t r, unsigned char* dst, int voff) {
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (__attribute__((address_space(3))) void*)(dst), 16, voff, 0, 0, 0);
+}
+
+size_t wide_lds_bytes(int mb, int H) {
+  const int nsl = (H / kTile + kWideSlice - 1) / kWideSlice;
+  return (size_t)(kWideDepth + 1) * mb * 1024 + 1024 + (size_t)nsl * 16 * mb * sizeof(float);
+}
+
+template <int MB, int EPI>
+__global__ __launch_bounds__(kWideWaves * 64, 1) void k_gemm_wide(GemvArgs a) {
+  static_assert(EPI == EPI_SWIGLU || EPI == EPI_ARGMAX, "normalised-input epilogues");
+  constexpr int ROWS = 16 * MB, TPW = kWideTpw, D = kWideDepth, NB = D + 1, NT = kWideWaves * 64;
+  constexpr int XPW = (MB + kWideWaves - 1) / kWideWaves;   // x blocks each wave stages per step
+  // loads issued after step c's x loads while they are awaited: that step's
+  // weights, then D - 1 steps of both
+  constexpr int WAITN = TPW + (D - 1) * (XPW + TPW);
+  extern __shared__ __align__(16) unsigned char lds[];
+  __shared__ float inv_rms[ROWS];
+  __shared__ int live_s[ROWS];
+  const int wave = __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6)), lane = threadIdx.x & 63;
+  const int M = a.M, N = a.N, ntiles = N / kTile;
+  const int T = (a.Kd + 31) >> 5;
+  const int tile0 = blockIdx.x * kWideTiles + wave * TPW;   // this wave's first tile
+  const __amdgpu_buffer_rsrc_t rw =
+      __builtin_amdgcn_make_buffer_rsrc(const_cast<bf16_t*>(a.pw), 0, ntiles * T * 1024, kRsrcWord3);
+  const __amdgpu_buffer_rsrc_t rx =
+      __builtin_amdgcn_make_buffer_rsrc(const_cast<bf16_t*>(a.x), 0, M * a.ldx * 2, kRsrcWord3);
+  unsigned char* xbuf = lds;                                   // [NB][MB] blocks of 1 KB
+  unsigned char* dummy = lds + NB * MB * 1024;                 // target of the spare x loads
+  float* rms_part = reinterpret_cast<float*>(dummy + 1024);    // [slices][ROWS]
+  const int nt16 = a.H / kTile, nsl = (nt16 + kWideSlice - 1) / kWideSlice;
+
+  for (int m = threadIdx.x; m < ROWS; m += NT) {
+    int lv = 0;
+    if (m < M) {
+      const int b = m / a.rps;
+      lv = (m - b * a.rps) < a.st[b].count ? 1 : 0;
+    }
+    live_s[m] = lv;
+  }
+
+  // 1/rms, first half: partial sums of kWideSlice consecutive per-16-column
+  // sums of squares per (slice, row)
+  const int lane_x = ((lane & 15) * a.ldx + 8 * (lane >> 4)) * 2;
+  const int lane_w = 16 * lane;
+  auto issue_x = [&](int c) {
+    const int st = min(c, T - 1);
+#pragma unroll
+    for (int j = 0; j < XPW; ++j) {
+      const int b = wave + kWideWaves * j;
+      unsigned char* dst = b < MB ? xbuf + ((c % NB) * MB + b) * 1024 : dummy;
+      lds_load16(rx, dst, b < MB ? lane_x + (b * 16 * a.ldx + st * 32) * 2 : kOut);
+    }
+  };
+  // Weights of step c (steps past the end: the last step again, never
+  // multiplied; tiles past N: the last tile, never stored), so that every
+  // load is issued whatever the step and no branch splits the loop.
+  auto issue_w = [&](int c, u32x4 (&wr)[TPW]) {
+    const int st = min(c, T - 1);
+#pragma unroll
+    for (int t = 0; t < TPW; ++t)
+      wr[t] = __builtin_amdgcn_raw_buffer_load_b128(rw, lane_w + (min(tile0 + t, ntiles - 1) * T + st) * 1024, 0,
+                                                    kNt);
+  };
+  for (int it = threadIdx.x; it < nsl * ROWS; it += 4 * NT) {   // up to 4 items per thread and round
+    float v[4][kWideSlice];
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int item = it + r * NT, sl = item / ROWS, m = item % ROWS;
+#pragma unroll
+      for (int k = 0; k < kWideSlice; ++k) {
+        const int g = sl * kWideSlice + k;
+        v[r][k] = (item < nsl * ROWS && g < nt16) ? a.ss_in[(size_t)g * a.mpad + m] : 0.f;
+      }
+    }
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int item = it + r * NT;
+      float sum = 0.f;
+#pragma unroll
+      for (int k = 0; k < kWideSlice; ++k) sum += v[r][k];
+      if (item < nsl * ROWS) rms_part[item] = sum;
+    }
+  }
+
+  u32x4 wr[D][TPW];
+#pragma unroll
+  for (int i = 0; i < D; ++i) {
+    issue_x(i);
+    issue_w(i, wr[i]);
+  }
+  f32x4 acc[TPW][MB];
+#pragma unroll
+  for (int t = 0; t < TPW; ++t)
+#pragma unroll
+    for (int mb = 0; mb < MB; ++mb) acc[t][mb] = f32x4{0.f, 0.f, 0.f, 0.f};
+  for (int c0 = 0; c0 < T; c0 += D) {   // workgroup-uniform
+#pragma unroll
+    for (int uu = 0; uu < D; ++uu) {
+      const int c = c0 + uu;
+      // step c's x (every wave's share) has landed and is visible; the
+      // memory clobbers keep LDS accesses on their side of the barrier
+      asm volatile("s_waitcnt vmcnt(%0)" ::"n"(WAITN) : "memory");
+      __builtin_amdgcn_s_barrier();
+      asm volatile("" ::: "memory");
+      const unsigned char* xb = xbuf + (c % NB) * (MB * 1024) + 16 * lane;
+      u32x4 w[TPW];
+#pragma unroll
+      for (int t = 0; t < TPW; ++t) w[t] = wr[uu][t];
+      if (c < T) {   // workgroup-uniform
+#pragma unroll
+        for (int mb = 0; mb < MB; ++mb) {
+          const u32x4 xv = *reinterpret_cast<const u32x4*>(xb + mb * 1024);
+#pragma unroll
+          for (int t = 0; t < TPW; ++t) acc[t][mb] = mfma16x16x32(w[t], xv, acc[t][mb]);
+        }
+      }
+      asm volatile("" ::: "memory");
+      // buffer (c + D) % NB was last read at step c - 1, before this step's barrier
+      issue_x(c + D);
+      issue_w(c + D, wr[uu]);
+    }
+  }
+  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");   // the spare loads past the end
+  __syncthreads();
+  // 1/rms, second half: the slices of each row in order
+  for (int m = threadIdx.x; m < ROWS; m += NT) {
+    float t = 0.f;
+    for (int sl = 0; sl < nsl; ++sl) t += rms_part[sl * ROWS + m];
+    inv_rms[m] = live_s[m] ? rsqrtf(t / a.H + a.eps) : 0.f;
+  }
+  __syncthreads();
+
+  const int grp = lane >> 4;
+  if constexpr (EPI == EPI_SWIGLU) {
+    // tiles tile0 + 2j, tile0 + 2j + 1: the gate and up rows of features
+    // 16 (tile0 / 2 + j) .. +16
+    const int F = N / 2;
+#pragma unroll
+    for (int j = 0; j < TPW / 2; ++j) {
+      const int f = ((tile0 >> 1) + j) * kTile + 4 * grp;
+#pragma unroll
+      for (int mb = 0; mb < MB; ++mb) {
+        const int m = mb * 16 + (lane & 15);
+        if (m >= M || f >= F) continue;
+        const float r = inv_rms[m];
+        float o[4];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const float g = acc[2 * j][mb][i] * r, up = acc[2 * j + 1][mb][i] * r;
+          o[i] = live_s[m] ? g / (1.f + expf(-g)) * up : 0.f;
+        }
+        *reinterpret_cast<u32x2*>(a.u + (size_t)m * F + f) = u32x2{pack2(o[0], o[1]), pack2(o[2], o[3])};
+      }
+    }
+  } else {   // EPI_ARGMAX: per tile and row, the (max, index) of its 16 logits
+#pragma unroll
+    for (int t = 0; t < TPW; ++t) {
+      const int tile = tile0 + t;
+      if (tile >= ntiles) continue;
+      const int n = tile * kTile + 4 * grp;
+#pragma unroll
+      for (int mb = 0; mb < MB; ++mb) {
+        const int m = mb * 16 + (lane & 15);
+        const int mm = m < ROWS ? m : ROWS - 1;
+        const bool live = m < M && live_s[mm];
+        const float r = inv_rms[mm];
+        float y[4];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) y[i] = live ? acc[t][mb][i] * r : 0.f;
+        if (a.allow_logits && m < M && a.st[m / a.rps].want_logits)
+          *reinterpret_cast<u32x2*>(a.logits + (size_t)m * N + n) = u32x2{pack2(y[0], y[1]), pack2(y[2], y[3])};
+        float best = -INFINITY;
+        int bi = n;
+        int nan = 0;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          float v = y[i];
+          if (v != v) {
+            nan = 1;
+            v = -INFINITY;
+          }
+          if (v > best) {
+            best = v;
+            bi = n + i;
+          }
+        }
+#pragma unroll
+        for (int o = 16; o <= 32; o <<= 1) {
+          const float v2 = __shfl_xor(best, o);
+          const int i2 = __shfl_xor(bi, o);
+          nan |= __shfl_xor(nan, o);
+          amax_merge(best, bi, v2, i2);
+        }
+        if (grp == 0 && m < M) {
+          a.amax_v[(size_t)tile * a.mpad + m] = best;
+          a.amax_i[(size_t)tile * a.mpad + m] = bi;
+          if (nan && live) atomicOr(const_cast<int32_t*>(&a.st[m / a.rps].err), ERR_NUMERIC);
+        }
+      }
+    }
+  }
+}
+
+template <int EPI>
+hipError_t launch_wide(const GemvArgs& g, hipStream_t s, hipEvent_t e0, hipEvent_t e1) {
+  const int mb = (g.M + 15) / 16;
+  const dim3 grid((g.N / kTile + kWideTiles - 1) / kWideTiles), block(kWideWaves * 64);
+  const size_t lds = wide_lds_bytes(mb, g.H);
+  switch (mb) {
+    case 5: hipExtLaunchKernelGGL((k_gemm_wide<5, EPI>), grid, block, lds, s, e0, e1, 0, g); break;
+    case 6: hipExtLaunchKernelGGL((k_gemm_wide<6, EPI>), grid, block, lds, s, e0, e1, 0, g); break;
+    case 7: hipExtLaunchKernelGGL((k_gemm_wide<7, EPI>), grid, block, lds, s, e0, e1, 0, g); break;
+    case 8: hipExtLaunchKernelGGL((k_gemm_wide<8, EPI>), grid, block, lds, s, e0, e1, 0, g); break;
+    case 9: hipExtLaunchKernelGGL((k_gemm_wide<9, EPI>), grid, block, lds, s, e0, e1, 0, g); break;
+    case 10: hipExtLaunchKernelGGL((k_gemm_wide<10, EPI>), grid, block, lds, s, e0, e1, 0, g); break;
+    default: return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
+
+template <int MB>
+void set_wide_attributes(int limit) {
+  const int lds = (int)std::min((size_t)limit, wide_lds_bytes(MB, 8192));
+  (void)hipFuncSetAttribute(reinterpret_cast<const void*>(&k_gemm_wide<MB, EPI_SWIGLU>),
+                            hipFuncAttributeMaxDynamicSharedMemorySize, lds);
+  (void)hipFuncSetAttribute(reinterpret_cast<const void*>(&k_gemm_wide<MB, EPI_ARGMAX>),
+                            hipFuncAttributeMaxDynamicSharedMemorySize, lds);
+}
+
 template <int EPI>
 hipError_t launch_mb(const GemvArgs& g, hipStream_t s, hipEvent_t e0, hipEvent_t e1) {
   const int mb = (g.M + 15) / 16;
@@ -456,6 +708,12 @@ void gemm_set_attributes(int limit) {
   set_mb_attributes<8>(limit);
   set_mb_attributes<9>(limit);
   set_mb_attributes<10>(limit);
+  set_wide_attributes<5>(limit);
+  set_wide_attributes<6>(limit);
+  set_wide_attributes<7>(limit);
+  set_wide_attributes<8>(limit);
+  set_wide_attributes<9>(limit);
+  set_wide_attributes<10>(limit);
 }
 
 hipError_t gemm_launch(int epi, const GemvArgs& g, hipStream_t s, hipEvent_t e0, hipEvent_t e1) {
@@ -472,6 +730,15 @@ hipError_t gemm_launch(int epi, const GemvArgs& g, hipStream_t s, hipEvent_t e0,
   }
   // every operand is addressed with 32-bit byte offsets below kOut
   if ((long long)g.N * ((g.Kd + 31) / 32) * 64 >= kOut || (long long)g.M * g.ldx * 2 >= kOut) return hipErrorInvalidValue;
+  // the normalised-input projections of passes of 5 to 10 row blocks over
+  // the tile-packed copy (gate/up in tile pairs): the wide-unit kernel
+  {
+    const int mb = (g.M + 15) / 16;
+    if (g.pw && (epi == EPI_SWIGLU || epi == EPI_ARGMAX) && mb >= 5 && mb <= 10 && g.splits == 1 &&
+        (g.N / kTile) % 2 == 0 &&
+        wide_lds_bytes(mb, g.H) <= (size_t)gemv_lds_limit())
+      return epi == EPI_SWIGLU ? launch_wide<EPI_SWIGLU>(g, s, e0, e1) : launch_wide<EPI_ARGMAX>(g, s, e0, e1);
+  }
   switch (epi) {
     case EPI_STORE: return launch_mb<EPI_STORE>(g, s, e0, e1);
     case EPI_ROPE: return launch_mb<EPI_ROPE>(g, s, e0, e1);
