@@ -162,6 +162,7 @@ struct Ctx {
   int Mpad1 = 16;                    // ... whose row count B is padded to this
   bool gemm_rows = false;              // layered row-major passes run on the batched-row GEMM
   bool gemm_pk = false;                // ... which streams the tile-packed weight copy
+  bool gemm_wide = false;              // ... on the wide-unit kernel (passes of more than 32 rows)
   bool poisoned = false;
   std::string err;
 

@@ -408,58 +408,92 @@ __global__ __launch_bounds__(threads_for(MB)) void k_gemm(GemvArgs a) {
 }
 
 // ---------------------------------------------------------------------------
-// Wide-unit GEMM for the gate/up and LM-head projections of passes of 65 to
-// 160 rows over the tile-packed weights.  A workgroup owns kWideTiles = 16
-// output tiles (256 columns) and the whole k-range; its 4 waves own 4
-// consecutive tiles each and every row block, so each x operand read from LDS
-// feeds 4 MFMAs and each weight block MB of them.  Per 32-wide k-step the x
-// operands of all rows are staged by buffer-to-LDS loads straight in MFMA
-// operand order (block rb of a step: 16 rows x 32 columns, lane l's 16 bytes
-// at 16 l), kWideDepth steps ahead; weights go to registers the same depth
-// ahead.  One barrier per step; its wait counts are set by hand (the loads of
-// a step are x, then weights, in a fixed number per wave), so that every
-// step in flight stays in flight.  Steps past the end load the last step's x
-// again (finite values) and no weights (zeros).  Rows past M read past the
-// end of x; their outputs are never stored.
+// Wide-unit GEMM over the tile-packed weights for passes of 33 to 160 rows
+// (3 to 10 row blocks): the gate/up and LM-head projections in one launch, and
+// the q/k/v, o and down projections as k-split partial sums.  A workgroup owns
+// kWideTiles = 16 output tiles (256 columns) and the k-range of split
+// blockIdx.y.  Its 8 waves are 4 column groups x 2 k-groups: wave (cg, kg)
+// multiplies tiles 4 cg .. 4 cg + 3 over the kg-th half of the k-range, so
+// each x operand it reads from LDS feeds 4 MFMAs and each weight block MB of
+// them, and the two k-groups keep two independent streams of loads in flight.
+// Per 32-wide k-step each k-group stages the x operands of all rows by
+// buffer-to-LDS loads straight in MFMA operand order (block rb of a step: 16
+// rows x 32 columns, lane l's 16 bytes at 16 l) into its own ring of D + 1
+// slots, D steps ahead; weights go to registers the same depth ahead.  One
+// barrier per step; its wait count is set by hand (every wave issues the same
+// loads per step: its share of its k-group's x blocks, then its 4 weight
+// blocks), so that every step in flight stays in flight.  A load past its
+// k-group's range or past the last tile gets an offset past the operand and
+// returns zeros without a memory access; rows past M read past the end of x
+// and are never stored.  At the end the second k-group's partial tiles are
+// added to the first's through LDS (first half + second half of the k-range),
+// and the first k-group runs the epilogue.
 // ---------------------------------------------------------------------------
 constexpr int kWideTiles = 16;
-constexpr int kWideWaves = 4;
-constexpr int kWideTpw = kWideTiles / kWideWaves;   // tiles per wave
-constexpr int kWideDepth = 3;
+constexpr int kWideWaves = 8;
+constexpr int kWideCg = 4;                          // column groups
+constexpr int kWideTpw = kWideTiles / kWideCg;      // tiles per wave
 constexpr int kWideSlice = 8;                       // sums of squares per partial of the 1/rms prologue
+// steps in flight per k-group: 4, or 3 for 9 and 10 row blocks (whose
+// accumulators take 144 and 160 of a wave's 256 registers)
+constexpr int wide_depth(int mb) { return mb >= 9 ? 3 : 4; }
 
 __device__ __forceinline__ void lds_load16(__amdgpu_buffer_rsrc_t r, unsigned char* dst, int voff) {
   __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (__attribute__((address_space(3))) void*)(dst), 16, voff, 0, 0, 0);
 }
 
+// the two x rings, the dummy block (target of the spare x loads) and the
+// 1/rms partials; the final k-group sum reuses the rings (8 MB blocks)
 size_t wide_lds_bytes(int mb, int H) {
   const int nsl = (H / kTile + kWideSlice - 1) / kWideSlice;
-  return (size_t)(kWideDepth + 1) * mb * 1024 + 1024 + (size_t)nsl * 16 * mb * sizeof(float);
+  return (size_t)2 * (wide_depth(mb) + 1) * mb * 1024 + 1024 + (size_t)nsl * 16 * mb * sizeof(float);
 }
 
 template <int MB, int EPI>
 __global__ __launch_bounds__(kWideWaves * 64, 1) void k_gemm_wide(GemvArgs a) {
-  static_assert(EPI == EPI_SWIGLU || EPI == EPI_ARGMAX, "normalised-input epilogues");
-  constexpr int ROWS = 16 * MB, TPW = kWideTpw, D = kWideDepth, NB = D + 1, NT = kWideWaves * 64;
-  constexpr int XPW = (MB + kWideWaves - 1) / kWideWaves;   // x blocks each wave stages per step
+  static_assert(EPI == EPI_SWIGLU || EPI == EPI_ARGMAX || EPI == EPI_STORE, "wide-unit epilogues");
+  constexpr bool kNorm = EPI != EPI_STORE;
+  constexpr int ROWS = 16 * MB, TPW = kWideTpw, D = wide_depth(MB), NB = D + 1, NT = kWideWaves * 64;
+  constexpr int XPW = (MB + kWideCg - 1) / kWideCg;   // x blocks each wave stages per step
   // loads issued after step c's x loads while they are awaited: that step's
   // weights, then D - 1 steps of both
   constexpr int WAITN = TPW + (D - 1) * (XPW + TPW);
+  static_assert(2 * NB >= 2 * kWideCg, "the k-group sum reuses the x rings");
+  static_assert(TPW == 4, "the weight wait names four register tuples");
   extern __shared__ __align__(16) unsigned char lds[];
   __shared__ float inv_rms[ROWS];
   __shared__ int live_s[ROWS];
   const int wave = __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6)), lane = threadIdx.x & 63;
+  const int cg = wave % kWideCg, kg = wave / kWideCg;
   const int M = a.M, N = a.N, ntiles = N / kTile;
   const int T = (a.Kd + 31) >> 5;
-  const int tile0 = blockIdx.x * kWideTiles + wave * TPW;   // this wave's first tile
-  const __amdgpu_buffer_rsrc_t rw =
-      __builtin_amdgcn_make_buffer_rsrc(const_cast<bf16_t*>(a.pw), 0, ntiles * T * 1024, kRsrcWord3);
+  const int split = blockIdx.y;
+  const int s0 = (int)((long long)split * T / a.splits), s1 = (int)((long long)(split + 1) * T / a.splits);
+  const int half = (s1 - s0 + 1) >> 1;
+  const int kb = kg ? s0 + half : s0, ke = kg ? s1 : s0 + half;   // this k-group's steps [kb, ke)
+  // Units of two tiles (a gate/up pair).  SwiGLU and argmax: contiguous
+  // ranges of units dealt evenly to the gridDim.x workgroups (one per CU), so
+  // that every CU streams the same share of the weights, each range walked in
+  // chunks of at most 8 units (16 tiles); k-split partial sums: 8 units per
+  // workgroup.
+  const int nunits = ntiles >> 1;
+  int u0, u1;
+  if constexpr (EPI == EPI_STORE) {
+    u0 = blockIdx.x * (kWideTiles / 2);
+    u1 = min(u0 + kWideTiles / 2, nunits);
+  } else {
+    u0 = (int)((long long)blockIdx.x * nunits / gridDim.x);
+    u1 = (int)((long long)(blockIdx.x + 1) * nunits / gridDim.x);
+  }
+  const int nch = (u1 - u0 + kWideTiles / 2 - 1) / (kWideTiles / 2);
+  const int cu = nch > 0 ? (u1 - u0 + nch - 1) / nch : 1;   // units per chunk
+  int tile0 = 0, tend = 0;   // this wave's first tile, the chunk's end tile
   const __amdgpu_buffer_rsrc_t rx =
       __builtin_amdgcn_make_buffer_rsrc(const_cast<bf16_t*>(a.x), 0, M * a.ldx * 2, kRsrcWord3);
-  unsigned char* xbuf = lds;                                   // [NB][MB] blocks of 1 KB
-  unsigned char* dummy = lds + NB * MB * 1024;                 // target of the spare x loads
-  float* rms_part = reinterpret_cast<float*>(dummy + 1024);    // [slices][ROWS]
-  const int nt16 = a.H / kTile, nsl = (nt16 + kWideSlice - 1) / kWideSlice;
+  unsigned char* ring = lds + (size_t)kg * NB * MB * 1024;           // [NB][MB] blocks of 1 KB
+  unsigned char* dummy = lds + (size_t)2 * NB * MB * 1024;           // target of the spare x loads
+  float* rms_part = reinterpret_cast<float*>(dummy + 1024);          // [slices][ROWS]
+  const int nt16 = kNorm ? a.H / kTile : 0, nsl = (nt16 + kWideSlice - 1) / kWideSlice;
 
   for (int m = threadIdx.x; m < ROWS; m += NT) {
     int lv = 0;
@@ -470,50 +504,78 @@ __global__ __launch_bounds__(kWideWaves * 64, 1) void k_gemm_wide(GemvArgs a) {
     live_s[m] = lv;
   }
 
-  // 1/rms, first half: partial sums of kWideSlice consecutive per-16-column
-  // sums of squares per (slice, row)
   const int lane_x = ((lane & 15) * a.ldx + 8 * (lane >> 4)) * 2;
   const int lane_w = 16 * lane;
+  // Offsets past a k-group's range or the last tile are ORed with kOut (a
+  // wave-uniform scalar select): every offset stays below 2^31, so the result
+  // lies past the operand, and no branch splits the loads (a branch would
+  // make the compiler drain every load in flight where the paths join).
   auto issue_x = [&](int c) {
-    const int st = min(c, T - 1);
+    const int st = kb + c;
+    const int oob = st < ke ? 0 : kOut;
+    unsigned char* slot = ring + (c % NB) * (MB * 1024);
 #pragma unroll
     for (int j = 0; j < XPW; ++j) {
-      const int b = wave + kWideWaves * j;
-      unsigned char* dst = b < MB ? xbuf + ((c % NB) * MB + b) * 1024 : dummy;
-      lds_load16(rx, dst, b < MB ? lane_x + (b * 16 * a.ldx + st * 32) * 2 : kOut);
+      const int b = cg + kWideCg * j;
+      const int ob = b < MB ? oob : kOut;
+      lds_load16(rx, b < MB ? slot + b * 1024 : dummy, (lane_x + (b * 16 * a.ldx + st * 32) * 2) | ob);
     }
   };
-  // Weights of step c (steps past the end: the last step again, never
-  // multiplied; tiles past N: the last tile, never stored), so that every
-  // load is issued whatever the step and no branch splits the loop.
+  // The weight loads are written as inline assembly, and waited for by hand
+  // below.  The compiler's own wait counts leave out the buffer-to-LDS loads
+  // it issues between them, so they would wait for several steps' loads at
+  // once where one step's are due.
+  const uint64_t wbase = reinterpret_cast<uint64_t>(a.pw);
+  const u32x4 wdesc = u32x4{(uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)wbase),
+                            (uint32_t)__builtin_amdgcn_readfirstlane((int)((wbase >> 32) & 0xffffu)),
+                            (uint32_t)(ntiles * T * 1024), (uint32_t)kRsrcWord3};
   auto issue_w = [&](int c, u32x4 (&wr)[TPW]) {
-    const int st = min(c, T - 1);
+    const int st = kb + c;
+    const int oob = st < ke ? 0 : kOut;
 #pragma unroll
-    for (int t = 0; t < TPW; ++t)
-      wr[t] = __builtin_amdgcn_raw_buffer_load_b128(rw, lane_w + (min(tile0 + t, ntiles - 1) * T + st) * 1024, 0,
-                                                    kNt);
+    for (int t = 0; t < TPW; ++t) {
+      const int ot = tile0 + t < tend ? oob : kOut;
+      const int off = (lane_w + ((tile0 + t) * T + st) * 1024) | ot;
+      asm volatile("buffer_load_dwordx4 %0, %1, %2, 0 offen nt" : "=v"(wr[t]) : "v"(off), "s"(wdesc) : "memory");
+    }
   };
-  for (int it = threadIdx.x; it < nsl * ROWS; it += 4 * NT) {   // up to 4 items per thread and round
-    float v[4][kWideSlice];
+
+  // 1/rms, first half: partial sums of kWideSlice consecutive per-16-column
+  // sums of squares per (slice, row)
+  if constexpr (kNorm) {
+    for (int it = threadIdx.x; it < nsl * ROWS; it += 4 * NT) {   // up to 4 items per thread and round
+      float v[4][kWideSlice];
 #pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      const int item = it + r * NT, sl = item / ROWS, m = item % ROWS;
+      for (int r = 0; r < 4; ++r) {
+        const int item = it + r * NT, sl = item / ROWS, m = item % ROWS;
 #pragma unroll
-      for (int k = 0; k < kWideSlice; ++k) {
-        const int g = sl * kWideSlice + k;
-        v[r][k] = (item < nsl * ROWS && g < nt16) ? a.ss_in[(size_t)g * a.mpad + m] : 0.f;
+        for (int k = 0; k < kWideSlice; ++k) {
+          const int g = sl * kWideSlice + k;
+          v[r][k] = (item < nsl * ROWS && g < nt16) ? a.ss_in[(size_t)g * a.mpad + m] : 0.f;
+        }
+      }
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int item = it + r * NT;
+        float sum = 0.f;
+#pragma unroll
+        for (int k = 0; k < kWideSlice; ++k) sum += v[r][k];
+        if (item < nsl * ROWS) rms_part[item] = sum;
       }
     }
-#pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      const int item = it + r * NT;
-      float sum = 0.f;
-#pragma unroll
-      for (int k = 0; k < kWideSlice; ++k) sum += v[r][k];
-      if (item < nsl * ROWS) rms_part[item] = sum;
+    __syncthreads();
+    // 1/rms, second half: the slices of each row in order
+    for (int m = threadIdx.x; m < ROWS; m += NT) {
+      float t = 0.f;
+      for (int sl = 0; sl < nsl; ++sl) t += rms_part[sl * ROWS + m];
+      inv_rms[m] = live_s[m] ? rsqrtf(t / a.H + a.eps) : 0.f;
     }
   }
+  __syncthreads();
 
+  for (int cs = u0; cs < u1; cs += cu) {   // workgroup-uniform
+  tile0 = 2 * cs + cg * TPW;
+  tend = 2 * min(cs + cu, u1);
   u32x4 wr[D][TPW];
 #pragma unroll
   for (int i = 0; i < D; ++i) {
@@ -525,7 +587,7 @@ __global__ __launch_bounds__(kWideWaves * 64, 1) void k_gemm_wide(GemvArgs a) {
   for (int t = 0; t < TPW; ++t)
 #pragma unroll
     for (int mb = 0; mb < MB; ++mb) acc[t][mb] = f32x4{0.f, 0.f, 0.f, 0.f};
-  for (int c0 = 0; c0 < T; c0 += D) {   // workgroup-uniform
+  for (int c0 = 0; c0 < half; c0 += D) {   // workgroup-uniform
 #pragma unroll
     for (int uu = 0; uu < D; ++uu) {
       const int c = c0 + uu;
@@ -534,11 +596,18 @@ __global__ __launch_bounds__(kWideWaves * 64, 1) void k_gemm_wide(GemvArgs a) {
       asm volatile("s_waitcnt vmcnt(%0)" ::"n"(WAITN) : "memory");
       __builtin_amdgcn_s_barrier();
       asm volatile("" ::: "memory");
-      const unsigned char* xb = xbuf + (c % NB) * (MB * 1024) + 16 * lane;
+      const unsigned char* xb = ring + (c % NB) * (MB * 1024) + 16 * lane;
+      // step c's weights: the loads issued after them are D - 1 steps of x
+      // and weights; the registers are operands of the wait, so nothing reads
+      // them before it
+      asm volatile("s_waitcnt vmcnt(%4)"
+                   : "+v"(wr[uu][0]), "+v"(wr[uu][1]), "+v"(wr[uu][2]), "+v"(wr[uu][3])
+                   : "n"((D - 1) * (XPW + TPW))
+                   : "memory");
       u32x4 w[TPW];
 #pragma unroll
       for (int t = 0; t < TPW; ++t) w[t] = wr[uu][t];
-      if (c < T) {   // workgroup-uniform
+      if (kb + c < ke) {   // wave-uniform
 #pragma unroll
         for (int mb = 0; mb < MB; ++mb) {
           const u32x4 xv = *reinterpret_cast<const u32x4*>(xb + mb * 1024);
@@ -547,23 +616,49 @@ __global__ __launch_bounds__(kWideWaves * 64, 1) void k_gemm_wide(GemvArgs a) {
         }
       }
       asm volatile("" ::: "memory");
-      // buffer (c + D) % NB was last read at step c - 1, before this step's barrier
+      // slot (c + D) % NB was last read at step c - 1, before this step's barrier
       issue_x(c + D);
       issue_w(c + D, wr[uu]);
     }
   }
   asm volatile("s_waitcnt vmcnt(0)" ::: "memory");   // the spare loads past the end
   __syncthreads();
-  // 1/rms, second half: the slices of each row in order
-  for (int m = threadIdx.x; m < ROWS; m += NT) {
-    float t = 0.f;
-    for (int sl = 0; sl < nsl; ++sl) t += rms_part[sl * ROWS + m];
-    inv_rms[m] = live_s[m] ? rsqrtf(t / a.H + a.eps) : 0.f;
-  }
-  __syncthreads();
 
+  // the second k-group's partial tiles onto the first's, two tiles at a time
+  f32x4* red = reinterpret_cast<f32x4*>(lds);   // [2][kWideCg][MB][64]
+#pragma unroll
+  for (int h = 0; h < TPW / 2; ++h) {
+    if (kg == 1) {
+#pragma unroll
+      for (int tt = 0; tt < 2; ++tt)
+#pragma unroll
+        for (int mb = 0; mb < MB; ++mb) red[((tt * kWideCg + cg) * MB + mb) * 64 + lane] = acc[2 * h + tt][mb];
+    }
+    __syncthreads();
+    if (kg == 0) {
+#pragma unroll
+      for (int tt = 0; tt < 2; ++tt)
+#pragma unroll
+        for (int mb = 0; mb < MB; ++mb) acc[2 * h + tt][mb] += red[((tt * kWideCg + cg) * MB + mb) * 64 + lane];
+    }
+    __syncthreads();
+  }
+  if (kg == 0) {
   const int grp = lane >> 4;
-  if constexpr (EPI == EPI_SWIGLU) {
+  if constexpr (EPI == EPI_STORE) {
+    // fp32 partial sums of this split: out[split][m][n]
+#pragma unroll
+    for (int t = 0; t < TPW; ++t) {
+      const int tile = tile0 + t;
+      if (tile >= tend) continue;
+      const int n = tile * kTile + 4 * grp;
+#pragma unroll
+      for (int mb = 0; mb < MB; ++mb) {
+        const int m = mb * 16 + (lane & 15);
+        if (m < M) *reinterpret_cast<f32x4*>(a.out + ((size_t)split * M + m) * N + n) = acc[t][mb];
+      }
+    }
+  } else if constexpr (EPI == EPI_SWIGLU) {
     // tiles tile0 + 2j, tile0 + 2j + 1: the gate and up rows of features
     // 16 (tile0 / 2 + j) .. +16
     const int F = N / 2;
@@ -573,7 +668,7 @@ __global__ __launch_bounds__(kWideWaves * 64, 1) void k_gemm_wide(GemvArgs a) {
 #pragma unroll
       for (int mb = 0; mb < MB; ++mb) {
         const int m = mb * 16 + (lane & 15);
-        if (m >= M || f >= F) continue;
+        if (m >= M || f >= F || tile0 + 2 * j >= tend) continue;
         const float r = inv_rms[m];
         float o[4];
 #pragma unroll
@@ -588,7 +683,7 @@ __global__ __launch_bounds__(kWideWaves * 64, 1) void k_gemm_wide(GemvArgs a) {
 #pragma unroll
     for (int t = 0; t < TPW; ++t) {
       const int tile = tile0 + t;
-      if (tile >= ntiles) continue;
+      if (tile >= tend) continue;
       const int n = tile * kTile + 4 * grp;
 #pragma unroll
       for (int mb = 0; mb < MB; ++mb) {
@@ -631,14 +726,31 @@ __global__ __launch_bounds__(kWideWaves * 64, 1) void k_gemm_wide(GemvArgs a) {
       }
     }
   }
+  }   // kg == 0
+  __syncthreads();   // the chunk's LDS reads are done before the next chunk's loads land
+  }   // chunks
+}
+
+// CUs of the current device (the wide kernel's grid for SwiGLU and argmax)
+int wide_cus() {
+  int dev = 0, n = 0;
+  if (hipGetDevice(&dev) != hipSuccess || hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+      n < 1) {
+    (void)hipGetLastError();
+    return 256;
+  }
+  return n;
 }
 
 template <int EPI>
 hipError_t launch_wide(const GemvArgs& g, hipStream_t s, hipEvent_t e0, hipEvent_t e1) {
   const int mb = (g.M + 15) / 16;
-  const dim3 grid((g.N / kTile + kWideTiles - 1) / kWideTiles), block(kWideWaves * 64);
-  const size_t lds = wide_lds_bytes(mb, g.H);
+  const int groups = (g.N / kTile + kWideTiles - 1) / kWideTiles;
+  const dim3 grid(EPI == EPI_STORE ? groups : std::min(wide_cus(), g.N / kTile / 2), g.splits), block(kWideWaves * 64);
+  const size_t lds = wide_lds_bytes(mb, EPI == EPI_STORE ? 0 : g.H);
   switch (mb) {
+    case 3: hipExtLaunchKernelGGL((k_gemm_wide<3, EPI>), grid, block, lds, s, e0, e1, 0, g); break;
+    case 4: hipExtLaunchKernelGGL((k_gemm_wide<4, EPI>), grid, block, lds, s, e0, e1, 0, g); break;
     case 5: hipExtLaunchKernelGGL((k_gemm_wide<5, EPI>), grid, block, lds, s, e0, e1, 0, g); break;
     case 6: hipExtLaunchKernelGGL((k_gemm_wide<6, EPI>), grid, block, lds, s, e0, e1, 0, g); break;
     case 7: hipExtLaunchKernelGGL((k_gemm_wide<7, EPI>), grid, block, lds, s, e0, e1, 0, g); break;
@@ -653,10 +765,10 @@ hipError_t launch_wide(const GemvArgs& g, hipStream_t s, hipEvent_t e0, hipEvent
 template <int MB>
 void set_wide_attributes(int limit) {
   const int lds = (int)std::min((size_t)limit, wide_lds_bytes(MB, 8192));
-  (void)hipFuncSetAttribute(reinterpret_cast<const void*>(&k_gemm_wide<MB, EPI_SWIGLU>),
-                            hipFuncAttributeMaxDynamicSharedMemorySize, lds);
-  (void)hipFuncSetAttribute(reinterpret_cast<const void*>(&k_gemm_wide<MB, EPI_ARGMAX>),
-                            hipFuncAttributeMaxDynamicSharedMemorySize, lds);
+  const void* f[3] = {reinterpret_cast<const void*>(&k_gemm_wide<MB, EPI_SWIGLU>),
+                      reinterpret_cast<const void*>(&k_gemm_wide<MB, EPI_ARGMAX>),
+                      reinterpret_cast<const void*>(&k_gemm_wide<MB, EPI_STORE>)};
+  for (const void* p : f) (void)hipFuncSetAttribute(p, hipFuncAttributeMaxDynamicSharedMemorySize, lds);
 }
 
 template <int EPI>
@@ -708,6 +820,8 @@ void gemm_set_attributes(int limit) {
   set_mb_attributes<8>(limit);
   set_mb_attributes<9>(limit);
   set_mb_attributes<10>(limit);
+  set_wide_attributes<3>(limit);
+  set_wide_attributes<4>(limit);
   set_wide_attributes<5>(limit);
   set_wide_attributes<6>(limit);
   set_wide_attributes<7>(limit);
@@ -730,14 +844,17 @@ hipError_t gemm_launch(int epi, const GemvArgs& g, hipStream_t s, hipEvent_t e0,
   }
   // every operand is addressed with 32-bit byte offsets below kOut
   if ((long long)g.N * ((g.Kd + 31) / 32) * 64 >= kOut || (long long)g.M * g.ldx * 2 >= kOut) return hipErrorInvalidValue;
-  // the normalised-input projections of passes of 5 to 10 row blocks over
-  // the tile-packed copy (gate/up in tile pairs): the wide-unit kernel
+  // passes of more than kSgMaxRows rows over the tile-packed copy: the
+  // wide-unit kernel for gate/up (tile pairs) and the LM head in one launch,
+  // and for the k-split partial sums of the other projections
   {
     const int mb = (g.M + 15) / 16;
-    if (g.pw && (epi == EPI_SWIGLU || epi == EPI_ARGMAX) && mb >= 5 && mb <= 10 && g.splits == 1 &&
-        (g.N / kTile) % 2 == 0 &&
-        wide_lds_bytes(mb, g.H) <= (size_t)gemv_lds_limit())
+    if (g.pw && g.M > kSgMaxRows && mb <= 10 && (g.N / kTile) % 2 == 0 &&
+        (epi == EPI_STORE || ((epi == EPI_SWIGLU || epi == EPI_ARGMAX) && g.splits == 1)) &&
+        wide_lds_bytes(mb, epi == EPI_STORE ? 0 : g.H) <= (size_t)gemv_lds_limit()) {
+      if (epi == EPI_STORE) return launch_wide<EPI_STORE>(g, s, e0, e1);
       return epi == EPI_SWIGLU ? launch_wide<EPI_SWIGLU>(g, s, e0, e1) : launch_wide<EPI_ARGMAX>(g, s, e0, e1);
+    }
   }
   switch (epi) {
     case EPI_STORE: return launch_mb<EPI_STORE>(g, s, e0, e1);
@@ -759,6 +876,14 @@ int gemm_down_splits(int N, int Kd, int ncu) {
   const int T = (Kd + 31) / 32;
   int s = std::max(1, ncu / groups);
   return std::max(1, std::min(s, T / 8));
+}
+
+int gemm_wide_splits(int N, int Kd, int ncu) {
+  // one round of resident workgroups (one per CU), at least 16 k-steps per
+  // split (8 per k-group)
+  const int groups = (N / kTile + kWideTiles - 1) / kWideTiles;
+  const int T = (Kd + 31) / 32;
+  return std::max(1, std::min(ncu / groups, T / 16));
 }
 
 int gemm_wgs_per_cu(int M) {
@@ -795,6 +920,10 @@ int gemm_qkv_splits(int N, int Kd, int M, int ncu) {
   // split only while 2 * s * M * N fp32 partial bytes <= (N * Kd bf16 weight
   // bytes) / 10.
   return (M > kSgMaxRows || (long long)40 * s * M <= Kd) ? s : 1;
+}
+
+int gemm_qkv_splits_for(int N, int Kd, int M, int ncu, bool wide) {
+  return (wide && M > kSgMaxRows) ? gemm_wide_splits(N, Kd, ncu) : gemm_qkv_splits(N, Kd, M, ncu);
 }
 
 }  // namespace specdec

@@ -68,6 +68,10 @@ void gemm_set_attributes(int limit);
 hipError_t gemm_launch(int epi, const GemvArgs& g, hipStream_t s, hipEvent_t e0, hipEvent_t e1);
 // k-splits of an EPI_STORE GEMM (the down projection) over N outputs and Kd inputs.
 int gemm_down_splits(int N, int Kd, int ncu);
+// k-splits of an EPI_STORE launch of the wide-unit kernel (passes of more
+// than kSgMaxRows rows over the tile-packed copy; 256-column workgroups, one
+// per CU): as many as fill one round of the CUs, at least 16 k-steps each.
+int gemm_wide_splits(int N, int Kd, int ncu);
 // Workgroups of the k-split GEMM over M rows resident per CU: the runtime's
 // occupancy for the shapes of up to three row blocks (at most 2), else 1;
 // the o and down projections split to fill every resident slot once.
@@ -77,5 +81,8 @@ int gemm_wgs_per_cu(int M);
 // partials it writes and reads back stay under a tenth of its weight bytes;
 // a split launch is finished by k_qkv_finish (kernels.hip).
 int gemm_qkv_splits(int N, int Kd, int M, int ncu);
+// The q/k/v k-splits of a pass of M rows: gemm_wide_splits on a context whose
+// passes run on the wide-unit kernel (wide), else gemm_qkv_splits.
+int gemm_qkv_splits_for(int N, int Kd, int M, int ncu, bool wide);
 
 }  // namespace specdec

@@ -1717,7 +1717,7 @@ hipError_t launch_qkv_rm(Ctx& c, Model& m, int li, bf16_t* kc, bf16_t* vt) {
   g.pt = c.pt;
   g.pps = c.pps;
   g.pw = pk;
-  const int sq = c.gemm_rows ? gemm_qkv_splits(g.N, H, M, c.ncu) : 1;
+  const int sq = c.gemm_rows ? gemm_qkv_splits_for(g.N, H, M, c.ncu, c.gemm_wide) : 1;
   if (sq > 1) {
     // too few 64-column workgroups to stream the matrix at full rate: k-split
     // partial sums, then the norm, rotation and cache append in k_qkv_finish

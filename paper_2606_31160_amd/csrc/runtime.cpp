@@ -290,18 +290,25 @@ Layout make_layout(const spec_config* cfg, const spec_seq_init* seqs) {
   return L;
 }
 
-void set_splits(Model& m, int M, bool gemm_rows) {
+// wide: the context's passes have more than kSgMaxRows rows and run on the
+// tile-packed copy (the wide-unit GEMM)
+void set_splits(Model& m, int M, bool gemm_rows, bool wide) {
+  if (wide) {
+    m.s_down = gemm_wide_splits(m.d.hidden, m.d.ffn, num_cus());
+    m.s_o = gemm_wide_splits(m.d.hidden, m.d.q_heads * m.d.head_dim, num_cus());
+    return;
+  }
   const int slots = gemm_rows ? num_cus() * gemm_wgs_per_cu(M) : num_cus();
   m.s_down = gemm_rows ? gemm_down_splits(m.d.hidden, m.d.ffn, slots) : down_splits(M, m.d.ffn, num_cus());
   m.s_o = gemm_rows ? gemm_down_splits(m.d.hidden, m.d.q_heads * m.d.head_dim, slots) : 1;
 }
 
-size_t part_elems_for(const Model& m, int M) {
+size_t part_elems_for(const Model& m, int M, bool wide) {
   // a pass of fewer rows may split the q/k/v GEMM where one of M rows does not
   const int nqkv = (m.d.q_heads + 2 * m.d.kv_heads) * m.d.head_dim;
   size_t qkv = 0;
   for (int r = 1; r <= M; ++r) {
-    const int sq = gemm_qkv_splits(nqkv, m.d.hidden, r, num_cus());
+    const int sq = gemm_qkv_splits_for(nqkv, m.d.hidden, r, num_cus(), wide);
     if (sq > 1) qkv = std::max(qkv, (size_t)sq * r * nqkv);
   }
   return std::max((size_t)std::max({m.s_down, m.s_o, kCondSplits}) * M * m.d.hidden, qkv);
@@ -391,21 +398,25 @@ size_t carve(Ctx& c, const spec_config* cfg, const spec_seq_init* seqs, bool has
   c.cross = c.cond && (cfg->flags & SPEC_FLAG_COND_CROSS) != 0;
   for (int i = 0; i < 3; ++i) c.cond_layers[i] = cfg->cond_layers[i];
   c.gemm_rows = gemm_rows_for(cfg, has_draft, L.M);
-  set_splits(c.tgt, L.M, c.gemm_rows);
+  // passes of more than kSgMaxRows rows never take the packed GEMV, so they
+  // stream the packed copy on the wide-unit GEMM unless the caller asks for
+  // row-major weights
+  c.gemm_wide = c.gemm_rows && L.M > kSgMaxRows && !(cfg->flags & SPEC_FLAG_ROWMAJOR);
+  set_splits(c.tgt, L.M, c.gemm_rows, c.gemm_wide);
   if (has_draft) {
     c.drf.d = cfg->draft;
     c.drf.flat = (cfg->flags & SPEC_FLAG_DRAFT_MROPE) == 0;
-    set_splits(c.drf, L.M, c.gemm_rows);
+    set_splits(c.drf, L.M, c.gemm_rows, c.gemm_wide);
   }
   const spec_dims& t = cfg->target;
   const int H = t.hidden, D = t.head_dim;
   int nqD = t.q_heads * D, F = t.ffn, nq = t.q_heads;
-  size_t part = part_elems_for(c.tgt, L.M);
+  size_t part = part_elems_for(c.tgt, L.M, c.gemm_wide);
   if (has_draft) {
     nqD = std::max(nqD, cfg->draft.q_heads * D);
     F = std::max(F, cfg->draft.ffn);
     nq = std::max(nq, cfg->draft.q_heads);
-    part = std::max(part, part_elems_for(c.drf, L.M));
+    part = std::max(part, part_elems_for(c.drf, L.M, c.gemm_wide));
   }
   Carver cv{base};
   c.st = cv.take<SeqState>(L.B);
