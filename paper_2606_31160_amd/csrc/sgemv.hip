@@ -644,14 +644,29 @@ bool sg_plan(SgJob& j, int epi, int ncu, int lds_limit) {
   if (j.ntiles < 1 || j.ntiles % tpu || j.M < 1 || j.M > kSgMaxRows || j.T < 1 || j.rps < 1 || ncu < 1) return false;
   if ((long long)j.ntiles * j.T * 1024 >= kOut || (long long)j.M * j.ldx * 2 >= kOut) return false;
   // A k-range longer than the workers can hold x for is streamed (x loaded
-  // with the weights, step by step) rather than cut into k-slices: no
-  // partial tiles and no cross-workgroup fixup.
+  // with the weights, step by step), which needs no partial tiles and no
+  // cross-workgroup fixup, unless k-slices share the work evenly (below).
   // x is held in registers while every worker's share of a tile's steps fits
   // its buffer (8 steps, or 9 for the 4096-wide inputs of the paper's
   // backbone); a row's sum is formed the same way in every variant
   j.xs = j.T > kSgWorkers * kSgDepthMax ? 1 : 0;
-  j.dep9 = (!j.xs && j.T > kSgMaxSpan) ? 1 : 0;
-  const int smin = 1;
+  int smin = 1;
+  if (j.xs) {
+    // k-slices short enough for x in registers (at most kSgDepth steps per
+    // worker) instead of streamed x, where the slices' workgroups then share
+    // the units evenly: no x re-read from L2 with every weight block, at the
+    // price of partial tiles (the paper backbone's down projection: 4 slices
+    // of 96 steps, 64 workgroups of 4 tiles each).  The choice depends on the
+    // shape only, so every pass of a context sums a row the same way.
+    const int sx = (j.T + kSgMaxSpan - 1) / kSgMaxSpan;
+    const int gx = ncu / sx;
+    const int units = j.ntiles / tpu;
+    if (ncu % sx == 0 && gx > 0 && gx <= units && units % gx == 0 && (units / gx) <= kSgPendMax) {
+      j.xs = 0;
+      smin = sx;
+    }
+  }
+  j.dep9 = (!j.xs && (j.T + smin - 1) / smin > kSgMaxSpan) ? 1 : 0;
   int S = smin;
   for (int s = smin; s <= 2 * smin; ++s)
     if (ncu % s == 0) {
