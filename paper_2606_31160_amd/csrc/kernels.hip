@@ -1008,7 +1008,7 @@ __global__ __launch_bounds__(NW * 64) void k_attn(AttnArgs a) {
 // the running (max, sum, output) of each row is rescaled when the max grows.
 // grid (groups of ppw pages, kv heads x row blocks, B), 256 threads.
 template <int D>
-__global__ __launch_bounds__(256) void k_attn_pages(AttnArgs a) {
+__global__ __launch_bounds__(256, 3) void k_attn_pages(AttnArgs a) {
   extern __shared__ __align__(16) unsigned char lds[];
   const int grp = blockIdx.x;
   const int kvh = blockIdx.y / a.row_blocks, rb = blockIdx.y % a.row_blocks;
@@ -1111,15 +1111,6 @@ __global__ __launch_bounds__(256) void k_attn_pages(AttnArgs a) {
       for (int t = 0; t < D / 32; ++t) acc = mfma16x16x32(*reinterpret_cast<const u32x4*>(kp + 32 * t), qf[t], acc);
       sc[h] = acc;
     }
-    u32x4 va[2][D / 16];
-#pragma unroll
-    for (int hb = 0; hb < 2; ++hb)
-#pragma unroll
-      for (int dt = 0; dt < D / 16; ++dt) {
-        const bf16_t* vp = Vs + (size_t)(16 * dt + (lane & 15)) * vst + 32 * hb + 4 * g4;
-        const u32x2 lo = *reinterpret_cast<const u32x2*>(vp), hi = *reinterpret_cast<const u32x2*>(vp + 16);
-        va[hb][dt] = u32x4{lo.x, lo.y, hi.x, hi.y};
-      }
     float p[16];
     float pm = -INFINITY;
 #pragma unroll
@@ -1150,8 +1141,14 @@ __global__ __launch_bounds__(256) void k_attn_pages(AttnArgs a) {
     for (int hb = 0; hb < 2; ++hb) {
       const float* ph = p + 8 * hb;
       const u32x4 pb = u32x4{pack2(ph[0], ph[1]), pack2(ph[2], ph[3]), pack2(ph[4], ph[5]), pack2(ph[6], ph[7])};
+      // V^T operands read here, not ahead of the softmax: fewer registers, so
+      // that three workgroups fit a CU and more pages are in flight
 #pragma unroll
-      for (int dt = 0; dt < D / 16; ++dt) o[dt] = mfma16x16x32(va[hb][dt], pb, o[dt]);
+      for (int dt = 0; dt < D / 16; ++dt) {
+        const bf16_t* vp = Vs + (size_t)(16 * dt + (lane & 15)) * vst + 32 * hb + 4 * g4;
+        const u32x2 lo = *reinterpret_cast<const u32x2*>(vp), hi = *reinterpret_cast<const u32x2*>(vp + 16);
+        o[dt] = mfma16x16x32(u32x4{lo.x, lo.y, hi.x, hi.y}, pb, o[dt]);
+      }
     }
     m_run = m_new;
   }
