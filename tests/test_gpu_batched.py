@@ -7,9 +7,12 @@ pass run on the batched-row GEMM, with caches in shuffled KV pages.
     against the oracle's logits over the sequence's own history;
   * 8 tiny scenes with K = 16 and 4 q heads per kv head (136 rows, two
     attention row blocks);
+  * the same 16 scenes with K = 2, 6 and 9 (48, 112 and 160 rows: 3, 7 and 10
+    row blocks of the wide-unit GEMM);
   * 16 scenes of the 16-scene workload's prompt structure (prompts of
     2048..8192 tokens, four camera grids each) at the 7B-class width through
-    one target layer, 144 rows: logits of every sequence against the oracle;
+    one target layer, 144 rows and 48 rows: logits of every sequence against
+    the oracle;
   * the 16-scene workload at full size (28 layers, the 152064-token head,
     one 144-row verify): its shortest- and longest-prompt scenes against the
     oracle;
@@ -128,6 +131,31 @@ def test_sixteen_scenes_one_verify(tiny16, path):
     s = _session(w, page_seed=11, flags=S.PATH_FLAGS[path])
     assert B.spec_debug_path(s.ctx) == path
     _verify_against_oracle(w, s, T, seed=5, check_kv=(0, 9, 15))
+    s.close()
+
+
+@pytest.mark.parametrize("K", [2, 6, 9])
+def test_sixteen_scenes_row_blocks_of_the_wide_gemm(tiny16, K):
+    # 48, 112 and 160 rows: 3, 7 and 10 row blocks of the wide-unit GEMM (the
+    # other tests cover 5 and 9; 10 blocks is the pass-size limit)
+    w, hp, T = tiny16
+    w = w.with_(K=K)
+    assert w.batch * (K + 1) in (48, 112, 160)
+    s = _session(w, page_seed=13)
+    _verify_against_oracle(w, s, T, seed=6 + K, check_kv=(0, 15))
+    s.close()
+
+
+def test_sixteen_scenes_7b_width_one_layer_three_row_blocks():
+    # 48 rows at the 7B-class width: the k-split q/k/v, o and down launches of
+    # the wide-unit GEMM with one x block per wave
+    c5 = W.get("C5")
+    w = W.get("C2").with_(seqs=c5.seqs, p_accept=c5.p_accept, draft=None, K=2)
+    assert w.batch * (w.K + 1) == 48 and w.target.hidden == 3584
+    src = W.DeviceWeights(w)
+    T, _ = S.oracle_decoders(w, src, cache_weights=True)
+    s = _session(w, source="device", provider=src, page_seed=15)
+    _verify_against_oracle(w, s, T, seed=8, check_kv=(0, 15), kv=S.device_kv)
     s.close()
 
 
