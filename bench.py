@@ -435,6 +435,28 @@ def pmc_pass(rounds, K):
     log("pmc pass done")
 
 
+def pmc_pass_batched(rounds, K):
+    """Verifies of the 16-scene workload (144 rows, random drafts, shuffled KV
+    pages) launched kernel by kernel, for counter collection; prints one line
+    per verify, then the calibration copy."""
+    import torch
+    import workloads as W
+    from paper_2606_31160_amd import binding as B
+    from paper_2606_31160_amd.harness import Session
+    w = W.get("C5").with_(draft=None, max_new_tokens=rounds * (K + 1) + 8)
+    s = Session(w, source="device", provider=W.DeviceWeights(w), page_seed=5, flags=B.SPEC_FLAG_NO_GRAPHS)
+    rng = np.random.default_rng(6)
+    for r in range(rounds):
+        d = torch.tensor(rng.integers(0, w.vocab, size=(w.batch, K)), dtype=torch.int32, device="cuda")
+        B.spec_verify(s.ctx, d.data_ptr(), 0)
+        B.spec_commit(s.ctx, 0, 0, 0, 0)
+        torch.cuda.synchronize()
+        log(f"verify {r} done")
+    s.close()
+    calibration_copy()
+    log("pmc pass done")
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -447,6 +469,9 @@ def main():
     ap.add_argument("--pmc-pass", type=int, default=0, metavar="R",
                     help="counter-collection pass: R speculative rounds with random drafts on direct "
                          "launches (no timing, no JSON line), then the calibration copy")
+    ap.add_argument("--pmc-pass-batched", type=int, default=0, metavar="R",
+                    help="counter-collection pass of the 16-scene workload: R 144-row verifies with random drafts "
+                         "on direct launches (no timing, no JSON line), then the calibration copy")
     args = ap.parse_args()
     if args.gpus != 1:
         print(json.dumps({"error": "one GPU only: independent scenes would shard across GPUs with no "
@@ -463,6 +488,9 @@ def main():
     K = 8
     if args.pmc_pass:
         pmc_pass(args.pmc_pass, K)
+        return
+    if args.pmc_pass_batched:
+        pmc_pass_batched(args.pmc_pass_batched, K)
         return
     n_after_free = 6
     rounds_total = args.warmup + args.steps + 3 + n_after_free
