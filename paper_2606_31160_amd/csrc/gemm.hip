@@ -1,12 +1,13 @@
-// Batched-row GEMM on MFMA for passes of more than kThinRows rows (several
-// sequences verified together), and of 17..kThinRows rows whose width the
-// thin GEMV cannot stage (one sequence with K = 16 at hidden 4096): y[m][n] =
-// sum_k x[m][k] W[n][k] for up to SPEC_MAX_ROWS rows, with the same fused
-// epilogues as the thin GEMV kernels (1/rms row scale, rotary + paged KV
-// append, residual + next-norm input, SwiGLU, per-tile argmax, or k-split
-// partial sums).
+// Batched-row GEMMs on MFMA: y[m][n] = sum_k x[m][k] W[n][k] for up to
+// SPEC_MAX_ROWS rows, with the same fused epilogues as the thin GEMV kernels
+// (1/rms row scale, rotary + paged KV append, residual + next-norm input,
+// SwiGLU, per-tile argmax, or k-split partial sums).  Two kernels:
+//   * k_gemm_wide (below k_gemm): passes of more than 32 rows over the
+//     tile-packed weights (several sequences verified together);
+//   * k_gemm: row-major weights (SPEC_FLAG_ROWMAJOR) for passes of more than
+//     16 rows, and 17..32-row passes whose width the thin GEMV cannot stage.
 //
-// A workgroup owns kGemmTiles = 4 output tiles of 16 columns and the k-range
+// k_gemm: a workgroup owns kGemmTiles = 4 output tiles of 16 columns and the k-range
 // of split blockIdx.y, walked in chunks of 32 * kSteps columns (kSteps
 // 32-wide MFMA steps; kSteps = 4 or 2 by the row count).  It has two kinds
 // of waves:

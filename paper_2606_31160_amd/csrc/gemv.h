@@ -63,8 +63,11 @@ constexpr int kGemmTiles = 4;   // 16-column output tiles per GEMM workgroup
 size_t gemm_lds_bytes(int M);
 // Raises the dynamic LDS limit of every GEMM instantiation that fits `limit` bytes.
 void gemm_set_attributes(int limit);
-// y = x W^T over g.M rows (kThinRows < M <= SPEC_MAX_ROWS) with epilogue
-// `epi`; grid (ceil(N / 64), g.splits).  Only EPI_STORE may use k-splits.
+// y = x W^T over g.M rows (kSgMaxRowsGemm < M <= SPEC_MAX_ROWS) with epilogue
+// `epi`.  Over the tile-packed copy (g.pw) with more than 32 rows: the
+// wide-unit kernel, one workgroup per CU for SwiGLU and the LM head, grid
+// (ceil(N / 256), g.splits) for EPI_STORE; otherwise k_gemm, grid
+// (ceil(N / 64), g.splits).  Only EPI_STORE may use k-splits.
 hipError_t gemm_launch(int epi, const GemvArgs& g, hipStream_t s, hipEvent_t e0, hipEvent_t e1);
 // k-splits of an EPI_STORE GEMM (the down projection) over N outputs and Kd inputs.
 int gemm_down_splits(int N, int Kd, int ncu);
