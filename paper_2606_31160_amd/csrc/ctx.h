@@ -163,6 +163,7 @@ struct Ctx {
   bool gemm_rows = false;              // layered row-major passes run on the batched-row GEMM
   bool gemm_pk = false;                // ... which streams the tile-packed weight copy
   bool gemm_wide = false;              // ... on the wide-unit kernel (passes of more than 32 rows)
+  bf16_t* xgp = nullptr;               // wide contexts: step-major copy of xg [H/32][M][32] for that kernel
   bool poisoned = false;
   std::string err;
 

@@ -489,8 +489,10 @@ __global__ __launch_bounds__(kWideWaves * 64, 1) void k_gemm_wide(GemvArgs a) {
   const int nch = (u1 - u0 + kWideTiles / 2 - 1) / (kWideTiles / 2);
   const int cu = nch > 0 ? (u1 - u0 + nch - 1) / nch : 1;   // units per chunk
   int tile0 = 0, tend = 0;   // this wave's first tile, the chunk's end tile
-  const __amdgpu_buffer_rsrc_t rx =
-      __builtin_amdgcn_make_buffer_rsrc(const_cast<bf16_t*>(a.x), 0, M * a.ldx * 2, kRsrcWord3);
+  // step-major x spans whole 32-wide steps (its buffer is padded to them:
+  // columns past Kd meet zero weight columns)
+  const __amdgpu_buffer_rsrc_t rx = __builtin_amdgcn_make_buffer_rsrc(const_cast<bf16_t*>(a.x), 0,
+                                                                      a.xpk ? T * M * 64 : M * a.ldx * 2, kRsrcWord3);
   unsigned char* ring = lds + (size_t)kg * NB * MB * 1024;           // [NB][MB] blocks of 1 KB
   unsigned char* dummy = lds + (size_t)2 * NB * MB * 1024;           // target of the spare x loads
   float* rms_part = reinterpret_cast<float*>(dummy + 1024);          // [slices][ROWS]
@@ -505,7 +507,18 @@ __global__ __launch_bounds__(kWideWaves * 64, 1) void k_gemm_wide(GemvArgs a) {
     live_s[m] = lv;
   }
 
-  const int lane_x = ((lane & 15) * a.ldx + 8 * (lane >> 4)) * 2;
+  // x operand of block b at step st: byte offset xbase[j] + st * xstride;
+  // lane l reads row 16 b + (l & 15), 16 bytes at column 32 st + 8 (l >> 4)
+  // (MFMA operand order).  Row-major x: 16 rows of 64 bytes ldx apart.
+  // Step-major x (xpk, [Kd/32][M][32]): the block is one contiguous 1 KB run.
+  const int xstride = a.xpk ? M * 64 : 64;
+  int xbase[XPW];
+#pragma unroll
+  for (int j = 0; j < XPW; ++j) {
+    const int b = cg + kWideCg * j;
+    const int r = 16 * b + (lane & 15);
+    xbase[j] = a.xpk ? r * 64 + 16 * (lane >> 4) : (r * a.ldx + 8 * (lane >> 4)) * 2;
+  }
   const int lane_w = 16 * lane;
   // Offsets past a k-group's range or the last tile are ORed with kOut (a
   // wave-uniform scalar select): every offset stays below 2^31, so the result
@@ -519,7 +532,7 @@ __global__ __launch_bounds__(kWideWaves * 64, 1) void k_gemm_wide(GemvArgs a) {
     for (int j = 0; j < XPW; ++j) {
       const int b = cg + kWideCg * j;
       const int ob = b < MB ? oob : kOut;
-      lds_load16(rx, b < MB ? slot + b * 1024 : dummy, (lane_x + (b * 16 * a.ldx + st * 32) * 2) | ob);
+      lds_load16(rx, b < MB ? slot + b * 1024 : dummy, (xbase[j] + st * xstride) | ob);
     }
   };
   // The weight loads are written as inline assembly, and waited for by hand
@@ -677,7 +690,8 @@ __global__ __launch_bounds__(kWideWaves * 64, 1) void k_gemm_wide(GemvArgs a) {
           const float g = acc[2 * j][mb][i] * r, up = acc[2 * j + 1][mb][i] * r;
           o[i] = live_s[m] ? g / (1.f + expf(-g)) * up : 0.f;
         }
-        *reinterpret_cast<u32x2*>(a.u + (size_t)m * F + f) = u32x2{pack2(o[0], o[1]), pack2(o[2], o[3])};
+        const size_t at = a.upk ? ((size_t)(f >> 5) * M + m) * 32 + (f & 31) : (size_t)m * F + f;
+        *reinterpret_cast<u32x2*>(a.u + at) = u32x2{pack2(o[0], o[1]), pack2(o[2], o[3])};
       }
     }
   } else {   // EPI_ARGMAX: per tile and row, the (max, index) of its 16 logits
@@ -850,9 +864,11 @@ hipError_t gemm_launch(int epi, const GemvArgs& g, hipStream_t s, hipEvent_t e0,
   // and for the k-split partial sums of the other projections
   {
     const int mb = (g.M + 15) / 16;
-    if (g.pw && g.M > kSgMaxRows && mb <= 10 && (g.N / kTile) % 2 == 0 &&
-        (epi == EPI_STORE || ((epi == EPI_SWIGLU || epi == EPI_ARGMAX) && g.splits == 1)) &&
-        wide_lds_bytes(mb, epi == EPI_STORE ? 0 : g.H) <= (size_t)gemv_lds_limit()) {
+    const bool wide = g.pw && g.M > kSgMaxRows && mb <= 10 && (g.N / kTile) % 2 == 0 &&
+                      (epi == EPI_STORE || ((epi == EPI_SWIGLU || epi == EPI_ARGMAX) && g.splits == 1)) &&
+                      wide_lds_bytes(mb, epi == EPI_STORE ? 0 : g.H) <= (size_t)gemv_lds_limit();
+    if (g.xpk && !wide) return hipErrorInvalidValue;   // only the wide kernel reads step-major x
+    if (wide) {
       if (epi == EPI_STORE) return launch_wide<EPI_STORE>(g, s, e0, e1);
       return epi == EPI_SWIGLU ? launch_wide<EPI_SWIGLU>(g, s, e0, e1) : launch_wide<EPI_ARGMAX>(g, s, e0, e1);
     }

@@ -24,8 +24,9 @@ struct GemvArgs {
   const bf16_t* pw;      // GEMM only: the tile-packed copy of these weights ([N/16][steps] blocks of
                          // 1 KB, sgemv.h; gate/up as gate, up tile pairs), or null to read w
   int N, Kd;
-  const bf16_t* x;       // [M][ldx]
+  const bf16_t* x;       // [M][ldx], or step-major [Kd/32][M][32] (xpk)
   int ldx, M, splits;
+  int xpk;               // x is step-major: a 32-wide step's rows are one contiguous run (wide-unit GEMM only)
   const SeqState* st;
   int rps;               // rows per sequence
   int mpad;              // row stride of ss / amax
@@ -45,7 +46,8 @@ struct GemvArgs {
   bf16_t* xg;            // [M][N] bf16(x * gain)
   float* ss_out;         // [N/16][mpad] sums of x^2
   // EPI_SWIGLU
-  bf16_t* u;             // [M][N/2]
+  bf16_t* u;             // [M][N/2], or step-major [N/64][M][32] (upk, wide-unit GEMM only)
+  int upk;
   // EPI_ARGMAX
   float* amax_v;         // [N/16][mpad]
   int32_t* amax_i;

@@ -667,6 +667,7 @@ struct FinishArgs {
   const bf16_t* gain;
   bf16_t* xg;
   float* ss;             // [H/16][mpad]
+  bf16_t* xgp;           // null, or a step-major copy of xg: [H/32][M][32] (all rows; not with select_last)
 };
 
 __global__ __launch_bounds__(256) void k_down_finish(FinishArgs p) {
@@ -686,7 +687,9 @@ __global__ __launch_bounds__(256) void k_down_finish(FinishArgs p) {
   for (int o = 1; o < 16; o <<= 1) sq += __shfl_xor(sq, o);
   const int out = p.select_last ? b : m;
   if (p.select_last && j != count - 1) return;
-  p.xg[(size_t)out * p.H + n] = f2bf(x * bf2f(p.gain[n]));
+  const bf16_t xb = f2bf(x * bf2f(p.gain[n]));
+  p.xg[(size_t)out * p.H + n] = xb;
+  if (p.xgp && !p.select_last) p.xgp[((size_t)(n >> 5) * p.M + m) * 32 + (n & 31)] = xb;
   if ((n & 15) == 0) p.ss[(size_t)(n >> 4) * p.mpad + out] = sq;
 }
 
@@ -1720,6 +1723,10 @@ hipError_t launch_qkv_rm(Ctx& c, Model& m, int li, bf16_t* kc, bf16_t* vt) {
     // partial sums, then the norm, rotation and cache append in k_qkv_finish
     g.splits = sq;
     g.out = c.part;
+    if (pk && c.xgp && li > 0) {   // the step-major copy the previous layer's down finish wrote
+      g.x = c.xgp;
+      g.xpk = 1;
+    }
     CK(gemm_run(c, EPI_STORE, g, SPEC_KERNEL_QKV, gemv_bytes(g.N, H, M, 4.0 * sq)));
     QkvFinishArgs p{c.st, c.part, sq, M, g.N, c.R, c.Mpad, H, d.rms_eps, c.ss, c.rcs, c.pt,
                     nq, nkv, D, c.pps, c.q, kc, vt};
@@ -1772,7 +1779,7 @@ hipError_t run_layer(Ctx& c, Model& m, int li, const bf16_t* next_gain, bool sel
       g.splits = m.s_o;
       g.out = c.part;
       CK(gemm_run(c, EPI_STORE, g, SPEC_KERNEL_O, gemv_bytes(H, nq * D, M, 4.0 * m.s_o)));
-      FinishArgs p{c.st, c.part, m.s_o, M, c.R, H, c.Mpad, 0, c.x, w.ffn_norm, c.xg, c.ss};
+      FinishArgs p{c.st, c.part, m.s_o, M, c.R, H, c.Mpad, 0, c.x, w.ffn_norm, c.xg, c.ss, c.xgp};
       Timed t(c, SPEC_KERNEL_OTHER, 0);
       hipExtLaunchKernelGGL(k_down_finish, dim3((H + 255) / 256, M), dim3(256), 0, S(c), t.e0, t.e1, 0, p);
       CK(hipGetLastError());
@@ -1796,6 +1803,11 @@ hipError_t run_layer(Ctx& c, Model& m, int li, const bf16_t* next_gain, bool sel
     g.eps = d.rms_eps;
     g.u = c.u;
     g.pw = pk ? pk + m.pk_gu : nullptr;
+    if (pk && c.xgp) {   // the wide-unit GEMM reads the step-major copy the o finish wrote
+      g.x = c.xgp;
+      g.xpk = 1;
+      g.upk = 1;         // and writes u step-major for the down projection
+    }
     if (c.gemm_rows)
       CK(gemm_run(c, EPI_SWIGLU, g, SPEC_KERNEL_GATEUP, gemv_bytes(2 * F, H, M, 1.0)));
     else
@@ -1816,6 +1828,7 @@ hipError_t run_layer(Ctx& c, Model& m, int li, const bf16_t* next_gain, bool sel
       g.splits = m.s_down;
       g.out = c.part;
       g.pw = pk ? pk + m.pk_dn : nullptr;
+      g.xpk = (pk && c.xgp) ? 1 : 0;   // u as the wide-unit gate/up GEMM wrote it
       if (c.gemm_rows) {
         CK(gemm_run(c, EPI_STORE, g, SPEC_KERNEL_DOWN, gemv_bytes(H, F, M, 4.0 * m.s_down)));
       } else {
@@ -1823,7 +1836,7 @@ hipError_t run_layer(Ctx& c, Model& m, int li, const bf16_t* next_gain, bool sel
         CK(gemv_launch_p<EPI_STORE>(c, g, per_split * m.s_down, SPEC_KERNEL_DOWN, gemv_bytes(H, F, M, 4.0 * m.s_down)));
       }
     }
-    FinishArgs p{c.st, c.part, S_down, M, c.R, H, c.Mpad, select_last ? 1 : 0, c.x, next_gain, c.xg, c.ss};
+    FinishArgs p{c.st, c.part, S_down, M, c.R, H, c.Mpad, select_last ? 1 : 0, c.x, next_gain, c.xg, c.ss, c.xgp};
     Timed t(c, SPEC_KERNEL_OTHER, 0);
     hipExtLaunchKernelGGL(k_down_finish, dim3((H + 255) / 256, M), dim3(256), 0, S(c), t.e0, t.e1, 0, p);
     CK(hipGetLastError());
@@ -2218,6 +2231,10 @@ hipError_t launch_forward(Ctx& c, PassMode mode) {
     const double bytes = gemv_bytes(c.V, d.hidden, g.M, 0.0) + 8.0 * (c.V / kTile) * g.M;
     if (g.M > kThinRows || (!draft && c.gemm_rows)) {
       g.pw = c.gemm_pk ? c.pk_head : nullptr;
+      if (!draft && g.pw && c.xgp) {   // the step-major copy the last down finish wrote
+        g.x = c.xgp;
+        g.xpk = 1;
+      }
       CK(gemm_run(c, EPI_ARGMAX, g, SPEC_KERNEL_LMHEAD, bytes));
     }
     else

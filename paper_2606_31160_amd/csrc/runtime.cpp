@@ -431,6 +431,7 @@ size_t carve(Ctx& c, const spec_config* cfg, const spec_seq_init* seqs, bool has
   c.o = cv.take<bf16_t>((size_t)L.Mpad * nqD);
   c.u = cv.take<bf16_t>((size_t)L.Mpad * align_up(F, 32));   // row-major, or step-major for the packed path
   c.xg = cv.take<bf16_t>((size_t)L.Mpad * H);
+  c.xgp = (c.gemm_wide && H % 32 == 0) ? cv.take<bf16_t>((size_t)L.Mpad * H) : nullptr;
   c.ss = cv.take<float>((size_t)(H / kTile) * L.Mpad);
   c.rcs = cv.take<float2>((size_t)L.Mpad * (D / 2));
   c.part = cv.take<float>(part);
