@@ -7,8 +7,9 @@ pass run on the batched-row GEMM, with caches in shuffled KV pages.
     against the oracle's logits over the sequence's own history;
   * 8 tiny scenes with K = 16 and 4 q heads per kv head (136 rows, two
     attention row blocks);
-  * the same 16 scenes with K = 2, 6 and 9 (48, 112 and 160 rows: 3, 7 and 10
-    row blocks of the wide-unit GEMM);
+  * the same 16 scenes with K = 6 and 9 (112 and 160 rows: 7 and 10 row
+    blocks of the wide-unit GEMM), and passes of 32, 33 and 48 rows (the
+    boundary of the packed GEMV);
   * 16 scenes of the 16-scene workload's prompt structure (prompts of
     2048..8192 tokens, four camera grids each) at the 7B-class width through
     one target layer, 144 rows and 48 rows: logits of every sequence against
@@ -134,15 +135,31 @@ def test_sixteen_scenes_one_verify(tiny16, path):
     s.close()
 
 
-@pytest.mark.parametrize("K", [2, 6, 9])
+@pytest.mark.parametrize("K", [6, 9])
 def test_sixteen_scenes_row_blocks_of_the_wide_gemm(tiny16, K):
-    # 48, 112 and 160 rows: 3, 7 and 10 row blocks of the wide-unit GEMM (the
-    # other tests cover 5 and 9; 10 blocks is the pass-size limit)
+    # 112 and 160 rows: 7 and 10 row blocks of the wide-unit GEMM (the other
+    # tests cover 3 at 7B width, 4 at the paper width, 5 and 9; 10 blocks is
+    # the pass-size limit)
     w, hp, T = tiny16
     w = w.with_(K=K)
-    assert w.batch * (K + 1) in (48, 112, 160)
+    assert w.batch * (K + 1) in (112, 160)
     s = _session(w, page_seed=13)
     _verify_against_oracle(w, s, T, seed=6 + K, check_kv=(0, 15))
+    s.close()
+
+
+@pytest.mark.parametrize("B,K,path", [(16, 1, "packed"), (2, 15, "packed"), (3, 10, "rowmajor"),
+                                      (16, 2, "rowmajor")])
+def test_pass_size_boundary_of_the_packed_gemv(tiny16, B, K, path):
+    # 32 rows (16 x 2 and 2 x 16): the packed GEMV with two full row blocks;
+    # 33 and 48 rows: past it, which at this width the row-major thin GEMV
+    # stages (wider models take the wide-unit GEMM there)
+    w, hp, T = tiny16
+    w = w.with_(K=K, seqs=w.seqs[:B], p_accept=w.p_accept[:B])
+    s = _session(w, page_seed=16)
+    from paper_2606_31160_amd import binding as B_
+    assert B_.spec_debug_path(s.ctx) == path
+    _verify_against_oracle(w, s, T, seed=9 + K, check_kv=(0, B - 1))
     s.close()
 
 
