@@ -411,16 +411,20 @@ __global__ __launch_bounds__(threads_for(MB)) void k_gemm(GemvArgs a) {
 // ---------------------------------------------------------------------------
 // Wide-unit GEMM over the tile-packed weights for passes of 33 to 160 rows
 // (3 to 10 row blocks): the gate/up and LM-head projections in one launch, and
-// the q/k/v, o and down projections as k-split partial sums.  A workgroup owns
-// kWideTiles = 16 output tiles (256 columns) and the k-range of split
-// blockIdx.y.  Its 8 waves are 4 column groups x 2 k-groups: wave (cg, kg)
+// the q/k/v, o and down projections as k-split partial sums.  Gate/up and the
+// LM head run one workgroup per CU, each over an even, contiguous share of the
+// tile pairs walked in chunks of at most kWideTiles = 16 tiles (256 columns);
+// a k-split launch gives each workgroup 16 tiles and the k-range of split
+// blockIdx.y.  The 8 waves are 4 column groups x 2 k-groups: wave (cg, kg)
 // multiplies tiles 4 cg .. 4 cg + 3 over the kg-th half of the k-range, so
 // each x operand it reads from LDS feeds 4 MFMAs and each weight block MB of
 // them, and the two k-groups keep two independent streams of loads in flight.
 // Per 32-wide k-step each k-group stages the x operands of all rows by
 // buffer-to-LDS loads straight in MFMA operand order (block rb of a step: 16
 // rows x 32 columns, lane l's 16 bytes at 16 l) into its own ring of D + 1
-// slots, D steps ahead; weights go to registers the same depth ahead.  One
+// slots, D steps ahead; weights go to registers the same depth ahead.  x is
+// read from a step-major copy where the producer wrote one (each block then
+// one contiguous 1 KB run), else from row-major rows.  One
 // barrier per step; its wait count is set by hand (every wave issues the same
 // loads per step: its share of its k-group's x blocks, then its 4 weight
 // blocks), so that every step in flight stays in flight.  A load past its
