@@ -1068,8 +1068,10 @@ __global__ __launch_bounds__(256, 3) void k_attn_pages(AttnArgs a) {
 #pragma unroll
     for (int u = 0; u < PER_T; ++u) {
       const int i = threadIdx.x + 256 * u;
-      kr[u] = ld16(Kb + (size_t)(i / (D / 8)) * D + 8 * (i % (D / 8)));
-      vr[u] = ld16(Vb + (size_t)(i / per_row) * kAttnChunk + 8 * (i % per_row));
+      // non-temporal: the 16 scenes' keys and values (~170 MB a layer) are
+      // read once per pass and do not fit the last-level cache
+      kr[u] = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(Kb + (size_t)(i / (D / 8)) * D + 8 * (i % (D / 8))));
+      vr[u] = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(Vb + (size_t)(i / per_row) * kAttnChunk + 8 * (i % per_row)));
     }
   };
   auto stage = [&](int k0, int k1) {   // registers -> LDS; values past the valid keys as zeros
