@@ -798,6 +798,38 @@ struct AttnArgs {
   int ppw;               // k_attn_pages: pages per split (workgroup)
 };
 
+// LDS tiles of a page: keys [chunk][D + kAttnPadK] and values transposed
+// [D][chunk + kAttnPadV].  A 16-byte LDS read is served eight lanes at a
+// time, in the groups lanes 0-3 with 20-23, 4-7 with 16-19, 8-11 with 28-31
+// and 12-15 with 24-27 (the same in the upper half).  An MFMA operand read
+// takes row (lane & 15) and 16-byte column group (lane >> 4); with rows 32
+// bytes past a multiple of 128 bytes, each group's eight reads fall in
+// distinct banks.  (Rows 16 bytes past: four times the bank-conflict cycles
+// in the multi-page kernel.)
+constexpr int kAttnPadK = 16, kAttnPadV = 16;
+
+// Store the 8 values (keys slot .. slot + 7 of value row d, as loaded from the
+// page; keys at or past k1 as zeros) into the value tile.  Within each 32-key
+// half of a row, key 16 hi + 4 g + e sits at 8 g + 4 hi + e: the eight keys a
+// lane of group g contracts in that half (4 g + e and 16 + 4 g + e) are then
+// one 16-byte read.  v8 = (slot - k0) / 8.
+__device__ __forceinline__ void attn_stage_values(bf16_t* vrow, int v8, int slot, int k1, u32x4 v) {
+  if (slot >= k1) {
+    v = u32x4{0, 0, 0, 0};
+  } else if (slot + 8 > k1) {                       // ragged end of the valid keys
+    uint32_t w[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+    for (int e = 0; e < 8; ++e)
+      if (slot + e >= k1) w[e >> 1] &= (e & 1) ? 0x0000FFFFu : 0xFFFF0000u;
+    v = u32x4{w[0], w[1], w[2], w[3]};
+  }
+  // keys 8 v8 .. 8 v8 + 3 are group 2 (v8 & 1) of half-row (v8 >> 1) & 1, the
+  // next four group 2 (v8 & 1) + 1
+  bf16_t* vd = vrow + 32 * (v8 >> 2) + 16 * (v8 & 1) + 4 * ((v8 >> 1) & 1);
+  *reinterpret_cast<u32x2*>(vd) = u32x2{v.x, v.y};
+  *reinterpret_cast<u32x2*>(vd + 8) = u32x2{v.z, v.w};
+}
+
 template <int D, bool RO, int NW>
 __device__ __forceinline__ void attn_partials(const AttnArgs& a, unsigned char* lds) {
   constexpr int NT = NW * 64;   // threads: NW waves of 16 query rows each
@@ -861,13 +893,12 @@ __device__ __forceinline__ void attn_partials(const AttnArgs& a, unsigned char* 
     for (int h = 0; h < 4; ++h) cw[h] = *reinterpret_cast<const uint32_t*>(cp + 16 * h);
   }
 
-  // Stage the chunk once for all waves: keys [chunk][D + 8] and values
-  // transposed [D][chunk + 8] (the pads spread rows over the LDS banks).  The
-  // whole page is loaded (its slots past k1 hold stale data): keys there only
-  // meet masked scores, values there are stored as zeros.  Every load of the
-  // thread is issued before the first LDS store so that their latencies
-  // overlap, and unconditionally so that no branch splits them.
-  const int kst = D + 8, vst = a.chunk + 8;
+  // Stage the chunk once for all waves.  The whole page is loaded (its slots
+  // past k1 hold stale data): keys there only meet masked scores, values there
+  // are stored as zeros.  Every load of the thread is issued before the first
+  // LDS store so that their latencies overlap, and unconditionally so that no
+  // branch splits them.
+  const int kst = D + kAttnPadK, vst = a.chunk + kAttnPadV;
   bf16_t* Ks = reinterpret_cast<bf16_t*>(lds);
   bf16_t* Vs = Ks + (size_t)a.chunk * kst;
   {
@@ -892,18 +923,7 @@ __device__ __forceinline__ void attn_partials(const AttnArgs& a, unsigned char* 
       const int key = i / (D / 8), c8 = i % (D / 8);
       *reinterpret_cast<u32x4*>(Ks + (size_t)key * kst + 8 * c8) = kr[u];
       const int d = i / per_row, v8 = i % per_row;
-      const int slot = k0 + 8 * v8;
-      u32x4 v = vr[u];
-      if (slot >= k1) {
-        v = u32x4{0, 0, 0, 0};
-      } else if (slot + 8 > k1) {                   // ragged end of the valid keys
-        uint32_t w[4] = {v.x, v.y, v.z, v.w};
-#pragma unroll
-        for (int e = 0; e < 8; ++e)
-          if (slot + e >= k1) w[e >> 1] &= (e & 1) ? 0x0000FFFFu : 0xFFFF0000u;
-        v = u32x4{w[0], w[1], w[2], w[3]};
-      }
-      *reinterpret_cast<u32x4*>(Vs + (size_t)d * vst + 8 * v8) = v;
+      attn_stage_values(Vs + (size_t)d * vst, v8, k0 + 8 * v8, k1, vr[u]);
     }
   }
   __syncthreads();
@@ -931,9 +951,7 @@ __device__ __forceinline__ void attn_partials(const AttnArgs& a, unsigned char* 
   for (int hb = 0; hb < 2; ++hb)
 #pragma unroll
     for (int dt = 0; dt < D / 16; ++dt) {
-      const bf16_t* vp = Vs + (size_t)(16 * dt + (lane & 15)) * vst + 32 * hb + 4 * g4;
-      const u32x2 lo = *reinterpret_cast<const u32x2*>(vp), hi = *reinterpret_cast<const u32x2*>(vp + 16);
-      va[hb][dt] = u32x4{lo.x, lo.y, hi.x, hi.y};
+      va[hb][dt] = *reinterpret_cast<const u32x4*>(Vs + (size_t)(16 * dt + (lane & 15)) * vst + 32 * hb + 8 * g4);
     }
   float p[16];
   float m_run = -INFINITY;
@@ -1010,6 +1028,7 @@ __global__ __launch_bounds__(NW * 64) void k_attn(AttnArgs a) {
 // keys and values are loaded while this one's scores and products run, and
 // the running (max, sum, output) of each row is rescaled when the max grows.
 // grid (groups of ppw pages, kv heads x row blocks, B), 256 threads.
+
 template <int D>
 __global__ __launch_bounds__(256, 3) void k_attn_pages(AttnArgs a) {
   extern __shared__ __align__(16) unsigned char lds[];
@@ -1053,7 +1072,7 @@ __global__ __launch_bounds__(256, 3) void k_attn_pages(AttnArgs a) {
 #pragma unroll
     for (int t = 0; t < D / 32; ++t) qf[t] = ld16(qp + 32 * t);
   }
-  const int kst = D + 8, vst = kAttnChunk + 8;
+  const int kst = D + kAttnPadK, vst = kAttnChunk + kAttnPadV;
   bf16_t* Ks = reinterpret_cast<bf16_t*>(lds);
   bf16_t* Vs = Ks + (size_t)kAttnChunk * kst;
   constexpr int PER_T = kAttnChunk * D / 8 / 256;   // 16-byte vectors per thread and operand
@@ -1080,18 +1099,7 @@ __global__ __launch_bounds__(256, 3) void k_attn_pages(AttnArgs a) {
       const int i = threadIdx.x + 256 * u;
       *reinterpret_cast<u32x4*>(Ks + (size_t)(i / (D / 8)) * kst + 8 * (i % (D / 8))) = kr[u];
       const int d = i / per_row, v8 = i % per_row;
-      const int slot = k0 + 8 * v8;
-      u32x4 v = vr[u];
-      if (slot >= k1) {
-        v = u32x4{0, 0, 0, 0};
-      } else if (slot + 8 > k1) {
-        uint32_t w[4] = {v.x, v.y, v.z, v.w};
-#pragma unroll
-        for (int e = 0; e < 8; ++e)
-          if (slot + e >= k1) w[e >> 1] &= (e & 1) ? 0x0000FFFFu : 0xFFFF0000u;
-        v = u32x4{w[0], w[1], w[2], w[3]};
-      }
-      *reinterpret_cast<u32x4*>(Vs + (size_t)d * vst + 8 * v8) = v;
+      attn_stage_values(Vs + (size_t)d * vst, v8, k0 + 8 * v8, k1, vr[u]);
     }
   };
 
@@ -1150,9 +1158,8 @@ __global__ __launch_bounds__(256, 3) void k_attn_pages(AttnArgs a) {
       // that three workgroups fit a CU and more pages are in flight
 #pragma unroll
       for (int dt = 0; dt < D / 16; ++dt) {
-        const bf16_t* vp = Vs + (size_t)(16 * dt + (lane & 15)) * vst + 32 * hb + 4 * g4;
-        const u32x2 lo = *reinterpret_cast<const u32x2*>(vp), hi = *reinterpret_cast<const u32x2*>(vp + 16);
-        o[dt] = mfma16x16x32(u32x4{lo.x, lo.y, hi.x, hi.y}, pb, o[dt]);
+        const bf16_t* vp = Vs + (size_t)(16 * dt + (lane & 15)) * vst + 32 * hb + 8 * g4;
+        o[dt] = mfma16x16x32(*reinterpret_cast<const u32x4*>(vp), pb, o[dt]);
       }
     }
     m_run = m_new;
@@ -1175,7 +1182,7 @@ __global__ __launch_bounds__(256, 3) void k_attn_pages(AttnArgs a) {
 
 
 size_t attn_lds_bytes(int chunk, int D) {
-  return ((size_t)chunk * (D + 8) + (size_t)D * (chunk + 8)) * sizeof(bf16_t);
+  return ((size_t)chunk * (D + kAttnPadK) + (size_t)D * (chunk + kAttnPadV)) * sizeof(bf16_t);
 }
 
 // Merge the splits of each (row, q head): o = sum_s 2^(m_s - M) O_s / sum_s
