@@ -1015,8 +1015,11 @@ __device__ __forceinline__ void attn_partials(const AttnArgs& a, unsigned char* 
   }
 }
 
+// The 8-wave form is held to 6 waves per SIMD (80 registers), three
+// workgroups per CU: a 36-layer backbone's 65 pages x 8 kv heads then fit the
+// chip at once instead of leaving 8 workgroups for a second round.
 template <int D, bool RO, int NW>
-__global__ __launch_bounds__(NW * 64) void k_attn(AttnArgs a) {
+__global__ __launch_bounds__(NW * 64, (NW == 8 && !RO) ? 6 : 1) void k_attn(AttnArgs a) {
   extern __shared__ __align__(16) unsigned char lds[];
   attn_partials<D, RO, NW>(a, lds);
 }
