@@ -385,11 +385,12 @@ size_t carve(Ctx& c, const spec_config* cfg, const spec_seq_init* seqs, bool has
   c.attn_chunk = L.chunk;
   c.ncu = num_cus();
   c.attn_splits = L.splits;
-  // one page per attention workgroup gives a pass over a few sequences
-  // enough workgroups; from 8 sequences on, four pages per workgroup (the
-  // choice depends on the batch only, so every pass of a context groups the
-  // attention sums the same way)
-  c.attn_ppw = L.B >= 8 ? 4 : 1;
+  // one page per attention workgroup gives a pass over one sequence of 4 kv
+  // heads enough workgroups; with 8 or more (sequence, kv head) pairs three
+  // pages per workgroup (a third of the partials to merge), from 8 sequences
+  // on four.  The choice depends on the batch and the target's kv heads only,
+  // so every pass of a context groups the attention sums the same way.
+  c.attn_ppw = L.B >= 8 ? 4 : (L.B * cfg->target.kv_heads >= 8 ? 3 : 1);
   c.tgt.d = cfg->target;
   c.tgt.flat = false;
   c.block_draft = has_draft && (cfg->flags & SPEC_FLAG_BLOCK_DRAFT) != 0;
