@@ -1016,8 +1016,8 @@ __device__ __forceinline__ void attn_partials(const AttnArgs& a, unsigned char* 
 }
 
 // The 8-wave form is held to 6 waves per SIMD (80 registers), three
-// workgroups per CU: a 36-layer backbone's 65 pages x 8 kv heads then fit the
-// chip at once instead of leaving 8 workgroups for a second round.
+// workgroups per CU, so that up to 768 of them run at once (at two per CU a
+// pass of 65 pages x 8 kv heads left 8 workgroups for a second round).
 template <int D, bool RO, int NW>
 __global__ __launch_bounds__(NW * 64, (NW == 8 && !RO) ? 6 : 1) void k_attn(AttnArgs a) {
   extern __shared__ __align__(16) unsigned char lds[];
